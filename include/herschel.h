@@ -1,0 +1,187 @@
+/*
+ * herschel.h -- C ABI of the MI355X trace-reconstruction library.
+ *
+ * The library reconstructs operator executions from one bounded profiling
+ * window, the data-parallel core of the analyzer in "Herschel: Continuous
+ * Optimization of Production LLM Inference through On-Demand Profiling".
+ *
+ *  - The records it consumes are the three kinds the profiler emits
+ *    (Section 5.2, "Python calls and object fields" and "Host API calls and
+ *    device activity"): CPU operator ranges with their native thread and
+ *    entry/return times, host launch-API intervals carrying a correlation id,
+ *    and device kernel records located by device stream and linked to their
+ *    launch by the same correlation id.
+ *  - Records are admitted to the window by their start time (Section 5.2,
+ *    "Session transitions": start-time filtering separates windows).
+ *  - The results are the observations of Section 6.1 ("Operator execution and
+ *    efficiency", "Execution progress and state") and of Figure "Key
+ *    performance observations": kernel composition of each operator from
+ *    call-to-kernel links, the operator span T_op from the first kernel start
+ *    to the last completion, idle intervals of the GPU activity (the idle
+ *    evidence of the case study in Section 9.1), communication overlapped
+ *    with computation measured as interval coverage, and cross-process waits.
+ *
+ * Every entry point takes DEVICE pointers for all arrays (events, params
+ * arrays, outputs, workspace), enqueues its kernels on params->hip_stream,
+ * waits for that stream once at the end and reads the counters back to form
+ * the return code.  The library never allocates device memory, keeps no
+ * pointer after it returns and is re-entrant given distinct workspaces.
+ * Arithmetic is integer only (int64 nanoseconds); sums wrap modulo 2^64.
+ */
+#ifndef HERSCHEL_H
+#define HERSCHEL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Record kinds (Section 5.2). */
+enum {
+  HERSCHEL_CPU_OP = 0, /* a recorded Python call: native thread, entry and return time */
+  HERSCHEL_LAUNCH = 1, /* a host API interval that submits device work; carries corr */
+  HERSCHEL_KERNEL = 2  /* a device activity record: stream, start, end, corr, name */
+};
+
+/* Return codes.  Precedence when several apply:
+ * EINVAL > EWORKSPACE > EEVENT > EDEVICE > ECAPACITY. */
+enum {
+  HERSCHEL_OK = 0,
+  HERSCHEL_EINVAL = -1,     /* a required pointer is NULL or a parameter is out of range */
+  HERSCHEL_EEVENT = -2,     /* an input row is invalid; counters->first_invalid = smallest such row */
+  HERSCHEL_ECAPACITY = -3,  /* more gaps than gap_capacity; the first gap_capacity are written */
+  HERSCHEL_EWORKSPACE = -4, /* workspace is NULL or smaller than herschel_workspace_size() */
+  HERSCHEL_EDEVICE = -5     /* a HIP call failed or a device-side consistency check tripped */
+};
+
+/* Optional outputs (params.flags).  Timelines, gaps, the launch/kernel join,
+ * the latency histogram and the per-name aggregates are always produced. */
+#define HERSCHEL_OUT_CONTAIN 0x1u /* op nesting, launch->op, kernel->op, per-op aggregates */
+#define HERSCHEL_OUT_OVERLAP 0x2u /* cross-stream overlap and class coverage */
+
+/* Implementation limits (checked; EINVAL when exceeded). */
+#define HERSCHEL_MAX_PROCS 4096
+#define HERSCHEL_MAX_STREAMS 64
+#define HERSCHEL_MAX_THREADS 2048
+#define HERSCHEL_MAX_WINDOW (1LL << 40)  /* W1 - W0 in ns (about 18 minutes) */
+#define HERSCHEL_MAX_ABS_TIME (1LL << 62) /* |ts|, |te|, |W0|, |W1|, |clock offset| must be below */
+#define HERSCHEL_CORR_LIMIT (1LL << 48)   /* LAUNCH/KERNEL corr must lie in [0, 2^48) */
+#define HERSCHEL_MAX_NAMES (1 << 24)
+
+/* Input records as a structure of arrays, n rows, in any order (delivery
+ * order).  37 bytes per row.  Row i is valid iff
+ *   kind[i] in {CPU_OP, LAUNCH, KERNEL}, 0 <= pid[i] < n_procs,
+ *   KERNEL: 0 <= lane < n_streams and 0 <= name < n_names,
+ *   CPU_OP: 0 <= lane < n_threads and 0 <= name < n_op_names,
+ *   LAUNCH: 0 <= lane < n_threads and name >= 0 (an API id),
+ *   LAUNCH/KERNEL: 0 <= corr < 2^48,
+ *   -2^62 < ts <= te < 2^62. */
+typedef struct {
+  const int64_t *ts;   /* start, ns on the process clock */
+  const int64_t *te;   /* end, ns on the process clock */
+  const int64_t *corr; /* correlation id, per process; ignored for CPU_OP */
+  const int32_t *pid;  /* process index */
+  const int32_t *lane; /* KERNEL: device stream; CPU_OP / LAUNCH: native thread */
+  const int32_t *name; /* KERNEL: kernel-name id; CPU_OP: op-name id; LAUNCH: API id */
+  const uint8_t *kind; /* HERSCHEL_CPU_OP / _LAUNCH / _KERNEL */
+} herschel_events;
+
+/* A cross-process dependency edge (Figure "Key performance observations",
+ * panel "Cross-process blocking"): the consumer's work waits on the
+ * producer's.  Keyed by (process, correlation id) of the two kernels. */
+typedef struct {
+  int32_t prod_pid, cons_pid;
+  int64_t prod_corr, cons_corr;
+} herschel_edge;
+
+typedef struct {
+  int64_t window_begin, window_end; /* [W0, W1) on the corrected clock; 0 < W1-W0 <= 2^40 */
+  int64_t gap_threshold;            /* a gap is emitted iff its length > gap_threshold */
+  int32_t n_procs, n_streams, n_threads, n_names, n_op_names;
+  const int64_t *clock_offset;  /* [n_procs] or NULL (all zero); corrected = raw - offset */
+  const uint8_t *stream_class;  /* [n_streams] 0 compute, 1 comm, 2 copy; NULL = all compute */
+  const herschel_edge *edges;   /* [n_edges]; may be NULL when n_edges == 0 */
+  int64_t n_edges;
+  uint32_t flags;               /* HERSCHEL_OUT_* */
+  void *hip_stream;             /* hipStream_t to enqueue on; NULL = the null stream */
+  void *workspace;              /* device scratch owned by the caller */
+  size_t workspace_bytes;
+} herschel_params;
+
+typedef struct {
+  int64_t n_admitted[3];          /* admitted rows per kind (W0 <= ts' < W1) */
+  int64_t n_outside_window;       /* rows not admitted */
+  int64_t n_matched;              /* admitted kernels joined to an admitted launch */
+  int64_t n_unmatched_kernels;    /* admitted kernels without a launch */
+  int64_t n_unmatched_launches;   /* admitted launches with no kernel joined to them */
+  int64_t n_dup_launch_corr;      /* extra admitted launches sharing a (pid, corr) */
+  int64_t n_unattributed_kernels; /* matched kernels whose launch lies in no op (CONTAIN) */
+  int64_t n_improper_nesting;     /* ops ending after their parent (CONTAIN) */
+  int64_t n_negative_latency;     /* matched kernels starting before their launch */
+  int64_t n_gaps_total;           /* gaps above the threshold (may exceed gap_capacity) */
+  int64_t first_invalid;          /* smallest invalid row, -1 if none */
+  int64_t device_status;          /* 0, or bits of internal device-side failures */
+} herschel_counters;
+
+/* Outputs.  Per-row arrays are indexed by input row.  Rows outside the
+ * window get link = aux = -2.  For admitted rows:
+ *   link: KERNEL -> row of its launch (-1 none); LAUNCH -> row of the innermost
+ *         enclosing CPU op (-1 none); CPU_OP -> row of its parent op (-1 root)
+ *   aux:  KERNEL -> row of the op its launch lies in (-1 none); LAUNCH -> number
+ *         of kernels joined to it; CPU_OP -> nesting depth (0 for a root)
+ * Without HERSCHEL_OUT_CONTAIN, the CPU_OP and LAUNCH link, the CPU_OP and
+ * KERNEL aux are -1 and the op_* arrays are not touched.
+ * op_* are written at admitted CPU_OP rows only: the inclusive aggregates of
+ * the kernels attributed to the op or to any of its descendants; an op with
+ * none gets (0, INT64_MAX, INT64_MIN, 0).  T_op = op_last - op_first. */
+typedef struct {
+  int32_t *link, *aux;               /* [n] */
+  int32_t *op_nkern;                 /* [n] */
+  int64_t *op_first, *op_last;       /* [n] first kernel start, last kernel end (unclipped) */
+  int64_t *op_ksum;                  /* [n] sum of kernel durations */
+  int64_t *busy, *idle;              /* [n_procs * n_streams] */
+  int64_t *pair_overlap;             /* [n_procs * n_streams * n_streams] (OVERLAP) */
+  int64_t *class_busy;               /* [n_procs * 3] (OVERLAP) */
+  int64_t *class_overlap;            /* [n_procs * 3 * 3] (OVERLAP) */
+  int64_t *any_busy;                 /* [n_procs] (OVERLAP) */
+  int64_t *name_count, *name_sum;    /* [n_names] */
+  int64_t *name_min, *name_max;      /* [n_names]; empty names: INT64_MAX, INT64_MIN */
+  int64_t *lat_hist;                 /* [64]: bin 0 for latency <= 0, else floor(log2)+1 */
+  int64_t *edge_wait;                /* [n_edges]; INT64_MIN when unresolved */
+  int32_t *edge_status;              /* [n_edges]; bit0 producer missing, bit1 consumer missing */
+  int64_t gap_capacity;              /* entries available in the gap_* arrays */
+  int32_t *gap_pid, *gap_stream;     /* [gap_capacity] */
+  int64_t *gap_begin, *gap_end;      /* [gap_capacity] */
+  uint8_t *gap_flags;                /* [gap_capacity] bit0 leading (at W0), bit1 trailing (at W1) */
+  herschel_counters *counters;       /* device pointer */
+} herschel_outputs;
+
+/* Bytes of device workspace that herschel_trace_analyze needs for n rows
+ * under params *p (only the sizes and limits in *p are read). */
+int herschel_workspace_size(int64_t n, const herschel_params *p, size_t *bytes);
+
+/* Reconstruct one window: n rows of ev under *p into *out.  Returns a
+ * HERSCHEL_* code.  On EEVENT only counters->first_invalid is defined. */
+int herschel_trace_analyze(const herschel_events *ev, int64_t n, const herschel_params *p,
+                           herschel_outputs *out);
+
+/* Reconstruct n_traces independent windows stored back to back in ev: trace
+ * t holds rows [trace_offsets[t], trace_offsets[t+1]) (a HOST array of
+ * n_traces + 1 entries) and uses p[t] and out[t] (HOST arrays of structs whose
+ * pointers are device pointers).  Row indices in trace t's outputs are local
+ * to the trace.  p[0].workspace must hold herschel_workspace_size() for the
+ * largest trace; the workspace and stream of p[0] are used for all traces.
+ * Returns the first non-OK code in trace order, or HERSCHEL_OK. */
+int herschel_trace_analyze_batch(const herschel_events *ev, const int64_t *trace_offsets,
+                                 int32_t n_traces, const herschel_params *p,
+                                 herschel_outputs *out);
+
+const char *herschel_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HERSCHEL_H */

@@ -1,0 +1,544 @@
+/*
+ * herschel_oracle.c -- TEST INFRASTRUCTURE ONLY: the CPU oracle.
+ *
+ * A plain, slow, single-threaded C implementation of the trace
+ * reconstruction that the Herschel analyzer performs on one bounded
+ * profiling window (Section 6.1, "Deriving Performance Observations", and
+ * Figure "Key performance observations").  Only the tests, the smoke check
+ * and the benchmark's CPU-baseline leg call it.  It shares no code with the
+ * HIP library.
+ *
+ * The paper states the analysis in prose only; every result here is a plain
+ * definition, written out step by step in the order below.  Readings of the
+ * prose that the paper leaves open are marked READING.
+ *
+ *   1. validate rows                      (record schema, Section 5.2)
+ *   2. correct clocks, 3. admit by start   (start-time filtering, Section 5.2)
+ *   4-6. per-stream coverage, busy/idle, gaps (idle intervals, Section 9.1)
+ *   7-8. launch/kernel join by correlation id, launch latency
+ *        (call-to-kernel links, Section 6.1; "CPU submission time" and
+ *        "correlation id" in panel "Operator execution and efficiency")
+ *   9-12. op nesting, launch -> op, kernel -> op, inclusive T_op aggregates
+ *        (kernel composition and T_op, Section 6.1; nested calls, Section 5.2)
+ *   13. per kernel-name aggregates
+ *   14. cross-stream overlap as interval coverage (panel "Overlap and exposed
+ *       work"; Section 6.1 "Execution progress and state")
+ *   15. cross-process dependency waits (panel "Cross-process blocking")
+ *
+ * Sorting uses the C library's qsort with comparators that end in the row
+ * index, so every order is total and the result does not depend on qsort's
+ * stability.  Sums use unsigned arithmetic and wrap modulo 2^64.
+ *
+ * Parity: pinned in the tests against the hand-built worked timeline, a
+ * per-nanosecond brute force on tiny traces, invariants and the trace
+ * generator's ground truth.  No output is "parity unpinned".
+ */
+#include "herschel_oracle.h"
+
+#include <stdlib.h>
+#include <string.h>
+
+#define K_CPU 0
+#define K_LAUNCH 1
+#define K_KERNEL 2
+#define I64_MAX ((int64_t)0x7fffffffffffffffLL)
+#define I64_MIN ((int64_t)(-0x7fffffffffffffffLL - 1))
+#define ABS_LIMIT (1LL << 62)
+#define CORR_LIMIT (1LL << 48)
+
+static int64_t wrap_add(int64_t a, int64_t b) { return (int64_t)((uint64_t)a + (uint64_t)b); }
+static int64_t wrap_sub(int64_t a, int64_t b) { return (int64_t)((uint64_t)a - (uint64_t)b); }
+static int in_abs(int64_t x) { return x > -ABS_LIMIT && x < ABS_LIMIT; }
+
+/* ---- step 1: row validity (record schema of Section 5.2) ---------------- */
+static int row_is_valid(const hro_events *ev, int64_t i, const hro_params *p) {
+  int k = ev->kind[i];
+  if (k != K_CPU && k != K_LAUNCH && k != K_KERNEL) return 0;
+  if (ev->pid[i] < 0 || ev->pid[i] >= p->n_procs) return 0;
+  if (k == K_KERNEL) {
+    if (ev->lane[i] < 0 || ev->lane[i] >= p->n_streams) return 0;
+    if (ev->name[i] < 0 || ev->name[i] >= p->n_names) return 0;
+  } else {
+    if (ev->lane[i] < 0 || ev->lane[i] >= p->n_threads) return 0;
+    if (k == K_CPU && (ev->name[i] < 0 || ev->name[i] >= p->n_op_names)) return 0;
+    if (k == K_LAUNCH && ev->name[i] < 0) return 0;
+  }
+  if (k != K_CPU && (ev->corr[i] < 0 || ev->corr[i] >= CORR_LIMIT)) return 0;
+  if (!in_abs(ev->ts[i]) || !in_abs(ev->te[i])) return 0;
+  if (ev->te[i] < ev->ts[i]) return 0;
+  return 1;
+}
+
+static int params_ok(int64_t n, const hro_params *p) {
+  if (n < 0 || n >= (1LL << 31)) return 0;
+  if (!in_abs(p->w0) || !in_abs(p->w1) || p->w1 <= p->w0) return 0;
+  if (p->w1 - p->w0 > (1LL << 40)) return 0;
+  if (p->n_procs < 1 || p->n_procs > 4096) return 0;
+  if (p->n_streams < 1 || p->n_streams > 64) return 0;
+  if (p->n_threads < 1 || p->n_threads > 2048) return 0;
+  if (p->n_names < 1 || p->n_names > (1 << 24)) return 0;
+  if (p->n_op_names < 1) return 0;
+  if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return 0;
+  if (p->clock_offset)
+    for (int q = 0; q < p->n_procs; ++q)
+      if (!in_abs(p->clock_offset[q])) return 0;
+  if (p->stream_class)
+    for (int s = 0; s < p->n_streams; ++s)
+      if (p->stream_class[s] > 2) return 0;
+  return 1;
+}
+
+/* ---- generic sort records --------------------------------------------- */
+typedef struct {
+  int64_t a, b, c; /* sort fields, compared in order */
+  int64_t row;
+} rec4;
+
+static int cmp_rec4(const void *x, const void *y) {
+  const rec4 *u = (const rec4 *)x, *v = (const rec4 *)y;
+  if (u->a != v->a) return u->a < v->a ? -1 : 1;
+  if (u->b != v->b) return u->b < v->b ? -1 : 1;
+  if (u->c != v->c) return u->c < v->c ? -1 : 1;
+  if (u->row != v->row) return u->row < v->row ? -1 : 1;
+  return 0;
+}
+
+typedef struct {
+  int64_t s, e;
+} ival;
+
+static int cmp_ival(const void *x, const void *y) {
+  const ival *u = (const ival *)x, *v = (const ival *)y;
+  if (u->s != v->s) return u->s < v->s ? -1 : 1;
+  if (u->e != v->e) return u->e < v->e ? -1 : 1;
+  return 0;
+}
+
+/* Merge a start-sorted list of half-open intervals into maximal disjoint runs.
+ * Touching intervals merge; empty intervals are never passed in (step 4). */
+static int64_t merge_runs(ival *v, int64_t m) {
+  int64_t r = 0;
+  for (int64_t i = 0; i < m; ++i) {
+    if (r > 0 && v[i].s <= v[r - 1].e) {
+      if (v[i].e > v[r - 1].e) v[r - 1].e = v[i].e;
+    } else {
+      v[r++] = v[i];
+    }
+  }
+  return r;
+}
+
+static int64_t runs_length(const ival *v, int64_t m) {
+  int64_t t = 0;
+  for (int64_t i = 0; i < m; ++i) t += v[i].e - v[i].s;
+  return t;
+}
+
+/* |A intersect B| for two sorted lists of disjoint runs. */
+static int64_t runs_intersection(const ival *a, int64_t na, const ival *b, int64_t nb) {
+  int64_t i = 0, j = 0, t = 0;
+  while (i < na && j < nb) {
+    int64_t lo = a[i].s > b[j].s ? a[i].s : b[j].s;
+    int64_t hi = a[i].e < b[j].e ? a[i].e : b[j].e;
+    if (hi > lo) t += hi - lo;
+    if (a[i].e < b[j].e) ++i; else ++j;
+  }
+  return t;
+}
+
+/* Union of several run lists: concatenate, sort by start, merge. */
+static int64_t union_of(ival *const *lists, const int64_t *lens, int nl, ival **outp) {
+  int64_t tot = 0;
+  for (int k = 0; k < nl; ++k) tot += lens[k];
+  ival *u = (ival *)malloc(sizeof(ival) * (size_t)(tot > 0 ? tot : 1));
+  int64_t w = 0;
+  for (int k = 0; k < nl; ++k) {
+    memcpy(u + w, lists[k], sizeof(ival) * (size_t)lens[k]);
+    w += lens[k];
+  }
+  qsort(u, (size_t)tot, sizeof(ival), cmp_ival);
+  int64_t r = merge_runs(u, tot);
+  *outp = u;
+  return r;
+}
+
+/* floor(log2 x) + 1 for x > 0, 0 otherwise (step 8's histogram bin). */
+static int latency_bin(int64_t x) {
+  int b = 0;
+  while (x > 0) {
+    ++b;
+    x >>= 1;
+  }
+  return b;
+}
+
+int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p,
+                            hro_outputs *out) {
+  if (!ev || !p || !out || !out->counters) return -1;
+  if (!params_ok(n, p)) return -1;
+  const int P = p->n_procs, S = p->n_streams;
+  const int64_t W0 = p->w0, W1 = p->w1, W = W1 - W0;
+  const int contain = (p->flags & 1u) != 0, overlap = (p->flags & 2u) != 0;
+  hro_counters *c = out->counters;
+  memset(c, 0, sizeof(*c));
+  c->first_invalid = -1;
+
+  /* 1. Validate every row; the smallest bad index is reported. */
+  for (int64_t i = 0; i < n; ++i)
+    if (!row_is_valid(ev, i, p)) {
+      c->first_invalid = i;
+      return -2;
+    }
+
+  /* 2. Correct each row onto the common clock: corrected = raw - offset[pid].
+   *    READING: the paper does not discuss clock alignment; offsets are given. */
+  int64_t *ts = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+  int64_t *te = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+  unsigned char *adm = (unsigned char *)calloc((size_t)(n > 0 ? n : 1), 1);
+  for (int64_t i = 0; i < n; ++i) {
+    int64_t off = p->clock_offset ? p->clock_offset[ev->pid[i]] : 0;
+    ts[i] = ev->ts[i] - off;
+    te[i] = ev->te[i] - off;
+  }
+
+  /* 3. Admit a row iff its corrected start lies in [W0, W1) (start-time
+   *    filtering, Section 5.2).  Rows outside get link = aux = -2. */
+  for (int64_t i = 0; i < n; ++i) {
+    adm[i] = (ts[i] >= W0 && ts[i] < W1);
+    if (adm[i]) {
+      c->n_admitted[ev->kind[i]]++;
+      out->link[i] = -1;
+      out->aux[i] = -1;
+    } else {
+      c->n_outside_window++;
+      out->link[i] = -2;
+      out->aux[i] = -2;
+    }
+  }
+
+  /* 4-6. Per (process, stream): coverage of the admitted kernels, each
+   * covering [ts', min(te', W1)); empty intervals cover nothing; touching
+   * intervals merge.  busy = |union|, idle = W - busy.  Gaps are the maximal
+   * uncovered sub-intervals of [W0, W1), emitted in (p, s, begin) order when
+   * longer than the threshold.  (Idle intervals of GPU activity, Section 9.1.) */
+  int64_t nk = 0;
+  for (int64_t i = 0; i < n; ++i)
+    if (adm[i] && ev->kind[i] == K_KERNEL) ++nk;
+  rec4 *kr = (rec4 *)malloc(sizeof(rec4) * (size_t)(nk > 0 ? nk : 1));
+  {
+    int64_t w = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (adm[i] && ev->kind[i] == K_KERNEL) {
+        kr[w].a = (int64_t)ev->pid[i] * S + ev->lane[i];
+        kr[w].b = ts[i];
+        kr[w].c = te[i] < W1 ? te[i] : W1;
+        kr[w].row = i;
+        ++w;
+      }
+    qsort(kr, (size_t)nk, sizeof(rec4), cmp_rec4);
+  }
+  ival **runs = (ival **)calloc((size_t)P * S, sizeof(ival *));
+  int64_t *nruns = (int64_t *)calloc((size_t)P * S, sizeof(int64_t));
+  int64_t gw = 0;
+  {
+    int64_t at = 0;
+    for (int64_t ps = 0; ps < (int64_t)P * S; ++ps) {
+      int64_t begin = at;
+      while (at < nk && kr[at].a == ps) ++at;
+      ival *v = (ival *)malloc(sizeof(ival) * (size_t)(at - begin + 1));
+      int64_t m = 0;
+      for (int64_t q = begin; q < at; ++q)
+        if (kr[q].c > kr[q].b) { /* non-empty after clipping */
+          v[m].s = kr[q].b;
+          v[m].e = kr[q].c;
+          ++m;
+        }
+      int64_t r = merge_runs(v, m);
+      runs[ps] = v;
+      nruns[ps] = r;
+      int64_t b = runs_length(v, r);
+      out->busy[ps] = b;
+      out->idle[ps] = W - b;
+      int64_t prev = W0;
+      for (int64_t q = 0; q <= r; ++q) {
+        int64_t gb = prev, ge = (q < r) ? v[q].s : W1;
+        if (ge > gb) {
+          if (ge - gb > p->thr) {
+            if (gw < out->gap_capacity) {
+              out->gap_pid[gw] = (int32_t)(ps / S);
+              out->gap_stream[gw] = (int32_t)(ps % S);
+              out->gap_begin[gw] = gb;
+              out->gap_end[gw] = ge;
+              out->gap_flags[gw] = (uint8_t)((gb == W0 ? 1 : 0) | (ge == W1 ? 2 : 0));
+            }
+            ++gw;
+          }
+        }
+        if (q < r) prev = v[q].e;
+      }
+    }
+  }
+  c->n_gaps_total = gw;
+
+  /* 7. Join each admitted kernel to the admitted launch with the same
+   *    (process, correlation id) (call-to-kernel links, Section 6.1).  Several
+   *    launches with one id: the smallest row wins, the others are counted as
+   *    duplicates.  One launch may own several kernels (graph replay). */
+  int64_t nl = 0;
+  for (int64_t i = 0; i < n; ++i)
+    if (adm[i] && ev->kind[i] == K_LAUNCH) ++nl;
+  rec4 *lr = (rec4 *)malloc(sizeof(rec4) * (size_t)(nl > 0 ? nl : 1));
+  {
+    int64_t w = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (adm[i] && ev->kind[i] == K_LAUNCH) {
+        lr[w].a = ev->pid[i];
+        lr[w].b = ev->corr[i];
+        lr[w].c = 0;
+        lr[w].row = i;
+        ++w;
+      }
+    qsort(lr, (size_t)nl, sizeof(rec4), cmp_rec4);
+    for (int64_t q = 1; q < nl; ++q)
+      if (lr[q].a == lr[q - 1].a && lr[q].b == lr[q - 1].b) c->n_dup_launch_corr++;
+    for (int64_t q = 0; q < nl; ++q) out->aux[lr[q].row] = 0;
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    if (!adm[i] || ev->kind[i] != K_KERNEL) continue;
+    /* lower bound of (pid, corr) among sorted launches */
+    int64_t lo = 0, hi = nl;
+    while (lo < hi) {
+      int64_t mid = lo + (hi - lo) / 2;
+      if (lr[mid].a < ev->pid[i] || (lr[mid].a == ev->pid[i] && lr[mid].b < ev->corr[i]))
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    if (lo < nl && lr[lo].a == ev->pid[i] && lr[lo].b == ev->corr[i]) {
+      int64_t l = lr[lo].row;
+      out->link[i] = (int32_t)l;
+      out->aux[l]++;
+      c->n_matched++;
+      /* 8. Launch latency: kernel start minus the launch's start (the "CPU
+       *    submission time" of the operator figure).  Signed.  Bin 0 for
+       *    x <= 0, else floor(log2 x) + 1. */
+      int64_t x = ts[i] - ts[l];
+      if (x < 0) c->n_negative_latency++;
+      out->lat_hist[latency_bin(x)]++;
+    } else {
+      out->link[i] = -1;
+      c->n_unmatched_kernels++;
+    }
+  }
+  for (int64_t q = 0; q < nl; ++q)
+    if (out->aux[lr[q].row] == 0) c->n_unmatched_launches++;
+
+  /* 9-12. Containment (Section 6.1 "kernel composition"; nested calls are
+   * recorded, Section 5.2). */
+  if (contain) {
+    int64_t nc = c->n_admitted[K_CPU];
+    rec4 *cr = (rec4 *)malloc(sizeof(rec4) * (size_t)(nc > 0 ? nc : 1));
+    int64_t *par = (int64_t *)malloc(sizeof(int64_t) * (size_t)(nc > 0 ? nc : 1));
+    int64_t *segstart = (int64_t *)malloc(sizeof(int64_t) * (size_t)(nc > 0 ? nc : 1));
+    int64_t w = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (adm[i] && ev->kind[i] == K_CPU) {
+        cr[w].a = (int64_t)ev->pid[i] * p->n_threads + ev->lane[i];
+        cr[w].b = ts[i];
+        cr[w].c = -te[i]; /* te' descending: the outer of two ops starting together first */
+        cr[w].row = i;
+        ++w;
+      }
+    qsort(cr, (size_t)nc, sizeof(rec4), cmp_rec4);
+    /* 9. Parent of op i: the nearest op before it in the (thread, ts' up,
+     *    te' down, row up) order whose end is after i's start.  READING: this
+     *    equals the innermost enclosing op for properly nested calls and is
+     *    defined for any input.  The backward scan may skip from a failing
+     *    candidate j straight to parent(j): every op strictly between them
+     *    ends no later than ts'_j <= ts'_i, so none of them qualifies. */
+    for (int64_t q = 0; q < nc; ++q) {
+      segstart[q] = (q > 0 && cr[q].a == cr[q - 1].a) ? segstart[q - 1] : q;
+      int64_t j = q - 1;
+      while (j >= segstart[q] && -cr[j].c <= cr[q].b) j = par[j];
+      if (j < segstart[q]) j = -1;
+      par[q] = j;
+      int64_t row = cr[q].row;
+      if (j < 0) {
+        out->link[row] = -1;
+        out->aux[row] = 0;
+      } else {
+        out->link[row] = (int32_t)cr[j].row;
+        out->aux[row] = out->aux[cr[j].row] + 1;
+        if (te[row] > te[cr[j].row]) c->n_improper_nesting++;
+      }
+    }
+    /* 10. A launch lies in the innermost op of its thread that contains its
+     *     start point t: the last op in the order with ts' <= t and te' > t. */
+    for (int64_t i = 0; i < n; ++i) {
+      if (!adm[i] || ev->kind[i] != K_LAUNCH) continue;
+      int64_t seg = (int64_t)ev->pid[i] * p->n_threads + ev->lane[i], t = ts[i];
+      /* last position with (seg, ts') <= (seg, t) */
+      int64_t lo = 0, hi = nc;
+      while (lo < hi) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (cr[mid].a < seg || (cr[mid].a == seg && cr[mid].b <= t))
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      int64_t j = lo - 1;
+      if (j >= 0 && cr[j].a != seg) j = -1;
+      while (j >= 0 && -cr[j].c <= t) j = par[j];
+      out->link[i] = j >= 0 ? (int32_t)cr[j].row : -1;
+    }
+    /* 11. A kernel belongs to the op its launch lies in. */
+    for (int64_t i = 0; i < n; ++i) {
+      if (!adm[i] || ev->kind[i] != K_KERNEL) continue;
+      int64_t l = out->link[i];
+      if (l < 0) {
+        out->aux[i] = -1;
+      } else {
+        out->aux[i] = out->link[l];
+        if (out->link[l] < 0) c->n_unattributed_kernels++;
+      }
+    }
+    /* 12. Inclusive per-op aggregates: every kernel counts for its op and
+     *     for each ancestor.  T_op spans the first kernel start to the last
+     *     kernel end (Section 6.1), unclipped. */
+    for (int64_t q = 0; q < nc; ++q) {
+      int64_t r = cr[q].row;
+      out->op_nkern[r] = 0;
+      out->op_first[r] = I64_MAX;
+      out->op_last[r] = I64_MIN;
+      out->op_ksum[r] = 0;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+      if (!adm[i] || ev->kind[i] != K_KERNEL) continue;
+      int64_t r = out->aux[i];
+      while (r >= 0) {
+        out->op_nkern[r]++;
+        if (ts[i] < out->op_first[r]) out->op_first[r] = ts[i];
+        if (te[i] > out->op_last[r]) out->op_last[r] = te[i];
+        out->op_ksum[r] = wrap_add(out->op_ksum[r], te[i] - ts[i]);
+        r = out->link[r];
+      }
+    }
+    free(cr);
+    free(par);
+    free(segstart);
+  }
+
+  /* 13. Per kernel-name aggregates over all admitted kernels, matched or not:
+   *     count, sum, min and max of the unclipped duration te' - ts'. */
+  for (int q = 0; q < p->n_names; ++q) {
+    out->name_count[q] = 0;
+    out->name_sum[q] = 0;
+    out->name_min[q] = I64_MAX;
+    out->name_max[q] = I64_MIN;
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    if (!adm[i] || ev->kind[i] != K_KERNEL) continue;
+    int q = ev->name[i];
+    int64_t d = te[i] - ts[i];
+    out->name_count[q]++;
+    out->name_sum[q] = wrap_add(out->name_sum[q], d);
+    if (d < out->name_min[q]) out->name_min[q] = d;
+    if (d > out->name_max[q]) out->name_max[q] = d;
+  }
+
+  /* 14. Overlap as interval coverage (panel "Overlap and exposed work"):
+   *     per process, with U_s the covered set of stream s,
+   *     pair_overlap[i][j] = |U_i and U_j|, class_busy[c] = |union over the
+   *     class|, class_overlap[c1][c2] = |class c1 union and class c2 union|,
+   *     any_busy = |union over all streams|. */
+  if (overlap) {
+    for (int pp = 0; pp < P; ++pp) {
+      ival **L = runs + (int64_t)pp * S;
+      int64_t *N = nruns + (int64_t)pp * S;
+      for (int i = 0; i < S; ++i)
+        for (int j = 0; j < S; ++j)
+          out->pair_overlap[((int64_t)pp * S + i) * S + j] =
+              runs_intersection(L[i], N[i], L[j], N[j]);
+      ival *cls[3];
+      int64_t ncls[3];
+      for (int cc = 0; cc < 3; ++cc) {
+        ival *sel[64];
+        int64_t seln[64];
+        int ns = 0;
+        for (int s = 0; s < S; ++s) {
+          int sc = p->stream_class ? p->stream_class[s] : 0;
+          if (sc == cc) {
+            sel[ns] = L[s];
+            seln[ns] = N[s];
+            ++ns;
+          }
+        }
+        ncls[cc] = union_of(sel, seln, ns, &cls[cc]);
+        out->class_busy[(int64_t)pp * 3 + cc] = runs_length(cls[cc], ncls[cc]);
+      }
+      for (int c1 = 0; c1 < 3; ++c1)
+        for (int c2 = 0; c2 < 3; ++c2)
+          out->class_overlap[((int64_t)pp * 3 + c1) * 3 + c2] =
+              runs_intersection(cls[c1], ncls[c1], cls[c2], ncls[c2]);
+      ival *all;
+      int64_t nall = union_of(L, N, S, &all);
+      out->any_busy[pp] = runs_length(all, nall);
+      free(all);
+      for (int cc = 0; cc < 3; ++cc) free(cls[cc]);
+    }
+  }
+
+  /* 15. Cross-process dependency waits (panel "Cross-process blocking"):
+   *     producer = the admitted kernel with (prod_pid, prod_corr) that ends
+   *     last, consumer = the one with (cons_pid, cons_corr) that starts first;
+   *     wait = consumer start - producer end, signed.  Missing side: status
+   *     bit (0 producer, 1 consumer) and wait = INT64_MIN. */
+  if (p->n_edges > 0) {
+    rec4 *kc = (rec4 *)malloc(sizeof(rec4) * (size_t)(nk > 0 ? nk : 1));
+    int64_t w = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (adm[i] && ev->kind[i] == K_KERNEL) {
+        kc[w].a = ev->pid[i];
+        kc[w].b = ev->corr[i];
+        kc[w].c = 0;
+        kc[w].row = i;
+        ++w;
+      }
+    qsort(kc, (size_t)nk, sizeof(rec4), cmp_rec4);
+    for (int64_t e = 0; e < p->n_edges; ++e) {
+      int found[2] = {0, 0};
+      int64_t prod_end = I64_MIN, cons_start = I64_MAX;
+      for (int side = 0; side < 2; ++side) {
+        int64_t qp = side == 0 ? p->edges[e].prod_pid : p->edges[e].cons_pid;
+        int64_t qc = side == 0 ? p->edges[e].prod_corr : p->edges[e].cons_corr;
+        int64_t lo = 0, hi = nk;
+        while (lo < hi) {
+          int64_t mid = lo + (hi - lo) / 2;
+          if (kc[mid].a < qp || (kc[mid].a == qp && kc[mid].b < qc))
+            lo = mid + 1;
+          else
+            hi = mid;
+        }
+        for (int64_t q = lo; q < nk && kc[q].a == qp && kc[q].b == qc; ++q) {
+          int64_t r = kc[q].row;
+          found[side] = 1;
+          if (side == 0 && te[r] > prod_end) prod_end = te[r];
+          if (side == 1 && ts[r] < cons_start) cons_start = ts[r];
+        }
+      }
+      out->edge_status[e] = (found[0] ? 0 : 1) | (found[1] ? 0 : 2);
+      out->edge_wait[e] = (found[0] && found[1]) ? wrap_sub(cons_start, prod_end) : I64_MIN;
+    }
+    free(kc);
+  }
+
+  for (int64_t ps = 0; ps < (int64_t)P * S; ++ps) free(runs[ps]);
+  free(runs);
+  free(nruns);
+  free(kr);
+  free(lr);
+  free(ts);
+  free(te);
+  free(adm);
+  return gw > out->gap_capacity ? -3 : 0;
+}

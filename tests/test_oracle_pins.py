@@ -1,0 +1,447 @@
+"""Pins of the CPU oracle against values fixed independently of it.
+
+* hand-built worked timelines (tests/golden, expected values derived by hand);
+* the per-nanosecond brute force of tests/bruteforce.py on tiny adversarial
+  traces (ties, zero-length kernels, duplicate ids, improper nesting, offsets);
+* invariants that hold for any input;
+* ground truth that the generator drew (latencies, drops, names, gaps);
+* metamorphic relations (row permutation, time shift, clock offsets);
+* the error paths of the boundary.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import bruteforce
+import oracle
+from compare import COUNTERS, assert_same
+from fixtures import I64_MAX, I64_MIN, load_golden
+from paper_2609_40247_amd import synth
+
+GOLDEN = ["t1_worked_timeline.json", "t2_worked_timeline.json"]
+
+
+def _check_expect(o, cols, exp):
+    for k, v in exp["counters"].items():
+        assert o["counters"][k] == v, k
+    assert o["link"].tolist() == exp["link"]
+    assert o["aux"].tolist() == exp["aux"]
+    for r, (nk, first, last, ksum) in exp["op"].items():
+        assert (o["op_nkern"][r], o["op_first"][r], o["op_last"][r], o["op_ksum"][r]) == (nk, first, last, ksum), r
+    # rows that are not admitted CPU ops are never written
+    not_op = [i for i in range(len(cols["ts"])) if i not in exp["op"]]
+    assert np.all(o["op_nkern"][not_op] == oracle.UNWRITTEN_I32)
+    assert o["busy"].tolist() == exp["busy"] and o["idle"].tolist() == exp["idle"]
+    gaps = list(zip(o["gap_pid"].tolist(), o["gap_stream"].tolist(), o["gap_begin"].tolist(),
+                    o["gap_end"].tolist(), o["gap_flags"].tolist()))
+    assert gaps == [tuple(g) for g in exp["gaps"]]
+    hist = np.zeros(64, np.int64)
+    for b, c in exp["lat_hist"].items():
+        hist[int(b)] = c
+    assert o["lat_hist"].tolist() == hist.tolist()
+    for k in ("name_count", "name_sum", "name_min", "name_max", "pair_overlap", "any_busy", "class_busy",
+              "class_overlap", "edge_wait", "edge_status"):
+        assert o[k].tolist() == exp[k], k
+
+
+@pytest.mark.parametrize("name", GOLDEN)
+def test_worked_timeline(name):
+    cols, p, g = load_golden(name)
+    code, o = oracle.analyze(cols, p)
+    assert code == g["expect"]["code"]
+    _check_expect(o, cols, g["expect"])
+
+
+def test_worked_timeline_all_compute():
+    cols, p, g = load_golden("t1_worked_timeline.json")
+    p["stream_class"] = None
+    code, o = oracle.analyze(cols, p)
+    assert o["class_busy"].tolist() == g["expect_all_compute"]["class_busy"]
+    assert o["class_overlap"].tolist() == g["expect_all_compute"]["class_overlap"]
+
+
+def test_worked_timeline_without_containment():
+    cols, p, g = load_golden("t1_worked_timeline.json")
+    p["flags"] = 0
+    code, o = oracle.analyze(cols, p)
+    kind = cols["kind"]
+    exp_link = np.array(g["expect"]["link"])
+    exp_aux = np.array(g["expect"]["aux"])
+    adm = exp_link != -2
+    # kernels keep their launch; launches keep their kernel count
+    assert (o["link"][kind == 2] == exp_link[kind == 2]).all()
+    assert (o["aux"][kind == 1] == exp_aux[kind == 1]).all()
+    assert (o["link"][(kind != 2) & adm] == -1).all()
+    assert (o["aux"][(kind != 1) & adm] == -1).all()
+    assert (o["op_nkern"] == oracle.UNWRITTEN_I32).all()
+    assert o["counters"]["n_unattributed_kernels"] == 0 and o["counters"]["n_improper_nesting"] == 0
+
+
+# --------------------------------------------------------------------------- brute force
+
+def _bf_compare(cols, p, o, b, ctx):
+    bc = b["counters"]
+    for k in COUNTERS:
+        assert o["counters"][k] == bc[k], f"{ctx}: {k} {o['counters'][k]} != {bc[k]}"
+    for k in ("link", "aux", "busy", "idle", "lat_hist", "name_count", "name_sum", "name_min", "name_max",
+              "edge_wait", "edge_status"):
+        assert o[k].tolist() == np.asarray(b[k]).tolist(), f"{ctx}: {k}"
+    gaps = list(zip(o["gap_pid"].tolist(), o["gap_stream"].tolist(), o["gap_begin"].tolist(),
+                    o["gap_end"].tolist(), o["gap_flags"].tolist()))
+    assert gaps == [tuple(int(x) for x in g) for g in b["gaps"]], ctx
+    if p["flags"] & 1:
+        for r, v in b["op"].items():
+            assert (int(o["op_nkern"][r]), int(o["op_first"][r]), int(o["op_last"][r]), int(o["op_ksum"][r])) == v, \
+                f"{ctx}: op {r}"
+    if p["flags"] & 2:
+        for k, v in b["overlap"].items():
+            assert o[k].tolist() == v.tolist(), f"{ctx}: {k}"
+
+
+BF_CASES = [dict(seed=s) for s in range(120)] + [
+    dict(seed=1000 + s, n_rows=120, window=900, n_procs=3, n_streams=4, n_threads=3, corr_range=30) for s in range(30)
+] + [dict(seed=2000 + s, n_rows=40, window=60, n_procs=1, n_streams=2, n_threads=1, corr_range=6, offsets=False)
+     for s in range(30)] + [dict(seed=3000 + s, flags=s % 4) for s in range(16)] + [
+    # many processes sharing few correlation ids: a join that forgets the
+    # process would find another process's launch
+    dict(seed=4000 + s, n_rows=30, window=200, n_procs=4, n_streams=2, n_threads=2, corr_range=3)
+    for s in range(40)]
+
+
+@pytest.mark.parametrize("case", BF_CASES, ids=lambda c: f"seed{c['seed']}")
+def test_bruteforce(case):
+    tr = synth.random_small(**case)
+    cols, p = tr.columns(), tr.params
+    code, o = oracle.analyze(cols, p)
+    bcode, b = bruteforce.analyze(cols, p)
+    assert code == bcode
+    if code == -2:
+        assert o["counters"]["first_invalid"] == b["counters"]["first_invalid"]
+        return
+    _bf_compare(cols, p, o, b, tr.label)
+
+
+def test_bruteforce_coverage_of_degenerate_cases():
+    """The random tiny traces really contain the cases they are meant to."""
+    seen = dict(dup=0, improper=0, neg=0, multi=0, unattributed=0, zero=0, outside=0)
+    for case in BF_CASES[:150]:
+        tr = synth.random_small(**case)
+        code, o = oracle.analyze(tr.columns(), tr.params)
+        c = o["counters"]
+        seen["dup"] += c["n_dup_launch_corr"] > 0
+        seen["improper"] += c["n_improper_nesting"] > 0
+        seen["neg"] += c["n_negative_latency"] > 0
+        seen["unattributed"] += c["n_unattributed_kernels"] > 0
+        seen["outside"] += c["n_outside_window"] > 0
+        seen["multi"] += bool((o["aux"][tr.kind == 1] > 1).any())
+        seen["zero"] += bool(((tr.te == tr.ts) & (tr.kind == 2) & (o["link"] != -2)).any())
+    assert all(v >= 5 for v in seen.values()), seen
+
+
+# --------------------------------------------------------------------------- invariants
+
+def _invariants(tr, o):
+    p = tr.params
+    c = o["counters"]
+    n = tr.n
+    W = p["window_end"] - p["window_begin"]
+    kind = tr.kind
+    adm = o["link"] != -2
+    assert c["n_admitted_cpu"] + c["n_admitted_launch"] + c["n_admitted_kernel"] + c["n_outside_window"] == n
+    assert (o["busy"] + o["idle"] == W).all() and (o["busy"] >= 0).all()
+    kern = np.flatnonzero((kind == 2) & adm)
+    lau = np.flatnonzero((kind == 1) & adm)
+    assert c["n_matched"] + c["n_unmatched_kernels"] == len(kern)
+    matched = kern[o["link"][kern] >= 0]
+    assert len(matched) == c["n_matched"]
+    L = o["link"][matched]
+    assert (kind[L] == 1).all() and (tr.pid[L] == tr.pid[matched]).all() and (tr.corr[L] == tr.corr[matched]).all()
+    assert o["aux"][lau].sum() == c["n_matched"]
+    assert (o["aux"][lau] == 0).sum() == c["n_unmatched_launches"]
+    assert o["lat_hist"].sum() == c["n_matched"]
+    assert o["name_count"].sum() == len(kern)
+    d = tr.te[kern] - tr.ts[kern]
+    assert o["name_sum"].sum() == d.sum()
+    if p["flags"] & 2:
+        P, S = p["n_procs"], p["n_streams"]
+        pair = o["pair_overlap"].reshape(P, S, S)
+        assert (np.diagonal(pair, axis1=1, axis2=2).reshape(-1) == o["busy"]).all()
+        assert (pair == pair.transpose(0, 2, 1)).all()
+        co = o["class_overlap"].reshape(P, 3, 3)
+        assert (np.diagonal(co, axis1=1, axis2=2) == o["class_busy"].reshape(P, 3)).all()
+        assert (o["any_busy"] <= o["class_busy"].reshape(P, 3).sum(1)).all()
+        assert (o["any_busy"] >= o["class_busy"].reshape(P, 3).max(1)).all()
+        assert (o["any_busy"] <= W).all()
+    if p["flags"] & 1:
+        ops = np.flatnonzero((kind == 0) & adm)
+        par = o["link"][ops]
+        # op n_kernels(parent) = self + sum over children
+        selfk = np.zeros(n, np.int64)
+        ka = o["aux"][kern]
+        np.add.at(selfk, ka[ka >= 0], 1)
+        child = np.zeros(n, np.int64)
+        np.add.at(child, par[par >= 0], o["op_nkern"][ops[par >= 0]])
+        assert (o["op_nkern"][ops] == selfk[ops] + child[ops]).all()
+        ne = ops[o["op_nkern"][ops] > 0]
+        assert (o["op_last"][ne] >= o["op_first"][ne]).all()
+        assert (o["aux"][ops[par >= 0]] == o["aux"][par[par >= 0]] + 1).all()
+        assert (o["aux"][ops[par < 0]] == 0).all()
+
+
+@pytest.fixture(scope="module")
+def cfg0():
+    tr = synth.config0()
+    return tr, oracle.analyze(tr.columns(), tr.params)
+
+
+def test_config0_invariants(cfg0):
+    tr, (code, o) = cfg0
+    assert code == 0
+    _invariants(tr, o)
+    c = o["counters"]
+    assert int((tr.kind == 0).sum()) == 20_000 and int((tr.kind == 1).sum()) == 20_000
+    assert 19_000 < c["n_admitted_kernel"] < 20_000 and c["n_admitted_cpu"] > 19_900
+    assert c["n_outside_window"] > 0
+
+
+@pytest.mark.parametrize("maker", [lambda: synth.config1(n_steps=40), lambda: synth.config2(scale=0.03),
+                                   lambda: synth.config3(n_procs=3, n_steps=20, n_edges=500)],
+                         ids=["config1-small", "config2-small", "config3-small"])
+def test_small_config_invariants(maker):
+    tr = maker()
+    code, o = oracle.analyze(tr.columns(), tr.params)
+    assert code == 0
+    _invariants(tr, o)
+
+
+def test_threshold_minus_one_gaps_sum_to_idle(cfg0):
+    tr, _ = cfg0
+    p = dict(tr.params, gap_threshold=-1)
+    code, o = oracle.analyze(tr.columns(), p)
+    S = p["n_streams"]
+    tot = np.zeros(p["n_procs"] * S, np.int64)
+    np.add.at(tot, o["gap_pid"] * S + o["gap_stream"], o["gap_end"] - o["gap_begin"])
+    assert (tot == o["idle"]).all()
+    # gaps tile the complement: begins after ends within a stream, sorted
+    key = o["gap_pid"].astype(np.int64) * S + o["gap_stream"]
+    assert (np.diff(key) >= 0).all()
+
+
+# --------------------------------------------------------------------------- generator ground truth
+
+def _truth_check(tr, o):
+    pr = tr.truth["procs"][0]
+    C, L, K = tr.truth["counts"][0]
+    row_of = tr.truth["row_of"]
+    p = tr.params
+    W0, W1 = p["window_begin"], p["window_end"]
+    kept = ~pr["dropped"]
+    Kg = len(pr["start"])
+    krow = np.full(Kg, -1, np.int64)
+    krow[kept] = row_of[C + L + np.arange(K)]
+    lrow = row_of[C + np.arange(Kg)]
+    k_in = (pr["start"] >= W0) & (pr["start"] < W1)
+    l_in = (pr["l_ts"] >= W0) & (pr["l_ts"] < W1)
+    both = kept & k_in & l_in
+    # every recorded kernel joins exactly its own launch, with the drawn latency
+    assert (o["link"][krow[both]] == lrow[both]).all()
+    x = pr["start"][both] - pr["l_ts"][both]
+    assert (x == pr["lat"][both]).all()
+    hist = np.zeros(64, np.int64)
+    b = np.where(x <= 0, 0, np.floor(np.log2(np.maximum(x, 1))).astype(np.int64) + 1)
+    np.add.at(hist, b, 1)
+    assert (o["lat_hist"] == hist).all()
+    # unmatched launches are those whose kernel was dropped or fell outside
+    assert o["counters"]["n_unmatched_launches"] == int((l_in & ~(kept & k_in)).sum())
+    assert o["counters"]["n_unmatched_kernels"] == int((kept & k_in & ~l_in).sum())
+    # names of the recorded, admitted kernels
+    cnt = np.bincount(pr["name"][kept & k_in], minlength=p["n_names"])
+    assert (o["name_count"] == cnt).all()
+    # each drawn gap between queue neighbours that were both recorded shows up
+    gaps = set(zip(o["gap_stream"].tolist(), o["gap_begin"].tolist(), o["gap_end"].tolist()))
+    st = np.argsort(pr["start"], kind="stable")
+    ok = 0
+    for s in range(p["n_streams"]):
+        m = st[pr["stream"][st] == s]
+        for a, c in zip(m[:-1], m[1:]):
+            if pr["first_in_queue"][c] or not (kept[a] and kept[c]) or not (k_in[a] and k_in[c]):
+                continue
+            assert pr["start"][c] - pr["end"][a] == pr["gap"][c]
+            if pr["gap"][c] > p["gap_threshold"] and pr["end"][a] < W1:
+                assert (s, int(pr["end"][a]), int(pr["start"][c])) in gaps
+                ok += 1
+            elif pr["end"][a] < W1:
+                assert (s, int(pr["end"][a]), int(pr["start"][c])) not in gaps
+    assert ok > 0
+
+
+def test_config0_ground_truth(cfg0):
+    tr, (code, o) = cfg0
+    _truth_check(tr, o)
+
+
+def test_config1_ground_truth():
+    tr = synth.config1(n_steps=60)
+    code, o = oracle.analyze(tr.columns(), tr.params)
+    _truth_check(tr, o)
+
+
+# --------------------------------------------------------------------------- metamorphic
+
+def test_row_permutation(cfg0):
+    tr, (code, o) = cfg0
+    rng = np.random.default_rng(7)
+    perm = rng.permutation(tr.n)  # new row j holds old row perm[j]
+    inv = np.empty_like(perm)
+    inv[perm] = np.arange(tr.n)
+    t2 = tr.take(perm)
+    code2, o2 = oracle.analyze(t2.columns(), t2.params)
+    assert code2 == code
+    kind = tr.kind
+    for k in ("link", "aux"):
+        old = o[k][perm]
+        is_row = (old >= 0) & ((k == "link") | ((kind[perm] == 2) & (k == "aux")))
+        exp = np.where(is_row, inv[np.maximum(old, 0)], old)
+        assert (o2[k] == exp).all(), k
+    for k in ("op_nkern", "op_first", "op_last", "op_ksum"):
+        assert (o2[k] == o[k][perm]).all(), k
+    for k in ("busy", "idle", "lat_hist", "name_count", "name_sum", "name_min", "name_max", "gap_begin",
+              "gap_end", "gap_flags", "pair_overlap", "class_busy", "class_overlap", "any_busy"):
+        assert (o2[k] == o[k]).all(), k
+    for k in COUNTERS:
+        assert o2["counters"][k] == o["counters"][k]
+
+
+def test_global_time_shift(cfg0):
+    tr, (code, o) = cfg0
+    d = -123_456_789_012
+    cols = tr.columns()
+    cols["ts"] = cols["ts"] + d
+    cols["te"] = cols["te"] + d
+    p = dict(tr.params, window_begin=tr.params["window_begin"] + d, window_end=tr.params["window_end"] + d)
+    code2, o2 = oracle.analyze(cols, p)
+    for k in ("link", "aux", "op_nkern", "op_ksum", "busy", "idle", "lat_hist", "name_count", "name_sum",
+              "name_min", "name_max", "gap_flags", "pair_overlap", "any_busy"):
+        assert (o2[k] == o[k]).all(), k
+    ops = o["op_nkern"] > 0
+    assert (o2["op_first"][ops] == o["op_first"][ops] + d).all()
+    assert (o2["gap_begin"] == o["gap_begin"] + d).all() and (o2["gap_end"] == o["gap_end"] + d).all()
+
+
+@pytest.fixture(scope="module")
+def cfg3():
+    tr = synth.config3(n_procs=3, n_steps=20, n_edges=400)
+    return tr, oracle.analyze(tr.columns(), tr.params)
+
+
+def test_clock_offset_shift_changes_nothing(cfg3):
+    tr, (code, o) = cfg3
+    rng = np.random.default_rng(3)
+    delta = rng.integers(-10**6, 10**6, tr.params["n_procs"])
+    cols = tr.columns()
+    cols["ts"] = cols["ts"] + delta[tr.pid]
+    cols["te"] = cols["te"] + delta[tr.pid]
+    p = dict(tr.params, clock_offset=tr.params["clock_offset"] + delta)
+    code2, o2 = oracle.analyze(cols, p)
+    assert_same((code2, o2), (code, o), p, "offset shift")
+    assert (o["edge_status"] == 0).mean() > 0.9
+
+
+def test_clock_shift_without_offset_changes_waits(cfg3):
+    """Negative control: moving one process's clock without telling the
+    analyzer must change the cross-process waits."""
+    tr, (code, o) = cfg3
+    cols = tr.columns()
+    sel = tr.pid == 1
+    cols["ts"] = np.where(sel, cols["ts"] + 7_000, cols["ts"])
+    cols["te"] = np.where(sel, cols["te"] + 7_000, cols["te"])
+    code2, o2 = oracle.analyze(cols, tr.params)
+    e = tr.params["edges"]
+    touched = ((e["prod_pid"] == 1) | (e["cons_pid"] == 1)) & (o["edge_status"] == 0) & (o2["edge_status"] == 0)
+    assert touched.sum() > 10
+    assert (o2["edge_wait"][touched] != o["edge_wait"][touched]).all()
+
+
+def test_config3_edges_nonnegative_waits(cfg3):
+    """Consumers were drawn to start at or after their producer's end."""
+    tr, (code, o) = cfg3
+    ok = o["edge_status"] == 0
+    assert (o["edge_wait"][ok] >= 0).all()
+
+
+# --------------------------------------------------------------------------- errors
+
+def _t1():
+    cols, p, g = load_golden("t1_worked_timeline.json")
+    return {k: v.copy() for k, v in cols.items()}, p
+
+
+@pytest.mark.parametrize("field,row,value", [
+    ("kind", 3, 3), ("pid", 5, 1), ("pid", 5, -1), ("lane", 12, 2), ("lane", 4, 1), ("name", 12, 3),
+    ("name", 2, 4), ("name", 6, -1), ("te", 7, 12), ("corr", 9, -1), ("corr", 9, 1 << 48),
+    ("ts", 0, -(1 << 62)), ("te", 0, 1 << 62),
+])
+def test_invalid_row(field, row, value):
+    cols, p = _t1()
+    if field == "ts":
+        cols["te"][row] = value + 5
+    cols[field][row] = value
+    code, o = oracle.analyze(cols, p)
+    assert code == -2 and o["counters"]["first_invalid"] == row
+    b = bruteforce.analyze(cols, p)
+    assert b[0] == -2 and b[1]["counters"]["first_invalid"] == row
+
+
+def test_invalid_smallest_row_reported():
+    cols, p = _t1()
+    cols["kind"][14] = 9
+    cols["pid"][6] = 4
+    code, o = oracle.analyze(cols, p)
+    assert code == -2 and o["counters"]["first_invalid"] == 6
+
+
+def test_cpu_op_corr_is_not_validated():
+    cols, p = _t1()
+    cols["corr"][0] = -5
+    code, o = oracle.analyze(cols, p)
+    assert code == 0
+
+
+@pytest.mark.parametrize("change", [
+    dict(window_end=0), dict(window_end=-5), dict(window_end=(1 << 40) + 1), dict(n_procs=0),
+    dict(n_procs=4097), dict(n_streams=65), dict(n_streams=0), dict(n_threads=2049), dict(n_names=0),
+    dict(n_op_names=0), dict(clock_offset=np.array([1 << 62])), dict(stream_class=np.array([0, 3], np.uint8)),
+    dict(window_begin=-(1 << 62), window_end=-(1 << 62) + 100),
+])
+def test_invalid_params(change):
+    cols, p = _t1()
+    p.update(change)
+    code, o = oracle.analyze(cols, p)
+    assert code == -1
+
+
+def test_gap_capacity():
+    cols, p = _t1()
+    code, full = oracle.analyze(cols, p)
+    for cap in (0, 1, 2, 4):
+        code2, o = oracle.analyze(cols, p, gap_capacity=cap)
+        assert code2 == -3 and o["counters"]["n_gaps_total"] == 5
+        for k in ("gap_pid", "gap_stream", "gap_begin", "gap_end", "gap_flags"):
+            assert (o[k] == full[k][:cap]).all()
+        assert (o["link"] == full["link"]).all() and (o["busy"] == full["busy"]).all()
+    code3, o = oracle.analyze(cols, p, gap_capacity=5)
+    assert code3 == 0
+
+
+def test_empty_trace():
+    p = synth.empty_params(n_procs=2, n_streams=3, gap_threshold=10, flags=3)
+    cols = dict(ts=np.zeros(0, np.int64), te=np.zeros(0, np.int64), corr=np.zeros(0, np.int64),
+                pid=np.zeros(0, np.int32), lane=np.zeros(0, np.int32), name=np.zeros(0, np.int32),
+                kind=np.zeros(0, np.uint8))
+    code, o = oracle.analyze(cols, p)
+    W = p["window_end"] - p["window_begin"]
+    assert code == 0 and (o["busy"] == 0).all() and (o["idle"] == W).all()
+    assert o["counters"]["n_gaps_total"] == 6 and (o["gap_flags"] == 3).all()
+    assert (o["name_min"] == I64_MAX).all() and (o["name_max"] == I64_MIN).all()
+    assert (o["any_busy"] == 0).all() and o["lat_hist"].sum() == 0
