@@ -64,11 +64,12 @@ enum {
 /* Implementation limits (checked; EINVAL when exceeded). */
 #define HERSCHEL_MAX_PROCS 4096
 #define HERSCHEL_MAX_STREAMS 64
-#define HERSCHEL_MAX_THREADS 2048
+#define HERSCHEL_MAX_THREADS 512
 #define HERSCHEL_MAX_WINDOW (1LL << 40)  /* W1 - W0 in ns (about 18 minutes) */
 #define HERSCHEL_MAX_ABS_TIME (1LL << 62) /* |ts|, |te|, |W0|, |W1|, |clock offset| must be below */
 #define HERSCHEL_CORR_LIMIT (1LL << 48)   /* LAUNCH/KERNEL corr must lie in [0, 2^48) */
 #define HERSCHEL_MAX_NAMES (1 << 24)
+#define HERSCHEL_MAX_ROWS (1LL << 30)      /* n must be below */
 
 /* Input records as a structure of arrays, n rows, in any order (delivery
  * order).  37 bytes per row.  Row i is valid iff

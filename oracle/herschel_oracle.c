@@ -70,12 +70,12 @@ static int row_is_valid(const hro_events *ev, int64_t i, const hro_params *p) {
 }
 
 static int params_ok(int64_t n, const hro_params *p) {
-  if (n < 0 || n >= (1LL << 31)) return 0;
+  if (n < 0 || n >= (1LL << 30)) return 0;
   if (!in_abs(p->w0) || !in_abs(p->w1) || p->w1 <= p->w0) return 0;
   if (p->w1 - p->w0 > (1LL << 40)) return 0;
   if (p->n_procs < 1 || p->n_procs > 4096) return 0;
   if (p->n_streams < 1 || p->n_streams > 64) return 0;
-  if (p->n_threads < 1 || p->n_threads > 2048) return 0;
+  if (p->n_threads < 1 || p->n_threads > 512) return 0;
   if (p->n_names < 1 || p->n_names > (1 << 24)) return 0;
   if (p->n_op_names < 1) return 0;
   if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return 0;

@@ -1,0 +1,431 @@
+// C ABI of the trace analyzer: argument checks, workspace layout, the order
+// of the stages on the caller's stream, and the return code.
+#include <string.h>
+
+#include "internal.hpp"
+
+namespace hx {
+
+int names_block_count(int64_t n_max, int NN);
+int names_lds_limit();
+
+static int bits_host(uint64_t x) {
+  int b = 0;
+  while (x) {
+    ++b;
+    x >>= 1;
+  }
+  return b;
+}
+
+// ---------------------------------------------------------------- layout
+static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Bump {
+  char* base;
+  size_t off = 0;
+  template <class T>
+  T* take(int64_t count) {
+    T* p = base ? (T*)(base + off) : nullptr;
+    off = align_up(off + (size_t)std::max<int64_t>(count, 1) * sizeof(T));
+    return p;
+  }
+};
+
+static void sort_plan(SortBufs& s, int id, int64_t n_max, int key_bits, bool vals) {
+  s.id = id;
+  s.n_max = n_max;
+  s.tiles_max = cdiv(std::max<int64_t>(n_max, 1), RS_TILE);
+  s.nd = (key_bits + 7) / 8;
+  (void)vals;
+}
+
+size_t layout_workspace(Ctx& c, char* base) {
+  Bump b{base};
+  const int64_t n = std::max<int64_t>(c.n, 1);
+  c.ds = b.take<DevState>(1);
+  // region cleared by the init kernel
+  c.zero_begin = base ? base + b.off : nullptr;
+  const size_t z0 = b.off;
+  c.prep_tiles = cdiv(c.n, prep_tile_rows());
+  c.prep_status = b.take<uint64_t>(3 * std::max<int64_t>(c.prep_tiles, 1));
+  c.union_tiles = std::max<int64_t>(cdiv(n, union_tile_elems()), 1);
+  c.union_status = b.take<uint64_t>(3 * c.union_tiles);
+  sort_plan(c.sK, 0, n, c.pb + c.sb + c.wb, true);
+  sort_plan(c.sJ, 1, n, 49 + c.pb, true);
+  sort_plan(c.sC, 2, n, c.pb + c.tb + c.wb + 1, true);
+  sort_plan(c.sE, 3, 2 * n, c.pb + c.wb1 + c.sb, false);
+  c.sK.status = b.take<uint32_t>((int64_t)c.sK.nd * c.sK.tiles_max * 256);
+  c.sJ.status = b.take<uint32_t>((int64_t)c.sJ.nd * c.sJ.tiles_max * 256);
+  if (c.contain) {
+    c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
+    c.vb_status = b.take<uint64_t>(c.vb_tiles);
+    c.sC.status = b.take<uint32_t>((int64_t)c.sC.nd * c.sC.tiles_max * 256);
+  }
+  if (c.overlap) {
+    c.sweep_tiles = std::max<int64_t>(cdiv(2 * n, 4096), 1);
+    c.sweep_status = b.take<uint64_t>(2 * c.sweep_tiles);
+    c.sE.status = b.take<uint32_t>((int64_t)c.sE.nd * c.sE.tiles_max * 256);
+  }
+  c.zero_bytes = align_up(b.off - z0);
+  // sort buffers
+  for (SortBufs* s : {&c.sK, &c.sJ, &c.sC}) {
+    if (s == &c.sC && !c.contain) {
+      // the containment list is still compacted by prep (ops and launches)
+      s->k[0] = b.take<uint64_t>(n);
+      s->v[0] = b.take<uint32_t>(n);
+      continue;
+    }
+    s->k[0] = b.take<uint64_t>(n);
+    s->k[1] = b.take<uint64_t>(n);
+    s->v[0] = b.take<uint32_t>(n);
+    s->v[1] = b.take<uint32_t>(n);
+  }
+  if (c.overlap) {
+    c.sE.k[0] = b.take<uint64_t>(2 * n);
+    c.sE.k[1] = b.take<uint64_t>(2 * n);
+  }
+  if (c.contain) {
+    c.V = b.take<uint64_t>(n);
+    c.nlev = 3;
+    while (cdiv(n, (int64_t)1 << (6 * (c.nlev - 1))) > 64) ++c.nlev;
+    c.M[0] = nullptr;
+    c.Mn[0] = n;
+    for (int l = 1; l < c.nlev; ++l) {
+      c.Mn[l] = cdiv(n, (int64_t)1 << (6 * l));
+      c.M[l] = b.take<uint64_t>(c.Mn[l]);
+    }
+    c.pmt = b.take<uint64_t>(c.vb_tiles);
+    c.par = b.take<int32_t>(n);
+    c.tie_cap = cdiv(n, 33) + 1;
+    c.tie_list = b.take<int32_t>(c.tie_cap);
+    c.tie_scratch = b.take<uint64_t>(4 * n);
+    c.lk_first = b.take<int64_t>(n);
+    c.lk_last = b.take<int64_t>(n);
+    c.lk_sum = b.take<int64_t>(n);
+  }
+  c.name_blocks = names_block_count(n, c.NN);
+  if (c.NN <= names_lds_limit()) c.name_part = b.take<uint64_t>((int64_t)c.name_blocks * c.NN * 4);
+  return b.off;
+}
+
+// ------------------------------------------------------------ init, final
+struct InitArgs {
+  DevState* ds;
+  uint4* zero;
+  int64_t zero_n;  // 16-byte words
+  herschel_counters* cnt;
+  int64_t* busy;
+  int nps;
+  int64_t* lat_hist;
+  bool overlap;
+  int64_t* pair;
+  int64_t* class_busy;
+  int64_t* class_overlap;
+  int64_t* any_busy;
+  int P, S;
+  bool names_direct;
+  int NN;
+  int64_t* name_count;
+  int64_t* name_sum;
+  int64_t* name_min;
+  int64_t* name_max;
+  const int64_t* off;
+  const uint8_t* cls;
+};
+
+__global__ __launch_bounds__(256) void k_init(InitArgs a) {
+  const int64_t tid = (int64_t)blockIdx.x * 256 + threadIdx.x, nth = (int64_t)gridDim.x * 256;
+  for (int64_t i = tid; i < a.zero_n; i += nth) a.zero[i] = make_uint4(0, 0, 0, 0);
+  if (blockIdx.x == 0) {
+    uint32_t* d = (uint32_t*)a.ds;
+    for (int i = threadIdx.x; i < (int)(sizeof(DevState) / 4); i += 256) d[i] = 0;
+    __syncthreads();
+    if (threadIdx.x == 0) a.ds->first_invalid = I64MAX;
+    int64_t* cz = (int64_t*)a.cnt;
+    for (int i = threadIdx.x; i < (int)(sizeof(herschel_counters) / 8); i += 256) cz[i] = 0;
+    if (threadIdx.x < 64) a.lat_hist[threadIdx.x] = 0;
+    bool bad = false;
+    if (a.off)
+      for (int q = threadIdx.x; q < a.P; q += 256)
+        bad |= !(a.off[q] > -HERSCHEL_MAX_ABS_TIME && a.off[q] < HERSCHEL_MAX_ABS_TIME);
+    if (a.cls)
+      for (int s = threadIdx.x; s < a.S; s += 256) bad |= a.cls[s] > 2;
+    if (bad) atomicOr(&a.ds->status, DS_PARAM);
+  }
+  for (int64_t i = tid; i < a.nps; i += nth) a.busy[i] = 0;
+  if (a.overlap) {
+    for (int64_t i = tid; i < (int64_t)a.nps * a.S; i += nth) a.pair[i] = 0;
+    for (int64_t i = tid; i < (int64_t)a.P * 3; i += nth) a.class_busy[i] = 0;
+    for (int64_t i = tid; i < (int64_t)a.P * 9; i += nth) a.class_overlap[i] = 0;
+    for (int64_t i = tid; i < a.P; i += nth) a.any_busy[i] = 0;
+  }
+  if (a.names_direct)
+    for (int64_t i = tid; i < a.NN; i += nth) {
+      a.name_count[i] = 0;
+      a.name_sum[i] = 0;
+      a.name_min[i] = I64MAX;
+      a.name_max[i] = I64MIN;
+    }
+}
+
+void launch_init(Ctx& c) {
+  InitArgs a;
+  a.ds = c.ds;
+  a.zero = (uint4*)c.zero_begin;
+  a.zero_n = (int64_t)(c.zero_bytes / 16);
+  a.cnt = c.o.counters;
+  a.busy = c.o.busy;
+  a.nps = c.P * c.S;
+  a.lat_hist = c.o.lat_hist;
+  a.overlap = c.overlap;
+  a.pair = c.o.pair_overlap;
+  a.class_busy = c.o.class_busy;
+  a.class_overlap = c.o.class_overlap;
+  a.any_busy = c.o.any_busy;
+  a.P = c.P;
+  a.S = c.S;
+  a.names_direct = c.NN > names_lds_limit();
+  a.NN = c.NN;
+  a.name_count = c.o.name_count;
+  a.name_sum = c.o.name_sum;
+  a.name_min = c.o.name_min;
+  a.name_max = c.o.name_max;
+  a.off = c.p.clock_offset;
+  a.cls = c.p.stream_class;
+  const int64_t work = std::max<int64_t>({a.zero_n, (int64_t)a.nps * (c.overlap ? c.S : 1), (int64_t)c.NN, 1});
+  const int grid = (int)std::min<int64_t>(cdiv(work, 256 * 4), 2048);
+  hipLaunchKernelGGL(k_init, dim3(std::max(grid, 1)), dim3(256), 0, c.st, a);
+}
+
+// Without containment, admitted ops and launches have no op links.
+__global__ __launch_bounds__(256) void k_nocontain(const uint64_t* keys, const uint32_t* rows, DevState* ds,
+                                                    int32_t* link, int32_t* aux) {
+  const int64_t n = ds->nCL;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const uint32_t r = rows[i];
+    link[r] = -1;
+    if ((keys[i] & 1) == 0) aux[r] = -1;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counters* cnt, int64_t* busy, int64_t* idle,
+                                                  int nps, int64_t W) {
+  for (int i = threadIdx.x; i < nps; i += 256) idle[i] = W - busy[i];
+  if (threadIdx.x == 0) {
+    cnt->first_invalid = ds->first_invalid == I64MAX ? -1 : ds->first_invalid;
+    cnt->device_status = ds->status;
+  }
+}
+
+void launch_finalize(Ctx& c) {
+  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, c.st, c.ds, c.o.counters, c.o.busy, c.o.idle, c.P * c.S, c.W);
+}
+
+// ------------------------------------------------------------- the call
+static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const herschel_params* p,
+                          const herschel_outputs* out) {
+  if (!ev || !p || !out) return HERSCHEL_EINVAL;
+  if (n < 0 || n >= (1LL << 30)) return HERSCHEL_EINVAL;
+  if (n > 0 && (!ev->ts || !ev->te || !ev->corr || !ev->pid || !ev->lane || !ev->name || !ev->kind))
+    return HERSCHEL_EINVAL;
+  const int64_t W0 = p->window_begin, W1 = p->window_end;
+  if (!(W0 > -HERSCHEL_MAX_ABS_TIME && W0 < HERSCHEL_MAX_ABS_TIME)) return HERSCHEL_EINVAL;
+  if (!(W1 > -HERSCHEL_MAX_ABS_TIME && W1 < HERSCHEL_MAX_ABS_TIME)) return HERSCHEL_EINVAL;
+  if (W1 <= W0 || W1 - W0 > HERSCHEL_MAX_WINDOW) return HERSCHEL_EINVAL;
+  if (p->n_procs < 1 || p->n_procs > HERSCHEL_MAX_PROCS) return HERSCHEL_EINVAL;
+  if (p->n_streams < 1 || p->n_streams > HERSCHEL_MAX_STREAMS) return HERSCHEL_EINVAL;
+  if (p->n_threads < 1 || p->n_threads > HERSCHEL_MAX_THREADS) return HERSCHEL_EINVAL;
+  if (p->n_names < 1 || p->n_names > HERSCHEL_MAX_NAMES) return HERSCHEL_EINVAL;
+  if (p->n_op_names < 1) return HERSCHEL_EINVAL;
+  if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return HERSCHEL_EINVAL;
+  if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP)) return HERSCHEL_EINVAL;
+  const bool contain = (p->flags & HERSCHEL_OUT_CONTAIN) != 0, overlap = (p->flags & HERSCHEL_OUT_OVERLAP) != 0;
+  if (!out->counters || !out->link || !out->aux || !out->busy || !out->idle || !out->name_count ||
+      !out->name_sum || !out->name_min || !out->name_max || !out->lat_hist)
+    return HERSCHEL_EINVAL;
+  if (out->gap_capacity < 0) return HERSCHEL_EINVAL;
+  if (out->gap_capacity > 0 &&
+      (!out->gap_pid || !out->gap_stream || !out->gap_begin || !out->gap_end || !out->gap_flags))
+    return HERSCHEL_EINVAL;
+  if (contain && (!out->op_nkern || !out->op_first || !out->op_last || !out->op_ksum)) return HERSCHEL_EINVAL;
+  if (overlap && (!out->pair_overlap || !out->class_busy || !out->class_overlap || !out->any_busy))
+    return HERSCHEL_EINVAL;
+  if (p->n_edges > 0 && (!out->edge_wait || !out->edge_status)) return HERSCHEL_EINVAL;
+
+  c.st = (hipStream_t)p->hip_stream;
+  c.ev = *ev;
+  c.n = n;
+  c.p = *p;
+  c.o = *out;
+  c.W0 = W0;
+  c.W1 = W1;
+  c.W = W1 - W0;
+  c.thr = p->gap_threshold;
+  c.P = p->n_procs;
+  c.S = p->n_streams;
+  c.T = p->n_threads;
+  c.NN = p->n_names;
+  c.NOP = p->n_op_names;
+  c.contain = contain;
+  c.overlap = overlap;
+  c.pb = bits_host((uint64_t)(c.P - 1));
+  c.sb = bits_host((uint64_t)(c.S - 1));
+  c.tb = bits_host((uint64_t)(c.T - 1));
+  c.wb = bits_host((uint64_t)(c.W - 1));
+  c.wb1 = bits_host((uint64_t)c.W);
+  c.vb = bits_host((uint64_t)c.W + 1);
+  return HERSCHEL_OK;
+}
+
+static int enqueue(Ctx& c) {
+  static bool lds_attr = false;
+  if (!lds_attr) {
+    names_set_lds_attr();
+    lds_attr = true;
+  }
+  launch_init(c);
+  launch_prep(c);
+  launch_hist(c, c.sK, &c.ds->nK);
+  launch_hist(c, c.sJ, &c.ds->nJ);
+  if (c.contain) launch_hist(c, c.sC, &c.ds->nCL);
+  launch_names(c);
+  launch_sort(c, c.sK, &c.ds->nK);
+  launch_timeline(c);
+  if (c.overlap) launch_overlap(c);
+  if (c.contain) {
+    launch_sort(c, c.sC, &c.ds->nCL);
+    launch_contain(c);
+  } else {
+    const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.n, 256 * 8), 1), 2048);
+    hipLaunchKernelGGL(k_nocontain, dim3(grid), dim3(256), 0, c.st, c.sC.k[0], c.sC.v[0], c.ds, c.o.link, c.o.aux);
+  }
+  launch_sort(c, c.sJ, &c.ds->nJ);
+  launch_join(c);
+  if (c.contain) launch_opagg(c);
+  launch_edges(c);
+  launch_names_reduce(c);
+  launch_finalize(c);
+  return hipGetLastError() == hipSuccess ? HERSCHEL_OK : HERSCHEL_EDEVICE;
+}
+
+static int code_from(const herschel_counters& h, int64_t gap_capacity) {
+  if (h.device_status & DS_PARAM) return HERSCHEL_EINVAL;
+  if (h.first_invalid >= 0) return HERSCHEL_EEVENT;
+  if (h.device_status) return HERSCHEL_EDEVICE;
+  if (h.n_gaps_total > gap_capacity) return HERSCHEL_ECAPACITY;
+  return HERSCHEL_OK;
+}
+
+}  // namespace hx
+
+using namespace hx;
+
+extern "C" {
+
+const char* herschel_strerror(int code) {
+  switch (code) {
+    case HERSCHEL_OK: return "ok";
+    case HERSCHEL_EINVAL: return "invalid argument";
+    case HERSCHEL_EEVENT: return "invalid input row (see counters.first_invalid)";
+    case HERSCHEL_ECAPACITY: return "gap list capacity exceeded (see counters.n_gaps_total)";
+    case HERSCHEL_EWORKSPACE: return "workspace missing or too small";
+    case HERSCHEL_EDEVICE: return "device error";
+    default: return "unknown error";
+  }
+}
+
+int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) {
+  if (!p || !bytes || n < 0 || n >= (1LL << 30)) return HERSCHEL_EINVAL;
+  if (p->window_end <= p->window_begin || p->window_end - p->window_begin > HERSCHEL_MAX_WINDOW)
+    return HERSCHEL_EINVAL;
+  if (p->n_procs < 1 || p->n_procs > HERSCHEL_MAX_PROCS || p->n_streams < 1 ||
+      p->n_streams > HERSCHEL_MAX_STREAMS || p->n_threads < 1 || p->n_threads > HERSCHEL_MAX_THREADS ||
+      p->n_names < 1 || p->n_names > HERSCHEL_MAX_NAMES)
+    return HERSCHEL_EINVAL;
+  Ctx c;
+  c.n = n;
+  c.P = p->n_procs;
+  c.S = p->n_streams;
+  c.T = p->n_threads;
+  c.NN = p->n_names;
+  c.W = p->window_end - p->window_begin;
+  c.contain = (p->flags & HERSCHEL_OUT_CONTAIN) != 0;
+  c.overlap = (p->flags & HERSCHEL_OUT_OVERLAP) != 0;
+  c.pb = bits_host((uint64_t)(c.P - 1));
+  c.sb = bits_host((uint64_t)(c.S - 1));
+  c.tb = bits_host((uint64_t)(c.T - 1));
+  c.wb = bits_host((uint64_t)(c.W - 1));
+  c.wb1 = bits_host((uint64_t)c.W);
+  c.vb = bits_host((uint64_t)c.W + 1);
+  *bytes = layout_workspace(c, nullptr);
+  return HERSCHEL_OK;
+}
+
+static int prepare(Ctx& c, const herschel_events* ev, int64_t n, const herschel_params* p, const herschel_outputs* out,
+                   void* ws, size_t ws_bytes) {
+  int code = check_and_plan(c, ev, n, p, out);
+  if (code) return code;
+  const size_t need = layout_workspace(c, nullptr);
+  if (!ws || ws_bytes < need) return HERSCHEL_EWORKSPACE;
+  layout_workspace(c, (char*)ws);
+  return HERSCHEL_OK;
+}
+
+int herschel_trace_analyze(const herschel_events* ev, int64_t n, const herschel_params* p, herschel_outputs* out) {
+  Ctx c;
+  int code = prepare(c, ev, n, p, out, p ? p->workspace : nullptr, p ? p->workspace_bytes : 0);
+  if (code) return code;
+  code = enqueue(c);
+  if (code) return code;
+  herschel_counters h;
+  if (hipMemcpyAsync(&h, out->counters, sizeof(h), hipMemcpyDeviceToHost, c.st) != hipSuccess) return HERSCHEL_EDEVICE;
+  if (hipStreamSynchronize(c.st) != hipSuccess) return HERSCHEL_EDEVICE;
+  return code_from(h, out->gap_capacity);
+}
+
+int herschel_trace_analyze_batch(const herschel_events* ev, const int64_t* trace_offsets, int32_t n_traces,
+                                 const herschel_params* p, herschel_outputs* out) {
+  if (!ev || !trace_offsets || !p || !out || n_traces < 0) return HERSCHEL_EINVAL;
+  if (n_traces == 0) return HERSCHEL_OK;
+  for (int32_t t = 0; t < n_traces; ++t)
+    if (trace_offsets[t + 1] < trace_offsets[t] || trace_offsets[t] < 0) return HERSCHEL_EINVAL;
+  int first_err = HERSCHEL_OK;
+  int32_t launched = 0;
+  for (int32_t t = 0; t < n_traces; ++t) {
+    herschel_events e = *ev;
+    const int64_t o = trace_offsets[t];
+    if (trace_offsets[t + 1] > o) {
+      e.ts += o;
+      e.te += o;
+      e.corr += o;
+      e.pid += o;
+      e.lane += o;
+      e.name += o;
+      e.kind += o;
+    }
+    herschel_params pt = p[t];
+    pt.hip_stream = p[0].hip_stream;
+    pt.workspace = p[0].workspace;
+    pt.workspace_bytes = p[0].workspace_bytes;
+    Ctx c;
+    int code = prepare(c, &e, trace_offsets[t + 1] - o, &pt, &out[t], pt.workspace, pt.workspace_bytes);
+    if (!code) code = enqueue(c);
+    if (code) {
+      if (first_err == HERSCHEL_OK) first_err = code;
+      break;
+    }
+    launched = t + 1;
+  }
+  hipStream_t st = (hipStream_t)p[0].hip_stream;
+  if (hipStreamSynchronize(st) != hipSuccess) return HERSCHEL_EDEVICE;
+  for (int32_t t = 0; t < launched; ++t) {
+    herschel_counters h;
+    if (hipMemcpy(&h, out[t].counters, sizeof(h), hipMemcpyDeviceToHost) != hipSuccess) return HERSCHEL_EDEVICE;
+    const int code = code_from(h, out[t].gap_capacity);
+    if (code != HERSCHEL_OK) return code;
+  }
+  return first_err;
+}
+
+}  // extern "C"

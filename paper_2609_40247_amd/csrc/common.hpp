@@ -1,0 +1,278 @@
+// Shared device helpers and internal data layout of the HIP trace analyzer.
+//
+// Everything here is CDNA4 (gfx950) wave64 code: 64-bit ballots, LDS
+// staging, decoupled look-back scans with a tile ticket, and agent-scope
+// atomics for the few cross-workgroup values.  Arithmetic is integer only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "herschel.h"
+
+#ifndef HERSCHEL_CHECKED
+#define HERSCHEL_CHECKED 0
+#endif
+
+namespace hx {
+
+constexpr int WAVE = 64;
+constexpr int64_t I64MAX = INT64_MAX;
+constexpr int64_t I64MIN = INT64_MIN;
+
+// Internal device-status bits (herschel_counters::device_status).
+enum : uint32_t {
+  DS_SPIN = 1u,      // a look-back wait exceeded its bound
+  DS_OOB = 2u,       // checked build: an index left its buffer
+  DS_PARAM = 4u,     // clock_offset or stream_class out of range
+  DS_TIES = 8u,      // more long runs of equal op starts than the list holds
+  DS_CAPACITY = 16u  // an internal list overflowed its bound
+};
+
+// Ticket slots: one per look-back kernel launch in a call.
+enum : int {
+  TK_PREP = 0,
+  TK_UNION = 1,
+  TK_VBUILD = 2,
+  TK_SWEEP = 3,
+  TK_RADIX = 8  // + 8 * sort + pass
+};
+constexpr int N_TICKETS = TK_RADIX + 8 * 4;
+
+constexpr int N_SORTS = 4;  // 0 timeline, 1 join, 2 containment, 3 overlap events
+
+// Per-call device state, zeroed by the init kernel.
+struct DevState {
+  uint32_t ticket[N_TICKETS];
+  uint32_t status;
+  uint32_t sort_parity[N_SORTS];  // buffer holding each sort's result
+  int32_t nK;   // admitted kernels (timeline list)
+  int32_t nCL;  // admitted ops + launches (containment list)
+  int32_t nJ;   // admitted launches + kernels (join list)
+  int32_t nEv;  // overlap events (2 per coverage run)
+  int32_t n_long_ties;
+  int32_t pad0;
+  int64_t first_invalid;  // smallest bad row (INT64_MAX = none)
+  int64_t n_gaps;
+  uint32_t hist[N_SORTS][8][256];  // radix digit histograms
+};
+
+// Largest process count the per-process correlation-id table supports.
+constexpr int MAX_PROCS = HERSCHEL_MAX_PROCS;
+
+// ---------------------------------------------------------------- wave ops
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  int l = lane_id();
+  return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+__device__ __forceinline__ int popc(uint64_t m) { return __popcll(m); }
+
+template <class T>
+__device__ __forceinline__ T shfl(T v, int src) { return __shfl(v, src, WAVE); }
+template <class T>
+__device__ __forceinline__ T shfl_up(T v, unsigned d) { return __shfl_up(v, d, WAVE); }
+template <class T>
+__device__ __forceinline__ T shfl_down(T v, unsigned d) { return __shfl_down(v, d, WAVE); }
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+  for (int d = 32; d >= 1; d >>= 1) v += shfl_down(v, d);
+  return shfl(v, 0);
+}
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
+  return (int64_t)wave_sum_u64((uint64_t)v);
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+  for (int d = 32; d >= 1; d >>= 1) {
+    uint64_t o = shfl_down(v, d);
+    v = o > v ? o : v;
+  }
+  return shfl(v, 0);
+}
+__device__ __forceinline__ int64_t wave_min_i64(int64_t v) {
+  for (int d = 32; d >= 1; d >>= 1) {
+    int64_t o = shfl_down(v, d);
+    v = o < v ? o : v;
+  }
+  return shfl(v, 0);
+}
+__device__ __forceinline__ int64_t wave_max_i64(int64_t v) {
+  for (int d = 32; d >= 1; d >>= 1) {
+    int64_t o = shfl_down(v, d);
+    v = o > v ? o : v;
+  }
+  return shfl(v, 0);
+}
+// Inclusive prefix sum across the wave.
+__device__ __forceinline__ uint32_t wave_incl_sum_u32(uint32_t v) {
+  int l = lane_id();
+  for (int d = 1; d < WAVE; d <<= 1) {
+    uint32_t o = shfl_up(v, d);
+    if (l >= d) v += o;
+  }
+  return v;
+}
+
+// --------------------------------------------------------- memory helpers
+__device__ __forceinline__ uint64_t ld_agent(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_agent(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void set_status(DevState* ds, uint32_t bit) {
+  atomicOr(&ds->status, bit);
+}
+
+// Bounds check of a data-dependent index (only in checked builds): on a
+// violation the status bit is set and the caller skips the access.
+__device__ __forceinline__ bool in_range(DevState* ds, int64_t i, int64_t n) {
+#if HERSCHEL_CHECKED
+  if ((uint64_t)i >= (uint64_t)n) {
+    set_status(ds, DS_OOB);
+    return false;
+  }
+#else
+  (void)ds;
+  (void)i;
+  (void)n;
+#endif
+  return true;
+}
+
+// Bound on look-back waits: ~2^22 sleeps of 64 cycles (about 0.1 s).  A wait
+// that runs out sets DS_SPIN and gives up, so a logic error can never hang.
+constexpr uint32_t SPIN_LIMIT = 1u << 22;
+
+// ------------------------------------------------------ decoupled look-back
+// 64-bit status words: bits 62-63 flag (0 empty, 1 aggregate, 2 prefix),
+// bits 0-61 value.
+constexpr uint64_t LB_AGG = 1ull << 62;
+constexpr uint64_t LB_PRE = 2ull << 62;
+constexpr uint64_t LB_VAL = (1ull << 62) - 1;
+
+struct OpSum {
+  __device__ static uint64_t combine(uint64_t older, uint64_t newer) { return (older + newer) & LB_VAL; }
+  __device__ static uint64_t identity() { return 0; }
+};
+struct OpMax {
+  __device__ static uint64_t combine(uint64_t older, uint64_t newer) { return older > newer ? older : newer; }
+  __device__ static uint64_t identity() { return 0; }
+};
+struct OpXor32 {
+  __device__ static uint64_t combine(uint64_t older, uint64_t newer) { return (older ^ newer) & 0xffffffffull; }
+  __device__ static uint64_t identity() { return 0; }
+};
+// Segmented max: value = seg (bits 42..59) | head (bit 41) | m (bits 0..40).
+// head: the span contains a segment start; m: max over the span's last
+// segment (0 = none); seg: segment of the span's last element.
+struct OpSegMax {
+  static constexpr uint64_t M_MASK = (1ull << 41) - 1;
+  static constexpr uint64_t HEAD = 1ull << 41;
+  __device__ static uint64_t make(uint32_t seg, bool head, uint64_t m) {
+    return ((uint64_t)seg << 42) | (head ? HEAD : 0) | (m & M_MASK);
+  }
+  __device__ static uint32_t seg(uint64_t v) { return (uint32_t)(v >> 42); }
+  __device__ static uint64_t m(uint64_t v) { return v & M_MASK; }
+  __device__ static uint64_t combine(uint64_t older, uint64_t newer) {
+    if (newer & HEAD) return newer;
+    uint64_t a = older & M_MASK, b = newer & M_MASK;
+    return (newer & ~(M_MASK | HEAD)) | (older & HEAD) | (a > b ? a : b);
+  }
+  __device__ static uint64_t identity() { return 0; }
+};
+
+// Decoupled look-back executed by ONE whole wave.  Publishes the tile's
+// aggregate, combines the predecessors' values newest-first 64 at a time,
+// publishes the inclusive prefix and returns the exclusive prefix (all
+// lanes).  Tile 0 publishes its prefix directly.
+template <class Op>
+__device__ uint64_t wave_lookback(uint64_t* status, int tile, uint64_t agg, DevState* ds) {
+  const int lane = lane_id();
+  if (tile == 0) {
+    if (lane == 0) st_agent(&status[0], LB_PRE | (agg & LB_VAL));
+    return Op::identity();
+  }
+  if (lane == 0) st_agent(&status[tile], LB_AGG | (agg & LB_VAL));
+  uint64_t acc = Op::identity();  // combination of the newer windows so far
+  bool have = false;
+  int pred = tile - 1;
+  bool give_up = false;
+  while (true) {
+    int idx = pred - lane;
+    uint64_t s = idx >= 0 ? ld_agent(&status[idx]) : (LB_PRE | Op::identity());
+    uint32_t spins = 0;
+    while (ballot((s >> 62) == 0)) {
+      if ((s >> 62) == 0) s = ld_agent(&status[idx]);
+      if (++spins > SPIN_LIMIT) {
+        give_up = true;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (give_up) break;
+    uint64_t pre_mask = ballot((s >> 62) == 2);
+    int last = pre_mask ? (__ffsll((unsigned long long)pre_mask) - 1) : (WAVE - 1);
+    // ordered fold over lanes 0..last, lane 0 newest: w = v[last] o ... o v[0]
+    uint64_t v = (lane <= last) ? (s & LB_VAL) : Op::identity();
+    for (int d = 1; d < WAVE; d <<= 1) {
+      uint64_t o = shfl_down(v, d);  // lane + d is older
+      if (lane + d <= last && (lane & ((d << 1) - 1)) == 0) v = Op::combine(o, v);
+    }
+    uint64_t w = shfl(v, 0);
+    acc = have ? Op::combine(w, acc) : w;
+    have = true;
+    if (pre_mask) break;
+    pred -= WAVE;
+  }
+  if (give_up) {
+    if (lane == 0) set_status(ds, DS_SPIN);
+    acc = Op::identity();
+  }
+  if (lane == 0) st_agent(&status[tile], LB_PRE | (Op::combine(acc, agg) & LB_VAL));
+  return acc;
+}
+
+// Tile ticket: tiles are handed out in launch order, so every predecessor a
+// look-back waits on is already running.
+__device__ __forceinline__ int take_ticket(DevState* ds, int slot, int* smem) {
+  if (threadIdx.x == 0) *smem = (int)atomicAdd(&ds->ticket[slot], 1u);
+  __syncthreads();
+  return *smem;
+}
+
+// ------------------------------------------------------------ block scans
+// Exclusive sum over a block of NT threads (NT a multiple of 64, <= 1024).
+template <int NT>
+__device__ uint32_t block_excl_sum(uint32_t v, uint32_t* scratch /* >= NT/64 + 1 */, uint32_t* total) {
+  const int lane = lane_id(), wv = threadIdx.x / WAVE;
+  uint32_t inc = wave_incl_sum_u32(v);
+  if (lane == WAVE - 1) scratch[wv] = inc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+    for (int w = 0; w < NT / WAVE; ++w) {
+      uint32_t t = scratch[w];
+      scratch[w] = run;
+      run += t;
+    }
+    scratch[NT / WAVE] = run;
+  }
+  __syncthreads();
+  uint32_t r = scratch[wv] + inc - v;
+  if (total) *total = scratch[NT / WAVE];
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ int bits_of(uint64_t x) { return x == 0 ? 0 : 64 - __clzll((long long)x); }
+
+}  // namespace hx

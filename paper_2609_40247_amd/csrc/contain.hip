@@ -1,0 +1,567 @@
+// Containment: op nesting, launch -> op, per-op inclusive aggregates.
+//
+// Kernel composition (Section 6.1) needs each launch's enclosing Python call
+// and each call's parent; calls are recorded with their native thread and
+// nest (Section 5.2).  With the admitted ops and launches of a thread sorted
+// by (ts' up, te' down, row up; ops before launches at equal ts'), the parent
+// of an op and the op of a launch are both "the nearest earlier op whose end
+// lies after my start".  That is a previous-greater query: every op stores
+// V = (thread segment, min(te', W1)) packed so that one unsigned comparison
+// against (my segment, my ts') decides both "same thread" and "ends after my
+// start"; launches store 0.  A 64-ary max pyramid over V (levels in LDS for
+// the tile, in HBM above it) and an exclusive prefix max per position answer
+// the query by walking back only as far as the answer.
+//
+// The answers form a forest whose preorder is the sorted order, so the
+// subtree of an op is a contiguous range.  Inclusive aggregates (T_op: first
+// kernel start, last kernel end, Section 6.1) are accumulated per tile in
+// LDS; only the few ops still open at a tile edge go through global atomics.
+#include "internal.hpp"
+
+namespace hx {
+
+constexpr int CT_THREADS = 256;
+constexpr int CT_ITEMS = 16;
+constexpr int CT_TILE = CT_THREADS * CT_ITEMS;  // 4096 positions = one M2 entry
+constexpr int TIE_SHORT = 32;
+
+struct ContainArgs {
+  uint64_t* k[2];
+  uint32_t* v[2];
+  const int64_t* ts;
+  const int64_t* te;
+  const int64_t* off;
+  int64_t W0, W1, W;
+  int tb, wb, vb;
+  DevState* ds;
+  herschel_counters* cnt;
+  int32_t* link;
+  int32_t* aux;
+  int32_t* op_nkern;
+  int64_t* op_first;
+  int64_t* op_last;
+  int64_t* op_ksum;
+  uint64_t* V;
+  uint64_t* M[6];
+  int64_t Mn[6];
+  int nlev;
+  uint64_t* pmt;
+  uint64_t* vb_status;
+  int32_t* par;
+  int32_t* tie_list;
+  int64_t tie_cap;
+  uint64_t* tie_scratch;
+  // per-launch kernel aggregates (by row), written by the join
+  const int64_t* lk_first;
+  const int64_t* lk_last;
+  const int64_t* lk_sum;
+};
+
+__device__ __forceinline__ int32_t key_pid(const ContainArgs& a, uint64_t key) {
+  return (int32_t)(key >> (a.tb + a.wb + 1));
+}
+__device__ __forceinline__ uint64_t key_seg(const ContainArgs& a, uint64_t key) { return key >> (a.wb + 1); }
+__device__ __forceinline__ int64_t key_rel(const ContainArgs& a, uint64_t key) {
+  return (int64_t)((key >> 1) & ((1ull << a.wb) - 1));
+}
+__device__ __forceinline__ bool key_is_op(uint64_t key) { return (key & 1) == 0; }
+
+// ----------------------------------------------------------------- ties
+// Ops of one thread starting at the same ns must be ordered by (te' down,
+// row up); the stable sort left them in row order.  Runs up to TIE_SHORT are
+// fixed in place by their first thread; longer runs are listed.
+__device__ __forceinline__ bool tie_before(int64_t te_a, uint32_t ra, int64_t te_b, uint32_t rb) {
+  return te_a > te_b || (te_a == te_b && ra < rb);
+}
+
+__global__ __launch_bounds__(256) void k_tiefix(ContainArgs a) {
+  const int64_t n = a.ds->nCL;
+  const int par = (int)a.ds->sort_parity[2];
+  const uint64_t* keys = a.k[par];
+  uint32_t* vals = a.v[par];
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < n; p += (int64_t)gridDim.x * 256) {
+    const uint64_t key = keys[p];
+    if (!key_is_op(key)) continue;
+    if (p + 1 >= n || keys[p + 1] != key) continue;
+    if (p > 0 && keys[p - 1] == key) continue;
+    int64_t e = p + 1;
+    while (e < n && keys[e] == key && e - p <= TIE_SHORT) ++e;
+    const int64_t len = e - p;
+    if (len > TIE_SHORT) {
+      const int slot = atomicAdd(&a.ds->n_long_ties, 1);
+      if (slot < a.tie_cap) a.tie_list[slot] = (int32_t)p;
+      else set_status(a.ds, DS_TIES);
+      continue;
+    }
+    // insertion sort of the run by (te down, row up); one process, so the
+    // raw end times order like the corrected ones
+    for (int64_t i = p + 1; i < e; ++i) {
+      const uint32_t r = vals[i];
+      const int64_t t = a.te[r];
+      int64_t j = i - 1;
+      while (j >= p) {
+        const uint32_t rj = vals[j];
+        if (!tie_before(t, r, a.te[rj], rj)) break;
+        vals[j + 1] = rj;
+        --j;
+      }
+      vals[j + 1] = r;
+    }
+  }
+}
+
+// Long runs: one workgroup per run, bitonic sort in a scratch region that
+// belongs to the run alone ([2p, 2p + m) with m <= 2 * len).
+__global__ __launch_bounds__(256) void k_tiefix_long(ContainArgs a) {
+  const int64_t n = a.ds->nCL;
+  const int64_t nl = min((int64_t)a.ds->n_long_ties, a.tie_cap);
+  const int par = (int)a.ds->sort_parity[2];
+  const uint64_t* keys = a.k[par];
+  uint32_t* vals = a.v[par];
+  __shared__ int64_t s_len;
+  for (int64_t r = blockIdx.x; r < nl; r += gridDim.x) {
+    const int64_t p = a.tie_list[r];
+    if (threadIdx.x == 0) {
+      int64_t e = p + 1;
+      while (e < n && keys[e] == keys[p]) ++e;
+      s_len = e - p;
+    }
+    __syncthreads();
+    const int64_t len = s_len;
+    int64_t m = 1;
+    while (m < len) m <<= 1;
+    int64_t* ste = (int64_t*)a.tie_scratch + 2 * p;
+    uint64_t* srow = a.tie_scratch + 2 * n + 2 * p;
+    for (int64_t i = threadIdx.x; i < m; i += 256) {
+      if (i < len) {
+        const uint32_t rr = vals[p + i];
+        ste[i] = a.te[rr];
+        srow[i] = rr;
+      } else {
+        ste[i] = I64MIN;
+        srow[i] = 0xffffffffull;
+      }
+    }
+    __syncthreads();
+    for (int64_t k = 2; k <= m; k <<= 1) {
+      for (int64_t j = k >> 1; j > 0; j >>= 1) {
+        for (int64_t i = threadIdx.x; i < m; i += 256) {
+          const int64_t l = i ^ j;
+          if (l > i) {
+            const bool up = (i & k) == 0;
+            const bool lb = tie_before(ste[l], (uint32_t)srow[l], ste[i], (uint32_t)srow[i]);
+            if (up ? lb : !lb) {
+              const int64_t t0 = ste[i];
+              ste[i] = ste[l];
+              ste[l] = t0;
+              const uint64_t r0 = srow[i];
+              srow[i] = srow[l];
+              srow[l] = r0;
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
+    for (int64_t i = threadIdx.x; i < len; i += 256) vals[p + i] = (uint32_t)srow[i];
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------- encoding, pyramid
+__global__ __launch_bounds__(CT_THREADS) void k_vbuild(ContainArgs a) {
+  __shared__ int s_tile;
+  __shared__ uint64_t s_w[CT_THREADS / WAVE];
+  __shared__ uint64_t s_tmax;
+  const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
+  const int64_t n = a.ds->nCL;
+  const int par = (int)a.ds->sort_parity[2];
+  const uint64_t* keys = a.k[par];
+  const uint32_t* vals = a.v[par];
+  const int tile = take_ticket(a.ds, TK_VBUILD, &s_tile);
+  const int64_t base = (int64_t)tile * CT_TILE;
+  if (base >= n) return;
+  // striped: item j of lane covers position base + wv*1024 + j*64 + lane, so
+  // a wave's 64 lanes form one 64-group of the pyramid
+  uint64_t wmax = 0;
+#pragma unroll 4
+  for (int j = 0; j < CT_ITEMS; ++j) {
+    const int64_t p = base + (int64_t)wv * (CT_ITEMS * WAVE) + j * WAVE + lane;
+    uint64_t v = 0;
+    if (p < n) {
+      const uint64_t key = keys[p];
+      if (key_is_op(key)) {
+        const uint32_t row = vals[p];
+        const int32_t pid = key_pid(a, key);
+        const int64_t tec = a.te[row] - (a.off ? a.off[pid] : 0);
+        const int64_t e = tec >= a.W1 ? a.W : tec - a.W0;
+        v = (key_seg(a, key) << a.vb) | (uint64_t)(e + 1);
+      }
+      a.V[p] = v;
+    }
+    const uint64_t g = wave_max_u64(v);
+    if (lane == 0 && p - lane < n) a.M[1][(p - lane) >> 6] = g;
+    wmax = g > wmax ? g : wmax;
+  }
+  if (lane == 0) s_w[wv] = wmax;
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t t = 0;
+    for (int w = 0; w < CT_THREADS / WAVE; ++w) t = s_w[w] > t ? s_w[w] : t;
+    s_tmax = t;
+    a.M[2][tile] = t;
+  }
+  __syncthreads();
+  if (wv == 0) {
+    const uint64_t ex = wave_lookback<OpMax>(a.vb_status, tile, s_tmax, a.ds);
+    if (lane == 0) a.pmt[tile] = ex;
+  }
+}
+
+// Levels 3 and up of the pyramid, from level 2 (one workgroup).
+__global__ __launch_bounds__(1024) void k_vlevels(ContainArgs a) {
+  const int64_t n = a.ds->nCL;
+  int64_t cnt = cdiv(n, CT_TILE);  // live level-2 entries
+  for (int l = 3; l < a.nlev; ++l) {
+    const int64_t out = cdiv(cnt, 64);
+    for (int64_t i = threadIdx.x; i < out; i += 1024) {
+      uint64_t m = 0;
+      const int64_t hi = min(cnt, (i + 1) * 64);
+      for (int64_t j = i * 64; j < hi; ++j) m = a.M[l - 1][j] > m ? a.M[l - 1][j] : m;
+      a.M[l][i] = m;
+    }
+    __syncthreads();
+    cnt = out;
+  }
+}
+
+// Last index in [lo, hi) of level l whose value exceeds q, or -1.
+__device__ __forceinline__ int64_t scan_back(const uint64_t* arr, int64_t lo, int64_t hi, uint64_t q) {
+  for (int64_t i = hi - 1; i >= lo; --i)
+    if (arr[i] > q) return i;
+  return -1;
+}
+
+// Live entries of pyramid level l for n positions.
+__device__ __forceinline__ int64_t live(int64_t n, int l) {
+  int64_t c = n;
+  for (int i = 0; i < l; ++i) c = cdiv(c, 64);
+  return c;
+}
+
+// Descend from entry i of level l to the last position below it with V > q.
+__device__ int64_t descend(const ContainArgs& a, int l, int64_t i, uint64_t q) {
+  const int64_t n = a.ds->nCL;
+  while (l > 0) {
+    const uint64_t* lower = l - 1 == 0 ? a.V : a.M[l - 1];
+    const int64_t lo = i * 64, hi = min(lo + 64, live(n, l - 1));
+    const int64_t f = scan_back(lower, lo, hi, q);
+    if (f < 0) return -1;  // cannot happen when the entry exceeded q
+    i = f;
+    --l;
+  }
+  return i;
+}
+
+__global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
+  __shared__ uint64_t s_v[CT_TILE];
+  __shared__ uint64_t s_m1[CT_TILE / 64];
+  __shared__ uint64_t s_tm[CT_THREADS];
+  const int tid = threadIdx.x;
+  const int64_t n = a.ds->nCL;
+  const int par = (int)a.ds->sort_parity[2];
+  const uint64_t* keys = a.k[par];
+  const uint32_t* vals = a.v[par];
+  const int64_t tile = blockIdx.x;
+  const int64_t base = tile * CT_TILE;
+  if (base >= n) return;
+  const int64_t tn = min((int64_t)CT_TILE, n - base);
+  for (int64_t i = tid; i < tn; i += CT_THREADS) s_v[i] = a.V[base + i];
+  for (int64_t i = tid; i < cdiv(tn, 64); i += CT_THREADS) s_m1[i] = a.M[1][tile * (CT_TILE / 64) + i];
+  __syncthreads();
+  // blocked items: thread t owns positions [t*16, t*16+16) of the tile
+  const int64_t l0 = (int64_t)tid * CT_ITEMS;
+  uint64_t tmax = 0;
+  for (int j = 0; j < CT_ITEMS; ++j)
+    if (l0 + j < tn) tmax = s_v[l0 + j] > tmax ? s_v[l0 + j] : tmax;
+  s_tm[tid] = tmax;
+  __syncthreads();
+  // exclusive prefix max over threads (256 values, one pass per thread is
+  // cheap: strided by the wave to stay conflict-free)
+  uint64_t pm = a.pmt[tile];
+  for (int t = 0; t < tid; ++t) pm = s_tm[t] > pm ? s_tm[t] : pm;
+  for (int j = 0; j < CT_ITEMS; ++j) {
+    const int64_t lp = l0 + j;
+    if (lp >= tn) break;
+    const int64_t p = base + lp;
+    const uint64_t key = keys[p];
+    const uint64_t q = (key_seg(a, key) << a.vb) | (uint64_t)(key_rel(a, key) + 1);
+    int64_t ans = -1;
+    if (pm > q) {
+      // level 0 within the 64-group, then the tile's groups (LDS)
+      const int64_t g = lp >> 6;
+      for (int64_t i = lp - 1; i >= g * 64; --i)
+        if (s_v[i] > q) {
+          ans = base + i;
+          break;
+        }
+      if (ans < 0) {
+        for (int64_t h = g - 1; h >= 0 && ans < 0; --h)
+          if (s_m1[h] > q) {
+            for (int64_t i = h * 64 + 63; i >= h * 64; --i)
+              if (s_v[i] > q) {
+                ans = base + i;
+                break;
+              }
+          }
+      }
+      // earlier tiles: climb the pyramid from level 2, then descend
+      int64_t idx = tile;  // index at level 2
+      for (int l = 2; ans < 0 && l < a.nlev; ++l) {
+        const int64_t lo = (idx >> 6) << 6;
+        const int64_t f = scan_back(a.M[l], lo, idx, q);
+        if (f >= 0) {
+          ans = descend(a, l, f, q);
+          break;
+        }
+        idx >>= 6;
+      }
+    }
+    a.par[p] = (int32_t)ans;
+    const uint32_t row = vals[p];
+    a.link[row] = ans >= 0 ? (int32_t)vals[ans] : -1;
+    const uint64_t vv = s_v[lp];
+    pm = vv > pm ? vv : pm;
+  }
+}
+
+// Depth by walking the parents; improper nesting; op aggregates reset.
+__global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
+  __shared__ unsigned long long s_imp;
+  if (threadIdx.x == 0) s_imp = 0;
+  __syncthreads();
+  const int64_t n = a.ds->nCL;
+  const int par = (int)a.ds->sort_parity[2];
+  const uint64_t* keys = a.k[par];
+  const uint32_t* vals = a.v[par];
+  uint32_t imp = 0;
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < n; p += (int64_t)gridDim.x * 256) {
+    if (!key_is_op(keys[p])) continue;
+    const uint32_t row = vals[p];
+    int32_t d = 0;
+    int64_t q = a.par[p];
+    if (q >= 0 && a.te[row] > a.te[vals[q]]) ++imp;  // same process: raw ends compare like corrected
+    while (q >= 0 && in_range(a.ds, q, n)) {
+      ++d;
+      q = a.par[q];
+    }
+    a.aux[row] = d;
+    a.op_nkern[row] = 0;
+    a.op_first[row] = I64MAX;
+    a.op_last[row] = I64MIN;
+    a.op_ksum[row] = 0;
+  }
+  const uint64_t w = wave_sum_u64(imp);
+  if (lane_id() == 0 && w) atomicAdd(&s_imp, (unsigned long long)w);
+  __syncthreads();
+  if (threadIdx.x == 0 && s_imp) atomicAdd((unsigned long long*)&a.cnt->n_improper_nesting, s_imp);
+}
+
+// ------------------------------------------------------ inclusive aggregates
+constexpr int AG_TILE = 1024;
+constexpr int AG_CHAIN = 64;
+
+__global__ __launch_bounds__(256) void k_opagg(ContainArgs a) {
+  __shared__ int32_t s_par[AG_TILE];
+  __shared__ uint32_t s_nk[AG_TILE];
+  __shared__ int64_t s_first[AG_TILE];
+  __shared__ int64_t s_last[AG_TILE];
+  __shared__ uint64_t s_sum[AG_TILE];
+  __shared__ int32_t s_chain[AG_CHAIN];      // ops open at the tile start, innermost first
+  __shared__ uint32_t c_nk[AG_CHAIN];
+  __shared__ int64_t c_first[AG_CHAIN], c_last[AG_CHAIN];
+  __shared__ uint64_t c_sum[AG_CHAIN];
+  __shared__ int s_nchain;
+  __shared__ uint8_t s_open[AG_TILE];
+  const int tid = threadIdx.x;
+  const int64_t n = a.ds->nCL;
+  const int par = (int)a.ds->sort_parity[2];
+  const uint64_t* keys = a.k[par];
+  const uint32_t* vals = a.v[par];
+  const int64_t base = (int64_t)blockIdx.x * AG_TILE;
+  if (base >= n) return;
+  const int64_t tn = min((int64_t)AG_TILE, n - base);
+  for (int64_t i = tid; i < tn; i += 256) {
+    s_par[i] = a.par[base + i];
+    s_nk[i] = 0;
+    s_first[i] = I64MAX;
+    s_last[i] = I64MIN;
+    s_sum[i] = 0;
+    s_open[i] = 0;
+  }
+  if (tid < AG_CHAIN) {
+    c_nk[tid] = 0;
+    c_first[tid] = I64MAX;
+    c_last[tid] = I64MIN;
+    c_sum[tid] = 0;
+  }
+  if (tid == 0) {
+    // stack after the element before the tile: that element (if an op) and
+    // its answer chain
+    int nc = 0;
+    if (base > 0) {
+      int64_t q = key_is_op(keys[base - 1]) ? base - 1 : a.par[base - 1];
+      while (q >= 0) {
+        if (nc < AG_CHAIN) s_chain[nc] = (int32_t)q;
+        ++nc;
+        q = a.par[q];
+      }
+    }
+    s_nchain = nc;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    // ops of this tile still open at its end receive later contributions
+    const int64_t last = tn - 1;
+    int64_t q = key_is_op(keys[base + last]) ? base + last : s_par[last];
+    while (q >= base) {
+      s_open[q - base] = 1;
+      q = s_par[q - base];
+    }
+  }
+  const int nc = s_nchain;
+  __syncthreads();
+  for (int64_t i = tid; i < tn; i += 256) {
+    const int64_t p = base + i;
+    const uint64_t key = keys[p];
+    if (key_is_op(key)) continue;
+    const uint32_t row = vals[p];
+    const int32_t nkl = a.aux[row];  // kernels joined to this launch
+    if (nkl <= 0) continue;
+    const int64_t f = a.lk_first[row], l = a.lk_last[row];
+    const uint64_t sm = (uint64_t)a.lk_sum[row];
+    int64_t q = s_par[i];
+    while (q >= base) {
+      const int64_t li = q - base;
+      atomicAdd(&s_nk[li], (uint32_t)nkl);
+      atomicMin((long long*)&s_first[li], (long long)f);
+      atomicMax((long long*)&s_last[li], (long long)l);
+      atomicAdd((unsigned long long*)&s_sum[li], (unsigned long long)sm);
+      q = s_par[li];
+    }
+    if (q >= 0) {
+      int k = 0;
+      while (k < nc && k < AG_CHAIN && s_chain[k] != q) ++k;
+      if (k < nc && k < AG_CHAIN) {
+        for (int c = k; c < nc && c < AG_CHAIN; ++c) {
+          atomicAdd(&c_nk[c], (uint32_t)nkl);
+          atomicMin((long long*)&c_first[c], (long long)f);
+          atomicMax((long long*)&c_last[c], (long long)l);
+          atomicAdd((unsigned long long*)&c_sum[c], (unsigned long long)sm);
+        }
+      }
+      if (nc > AG_CHAIN) {
+        // chain deeper than the table: walk the rest in HBM
+        int64_t r = k < nc && k < AG_CHAIN ? (int64_t)s_chain[AG_CHAIN - 1] : q;
+        if (k < nc && k < AG_CHAIN) r = a.par[r];
+        while (r >= 0) {
+          const uint32_t rr = vals[r];
+          atomicAdd(&a.op_nkern[rr], nkl);
+          atomicMin((long long*)&a.op_first[rr], (long long)f);
+          atomicMax((long long*)&a.op_last[rr], (long long)l);
+          atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)sm);
+          r = a.par[r];
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int64_t i = tid; i < tn; i += 256) {
+    const int64_t p = base + i;
+    if (!key_is_op(keys[p])) continue;
+    const uint32_t rr = vals[p];
+    if (s_open[i]) {
+      if (s_nk[i]) {
+        atomicAdd(&a.op_nkern[rr], (int32_t)s_nk[i]);
+        atomicMin((long long*)&a.op_first[rr], (long long)s_first[i]);
+        atomicMax((long long*)&a.op_last[rr], (long long)s_last[i]);
+        atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)s_sum[i]);
+      }
+    } else {
+      a.op_nkern[rr] = (int32_t)s_nk[i];
+      a.op_first[rr] = s_first[i];
+      a.op_last[rr] = s_last[i];
+      a.op_ksum[rr] = (int64_t)s_sum[i];
+    }
+  }
+  for (int c = tid; c < nc && c < AG_CHAIN; c += 256) {
+    if (c_nk[c]) {
+      const uint32_t rr = vals[s_chain[c]];
+      atomicAdd(&a.op_nkern[rr], (int32_t)c_nk[c]);
+      atomicMin((long long*)&a.op_first[rr], (long long)c_first[c]);
+      atomicMax((long long*)&a.op_last[rr], (long long)c_last[c]);
+      atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)c_sum[c]);
+    }
+  }
+}
+
+static ContainArgs contain_args(Ctx& c) {
+  ContainArgs a;
+  a.k[0] = c.sC.k[0];
+  a.k[1] = c.sC.k[1];
+  a.v[0] = c.sC.v[0];
+  a.v[1] = c.sC.v[1];
+  a.ts = c.ev.ts;
+  a.te = c.ev.te;
+  a.off = c.p.clock_offset;
+  a.W0 = c.W0;
+  a.W1 = c.W1;
+  a.W = c.W;
+  a.tb = c.tb;
+  a.wb = c.wb;
+  a.vb = c.vb;
+  a.ds = c.ds;
+  a.cnt = c.o.counters;
+  a.link = c.o.link;
+  a.aux = c.o.aux;
+  a.op_nkern = c.o.op_nkern;
+  a.op_first = c.o.op_first;
+  a.op_last = c.o.op_last;
+  a.op_ksum = c.o.op_ksum;
+  a.V = c.V;
+  for (int l = 0; l < 6; ++l) {
+    a.M[l] = c.M[l];
+    a.Mn[l] = c.Mn[l];
+  }
+  a.nlev = c.nlev;
+  a.pmt = c.pmt;
+  a.vb_status = c.vb_status;
+  a.par = c.par;
+  a.tie_list = c.tie_list;
+  a.tie_cap = c.tie_cap;
+  a.tie_scratch = c.tie_scratch;
+  a.lk_first = c.lk_first;
+  a.lk_last = c.lk_last;
+  a.lk_sum = c.lk_sum;
+  return a;
+}
+
+void launch_contain(Ctx& c) {
+  ContainArgs a = contain_args(c);
+  const int64_t tiles = std::max<int64_t>(cdiv(c.sC.n_max, CT_TILE), 1);
+  const int grid_stride = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.sC.n_max, 256 * 8), 1), 2048);
+  hipLaunchKernelGGL(k_tiefix, dim3(grid_stride), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_tiefix_long, dim3(64), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_vbuild, dim3((unsigned)tiles), dim3(CT_THREADS), 0, c.st, a);
+  if (c.nlev > 3) hipLaunchKernelGGL(k_vlevels, dim3(1), dim3(1024), 0, c.st, a);
+  hipLaunchKernelGGL(k_query, dim3((unsigned)tiles), dim3(CT_THREADS), 0, c.st, a);
+  hipLaunchKernelGGL(k_depth, dim3(grid_stride), dim3(256), 0, c.st, a);
+}
+
+void launch_opagg(Ctx& c) {
+  ContainArgs a = contain_args(c);
+  const int64_t tiles = std::max<int64_t>(cdiv(c.sC.n_max, AG_TILE), 1);
+  hipLaunchKernelGGL(k_opagg, dim3((unsigned)tiles), dim3(256), 0, c.st, a);
+}
+
+}  // namespace hx

@@ -1,0 +1,94 @@
+// Host-side plan of one analysis call and the launchers of each stage.
+#pragma once
+
+#include <algorithm>
+
+#include "common.hpp"
+
+namespace hx {
+
+// One LSD radix sort: 64-bit keys with optional 32-bit payload, ping-pong
+// buffers, digit histograms in DevState::hist[id], result buffer index in
+// DevState::sort_parity[id].
+struct SortBufs {
+  uint64_t* k[2] = {nullptr, nullptr};
+  uint32_t* v[2] = {nullptr, nullptr};  // both null for keys-only sorts
+  uint32_t* status = nullptr;           // [8 passes][tiles_max * 256]
+  int64_t n_max = 0;                    // capacity (host upper bound of the count)
+  int64_t tiles_max = 0;
+  int nd = 0;                           // digit passes to launch (8-bit digits)
+  int id = 0;                           // sort index: histogram, parity, tickets
+};
+
+struct Ctx {
+  hipStream_t st = nullptr;
+  herschel_events ev{};
+  int64_t n = 0;
+  herschel_params p{};
+  herschel_outputs o{};
+  int64_t W0 = 0, W1 = 0, W = 0, thr = 0;
+  int P = 0, S = 0, T = 0, NN = 0, NOP = 0;
+  bool contain = false, overlap = false;
+  int pb = 0, sb = 0, tb = 0, wb = 0;  // key field widths: pid, stream, thread, ts'-W0
+  int wb1 = 0;                         // bits of W (values 0..W)
+  int vb = 0;                          // bits of W+1 (containment encoding)
+
+  // workspace
+  DevState* ds = nullptr;
+  uint64_t* prep_status = nullptr;   // [prep_tiles * 3]
+  int64_t prep_tiles = 0;
+  uint64_t* union_status = nullptr;  // [union_tiles * 3]
+  int64_t union_tiles = 0;
+  uint64_t* vb_status = nullptr;     // [vb_tiles]
+  uint64_t* sweep_status = nullptr;  // [2 * sweep_tiles]
+  int64_t sweep_tiles = 0;
+  int64_t vb_tiles = 0;
+  int64_t* corr_min = nullptr;       // [P]
+  SortBufs sK, sJ, sC, sE;           // timeline, join, containment, overlap events
+  uint64_t* V = nullptr;             // [n] containment encoding per sorted position
+  uint64_t* M[6] = {};               // max pyramid, level l covers 64^l positions
+  int64_t Mn[6] = {};
+  int nlev = 0;
+  uint64_t* pmt = nullptr;           // [vb_tiles] exclusive prefix max before each tile
+  int32_t* par = nullptr;            // [n] answer position per sorted position
+  int32_t* tie_list = nullptr;       // [tie_cap * 2] long runs of equal op starts
+  int64_t tie_cap = 0;
+  uint64_t* tie_scratch = nullptr;   // [4n] end times and rows of long tie runs
+  int64_t* lk_first = nullptr;       // [n] per launch row: first start of its kernels
+  int64_t* lk_last = nullptr;        // [n] last end of its kernels
+  int64_t* lk_sum = nullptr;         // [n] sum of its kernels' durations
+  uint64_t* name_part = nullptr;     // [name_blocks * NN * 4] per-block name tables
+  int name_blocks = 0;
+  char* zero_begin = nullptr;        // region cleared at the start of a call
+  size_t zero_bytes = 0;
+};
+
+// Returns the workspace bytes and, when base != nullptr, points c's workspace
+// members into it.
+size_t layout_workspace(Ctx& c, char* base);
+
+void launch_init(Ctx& c);
+void launch_prep(Ctx& c);
+void launch_hist(Ctx& c, SortBufs& s, const int32_t* count);
+void launch_sort(Ctx& c, SortBufs& s, const int32_t* count);
+void launch_names(Ctx& c);
+void launch_timeline(Ctx& c);
+void launch_overlap(Ctx& c);
+void launch_contain(Ctx& c);
+void launch_opagg(Ctx& c);
+void launch_names_reduce(Ctx& c);
+void launch_join(Ctx& c);
+void launch_edges(Ctx& c);
+void launch_finalize(Ctx& c);
+
+int64_t prep_tile_rows();
+int64_t union_tile_elems();
+void names_set_lds_attr();
+
+constexpr int RS_THREADS = 256;
+constexpr int RS_ITEMS = 16;
+constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 4096 keys per tile
+
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace hx

@@ -1,0 +1,201 @@
+// Prep: one pass over the raw records (37 bytes per row).
+//
+// Validates each row (record schema of Section 5.2), moves it onto the
+// common clock, admits it by its start time (start-time filtering, Section
+// 5.2), marks rows outside the window, and compacts the admitted rows, in
+// row order, into the inputs of the three sorts:
+//   timeline    (pid, stream, ts'-W0)            kernels
+//   containment (pid, thread, ts'-W0, is_launch) ops and launches
+//   join        (pid, corr, is_kernel)            launches and kernels
+// Compaction offsets come from a decoupled look-back per list; the last
+// tile's prefixes are the admitted counts.
+#include "internal.hpp"
+
+namespace hx {
+
+constexpr int PREP_THREADS = 256;
+constexpr int PREP_ITEMS = 8;
+constexpr int PREP_TILE = PREP_THREADS * PREP_ITEMS;
+
+struct PrepArgs {
+  herschel_events ev;
+  int64_t n;
+  const int64_t* off;
+  int64_t W0, W1;
+  int P, S, T, NN, NOP;
+  int sb, tb, wb;
+  int64_t n_tiles;
+  DevState* ds;
+  herschel_counters* cnt;
+  int32_t* link;
+  int32_t* aux;
+  uint64_t* status;  // [3][n_tiles]
+  uint64_t* kK;
+  uint32_t* vK;
+  uint64_t* kC;
+  uint32_t* vC;
+  uint64_t* kJ;
+  uint32_t* vJ;
+};
+
+__global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
+  __shared__ int s_tile;
+  __shared__ uint64_t s_bal[PREP_ITEMS][PREP_THREADS / WAVE][3];
+  __shared__ uint32_t s_off[PREP_ITEMS][PREP_THREADS / WAVE][3];
+  __shared__ uint32_t s_tot[3];
+  __shared__ uint64_t s_base[3];
+  __shared__ unsigned long long s_bad;
+
+  const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
+  const int tile = take_ticket(a.ds, TK_PREP, &s_tile);
+  const int64_t base = (int64_t)tile * PREP_TILE;
+  if (tid == 0) s_bad = ~0ull;
+
+  uint64_t kA[PREP_ITEMS], kB[PREP_ITEMS];  // kA: timeline or containment key, kB: join key
+  uint32_t fl = 0;                          // per item: bit 3j list K, 3j+1 list C, 3j+2 list J
+  uint64_t bad = ~0ull;
+  const uint64_t lt = lanemask_lt();
+#pragma unroll
+  for (int j = 0; j < PREP_ITEMS; ++j) {
+    const int64_t r = base + (int64_t)j * PREP_THREADS + tid;
+    bool fK = false, fC = false, fJ = false;
+    kA[j] = 0;
+    kB[j] = 0;
+    if (r < a.n) {
+      const int kind = a.ev.kind[r];
+      const int32_t pid = a.ev.pid[r], lane_ = a.ev.lane[r], name = a.ev.name[r];
+      const int64_t ts = a.ev.ts[r], te = a.ev.te[r];
+      const int64_t corr = kind != HERSCHEL_CPU_OP ? a.ev.corr[r] : 0;
+      constexpr int64_t LIM = HERSCHEL_MAX_ABS_TIME;
+      bool ok = kind <= 2 && pid >= 0 && pid < a.P;
+      if (kind == HERSCHEL_KERNEL)
+        ok = ok && lane_ >= 0 && lane_ < a.S && name >= 0 && name < a.NN;
+      else
+        ok = ok && lane_ >= 0 && lane_ < a.T && name >= 0 && (kind != HERSCHEL_CPU_OP || name < a.NOP);
+      ok = ok && (kind == HERSCHEL_CPU_OP || (corr >= 0 && corr < HERSCHEL_CORR_LIMIT));
+      ok = ok && ts > -LIM && ts < LIM && te > -LIM && te < LIM && te >= ts;
+      bool adm = false;
+      int64_t rel = 0;
+      if (ok) {
+        const int64_t o = a.off ? a.off[pid] : 0;
+        const int64_t tsc = ts - o;
+        adm = tsc >= a.W0 && tsc < a.W1;
+        rel = tsc - a.W0;
+      } else {
+        bad = (uint64_t)r < bad ? (uint64_t)r : bad;
+      }
+      if (!adm) {
+        a.link[r] = -2;
+        a.aux[r] = -2;
+      } else {
+        fK = kind == HERSCHEL_KERNEL;
+        fC = !fK;
+        fJ = kind != HERSCHEL_CPU_OP;
+        if (fK)
+          kA[j] = ((uint64_t)pid << (a.sb + a.wb)) | ((uint64_t)lane_ << a.wb) | (uint64_t)rel;
+        else
+          kA[j] = ((uint64_t)pid << (a.tb + a.wb + 1)) | ((uint64_t)lane_ << (a.wb + 1)) | ((uint64_t)rel << 1) |
+                  (uint64_t)(kind == HERSCHEL_LAUNCH);
+        kB[j] = ((uint64_t)pid << 49) | ((uint64_t)corr << 1) | (uint64_t)(kind == HERSCHEL_KERNEL);
+      }
+    }
+    fl |= (fK ? 1u : 0u) << (3 * j) | (fC ? 1u : 0u) << (3 * j + 1) | (fJ ? 1u : 0u) << (3 * j + 2);
+    const uint64_t b0 = ballot(fK), b1 = ballot(fC), b2 = ballot(fJ);
+    if (lane == 0) {
+      s_bal[j][wv][0] = b0;
+      s_bal[j][wv][1] = b1;
+      s_bal[j][wv][2] = b2;
+    }
+  }
+  if (bad != ~0ull) atomicMin(&s_bad, (unsigned long long)bad);
+  __syncthreads();
+  if (tid < 3) {
+    uint32_t run = 0;
+    for (int j = 0; j < PREP_ITEMS; ++j)
+      for (int w = 0; w < PREP_THREADS / WAVE; ++w) {
+        s_off[j][w][tid] = run;
+        run += (uint32_t)popc(s_bal[j][w][tid]);
+      }
+    s_tot[tid] = run;
+  }
+  if (tid == 0 && s_bad != ~0ull) atomicMin((unsigned long long*)&a.ds->first_invalid, s_bad);
+  __syncthreads();
+  if (wv < 3) {
+    const uint64_t ex = wave_lookback<OpSum>(a.status + (int64_t)wv * a.n_tiles, tile, s_tot[wv], a.ds);
+    if (lane == 0) s_base[wv] = ex;
+  }
+  __syncthreads();
+  if (tile == a.n_tiles - 1 && tid == 0) {
+    const int64_t nK = (int64_t)(s_base[0] + s_tot[0]);
+    const int64_t nC = (int64_t)(s_base[1] + s_tot[1]);
+    const int64_t nJ = (int64_t)(s_base[2] + s_tot[2]);
+    a.ds->nK = (int32_t)nK;
+    a.ds->nCL = (int32_t)nC;
+    a.ds->nJ = (int32_t)nJ;
+    const int64_t nLaunch = nJ - nK;
+    a.cnt->n_admitted[HERSCHEL_KERNEL] = nK;
+    a.cnt->n_admitted[HERSCHEL_LAUNCH] = nLaunch;
+    a.cnt->n_admitted[HERSCHEL_CPU_OP] = nC - nLaunch;
+    a.cnt->n_outside_window = a.n - nK - nC;
+  }
+#pragma unroll
+  for (int j = 0; j < PREP_ITEMS; ++j) {
+    const uint32_t r = (uint32_t)(base + (int64_t)j * PREP_THREADS + tid);
+    if (fl & (1u << (3 * j))) {
+      const uint64_t pos = s_base[0] + s_off[j][wv][0] + popc(s_bal[j][wv][0] & lt);
+      if (in_range(a.ds, (int64_t)pos, a.n)) {
+        a.kK[pos] = kA[j];
+        a.vK[pos] = r;
+      }
+    }
+    if (fl & (2u << (3 * j))) {
+      const uint64_t pos = s_base[1] + s_off[j][wv][1] + popc(s_bal[j][wv][1] & lt);
+      if (in_range(a.ds, (int64_t)pos, a.n)) {
+        a.kC[pos] = kA[j];
+        a.vC[pos] = r;
+      }
+    }
+    if (fl & (4u << (3 * j))) {
+      const uint64_t pos = s_base[2] + s_off[j][wv][2] + popc(s_bal[j][wv][2] & lt);
+      if (in_range(a.ds, (int64_t)pos, a.n)) {
+        a.kJ[pos] = kB[j];
+        a.vJ[pos] = r;
+      }
+    }
+  }
+}
+
+void launch_prep(Ctx& c) {
+  if (c.n == 0) return;
+  PrepArgs a;
+  a.ev = c.ev;
+  a.n = c.n;
+  a.off = c.p.clock_offset;
+  a.W0 = c.W0;
+  a.W1 = c.W1;
+  a.P = c.P;
+  a.S = c.S;
+  a.T = c.T;
+  a.NN = c.NN;
+  a.NOP = c.NOP;
+  a.sb = c.sb;
+  a.tb = c.tb;
+  a.wb = c.wb;
+  a.n_tiles = c.prep_tiles;
+  a.ds = c.ds;
+  a.cnt = c.o.counters;
+  a.link = c.o.link;
+  a.aux = c.o.aux;
+  a.status = c.prep_status;
+  a.kK = c.sK.k[0];
+  a.vK = c.sK.v[0];
+  a.kC = c.sC.k[0];
+  a.vC = c.sC.v[0];
+  a.kJ = c.sJ.k[0];
+  a.vJ = c.sJ.v[0];
+  hipLaunchKernelGGL(k_prep, dim3((unsigned)c.prep_tiles), dim3(PREP_THREADS), 0, c.st, a);
+}
+
+int64_t prep_tile_rows() { return PREP_TILE; }
+
+}  // namespace hx

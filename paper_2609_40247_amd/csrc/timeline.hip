@@ -1,0 +1,376 @@
+// Per-stream timelines: busy time, idle gaps and coverage runs.
+//
+// Input: the admitted kernels sorted by (pid, stream, ts').  A kernel covers
+// [ts', min(te', W1)) (empty when te' == ts').  Walking a stream in start
+// order with the running maximum M of the covered ends, a kernel starts a
+// new coverage run iff its start lies beyond M, leaves the gap [M, ts')
+// uncovered, and adds max(0, end - max(ts', M)) to the busy time -- the idle
+// intervals of GPU activity that the case study of Section 9.1 starts from.
+//
+// The running maximum is a segmented max-scan (segments = streams) carried
+// across tiles by a decoupled look-back; a second look-back pair compacts
+// the gaps (in (pid, stream, begin) order, including the full-window gap of
+// a stream without kernels) and the run endpoints used by the overlap sweep.
+#include "internal.hpp"
+
+namespace hx {
+
+constexpr int UN_THREADS = 256;
+constexpr int UN_ITEMS = 16;
+constexpr int UN_TILE = UN_THREADS * UN_ITEMS;
+
+struct UnionArgs {
+  const uint64_t* k[2];
+  const uint32_t* v[2];
+  const int64_t* te;
+  const int32_t* pid_col;
+  const int64_t* off;
+  int64_t W0, W1, W, thr;
+  int P, S, sb, wb, wb1, pb;
+  bool overlap;
+  DevState* ds;
+  herschel_counters* cnt;
+  int64_t* busy;
+  int64_t gap_cap;
+  int32_t* gap_pid;
+  int32_t* gap_stream;
+  int64_t* gap_begin;
+  int64_t* gap_end;
+  uint8_t* gap_flags;
+  uint64_t* ev_keys;  // overlap events (sort input)
+  int64_t ev_cap;
+  uint64_t* status;   // [3][tiles_max]: segmax, gap count, event count
+  int64_t tiles_max;
+};
+
+struct Elem {
+  int32_t seg;    // pid * S + stream
+  int64_t s, e;   // start and clipped end, relative to W0
+};
+
+__device__ __forceinline__ Elem load_elem(const UnionArgs& a, const uint64_t* keys, const uint32_t* vals, int64_t i) {
+  Elem x;
+  const uint64_t key = keys[i];
+  const uint32_t row = vals[i];
+  const uint64_t segbits = key >> a.wb;
+  const int32_t pid = (int32_t)(segbits >> a.sb);
+  const int32_t stream = (int32_t)(segbits & ((1u << a.sb) - 1));
+  x.seg = pid * a.S + stream;
+  x.s = (int64_t)(key & ((1ull << a.wb) - 1));
+  const int64_t o = a.off ? a.off[pid] : 0;
+  const int64_t tec = a.te[row] - o;  // corrected end; may lie far beyond W1
+  x.e = tec >= a.W1 ? a.W : tec - a.W0;
+  return x;
+}
+
+__device__ __forceinline__ int32_t seg_of_key(const UnionArgs& a, uint64_t key) {
+  const uint64_t segbits = key >> a.wb;
+  return (int32_t)(segbits >> a.sb) * a.S + (int32_t)(segbits & ((1u << a.sb) - 1));
+}
+
+__device__ __forceinline__ void put_gap(const UnionArgs& a, int64_t pos, int32_t seg, int64_t b, int64_t e) {
+  if (pos < a.gap_cap) {
+    a.gap_pid[pos] = seg / a.S;
+    a.gap_stream[pos] = seg % a.S;
+    a.gap_begin[pos] = a.W0 + b;
+    a.gap_end[pos] = a.W0 + e;
+    a.gap_flags[pos] = (uint8_t)((b == 0 ? 1 : 0) | (e == a.W ? 2 : 0));
+  }
+}
+
+__device__ __forceinline__ void put_event(const UnionArgs& a, int64_t pos, int32_t seg, int64_t t) {
+  if (in_range(a.ds, pos, a.ev_cap)) {
+    const uint64_t pid = (uint64_t)(seg / a.S), stream = (uint64_t)(seg % a.S);
+    a.ev_keys[pos] = (pid << (a.wb1 + a.sb)) | ((uint64_t)t << a.sb) | stream;
+  }
+}
+
+// Walks this thread's elements with the incoming carry.  MODE 0 counts gaps
+// and events and accumulates busy time; MODE 1 writes gaps and events.
+template <int MODE>
+__device__ void walk(const UnionArgs& a, const Elem* x, int nv, int32_t prev_seg, int32_t next_seg, uint64_t m_in,
+                     int64_t i0, int64_t nK, uint32_t* ngap, uint32_t* nev, int64_t gbase, int64_t ebase,
+                     int64_t* s_busy, int32_t seg0) {
+  const int nseg = a.P * a.S;
+  const bool full_gap = a.W > a.thr;
+  uint64_t m = m_in;  // 0 none, else (max covered end) + 1
+  int32_t prev = prev_seg;
+  uint32_t g = 0, v = 0;
+  int64_t busy_acc = 0;
+  int32_t busy_seg = -1;
+#pragma unroll
+  for (int j = 0; j < UN_ITEMS; ++j) {
+    if (j >= nv) break;
+    const Elem& q = x[j];
+    if (q.seg != prev) {
+      const int32_t from = prev + 1;  // empty streams strictly between
+      for (int32_t s = from; s < q.seg; ++s) {
+        if (full_gap) {
+          if (MODE == 1) put_gap(a, gbase + g, s, 0, a.W);
+          ++g;
+        }
+      }
+      m = 0;
+    }
+    const int64_t C = m ? (int64_t)m - 1 : 0;
+    if (q.e > q.s) {
+      if (q.s > C && q.s - C > a.thr) {
+        if (MODE == 1) put_gap(a, gbase + g, q.seg, C, q.s);
+        ++g;
+      }
+      if (a.overlap && (m == 0 || q.s > C)) {
+        if (m != 0) {
+          if (MODE == 1) put_event(a, ebase + v, q.seg, C);
+          ++v;
+        }
+        if (MODE == 1) put_event(a, ebase + v, q.seg, q.s);
+        ++v;
+      }
+      if (MODE == 0) {
+        const int64_t lo = q.s > C ? q.s : C;
+        if (q.e > lo) {
+          if (busy_seg != q.seg) {
+            if (busy_seg >= 0 && busy_acc) {
+              if (busy_seg - seg0 < 64) atomicAdd((unsigned long long*)&s_busy[busy_seg - seg0], (unsigned long long)busy_acc);
+              else atomicAdd((unsigned long long*)&a.busy[busy_seg], (unsigned long long)busy_acc);
+            }
+            busy_seg = q.seg;
+            busy_acc = 0;
+          }
+          busy_acc += q.e - lo;
+        }
+      }
+      const uint64_t me = (uint64_t)q.e + 1;
+      m = me > m ? me : m;
+    }
+    const int32_t nxt = (j + 1 < nv) ? x[j + 1].seg : next_seg;
+    if (nxt != q.seg) {
+      const int64_t Cl = m ? (int64_t)m - 1 : 0;
+      if (Cl < a.W && a.W - Cl > a.thr) {
+        if (MODE == 1) put_gap(a, gbase + g, q.seg, Cl, a.W);
+        ++g;
+      }
+      if (a.overlap && m != 0) {
+        if (MODE == 1) put_event(a, ebase + v, q.seg, Cl);
+        ++v;
+      }
+      if (i0 + j == nK - 1) {
+        for (int32_t s = q.seg + 1; s < nseg; ++s) {
+          if (full_gap) {
+            if (MODE == 1) put_gap(a, gbase + g, s, 0, a.W);
+            ++g;
+          }
+        }
+      }
+    }
+    prev = q.seg;
+  }
+  if (MODE == 0 && busy_seg >= 0 && busy_acc) {
+    if (busy_seg - seg0 < 64) atomicAdd((unsigned long long*)&s_busy[busy_seg - seg0], (unsigned long long)busy_acc);
+    else atomicAdd((unsigned long long*)&a.busy[busy_seg], (unsigned long long)busy_acc);
+  }
+  *ngap = g;
+  *nev = v;
+}
+
+__global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
+  __shared__ int s_tile;
+  __shared__ uint64_t s_wv[UN_THREADS / WAVE];
+  __shared__ int s_wh[UN_THREADS / WAVE];
+  __shared__ uint64_t s_tile_excl;
+  __shared__ int64_t s_busy[64];
+  __shared__ int32_t s_seg0;
+  __shared__ uint32_t s_scan[UN_THREADS / WAVE + 1];
+  __shared__ uint32_t s_tot[2];
+  __shared__ uint64_t s_base[2];
+
+  const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
+  const int64_t nK = a.ds->nK;
+  const int par = (int)a.ds->sort_parity[0];
+  const uint64_t* keys = a.k[par];
+  const uint32_t* vals = a.v[par];
+  const int tile = take_ticket(a.ds, TK_UNION, &s_tile);
+  const int64_t ntiles = nK > 0 ? cdiv(nK, UN_TILE) : 1;
+  if (tile >= ntiles) return;
+  const int64_t base = (int64_t)tile * UN_TILE;
+  const int nseg = a.P * a.S;
+
+  if (nK == 0) {  // no kernels: one full-window gap per stream
+    const bool full_gap = a.W > a.thr;
+    for (int s = tid; s < nseg; s += UN_THREADS)
+      if (full_gap) put_gap(a, s, s, 0, a.W);
+    if (tid == 0) {
+      a.ds->n_gaps = full_gap ? nseg : 0;
+      a.cnt->n_gaps_total = full_gap ? nseg : 0;
+      a.ds->nEv = 0;
+    }
+    return;
+  }
+
+  if (tid < 64) s_busy[tid] = 0;
+  if (tid == 0) s_seg0 = seg_of_key(a, keys[base]);
+
+  const int64_t i0 = base + (int64_t)tid * UN_ITEMS;
+  Elem x[UN_ITEMS];
+  int nv = 0;
+#pragma unroll
+  for (int j = 0; j < UN_ITEMS; ++j) {
+    if (i0 + j < nK) {
+      x[j] = load_elem(a, keys, vals, i0 + j);
+      nv = j + 1;
+    } else {
+      x[j].seg = -1;
+      x[j].s = x[j].e = 0;
+    }
+  }
+  const bool has = nv > 0;
+  const int32_t prev_seg = (has && i0 > 0) ? seg_of_key(a, keys[i0 - 1]) : -1;
+  const int32_t next_seg = (has && i0 + nv < nK) ? seg_of_key(a, keys[i0 + nv]) : -1;
+
+  // Thread aggregate for the segmented max-scan.
+  uint64_t agg = 0;
+  if (has) {
+    bool head = false;
+    uint64_t m = 0;
+    int32_t prev = prev_seg;
+#pragma unroll
+    for (int j = 0; j < UN_ITEMS; ++j) {
+      if (j >= nv) break;
+      if (x[j].seg != prev) {
+        head = true;
+        m = 0;
+      }
+      if (x[j].e > x[j].s) {
+        const uint64_t me = (uint64_t)x[j].e + 1;
+        m = me > m ? me : m;
+      }
+      prev = x[j].seg;
+    }
+    int32_t last_seg = x[0].seg;
+#pragma unroll
+    for (int j = 1; j < UN_ITEMS; ++j)
+      if (j < nv) last_seg = x[j].seg;
+    agg = OpSegMax::make((uint32_t)last_seg, head, m);
+  }
+  // Ordered inclusive scan over the wave (valid threads form a prefix).
+  uint64_t inc = agg;
+  bool hv = has;
+  for (int d = 1; d < WAVE; d <<= 1) {
+    const uint64_t o = shfl_up(inc, d);
+    const int oh = shfl_up((int)hv, d);
+    if (lane >= d && oh) {
+      inc = hv ? OpSegMax::combine(o, inc) : o;
+      hv = true;
+    }
+  }
+  // every lane takes part in the shuffles; lane 0 discards the result
+  const uint64_t lane_excl = shfl_up(inc, 1);
+  const int prev_hv = shfl_up((int)hv, 1);
+  const bool lane_excl_has = lane > 0 && prev_hv;
+  if (lane == WAVE - 1) {
+    s_wv[wv] = inc;
+    s_wh[wv] = hv;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t run = 0;
+    bool rh = false;
+    for (int w = 0; w < UN_THREADS / WAVE; ++w) {
+      const uint64_t t = s_wv[w];
+      const bool th = s_wh[w];
+      s_wv[w] = run;
+      s_wh[w] = rh;
+      if (th) {
+        run = rh ? OpSegMax::combine(run, t) : t;
+        rh = true;
+      }
+    }
+    s_tile_excl = run;  // tile aggregate (temporarily)
+  }
+  __syncthreads();
+  if (wv == 0) {
+    const uint64_t ex = wave_lookback<OpSegMax>(a.status, tile, s_tile_excl, a.ds);
+    if (lane == 0) s_tile_excl = ex;
+  }
+  __syncthreads();
+  // Exclusive prefix for this thread: tile prefix, then waves, then lanes.
+  uint64_t pre = s_tile_excl;
+  bool pre_has = tile > 0;
+  if (s_wh[wv]) {
+    pre = pre_has ? OpSegMax::combine(pre, s_wv[wv]) : s_wv[wv];
+    pre_has = true;
+  }
+  if (lane_excl_has) {
+    pre = pre_has ? OpSegMax::combine(pre, lane_excl) : lane_excl;
+    pre_has = true;
+  }
+  const uint64_t m_in = (has && pre_has && (int32_t)OpSegMax::seg(pre) == x[0].seg) ? OpSegMax::m(pre) : 0;
+
+  uint32_t ngap = 0, nev = 0;
+  if (has) walk<0>(a, x, nv, prev_seg, next_seg, m_in, i0, nK, &ngap, &nev, 0, 0, s_busy, s_seg0);
+  uint32_t gtot, etot;
+  const uint32_t gex = block_excl_sum<UN_THREADS>(ngap, s_scan, &gtot);
+  const uint32_t eex = block_excl_sum<UN_THREADS>(nev, s_scan, &etot);
+  if (tid == 0) {
+    s_tot[0] = gtot;
+    s_tot[1] = etot;
+  }
+  __syncthreads();
+  if (wv < 2) {
+    const uint64_t ex = wave_lookback<OpSum>(a.status + (int64_t)(1 + wv) * a.tiles_max, tile, s_tot[wv], a.ds);
+    if (lane == 0) s_base[wv] = ex;
+  }
+  if (tid < 64 && s_busy[tid]) atomicAdd((unsigned long long*)&a.busy[s_seg0 + tid], (unsigned long long)s_busy[tid]);
+  __syncthreads();
+  if (tile == ntiles - 1 && tid == 0) {
+    const int64_t g = (int64_t)(s_base[0] + s_tot[0]);
+    a.ds->n_gaps = g;
+    a.cnt->n_gaps_total = g;
+    a.ds->nEv = (int32_t)(s_base[1] + s_tot[1]);
+  }
+  if (has && (ngap || nev)) {
+    uint32_t g2, e2;
+    walk<1>(a, x, nv, prev_seg, next_seg, m_in, i0, nK, &g2, &e2, (int64_t)s_base[0] + gex, (int64_t)s_base[1] + eex,
+            s_busy, s_seg0);
+  }
+}
+
+void launch_timeline(Ctx& c) {
+  UnionArgs a;
+  a.k[0] = c.sK.k[0];
+  a.k[1] = c.sK.k[1];
+  a.v[0] = c.sK.v[0];
+  a.v[1] = c.sK.v[1];
+  a.te = c.ev.te;
+  a.pid_col = c.ev.pid;
+  a.off = c.p.clock_offset;
+  a.W0 = c.W0;
+  a.W1 = c.W1;
+  a.W = c.W;
+  a.thr = c.thr;
+  a.P = c.P;
+  a.S = c.S;
+  a.sb = c.sb;
+  a.wb = c.wb;
+  a.wb1 = c.wb1;
+  a.pb = c.pb;
+  a.overlap = c.overlap;
+  a.ds = c.ds;
+  a.cnt = c.o.counters;
+  a.busy = c.o.busy;
+  a.gap_cap = c.o.gap_capacity;
+  a.gap_pid = c.o.gap_pid;
+  a.gap_stream = c.o.gap_stream;
+  a.gap_begin = c.o.gap_begin;
+  a.gap_end = c.o.gap_end;
+  a.gap_flags = c.o.gap_flags;
+  a.ev_keys = c.sE.k[0];
+  a.ev_cap = c.sE.n_max;
+  a.status = c.union_status;
+  a.tiles_max = c.union_tiles;
+  hipLaunchKernelGGL(k_union, dim3((unsigned)c.union_tiles), dim3(UN_THREADS), 0, c.st, a);
+}
+
+int64_t union_tile_elems() { return UN_TILE; }
+
+}  // namespace hx

@@ -1,0 +1,320 @@
+"""GPU parity: the HIP library against the CPU oracle, element by element.
+
+Every output array is compared exactly (all of this is integer work).  Cases:
+hand-built worked timelines, adversarial tiny traces, the five workload
+configurations (configs 0-2 at full size; config 3 at full size; config 4's
+traces through the batch entry point), degenerate shapes (long runs of equal
+op starts, nesting deeper than the per-tile table, 64 streams, 4096
+processes, the largest window), error paths, and determinism.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+from compare import assert_same
+from fixtures import I64_MAX, I64_MIN, load_golden
+from paper_2609_40247_amd import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def H():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_40247_amd import herschel
+    herschel.load()
+    return herschel
+
+
+def check(H, cols, p, label, cap=None):
+    g = H.analyze(cols, p, gap_capacity=cap)
+    o = oracle.analyze(cols, p, gap_capacity=cap)
+    assert g[1]["counters"]["device_status"] == 0, f"{label}: device status {g[1]['counters']['device_status']}"
+    assert_same(g, o, p, label)
+    return g, o
+
+
+# --------------------------------------------------------------- worked
+@pytest.mark.parametrize("name", ["t1_worked_timeline.json", "t2_worked_timeline.json"])
+def test_worked_timelines(H, name):
+    cols, p, gj = load_golden(name)
+    (code, o), _ = check(H, cols, p, name)
+    exp = gj["expect"]
+    assert code == exp["code"]
+    assert o["link"].tolist() == exp["link"] and o["aux"].tolist() == exp["aux"]
+    for r, v in exp["op"].items():
+        assert [int(o["op_nkern"][r]), int(o["op_first"][r]), int(o["op_last"][r]), int(o["op_ksum"][r])] == v
+    assert o["edge_wait"].tolist() == exp["edge_wait"]
+
+
+@pytest.mark.parametrize("flags", [0, 1, 2, 3])
+def test_worked_timeline_flags(H, flags):
+    cols, p, _ = load_golden("t2_worked_timeline.json")
+    p["flags"] = flags
+    check(H, cols, p, f"T2 flags={flags}")
+
+
+# --------------------------------------------------------------- tiny adversarial
+SMALL = [dict(seed=s) for s in range(60)] + [
+    dict(seed=1000 + s, n_rows=400, window=3000, n_procs=3, n_streams=4, n_threads=3, corr_range=60)
+    for s in range(20)] + [
+    dict(seed=2000 + s, n_rows=40, window=60, n_procs=1, n_streams=2, n_threads=1, corr_range=6, offsets=False)
+    for s in range(20)] + [dict(seed=3000 + s, flags=s % 4) for s in range(12)] + [
+    dict(seed=4000 + s, n_rows=30, window=200, n_procs=4, n_streams=2, n_threads=2, corr_range=3) for s in range(12)]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: f"seed{c['seed']}")
+def test_random_small(H, case):
+    tr = synth.random_small(**case)
+    check(H, tr.columns(), tr.params, tr.label)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_medium_spans_tiles(H, seed):
+    """Tens of thousands of adversarial rows: every kernel spans several tiles."""
+    tr = synth.random_small(seed=9000 + seed, n_rows=60_000, window=400_000, n_procs=3, n_streams=5,
+                            n_threads=2, corr_range=20_000, edges=300)
+    check(H, tr.columns(), tr.params, tr.label)
+
+
+# --------------------------------------------------------------- workloads
+def test_config0(H):
+    tr = synth.config0()
+    check(H, tr.columns(), tr.params, "config0")
+
+
+def test_config0_delivery_shuffled(H):
+    tr = synth.config0(shuffle=True)
+    check(H, tr.columns(), tr.params, "config0 shuffled")
+
+
+def test_config0_thresholds(H):
+    tr = synth.config0()
+    for thr in (-1, 0, 3_000, 10**9):
+        p = dict(tr.params, gap_threshold=thr)
+        check(H, tr.columns(), p, f"config0 thr={thr}")
+
+
+def test_config1_full(H):
+    tr = synth.config1()
+    (code, g), _ = check(H, tr.columns(), tr.params, "config1")
+    assert code == 0 and g["counters"]["n_admitted_kernel"] > 980_000
+
+
+def test_config1_clock_offset(H):
+    tr = synth.config1(n_steps=50, clock_offset=-37_123)
+    check(H, tr.columns(), tr.params, "config1 offset")
+
+
+def test_config2_full(H):
+    tr = synth.config2()
+    (code, g), _ = check(H, tr.columns(), tr.params, "config2")
+    assert g["any_busy"][0] > 0 and g["class_overlap"][1] > 0  # comm overlaps compute
+
+
+@pytest.mark.slow
+def test_config3_full(H):
+    tr = synth.config3()
+    (code, g), _ = check(H, tr.columns(), tr.params, "config3")
+    assert (g["edge_status"] == 0).mean() > 0.95
+
+
+def test_config3_small(H):
+    tr = synth.config3(n_procs=8, n_steps=30, n_edges=2000)
+    check(H, tr.columns(), tr.params, "config3 small")
+
+
+# --------------------------------------------------------------- degenerate shapes
+def _rows(rows, P=1, S=1, T=1, NN=4, NOP=4, W0=0, W=100_000, thr=0, flags=3, off=None, cls=None, edges=None):
+    a = np.array(rows, dtype=np.int64).reshape(-1, 7)
+    cols = dict(kind=a[:, 0].astype(np.uint8), pid=a[:, 1].astype(np.int32), lane=a[:, 2].astype(np.int32),
+                ts=a[:, 3], te=a[:, 4], corr=a[:, 5], name=a[:, 6].astype(np.int32))
+    p = synth.empty_params(window_begin=W0, window_end=W0 + W, gap_threshold=thr, n_procs=P, n_streams=S,
+                           n_threads=T, n_names=NN, n_op_names=NOP, flags=flags,
+                           clock_offset=off, stream_class=cls,
+                           edges=np.zeros(0, synth.EDGE_DTYPE) if edges is None else edges)
+    return cols, p
+
+
+def test_long_runs_of_equal_op_starts(H):
+    """More than 32 ops of one thread starting at the same ns (the tie fix's
+    long path), with equal ends among them, plus launches and kernels."""
+    rng = np.random.default_rng(5)
+    rows = []
+    for g, L in enumerate((40, 300, 33, 2000)):
+        t0 = 1_000 + g * 20_000
+        ends = t0 + 50 + rng.integers(0, 60, L) * 100
+        for i in range(L):
+            rows.append((0, 0, 0, t0, int(ends[i]), 0, i % 4))
+        for j in range(30):
+            t = t0 + 20 + j * 200
+            rows.append((1, 0, 0, t, t + 10, g * 100 + j, 0))
+            rows.append((2, 0, 0, t + 30, t + 60, g * 100 + j, j % 4))
+    perm = rng.permutation(len(rows))
+    rows = [rows[i] for i in perm]
+    cols, p = _rows(rows)
+    check(H, cols, p, "long tie runs")
+
+
+def test_deep_nesting(H):
+    """A chain of 300 nested ops with thousands of launches inside: the
+    stack open at a tile edge is deeper than the per-tile table."""
+    rows = []
+    D = 300
+    for i in range(D):
+        rows.append((0, 0, 0, 1_000 + i, 90_000 - i, 0, i % 4))
+    for j in range(3000):
+        t = 2_000 + j * 25
+        rows.append((1, 0, 0, t, t + 5, j, 0))
+        rows.append((2, 0, j % 2, t + 7, t + 19, j, j % 4))
+    rows.append((1, 0, 0, 95_000, 95_001, 77_777, 0))
+    cols, p = _rows(rows, S=2)
+    (code, g), _ = check(H, cols, p, "deep nesting")
+    assert g["aux"][D - 1] == D - 1
+
+
+def test_64_streams_overlap(H):
+    tr = synth.random_small(seed=77, n_rows=6000, window=20_000, n_procs=2, n_streams=64, n_threads=2,
+                            corr_range=3000)
+    p = dict(tr.params, stream_class=(np.arange(64) % 3).astype(np.uint8))
+    check(H, tr.columns(), p, "64 streams")
+
+
+def test_4096_processes(H):
+    tr = synth.random_small(seed=78, n_rows=20_000, window=5_000, n_procs=4096, n_streams=3, n_threads=2,
+                            corr_range=50)
+    check(H, tr.columns(), tr.params, "4096 processes")
+
+
+def test_largest_window_and_extreme_times(H):
+    """W = 2^40 ns near the int64 time limits, unclipped ends far beyond W1."""
+    W0 = (1 << 62) - (1 << 41)
+    W = 1 << 40
+    rng = np.random.default_rng(9)
+    rows = []
+    for j in range(2000):
+        t = W0 + int(rng.integers(0, W))
+        rows.append((1, 0, 0, t, t + 3, j, 0))
+        e = t + 50 if j % 7 else (1 << 62) - 1
+        rows.append((2, 0, j % 3, t + int(rng.integers(0, 100)), max(e, t + 200), j, j % 4))
+        if j % 5 == 0:
+            rows.append((0, 0, 0, t - 1, min(t + int(rng.integers(1, 1 << 30)), (1 << 62) - 1), 0, 1))
+    cols, p = _rows(rows, S=3, W0=W0, W=W, thr=1000)
+    check(H, cols, p, "largest window")
+
+
+def test_empty_and_all_outside(H):
+    cols, p = _rows([], P=3, S=2)
+    check(H, cols, p, "empty")
+    cols, p = _rows([(2, 0, 0, -50, -10, 1, 0), (1, 0, 0, 200_000, 200_010, 1, 0)], S=2)
+    check(H, cols, p, "all outside")
+
+
+def test_single_kernel_covering_window(H):
+    cols, p = _rows([(2, 0, 0, 0, 10**9, 1, 0), (1, 0, 0, 0, 3, 1, 0), (0, 0, 0, 0, 10**9, 0, 0)], S=2)
+    check(H, cols, p, "covering kernel")
+
+
+# --------------------------------------------------------------- errors
+def test_invalid_rows(H):
+    cols, p, _ = load_golden("t1_worked_timeline.json")
+    for field, row, val in (("kind", 3, 3), ("pid", 5, 1), ("lane", 12, 2), ("te", 7, 12), ("corr", 9, -1),
+                            ("name", 2, 4)):
+        c = {k: v.copy() for k, v in cols.items()}
+        c[field][row] = val
+        c["kind"][16] = 7  # a second, later invalid row
+        code, g = H.analyze(c, p)
+        assert code == -2 and g["counters"]["first_invalid"] == row, (field, code)
+
+
+def test_invalid_params(H):
+    cols, p, _ = load_golden("t1_worked_timeline.json")
+    n = len(cols["ts"])
+    an = H.Analyzer(p, n)
+    ev = H.events_struct(H.device_columns(cols))
+    for change in (dict(window_end=0), dict(n_streams=65), dict(n_threads=513), dict(n_procs=0),
+                   dict(flags=8), dict(n_names=0)):
+        an.p = dict(p, **change)
+        params = an._params_struct(an.ws.data_ptr(), an.ws_bytes)
+        assert H.herschel_trace_analyze(ev, n, params, an.outs) == -1, change
+        if "flags" not in change:
+            with pytest.raises(ValueError):
+                H.herschel_workspace_size(n, params)
+    an.p = dict(p)
+    assert an.run(ev, n) == 0
+    # checked on the device: offsets and stream classes
+    for change in (dict(clock_offset=np.array([1 << 62], np.int64)), dict(stream_class=np.array([0, 5], np.uint8))):
+        q = dict(p, **change)
+        code, _ = H.analyze(cols, q)
+        assert code == -1, change
+
+
+def test_gap_capacity(H):
+    cols, p, _ = load_golden("t1_worked_timeline.json")
+    for cap in (0, 1, 4):
+        g = H.analyze(cols, p, gap_capacity=cap)
+        o = oracle.analyze(cols, p, gap_capacity=cap)
+        assert g[0] == -3 and o[0] == -3
+        assert_same(g, o, p, f"capacity {cap}")
+
+
+def test_workspace_too_small(H):
+    cols, p, _ = load_golden("t1_worked_timeline.json")
+    an = H.Analyzer(p, len(cols["ts"]))
+    d = H.device_columns(cols)
+    ev = H.events_struct(d)
+    params = an._params_struct(an.ws.data_ptr(), an.ws_bytes - 256)
+    assert H.herschel_trace_analyze(ev, len(cols["ts"]), params, an.outs) == -4
+    params = an._params_struct(None, 0)
+    assert H.herschel_trace_analyze(ev, len(cols["ts"]), params, an.outs) == -4
+    assert an.run(ev, len(cols["ts"])) == 0
+
+
+# --------------------------------------------------------------- determinism, reuse, batch
+def test_determinism_and_reuse(H):
+    """Two calls on one analyzer (workspace reused) give identical bytes; a
+    smaller second call is not disturbed by the first's leftovers."""
+    big = synth.config1(n_steps=60)
+    small = synth.config1(seed=5, n_steps=20)
+    an = H.Analyzer(big.params, big.n)
+    d = H.device_columns(big.columns())
+    assert an.run(H.events_struct(d), big.n) == 0
+    torch.cuda.synchronize()
+    r1 = an.results(big.n)
+    assert an.run(H.events_struct(d), big.n) == 0
+    torch.cuda.synchronize()
+    r2 = an.results(big.n)
+    for k in r1:
+        if k != "counters":
+            assert np.array_equal(r1[k], r2[k]), k
+    assert r1["counters"] == r2["counters"]
+    ds = H.device_columns(small.columns())
+    an.prefill()
+    assert an.run(H.events_struct(ds), small.n) == 0
+    torch.cuda.synchronize()
+    rs = an.results(small.n)
+    assert_same((0, rs), oracle.analyze(small.columns(), small.params, gap_capacity=an.gap_capacity),
+                small.params, "reuse small")
+
+
+def test_batch_matches_single_calls(H):
+    """Config 4 traces through the batch entry point equal single calls."""
+    traces = [synth.config4_trace(t, kernels=k) for t, k in enumerate((30_000, 5_000, 61_000))]
+    traces.insert(1, synth.config1(n_steps=15))
+    cols = {k: np.concatenate([t.columns()[k] for t in traces]) for k in traces[0].columns()}
+    offs = np.cumsum([0] + [t.n for t in traces]).astype(np.int64)
+    d = H.device_columns(cols)
+    ans = [H.Analyzer(t.params, max(t.n for t in traces)) for t in traces]
+    for a in ans:
+        a.prefill()
+    code = H.herschel_trace_analyze_batch(H.events_struct(d), offs, [ans[0].params] + [a.params for a in ans[1:]],
+                                          [a.outs for a in ans])
+    torch.cuda.synchronize()
+    assert code == 0
+    for t, a in zip(traces, ans):
+        o = oracle.analyze(t.columns(), t.params, gap_capacity=a.gap_capacity)
+        assert_same((0, a.results(t.n)), o, t.params, t.label)

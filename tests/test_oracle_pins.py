@@ -410,7 +410,7 @@ def test_cpu_op_corr_is_not_validated():
 
 @pytest.mark.parametrize("change", [
     dict(window_end=0), dict(window_end=-5), dict(window_end=(1 << 40) + 1), dict(n_procs=0),
-    dict(n_procs=4097), dict(n_streams=65), dict(n_streams=0), dict(n_threads=2049), dict(n_names=0),
+    dict(n_procs=4097), dict(n_streams=65), dict(n_streams=0), dict(n_threads=513), dict(n_names=0),
     dict(n_op_names=0), dict(clock_offset=np.array([1 << 62])), dict(stream_class=np.array([0, 3], np.uint8)),
     dict(window_begin=-(1 << 62), window_end=-(1 << 62) + 100),
 ])
