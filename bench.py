@@ -1,0 +1,164 @@
+#!/usr/bin/env python3
+"""Benchmark of the trace analyzer on one MI355X.
+
+One step = one full analysis (every output: timelines, gaps, join and
+latency histogram, containment with per-op aggregates, per-name
+aggregates, cross-stream overlap) of the decode-step trace: 1 process,
+4 streams, a 30 s window, 1,000 steps of 1,000 kernels (about 1M kernel
+records, 1M launches, 1M CPU ops: 2.99M rows).  The input is resident in
+HBM before timing.  Prints one JSON line: events (all input rows) per
+second, the roofline of the dominant kernel measured live with HIP events
+on the library's stream, and the CPU oracle timed on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+METRIC = "trace events analyzed/sec (M ev/s) at 1 MI355X + achieved HBM GB/s % peak"
+HBM_PEAK_GBS = 8000.0
+# Stage used for the roofline and the sources that define it (the profile
+# traffic is only trusted while these files are unchanged).
+ROOFLINE_STAGE = "prep"
+STAGE_SOURCES = {"prep": ["paper_2609_40247_amd/csrc/prep.hip", "paper_2609_40247_amd/csrc/common.hpp",
+                          "paper_2609_40247_amd/csrc/internal.hpp"]}
+
+
+def source_hash(stage: str) -> str:
+    h = hashlib.sha256()
+    for f in STAGE_SOURCES[stage]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(stage: str, n: int, c: dict) -> int:
+    """Bytes the stage must move for one call (inputs read once, outputs
+    written once; no look-back or scratch traffic)."""
+    if stage == "prep":
+        n_lists = c["n_admitted_kernel"] + (c["n_admitted_cpu"] + c["n_admitted_launch"]) + \
+            (c["n_admitted_launch"] + c["n_admitted_kernel"])
+        return 37 * n + 12 * n_lists + 8 * c["n_outside_window"]
+    raise ValueError(stage)
+
+
+def profiled_traffic(stage: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{stage}_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", txt)
+    m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9]+)", txt)
+    if not m_sha or not m_b or m_sha.group(1) != source_hash(stage):
+        return None
+    return int(m_b.group(1))
+
+
+def cpu_baseline(cols, params, n, budget_s=12.0, max_calls=30):
+    import oracle  # the CPU oracle: test infrastructure, used here only as the baseline
+    oracle.analyze(cols, params)  # load / build outside the timing
+    calls, t0 = 0, time.perf_counter()
+    while calls < max_calls:
+        oracle.analyze(cols, params)
+        calls += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": round(n * calls / dt / 1e6, 3), "unit": "M ev/s", "cores": 1, "kind": "oracle",
+            "sample": f"the same 2.99M-row trace analyzed {calls} times by the single-threaded C oracle "
+                      f"({dt:.1f} s on {os.cpu_count()} host cores, 1 used)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stages", action="store_true", help="also print a per-stage breakdown to stderr")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "run it with --gpus 1", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    from paper_2609_40247_amd import herschel as H
+    from paper_2609_40247_amd import synth
+
+    tr = synth.config1()
+    n = tr.n
+    an = H.Analyzer(tr.params, n)
+    dcols = H.device_columns(tr.columns())
+    ev = H.events_struct(dcols)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        code = an.run(ev, n)
+        if code != 0:
+            raise RuntimeError(f"analysis failed: {H.herschel_strerror(code)}")
+    c = an.results(n)["counters"]
+
+    stage_id = H.STAGES.index(ROOFLINE_STAGE)
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    stream = torch.cuda.current_stream()
+    for a, b in pairs:  # create the events
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in pairs:
+        H.herschel_time_stage(stage_id, a, b)
+        code = an.run(ev, n)
+        if code != 0:
+            raise RuntimeError(f"analysis failed: {H.herschel_strerror(code)}")
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    H.herschel_time_stage(stage_id, None, None)
+    ms = (t1 - t0) * 1e3 / args.steps
+    stage_ms = sum(a.elapsed_time(b) for a, b in pairs) / args.steps
+
+    if args.stages:
+        for sid, name in enumerate(H.STAGES):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            tot = 0.0
+            for _ in range(5):
+                H.herschel_time_stage(sid, e0, e1)
+                an.run(ev, n)
+                tot += e0.elapsed_time(e1)
+            H.herschel_time_stage(sid, None, None)
+            print(f"stage {name:14s} {tot / 5 * 1e3:9.1f} us", file=sys.stderr)
+
+    alg = algorithmic_bytes(ROOFLINE_STAGE, n, c)
+    achieved = alg / (stage_ms * 1e-3) / 1e9
+    traffic = profiled_traffic(ROOFLINE_STAGE, "config1")
+    out = {
+        "metric": METRIC, "value": round(n / (ms * 1e-3) / 1e6, 3), "unit": "M ev/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "config": {"workload": "decode-step trace: 1 process, 4 streams, 30 s window, 1000 steps x 1000 kernels",
+                   "rows": n, "kernels": c["n_admitted_kernel"], "launches": c["n_admitted_launch"],
+                   "cpu_ops": c["n_admitted_cpu"], "outputs": "all"},
+        "roofline": {"kernel": f"k_{ROOFLINE_STAGE}", "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "algorithmic_bytes": alg, "launch_us": round(stage_ms * 1e3, 2)},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(tr.columns(), tr.params, n)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

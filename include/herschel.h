@@ -172,14 +172,41 @@ int herschel_trace_analyze(const herschel_events *ev, int64_t n, const herschel_
  * t holds rows [trace_offsets[t], trace_offsets[t+1]) (a HOST array of
  * n_traces + 1 entries) and uses p[t] and out[t] (HOST arrays of structs whose
  * pointers are device pointers).  Row indices in trace t's outputs are local
- * to the trace.  p[0].workspace must hold herschel_workspace_size() for the
- * largest trace; the workspace and stream of p[0] are used for all traces.
+ * to the trace.  p[0].workspace must hold the largest herschel_workspace_size()
+ * over the traces (each with its own p[t]); the workspace and stream of p[0]
+ * are used for all traces, one after the other.
  * Returns the first non-OK code in trace order, or HERSCHEL_OK. */
 int herschel_trace_analyze_batch(const herschel_events *ev, const int64_t *trace_offsets,
                                  int32_t n_traces, const herschel_params *p,
                                  herschel_outputs *out);
 
 const char *herschel_strerror(int code);
+
+/* Diagnostics for benchmarks.  Stages of one analysis call, in launch order. */
+enum {
+  HERSCHEL_STAGE_INIT = 0,     /* clear the workspace state and accumulating outputs */
+  HERSCHEL_STAGE_PREP = 1,     /* validate, correct, admit, compact (one kernel) */
+  HERSCHEL_STAGE_HIST = 2,     /* digit histograms of the three sort inputs */
+  HERSCHEL_STAGE_NAMES = 3,    /* per-name partial tables */
+  HERSCHEL_STAGE_SORT_TIMELINE = 4,
+  HERSCHEL_STAGE_TIMELINE = 5, /* busy/idle, gaps, coverage runs (one kernel) */
+  HERSCHEL_STAGE_OVERLAP = 6,  /* event sort and sweep */
+  HERSCHEL_STAGE_SORT_CONTAIN = 7,
+  HERSCHEL_STAGE_CONTAIN = 8,  /* op nesting and launch -> op */
+  HERSCHEL_STAGE_SORT_JOIN = 9,
+  HERSCHEL_STAGE_JOIN = 10,    /* launch <-> kernel join, latency (one kernel) */
+  HERSCHEL_STAGE_OPAGG = 11,   /* inclusive per-op aggregates (one kernel) */
+  HERSCHEL_STAGE_EDGES = 12,
+  HERSCHEL_STAGE_FINAL = 13,
+  HERSCHEL_N_STAGES = 14
+};
+
+/* Record start_event / stop_event (hipEvent_t, created by the caller) on
+ * params->hip_stream around stage `stage` of every following analysis call in
+ * this process, for measuring one stage's device time live.  NULL events turn
+ * the recording off.  Returns HERSCHEL_EINVAL for an unknown stage.  Not
+ * thread-safe: meant for single-threaded benchmarks. */
+int herschel_time_stage(int stage, void *start_event, void *stop_event);
 
 #ifdef __cplusplus
 }

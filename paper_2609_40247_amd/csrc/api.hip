@@ -278,34 +278,72 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   return HERSCHEL_OK;
 }
 
+// Stage timing for benchmarks (herschel_time_stage).
+static int g_stage = -1;
+static hipEvent_t g_ev0 = nullptr, g_ev1 = nullptr;
+static inline void stage_begin(Ctx& c, int s) {
+  if (s == g_stage && g_ev0) (void)hipEventRecord(g_ev0, c.st);
+}
+static inline void stage_end(Ctx& c, int s) {
+  if (s == g_stage && g_ev1) (void)hipEventRecord(g_ev1, c.st);
+}
+
 static int enqueue(Ctx& c) {
   static bool lds_attr = false;
   if (!lds_attr) {
     names_set_lds_attr();
     lds_attr = true;
   }
+  stage_begin(c, HERSCHEL_STAGE_INIT);
   launch_init(c);
+  stage_end(c, HERSCHEL_STAGE_INIT);
+  stage_begin(c, HERSCHEL_STAGE_PREP);
   launch_prep(c);
+  stage_end(c, HERSCHEL_STAGE_PREP);
+  stage_begin(c, HERSCHEL_STAGE_HIST);
   launch_hist(c, c.sK, &c.ds->nK);
   launch_hist(c, c.sJ, &c.ds->nJ);
   if (c.contain) launch_hist(c, c.sC, &c.ds->nCL);
+  stage_end(c, HERSCHEL_STAGE_HIST);
+  stage_begin(c, HERSCHEL_STAGE_NAMES);
   launch_names(c);
+  stage_end(c, HERSCHEL_STAGE_NAMES);
+  stage_begin(c, HERSCHEL_STAGE_SORT_TIMELINE);
   launch_sort(c, c.sK, &c.ds->nK);
+  stage_end(c, HERSCHEL_STAGE_SORT_TIMELINE);
+  stage_begin(c, HERSCHEL_STAGE_TIMELINE);
   launch_timeline(c);
+  stage_end(c, HERSCHEL_STAGE_TIMELINE);
+  stage_begin(c, HERSCHEL_STAGE_OVERLAP);
   if (c.overlap) launch_overlap(c);
+  stage_end(c, HERSCHEL_STAGE_OVERLAP);
   if (c.contain) {
+    stage_begin(c, HERSCHEL_STAGE_SORT_CONTAIN);
     launch_sort(c, c.sC, &c.ds->nCL);
+    stage_end(c, HERSCHEL_STAGE_SORT_CONTAIN);
+    stage_begin(c, HERSCHEL_STAGE_CONTAIN);
     launch_contain(c);
+    stage_end(c, HERSCHEL_STAGE_CONTAIN);
   } else {
     const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.n, 256 * 8), 1), 2048);
     hipLaunchKernelGGL(k_nocontain, dim3(grid), dim3(256), 0, c.st, c.sC.k[0], c.sC.v[0], c.ds, c.o.link, c.o.aux);
   }
+  stage_begin(c, HERSCHEL_STAGE_SORT_JOIN);
   launch_sort(c, c.sJ, &c.ds->nJ);
+  stage_end(c, HERSCHEL_STAGE_SORT_JOIN);
+  stage_begin(c, HERSCHEL_STAGE_JOIN);
   launch_join(c);
+  stage_end(c, HERSCHEL_STAGE_JOIN);
+  stage_begin(c, HERSCHEL_STAGE_OPAGG);
   if (c.contain) launch_opagg(c);
+  stage_end(c, HERSCHEL_STAGE_OPAGG);
+  stage_begin(c, HERSCHEL_STAGE_EDGES);
   launch_edges(c);
+  stage_end(c, HERSCHEL_STAGE_EDGES);
+  stage_begin(c, HERSCHEL_STAGE_FINAL);
   launch_names_reduce(c);
   launch_finalize(c);
+  stage_end(c, HERSCHEL_STAGE_FINAL);
   return hipGetLastError() == hipSuccess ? HERSCHEL_OK : HERSCHEL_EDEVICE;
 }
 
@@ -333,6 +371,14 @@ const char* herschel_strerror(int code) {
     case HERSCHEL_EDEVICE: return "device error";
     default: return "unknown error";
   }
+}
+
+int herschel_time_stage(int stage, void* start_event, void* stop_event) {
+  if (stage < 0 || stage >= HERSCHEL_N_STAGES) return HERSCHEL_EINVAL;
+  g_stage = (start_event && stop_event) ? stage : -1;
+  g_ev0 = (hipEvent_t)start_event;
+  g_ev1 = (hipEvent_t)stop_event;
+  return HERSCHEL_OK;
 }
 
 int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) {

@@ -86,6 +86,8 @@ def load(variant: str | None = None) -> ctypes.CDLL:
                                                      ctypes.POINTER(HerschelOutputs)]
         lib.herschel_strerror.restype = ctypes.c_char_p
         lib.herschel_strerror.argtypes = [ctypes.c_int]
+        lib.herschel_time_stage.restype = ctypes.c_int
+        lib.herschel_time_stage.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
         _lib[path] = lib
     return _lib[path]
 
@@ -116,6 +118,21 @@ def herschel_trace_analyze_batch(events: HerschelEvents, offsets: np.ndarray, pa
     return int(lib.herschel_trace_analyze_batch(ctypes.byref(events),
                                                 offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
                                                 T, parr, oarr))
+
+
+STAGES = ("init", "prep", "hist", "names", "sort_timeline", "timeline", "overlap", "sort_contain", "contain",
+          "sort_join", "join", "opagg", "edges", "final")
+
+
+def herschel_time_stage(stage: int, start_event, stop_event, lib=None) -> int:
+    """Record two torch.cuda.Event objects around one stage of following
+    calls (None, None stops)."""
+    lib = lib or load()
+    a = None if start_event is None else start_event.cuda_event
+    b = None if stop_event is None else stop_event.cuda_event
+    if (start_event is not None and not a) or (stop_event is not None and not b):
+        raise ValueError("record the events once before handing them over (torch creates them lazily)")
+    return int(lib.herschel_time_stage(int(stage), a, b))
 
 
 def herschel_strerror(code: int, lib=None) -> str:
