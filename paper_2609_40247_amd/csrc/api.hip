@@ -301,9 +301,11 @@ static int enqueue(Ctx& c) {
   launch_prep(c);
   stage_end(c, HERSCHEL_STAGE_PREP);
   stage_begin(c, HERSCHEL_STAGE_HIST);
-  launch_hist(c, c.sK, &c.ds->nK);
-  launch_hist(c, c.sJ, &c.ds->nJ);
-  if (c.contain) launch_hist(c, c.sC, &c.ds->nCL);
+  {
+    SortBufs* ss[3] = {&c.sK, &c.sJ, &c.sC};
+    const int32_t* cc[3] = {&c.ds->nK, &c.ds->nJ, &c.ds->nCL};
+    launch_hist_multi(c, ss, cc, c.contain ? 3 : 2);
+  }
   stage_end(c, HERSCHEL_STAGE_HIST);
   stage_begin(c, HERSCHEL_STAGE_NAMES);
   launch_names(c);

@@ -26,7 +26,8 @@ enum : uint32_t {
   DS_OOB = 2u,       // checked build: an index left its buffer
   DS_PARAM = 4u,     // clock_offset or stream_class out of range
   DS_TIES = 8u,      // more long runs of equal op starts than the list holds
-  DS_CAPACITY = 16u  // an internal list overflowed its bound
+  DS_CAPACITY = 16u, // an internal list overflowed its bound
+  DS_LOGIC = 32u     // an internal consistency check failed
 };
 
 // Ticket slots: one per look-back kernel launch in a call.
@@ -54,7 +55,11 @@ struct DevState {
   int32_t pad0;
   int64_t first_invalid;  // smallest bad row (INT64_MAX = none)
   int64_t n_gaps;
-  uint32_t hist[N_SORTS][8][256];  // radix digit histograms
+  uint32_t hist_done[N_SORTS];     // workgroups of the histogram kernel that finished
+  uint32_t sort_trivial[N_SORTS];  // bit d: every key has the same digit d (pass skipped)
+  // radix digit histograms; the last histogram workgroup turns each into the
+  // exclusive prefix over digit values (the global offset of every bin)
+  uint32_t hist[N_SORTS][8][256];
 };
 
 // Largest process count the per-process correlation-id table supports.

@@ -178,9 +178,9 @@ __global__ __launch_bounds__(CT_THREADS) void k_vbuild(ContainArgs a) {
   const int par = (int)a.ds->sort_parity[2];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
+  if ((int64_t)blockIdx.x * CT_TILE >= n) return;  // no tile: stay off the ticket counter
   const int tile = take_ticket(a.ds, TK_VBUILD, &s_tile);
   const int64_t base = (int64_t)tile * CT_TILE;
-  if (base >= n) return;
   // striped: item j of lane covers position base + wv*1024 + j*64 + lane, so
   // a wave's 64 lanes form one 64-group of the pyramid
   uint64_t wmax = 0;
@@ -235,13 +235,6 @@ __global__ __launch_bounds__(1024) void k_vlevels(ContainArgs a) {
   }
 }
 
-// Last index in [lo, hi) of level l whose value exceeds q, or -1.
-__device__ __forceinline__ int64_t scan_back(const uint64_t* arr, int64_t lo, int64_t hi, uint64_t q) {
-  for (int64_t i = hi - 1; i >= lo; --i)
-    if (arr[i] > q) return i;
-  return -1;
-}
-
 // Live entries of pyramid level l for n positions.
 __device__ __forceinline__ int64_t live(int64_t n, int l) {
   int64_t c = n;
@@ -249,25 +242,62 @@ __device__ __forceinline__ int64_t live(int64_t n, int l) {
   return c;
 }
 
-// Descend from entry i of level l to the last position below it with V > q.
-__device__ int64_t descend(const ContainArgs& a, int l, int64_t i, uint64_t q) {
-  const int64_t n = a.ds->nCL;
+// Answer of a query whose answer lies before its tile: one wave climbs the
+// pyramid from level 2 and descends, loading 64 entries per step and taking
+// the highest lane above q with a ballot.  Called by a whole wave.
+__device__ int64_t wave_escape(const ContainArgs& a, int64_t tile, uint64_t q, int64_t n) {
+  const int lane = lane_id();
+  int l = 2;
+  int64_t idx = tile;
+  int64_t f = -1;
+  while (l < a.nlev) {
+    const int64_t lo = (idx >> 6) << 6;
+    const int64_t e = lo + lane;
+    const uint64_t v = e < idx ? a.M[l][e] : 0ull;
+    const uint64_t b = ballot(v > q);
+    if (b) {
+      f = lo + 63 - __clzll((long long)b);
+      break;
+    }
+    idx >>= 6;
+    ++l;
+  }
+  if (f < 0) return -1;  // only when the prefix maximum said otherwise
   while (l > 0) {
     const uint64_t* lower = l - 1 == 0 ? a.V : a.M[l - 1];
-    const int64_t lo = i * 64, hi = min(lo + 64, live(n, l - 1));
-    const int64_t f = scan_back(lower, lo, hi, q);
-    if (f < 0) return -1;  // cannot happen when the entry exceeded q
-    i = f;
+    const int64_t lo = f * 64;
+    const int64_t hi = min(lo + 64, live(n, l - 1));
+    const int64_t e = lo + lane;
+    const uint64_t v = e < hi ? lower[e] : 0ull;
+    const uint64_t b = ballot(v > q);
+    if (!b) return -1;
+    f = lo + 63 - __clzll((long long)b);
     --l;
   }
-  return i;
+  return f;
+}
+
+// Largest j <= pos whose value exceeds q, given the wave's window maxima
+// w[k] = max(v[l - 2^k + 1 .. l]) held by every lane l (k = 0..5): skip
+// windows with no value above q, widest first.  -1 when there is none.
+__device__ __forceinline__ int wave_lift(const uint64_t (&w)[6], int pos, uint64_t q) {
+#pragma unroll
+  for (int k = 5; k >= 0; --k) {
+    const int src = pos < 0 ? 0 : pos;
+    const uint64_t wm = __shfl(w[k], src, WAVE);  // every lane takes part
+    if (pos - (1 << k) + 1 >= 0 && wm <= q) pos -= 1 << k;
+  }
+  return pos;
 }
 
 __global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
   __shared__ uint64_t s_v[CT_TILE];
   __shared__ uint64_t s_m1[CT_TILE / 64];
-  __shared__ uint64_t s_tm[CT_THREADS];
-  const int tid = threadIdx.x;
+  __shared__ uint64_t s_g[6][CT_TILE / 64];  // window maxima over the tile's groups
+  __shared__ uint64_t s_gpre[CT_TILE / 64];  // max over the tile's earlier groups and all earlier tiles
+  __shared__ uint16_t s_esc[CT_TILE];
+  __shared__ int s_nesc;
+  const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int64_t n = a.ds->nCL;
   const int par = (int)a.ds->sort_parity[2];
   const uint64_t* keys = a.k[par];
@@ -276,62 +306,101 @@ __global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
   const int64_t base = tile * CT_TILE;
   if (base >= n) return;
   const int64_t tn = min((int64_t)CT_TILE, n - base);
+  const int ng = (int)cdiv(tn, 64);
   for (int64_t i = tid; i < tn; i += CT_THREADS) s_v[i] = a.V[base + i];
-  for (int64_t i = tid; i < cdiv(tn, 64); i += CT_THREADS) s_m1[i] = a.M[1][tile * (CT_TILE / 64) + i];
+  if (tid < CT_TILE / 64) s_m1[tid] = tid < ng ? a.M[1][tile * (CT_TILE / 64) + tid] : 0ull;
+  if (tid == 0) s_nesc = 0;
   __syncthreads();
-  // blocked items: thread t owns positions [t*16, t*16+16) of the tile
-  const int64_t l0 = (int64_t)tid * CT_ITEMS;
-  uint64_t tmax = 0;
-  for (int j = 0; j < CT_ITEMS; ++j)
-    if (l0 + j < tn) tmax = s_v[l0 + j] > tmax ? s_v[l0 + j] : tmax;
-  s_tm[tid] = tmax;
+  if (wv == 0) {  // group-level window maxima and exclusive prefix maxima
+    uint64_t w = s_m1[lane];
+    s_g[0][lane] = w;
+#pragma unroll
+    for (int k = 1; k < 6; ++k) {
+      const uint64_t o = shfl_up(w, 1u << (k - 1));
+      if (lane >= (1 << (k - 1))) w = o > w ? o : w;
+      s_g[k][lane] = w;
+    }
+    uint64_t inc = s_m1[lane];
+    for (int d = 1; d < WAVE; d <<= 1) {
+      const uint64_t o = shfl_up(inc, d);
+      if (lane >= d) inc = o > inc ? o : inc;
+    }
+    const uint64_t ex = shfl_up(inc, 1);
+    const uint64_t pt = a.pmt[tile];
+    s_gpre[lane] = lane == 0 ? pt : (ex > pt ? ex : pt);
+  }
   __syncthreads();
-  // exclusive prefix max over threads (256 values, one pass per thread is
-  // cheap: strided by the wave to stay conflict-free)
-  uint64_t pm = a.pmt[tile];
-  for (int t = 0; t < tid; ++t) pm = s_tm[t] > pm ? s_tm[t] : pm;
-  for (int j = 0; j < CT_ITEMS; ++j) {
-    const int64_t lp = l0 + j;
-    if (lp >= tn) break;
+  // one wave per 64-position group, one lane per position
+  for (int g = wv; g < ng; g += CT_THREADS / WAVE) {
+    const int64_t lp = (int64_t)g * 64 + lane;
+    const bool live = lp < tn;
     const int64_t p = base + lp;
-    const uint64_t key = keys[p];
+    const uint64_t key = live ? keys[p] : 0ull;
     const uint64_t q = (key_seg(a, key) << a.vb) | (uint64_t)(key_rel(a, key) + 1);
+    const uint64_t v = live ? s_v[lp] : 0ull;
+    uint64_t w[6];
+    w[0] = v;
+#pragma unroll
+    for (int k = 1; k < 6; ++k) {
+      const uint64_t o = shfl_up(w[k - 1], 1u << (k - 1));
+      w[k] = (lane >= (1 << (k - 1)) && o > w[k - 1]) ? o : w[k - 1];
+    }
+    // exclusive prefix max inside the group, then the prefix before it
+    uint64_t inc = v;
+    for (int d = 1; d < WAVE; d <<= 1) {
+      const uint64_t o = shfl_up(inc, d);
+      if (lane >= d) inc = o > inc ? o : inc;
+    }
+    uint64_t pm = shfl_up(inc, 1);
+    if (lane == 0) pm = 0ull;
+    const uint64_t gp = s_gpre[g];
+    pm = pm > gp ? pm : gp;
+    const bool want = live && pm > q;
+    // level 0: this group
+    const int f0 = wave_lift(w, lane - 1, q);
     int64_t ans = -1;
-    if (pm > q) {
-      // level 0 within the 64-group, then the tile's groups (LDS)
-      const int64_t g = lp >> 6;
-      for (int64_t i = lp - 1; i >= g * 64; --i)
-        if (s_v[i] > q) {
-          ans = base + i;
-          break;
+    bool escape = false;
+    if (want) {
+      if (f0 >= 0) {
+        ans = base + (int64_t)g * 64 + f0;
+      } else {
+        // level 1: the tile's earlier groups, widest windows first
+        int h = g - 1;
+#pragma unroll
+        for (int k = 5; k >= 0; --k)
+          if (h - (1 << k) + 1 >= 0 && s_g[k][h] <= q) h -= 1 << k;
+        if (h >= 0) {
+          for (int i = h * 64 + 63; i >= h * 64; --i)
+            if (s_v[i] > q) {
+              ans = base + i;
+              break;
+            }
+        } else {
+          escape = true;
         }
-      if (ans < 0) {
-        for (int64_t h = g - 1; h >= 0 && ans < 0; --h)
-          if (s_m1[h] > q) {
-            for (int64_t i = h * 64 + 63; i >= h * 64; --i)
-              if (s_v[i] > q) {
-                ans = base + i;
-                break;
-              }
-          }
-      }
-      // earlier tiles: climb the pyramid from level 2, then descend
-      int64_t idx = tile;  // index at level 2
-      for (int l = 2; ans < 0 && l < a.nlev; ++l) {
-        const int64_t lo = (idx >> 6) << 6;
-        const int64_t f = scan_back(a.M[l], lo, idx, q);
-        if (f >= 0) {
-          ans = descend(a, l, f, q);
-          break;
-        }
-        idx >>= 6;
       }
     }
-    a.par[p] = (int32_t)ans;
-    const uint32_t row = vals[p];
-    a.link[row] = ans >= 0 ? (int32_t)vals[ans] : -1;
-    const uint64_t vv = s_v[lp];
-    pm = vv > pm ? vv : pm;
+    if (escape) {
+      const int slot = atomicAdd(&s_nesc, 1);
+      s_esc[slot] = (uint16_t)lp;
+    } else if (live) {
+      a.par[p] = (int32_t)ans;
+      a.link[vals[p]] = ans >= 0 ? (int32_t)vals[ans] : -1;
+    }
+  }
+  __syncthreads();
+  // answers in earlier tiles, one wave per query
+  const int nesc = s_nesc;
+  for (int e = wv; e < nesc; e += CT_THREADS / WAVE) {
+    const int64_t p = base + s_esc[e];
+    const uint64_t key = keys[p];
+    const uint64_t q = (key_seg(a, key) << a.vb) | (uint64_t)(key_rel(a, key) + 1);
+    const int64_t ans = wave_escape(a, tile, q, n);
+    if (lane == 0) {
+      if (ans < 0) set_status(a.ds, DS_LOGIC);
+      a.par[p] = (int32_t)ans;
+      a.link[vals[p]] = ans >= 0 ? (int32_t)vals[ans] : -1;
+    }
   }
 }
 

@@ -70,6 +70,7 @@ size_t layout_workspace(Ctx& c, char* base);
 void launch_init(Ctx& c);
 void launch_prep(Ctx& c);
 void launch_hist(Ctx& c, SortBufs& s, const int32_t* count);
+void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k);
 void launch_sort(Ctx& c, SortBufs& s, const int32_t* count);
 void launch_names(Ctx& c);
 void launch_timeline(Ctx& c);
@@ -85,9 +86,9 @@ int64_t prep_tile_rows();
 int64_t union_tile_elems();
 void names_set_lds_attr();
 
-constexpr int RS_THREADS = 256;
-constexpr int RS_ITEMS = 16;
-constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 4096 keys per tile
+constexpr int RS_THREADS = 1024;
+constexpr int RS_ITEMS = 8;
+constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 8192 keys per tile
 
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

@@ -66,22 +66,34 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
   for (int i = tid; i < a.NN * 4; i += NM_THREADS) out[i] = tab[i];
 }
 
+// One thread per (name, statistic): the tables are read with independent,
+// coalesced loads (consecutive threads read consecutive words).
 __global__ __launch_bounds__(256) void k_names_reduce(NamesArgs a) {
-  const int q = blockIdx.x * 256 + threadIdx.x;
-  if (q >= a.NN) return;
-  uint64_t c = 0, s = 0;
-  int64_t mn = I64MAX, mx = I64MIN;
-  for (int b = 0; b < a.blocks; ++b) {
-    const uint64_t* t = a.part + ((int64_t)b * a.NN + q) * 4;
-    c += t[0];
-    s += t[1];
-    mn = (int64_t)t[2] < mn ? (int64_t)t[2] : mn;
-    mx = (int64_t)t[3] > mx ? (int64_t)t[3] : mx;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)a.NN * 4) return;
+  const int q = (int)(t >> 2), stat = (int)(t & 3);
+  const int64_t stride = (int64_t)a.NN * 4;
+  uint64_t acc = stat == 2 ? (uint64_t)I64MAX : stat == 3 ? (uint64_t)I64MIN : 0;
+  int b = 0;
+  for (; b + 8 <= a.blocks; b += 8) {
+    uint64_t v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = a.part[(int64_t)(b + i) * stride + t];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (stat < 2) acc += v[i];
+      else if (stat == 2) acc = (int64_t)v[i] < (int64_t)acc ? v[i] : acc;
+      else acc = (int64_t)v[i] > (int64_t)acc ? v[i] : acc;
+    }
   }
-  a.count[q] = (int64_t)c;
-  a.sum[q] = (int64_t)s;
-  a.mn[q] = mn;
-  a.mx[q] = mx;
+  for (; b < a.blocks; ++b) {
+    const uint64_t v = a.part[(int64_t)b * stride + t];
+    if (stat < 2) acc += v;
+    else if (stat == 2) acc = (int64_t)v < (int64_t)acc ? v : acc;
+    else acc = (int64_t)v > (int64_t)acc ? v : acc;
+  }
+  int64_t* dst = stat == 0 ? a.count : stat == 1 ? a.sum : stat == 2 ? a.mn : a.mx;
+  dst[q] = (int64_t)acc;
 }
 
 static NamesArgs names_args(Ctx& c) {
@@ -115,7 +127,7 @@ void launch_names(Ctx& c) {
 void launch_names_reduce(Ctx& c) {
   if (c.NN > NM_LDS_NAMES) return;
   NamesArgs a = names_args(c);
-  hipLaunchKernelGGL(k_names_reduce, dim3((unsigned)cdiv(c.NN, 256)), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_names_reduce, dim3((unsigned)cdiv((int64_t)c.NN * 4, 256)), dim3(256), 0, c.st, a);
 }
 
 int names_lds_limit() { return NM_LDS_NAMES; }

@@ -1,9 +1,9 @@
 // LSD radix sort of 64-bit keys (optionally with a 32-bit payload) for CDNA4.
 //
-// One launch per 8-bit digit.  Each workgroup ranks a tile of 4096 keys with
+// One launch per 8-bit digit.  Each workgroup ranks a tile of 8192 keys with
 // wave64 ballots (a 64-lane match of the digit built from 8 ballots gives the
 // rank among equal digits in one step), publishes its 256 per-digit counts
-// through a decoupled look-back (one chain per digit, a lane per digit),
+// through a decoupled look-back (one chain per digit, four lanes per digit),
 // reorders the tile in LDS and writes each digit's run contiguously.  The
 // global offset of each digit comes from a histogram of all digits taken in
 // one pass before the first digit pass.  A digit on which every key agrees
@@ -17,80 +17,136 @@ constexpr uint32_t RS_FLAG_A = 1u << 30;
 constexpr uint32_t RS_FLAG_P = 2u << 30;
 constexpr uint32_t RS_VAL = (1u << 30) - 1;
 
-__global__ __launch_bounds__(256) void k_digit_hist(const uint64_t* __restrict__ keys, const int32_t* count,
-                                                    int nd, uint32_t* __restrict__ hist) {
+struct HistJob {
+  const uint64_t* keys;
+  const int32_t* count;
+  int nd;
+  int id;
+};
+struct HistJobs {
+  HistJob j[4];
+};
+
+// Digit histograms of several sort inputs in one launch (blockIdx.y picks
+// the sort).  Few, wide workgroups keep the number of global atomics on the
+// 256 * nd counters low.
+constexpr int HIST_THREADS = 512;
+
+__device__ __forceinline__ void hist_add(uint32_t* h, uint64_t k, int nd, uint64_t active, int first, int lane) {
+  for (int d = 0; d < nd; ++d) {
+    const int dg = (int)((k >> (8 * d)) & 255);
+    const int d0 = __shfl(dg, first, WAVE);
+    if (ballot(dg != d0) == 0) {
+      if (lane == first) atomicAdd(&h[d * 256 + d0], (uint32_t)popc(active));
+    } else {
+      atomicAdd(&h[d * 256 + dg], 1u);
+    }
+  }
+}
+
+__global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, DevState* ds) {
+  const HistJob jb = jobs.j[blockIdx.y];
+  const uint64_t* __restrict__ keys = jb.keys;
+  const int nd = jb.nd;
+  uint32_t* __restrict__ hist = &ds->hist[jb.id][0][0];
   __shared__ uint32_t h[8 * 256];
-  for (int i = threadIdx.x; i < 8 * 256; i += 256) h[i] = 0;
+  __shared__ uint32_t s_scan[HIST_THREADS / WAVE + 1];
+  __shared__ int s_last;
+  __shared__ int s_triv;
+  for (int i = threadIdx.x; i < 8 * 256; i += HIST_THREADS) h[i] = 0;
   __syncthreads();
-  const int64_t n = *count;
+  const int64_t n = *jb.count;
   const int lane = lane_id();
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+  // eight independent loads in flight per thread
+  constexpr int U = 8;
+  const int64_t stride = (int64_t)gridDim.x * HIST_THREADS;
+  int64_t i = (int64_t)blockIdx.x * HIST_THREADS + threadIdx.x;
+  for (; i + (U - 1) * stride < n; i += U * stride) {
+    uint64_t k[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) k[u] = keys[i + u * stride];
+    const uint64_t active = ballot(true);
+    const int first = __ffsll((unsigned long long)active) - 1;
+#pragma unroll
+    for (int u = 0; u < U; ++u) hist_add(h, k[u], nd, active, first, lane);
+  }
+  for (; i < n; i += stride) {
     const uint64_t k = keys[i];
     const uint64_t active = ballot(true);
     const int first = __ffsll((unsigned long long)active) - 1;
-    for (int d = 0; d < nd; ++d) {
-      const int dg = (int)((k >> (8 * d)) & 255);
-      const int d0 = __shfl(dg, first, WAVE);
-      if (ballot(dg != d0) == 0) {
-        if (lane == first) atomicAdd(&h[d * 256 + d0], (uint32_t)popc(active));
-      } else {
-        atomicAdd(&h[d * 256 + dg], 1u);
-      }
-    }
+    hist_add(h, k, nd, active, first, lane);
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < nd * 256; i += 256)
-    if (h[i]) atomicAdd(&hist[i], h[i]);
+  for (int j = threadIdx.x; j < nd * 256; j += HIST_THREADS)
+    if (h[j]) atomicAdd(&hist[j], h[j]);
+  // the last workgroup of this sort turns the counts into offsets
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(&ds->hist_done[jb.id], 1u) == gridDim.x - 1;
+  if (threadIdx.x == 0) s_triv = 0;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  uint32_t triv = 0;
+  for (int d = 0; d < nd; ++d) {
+    const uint32_t c = threadIdx.x < 256 ? ld_agent(&hist[d * 256 + threadIdx.x]) : 0u;
+    const int full = __syncthreads_or(threadIdx.x < 256 && c == (uint32_t)n);
+    if (full) triv |= 1u << d;
+    const uint32_t ex = block_excl_sum<HIST_THREADS>(c, s_scan, nullptr);
+    if (threadIdx.x < 256) hist[d * 256 + threadIdx.x] = ex;
+  }
+  if (threadIdx.x == 0) {
+    ds->sort_trivial[jb.id] = triv;
+    const uint32_t ran = ~triv & ((nd >= 32 ? 0u : (1u << nd)) - 1u);
+    ds->sort_parity[jb.id] = (uint32_t)(popc(ran) & 1);
+  }
 }
 
 template <bool VALS>
 __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_t* k1, uint32_t* v0, uint32_t* v1,
                                                            const int32_t* count, DevState* ds, int id, int d,
                                                            uint32_t* status) {
+  constexpr int NW = RS_THREADS / WAVE;     // waves per workgroup
+  constexpr int NSL = RS_THREADS / 256;     // look-back slices per digit
   __shared__ uint64_t s_key[RS_TILE];
   __shared__ uint32_t s_val[VALS ? RS_TILE : 1];
-  __shared__ uint32_t s_wh[RS_THREADS / WAVE][256];
+  __shared__ uint32_t s_wh[NW][256];
   __shared__ uint32_t s_local[256];
   __shared__ uint32_t s_glob[256];
-  __shared__ uint32_t s_scan[RS_THREADS / WAVE + 1];
+  __shared__ uint32_t s_scan[NW + 1];
+  __shared__ uint32_t s_lb_sum[NSL][256];
+  __shared__ uint8_t s_lb_state[NSL][256];
   __shared__ int s_tile;
 
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
+  const int dgt = tid & 255, slice = tid >> 8;
+  // The plan (trivial digits, offsets) was made by the histogram kernel.  A
+  // digit is trivial iff one bin holds every key; the input buffer's parity
+  // is the number of non-trivial digits below this one.  Workgroups with no
+  // tile to sort leave before the ticket: the ticket counter is one address,
+  // and every request to it is served in turn.  The first cdiv(n, tile)
+  // workgroups stay, so they draw exactly the tickets of the real tiles.
   const uint32_t n = (uint32_t)*count;
-
-  // Which buffer holds the input, and is this digit trivial?  A digit is
-  // trivial iff one bin holds every key.  Every block decides identically.
-  int parity = 0, trivial = 0;
-  for (int dd = 0; dd <= d; ++dd) {
-    const int full = ds->hist[id][dd][tid] == n;
-    const int any = __syncthreads_or(full);
-    if (dd < d)
-      parity += any ? 0 : 1;
-    else
-      trivial = any;
-  }
-  if (trivial) {
-    if (blockIdx.x == 0 && tid == 0) ds->sort_parity[id] = (uint32_t)(parity & 1);
-    return;
-  }
-  if (blockIdx.x == 0 && tid == 0) ds->sort_parity[id] = (uint32_t)((parity + 1) & 1);
-  const uint64_t* kin = (parity & 1) ? k1 : k0;
-  uint64_t* kout = (parity & 1) ? k0 : k1;
-  const uint32_t* vin = (parity & 1) ? v1 : v0;
-  uint32_t* vout = (parity & 1) ? v0 : v1;
-
-  const int tile = take_ticket(ds, TK_RADIX + 8 * id + d, &s_tile);
-  const int64_t base = (int64_t)tile * RS_TILE;
-  if (base >= (int64_t)n) return;
-
-  for (int i = tid; i < (RS_THREADS / WAVE) * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
+  const uint32_t triv = ds->sort_trivial[id];
+  const uint32_t gexcl = ds->hist[id][d][dgt];
+  if (((triv >> d) & 1) || (int64_t)blockIdx.x * RS_TILE >= (int64_t)n) return;
+  if (tid == 0) s_tile = (int)atomicAdd(&ds->ticket[TK_RADIX + 8 * id + d], 1u);
+  for (int i = tid; i < NW * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
   __syncthreads();
+  const int parity = popc(~triv & ((1u << d) - 1u)) & 1;
+  const uint64_t* kin = parity ? k1 : k0;
+  uint64_t* kout = parity ? k0 : k1;
+  const uint32_t* vin = parity ? v1 : v0;
+  uint32_t* vout = parity ? v0 : v1;
+  const int tile = s_tile;
+  const int64_t base = (int64_t)tile * RS_TILE;
 
   const int shift = 8 * d;
   uint64_t key[RS_ITEMS];
   uint32_t val[RS_ITEMS];
   uint32_t rank[RS_ITEMS];
   int dig[RS_ITEMS];
+  // each wave owns RS_ITEMS * 64 consecutive keys, item j of lane l at j*64+l
   const int64_t wbase = base + (int64_t)wv * (RS_ITEMS * WAVE);
 #pragma unroll
   for (int j = 0; j < RS_ITEMS; ++j) {
@@ -98,10 +154,13 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
     const bool ok = idx < (int64_t)n;
     key[j] = ok ? kin[idx] : 0ull;
     if (VALS) val[j] = ok ? vin[idx] : 0u;
-    dig[j] = ok ? (int)((key[j] >> shift) & 255) : 256;
   }
-  // Wave-private ranking in input order: sub-tile of the wave, rounds in
-  // order, lanes in order.
+#pragma unroll
+  for (int j = 0; j < RS_ITEMS; ++j) {
+    const int64_t idx = wbase + j * WAVE + lane;
+    dig[j] = idx < (int64_t)n ? (int)((key[j] >> shift) & 255) : 256;
+  }
+  // Wave-private ranking in input order: items in order, lanes in order.
   const uint64_t lt = lanemask_lt();
 #pragma unroll
   for (int j = 0; j < RS_ITEMS; ++j) {
@@ -121,41 +180,93 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
   }
   __syncthreads();
 
-  // Thread t owns digit t: tile count, per-wave exclusive offsets.
+  // Threads 0..255 own one digit each: tile count, per-wave exclusive offsets.
   uint32_t cnt = 0;
+  if (tid < 256) {
 #pragma unroll
-  for (int w = 0; w < RS_THREADS / WAVE; ++w) {
-    const uint32_t c = s_wh[w][tid];
-    s_wh[w][tid] = cnt;
-    cnt += c;
+    for (int w = 0; w < NW; ++w) {
+      const uint32_t c = s_wh[w][tid];
+      s_wh[w][tid] = cnt;
+      cnt += c;
+    }
   }
   uint32_t* st = status + (int64_t)tile * 256;
-  st_agent(&st[tid], (tile == 0 ? RS_FLAG_P : RS_FLAG_A) | cnt);
+  if (tid < 256) st_agent(&st[tid], (tile == 0 ? RS_FLAG_P : RS_FLAG_A) | cnt);
   const uint32_t local_excl = block_excl_sum<RS_THREADS>(cnt, s_scan, nullptr);
-  s_local[tid] = local_excl;
-  const uint32_t gexcl = block_excl_sum<RS_THREADS>(ds->hist[id][d][tid], s_scan, nullptr);
+  if (tid < 256) s_local[tid] = local_excl;
 
+  // Look-back: every digit has NSL threads, each polling LB_WIN predecessors
+  // per round trip (independent loads), so one round covers NSL * LB_WIN
+  // tiles.  A round is used up to the nearest tile that published its
+  // inclusive prefix; a round with an unpublished tile before that is
+  // polled again.  The loop condition is uniform over the workgroup.
   uint32_t excl = 0;
   if (tile > 0) {
-    int pred = tile - 1;
+    constexpr int LB_WIN = 16;
+    int pred = tile - 1;  // newest predecessor not yet counted
+    bool done = false;
     uint32_t spins = 0;
-    while (pred >= 0) {
-      const uint32_t s = ld_agent(&status[(int64_t)pred * 256 + tid]);
-      if ((s >> 30) == 0) {
-        if (++spins > SPIN_LIMIT) {
-          set_status(ds, DS_SPIN);
-          break;
+    for (;;) {
+      const int top = pred - slice * LB_WIN;
+      uint32_t sum = 0;
+      int state = 1;  // 0: not ready, 1: all aggregates, 2: reached a prefix
+      if (!done) {
+        uint32_t sv[LB_WIN];
+#pragma unroll
+        for (int i = 0; i < LB_WIN; ++i)
+          sv[i] = top - i >= 0 ? ld_agent(&status[(int64_t)(top - i) * 256 + dgt]) : RS_FLAG_P;
+#pragma unroll
+        for (int i = 0; i < LB_WIN; ++i) {
+          if (state != 1) break;
+          const uint32_t f = sv[i] >> 30;
+          if (f == 0) {
+            state = 0;
+          } else {
+            sum += sv[i] & RS_VAL;
+            if (f == 2) state = 2;
+          }
         }
-        __builtin_amdgcn_s_sleep(1);
-        continue;
       }
-      excl += s & RS_VAL;
-      if ((s >> 30) == 2) break;
-      --pred;
+      s_lb_sum[slice][dgt] = sum;
+      s_lb_state[slice][dgt] = (uint8_t)state;
+      __syncthreads();
+      bool again = false;
+      if (!done) {
+        // combine the slices newest-first; every thread of the digit does it
+        uint32_t add = 0;
+        int res = 1;
+#pragma unroll
+        for (int sl = 0; sl < NSL; ++sl) {
+          const int stt = s_lb_state[sl][dgt];
+          if (stt == 0) {
+            res = 0;
+            break;
+          }
+          add += s_lb_sum[sl][dgt];
+          if (stt == 2) {
+            res = 2;
+            break;
+          }
+        }
+        if (res == 0) {
+          if (++spins > SPIN_LIMIT) {
+            set_status(ds, DS_SPIN);
+            done = true;
+          } else {
+            again = true;
+          }
+        } else {
+          excl += add;
+          pred -= NSL * LB_WIN;
+          if (res == 2 || pred < 0) done = true;
+        }
+      }
+      if (!__syncthreads_or(!done)) break;
+      if (again) __builtin_amdgcn_s_sleep(1);
     }
-    st_agent(&st[tid], RS_FLAG_P | ((excl + cnt) & RS_VAL));
+    if (tid < 256) st_agent(&st[tid], RS_FLAG_P | ((excl + cnt) & RS_VAL));
   }
-  s_glob[tid] = gexcl + excl;
+  if (tid < 256) s_glob[tid] = gexcl + excl;
   __syncthreads();
 
 #pragma unroll
@@ -182,11 +293,24 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
   }
 }
 
+void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k) {
+  HistJobs jobs{};
+  int m = 0;
+  int64_t n_max = 1;
+  for (int i = 0; i < k; ++i) {
+    if (s[i]->nd == 0) continue;
+    jobs.j[m++] = HistJob{s[i]->k[0], count[i], s[i]->nd, s[i]->id};
+    n_max = std::max<int64_t>(n_max, s[i]->n_max);
+  }
+  if (m == 0) return;
+  const int64_t grid = std::min<int64_t>(std::max<int64_t>(cdiv(n_max, 32768), 1), 64);
+  hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid, (unsigned)m), dim3(HIST_THREADS), 0, c.st, jobs, c.ds);
+}
+
 void launch_hist(Ctx& c, SortBufs& s, const int32_t* count) {
-  if (s.nd == 0) return;
-  const int64_t grid = std::min<int64_t>(std::max<int64_t>(cdiv(s.n_max, 8192), 1), 512);
-  hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid), dim3(256), 0, c.st, s.k[0], count, s.nd,
-                     &c.ds->hist[s.id][0][0]);
+  SortBufs* ss[1] = {&s};
+  const int32_t* cc[1] = {count};
+  launch_hist_multi(c, ss, cc, 1);
 }
 
 void launch_sort(Ctx& c, SortBufs& s, const int32_t* count) {

@@ -88,7 +88,7 @@ __device__ __forceinline__ void put_event(const UnionArgs& a, int64_t pos, int32
 // Walks this thread's elements with the incoming carry.  MODE 0 counts gaps
 // and events and accumulates busy time; MODE 1 writes gaps and events.
 template <int MODE>
-__device__ void walk(const UnionArgs& a, const Elem* x, int nv, int32_t prev_seg, int32_t next_seg, uint64_t m_in,
+__device__ __forceinline__ void walk(const UnionArgs& a, const Elem* x, int nv, int32_t prev_seg, int32_t next_seg, uint64_t m_in,
                      int64_t i0, int64_t nK, uint32_t* ngap, uint32_t* nev, int64_t gbase, int64_t ebase,
                      int64_t* s_busy, int32_t seg0) {
   const int nseg = a.P * a.S;
@@ -100,7 +100,7 @@ __device__ void walk(const UnionArgs& a, const Elem* x, int nv, int32_t prev_seg
   int32_t busy_seg = -1;
 #pragma unroll
   for (int j = 0; j < UN_ITEMS; ++j) {
-    if (j >= nv) break;
+    if (j >= nv) continue;
     const Elem& q = x[j];
     if (q.seg != prev) {
       const int32_t from = prev + 1;  // empty streams strictly between
@@ -189,9 +189,9 @@ __global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
   const int par = (int)a.ds->sort_parity[0];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
-  const int tile = take_ticket(a.ds, TK_UNION, &s_tile);
   const int64_t ntiles = nK > 0 ? cdiv(nK, UN_TILE) : 1;
-  if (tile >= ntiles) return;
+  if ((int64_t)blockIdx.x >= ntiles) return;  // no tile: stay off the ticket counter
+  const int tile = take_ticket(a.ds, TK_UNION, &s_tile);
   const int64_t base = (int64_t)tile * UN_TILE;
   const int nseg = a.P * a.S;
 
@@ -235,7 +235,7 @@ __global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
     int32_t prev = prev_seg;
 #pragma unroll
     for (int j = 0; j < UN_ITEMS; ++j) {
-      if (j >= nv) break;
+      if (j >= nv) continue;
       if (x[j].seg != prev) {
         head = true;
         m = 0;
