@@ -54,18 +54,12 @@ size_t layout_workspace(Ctx& c, char* base) {
   sort_plan(c.sK, 0, n, c.pb + c.sb + c.wb, true);
   sort_plan(c.sJ, 1, n, 49 + c.pb, true);
   sort_plan(c.sC, 2, n, c.pb + c.tb + c.wb + 1, true);
-  sort_plan(c.sE, 3, 2 * n, c.pb + c.wb1 + c.sb, false);
   c.sK.status = b.take<uint32_t>((int64_t)c.sK.nd * c.sK.tiles_max * 256);
   c.sJ.status = b.take<uint32_t>((int64_t)c.sJ.nd * c.sJ.tiles_max * 256);
   if (c.contain) {
     c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
     c.vb_status = b.take<uint64_t>(c.vb_tiles);
     c.sC.status = b.take<uint32_t>((int64_t)c.sC.nd * c.sC.tiles_max * 256);
-  }
-  if (c.overlap) {
-    c.sweep_tiles = std::max<int64_t>(cdiv(2 * n, 4096), 1);
-    c.sweep_status = b.take<uint64_t>(2 * c.sweep_tiles);
-    c.sE.status = b.take<uint32_t>((int64_t)c.sE.nd * c.sE.tiles_max * 256);
   }
   c.zero_bytes = align_up(b.off - z0);
   // sort buffers
@@ -82,8 +76,10 @@ size_t layout_workspace(Ctx& c, char* base) {
     s->v[1] = b.take<uint32_t>(n);
   }
   if (c.overlap) {
-    c.sE.k[0] = b.take<uint64_t>(2 * n);
-    c.sE.k[1] = b.take<uint64_t>(2 * n);
+    c.ev_cap = 2 * n;
+    c.ev_keys = b.take<uint64_t>(c.ev_cap);
+    c.seg_off = b.take<int32_t>((int64_t)c.P * c.S + 1);
+    if (c.S > 1 && c.S <= 8) c.corank = b.take<int32_t>(c.ev_cap * c.S);
   }
   if (c.contain) {
     c.V = b.take<uint64_t>(n);

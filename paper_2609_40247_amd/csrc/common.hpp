@@ -35,12 +35,11 @@ enum : int {
   TK_PREP = 0,
   TK_UNION = 1,
   TK_VBUILD = 2,
-  TK_SWEEP = 3,
   TK_RADIX = 8  // + 8 * sort + pass
 };
-constexpr int N_TICKETS = TK_RADIX + 8 * 4;
+constexpr int N_TICKETS = TK_RADIX + 8 * 3;
 
-constexpr int N_SORTS = 4;  // 0 timeline, 1 join, 2 containment, 3 overlap events
+constexpr int N_SORTS = 3;  // 0 timeline, 1 join, 2 containment
 
 // Per-call device state, zeroed by the init kernel.
 struct DevState {

@@ -40,11 +40,13 @@ struct Ctx {
   uint64_t* union_status = nullptr;  // [union_tiles * 3]
   int64_t union_tiles = 0;
   uint64_t* vb_status = nullptr;     // [vb_tiles]
-  uint64_t* sweep_status = nullptr;  // [2 * sweep_tiles]
-  int64_t sweep_tiles = 0;
   int64_t vb_tiles = 0;
   int64_t* corr_min = nullptr;       // [P]
-  SortBufs sK, sJ, sC, sE;           // timeline, join, containment, overlap events
+  SortBufs sK, sJ, sC;               // timeline, join, containment
+  uint64_t* ev_keys = nullptr;       // [ev_cap] coverage run endpoints, grouped by (pid, stream)
+  int64_t ev_cap = 0;
+  int32_t* seg_off = nullptr;        // [P * S + 1] first endpoint of each (pid, stream)
+  int32_t* corank = nullptr;         // [ev_cap * S] endpoint co-ranks in sibling streams (S <= 8)
   uint64_t* V = nullptr;             // [n] containment encoding per sorted position
   uint64_t* M[6] = {};               // max pyramid, level l covers 64^l positions
   int64_t Mn[6] = {};

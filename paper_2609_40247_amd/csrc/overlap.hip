@@ -2,13 +2,19 @@
 // observations", panel "Overlap and exposed work"; Section 6.1 separates
 // communication hidden by computation from exposed time).
 //
-// Every coverage run of a stream contributes a start and an end event; with
-// the events of a process sorted by time, the set of active streams between
-// consecutive events is the XOR of all earlier events' stream bits.  Whole
-// processes XOR to zero (every run closes), so a plain prefix XOR across the
-// sorted list -- carried between tiles by a decoupled look-back on its two
-// 32-bit halves -- gives each elementary interval's active mask.  Its length
-// is added to every active pair, to the classes present and to "any".
+// Every coverage run of a stream contributes a start and an end event.  The
+// timeline stage emits them grouped by (pid, stream) with strictly rising
+// times inside a group, so starts and ends alternate.  Ordering a process's
+// events by (time, stream) -- the order of the keys -- the elementary
+// interval after event e ends at the first later event of any stream, and a
+// stream is active in it iff an odd number of its events precede it.  Both
+// follow from e's co-rank in each sibling group (how many of its events
+// order before e), so the events are never merged into one sorted list.
+// With up to 8 streams the co-ranks come from a merge path over every pair
+// of a process's groups (each thread takes a fixed number of merge steps,
+// whatever the two groups' densities); with more, from binary searches.
+// The interval's length is added to every active pair, to the classes
+// present and to "any".
 #include "internal.hpp"
 
 namespace hx {
@@ -16,9 +22,14 @@ namespace hx {
 constexpr int SW_THREADS = 256;
 constexpr int SW_ITEMS = 16;
 constexpr int SW_TILE = SW_THREADS * SW_ITEMS;
+constexpr int CR_STEPS = 16;  // merge-path steps per thread
+constexpr int CR_SMAX = 8;    // most streams handled with pairwise merges
 
 struct SweepArgs {
-  const uint64_t* k[2];
+  const uint64_t* ev;  // (pid << (wb1 + sb)) | (t << sb) | stream, grouped by (pid, stream)
+  int32_t* seg_off;    // [P * S + 1] first event of each group
+  int32_t* corank;     // [S][ev_cap] co-rank of each event in each sibling group (S <= 8)
+  int64_t ev_cap;
   const uint8_t* cls;
   int P, S, sb, wb1;
   DevState* ds;
@@ -26,8 +37,6 @@ struct SweepArgs {
   int64_t* class_busy;
   int64_t* class_overlap;
   int64_t* any_busy;
-  uint64_t* status;  // [2][tiles_max]
-  int64_t tiles_max;
 };
 
 __device__ __forceinline__ void add_interval(const SweepArgs& a, uint64_t m, int64_t len, int pid, int pid0,
@@ -71,68 +80,139 @@ __device__ __forceinline__ void add_interval(const SweepArgs& a, uint64_t m, int
   }
 }
 
-// Sums over one thread's intervals, kept in registers for up to SMAX streams
-// (upper triangles of the symmetric pair and class matrices).
-template <int SMAX>
-struct SweepAcc {
-  static constexpr int NP = SMAX * (SMAX + 1) / 2;
-  uint64_t pair[NP];
-  uint64_t co[6];  // class overlap upper triangle: 00 01 02 11 12 22
-  uint64_t cb[3];
-  uint64_t any;
-  __device__ void zero() {
-#pragma unroll
-    for (int i = 0; i < NP; ++i) pair[i] = 0;
-#pragma unroll
-    for (int i = 0; i < 6; ++i) co[i] = 0;
-    cb[0] = cb[1] = cb[2] = 0;
-    any = 0;
-  }
-  __device__ void add(uint64_t m, uint64_t len, const uint64_t* cmask) {
-    if (m == 0) return;
-    any += len;
-    const bool p0 = (m & cmask[0]) != 0, p1 = (m & cmask[1]) != 0, p2 = (m & cmask[2]) != 0;
-    cb[0] += p0 ? len : 0;
-    cb[1] += p1 ? len : 0;
-    cb[2] += p2 ? len : 0;
-    co[0] += p0 ? len : 0;
-    co[1] += (p0 && p1) ? len : 0;
-    co[2] += (p0 && p2) ? len : 0;
-    co[3] += p1 ? len : 0;
-    co[4] += (p1 && p2) ? len : 0;
-    co[5] += p2 ? len : 0;
-    int k = 0;
-#pragma unroll
-    for (int i = 0; i < SMAX; ++i) {
-      const bool bi = (m >> i) & 1;
-#pragma unroll
-      for (int j = i; j < SMAX; ++j) {
-        pair[k] += (bi && ((m >> j) & 1)) ? len : 0;
-        ++k;
+// First event of every (pid, stream) group, by binary search over the group
+// order of the events; entry P * S is the event count.
+__global__ __launch_bounds__(256) void k_segoff(SweepArgs a) {
+  const int32_t n = a.ds->nEv;
+  const int nseg = a.P * a.S;
+  const int pshift = a.wb1 + a.sb;
+  const uint64_t smask = (1ull << a.sb) - 1;
+  for (int g = blockIdx.x * 256 + threadIdx.x; g <= nseg; g += gridDim.x * 256) {
+    int32_t lo = 0, len = n;
+    while (len > 0) {
+      const int32_t half = len >> 1;
+      const uint64_t k = a.ev[lo + half];
+      const int sg = (int)(k >> pshift) * a.S + (int)(k & smask);
+      if (sg < g) {
+        lo += half + 1;
+        len -= half + 1;
+      } else {
+        len = half;
       }
     }
+    a.seg_off[g] = lo;
   }
-};
+}
 
+// Co-ranks by merge path.  For process p the pairs (s, s2), s < s2, of its
+// groups are laid end to end; the merge of pair (s, s2) has n_s + n_s2
+// steps, so p owns (S - 1) * n_p steps and the steps of all processes form
+// one index space in process order.  A thread takes CR_STEPS consecutive
+// steps: it finds its process by binary search, its pair by a walk over at
+// most 28 pairs and its position in the merge by the usual diagonal binary
+// search, then merges; each step emits the co-rank of the smaller head in
+// the other group (keys of different streams never tie).
+__global__ __launch_bounds__(256) void k_corank(SweepArgs a) {
+  const int64_t n = a.ds->nEv;
+  const int S = a.S, P = a.P;
+  const int64_t total = (int64_t)(S - 1) * n;
+  const int64_t d0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * CR_STEPS;
+  if (d0 >= total) return;
+  const int32_t* off = a.seg_off;
+  int lo = 0, hi = P - 1;  // the last process whose steps start at or before d0
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if ((int64_t)(S - 1) * off[mid * S] <= d0)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  int p = lo;
+  int64_t dl = d0 - (int64_t)(S - 1) * off[p * S];
+  int s = 0, s2 = 1;
+  int32_t LA = off[p * S], nA = off[p * S + 1] - LA;
+  int32_t LB = off[p * S + 1], nB = off[p * S + 2] - LB;
+  while (dl >= (int64_t)nA + nB) {  // pairs wholly before d0 (all in process p)
+    dl -= (int64_t)nA + nB;
+    if (++s2 == S) {
+      ++s;
+      s2 = s + 1;
+    }
+    LA = off[p * S + s];
+    nA = off[p * S + s + 1] - LA;
+    LB = off[p * S + s2];
+    nB = off[p * S + s2 + 1] - LB;
+  }
+  // position on the diagonal: i heads of A among the first dl merged keys
+  int32_t ilo = (int32_t)max<int64_t>(0, dl - nB), ihi = (int32_t)min<int64_t>(dl, nA);
+  while (ilo < ihi) {
+    const int32_t mid = (ilo + ihi) >> 1;
+    if (a.ev[LA + mid] < a.ev[LB + (int32_t)dl - mid - 1])
+      ilo = mid + 1;
+    else
+      ihi = mid;
+  }
+  int32_t i = ilo, j = (int32_t)dl - ilo;
+  uint64_t va = i < nA ? a.ev[LA + i] : ~0ull;
+  uint64_t vb = j < nB ? a.ev[LB + j] : ~0ull;
+  int64_t steps = min<int64_t>(CR_STEPS, total - d0);
+  while (steps > 0) {
+    if (i == nA && j == nB) {  // next pair, or the first pair of the next process
+      if (++s2 == S) {
+        ++s;
+        s2 = s + 1;
+      }
+      if (s >= S - 1) {
+        ++p;
+        s = 0;
+        s2 = 1;
+      }
+      LA = off[p * S + s];
+      nA = off[p * S + s + 1] - LA;
+      LB = off[p * S + s2];
+      nB = off[p * S + s2 + 1] - LB;
+      i = j = 0;
+      va = nA > 0 ? a.ev[LA] : ~0ull;
+      vb = nB > 0 ? a.ev[LB] : ~0ull;
+      continue;
+    }
+    if (va < vb) {
+      a.corank[(int64_t)s2 * a.ev_cap + LA + i] = j;
+      ++i;
+      va = i < nA ? a.ev[LA + i] : ~0ull;
+    } else {
+      a.corank[(int64_t)s * a.ev_cap + LB + j] = i;
+      ++j;
+      vb = j < nB ? a.ev[LB + j] : ~0ull;
+    }
+    --steps;
+  }
+}
+
+// One event per thread and item (items striped over the workgroup).  With
+// at most 8 streams a workgroup sums interval lengths per active-stream mask
+// in LDS and expands the 2^S sums into pairs, classes and "any" at the end;
+// with more streams every interval is added to the pair matrix in LDS
+// directly.  Intervals of a process other than the workgroup's first go
+// straight to the outputs.
 template <int SMAX>
 __global__ __launch_bounds__(SW_THREADS) void k_sweep(SweepArgs a) {
-  __shared__ int s_tile;
-  __shared__ unsigned long long s_pair[SMAX <= 8 ? SweepAcc<8>::NP : 64 * 64];
+  constexpr bool SMALL = SMAX <= CR_SMAX;
+  __shared__ unsigned long long s_mlen[SMALL ? 256 : 1];
+  __shared__ unsigned long long s_pair[SMALL ? 1 : 64 * 64];
   __shared__ unsigned long long s_cls[13];  // class_busy[3], class_overlap[9], any
   __shared__ uint64_t s_cmask[3];
-  __shared__ uint64_t s_wx[SW_THREADS / WAVE];
-  __shared__ uint64_t s_tx;
-  __shared__ uint64_t s_pre[2];
-  const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
-  const int64_t n = a.ds->nEv;
-  const int par = (int)a.ds->sort_parity[3];
-  const uint64_t* keys = a.k[par];
-  if ((int64_t)blockIdx.x * SW_TILE >= n) return;  // no tile: stay off the ticket counter
-  const int tile = take_ticket(a.ds, TK_SWEEP, &s_tile);
-  const int64_t base = (int64_t)tile * SW_TILE;
+  __shared__ int32_t s_off0[SMAX + 1];  // group starts of the workgroup's first process
+  const int tid = threadIdx.x;
+  const int32_t n = a.ds->nEv;
+  const int64_t base = (int64_t)blockIdx.x * SW_TILE;
+  if (base >= n) return;
   const int S = a.S;
-  constexpr int NPAIR = SMAX <= 8 ? SweepAcc<8>::NP : 64 * 64;
-  for (int i = tid; i < NPAIR; i += SW_THREADS) s_pair[i] = 0;
+  if (SMALL) {
+    for (int i = tid; i < 256; i += SW_THREADS) s_mlen[i] = 0;
+  } else {
+    for (int i = tid; i < 64 * 64; i += SW_THREADS) s_pair[i] = 0;
+  }
   if (tid < 13) s_cls[tid] = 0;
   if (tid < 3) {
     uint64_t m = 0;
@@ -143,114 +223,163 @@ __global__ __launch_bounds__(SW_THREADS) void k_sweep(SweepArgs a) {
   const uint64_t tmask = (1ull << a.wb1) - 1;
   const uint64_t smask = (1ull << a.sb) - 1;
   const int pshift = a.wb1 + a.sb;
-  const int64_t i0 = base + (int64_t)tid * SW_ITEMS;
-  uint64_t key[SW_ITEMS];
-  uint64_t x = 0;
-#pragma unroll
-  for (int j = 0; j < SW_ITEMS; ++j) {
-    key[j] = i0 + j < n ? keys[i0 + j] : 0;
-    if (i0 + j < n) x ^= 1ull << (key[j] & smask);
-  }
-  // exclusive XOR over the block
-  uint64_t inc = x;
-  for (int d = 1; d < WAVE; d <<= 1) {
-    const uint64_t o = shfl_up(inc, d);
-    if (lane >= d) inc ^= o;
-  }
-  if (lane == WAVE - 1) s_wx[wv] = inc;
+  const int pid0 = (int)(a.ev[base] >> pshift);
+  if (SMALL && tid <= S) s_off0[tid] = a.seg_off[pid0 * S + tid];
   __syncthreads();
-  if (tid == 0) {
-    uint64_t run = 0;
-    for (int w = 0; w < SW_THREADS / WAVE; ++w) {
-      const uint64_t t = s_wx[w];
-      s_wx[w] = run;
-      run ^= t;
-    }
-    s_tx = run;
-  }
-  __syncthreads();
-  if (wv < 2) {
-    const uint64_t half = wv == 0 ? (s_tx & 0xffffffffull) : (s_tx >> 32);
-    const uint64_t ex = wave_lookback<OpXor32>(a.status + (int64_t)wv * a.tiles_max, tile, half, a.ds);
-    if (lane == 0) s_pre[wv] = ex;
-  }
-  __syncthreads();
-  uint64_t m = (s_pre[0] | (s_pre[1] << 32)) ^ s_wx[wv] ^ (inc ^ x);
-  const uint64_t nextkey = i0 + SW_ITEMS < n ? keys[i0 + SW_ITEMS] : 0;
-  const int pid0 = (int)(keys[base] >> pshift);
-  uint64_t cm[3] = {s_cmask[0], s_cmask[1], s_cmask[2]};
-  SweepAcc<SMAX <= 8 ? SMAX : 1> acc;
-  acc.zero();
+  const uint64_t cm[3] = {s_cmask[0], s_cmask[1], s_cmask[2]};
+
+  if constexpr (SMALL) {
+    // Items in batches whose loads are issued together: keys, own successors
+    // and co-ranks (addresses known up front), then the sibling heads.
+    constexpr int BT = 32 / SMAX;
+    for (int jb = 0; jb < SW_ITEMS; jb += BT) {
+      uint64_t key[BT], nk[BT];
+      int32_t cr[BT][SMAX];
 #pragma unroll
-  for (int j = 0; j < SW_ITEMS; ++j) {
-    if (i0 + j >= n) break;
-    m ^= 1ull << (key[j] & smask);
-    const bool has_next = i0 + j + 1 < n;
-    const uint64_t nk = j + 1 < SW_ITEMS ? key[j + 1] : nextkey;
-    const int pid = (int)(key[j] >> pshift);
-    if (has_next && (int)(nk >> pshift) == pid) {
-      const int64_t len = (int64_t)((nk >> a.sb) & tmask) - (int64_t)((key[j] >> a.sb) & tmask);
-      if (SMAX <= 8 && pid == pid0)
-        acc.add(m, (uint64_t)len, cm);
-      else
-        add_interval(a, m, len, pid, pid0, cm, s_pair, s_cls);
-    }
-  }
-  if (SMAX <= 8) {
-    // wave sums, then one LDS add per wave
-    constexpr int NP = SweepAcc<SMAX <= 8 ? SMAX : 1>::NP;
+      for (int b = 0; b < BT; ++b) {
+        const int64_t i = base + (int64_t)(jb + b) * SW_THREADS + tid;
+        key[b] = i < n ? a.ev[i] : ~0ull;
+        nk[b] = i + 1 < n ? a.ev[i + 1] : ~0ull;
+        // the co-rank buffer exists only with two or more streams; the entry
+        // of the event's own stream is loaded (it lies inside the buffer)
+        // before the stream is known, and never used
 #pragma unroll
-    for (int k = 0; k < NP; ++k) {
-      const uint64_t w = wave_sum_u64(acc.pair[k]);
-      if (lane == 0 && w) atomicAdd(&s_pair[k], (unsigned long long)w);
-    }
-#pragma unroll
-    for (int c = 0; c < 3; ++c) {
-      const uint64_t w = wave_sum_u64(acc.cb[c]);
-      if (lane == 0 && w) atomicAdd(&s_cls[c], (unsigned long long)w);
-    }
-    const int co_idx[6] = {0, 1, 2, 4, 5, 8};
-#pragma unroll
-    for (int c = 0; c < 6; ++c) {
-      const uint64_t w = wave_sum_u64(acc.co[c]);
-      if (lane == 0 && w) atomicAdd(&s_cls[3 + co_idx[c]], (unsigned long long)w);
-    }
-    const uint64_t w = wave_sum_u64(acc.any);
-    if (lane == 0 && w) atomicAdd(&s_cls[12], (unsigned long long)w);
-  }
-  __syncthreads();
-  if (SMAX <= 8) {
-    // upper triangles back to full symmetric matrices
-    int k = 0;
-    for (int i = 0; i < SMAX && i < S; ++i)
-      for (int j = i; j < SMAX; ++j, ++k) {
-        if (j >= S || tid != 0) continue;
-        const unsigned long long v = s_pair[k];
-        if (!v) continue;
-        atomicAdd((unsigned long long*)&a.pair[((int64_t)pid0 * S + i) * S + j], v);
-        if (j != i) atomicAdd((unsigned long long*)&a.pair[((int64_t)pid0 * S + j) * S + i], v);
+        for (int s = 0; s < SMAX; ++s)
+          cr[b][s] = S > 1 && i < n && s < S ? a.corank[(int64_t)s * a.ev_cap + i] : 0;
       }
-    if (tid < 3 && s_cls[tid]) atomicAdd((unsigned long long*)&a.class_busy[pid0 * 3 + tid], s_cls[tid]);
-    if (tid >= 3 && tid < 12) {
-      const int c1 = (tid - 3) / 3, c2 = (tid - 3) % 3;
-      const unsigned long long v = c1 <= c2 ? s_cls[3 + c1 * 3 + c2] : s_cls[3 + c2 * 3 + c1];
-      if (v) atomicAdd((unsigned long long*)&a.class_overlap[pid0 * 9 + (tid - 3)], v);
+#pragma unroll
+      for (int b = 0; b < BT; ++b) {
+        const int64_t i = base + (int64_t)(jb + b) * SW_THREADS + tid;
+        if (i >= n) continue;
+        const int pid = (int)(key[b] >> pshift);
+        const int st = (int)(key[b] & smask);
+        int32_t off[SMAX + 1];
+#pragma unroll
+        for (int s = 0; s <= SMAX; ++s)
+          off[s] = s <= S ? (pid == pid0 ? s_off0[s] : a.seg_off[pid * S + s]) : 0;
+        int32_t own_L = 0, own_R = 0;
+#pragma unroll
+        for (int s = 0; s < SMAX; ++s)
+          if (s == st) {
+            own_L = off[s];
+            own_R = off[s + 1];
+          }
+        // its own stream is active after a start (even index in its group);
+        // a sibling iff an odd number of its events precede this one
+        uint64_t m = ((i - own_L) & 1) == 0 ? 1ull << st : 0ull;
+        uint64_t tn = i + 1 < own_R ? (nk[b] >> a.sb) & tmask : ~0ull;
+        uint64_t hv[SMAX];
+#pragma unroll
+        for (int s = 0; s < SMAX; ++s) {
+          const bool sib = s < S && s != st;
+          hv[s] = sib && (uint32_t)cr[b][s] < (uint32_t)(off[s + 1] - off[s]) ? a.ev[off[s] + cr[b][s]] : ~0ull;
+        }
+#pragma unroll
+        for (int s = 0; s < SMAX; ++s) {
+          if (s >= S || s == st) continue;
+          if (cr[b][s] & 1) m |= 1ull << s;
+          if (hv[s] != ~0ull) {
+            const uint64_t t2 = (hv[s] >> a.sb) & tmask;
+            tn = t2 < tn ? t2 : tn;
+          }
+        }
+        if (m == 0 || tn == ~0ull) continue;
+        const int64_t len = (int64_t)tn - (int64_t)((key[b] >> a.sb) & tmask);
+        if (len <= 0) continue;
+        if (pid == pid0)
+          atomicAdd(&s_mlen[m], (unsigned long long)len);
+        else
+          add_interval(a, m, len, pid, pid0, cm, s_pair, s_cls);
+      }
     }
-    if (tid == 12 && s_cls[12]) atomicAdd((unsigned long long*)&a.any_busy[pid0], s_cls[12]);
   } else {
+    for (int jt = 0; jt < SW_ITEMS; ++jt) {
+      const int64_t i = base + (int64_t)jt * SW_THREADS + tid;
+      if (i >= n) break;
+      const uint64_t key = a.ev[i];
+      const int pid = (int)(key >> pshift);
+      const int st = (int)(key & smask);
+      const int g = pid * S + st;
+      uint64_t m = 0, tn = ~0ull;
+      const int32_t own_L = a.seg_off[g], own_R = a.seg_off[g + 1];
+      // many streams: one plain binary search per sibling
+      for (int s = 0; s < S; ++s) {
+        if (s == st) continue;
+        const int32_t Lq = a.seg_off[pid * S + s], Rq = a.seg_off[pid * S + s + 1];
+        int32_t lo = Lq, len = Rq - Lq;
+        uint64_t nx = ~0ull;
+        while (len > 0) {
+          const int32_t half = len >> 1;
+          const uint64_t v = a.ev[lo + half];
+          if (v < key) {
+            lo += half + 1;
+            len -= half + 1;
+          } else {
+            nx = v;
+            len = half;
+          }
+        }
+        if ((lo - Lq) & 1) m |= 1ull << s;
+        if (lo < Rq) {
+          const uint64_t t2 = (nx >> a.sb) & tmask;
+          tn = t2 < tn ? t2 : tn;
+        }
+      }
+      // its own stream is active after a start (even index in its group)
+      if (((i - own_L) & 1) == 0) m |= 1ull << st;
+      if (i + 1 < own_R) {
+        const uint64_t t2 = (a.ev[i + 1] >> a.sb) & tmask;
+        tn = t2 < tn ? t2 : tn;
+      }
+      if (m == 0 || tn == ~0ull) continue;
+      const int64_t len = (int64_t)tn - (int64_t)((key >> a.sb) & tmask);
+      if (len <= 0) continue;
+      add_interval(a, m, len, pid, pid0, cm, s_pair, s_cls);
+    }
+  }
+  __syncthreads();
+  if (SMALL) {
+    // expand the per-mask sums: one thread per output entry
+    const int nm = 1 << S;
+    if (tid < S * S) {
+      const int i = tid / S, jj = tid % S;
+      const uint64_t need = (1ull << i) | (1ull << jj);
+      unsigned long long v = 0;
+      for (int mk = 1; mk < nm; ++mk)
+        if (((uint64_t)mk & need) == need) v += s_mlen[mk];
+      if (v) atomicAdd((unsigned long long*)&a.pair[((int64_t)pid0 * S + i) * S + jj], v);
+    } else if (tid >= 64 && tid < 64 + 13) {
+      const int e = tid - 64;  // 0..2 class busy, 3..11 class pairs, 12 any
+      unsigned long long v = 0;
+      for (int mk = 1; mk < nm; ++mk) {
+        const uint64_t mm = (uint64_t)mk;
+        bool hit;
+        if (e < 3)
+          hit = (mm & cm[e]) != 0;
+        else if (e < 12)
+          hit = (mm & cm[(e - 3) / 3]) != 0 && (mm & cm[(e - 3) % 3]) != 0;
+        else
+          hit = true;
+        if (hit) v += s_mlen[mk];
+      }
+      s_cls[e] = v;
+    }
+    __syncthreads();
+  }
+  if (!SMALL) {
     for (int i = tid; i < S * S; i += SW_THREADS)
       if (s_pair[i]) atomicAdd((unsigned long long*)&a.pair[(int64_t)pid0 * S * S + i], s_pair[i]);
-    if (tid < 3 && s_cls[tid]) atomicAdd((unsigned long long*)&a.class_busy[pid0 * 3 + tid], s_cls[tid]);
-    if (tid >= 3 && tid < 12 && s_cls[tid])
-      atomicAdd((unsigned long long*)&a.class_overlap[pid0 * 9 + (tid - 3)], s_cls[tid]);
-    if (tid == 12 && s_cls[12]) atomicAdd((unsigned long long*)&a.any_busy[pid0], s_cls[12]);
   }
+  if (tid < 3 && s_cls[tid]) atomicAdd((unsigned long long*)&a.class_busy[pid0 * 3 + tid], s_cls[tid]);
+  if (tid >= 3 && tid < 12 && s_cls[tid])
+    atomicAdd((unsigned long long*)&a.class_overlap[pid0 * 9 + (tid - 3)], s_cls[tid]);
+  if (tid == 12 && s_cls[12]) atomicAdd((unsigned long long*)&a.any_busy[pid0], s_cls[12]);
 }
 
 void launch_overlap(Ctx& c) {
   SweepArgs a;
-  a.k[0] = c.sE.k[0];
-  a.k[1] = c.sE.k[1];
+  a.ev = c.ev_keys;
+  a.seg_off = c.seg_off;
   a.cls = c.p.stream_class;
   a.P = c.P;
   a.S = c.S;
@@ -261,15 +390,19 @@ void launch_overlap(Ctx& c) {
   a.class_busy = c.o.class_busy;
   a.class_overlap = c.o.class_overlap;
   a.any_busy = c.o.any_busy;
-  a.status = c.sweep_status;
-  a.tiles_max = c.sweep_tiles;
-  launch_hist(c, c.sE, &c.ds->nEv);
-  launch_sort(c, c.sE, &c.ds->nEv);
-  const dim3 grid((unsigned)std::max<int64_t>(c.sweep_tiles, 1));
+  a.corank = c.corank;
+  a.ev_cap = c.ev_cap;
+  const int64_t nseg = (int64_t)c.P * c.S + 1;
+  hipLaunchKernelGGL(k_segoff, dim3((unsigned)std::min<int64_t>(cdiv(nseg, 256), 1024)), dim3(256), 0, c.st, a);
+  const dim3 grid((unsigned)std::max<int64_t>(cdiv(c.ev_cap, SW_TILE), 1));
+  if (c.S > 1 && c.S <= CR_SMAX) {
+    const int64_t steps = (int64_t)(c.S - 1) * c.ev_cap;
+    hipLaunchKernelGGL(k_corank, dim3((unsigned)std::max<int64_t>(cdiv(steps, 256 * CR_STEPS), 1)), dim3(256), 0, c.st, a);
+  }
   if (c.S <= 4)
     hipLaunchKernelGGL(k_sweep<4>, grid, dim3(SW_THREADS), 0, c.st, a);
-  else if (c.S <= 8)
-    hipLaunchKernelGGL(k_sweep<8>, grid, dim3(SW_THREADS), 0, c.st, a);
+  else if (c.S <= CR_SMAX)
+    hipLaunchKernelGGL(k_sweep<CR_SMAX>, grid, dim3(SW_THREADS), 0, c.st, a);
   else
     hipLaunchKernelGGL(k_sweep<64>, grid, dim3(SW_THREADS), 0, c.st, a);
 }

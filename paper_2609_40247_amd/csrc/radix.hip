@@ -52,7 +52,6 @@ __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, DevS
   __shared__ uint32_t h[8 * 256];
   __shared__ uint32_t s_scan[HIST_THREADS / WAVE + 1];
   __shared__ int s_last;
-  __shared__ int s_triv;
   for (int i = threadIdx.x; i < 8 * 256; i += HIST_THREADS) h[i] = 0;
   __syncthreads();
   const int64_t n = *jb.count;
@@ -83,7 +82,6 @@ __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, DevS
   __threadfence();
   __syncthreads();
   if (threadIdx.x == 0) s_last = atomicAdd(&ds->hist_done[jb.id], 1u) == gridDim.x - 1;
-  if (threadIdx.x == 0) s_triv = 0;
   __syncthreads();
   if (!s_last) return;
   __threadfence();
@@ -217,13 +215,14 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
           sv[i] = top - i >= 0 ? ld_agent(&status[(int64_t)(top - i) * 256 + dgt]) : RS_FLAG_P;
 #pragma unroll
         for (int i = 0; i < LB_WIN; ++i) {
-          if (state != 1) break;
           const uint32_t f = sv[i] >> 30;
-          if (f == 0) {
-            state = 0;
-          } else {
-            sum += sv[i] & RS_VAL;
-            if (f == 2) state = 2;
+          if (state == 1) {
+            if (f == 0) {
+              state = 0;
+            } else {
+              sum += sv[i] & RS_VAL;
+              if (f == 2) state = 2;
+            }
           }
         }
       }
@@ -238,14 +237,13 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
 #pragma unroll
         for (int sl = 0; sl < NSL; ++sl) {
           const int stt = s_lb_state[sl][dgt];
-          if (stt == 0) {
-            res = 0;
-            break;
-          }
-          add += s_lb_sum[sl][dgt];
-          if (stt == 2) {
-            res = 2;
-            break;
+          if (res == 1) {
+            if (stt == 0) {
+              res = 0;
+            } else {
+              add += s_lb_sum[sl][dgt];
+              if (stt == 2) res = 2;
+            }
           }
         }
         if (res == 0) {

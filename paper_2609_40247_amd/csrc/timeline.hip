@@ -37,7 +37,7 @@ struct UnionArgs {
   int64_t* gap_begin;
   int64_t* gap_end;
   uint8_t* gap_flags;
-  uint64_t* ev_keys;  // overlap events (sort input)
+  uint64_t* ev_keys;  // coverage run endpoints for the overlap stage
   int64_t ev_cap;
   uint64_t* status;   // [3][tiles_max]: segmax, gap count, event count
   int64_t tiles_max;
@@ -364,8 +364,8 @@ void launch_timeline(Ctx& c) {
   a.gap_begin = c.o.gap_begin;
   a.gap_end = c.o.gap_end;
   a.gap_flags = c.o.gap_flags;
-  a.ev_keys = c.sE.k[0];
-  a.ev_cap = c.sE.n_max;
+  a.ev_keys = c.ev_keys;
+  a.ev_cap = c.ev_cap;
   a.status = c.union_status;
   a.tiles_max = c.union_tiles;
   hipLaunchKernelGGL(k_union, dim3((unsigned)c.union_tiles), dim3(UN_THREADS), 0, c.st, a);
