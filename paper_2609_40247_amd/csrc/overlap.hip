@@ -107,43 +107,90 @@ __global__ __launch_bounds__(256) void k_segoff(SweepArgs a) {
 // Co-ranks by merge path.  For process p the pairs (s, s2), s < s2, of its
 // groups are laid end to end; the merge of pair (s, s2) has n_s + n_s2
 // steps, so p owns (S - 1) * n_p steps and the steps of all processes form
-// one index space in process order.  A thread takes CR_STEPS consecutive
-// steps: it finds its process by binary search, its pair by a walk over at
-// most 28 pairs and its position in the merge by the usual diagonal binary
-// search, then merges; each step emits the co-rank of the smaller head in
-// the other group (keys of different streams never tie).
-__global__ __launch_bounds__(256) void k_corank(SweepArgs a) {
-  const int64_t n = a.ds->nEv;
-  const int S = a.S, P = a.P;
-  const int64_t total = (int64_t)(S - 1) * n;
-  const int64_t d0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * CR_STEPS;
-  if (d0 >= total) return;
+// one index space in process order.  A workgroup takes CR_TILE consecutive
+// steps.  Inside one pair (the common case) it finds the merge positions of
+// its two ends with 64-ary wave searches, stages the two key ranges in LDS,
+// gives each thread CR_STEPS steps located by a binary search in LDS, and
+// writes both co-rank ranges coalesced.  A workgroup whose steps straddle
+// pairs lets every thread find its own position in global memory instead.
+// Each merge step emits the co-rank of the smaller head in the other group
+// (keys of different streams never tie).
+constexpr int CR_THREADS = 256;
+constexpr int CR_TILE = CR_THREADS * CR_STEPS;
+
+struct PairPos {
+  int p, s, s2;
+  int32_t LA, nA, LB, nB;
+  int64_t dl;  // steps into the pair's merge
+};
+
+// Pair and offset of global step d (d < (S - 1) * n).
+__device__ PairPos locate_step(const SweepArgs& a, int64_t d) {
   const int32_t* off = a.seg_off;
-  int lo = 0, hi = P - 1;  // the last process whose steps start at or before d0
+  const int S = a.S;
+  int lo = 0, hi = a.P - 1;  // the last process whose steps start at or before d
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if ((int64_t)(S - 1) * off[mid * S] <= d0)
+    if ((int64_t)(S - 1) * off[mid * S] <= d)
       lo = mid;
     else
       hi = mid - 1;
   }
-  int p = lo;
-  int64_t dl = d0 - (int64_t)(S - 1) * off[p * S];
-  int s = 0, s2 = 1;
-  int32_t LA = off[p * S], nA = off[p * S + 1] - LA;
-  int32_t LB = off[p * S + 1], nB = off[p * S + 2] - LB;
-  while (dl >= (int64_t)nA + nB) {  // pairs wholly before d0 (all in process p)
-    dl -= (int64_t)nA + nB;
-    if (++s2 == S) {
-      ++s;
-      s2 = s + 1;
+  PairPos q;
+  q.p = lo;
+  q.s = 0;
+  q.s2 = 1;
+  q.dl = d - (int64_t)(S - 1) * off[lo * S];
+  const int32_t* o = off + (int64_t)lo * S;
+  q.LA = o[0];
+  q.nA = o[1] - q.LA;
+  q.LB = o[1];
+  q.nB = o[2] - q.LB;
+  while (q.dl >= (int64_t)q.nA + q.nB) {  // pairs wholly before d (all in process p)
+    q.dl -= (int64_t)q.nA + q.nB;
+    if (++q.s2 == S) {
+      ++q.s;
+      q.s2 = q.s + 1;
     }
-    LA = off[p * S + s];
-    nA = off[p * S + s + 1] - LA;
-    LB = off[p * S + s2];
-    nB = off[p * S + s2 + 1] - LB;
+    q.LA = o[q.s];
+    q.nA = o[q.s + 1] - q.LA;
+    q.LB = o[q.s2];
+    q.nB = o[q.s2 + 1] - q.LB;
   }
-  // position on the diagonal: i heads of A among the first dl merged keys
+  return q;
+}
+
+// Number of A keys among the first d merged keys of A = ev[LA, LA + nA) and
+// B = ev[LB, LB + nB), by a 64-ary search of the diagonal: every lane probes
+// one point per round and a ballot keeps the stretch where the answer lies.
+// Called by a whole wave; every lane gets the answer.
+__device__ int32_t wave_diag_search(const uint64_t* __restrict__ ev, int32_t LA, int32_t nA, int32_t LB, int32_t nB,
+                                    int64_t d) {
+  const int lane = lane_id();
+  int32_t lo = (int32_t)max<int64_t>(0, d - nB), hi = (int32_t)min<int64_t>(d, nA);
+  while (lo < hi) {  // answer in [lo, hi]; A[i] < B[d-1-i] holds exactly for i < answer
+    const int32_t step = (hi - lo + WAVE - 1) / WAVE;
+    const int32_t x = lo + lane * step;
+    const bool probe = x < hi;
+    const bool f = probe && ev[LA + x] < ev[LB + (int32_t)(d - 1 - x)];
+    const uint64_t bf = ballot(f);
+    const int k = popc(bf);  // lanes 0..k-1 probed true (monotone)
+    const int32_t nlo = k > 0 ? lo + (k - 1) * step + 1 : lo;
+    const int32_t xk = lo + k * step;
+    hi = xk < hi ? xk : hi;
+    lo = nlo;
+  }
+  return lo;
+}
+
+// Generic path: the thread locates its own first step and merges.
+__device__ void corank_steps(const SweepArgs& a, int64_t d0, int64_t steps) {
+  const int S = a.S;
+  const int32_t* off = a.seg_off;
+  PairPos q = locate_step(a, d0);
+  int p = q.p, s = q.s, s2 = q.s2;
+  int32_t LA = q.LA, nA = q.nA, LB = q.LB, nB = q.nB;
+  const int64_t dl = q.dl;
   int32_t ilo = (int32_t)max<int64_t>(0, dl - nB), ihi = (int32_t)min<int64_t>(dl, nA);
   while (ilo < ihi) {
     const int32_t mid = (ilo + ihi) >> 1;
@@ -155,7 +202,6 @@ __global__ __launch_bounds__(256) void k_corank(SweepArgs a) {
   int32_t i = ilo, j = (int32_t)dl - ilo;
   uint64_t va = i < nA ? a.ev[LA + i] : ~0ull;
   uint64_t vb = j < nB ? a.ev[LB + j] : ~0ull;
-  int64_t steps = min<int64_t>(CR_STEPS, total - d0);
   while (steps > 0) {
     if (i == nA && j == nB) {  // next pair, or the first pair of the next process
       if (++s2 == S) {
@@ -187,6 +233,69 @@ __global__ __launch_bounds__(256) void k_corank(SweepArgs a) {
     }
     --steps;
   }
+}
+
+__global__ __launch_bounds__(CR_THREADS) void k_corank(SweepArgs a) {
+  __shared__ uint64_t s_key[CR_TILE];  // A range, then B range
+  __shared__ int32_t s_out[CR_TILE];   // co-ranks in the same layout
+  __shared__ int32_t s_split[2];
+  const int tid = threadIdx.x, wv = tid / WAVE;
+  const int64_t n = a.ds->nEv;
+  const int S = a.S;
+  const int64_t total = (int64_t)(S - 1) * n;
+  const int64_t D0 = (int64_t)blockIdx.x * CR_TILE;
+  if (D0 >= total) return;
+  const int64_t cnt = min<int64_t>(CR_TILE, total - D0);
+  const PairPos q0 = locate_step(a, D0);
+  const bool one_pair = q0.dl + cnt <= (int64_t)q0.nA + q0.nB;
+  if (!one_pair) {
+    const int64_t d0 = D0 + (int64_t)tid * CR_STEPS;
+    if (d0 < total) corank_steps(a, d0, min<int64_t>(CR_STEPS, total - d0));
+    return;
+  }
+  // merge positions of the tile's two ends
+  if (wv < 2) {
+    const int64_t d = q0.dl + (wv == 0 ? 0 : cnt);
+    const int32_t i = wave_diag_search(a.ev, q0.LA, q0.nA, q0.LB, q0.nB, d);
+    if (lane_id() == 0) s_split[wv] = i;
+  }
+  __syncthreads();
+  const int32_t i0 = s_split[0], i1 = s_split[1];
+  const int32_t j0 = (int32_t)q0.dl - i0, j1 = (int32_t)(q0.dl + cnt) - i1;
+  const int32_t na = i1 - i0, nb = j1 - j0;  // na + nb == cnt
+  for (int x = tid; x < na; x += CR_THREADS) s_key[x] = a.ev[q0.LA + i0 + x];
+  for (int y = tid; y < nb; y += CR_THREADS) s_key[na + y] = a.ev[q0.LB + j0 + y];
+  __syncthreads();
+  const uint64_t* A = s_key;
+  const uint64_t* B = s_key + na;
+  const int32_t dd = tid * CR_STEPS;
+  if (dd < cnt) {
+    int32_t lo = max(0, dd - nb), hi = min(dd, na);
+    while (lo < hi) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (A[mid] < B[dd - 1 - mid])
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    int32_t i = lo, j = dd - lo;
+    const int32_t steps = min<int32_t>(CR_STEPS, (int32_t)cnt - dd);
+    for (int k = 0; k < steps; ++k) {
+      const bool takeA = j >= nb || (i < na && A[i] < B[j]);
+      if (takeA) {
+        s_out[i] = j0 + j;
+        ++i;
+      } else {
+        s_out[na + j] = i0 + i;
+        ++j;
+      }
+    }
+  }
+  __syncthreads();
+  int32_t* outA = a.corank + (int64_t)q0.s2 * a.ev_cap + q0.LA + i0;
+  int32_t* outB = a.corank + (int64_t)q0.s * a.ev_cap + q0.LB + j0;
+  for (int x = tid; x < na; x += CR_THREADS) outA[x] = s_out[x];
+  for (int y = tid; y < nb; y += CR_THREADS) outB[y] = s_out[na + y];
 }
 
 // One event per thread and item (items striped over the workgroup).  With
@@ -397,7 +506,8 @@ void launch_overlap(Ctx& c) {
   const dim3 grid((unsigned)std::max<int64_t>(cdiv(c.ev_cap, SW_TILE), 1));
   if (c.S > 1 && c.S <= CR_SMAX) {
     const int64_t steps = (int64_t)(c.S - 1) * c.ev_cap;
-    hipLaunchKernelGGL(k_corank, dim3((unsigned)std::max<int64_t>(cdiv(steps, 256 * CR_STEPS), 1)), dim3(256), 0, c.st, a);
+    hipLaunchKernelGGL(k_corank, dim3((unsigned)std::max<int64_t>(cdiv(steps, CR_TILE), 1)), dim3(CR_THREADS), 0, c.st,
+                       a);
   }
   if (c.S <= 4)
     hipLaunchKernelGGL(k_sweep<4>, grid, dim3(SW_THREADS), 0, c.st, a);
