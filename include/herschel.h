@@ -186,19 +186,17 @@ const char *herschel_strerror(int code);
 enum {
   HERSCHEL_STAGE_INIT = 0,     /* clear the workspace state and accumulating outputs */
   HERSCHEL_STAGE_PREP = 1,     /* validate, correct, admit, compact (one kernel) */
-  HERSCHEL_STAGE_HIST = 2,     /* digit histograms of the three sort inputs */
+  HERSCHEL_STAGE_HIST = 2,     /* digit histograms and pass plans of the sorts */
   HERSCHEL_STAGE_NAMES = 3,    /* per-name partial tables */
-  HERSCHEL_STAGE_SORT_TIMELINE = 4,
+  HERSCHEL_STAGE_SORT = 4,     /* radix passes of the timeline, join and containment sorts */
   HERSCHEL_STAGE_TIMELINE = 5, /* busy/idle, gaps, coverage runs (one kernel) */
-  HERSCHEL_STAGE_OVERLAP = 6,  /* event sort and sweep */
-  HERSCHEL_STAGE_SORT_CONTAIN = 7,
-  HERSCHEL_STAGE_CONTAIN = 8,  /* op nesting and launch -> op */
-  HERSCHEL_STAGE_SORT_JOIN = 9,
-  HERSCHEL_STAGE_JOIN = 10,    /* launch <-> kernel join, latency (one kernel) */
-  HERSCHEL_STAGE_OPAGG = 11,   /* inclusive per-op aggregates (one kernel) */
-  HERSCHEL_STAGE_EDGES = 12,
-  HERSCHEL_STAGE_FINAL = 13,
-  HERSCHEL_N_STAGES = 14
+  HERSCHEL_STAGE_OVERLAP = 6,  /* co-ranks of the coverage runs and the sweep */
+  HERSCHEL_STAGE_CONTAIN = 7,  /* op nesting and launch -> op */
+  HERSCHEL_STAGE_JOIN = 8,     /* launch <-> kernel join, latency (one kernel) */
+  HERSCHEL_STAGE_OPAGG = 9,    /* inclusive per-op aggregates (one kernel) */
+  HERSCHEL_STAGE_EDGES = 10,
+  HERSCHEL_STAGE_FINAL = 11,
+  HERSCHEL_N_STAGES = 12
 };
 
 /* Record start_event / stop_event (hipEvent_t, created by the caller) on

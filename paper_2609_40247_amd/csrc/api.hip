@@ -306,9 +306,13 @@ static int enqueue(Ctx& c) {
   stage_begin(c, HERSCHEL_STAGE_NAMES);
   launch_names(c);
   stage_end(c, HERSCHEL_STAGE_NAMES);
-  stage_begin(c, HERSCHEL_STAGE_SORT_TIMELINE);
-  launch_sort(c, c.sK, &c.ds->nK);
-  stage_end(c, HERSCHEL_STAGE_SORT_TIMELINE);
+  stage_begin(c, HERSCHEL_STAGE_SORT);
+  {
+    SortBufs* ss[3] = {&c.sK, &c.sJ, &c.sC};
+    const int32_t* cc[3] = {&c.ds->nK, &c.ds->nJ, &c.ds->nCL};
+    launch_sort_multi(c, ss, cc, c.contain ? 3 : 2);
+  }
+  stage_end(c, HERSCHEL_STAGE_SORT);
   stage_begin(c, HERSCHEL_STAGE_TIMELINE);
   launch_timeline(c);
   stage_end(c, HERSCHEL_STAGE_TIMELINE);
@@ -316,9 +320,6 @@ static int enqueue(Ctx& c) {
   if (c.overlap) launch_overlap(c);
   stage_end(c, HERSCHEL_STAGE_OVERLAP);
   if (c.contain) {
-    stage_begin(c, HERSCHEL_STAGE_SORT_CONTAIN);
-    launch_sort(c, c.sC, &c.ds->nCL);
-    stage_end(c, HERSCHEL_STAGE_SORT_CONTAIN);
     stage_begin(c, HERSCHEL_STAGE_CONTAIN);
     launch_contain(c);
     stage_end(c, HERSCHEL_STAGE_CONTAIN);
@@ -326,9 +327,6 @@ static int enqueue(Ctx& c) {
     const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.n, 256 * 8), 1), 2048);
     hipLaunchKernelGGL(k_nocontain, dim3(grid), dim3(256), 0, c.st, c.sC.k[0], c.sC.v[0], c.ds, c.o.link, c.o.aux);
   }
-  stage_begin(c, HERSCHEL_STAGE_SORT_JOIN);
-  launch_sort(c, c.sJ, &c.ds->nJ);
-  stage_end(c, HERSCHEL_STAGE_SORT_JOIN);
   stage_begin(c, HERSCHEL_STAGE_JOIN);
   launch_join(c);
   stage_end(c, HERSCHEL_STAGE_JOIN);

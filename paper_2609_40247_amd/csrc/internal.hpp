@@ -7,12 +7,12 @@
 
 namespace hx {
 
-// One LSD radix sort: 64-bit keys with optional 32-bit payload, ping-pong
+// One LSD radix sort: 64-bit keys with a 32-bit payload, ping-pong
 // buffers, digit histograms in DevState::hist[id], result buffer index in
 // DevState::sort_parity[id].
 struct SortBufs {
   uint64_t* k[2] = {nullptr, nullptr};
-  uint32_t* v[2] = {nullptr, nullptr};  // both null for keys-only sorts
+  uint32_t* v[2] = {nullptr, nullptr};
   uint32_t* status = nullptr;           // [8 passes][tiles_max * 256]
   int64_t n_max = 0;                    // capacity (host upper bound of the count)
   int64_t tiles_max = 0;
@@ -73,7 +73,7 @@ void launch_init(Ctx& c);
 void launch_prep(Ctx& c);
 void launch_hist(Ctx& c, SortBufs& s, const int32_t* count);
 void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k);
-void launch_sort(Ctx& c, SortBufs& s, const int32_t* count);
+void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k);
 void launch_names(Ctx& c);
 void launch_timeline(Ctx& c);
 void launch_overlap(Ctx& c);

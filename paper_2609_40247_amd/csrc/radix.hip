@@ -1,6 +1,6 @@
 // LSD radix sort of 64-bit keys (optionally with a 32-bit payload) for CDNA4.
 //
-// One launch per 8-bit digit.  Each workgroup ranks a tile of 8192 keys with
+// One launch per 8-bit digit, shared by the independent sorts of a call.  Each workgroup ranks a tile of 8192 keys with
 // wave64 ballots (a 64-lane match of the digit built from 8 ballots gives the
 // rank among equal digits in one step), publishes its 256 per-digit counts
 // through a decoupled look-back (one chain per digit, four lanes per digit),
@@ -100,14 +100,24 @@ __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, DevS
   }
 }
 
-template <bool VALS>
-__global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_t* k1, uint32_t* v0, uint32_t* v1,
-                                                           const int32_t* count, DevState* ds, int id, int d,
-                                                           uint32_t* status) {
+struct SortJob {
+  uint64_t* k[2];
+  uint32_t* v[2];
+  const int32_t* count;
+  uint32_t* status;  // [nd][tiles_max * 256]
+  int64_t tiles_max;
+  int nd, id;
+};
+struct SortJobs {
+  SortJob j[N_SORTS];
+};
+
+// One digit pass of up to N_SORTS independent sorts (blockIdx.y picks one).
+__global__ __launch_bounds__(RS_THREADS) void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   constexpr int NW = RS_THREADS / WAVE;     // waves per workgroup
   constexpr int NSL = RS_THREADS / 256;     // look-back slices per digit
   __shared__ uint64_t s_key[RS_TILE];
-  __shared__ uint32_t s_val[VALS ? RS_TILE : 1];
+  __shared__ uint32_t s_val[RS_TILE];
   __shared__ uint32_t s_wh[NW][256];
   __shared__ uint32_t s_local[256];
   __shared__ uint32_t s_glob[256];
@@ -116,6 +126,9 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
   __shared__ uint8_t s_lb_state[NSL][256];
   __shared__ int s_tile;
 
+  const SortJob& jb = jobs.j[blockIdx.y];
+  if (d >= jb.nd) return;
+  const int id = jb.id;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int dgt = tid & 255, slice = tid >> 8;
   // The plan (trivial digits, offsets) was made by the histogram kernel.  A
@@ -124,7 +137,7 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
   // tile to sort leave before the ticket: the ticket counter is one address,
   // and every request to it is served in turn.  The first cdiv(n, tile)
   // workgroups stay, so they draw exactly the tickets of the real tiles.
-  const uint32_t n = (uint32_t)*count;
+  const uint32_t n = (uint32_t)*jb.count;
   const uint32_t triv = ds->sort_trivial[id];
   const uint32_t gexcl = ds->hist[id][d][dgt];
   if (((triv >> d) & 1) || (int64_t)blockIdx.x * RS_TILE >= (int64_t)n) return;
@@ -132,10 +145,11 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
   for (int i = tid; i < NW * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
   __syncthreads();
   const int parity = popc(~triv & ((1u << d) - 1u)) & 1;
-  const uint64_t* kin = parity ? k1 : k0;
-  uint64_t* kout = parity ? k0 : k1;
-  const uint32_t* vin = parity ? v1 : v0;
-  uint32_t* vout = parity ? v0 : v1;
+  const uint64_t* kin = jb.k[parity];
+  uint64_t* kout = jb.k[parity ^ 1];
+  const uint32_t* vin = jb.v[parity];
+  uint32_t* vout = jb.v[parity ^ 1];
+  uint32_t* status = jb.status + (int64_t)d * jb.tiles_max * 256;
   const int tile = s_tile;
   const int64_t base = (int64_t)tile * RS_TILE;
 
@@ -151,7 +165,7 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
     const int64_t idx = wbase + j * WAVE + lane;
     const bool ok = idx < (int64_t)n;
     key[j] = ok ? kin[idx] : 0ull;
-    if (VALS) val[j] = ok ? vin[idx] : 0u;
+    val[j] = ok ? vin[idx] : 0u;
   }
 #pragma unroll
   for (int j = 0; j < RS_ITEMS; ++j) {
@@ -273,7 +287,7 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
       const uint32_t pos = s_local[dig[j]] + s_wh[wv][dig[j]] + rank[j];
       if (in_range(ds, pos, RS_TILE)) {
         s_key[pos] = key[j];
-        if (VALS) s_val[pos] = val[j];
+        s_val[pos] = val[j];
       }
     }
   }
@@ -286,7 +300,7 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(uint64_t* k0, uint64_
     const uint32_t gpos = s_glob[dg] + (i - s_local[dg]);
     if (in_range(ds, gpos, n)) {
       kout[gpos] = kk;
-      if (VALS) vout[gpos] = s_val[i];
+      vout[gpos] = s_val[i];
     }
   }
 }
@@ -311,17 +325,18 @@ void launch_hist(Ctx& c, SortBufs& s, const int32_t* count) {
   launch_hist_multi(c, ss, cc, 1);
 }
 
-void launch_sort(Ctx& c, SortBufs& s, const int32_t* count) {
-  const int64_t grid = std::max<int64_t>(s.tiles_max, 1);
-  for (int d = 0; d < s.nd; ++d) {
-    uint32_t* status = s.status + (int64_t)d * s.tiles_max * 256;
-    if (s.v[0])
-      hipLaunchKernelGGL(k_radix_pass<true>, dim3((unsigned)grid), dim3(RS_THREADS), 0, c.st, s.k[0], s.k[1],
-                         s.v[0], s.v[1], count, c.ds, s.id, d, status);
-    else
-      hipLaunchKernelGGL(k_radix_pass<false>, dim3((unsigned)grid), dim3(RS_THREADS), 0, c.st, s.k[0], s.k[1],
-                         s.v[0], s.v[1], count, c.ds, s.id, d, status);
+void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k) {
+  SortJobs jobs{};
+  int64_t grid = 1;
+  int nd = 0;
+  for (int i = 0; i < k; ++i) {
+    jobs.j[i] = SortJob{{s[i]->k[0], s[i]->k[1]}, {s[i]->v[0], s[i]->v[1]}, count[i], s[i]->status,
+                        s[i]->tiles_max, s[i]->nd, s[i]->id};
+    grid = std::max<int64_t>(grid, s[i]->tiles_max);
+    nd = std::max(nd, s[i]->nd);
   }
+  for (int d = 0; d < nd; ++d)
+    hipLaunchKernelGGL(k_radix_pass, dim3((unsigned)grid, (unsigned)k), dim3(RS_THREADS), 0, c.st, jobs, c.ds, d);
 }
 
 }  // namespace hx

@@ -120,8 +120,8 @@ def herschel_trace_analyze_batch(events: HerschelEvents, offsets: np.ndarray, pa
                                                 T, parr, oarr))
 
 
-STAGES = ("init", "prep", "hist", "names", "sort_timeline", "timeline", "overlap", "sort_contain", "contain",
-          "sort_join", "join", "opagg", "edges", "final")
+STAGES = ("init", "prep", "hist", "names", "sort", "timeline", "overlap", "contain", "join", "opagg", "edges",
+          "final")
 
 
 def herschel_time_stage(stage: int, start_event, stop_event, lib=None) -> int:
