@@ -62,6 +62,7 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.sC.status = b.take<uint32_t>((int64_t)c.sC.nd * c.sC.tiles_max * 256);
   }
   c.zero_bytes = align_up(b.off - z0);
+  c.hist_part = b.take<uint32_t>((int64_t)N_SORTS * HIST_MAX_BLOCKS * 8 * 256);
   // sort buffers
   for (SortBufs* s : {&c.sK, &c.sJ, &c.sC}) {
     if (s == &c.sC && !c.contain) {

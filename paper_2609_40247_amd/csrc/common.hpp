@@ -54,7 +54,6 @@ struct DevState {
   int32_t pad0;
   int64_t first_invalid;  // smallest bad row (INT64_MAX = none)
   int64_t n_gaps;
-  uint32_t hist_done[N_SORTS];     // workgroups of the histogram kernel that finished
   uint32_t sort_trivial[N_SORTS];  // bit d: every key has the same digit d (pass skipped)
   // radix digit histograms; the last histogram workgroup turns each into the
   // exclusive prefix over digit values (the global offset of every bin)

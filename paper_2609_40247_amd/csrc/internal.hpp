@@ -43,6 +43,7 @@ struct Ctx {
   int64_t vb_tiles = 0;
   int64_t* corr_min = nullptr;       // [P]
   SortBufs sK, sJ, sC;               // timeline, join, containment
+  uint32_t* hist_part = nullptr;     // [N_SORTS][HIST_MAX_BLOCKS][8 * 256] per-workgroup digit counts
   uint64_t* ev_keys = nullptr;       // [ev_cap] coverage run endpoints, grouped by (pid, stream)
   int64_t ev_cap = 0;
   int32_t* seg_off = nullptr;        // [P * S + 1] first endpoint of each (pid, stream)
@@ -71,7 +72,6 @@ size_t layout_workspace(Ctx& c, char* base);
 
 void launch_init(Ctx& c);
 void launch_prep(Ctx& c);
-void launch_hist(Ctx& c, SortBufs& s, const int32_t* count);
 void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k);
 void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k);
 void launch_names(Ctx& c);
@@ -87,6 +87,10 @@ void launch_finalize(Ctx& c);
 int64_t prep_tile_rows();
 int64_t union_tile_elems();
 void names_set_lds_attr();
+
+// digit histograms: keys per workgroup (at least), most workgroups per sort
+constexpr int HIST_CHUNK = 32768;
+constexpr int HIST_MAX_BLOCKS = 64;
 
 constexpr int RS_THREADS = 1024;
 constexpr int RS_ITEMS = 8;

@@ -24,80 +24,115 @@ struct HistJob {
   int id;
 };
 struct HistJobs {
-  HistJob j[4];
+  HistJob j[N_SORTS];
+  uint32_t* part;  // [N_SORTS][HIST_MAX_BLOCKS][8 * 256] per-workgroup counts
 };
 
 // Digit histograms of several sort inputs in one launch (blockIdx.y picks
-// the sort).  Few, wide workgroups keep the number of global atomics on the
-// 256 * nd counters low.
-constexpr int HIST_THREADS = 512;
+// the sort).  Each workgroup counts a contiguous share of the keys in LDS
+// and stores its table; the plan kernel that follows sums the tables.  No
+// global atomics and no fences: counters shared by many workgroups serialise
+// on their cache line, and a device-scope fence writes back the whole L2.
+constexpr int HIST_THREADS = 1024;
 
-__device__ __forceinline__ void hist_add(uint32_t* h, uint64_t k, int nd, uint64_t active, int first, int lane) {
-  for (int d = 0; d < nd; ++d) {
-    const int dg = (int)((k >> (8 * d)) & 255);
-    const int d0 = __shfl(dg, first, WAVE);
-    if (ballot(dg != d0) == 0) {
-      if (lane == first) atomicAdd(&h[d * 256 + d0], (uint32_t)popc(active));
-    } else {
+// Adds one key's ND digits to the LDS table.  Digits 0 and 1 of these keys
+// (nanoseconds, correlation ids) differ across a wave, so every lane adds;
+// for higher digits, when the whole wave agrees, one lane adds the count.
+template <int ND>
+__device__ __forceinline__ void hist_add(uint32_t* h, uint64_t k, uint32_t nact, bool leader) {
+  const uint32_t lo = (uint32_t)k, hi = (uint32_t)(k >> 32);
+#pragma unroll
+  for (int d = 0; d < ND; ++d) {
+    const uint32_t dg = ((d < 4 ? lo : hi) >> (8 * (d & 3))) & 255u;
+    if (d < 2) {
       atomicAdd(&h[d * 256 + dg], 1u);
+    } else {
+      const uint32_t d0 = __builtin_amdgcn_readfirstlane(dg);
+      if (ballot(dg != d0) == 0) {
+        if (leader) atomicAdd(&h[d * 256 + d0], nact);
+      } else {
+        atomicAdd(&h[d * 256 + dg], 1u);
+      }
     }
   }
 }
 
-__global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, DevState* ds) {
-  const HistJob jb = jobs.j[blockIdx.y];
-  const uint64_t* __restrict__ keys = jb.keys;
-  const int nd = jb.nd;
-  uint32_t* __restrict__ hist = &ds->hist[jb.id][0][0];
-  __shared__ uint32_t h[8 * 256];
-  __shared__ uint32_t s_scan[HIST_THREADS / WAVE + 1];
-  __shared__ int s_last;
-  for (int i = threadIdx.x; i < 8 * 256; i += HIST_THREADS) h[i] = 0;
-  __syncthreads();
-  const int64_t n = *jb.count;
+template <int ND>
+__device__ void hist_range(uint32_t* h, const uint64_t* __restrict__ keys, int64_t lo, int64_t hi) {
   const int lane = lane_id();
-  // eight independent loads in flight per thread
-  constexpr int U = 8;
-  const int64_t stride = (int64_t)gridDim.x * HIST_THREADS;
-  int64_t i = (int64_t)blockIdx.x * HIST_THREADS + threadIdx.x;
-  for (; i + (U - 1) * stride < n; i += U * stride) {
+  constexpr int U = 8;  // loads in flight per thread
+  int64_t i = lo + threadIdx.x;
+  for (; i + (U - 1) * HIST_THREADS < hi; i += U * HIST_THREADS) {
     uint64_t k[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) k[u] = keys[i + u * stride];
+    for (int u = 0; u < U; ++u) k[u] = keys[i + u * HIST_THREADS];
     const uint64_t active = ballot(true);
-    const int first = __ffsll((unsigned long long)active) - 1;
+    const bool leader = lane == __ffsll((unsigned long long)active) - 1;
+    const uint32_t nact = (uint32_t)popc(active);
 #pragma unroll
-    for (int u = 0; u < U; ++u) hist_add(h, k[u], nd, active, first, lane);
+    for (int u = 0; u < U; ++u) hist_add<ND>(h, k[u], nact, leader);
   }
-  for (; i < n; i += stride) {
+  for (; i < hi; i += HIST_THREADS) {
     const uint64_t k = keys[i];
     const uint64_t active = ballot(true);
-    const int first = __ffsll((unsigned long long)active) - 1;
-    hist_add(h, k, nd, active, first, lane);
+    const bool leader = lane == __ffsll((unsigned long long)active) - 1;
+    hist_add<ND>(h, k, (uint32_t)popc(active), leader);
+  }
+}
+
+__device__ __forceinline__ int hist_blocks(int64_t n) {
+  return (int)min<int64_t>(max<int64_t>(cdiv(n, HIST_CHUNK), 1), HIST_MAX_BLOCKS);
+}
+
+__global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs) {
+  const HistJob jb = jobs.j[blockIdx.y];
+  const int nd = jb.nd, nbins = nd * 256;
+  __shared__ uint32_t h[8 * 256];
+  const int64_t n = *jb.count;
+  const int nblk = hist_blocks(n);
+  const int blk = blockIdx.x;
+  if (blk >= nblk) return;
+  for (int i = threadIdx.x; i < 8 * 256; i += HIST_THREADS) h[i] = 0;
+  __syncthreads();
+  const int64_t per = cdiv(n, nblk);
+  const int64_t lo = min<int64_t>(n, (int64_t)blk * per), hi = min<int64_t>(n, lo + per);
+  switch (nd) {
+    case 1: hist_range<1>(h, jb.keys, lo, hi); break;
+    case 2: hist_range<2>(h, jb.keys, lo, hi); break;
+    case 3: hist_range<3>(h, jb.keys, lo, hi); break;
+    case 4: hist_range<4>(h, jb.keys, lo, hi); break;
+    case 5: hist_range<5>(h, jb.keys, lo, hi); break;
+    case 6: hist_range<6>(h, jb.keys, lo, hi); break;
+    case 7: hist_range<7>(h, jb.keys, lo, hi); break;
+    default: hist_range<8>(h, jb.keys, lo, hi); break;
   }
   __syncthreads();
-  for (int j = threadIdx.x; j < nd * 256; j += HIST_THREADS)
-    if (h[j]) atomicAdd(&hist[j], h[j]);
-  // the last workgroup of this sort turns the counts into offsets
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = atomicAdd(&ds->hist_done[jb.id], 1u) == gridDim.x - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  uint32_t triv = 0;
-  for (int d = 0; d < nd; ++d) {
-    const uint32_t c = threadIdx.x < 256 ? ld_agent(&hist[d * 256 + threadIdx.x]) : 0u;
-    const int full = __syncthreads_or(threadIdx.x < 256 && c == (uint32_t)n);
-    if (full) triv |= 1u << d;
-    const uint32_t ex = block_excl_sum<HIST_THREADS>(c, s_scan, nullptr);
-    if (threadIdx.x < 256) hist[d * 256 + threadIdx.x] = ex;
+  uint32_t* part = jobs.part + ((int64_t)jb.id * HIST_MAX_BLOCKS + blk) * 8 * 256;
+  for (int j = threadIdx.x; j < nbins; j += HIST_THREADS) part[j] = h[j];
+}
+
+// Plan of one digit of one sort (blockIdx.x = digit, blockIdx.y = sort):
+// the digit's counts summed over the workgroup tables, its trivial flag
+// (one bin holds every key) and each bin's exclusive offset.
+__global__ __launch_bounds__(256) void k_hist_plan(HistJobs jobs, DevState* ds) {
+  __shared__ uint32_t s_scan[256 / WAVE + 1];
+  const HistJob jb = jobs.j[blockIdx.y];
+  const int d = blockIdx.x;
+  if (d >= jb.nd) return;
+  const int64_t n = *jb.count;
+  const int nblk = hist_blocks(n);
+  const uint32_t* src = jobs.part + (int64_t)jb.id * HIST_MAX_BLOCKS * 8 * 256 + d * 256 + threadIdx.x;
+  uint32_t c = 0;
+  for (int b0 = 0; b0 < nblk; b0 += 16) {
+    uint32_t v[16];
+#pragma unroll
+    for (int b = 0; b < 16; ++b) v[b] = b0 + b < nblk ? src[(int64_t)(b0 + b) * 8 * 256] : 0u;
+#pragma unroll
+    for (int b = 0; b < 16; ++b) c += v[b];
   }
-  if (threadIdx.x == 0) {
-    ds->sort_trivial[jb.id] = triv;
-    const uint32_t ran = ~triv & ((nd >= 32 ? 0u : (1u << nd)) - 1u);
-    ds->sort_parity[jb.id] = (uint32_t)(popc(ran) & 1);
-  }
+  if (__syncthreads_or(c == (uint32_t)n) && threadIdx.x == 0) atomicOr(&ds->sort_trivial[jb.id], 1u << d);
+  const uint32_t ex = block_excl_sum<256>(c, s_scan, nullptr);
+  ds->hist[jb.id][d][threadIdx.x] = ex;
 }
 
 struct SortJob {
@@ -140,6 +175,9 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(SortJobs jobs, DevSta
   const uint32_t n = (uint32_t)*jb.count;
   const uint32_t triv = ds->sort_trivial[id];
   const uint32_t gexcl = ds->hist[id][d][dgt];
+  // which buffer holds the result: parity of the digits that move data
+  if (d == 0 && blockIdx.x == 0 && tid == 0)
+    ds->sort_parity[id] = (uint32_t)(popc(~triv & ((jb.nd >= 32 ? 0u : 1u << jb.nd) - 1u)) & 1);
   if (((triv >> d) & 1) || (int64_t)blockIdx.x * RS_TILE >= (int64_t)n) return;
   if (tid == 0) s_tile = (int)atomicAdd(&ds->ticket[TK_RADIX + 8 * id + d], 1u);
   for (int i = tid; i < NW * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
@@ -307,22 +345,19 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(SortJobs jobs, DevSta
 
 void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k) {
   HistJobs jobs{};
-  int m = 0;
+  jobs.part = c.hist_part;
+  int m = 0, nd = 0;
   int64_t n_max = 1;
   for (int i = 0; i < k; ++i) {
     if (s[i]->nd == 0) continue;
     jobs.j[m++] = HistJob{s[i]->k[0], count[i], s[i]->nd, s[i]->id};
     n_max = std::max<int64_t>(n_max, s[i]->n_max);
+    nd = std::max(nd, s[i]->nd);
   }
   if (m == 0) return;
-  const int64_t grid = std::min<int64_t>(std::max<int64_t>(cdiv(n_max, 32768), 1), 64);
-  hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid, (unsigned)m), dim3(HIST_THREADS), 0, c.st, jobs, c.ds);
-}
-
-void launch_hist(Ctx& c, SortBufs& s, const int32_t* count) {
-  SortBufs* ss[1] = {&s};
-  const int32_t* cc[1] = {count};
-  launch_hist_multi(c, ss, cc, 1);
+  const int64_t grid = std::min<int64_t>(cdiv(n_max, HIST_CHUNK), HIST_MAX_BLOCKS);
+  hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid, (unsigned)m), dim3(HIST_THREADS), 0, c.st, jobs);
+  hipLaunchKernelGGL(k_hist_plan, dim3((unsigned)nd, (unsigned)m), dim3(256), 0, c.st, jobs, c.ds);
 }
 
 void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k) {
