@@ -290,11 +290,19 @@ __device__ __forceinline__ int wave_lift(const uint64_t (&w)[6], int pos, uint64
   return pos;
 }
 
-__global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
+// One workgroup per 4096-position tile, 16 waves: a wave answers four
+// 64-position groups, one lane per position.  Keys, rows and values of the
+// tile are loaded up front; inside the tile every step reads LDS.
+constexpr int QY_THREADS = 1024;
+constexpr int QY_GROUPS = CT_TILE / 64;                  // 64 groups per tile
+constexpr int QY_ROUNDS = QY_GROUPS / (QY_THREADS / WAVE);  // groups per wave
+
+__global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
   __shared__ uint64_t s_v[CT_TILE];
-  __shared__ uint64_t s_m1[CT_TILE / 64];
-  __shared__ uint64_t s_g[6][CT_TILE / 64];  // window maxima over the tile's groups
-  __shared__ uint64_t s_gpre[CT_TILE / 64];  // max over the tile's earlier groups and all earlier tiles
+  __shared__ uint32_t s_val[CT_TILE];
+  __shared__ uint64_t s_sub[CT_TILE / 8];   // maxima of 8-position blocks
+  __shared__ uint64_t s_g[6][QY_GROUPS];    // window maxima over the tile's groups
+  __shared__ uint64_t s_gpre[QY_GROUPS];    // max over the tile's earlier groups and all earlier tiles
   __shared__ uint16_t s_esc[CT_TILE];
   __shared__ int s_nesc;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
@@ -307,12 +315,29 @@ __global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
   if (base >= n) return;
   const int64_t tn = min((int64_t)CT_TILE, n - base);
   const int ng = (int)cdiv(tn, 64);
-  for (int64_t i = tid; i < tn; i += CT_THREADS) s_v[i] = a.V[base + i];
-  if (tid < CT_TILE / 64) s_m1[tid] = tid < ng ? a.M[1][tile * (CT_TILE / 64) + tid] : 0ull;
+  uint64_t key[QY_ROUNDS];
+  uint32_t row[QY_ROUNDS];
+#pragma unroll
+  for (int r = 0; r < QY_ROUNDS; ++r) {
+    const int lp = (wv + r * (QY_THREADS / WAVE)) * 64 + lane;
+    const bool live = lp < tn;
+    key[r] = live ? keys[base + lp] : 0ull;
+    row[r] = live ? vals[base + lp] : 0u;
+    const uint64_t v = live ? a.V[base + lp] : 0ull;
+    s_v[lp] = v;
+    s_val[lp] = row[r];
+  }
   if (tid == 0) s_nesc = 0;
   __syncthreads();
+  if (tid < CT_TILE / 8) {
+    uint64_t m = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) m = s_v[tid * 8 + i] > m ? s_v[tid * 8 + i] : m;
+    s_sub[tid] = m;
+  }
   if (wv == 0) {  // group-level window maxima and exclusive prefix maxima
-    uint64_t w = s_m1[lane];
+    const uint64_t m1 = lane < ng ? a.M[1][tile * QY_GROUPS + lane] : 0ull;
+    uint64_t w = m1;
     s_g[0][lane] = w;
 #pragma unroll
     for (int k = 1; k < 6; ++k) {
@@ -320,7 +345,7 @@ __global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
       if (lane >= (1 << (k - 1))) w = o > w ? o : w;
       s_g[k][lane] = w;
     }
-    uint64_t inc = s_m1[lane];
+    uint64_t inc = m1;
     for (int d = 1; d < WAVE; d <<= 1) {
       const uint64_t o = shfl_up(inc, d);
       if (lane >= d) inc = o > inc ? o : inc;
@@ -330,14 +355,13 @@ __global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
     s_gpre[lane] = lane == 0 ? pt : (ex > pt ? ex : pt);
   }
   __syncthreads();
-  // one wave per 64-position group, one lane per position
-  for (int g = wv; g < ng; g += CT_THREADS / WAVE) {
-    const int64_t lp = (int64_t)g * 64 + lane;
+#pragma unroll
+  for (int r = 0; r < QY_ROUNDS; ++r) {
+    const int g = wv + r * (QY_THREADS / WAVE);
+    const int lp = g * 64 + lane;
     const bool live = lp < tn;
-    const int64_t p = base + lp;
-    const uint64_t key = live ? keys[p] : 0ull;
-    const uint64_t q = (key_seg(a, key) << a.vb) | (uint64_t)(key_rel(a, key) + 1);
-    const uint64_t v = live ? s_v[lp] : 0ull;
+    const uint64_t q = (key_seg(a, key[r]) << a.vb) | (uint64_t)(key_rel(a, key[r]) + 1);
+    const uint64_t v = s_v[lp];
     uint64_t w[6];
     w[0] = v;
 #pragma unroll
@@ -358,11 +382,11 @@ __global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
     const bool want = live && pm > q;
     // level 0: this group
     const int f0 = wave_lift(w, lane - 1, q);
-    int64_t ans = -1;
+    int ans = -1;  // position in the tile
     bool escape = false;
     if (want) {
       if (f0 >= 0) {
-        ans = base + (int64_t)g * 64 + f0;
+        ans = g * 64 + f0;
       } else {
         // level 1: the tile's earlier groups, widest windows first
         int h = g - 1;
@@ -370,11 +394,16 @@ __global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
         for (int k = 5; k >= 0; --k)
           if (h - (1 << k) + 1 >= 0 && s_g[k][h] <= q) h -= 1 << k;
         if (h >= 0) {
-          for (int i = h * 64 + 63; i >= h * 64; --i)
-            if (s_v[i] > q) {
-              ans = base + i;
-              break;
-            }
+          // the last 8-block of group h above q, then its last position
+          // (group h holds a value above q; the bounds only guard that)
+          int sb = h * 8 + 7;
+          while (sb > h * 8 && s_sub[sb] <= q) --sb;
+          int i = sb * 8 + 7;
+          while (i > sb * 8 && s_v[i] <= q) --i;
+          if (s_v[i] > q)
+            ans = i;
+          else
+            set_status(a.ds, DS_LOGIC);
         } else {
           escape = true;
         }
@@ -384,22 +413,23 @@ __global__ __launch_bounds__(CT_THREADS) void k_query(ContainArgs a) {
       const int slot = atomicAdd(&s_nesc, 1);
       s_esc[slot] = (uint16_t)lp;
     } else if (live) {
-      a.par[p] = (int32_t)ans;
-      a.link[vals[p]] = ans >= 0 ? (int32_t)vals[ans] : -1;
+      a.par[base + lp] = ans >= 0 ? (int32_t)(base + ans) : -1;
+      a.link[row[r]] = ans >= 0 ? (int32_t)s_val[ans] : -1;
     }
   }
   __syncthreads();
   // answers in earlier tiles, one wave per query
   const int nesc = s_nesc;
-  for (int e = wv; e < nesc; e += CT_THREADS / WAVE) {
-    const int64_t p = base + s_esc[e];
-    const uint64_t key = keys[p];
-    const uint64_t q = (key_seg(a, key) << a.vb) | (uint64_t)(key_rel(a, key) + 1);
+  for (int e = wv; e < nesc; e += QY_THREADS / WAVE) {
+    const int lp = s_esc[e];
+    const int64_t p = base + lp;
+    const uint64_t kk = keys[p];
+    const uint64_t q = (key_seg(a, kk) << a.vb) | (uint64_t)(key_rel(a, kk) + 1);
     const int64_t ans = wave_escape(a, tile, q, n);
     if (lane == 0) {
       if (ans < 0) set_status(a.ds, DS_LOGIC);
       a.par[p] = (int32_t)ans;
-      a.link[vals[p]] = ans >= 0 ? (int32_t)vals[ans] : -1;
+      a.link[s_val[lp]] = ans >= 0 ? (int32_t)vals[ans] : -1;
     }
   }
 }
@@ -623,7 +653,7 @@ void launch_contain(Ctx& c) {
   hipLaunchKernelGGL(k_tiefix_long, dim3(64), dim3(256), 0, c.st, a);
   hipLaunchKernelGGL(k_vbuild, dim3((unsigned)tiles), dim3(CT_THREADS), 0, c.st, a);
   if (c.nlev > 3) hipLaunchKernelGGL(k_vlevels, dim3(1), dim3(1024), 0, c.st, a);
-  hipLaunchKernelGGL(k_query, dim3((unsigned)tiles), dim3(CT_THREADS), 0, c.st, a);
+  hipLaunchKernelGGL(k_query, dim3((unsigned)tiles), dim3(QY_THREADS), 0, c.st, a);
   hipLaunchKernelGGL(k_depth, dim3(grid_stride), dim3(256), 0, c.st, a);
 }
 
