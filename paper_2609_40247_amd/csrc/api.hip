@@ -206,9 +206,28 @@ __global__ __launch_bounds__(256) void k_nocontain(const uint64_t* keys, const u
   }
 }
 
-__global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counters* cnt, int64_t* busy, int64_t* idle,
-                                                  int nps, int64_t W) {
+__global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counters* cnt, int64_t* lat_hist, int64_t* busy,
+                                                  int64_t* idle, int nps, int64_t W) {
   for (int i = threadIdx.x; i < nps; i += 256) idle[i] = W - busy[i];
+  // join counts and latency bins from their accumulator copies
+  if (threadIdx.x < JC_N + 64) {
+    unsigned long long v = 0;
+    for (int k = 0; k < JOIN_COPIES; ++k) v += ds->join_acc[k][threadIdx.x];
+    if (threadIdx.x >= JC_N) {
+      lat_hist[threadIdx.x - JC_N] += (int64_t)v;
+    } else {
+      int64_t* dst = nullptr;
+      switch (threadIdx.x) {
+        case JC_MATCHED: dst = &cnt->n_matched; break;
+        case JC_UNM_K: dst = &cnt->n_unmatched_kernels; break;
+        case JC_UNM_L: dst = &cnt->n_unmatched_launches; break;
+        case JC_DUP: dst = &cnt->n_dup_launch_corr; break;
+        case JC_NEG: dst = &cnt->n_negative_latency; break;
+        default: dst = &cnt->n_unattributed_kernels; break;
+      }
+      *dst += (int64_t)v;
+    }
+  }
   if (threadIdx.x == 0) {
     cnt->first_invalid = ds->first_invalid == I64MAX ? -1 : ds->first_invalid;
     cnt->device_status = ds->status;
@@ -216,7 +235,8 @@ __global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counter
 }
 
 void launch_finalize(Ctx& c) {
-  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, c.st, c.ds, c.o.counters, c.o.busy, c.o.idle, c.P * c.S, c.W);
+  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, c.st, c.ds, c.o.counters, c.o.lat_hist, c.o.busy, c.o.idle,
+                     c.P * c.S, c.W);
 }
 
 // ------------------------------------------------------------- the call

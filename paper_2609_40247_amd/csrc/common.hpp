@@ -40,6 +40,8 @@ enum : int {
 constexpr int N_TICKETS = TK_RADIX + 8 * 3;
 
 constexpr int N_SORTS = 3;  // 0 timeline, 1 join, 2 containment
+enum { JC_MATCHED, JC_UNM_K, JC_UNM_L, JC_DUP, JC_NEG, JC_UNATTR, JC_N };
+constexpr int JOIN_COPIES = 16;
 
 // Per-call device state, zeroed by the init kernel.
 struct DevState {
@@ -55,6 +57,8 @@ struct DevState {
   int64_t first_invalid;  // smallest bad row (INT64_MAX = none)
   int64_t n_gaps;
   uint32_t sort_trivial[N_SORTS];  // bit d: every key has the same digit d (pass skipped)
+  // join counts (JC_* order) and latency bins, in copies summed at the end
+  unsigned long long join_acc[JOIN_COPIES][JC_N + 64];
   // radix digit histograms; the last histogram workgroup turns each into the
   // exclusive prefix over digit values (the global offset of every bin)
   uint32_t hist[N_SORTS][8][256];

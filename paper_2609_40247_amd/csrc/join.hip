@@ -78,8 +78,11 @@ __device__ int64_t gallop_back_ge(const uint64_t* keys, int64_t i, uint64_t targ
   return b;
 }
 
-enum { JC_MATCHED, JC_UNM_K, JC_UNM_L, JC_DUP, JC_NEG, JC_UNATTR, JC_N };
-
+// One sorted position per thread.  The neighbours i-2 .. i+2 are
+// loaded with the position itself: they settle the usual groups (one launch
+// and its kernel) without a search, and the gallops handle the rest.  Counts
+// and latency bins go to one of JOIN_COPIES accumulator copies (spread so
+// that few workgroups add to one address); the final kernel sums them.
 __global__ __launch_bounds__(256) void k_join(JoinArgs a) {
   __shared__ unsigned long long s_c[JC_N];
   __shared__ unsigned long long s_h[64];
@@ -91,16 +94,28 @@ __global__ __launch_bounds__(256) void k_join(JoinArgs a) {
   const int par = (int)a.ds->sort_parity[1];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
+  const int64_t i = (int64_t)blockIdx.x * 256 + tid;
   uint32_t c[JC_N] = {0, 0, 0, 0, 0, 0};
-  for (int64_t i = (int64_t)blockIdx.x * 256 + tid; i < n; i += (int64_t)gridDim.x * 256) {
+  if (i < n) {
     const uint64_t key = keys[i];
     const uint32_t row = vals[i];
+    const uint64_t kprev = i > 0 ? keys[i - 1] : ~0ull;
+    const uint64_t kprev2 = i > 1 ? keys[i - 2] : ~0ull;
+    const uint64_t knext = i + 1 < n ? keys[i + 1] : ~0ull;
+    const uint64_t knext2 = i + 2 < n ? keys[i + 2] : ~0ull;
     const uint64_t g = key >> 1;
     if ((key & 1) == 0) {  // launch
-      const bool head = i == 0 || (keys[i - 1] >> 1) != g;
-      if (head) {
-        const int64_t fk = gallop_ge(keys, i + 1, n, (g << 1) | 1);
-        const int64_t end = gallop_ge(keys, fk, n, (g + 1) << 1);
+      if ((kprev >> 1) != g) {  // the group's head
+        int64_t fk, end;
+        if (knext == ((g << 1) | 1)) {
+          fk = i + 1;
+          end = (knext2 >> 1) != g ? i + 2 : gallop_ge(keys, i + 2, n, (g + 1) << 1);
+        } else if ((knext >> 1) != g) {
+          fk = end = i + 1;
+        } else {
+          fk = gallop_ge(keys, i + 1, n, (g << 1) | 1);
+          end = gallop_ge(keys, fk, n, (g + 1) << 1);
+        }
         const int64_t nk = end - fk;
         a.aux[row] = (int32_t)nk;
         if (nk == 0) ++c[JC_UNM_L];
@@ -124,9 +139,14 @@ __global__ __launch_bounds__(256) void k_join(JoinArgs a) {
         ++c[JC_DUP];
         ++c[JC_UNM_L];
       }
-    } else {  // kernel
-      const int64_t f = gallop_back_ge(keys, i, g << 1);
-      if ((keys[f] & 1) == 0) {
+    } else {  // kernel: the group's head decides
+      // the first position of the group: i, i - 1 (one launch before), or
+      // found by galloping back (several launches, or kernels before i)
+      const int64_t f = (kprev >> 1) != g                          ? i
+                        : (kprev & 1) == 0 && (kprev2 >> 1) != g ? i - 1
+                                                                 : gallop_back_ge(keys, i, g << 1);
+      const uint64_t kf = f == i ? key : f == i - 1 ? kprev : keys[f];
+      if ((kf & 1) == 0) {
         const uint32_t lrow = vals[f];
         a.link[row] = (int32_t)lrow;
         ++c[JC_MATCHED];
@@ -154,19 +174,9 @@ __global__ __launch_bounds__(256) void k_join(JoinArgs a) {
     if (lane_id() == 0 && w) atomicAdd(&s_c[q], (unsigned long long)w);
   }
   __syncthreads();
-  if (tid < JC_N && s_c[tid]) {
-    int64_t* dst = nullptr;
-    switch (tid) {
-      case JC_MATCHED: dst = &a.cnt->n_matched; break;
-      case JC_UNM_K: dst = &a.cnt->n_unmatched_kernels; break;
-      case JC_UNM_L: dst = &a.cnt->n_unmatched_launches; break;
-      case JC_DUP: dst = &a.cnt->n_dup_launch_corr; break;
-      case JC_NEG: dst = &a.cnt->n_negative_latency; break;
-      default: dst = &a.cnt->n_unattributed_kernels; break;
-    }
-    atomicAdd((unsigned long long*)dst, s_c[tid]);
-  }
-  if (tid < 64 && s_h[tid]) atomicAdd((unsigned long long*)&a.lat_hist[tid], s_h[tid]);
+  unsigned long long* acc = &a.ds->join_acc[blockIdx.x % JOIN_COPIES][0];
+  if (tid < JC_N && s_c[tid]) atomicAdd(&acc[tid], s_c[tid]);
+  if (tid < 64 && s_h[tid]) atomicAdd(&acc[JC_N + tid], s_h[tid]);
 }
 
 __global__ __launch_bounds__(256) void k_edges(JoinArgs a) {
@@ -237,8 +247,8 @@ static JoinArgs join_args(Ctx& c) {
 
 void launch_join(Ctx& c) {
   JoinArgs a = join_args(c);
-  const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.sJ.n_max, 256 * 8), 1), 1024);
-  hipLaunchKernelGGL(k_join, dim3(grid), dim3(256), 0, c.st, a);
+  const int64_t grid = std::max<int64_t>(cdiv(c.sJ.n_max, 256), 1);
+  hipLaunchKernelGGL(k_join, dim3((unsigned)grid), dim3(256), 0, c.st, a);
 }
 
 void launch_edges(Ctx& c) {
