@@ -8,7 +8,8 @@ aggregates, cross-stream overlap) of the decode-step trace: 1 process,
 records, 1M launches, 1M CPU ops: 2.99M rows).  The input is resident in
 HBM before timing.  Prints one JSON line: events (all input rows) per
 second, the roofline of the dominant kernel measured live with HIP events
-on the library's stream, and the CPU oracle timed on this host.
+on the library's stream (the radix-sort passes), and the CPU oracle timed
+on this host.
 """
 from __future__ import annotations
 
@@ -23,11 +24,14 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 METRIC = "trace events analyzed/sec (M ev/s) at 1 MI355X + achieved HBM GB/s % peak"
 HBM_PEAK_GBS = 8000.0
-# Stage used for the roofline and the sources that define it (the profile
-# traffic is only trusted while these files are unchanged).
-ROOFLINE_STAGE = "prep"
-STAGE_SOURCES = {"prep": ["paper_2609_40247_amd/csrc/prep.hip", "paper_2609_40247_amd/csrc/common.hpp",
+# Stage used for the roofline (the radix passes: the largest share of the
+# device time) and the sources that define its kernels (the profiled traffic
+# is only trusted while these files are unchanged).
+ROOFLINE_STAGE = "sort"
+ROOFLINE_KERNEL = "k_radix_pass"
+STAGE_SOURCES = {"sort": ["paper_2609_40247_amd/csrc/radix.hip", "paper_2609_40247_amd/csrc/common.hpp",
                           "paper_2609_40247_amd/csrc/internal.hpp"]}
+BYTES_PER_KEY_PASS = 24  # a digit pass reads and writes one 8-byte key and one 4-byte row index
 
 
 def source_hash(stage: str) -> str:
@@ -38,25 +42,25 @@ def source_hash(stage: str) -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(stage: str, n: int, c: dict) -> int:
-    """Bytes the stage must move for one call (inputs read once, outputs
-    written once; no look-back or scratch traffic)."""
-    if stage == "prep":
-        n_lists = c["n_admitted_kernel"] + (c["n_admitted_cpu"] + c["n_admitted_launch"]) + \
-            (c["n_admitted_launch"] + c["n_admitted_kernel"])
-        return 37 * n + 12 * n_lists + 8 * c["n_outside_window"]
-    raise ValueError(stage)
+def sort_units(stats):
+    """Key-passes the radix sorts must make: each sort moves its keys once
+    per digit on which they differ.  Also the number of pass launches (the
+    sorts share launches; one per digit of the widest key)."""
+    units = 0
+    for nkeys, skipped, nd in stats:
+        units += nkeys * sum(1 for d in range(nd) if not (skipped >> d) & 1)
+    return units, max(nd for _, _, nd in stats)
 
 
 def profiled_traffic(stage: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if
-    it was taken on the current sources."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{stage}_{workload}.md")
+    """HBM bytes per call of the stage from the committed rocprofv3 counter
+    summary, if it was taken on the current sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{ROOFLINE_KERNEL}_{workload}.md")
     if not os.path.exists(path):
         return None
     txt = open(path).read()
     m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", txt)
-    m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9]+)", txt)
+    m_b = re.search(r"hbm_bytes_per_call:\s*([0-9]+)", txt)
     if not m_sha or not m_b or m_sha.group(1) != source_hash(stage):
         return None
     return int(m_b.group(1))
@@ -84,6 +88,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stages", action="store_true", help="also print a per-stage breakdown to stderr")
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="first copy a buffer of this many MiB on the device (a plain copy kernel of known "
+                         "size, for scaling rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -94,6 +101,14 @@ def main() -> int:
     import torch
     from paper_2609_40247_amd import herschel as H
     from paper_2609_40247_amd import synth
+
+    if args.copy_mb > 0:
+        src = torch.empty(args.copy_mb << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     tr = synth.config1()
     n = tr.n
@@ -106,6 +121,7 @@ def main() -> int:
         if code != 0:
             raise RuntimeError(f"analysis failed: {H.herschel_strerror(code)}")
     c = an.results(n)["counters"]
+    units, launches = sort_units(H.herschel_sort_stats(an.params))
 
     stage_id = H.STAGES.index(ROOFLINE_STAGE)
     pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
@@ -140,9 +156,12 @@ def main() -> int:
             H.herschel_time_stage(sid, None, None)
             print(f"stage {name:14s} {tot / 5 * 1e3:9.1f} us", file=sys.stderr)
 
-    alg = algorithmic_bytes(ROOFLINE_STAGE, n, c)
-    achieved = alg / (stage_ms * 1e-3) / 1e9
+    # per launch of k_radix_pass: the stage's bytes and time over its launches
+    alg = BYTES_PER_KEY_PASS * units / launches
+    launch_s = stage_ms * 1e-3 / launches
+    achieved = alg / launch_s / 1e9
     traffic = profiled_traffic(ROOFLINE_STAGE, "config1")
+    traffic = None if traffic is None else round(traffic / launches)
     out = {
         "metric": METRIC, "value": round(n / (ms * 1e-3) / 1e6, 3), "unit": "M ev/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
@@ -150,9 +169,10 @@ def main() -> int:
         "config": {"workload": "decode-step trace: 1 process, 4 streams, 30 s window, 1000 steps x 1000 kernels",
                    "rows": n, "kernels": c["n_admitted_kernel"], "launches": c["n_admitted_launch"],
                    "cpu_ops": c["n_admitted_cpu"], "outputs": "all"},
-        "roofline": {"kernel": f"k_{ROOFLINE_STAGE}", "bound": "hbm", "achieved": round(achieved, 1),
+        "roofline": {"kernel": ROOFLINE_KERNEL, "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "algorithmic_bytes": alg, "launch_us": round(stage_ms * 1e3, 2)},
+                     "traffic": traffic, "algorithmic_bytes": round(alg), "launch_us": round(launch_s * 1e6, 2),
+                     "launches_per_step": launches, "key_passes_per_step": units},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(tr.columns(), tr.params, n)

@@ -206,6 +206,16 @@ enum {
  * thread-safe: meant for single-threaded benchmarks. */
 int herschel_time_stage(int stage, void *start_event, void *stop_event);
 
+/* Sort statistics of the last analysis call made with this workspace and
+ * these params, for computing the bytes the radix passes must move: waits
+ * for params->hip_stream, then writes, for s = 0 timeline, 1 join,
+ * 2 containment sort: out[3 * s + 0] = its keys, out[3 * s + 1] = bit mask
+ * of the 8-bit digits it skipped (every key agreed on them), out[3 * s + 2]
+ * = its digits.  out must hold 9 entries (host memory).  Returns
+ * HERSCHEL_EINVAL for NULL arguments, no workspace or an invalid window or
+ * size, HERSCHEL_EDEVICE when the copy fails. */
+int herschel_sort_stats(const herschel_params *p, int32_t *out);
+
 #ifdef __cplusplus
 }
 #endif

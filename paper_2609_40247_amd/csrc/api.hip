@@ -51,6 +51,7 @@ size_t layout_workspace(Ctx& c, char* base) {
   c.prep_status = b.take<uint64_t>(3 * std::max<int64_t>(c.prep_tiles, 1));
   c.union_tiles = std::max<int64_t>(cdiv(n, union_tile_elems()), 1);
   c.union_status = b.take<uint64_t>(3 * c.union_tiles);
+  // key widths (also reported by herschel_sort_stats)
   sort_plan(c.sK, 0, n, c.pb + c.sb + c.wb, true);
   sort_plan(c.sJ, 1, n, 49 + c.pb, true);
   sort_plan(c.sC, 2, n, c.pb + c.tb + c.wb + 1, true);
@@ -395,6 +396,28 @@ int herschel_time_stage(int stage, void* start_event, void* stop_event) {
   g_stage = (start_event && stop_event) ? stage : -1;
   g_ev0 = (hipEvent_t)start_event;
   g_ev1 = (hipEvent_t)stop_event;
+  return HERSCHEL_OK;
+}
+
+int herschel_sort_stats(const herschel_params* p, int32_t* out) {
+  if (!p || !out || !p->workspace) return HERSCHEL_EINVAL;
+  if (p->window_end <= p->window_begin || p->n_procs < 1 || p->n_streams < 1 || p->n_threads < 1)
+    return HERSCHEL_EINVAL;
+  DevState ds;  // the workspace starts with the device state of the last call
+  if (hipStreamSynchronize((hipStream_t)p->hip_stream) != hipSuccess ||
+      hipMemcpy(&ds, p->workspace, sizeof(DevState), hipMemcpyDeviceToHost) != hipSuccess)
+    return HERSCHEL_EDEVICE;
+  // digit passes per sort, as layout_workspace plans them
+  const int pb = bits_host((uint64_t)(p->n_procs - 1)), sb = bits_host((uint64_t)(p->n_streams - 1));
+  const int tb = bits_host((uint64_t)(p->n_threads - 1));
+  const int wb = bits_host((uint64_t)(p->window_end - p->window_begin - 1));
+  const int key_bits[N_SORTS] = {pb + sb + wb, 49 + pb, pb + tb + wb + 1};
+  const int32_t counts[N_SORTS] = {ds.nK, ds.nJ, ds.nCL};
+  for (int i = 0; i < N_SORTS; ++i) {
+    out[3 * i + 0] = counts[i];
+    out[3 * i + 1] = (int32_t)ds.sort_trivial[i];
+    out[3 * i + 2] = (key_bits[i] + 7) / 8;
+  }
   return HERSCHEL_OK;
 }
 

@@ -88,6 +88,8 @@ def load(variant: str | None = None) -> ctypes.CDLL:
         lib.herschel_strerror.argtypes = [ctypes.c_int]
         lib.herschel_time_stage.restype = ctypes.c_int
         lib.herschel_time_stage.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+        lib.herschel_sort_stats.restype = ctypes.c_int
+        lib.herschel_sort_stats.argtypes = [ctypes.POINTER(HerschelParams), ctypes.POINTER(ctypes.c_int32)]
         _lib[path] = lib
     return _lib[path]
 
@@ -133,6 +135,17 @@ def herschel_time_stage(stage: int, start_event, stop_event, lib=None) -> int:
     if (start_event is not None and not a) or (stop_event is not None and not b):
         raise ValueError("record the events once before handing them over (torch creates them lazily)")
     return int(lib.herschel_time_stage(int(stage), a, b))
+
+
+def herschel_sort_stats(params: "HerschelParams", lib=None) -> list[tuple[int, int, int]]:
+    """(keys, skipped-digit mask, digits) of the timeline, join and
+    containment sorts of the last call made with params' workspace."""
+    lib = lib or load()
+    out = (ctypes.c_int32 * 9)()
+    code = int(lib.herschel_sort_stats(ctypes.byref(params), out))
+    if code != 0:
+        raise RuntimeError(f"herschel_sort_stats: {code}")
+    return [(int(out[3 * i]), int(out[3 * i + 1]) & 0xFFFFFFFF, int(out[3 * i + 2])) for i in range(3)]
 
 
 def herschel_strerror(code: int, lib=None) -> str:

@@ -33,7 +33,7 @@ def libs():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for f in ("herschel_trace_analyze", "herschel_trace_analyze_batch", "herschel_workspace_size",
-              "herschel_strerror", "herschel_time_stage"):
+              "herschel_strerror", "herschel_time_stage", "herschel_sort_stats"):
         assert f in names
 
 
@@ -62,3 +62,5 @@ def test_host_only_entry_points(libs):
     lib.herschel_time_stage.restype = ctypes.c_int
     assert lib.herschel_time_stage(99, None, None) == -1
     assert lib.herschel_time_stage(1, None, None) == 0
+    lib.herschel_sort_stats.restype = ctypes.c_int
+    assert lib.herschel_sort_stats(None, None) == -1
