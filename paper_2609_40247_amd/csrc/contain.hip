@@ -648,7 +648,8 @@ static ContainArgs contain_args(Ctx& c) {
 void launch_contain(Ctx& c) {
   ContainArgs a = contain_args(c);
   const int64_t tiles = std::max<int64_t>(cdiv(c.sC.n_max, CT_TILE), 1);
-  const int grid_stride = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.sC.n_max, 256 * 8), 1), 2048);
+  // one position per thread: these kernels are chains of dependent loads
+  const int grid_stride = (int)std::max<int64_t>(cdiv(c.sC.n_max, 256), 1);
   hipLaunchKernelGGL(k_tiefix, dim3(grid_stride), dim3(256), 0, c.st, a);
   hipLaunchKernelGGL(k_tiefix_long, dim3(64), dim3(256), 0, c.st, a);
   hipLaunchKernelGGL(k_vbuild, dim3((unsigned)tiles), dim3(CT_THREADS), 0, c.st, a);

@@ -14,6 +14,7 @@ namespace hx {
 
 constexpr int NM_THREADS = 256;
 constexpr int NM_LDS_NAMES = 4096;  // 128 KB of LDS
+constexpr int NM_BATCH = 8;
 
 struct NamesArgs {
   const uint32_t* rows;  // admitted kernels (any order)
@@ -44,20 +45,33 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
     __syncthreads();
   }
   const int64_t n = a.ds->nK;
-  for (int64_t i = (int64_t)blockIdx.x * NM_THREADS + tid; i < n; i += (int64_t)gridDim.x * NM_THREADS) {
-    const uint32_t r = a.rows[i];
-    const int32_t q = a.name[r];
-    const int64_t d = a.te[r] - a.ts[r];
-    if (lds) {
-      atomicAdd(&tab[q * 4 + 0], 1ull);
-      atomicAdd(&tab[q * 4 + 1], (unsigned long long)d);
-      atomicMin((long long*)&tab[q * 4 + 2], (long long)d);
-      atomicMax((long long*)&tab[q * 4 + 3], (long long)d);
-    } else {
-      atomicAdd((unsigned long long*)&a.count[q], 1ull);
-      atomicAdd((unsigned long long*)&a.sum[q], (unsigned long long)d);
-      atomicMin((long long*)&a.mn[q], (long long)d);
-      atomicMax((long long*)&a.mx[q], (long long)d);
+  // NM_BATCH kernels per thread and round, their loads issued together
+  const int64_t stride = (int64_t)gridDim.x * NM_THREADS;
+  for (int64_t i0 = (int64_t)blockIdx.x * NM_THREADS + tid; i0 < n; i0 += NM_BATCH * stride) {
+    uint32_t r[NM_BATCH];
+#pragma unroll
+    for (int u = 0; u < NM_BATCH; ++u) r[u] = i0 + u * stride < n ? a.rows[i0 + u * stride] : ~0u;
+    int32_t q[NM_BATCH];
+    int64_t d[NM_BATCH];
+#pragma unroll
+    for (int u = 0; u < NM_BATCH; ++u) {
+      q[u] = r[u] != ~0u ? a.name[r[u]] : -1;
+      d[u] = r[u] != ~0u ? a.te[r[u]] - a.ts[r[u]] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < NM_BATCH; ++u) {
+      if (q[u] < 0) continue;
+      if (lds) {
+        atomicAdd(&tab[q[u] * 4 + 0], 1ull);
+        atomicAdd(&tab[q[u] * 4 + 1], (unsigned long long)d[u]);
+        atomicMin((long long*)&tab[q[u] * 4 + 2], (long long)d[u]);
+        atomicMax((long long*)&tab[q[u] * 4 + 3], (long long)d[u]);
+      } else {
+        atomicAdd((unsigned long long*)&a.count[q[u]], 1ull);
+        atomicAdd((unsigned long long*)&a.sum[q[u]], (unsigned long long)d[u]);
+        atomicMin((long long*)&a.mn[q[u]], (long long)d[u]);
+        atomicMax((long long*)&a.mx[q[u]], (long long)d[u]);
+      }
     }
   }
   if (!lds) return;
@@ -75,12 +89,12 @@ __global__ __launch_bounds__(256) void k_names_reduce(NamesArgs a) {
   const int64_t stride = (int64_t)a.NN * 4;
   uint64_t acc = stat == 2 ? (uint64_t)I64MAX : stat == 3 ? (uint64_t)I64MIN : 0;
   int b = 0;
-  for (; b + 8 <= a.blocks; b += 8) {
-    uint64_t v[8];
+  for (; b + 32 <= a.blocks; b += 32) {
+    uint64_t v[32];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = a.part[(int64_t)(b + i) * stride + t];
+    for (int i = 0; i < 32; ++i) v[i] = a.part[(int64_t)(b + i) * stride + t];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < 32; ++i) {
       if (stat < 2) acc += v[i];
       else if (stat == 2) acc = (int64_t)v[i] < (int64_t)acc ? v[i] : acc;
       else acc = (int64_t)v[i] > (int64_t)acc ? v[i] : acc;

@@ -19,10 +19,10 @@
 
 namespace hx {
 
-constexpr int SW_THREADS = 256;
-constexpr int SW_ITEMS = 16;
+constexpr int SW_THREADS = 512;
+constexpr int SW_ITEMS = 8;
 constexpr int SW_TILE = SW_THREADS * SW_ITEMS;
-constexpr int CR_STEPS = 16;  // merge-path steps per thread
+constexpr int CR_STEPS = 8;  // merge-path steps per thread
 constexpr int CR_SMAX = 8;    // most streams handled with pairwise merges
 
 struct SweepArgs {
@@ -115,7 +115,7 @@ __global__ __launch_bounds__(256) void k_segoff(SweepArgs a) {
 // pairs lets every thread find its own position in global memory instead.
 // Each merge step emits the co-rank of the smaller head in the other group
 // (keys of different streams never tie).
-constexpr int CR_THREADS = 256;
+constexpr int CR_THREADS = 512;
 constexpr int CR_TILE = CR_THREADS * CR_STEPS;
 
 struct PairPos {

@@ -13,7 +13,7 @@
 
 namespace hx {
 
-constexpr int PREP_THREADS = 256;
+constexpr int PREP_THREADS = 512;
 constexpr int PREP_ITEMS = 8;
 constexpr int PREP_TILE = PREP_THREADS * PREP_ITEMS;
 

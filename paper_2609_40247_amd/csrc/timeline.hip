@@ -15,8 +15,8 @@
 
 namespace hx {
 
-constexpr int UN_THREADS = 256;
-constexpr int UN_ITEMS = 16;
+constexpr int UN_THREADS = 512;
+constexpr int UN_ITEMS = 8;
 constexpr int UN_TILE = UN_THREADS * UN_ITEMS;
 
 struct UnionArgs {
