@@ -64,6 +64,17 @@ size_t layout_workspace(Ctx& c, char* base) {
   }
   c.zero_bytes = align_up(b.off - z0);
   c.hist_part = b.take<uint32_t>((int64_t)N_SORTS * HIST_MAX_BLOCKS * 8 * 256);
+  if (c.P <= JT_PROCS) {
+    // correlation table of the join: two slots per row bound every id range it accepts
+    c.jt_cap = 2 * n;
+    c.jt_tab = b.take<uint32_t>(c.jt_cap);
+    c.jt_own = b.take<uint32_t>(c.jt_cap);
+    c.jt_multi = b.take<uint8_t>(c.jt_cap);
+    if (c.p.n_edges > 0) {
+      c.jt_kmax = b.take<int64_t>(c.jt_cap);
+      c.jt_kmin = b.take<int64_t>(c.jt_cap);
+    }
+  }
   // sort buffers
   for (SortBufs* s : {&c.sK, &c.sJ, &c.sC}) {
     if (s == &c.sC && !c.contain) {
@@ -215,7 +226,7 @@ __global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counter
     unsigned long long v = 0;
     for (int k = 0; k < JOIN_COPIES; ++k) v += ds->join_acc[k][threadIdx.x];
     if (threadIdx.x >= JC_N) {
-      lat_hist[threadIdx.x - JC_N] += (int64_t)v;
+      if (v) lat_hist[threadIdx.x - JC_N] += (int64_t)v;
     } else {
       int64_t* dst = nullptr;
       switch (threadIdx.x) {
@@ -224,9 +235,14 @@ __global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counter
         case JC_UNM_L: dst = &cnt->n_unmatched_launches; break;
         case JC_DUP: dst = &cnt->n_dup_launch_corr; break;
         case JC_NEG: dst = &cnt->n_negative_latency; break;
-        default: dst = &cnt->n_unattributed_kernels; break;
+        case JC_UNATTR: dst = &cnt->n_unattributed_kernels; break;
+        default: dst = &cnt->n_unmatched_launches; break;  // JC_MLAUNCH
       }
-      *dst += (int64_t)v;
+      // two threads may add to one counter (the table path derives the
+      // unmatched launches from the launches with a kernel)
+      int64_t add = (int64_t)v;
+      if (threadIdx.x == JC_MLAUNCH) add = ds->join_direct ? cnt->n_admitted[HERSCHEL_LAUNCH] - (int64_t)v : 0;
+      if (add) atomicAdd((unsigned long long*)dst, (unsigned long long)add);
     }
   }
   if (threadIdx.x == 0) {
@@ -317,6 +333,7 @@ static int enqueue(Ctx& c) {
   stage_end(c, HERSCHEL_STAGE_INIT);
   stage_begin(c, HERSCHEL_STAGE_PREP);
   launch_prep(c);
+  launch_join_plan(c);
   stage_end(c, HERSCHEL_STAGE_PREP);
   stage_begin(c, HERSCHEL_STAGE_HIST);
   {
@@ -430,6 +447,7 @@ int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) 
       p->n_names < 1 || p->n_names > HERSCHEL_MAX_NAMES)
     return HERSCHEL_EINVAL;
   Ctx c;
+  c.p = *p;
   c.n = n;
   c.P = p->n_procs;
   c.S = p->n_streams;

@@ -40,8 +40,13 @@ enum : int {
 constexpr int N_TICKETS = TK_RADIX + 8 * 3;
 
 constexpr int N_SORTS = 3;  // 0 timeline, 1 join, 2 containment
-enum { JC_MATCHED, JC_UNM_K, JC_UNM_L, JC_DUP, JC_NEG, JC_UNATTR, JC_N };
+// join counters; the correlation table path keeps JC_MLAUNCH (launches with a
+// kernel) instead of JC_UNM_L and derives the unmatched launches at the end
+enum { JC_MATCHED, JC_UNM_K, JC_UNM_L, JC_DUP, JC_NEG, JC_UNATTR, JC_MLAUNCH, JC_N };
 constexpr int JOIN_COPIES = 16;
+// The join uses a table indexed by correlation id when the call has at most
+// JT_PROCS processes and their id ranges fit the table (2 slots per row).
+constexpr int JT_PROCS = 64;
 
 // Per-call device state, zeroed by the init kernel.
 struct DevState {
@@ -57,6 +62,13 @@ struct DevState {
   int64_t first_invalid;  // smallest bad row (INT64_MAX = none)
   int64_t n_gaps;
   uint32_t sort_trivial[N_SORTS];  // bit d: every key has the same digit d (pass skipped)
+  uint32_t join_direct;            // 1: the correlation table replaces the join sort
+  uint32_t pad1;
+  int64_t jt_slots;                // table slots in use
+  uint64_t jt_key_lo[JT_PROCS];    // bitwise complement of each process's smallest join key (0: none)
+  uint64_t jt_key_hi[JT_PROCS];    // each process's largest join key
+  int64_t jt_cmin[JT_PROCS];       // smallest correlation id of each process
+  int64_t jt_base[JT_PROCS];       // first table slot of each process
   // join counts (JC_* order) and latency bins, in copies summed at the end
   unsigned long long join_acc[JOIN_COPIES][JC_N + 64];
   // radix digit histograms; the last histogram workgroup turns each into the
@@ -82,6 +94,8 @@ template <class T>
 __device__ __forceinline__ T shfl_up(T v, unsigned d) { return __shfl_up(v, d, WAVE); }
 template <class T>
 __device__ __forceinline__ T shfl_down(T v, unsigned d) { return __shfl_down(v, d, WAVE); }
+template <class T>
+__device__ __forceinline__ T shfl_xor(T v, int m) { return __shfl_xor(v, m, WAVE); }
 
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
   for (int d = 32; d >= 1; d >>= 1) v += shfl_down(v, d);

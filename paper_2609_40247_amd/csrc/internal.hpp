@@ -44,6 +44,12 @@ struct Ctx {
   int64_t* corr_min = nullptr;       // [P]
   SortBufs sK, sJ, sC;               // timeline, join, containment
   uint32_t* hist_part = nullptr;     // [N_SORTS][HIST_MAX_BLOCKS][8 * 256] per-workgroup digit counts
+  uint32_t* jt_tab = nullptr;        // [jt_cap] smallest launch row per correlation slot
+  uint32_t* jt_own = nullptr;        // [jt_cap] one kernel row per slot
+  uint8_t* jt_multi = nullptr;       // [jt_cap] 1: the slot has several kernels
+  int64_t* jt_kmax = nullptr;        // [jt_cap] latest kernel end per slot (edges only)
+  int64_t* jt_kmin = nullptr;        // [jt_cap] earliest kernel start per slot (edges only)
+  int64_t jt_cap = 0;
   uint64_t* ev_keys = nullptr;       // [ev_cap] coverage run endpoints, grouped by (pid, stream)
   int64_t ev_cap = 0;
   int32_t* seg_off = nullptr;        // [P * S + 1] first endpoint of each (pid, stream)
@@ -81,6 +87,7 @@ void launch_contain(Ctx& c);
 void launch_opagg(Ctx& c);
 void launch_names_reduce(Ctx& c);
 void launch_join(Ctx& c);
+void launch_join_plan(Ctx& c);
 void launch_edges(Ctx& c);
 void launch_finalize(Ctx& c);
 
@@ -97,5 +104,11 @@ constexpr int RS_ITEMS = 8;
 constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 8192 keys per tile
 
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Workgroups of the histogram kernel for n keys (each stores one table).
+__host__ __device__ inline int hist_blocks(int64_t n) {
+  const int64_t b = cdiv(n, HIST_CHUNK);
+  return (int)(b < 1 ? 1 : b > HIST_MAX_BLOCKS ? HIST_MAX_BLOCKS : b);
+}
 
 }  // namespace hx

@@ -10,6 +10,17 @@
 // the kernel start minus the launch start (the "CPU submission time" of the
 // operator figure) binned by floor(log2)+1.  Dependency edges (panel
 // "Cross-process blocking") are binary searches into the same sorted runs.
+//
+// When a call has at most JT_PROCS processes and their correlation ids span
+// at most two slots per row (ids are dense per process: every API call takes
+// the next one), a table indexed by (process, id) replaces the sort.  Bulk
+// global atomics are slow on this GPU, so the table is built with plain
+// stores and checked: launches store their rows (one writer wins), those
+// that lost are the duplicates and put the smallest row in (atomics, rare);
+// kernels store their rows in an owner word, and only kernels sharing a slot
+// (graph replays) add to their launch's counts with atomics.  The decision
+// is taken on the device right after prep, which finds each process's id
+// range; the join sort's histogram and digit passes are then skipped.
 #include "internal.hpp"
 
 namespace hx {
@@ -34,6 +45,13 @@ struct JoinArgs {
   int P;
   int64_t* edge_wait;
   int32_t* edge_status;
+  // correlation table (processes <= JT_PROCS)
+  uint32_t* tab;
+  uint32_t* own;
+  uint8_t* multi;
+  int64_t* kmax;
+  int64_t* kmin;
+  int64_t cap;
 };
 
 // Smallest index in [lo, hi) whose key is >= target (hi if none); galloping
@@ -90,12 +108,13 @@ __global__ __launch_bounds__(256) void k_join(JoinArgs a) {
   if (tid < JC_N) s_c[tid] = 0;
   if (tid < 64) s_h[tid] = 0;
   __syncthreads();
+  if (a.ds->join_direct) return;  // the correlation table did the join
   const int64_t n = a.ds->nJ;
   const int par = (int)a.ds->sort_parity[1];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
   const int64_t i = (int64_t)blockIdx.x * 256 + tid;
-  uint32_t c[JC_N] = {0, 0, 0, 0, 0, 0};
+  uint32_t c[JC_N] = {};
   if (i < n) {
     const uint64_t key = keys[i];
     const uint32_t row = vals[i];
@@ -179,7 +198,286 @@ __global__ __launch_bounds__(256) void k_join(JoinArgs a) {
   if (tid < 64 && s_h[tid]) atomicAdd(&acc[JC_N + tid], s_h[tid]);
 }
 
+// Correlation-table plan: each process's id range (from the key range prep
+// found), slot bases by an exclusive scan, and the decision.  One wave, one
+// lane per process.
+__global__ __launch_bounds__(64) void k_jt_plan(JoinArgs a) {
+  const int p = threadIdx.x;
+  const uint64_t lo = p < a.P ? a.ds->jt_key_lo[p] : 0ull, hi = p < a.P ? a.ds->jt_key_hi[p] : 0ull;
+  constexpr uint64_t CORR_MASK = (1ull << 48) - 1;
+  const bool present = lo != 0;  // lo holds ~(smallest key); keys never reach ~0
+  const int64_t cmin = present ? (int64_t)((~lo >> 1) & CORR_MASK) : 0;
+  const int64_t cmax = present ? (int64_t)((hi >> 1) & CORR_MASK) : -1;
+  // ranges beyond the capacity saturate, so the sum cannot overflow
+  int64_t range = cmax - cmin + 1;
+  range = range > a.cap ? a.cap + 1 : range;
+  int64_t inc = range;
+  for (int d = 1; d < WAVE; d <<= 1) {
+    const int64_t o = (int64_t)shfl_up((uint64_t)inc, d);
+    if (p >= d) inc += o;
+  }
+  const int64_t total = (int64_t)shfl((uint64_t)inc, WAVE - 1);
+  const bool direct = total <= a.cap;
+  a.ds->jt_cmin[p] = cmin;
+  a.ds->jt_base[p] = inc - range;
+  if (p == 0) {
+    a.ds->join_direct = direct ? 1u : 0u;
+    a.ds->jt_slots = direct ? total : 0;
+    if (direct) a.ds->sort_trivial[1] = 0xFFu;  // no join sort: every digit pass skipped
+  }
+}
+
+__device__ __forceinline__ int64_t jt_slot(const DevState* ds, uint64_t key) {
+  const int p = (int)(key >> 49);
+  return ds->jt_base[p] + (int64_t)((key >> 1) & ((1ull << 48) - 1)) - ds->jt_cmin[p];
+}
+
+// Empty every slot in use (and the kernel-time tables when there are edges).
+__global__ __launch_bounds__(256) void k_jt_clear(JoinArgs a) {
+  if (!a.ds->join_direct) return;
+  const int64_t R = a.ds->jt_slots;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < R; i += (int64_t)gridDim.x * 256) {
+    a.tab[i] = ~0u;
+    a.multi[i] = 0;
+    if (a.kmax) {
+      a.kmax[i] = I64MIN;
+      a.kmin[i] = I64MAX;
+    }
+  }
+}
+
+__device__ __forceinline__ void jt_flush(const JoinArgs& a, uint32_t (&c)[JC_N], unsigned long long* s_c,
+                                         unsigned long long* s_h) {
+#pragma unroll
+  for (int q = 0; q < JC_N; ++q) {
+    const uint64_t w = wave_sum_u64(c[q]);
+    if (lane_id() == 0 && w) atomicAdd(&s_c[q], (unsigned long long)w);
+  }
+  __syncthreads();
+  unsigned long long* acc = &a.ds->join_acc[blockIdx.x % JOIN_COPIES][0];
+  if (threadIdx.x < JC_N && s_c[threadIdx.x]) atomicAdd(&acc[threadIdx.x], s_c[threadIdx.x]);
+  if (s_h && threadIdx.x < 64 && s_h[threadIdx.x]) atomicAdd(&acc[JC_N + threadIdx.x], s_h[threadIdx.x]);
+}
+
+// The table passes give each thread JT_ITEMS positions (striped over the
+// workgroup) and issue each round of their loads together: a pass is a
+// short chain of dependent loads, and batching positions per thread keeps
+// the number of waves the chip must cycle through low.
+constexpr int JT_ITEMS = 4;
+constexpr int JT_TILE = 256 * JT_ITEMS;
+
+// Pass 1: every launch stores its row in its slot and every kernel in its
+// slot's owner word, with plain stores (one writer of each wins).
+__global__ __launch_bounds__(256) void k_jt_store(JoinArgs a) {
+  if (!a.ds->join_direct) return;
+  const int64_t n = a.ds->nJ;
+  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + threadIdx.x;
+  uint64_t key[JT_ITEMS];
+  uint32_t row[JT_ITEMS];
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    const int64_t i = i0 + u * 256;
+    key[u] = i < n ? a.k[0][i] : ~0ull;  // unsorted: the join sort did not run
+    row[u] = i < n ? a.v[0][i] : 0u;
+  }
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    if (key[u] == ~0ull) continue;
+    const int64_t slot = jt_slot(a.ds, key[u]);
+    if (!in_range(a.ds, slot, a.cap)) continue;
+    if (key[u] & 1)
+      a.own[slot] = row[u];
+    else
+      a.tab[slot] = row[u];
+  }
+}
+
+// Pass 2: a launch that lost its slot is a duplicate; a kernel that lost its
+// owner word marks the slot as holding several kernels.  Launches start with
+// no kernels.
+__global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
+  __shared__ unsigned long long s_c[JC_N];
+  const int tid = threadIdx.x;
+  if (tid < JC_N) s_c[tid] = 0;
+  __syncthreads();
+  if (!a.ds->join_direct) return;
+  const int64_t n = a.ds->nJ;
+  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + tid;
+  uint32_t c[JC_N] = {};
+  uint64_t key[JT_ITEMS];
+  uint32_t row[JT_ITEMS], w[JT_ITEMS];
+  int64_t slot[JT_ITEMS];
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    const int64_t i = i0 + u * 256;
+    key[u] = i < n ? a.k[0][i] : ~0ull;
+    row[u] = i < n ? a.v[0][i] : 0u;
+  }
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    slot[u] = key[u] != ~0ull ? jt_slot(a.ds, key[u]) : -1;
+    const bool ok = slot[u] >= 0 && in_range(a.ds, slot[u], a.cap);
+    w[u] = !ok ? row[u] : (key[u] & 1) ? a.own[slot[u]] : a.tab[slot[u]];
+  }
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    if (key[u] == ~0ull) continue;
+    if (key[u] & 1) {
+      if (w[u] != row[u]) a.multi[slot[u]] = 1;
+    } else {
+      if (w[u] != row[u]) ++c[JC_DUP];
+      a.aux[row[u]] = 0;
+      if (a.contain) {
+        a.lk_first[row[u]] = I64MAX;
+        a.lk_last[row[u]] = I64MIN;
+        a.lk_sum[row[u]] = 0;
+      }
+    }
+  }
+  jt_flush(a, c, s_c, nullptr);
+}
+
+// Pass 3: duplicates put the smallest row into their slot (rare: atomics).
+__global__ __launch_bounds__(256) void k_jt_fix(JoinArgs a) {
+  if (!a.ds->join_direct) return;
+  const int64_t n = a.ds->nJ;
+  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + threadIdx.x;
+  uint64_t key[JT_ITEMS];
+  uint32_t row[JT_ITEMS];
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    const int64_t i = i0 + u * 256;
+    key[u] = i < n ? a.k[0][i] : 1ull;  // past the end: treated as a kernel
+    row[u] = i < n ? a.v[0][i] : 0u;
+  }
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    if (key[u] & 1) continue;
+    const int64_t slot = jt_slot(a.ds, key[u]);
+    if (in_range(a.ds, slot, a.cap) && a.tab[slot] != row[u]) atomicMin(&a.tab[slot], row[u]);
+  }
+}
+
+// Pass 4: each kernel reads its launch, records the latency, and adds itself
+// to the launch's counts: with plain stores when it is its slot's only kernel
+// (the usual case), with atomics otherwise.
+__global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
+  __shared__ unsigned long long s_c[JC_N];
+  __shared__ unsigned long long s_h[64];
+  const int tid = threadIdx.x;
+  if (tid < JC_N) s_c[tid] = 0;
+  if (tid < 64) s_h[tid] = 0;
+  __syncthreads();
+  if (!a.ds->join_direct) return;
+  const int64_t n = a.ds->nJ;
+  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + tid;
+  uint32_t c[JC_N] = {};
+  uint64_t key[JT_ITEMS];
+  uint32_t row[JT_ITEMS];
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    const int64_t i = i0 + u * 256;
+    key[u] = i < n ? a.k[0][i] : 0ull;  // past the end: treated as a launch (skipped)
+    row[u] = i < n ? a.v[0][i] : 0u;
+  }
+  // round 2: the slot's launch and kernel count, the kernel's times
+  int64_t slot[JT_ITEMS], ts[JT_ITEMS], te[JT_ITEMS];
+  uint32_t l[JT_ITEMS];
+  bool single[JT_ITEMS];
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    const bool kern = (key[u] & 1) != 0;
+    slot[u] = kern ? jt_slot(a.ds, key[u]) : -1;
+    const bool ok = slot[u] >= 0 && in_range(a.ds, slot[u], a.cap);
+    l[u] = ok ? a.tab[slot[u]] : ~0u;
+    single[u] = ok && a.multi[slot[u]] == 0;
+    ts[u] = kern ? a.ts[row[u]] : 0;
+    te[u] = kern ? a.te[row[u]] : 0;
+  }
+  // round 3: the launch's start and op
+  int64_t lts[JT_ITEMS];
+  int32_t lop[JT_ITEMS];
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    const bool m = (key[u] & 1) && l[u] != ~0u;
+    lts[u] = m ? a.ts[l[u]] : 0;
+    lop[u] = m && a.contain ? a.link[l[u]] : -1;
+  }
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    if (!(key[u] & 1)) continue;
+    const int64_t o = a.off ? a.off[(int32_t)(key[u] >> 49)] : 0;
+    if (a.kmax && slot[u] >= 0) {
+      if (single[u]) {
+        a.kmax[slot[u]] = te[u] - o;
+        a.kmin[slot[u]] = ts[u] - o;
+      } else {
+        atomicMax((long long*)&a.kmax[slot[u]], (long long)(te[u] - o));
+        atomicMin((long long*)&a.kmin[slot[u]], (long long)(ts[u] - o));
+      }
+    }
+    if (l[u] != ~0u) {
+      a.link[row[u]] = (int32_t)l[u];
+      ++c[JC_MATCHED];
+      const int64_t x = ts[u] - lts[u];  // same process: the offset cancels
+      if (x < 0) ++c[JC_NEG];
+      atomicAdd(&s_h[x <= 0 ? 0 : bits_of((uint64_t)x)], 1ull);
+      a.aux[row[u]] = a.contain ? lop[u] : -1;
+      if (a.contain && lop[u] < 0) ++c[JC_UNATTR];
+      if (single[u]) {
+        a.aux[l[u]] = 1;
+        ++c[JC_MLAUNCH];
+        if (a.contain) {
+          a.lk_first[l[u]] = ts[u] - o;
+          a.lk_last[l[u]] = te[u] - o;
+          a.lk_sum[l[u]] = te[u] - ts[u];
+        }
+      } else {
+        if (atomicAdd(&a.aux[l[u]], 1) == 0) ++c[JC_MLAUNCH];
+        if (a.contain) {
+          atomicMin((long long*)&a.lk_first[l[u]], (long long)(ts[u] - o));
+          atomicMax((long long*)&a.lk_last[l[u]], (long long)(te[u] - o));
+          atomicAdd((unsigned long long*)&a.lk_sum[l[u]], (unsigned long long)(te[u] - ts[u]));
+        }
+      }
+    } else {
+      a.link[row[u]] = -1;
+      a.aux[row[u]] = -1;
+      ++c[JC_UNM_K];
+    }
+  }
+  jt_flush(a, c, s_c, s_h);
+}
+
 __global__ __launch_bounds__(256) void k_edges(JoinArgs a) {
+  if (a.ds->join_direct) {
+    // table path: the kernels' latest end and earliest start per slot
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < a.n_edges; e += (int64_t)gridDim.x * 256) {
+      const herschel_edge ed = a.edges[e];
+      int found[2] = {0, 0};
+      int64_t prod_end = I64MIN, cons_start = I64MAX;
+      for (int side = 0; side < 2; ++side) {
+        const int32_t pid = side == 0 ? ed.prod_pid : ed.cons_pid;
+        const int64_t corr = side == 0 ? ed.prod_corr : ed.cons_corr;
+        if (pid < 0 || pid >= a.P || corr < 0 || corr >= HERSCHEL_CORR_LIMIT) continue;
+        const int64_t rel = corr - a.ds->jt_cmin[pid];
+        const int64_t lim = (pid + 1 < a.P ? a.ds->jt_base[pid + 1] : a.ds->jt_slots) - a.ds->jt_base[pid];
+        if (rel < 0 || rel >= lim) continue;
+        const int64_t slot = a.ds->jt_base[pid] + rel;
+        if (side == 0 && a.kmax[slot] != I64MIN) {
+          found[0] = 1;
+          prod_end = a.kmax[slot];
+        }
+        if (side == 1 && a.kmin[slot] != I64MAX) {
+          found[1] = 1;
+          cons_start = a.kmin[slot];
+        }
+      }
+      a.edge_status[e] = (found[0] ? 0 : 1) | (found[1] ? 0 : 2);
+      a.edge_wait[e] = (found[0] && found[1]) ? (int64_t)((uint64_t)cons_start - (uint64_t)prod_end) : I64MIN;
+    }
+    return;
+  }
   const int64_t n = a.ds->nJ;
   const int par = (int)a.ds->sort_parity[1];
   const uint64_t* keys = a.k[par];
@@ -242,12 +540,33 @@ static JoinArgs join_args(Ctx& c) {
   a.P = c.P;
   a.edge_wait = c.o.edge_wait;
   a.edge_status = c.o.edge_status;
+  a.tab = c.jt_tab;
+  a.own = c.jt_own;
+  a.multi = c.jt_multi;
+  a.kmax = c.jt_kmax;
+  a.kmin = c.jt_kmin;
+  a.cap = c.jt_cap;
   return a;
+}
+
+void launch_join_plan(Ctx& c) {
+  if (c.P > JT_PROCS) return;  // join_direct stays 0: the sort path
+  JoinArgs a = join_args(c);
+  hipLaunchKernelGGL(k_jt_plan, dim3(1), dim3(64), 0, c.st, a);
 }
 
 void launch_join(Ctx& c) {
   JoinArgs a = join_args(c);
   const int64_t grid = std::max<int64_t>(cdiv(c.sJ.n_max, 256), 1);
+  if (c.P <= JT_PROCS) {
+    const int64_t cgrid = std::min<int64_t>(std::max<int64_t>(cdiv(c.jt_cap, 256 * 8), 1), 4096);
+    const int64_t tgrid = std::max<int64_t>(cdiv(c.sJ.n_max, JT_TILE), 1);
+    hipLaunchKernelGGL(k_jt_clear, dim3((unsigned)cgrid), dim3(256), 0, c.st, a);
+    hipLaunchKernelGGL(k_jt_store, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
+    hipLaunchKernelGGL(k_jt_check, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
+    hipLaunchKernelGGL(k_jt_fix, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
+    hipLaunchKernelGGL(k_jt_kernel, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
+  }
   hipLaunchKernelGGL(k_join, dim3((unsigned)grid), dim3(256), 0, c.st, a);
 }
 

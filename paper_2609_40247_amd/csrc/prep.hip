@@ -25,6 +25,7 @@ struct PrepArgs {
   int P, S, T, NN, NOP;
   int sb, tb, wb;
   int64_t n_tiles;
+  bool jt_range;  // find each process's join key range (at most JT_PROCS processes)
   DevState* ds;
   herschel_counters* cnt;
   int32_t* link;
@@ -45,11 +46,13 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
   __shared__ uint32_t s_tot[3];
   __shared__ uint64_t s_base[3];
   __shared__ unsigned long long s_bad;
+  __shared__ unsigned long long s_jr[2 * JT_PROCS];  // per process: max of ~key, max of key
 
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int tile = take_ticket(a.ds, TK_PREP, &s_tile);
   const int64_t base = (int64_t)tile * PREP_TILE;
   if (tid == 0) s_bad = ~0ull;
+  if (tid < 2 * JT_PROCS) s_jr[tid] = 0;
 
   uint64_t kA[PREP_ITEMS], kB[PREP_ITEMS];  // kA: timeline or containment key, kB: join key
   uint32_t fl = 0;                          // per item: bit 3j list K, 3j+1 list C, 3j+2 list J
@@ -109,6 +112,49 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
   }
   if (bad != ~0ull) atomicMin(&s_bad, (unsigned long long)bad);
   __syncthreads();
+  if (a.jt_range) {
+    // each process's smallest and largest join key (the correlation table's
+    // id ranges): a thread's keys of one process are combined in registers,
+    // a wave whose keys all belong to one process combines them by shuffles
+    int tp = -1;
+    uint64_t lo = 0, hi = 0;  // lo: max of ~key
+#pragma unroll
+    for (int j = 0; j < PREP_ITEMS; ++j) {
+      if (!(fl & (4u << (3 * j)))) continue;
+      const int pj = (int)(kB[j] >> 49);
+      if (pj != tp) {
+        if (tp >= 0) {
+          atomicMax(&s_jr[2 * tp], (unsigned long long)lo);
+          atomicMax(&s_jr[2 * tp + 1], (unsigned long long)hi);
+        }
+        tp = pj;
+        lo = ~kB[j];
+        hi = kB[j];
+      } else {
+        lo = ~kB[j] > lo ? ~kB[j] : lo;
+        hi = kB[j] > hi ? kB[j] : hi;
+      }
+    }
+    int pm = tp;
+    for (int d = 1; d < WAVE; d <<= 1) {
+      const int o = __shfl_xor(pm, d, WAVE);
+      pm = o > pm ? o : pm;
+    }
+    if (pm >= 0 && ballot(tp >= 0 && tp != pm) == 0) {
+      for (int d = 1; d < WAVE; d <<= 1) {
+        const uint64_t ol = shfl_xor(lo, d), oh = shfl_xor(hi, d);
+        lo = ol > lo ? ol : lo;
+        hi = oh > hi ? oh : hi;
+      }
+      if (lane == 0) {
+        atomicMax(&s_jr[2 * pm], (unsigned long long)lo);
+        atomicMax(&s_jr[2 * pm + 1], (unsigned long long)hi);
+      }
+    } else if (tp >= 0) {
+      atomicMax(&s_jr[2 * tp], (unsigned long long)lo);
+      atomicMax(&s_jr[2 * tp + 1], (unsigned long long)hi);
+    }
+  }
   if (tid < 3) {
     uint32_t run = 0;
     for (int j = 0; j < PREP_ITEMS; ++j)
@@ -120,6 +166,10 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
   }
   if (tid == 0 && s_bad != ~0ull) atomicMin((unsigned long long*)&a.ds->first_invalid, s_bad);
   __syncthreads();
+  if (a.jt_range && tid < 2 * JT_PROCS && s_jr[tid]) {
+    unsigned long long* dst = (unsigned long long*)(tid & 1 ? &a.ds->jt_key_hi[tid >> 1] : &a.ds->jt_key_lo[tid >> 1]);
+    atomicMax(dst, s_jr[tid]);
+  }
   if (wv < 3) {
     const uint64_t ex = wave_lookback<OpSum>(a.status + (int64_t)wv * a.n_tiles, tile, s_tot[wv], a.ds);
     if (lane == 0) s_base[wv] = ex;
@@ -182,6 +232,7 @@ void launch_prep(Ctx& c) {
   a.tb = c.tb;
   a.wb = c.wb;
   a.n_tiles = c.prep_tiles;
+  a.jt_range = c.P <= JT_PROCS;
   a.ds = c.ds;
   a.cnt = c.o.counters;
   a.link = c.o.link;

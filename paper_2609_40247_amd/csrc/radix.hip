@@ -80,12 +80,9 @@ __device__ void hist_range(uint32_t* h, const uint64_t* __restrict__ keys, int64
   }
 }
 
-__device__ __forceinline__ int hist_blocks(int64_t n) {
-  return (int)min<int64_t>(max<int64_t>(cdiv(n, HIST_CHUNK), 1), HIST_MAX_BLOCKS);
-}
-
-__global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs) {
+__global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, const DevState* ds) {
   const HistJob jb = jobs.j[blockIdx.y];
+  if (jb.id == 1 && ds->join_direct) return;  // the correlation table replaces the join sort
   const int nd = jb.nd, nbins = nd * 256;
   __shared__ uint32_t h[8 * 256];
   const int64_t n = *jb.count;
@@ -118,7 +115,7 @@ __global__ __launch_bounds__(256) void k_hist_plan(HistJobs jobs, DevState* ds) 
   __shared__ uint32_t s_scan[256 / WAVE + 1];
   const HistJob jb = jobs.j[blockIdx.y];
   const int d = blockIdx.x;
-  if (d >= jb.nd) return;
+  if (d >= jb.nd || (jb.id == 1 && ds->join_direct)) return;
   const int64_t n = *jb.count;
   const int nblk = hist_blocks(n);
   const uint32_t* src = jobs.part + (int64_t)jb.id * HIST_MAX_BLOCKS * 8 * 256 + d * 256 + threadIdx.x;
@@ -356,7 +353,7 @@ void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
   }
   if (m == 0) return;
   const int64_t grid = std::min<int64_t>(cdiv(n_max, HIST_CHUNK), HIST_MAX_BLOCKS);
-  hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid, (unsigned)m), dim3(HIST_THREADS), 0, c.st, jobs);
+  hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid, (unsigned)m), dim3(HIST_THREADS), 0, c.st, jobs, c.ds);
   hipLaunchKernelGGL(k_hist_plan, dim3((unsigned)nd, (unsigned)m), dim3(256), 0, c.st, jobs, c.ds);
 }
 
