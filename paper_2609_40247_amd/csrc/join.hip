@@ -559,6 +559,7 @@ void launch_join(Ctx& c) {
   JoinArgs a = join_args(c);
   const int64_t grid = std::max<int64_t>(cdiv(c.sJ.n_max, 256), 1);
   if (c.P <= JT_PROCS) {
+    // the sort join below is a no-op when the table does the join
     const int64_t cgrid = std::min<int64_t>(std::max<int64_t>(cdiv(c.jt_cap, 256 * 8), 1), 4096);
     const int64_t tgrid = std::max<int64_t>(cdiv(c.sJ.n_max, JT_TILE), 1);
     hipLaunchKernelGGL(k_jt_clear, dim3((unsigned)cgrid), dim3(256), 0, c.st, a);

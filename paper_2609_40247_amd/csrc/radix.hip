@@ -39,8 +39,10 @@ constexpr int HIST_THREADS = 1024;
 // (nanoseconds, correlation ids) differ across a wave, so every lane adds;
 // for higher digits, when the whole wave agrees, one lane adds the count.
 template <int ND>
-__device__ __forceinline__ void hist_add(uint32_t* h, uint64_t k, uint32_t nact, bool leader) {
+__device__ __forceinline__ void hist_add(uint32_t* h, uint64_t k) {
   const uint32_t lo = (uint32_t)k, hi = (uint32_t)(k >> 32);
+  const uint64_t active = ballot(true);
+  const bool leader = lane_id() == __ffsll((unsigned long long)active) - 1;
 #pragma unroll
   for (int d = 0; d < ND; ++d) {
     const uint32_t dg = ((d < 4 ? lo : hi) >> (8 * (d & 3))) & 255u;
@@ -49,7 +51,7 @@ __device__ __forceinline__ void hist_add(uint32_t* h, uint64_t k, uint32_t nact,
     } else {
       const uint32_t d0 = __builtin_amdgcn_readfirstlane(dg);
       if (ballot(dg != d0) == 0) {
-        if (leader) atomicAdd(&h[d * 256 + d0], nact);
+        if (leader) atomicAdd(&h[d * 256 + d0], (uint32_t)popc(active));
       } else {
         atomicAdd(&h[d * 256 + dg], 1u);
       }
@@ -59,25 +61,16 @@ __device__ __forceinline__ void hist_add(uint32_t* h, uint64_t k, uint32_t nact,
 
 template <int ND>
 __device__ void hist_range(uint32_t* h, const uint64_t* __restrict__ keys, int64_t lo, int64_t hi) {
-  const int lane = lane_id();
   constexpr int U = 8;  // loads in flight per thread
   int64_t i = lo + threadIdx.x;
   for (; i + (U - 1) * HIST_THREADS < hi; i += U * HIST_THREADS) {
     uint64_t k[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) k[u] = keys[i + u * HIST_THREADS];
-    const uint64_t active = ballot(true);
-    const bool leader = lane == __ffsll((unsigned long long)active) - 1;
-    const uint32_t nact = (uint32_t)popc(active);
 #pragma unroll
-    for (int u = 0; u < U; ++u) hist_add<ND>(h, k[u], nact, leader);
+    for (int u = 0; u < U; ++u) hist_add<ND>(h, k[u]);
   }
-  for (; i < hi; i += HIST_THREADS) {
-    const uint64_t k = keys[i];
-    const uint64_t active = ballot(true);
-    const bool leader = lane == __ffsll((unsigned long long)active) - 1;
-    hist_add<ND>(h, k, (uint32_t)popc(active), leader);
-  }
+  for (; i < hi; i += HIST_THREADS) hist_add<ND>(h, keys[i]);
 }
 
 __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, const DevState* ds) {

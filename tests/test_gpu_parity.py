@@ -184,6 +184,23 @@ def test_64_streams_overlap(H):
     check(H, tr.columns(), p, "64 streams")
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_sparse_correlation_ids(H, seed):
+    """The same traces with every correlation id spread by 2^30: no id table
+    fits them, so the join sorts instead; results must match the oracle (and
+    the dense version's structure: the join only compares ids)."""
+    tr = synth.random_small(seed=9100 + seed, n_rows=3000, window=4000, n_procs=3, n_streams=4, n_threads=3,
+                            corr_range=300, edges=40)
+    cols = tr.columns()
+    cols["corr"] = cols["corr"] << 30
+    p = dict(tr.params)
+    e = p["edges"].copy()
+    e["prod_corr"] = e["prod_corr"] << 30
+    e["cons_corr"] = e["cons_corr"] << 30
+    p["edges"] = e
+    check(H, cols, p, f"sparse corr seed {seed}")
+
+
 def test_4096_processes(H):
     tr = synth.random_small(seed=78, n_rows=20_000, window=5_000, n_procs=4096, n_streams=3, n_threads=2,
                             corr_range=50)
