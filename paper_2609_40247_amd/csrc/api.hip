@@ -2,6 +2,8 @@
 // of the stages on the caller's stream, and the return code.
 #include <string.h>
 
+#include <mutex>
+
 #include "internal.hpp"
 
 namespace hx {
@@ -322,12 +324,44 @@ static inline void stage_end(Ctx& c, int s) {
   if (s == g_stage && g_ev1) (void)hipEventRecord(g_ev1, c.st);
 }
 
+// After the sorts three chains are independent and each is latency-bound,
+// so they run side by side: the timeline, overlap and name tables on one
+// library stream, the join on another, containment on the caller's stream,
+// which then waits for both.  The library's streams and events are created
+// once per device (default priority); enqueueing is serialised so that
+// concurrent callers cannot interleave their event records.
+struct DeviceStreams {
+  hipStream_t s[2] = {nullptr, nullptr};
+  hipEvent_t e[4] = {nullptr, nullptr, nullptr, nullptr};  // sorts, timeline chain, join, prep done
+  bool ok = false;
+};
+static std::mutex g_enqueue_mutex;
+static DeviceStreams g_dev_streams[64];
+
+static DeviceStreams* device_streams() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  DeviceStreams& d = g_dev_streams[dev];
+  if (!d.ok) {
+    for (auto& st : d.s)
+      if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    for (auto& ev : d.e)
+      if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return nullptr;
+    d.ok = true;
+  }
+  return &d;
+}
+
 static int enqueue(Ctx& c) {
+  std::lock_guard<std::mutex> lock(g_enqueue_mutex);
   static bool lds_attr = false;
   if (!lds_attr) {
     names_set_lds_attr();
     lds_attr = true;
   }
+  DeviceStreams* dsx = device_streams();
+  if (!dsx) return HERSCHEL_EDEVICE;
+  const hipStream_t s0 = c.st;
   stage_begin(c, HERSCHEL_STAGE_INIT);
   launch_init(c);
   stage_end(c, HERSCHEL_STAGE_INIT);
@@ -335,6 +369,16 @@ static int enqueue(Ctx& c) {
   launch_prep(c);
   launch_join_plan(c);
   stage_end(c, HERSCHEL_STAGE_PREP);
+  (void)hipEventRecord(dsx->e[3], s0);
+
+  // chain 2 starts here: the correlation-table join needs only prep's lists
+  c.st = dsx->s[1];
+  (void)hipStreamWaitEvent(c.st, dsx->e[3], 0);
+  stage_begin(c, HERSCHEL_STAGE_JOIN);
+  launch_join_table(c);
+  stage_end(c, HERSCHEL_STAGE_JOIN);
+  c.st = s0;
+
   stage_begin(c, HERSCHEL_STAGE_HIST);
   {
     SortBufs* ss[3] = {&c.sK, &c.sJ, &c.sC};
@@ -342,9 +386,6 @@ static int enqueue(Ctx& c) {
     launch_hist_multi(c, ss, cc, c.contain ? 3 : 2);
   }
   stage_end(c, HERSCHEL_STAGE_HIST);
-  stage_begin(c, HERSCHEL_STAGE_NAMES);
-  launch_names(c);
-  stage_end(c, HERSCHEL_STAGE_NAMES);
   stage_begin(c, HERSCHEL_STAGE_SORT);
   {
     SortBufs* ss[3] = {&c.sK, &c.sJ, &c.sC};
@@ -352,12 +393,35 @@ static int enqueue(Ctx& c) {
     launch_sort_multi(c, ss, cc, c.contain ? 3 : 2);
   }
   stage_end(c, HERSCHEL_STAGE_SORT);
+  (void)hipEventRecord(dsx->e[0], s0);
+
+  // chain 1: timeline, overlap, per-name tables
+  c.st = dsx->s[0];
+  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
   stage_begin(c, HERSCHEL_STAGE_TIMELINE);
   launch_timeline(c);
   stage_end(c, HERSCHEL_STAGE_TIMELINE);
   stage_begin(c, HERSCHEL_STAGE_OVERLAP);
   if (c.overlap) launch_overlap(c);
   stage_end(c, HERSCHEL_STAGE_OVERLAP);
+  stage_begin(c, HERSCHEL_STAGE_NAMES);
+  launch_names(c);
+  launch_names_reduce(c);
+  stage_end(c, HERSCHEL_STAGE_NAMES);
+  (void)hipEventRecord(dsx->e[1], c.st);
+
+  // chain 2 continued: the sort-merge join (when the table was not used)
+  // and the dependency waits
+  c.st = dsx->s[1];
+  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
+  launch_join(c);
+  stage_begin(c, HERSCHEL_STAGE_EDGES);
+  launch_edges(c);
+  stage_end(c, HERSCHEL_STAGE_EDGES);
+  (void)hipEventRecord(dsx->e[2], c.st);
+
+  // chain 3 on the caller's stream: containment, then what needs the join
+  c.st = s0;
   if (c.contain) {
     stage_begin(c, HERSCHEL_STAGE_CONTAIN);
     launch_contain(c);
@@ -366,17 +430,15 @@ static int enqueue(Ctx& c) {
     const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.n, 256 * 8), 1), 2048);
     hipLaunchKernelGGL(k_nocontain, dim3(grid), dim3(256), 0, c.st, c.sC.k[0], c.sC.v[0], c.ds, c.o.link, c.o.aux);
   }
-  stage_begin(c, HERSCHEL_STAGE_JOIN);
-  launch_join(c);
-  stage_end(c, HERSCHEL_STAGE_JOIN);
+  (void)hipStreamWaitEvent(c.st, dsx->e[2], 0);
   stage_begin(c, HERSCHEL_STAGE_OPAGG);
-  if (c.contain) launch_opagg(c);
+  if (c.contain) {
+    launch_join_ops(c);
+    launch_opagg(c);
+  }
   stage_end(c, HERSCHEL_STAGE_OPAGG);
-  stage_begin(c, HERSCHEL_STAGE_EDGES);
-  launch_edges(c);
-  stage_end(c, HERSCHEL_STAGE_EDGES);
+  (void)hipStreamWaitEvent(c.st, dsx->e[1], 0);
   stage_begin(c, HERSCHEL_STAGE_FINAL);
-  launch_names_reduce(c);
   launch_finalize(c);
   stage_end(c, HERSCHEL_STAGE_FINAL);
   return hipGetLastError() == hipSuccess ? HERSCHEL_OK : HERSCHEL_EDEVICE;

@@ -88,6 +88,8 @@ void launch_opagg(Ctx& c);
 void launch_names_reduce(Ctx& c);
 void launch_join(Ctx& c);
 void launch_join_plan(Ctx& c);
+void launch_join_ops(Ctx& c);
+void launch_join_table(Ctx& c);
 void launch_edges(Ctx& c);
 void launch_finalize(Ctx& c);
 

@@ -173,13 +173,7 @@ __global__ __launch_bounds__(256) void k_join(JoinArgs a) {
         if (x < 0) ++c[JC_NEG];
         const int bin = x <= 0 ? 0 : bits_of((uint64_t)x);
         atomicAdd(&s_h[bin], 1ull);
-        if (a.contain) {
-          const int32_t op = a.link[lrow];
-          a.aux[row] = op;
-          if (op < 0) ++c[JC_UNATTR];
-        } else {
-          a.aux[row] = -1;
-        }
+        a.aux[row] = -1;  // the kernel's op comes later (k_join_ops)
       } else {
         a.link[row] = -1;
         a.aux[row] = -1;
@@ -394,15 +388,10 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
     ts[u] = kern ? a.ts[row[u]] : 0;
     te[u] = kern ? a.te[row[u]] : 0;
   }
-  // round 3: the launch's start and op
+  // round 3: the launch's start
   int64_t lts[JT_ITEMS];
-  int32_t lop[JT_ITEMS];
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
-    const bool m = (key[u] & 1) && l[u] != ~0u;
-    lts[u] = m ? a.ts[l[u]] : 0;
-    lop[u] = m && a.contain ? a.link[l[u]] : -1;
-  }
+  for (int u = 0; u < JT_ITEMS; ++u) lts[u] = (key[u] & 1) && l[u] != ~0u ? a.ts[l[u]] : 0;
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
     if (!(key[u] & 1)) continue;
@@ -422,8 +411,7 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
       const int64_t x = ts[u] - lts[u];  // same process: the offset cancels
       if (x < 0) ++c[JC_NEG];
       atomicAdd(&s_h[x <= 0 ? 0 : bits_of((uint64_t)x)], 1ull);
-      a.aux[row[u]] = a.contain ? lop[u] : -1;
-      if (a.contain && lop[u] < 0) ++c[JC_UNATTR];
+      a.aux[row[u]] = -1;  // the kernel's op comes later (k_join_ops)
       if (single[u]) {
         a.aux[l[u]] = 1;
         ++c[JC_MLAUNCH];
@@ -447,6 +435,38 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
     }
   }
   jt_flush(a, c, s_c, s_h);
+}
+
+// Kernel -> op: the op of the kernel's launch (containment and the join run
+// concurrently; this pass follows both).  Counts matched kernels whose launch
+// has no op.
+__global__ __launch_bounds__(256) void k_join_ops(JoinArgs a) {
+  __shared__ unsigned long long s_c[JC_N];
+  const int tid = threadIdx.x;
+  if (tid < JC_N) s_c[tid] = 0;
+  __syncthreads();
+  const int64_t n = a.ds->nJ;
+  const int par = (int)a.ds->sort_parity[1];
+  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + tid;
+  uint32_t c[JC_N] = {};
+  uint32_t row[JT_ITEMS];
+  int32_t l[JT_ITEMS];
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    const int64_t i = i0 + u * 256;
+    const bool kern = i < n && (a.k[par][i] & 1);
+    row[u] = kern ? a.v[par][i] : ~0u;
+  }
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) l[u] = row[u] != ~0u ? a.link[row[u]] : -1;
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    if (l[u] < 0) continue;
+    const int32_t op = a.link[l[u]];
+    a.aux[row[u]] = op;
+    if (op < 0) ++c[JC_UNATTR];
+  }
+  jt_flush(a, c, s_c, nullptr);
 }
 
 __global__ __launch_bounds__(256) void k_edges(JoinArgs a) {
@@ -555,20 +575,31 @@ void launch_join_plan(Ctx& c) {
   hipLaunchKernelGGL(k_jt_plan, dim3(1), dim3(64), 0, c.st, a);
 }
 
+// The correlation-table join (no-ops unless the plan chose it); it needs only
+// prep's lists, so it can run beside the sorts.
+void launch_join_table(Ctx& c) {
+  if (c.P > JT_PROCS) return;
+  JoinArgs a = join_args(c);
+  const int64_t cgrid = std::min<int64_t>(std::max<int64_t>(cdiv(c.jt_cap, 256 * 8), 1), 4096);
+  const int64_t tgrid = std::max<int64_t>(cdiv(c.sJ.n_max, JT_TILE), 1);
+  hipLaunchKernelGGL(k_jt_clear, dim3((unsigned)cgrid), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_store, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_check, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_fix, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_kernel, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
+}
+
+// The sort-merge join (a no-op when the table did the join); after the sorts.
 void launch_join(Ctx& c) {
   JoinArgs a = join_args(c);
   const int64_t grid = std::max<int64_t>(cdiv(c.sJ.n_max, 256), 1);
-  if (c.P <= JT_PROCS) {
-    // the sort join below is a no-op when the table does the join
-    const int64_t cgrid = std::min<int64_t>(std::max<int64_t>(cdiv(c.jt_cap, 256 * 8), 1), 4096);
-    const int64_t tgrid = std::max<int64_t>(cdiv(c.sJ.n_max, JT_TILE), 1);
-    hipLaunchKernelGGL(k_jt_clear, dim3((unsigned)cgrid), dim3(256), 0, c.st, a);
-    hipLaunchKernelGGL(k_jt_store, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
-    hipLaunchKernelGGL(k_jt_check, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
-    hipLaunchKernelGGL(k_jt_fix, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
-    hipLaunchKernelGGL(k_jt_kernel, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
-  }
   hipLaunchKernelGGL(k_join, dim3((unsigned)grid), dim3(256), 0, c.st, a);
+}
+
+void launch_join_ops(Ctx& c) {
+  JoinArgs a = join_args(c);
+  const int64_t grid = std::max<int64_t>(cdiv(c.sJ.n_max, JT_TILE), 1);
+  hipLaunchKernelGGL(k_join_ops, dim3((unsigned)grid), dim3(256), 0, c.st, a);
 }
 
 void launch_edges(Ctx& c) {
