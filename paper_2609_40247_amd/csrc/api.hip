@@ -63,6 +63,13 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
     c.vb_status = b.take<uint64_t>(c.vb_tiles);
     c.sC.status = b.take<uint32_t>((int64_t)c.sC.nd * c.sC.tiles_max * 256);
+    // pyramid levels above the tile maxima: built by atomic maxima, from zero
+    c.nlev = 3;
+    while (cdiv(n, (int64_t)1 << (6 * (c.nlev - 1))) > 64) ++c.nlev;
+    for (int l = 3; l < c.nlev; ++l) {
+      c.Mn[l] = cdiv(n, (int64_t)1 << (6 * l));
+      c.M[l] = b.take<uint64_t>(c.Mn[l]);
+    }
   }
   c.zero_bytes = align_up(b.off - z0);
   c.hist_part = b.take<uint32_t>((int64_t)N_SORTS * HIST_MAX_BLOCKS * 8 * 256);
@@ -98,11 +105,9 @@ size_t layout_workspace(Ctx& c, char* base) {
   }
   if (c.contain) {
     c.V = b.take<uint64_t>(n);
-    c.nlev = 3;
-    while (cdiv(n, (int64_t)1 << (6 * (c.nlev - 1))) > 64) ++c.nlev;
     c.M[0] = nullptr;
     c.Mn[0] = n;
-    for (int l = 1; l < c.nlev; ++l) {
+    for (int l = 1; l < 3; ++l) {
       c.Mn[l] = cdiv(n, (int64_t)1 << (6 * l));
       c.M[l] = b.take<uint64_t>(c.Mn[l]);
     }

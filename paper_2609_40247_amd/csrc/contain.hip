@@ -169,9 +169,18 @@ __global__ __launch_bounds__(256) void k_tiefix_long(ContainArgs a) {
 }
 
 // ------------------------------------------------------- encoding, pyramid
-__global__ __launch_bounds__(CT_THREADS) void k_vbuild(ContainArgs a) {
+// V and the first pyramid levels of one 4096-position tile: 16 waves, each
+// wave four 64-position groups (one M1 entry each), every round of loads
+// (keys, rows, end times) issued for all four groups together.  The tile
+// maximum is M2; the levels above it take atomic maxima (they start at
+// zero); the exclusive prefix maximum over earlier tiles comes from a
+// decoupled look-back.
+constexpr int VB_THREADS = 1024;
+constexpr int VB_ITEMS = CT_TILE / VB_THREADS;
+
+__global__ __launch_bounds__(VB_THREADS) void k_vbuild(ContainArgs a) {
   __shared__ int s_tile;
-  __shared__ uint64_t s_w[CT_THREADS / WAVE];
+  __shared__ uint64_t s_w[VB_THREADS / WAVE];
   __shared__ uint64_t s_tmax;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int64_t n = a.ds->nCL;
@@ -181,24 +190,34 @@ __global__ __launch_bounds__(CT_THREADS) void k_vbuild(ContainArgs a) {
   if ((int64_t)blockIdx.x * CT_TILE >= n) return;  // no tile: stay off the ticket counter
   const int tile = take_ticket(a.ds, TK_VBUILD, &s_tile);
   const int64_t base = (int64_t)tile * CT_TILE;
-  // striped: item j of lane covers position base + wv*1024 + j*64 + lane, so
-  // a wave's 64 lanes form one 64-group of the pyramid
+  // item j of lane covers position base + wv*256 + j*64 + lane
+  uint64_t key[VB_ITEMS];
+  uint32_t row[VB_ITEMS];
+  int64_t te[VB_ITEMS];
+#pragma unroll
+  for (int j = 0; j < VB_ITEMS; ++j) {
+    const int64_t p = base + (int64_t)wv * (VB_ITEMS * WAVE) + j * WAVE + lane;
+    key[j] = p < n ? keys[p] : 0ull;
+  }
+#pragma unroll
+  for (int j = 0; j < VB_ITEMS; ++j) {
+    const int64_t p = base + (int64_t)wv * (VB_ITEMS * WAVE) + j * WAVE + lane;
+    row[j] = p < n && key_is_op(key[j]) ? vals[p] : ~0u;
+  }
+#pragma unroll
+  for (int j = 0; j < VB_ITEMS; ++j) te[j] = row[j] != ~0u ? a.te[row[j]] : 0;
   uint64_t wmax = 0;
-#pragma unroll 4
-  for (int j = 0; j < CT_ITEMS; ++j) {
-    const int64_t p = base + (int64_t)wv * (CT_ITEMS * WAVE) + j * WAVE + lane;
+#pragma unroll
+  for (int j = 0; j < VB_ITEMS; ++j) {
+    const int64_t p = base + (int64_t)wv * (VB_ITEMS * WAVE) + j * WAVE + lane;
     uint64_t v = 0;
-    if (p < n) {
-      const uint64_t key = keys[p];
-      if (key_is_op(key)) {
-        const uint32_t row = vals[p];
-        const int32_t pid = key_pid(a, key);
-        const int64_t tec = a.te[row] - (a.off ? a.off[pid] : 0);
-        const int64_t e = tec >= a.W1 ? a.W : tec - a.W0;
-        v = (key_seg(a, key) << a.vb) | (uint64_t)(e + 1);
-      }
-      a.V[p] = v;
+    if (row[j] != ~0u) {
+      const int32_t pid = key_pid(a, key[j]);
+      const int64_t tec = te[j] - (a.off ? a.off[pid] : 0);
+      const int64_t e = tec >= a.W1 ? a.W : tec - a.W0;
+      v = (key_seg(a, key[j]) << a.vb) | (uint64_t)(e + 1);
     }
+    if (p < n) a.V[p] = v;
     const uint64_t g = wave_max_u64(v);
     if (lane == 0 && p - lane < n) a.M[1][(p - lane) >> 6] = g;
     wmax = g > wmax ? g : wmax;
@@ -207,31 +226,16 @@ __global__ __launch_bounds__(CT_THREADS) void k_vbuild(ContainArgs a) {
   __syncthreads();
   if (tid == 0) {
     uint64_t t = 0;
-    for (int w = 0; w < CT_THREADS / WAVE; ++w) t = s_w[w] > t ? s_w[w] : t;
+    for (int w = 0; w < VB_THREADS / WAVE; ++w) t = s_w[w] > t ? s_w[w] : t;
     s_tmax = t;
     a.M[2][tile] = t;
+    for (int l = 3; l < a.nlev; ++l)
+      if (t) atomicMax((unsigned long long*)&a.M[l][tile >> (6 * (l - 2))], (unsigned long long)t);
   }
   __syncthreads();
   if (wv == 0) {
     const uint64_t ex = wave_lookback<OpMax>(a.vb_status, tile, s_tmax, a.ds);
     if (lane == 0) a.pmt[tile] = ex;
-  }
-}
-
-// Levels 3 and up of the pyramid, from level 2 (one workgroup).
-__global__ __launch_bounds__(1024) void k_vlevels(ContainArgs a) {
-  const int64_t n = a.ds->nCL;
-  int64_t cnt = cdiv(n, CT_TILE);  // live level-2 entries
-  for (int l = 3; l < a.nlev; ++l) {
-    const int64_t out = cdiv(cnt, 64);
-    for (int64_t i = threadIdx.x; i < out; i += 1024) {
-      uint64_t m = 0;
-      const int64_t hi = min(cnt, (i + 1) * 64);
-      for (int64_t j = i * 64; j < hi; ++j) m = a.M[l - 1][j] > m ? a.M[l - 1][j] : m;
-      a.M[l][i] = m;
-    }
-    __syncthreads();
-    cnt = out;
   }
 }
 
@@ -434,7 +438,11 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
   }
 }
 
-// Depth by walking the parents; improper nesting; op aggregates reset.
+// Depth by walking the parents; improper nesting; op aggregates reset.  Each
+// thread walks DP_ITEMS positions' parent chains side by side, so the loads
+// of one step of all chains are in flight together.
+constexpr int DP_ITEMS = 4;
+
 __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
   __shared__ unsigned long long s_imp;
   if (threadIdx.x == 0) s_imp = 0;
@@ -443,22 +451,47 @@ __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
   const int par = (int)a.ds->sort_parity[2];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
+  const int64_t p0 = (int64_t)blockIdx.x * 256 * DP_ITEMS + threadIdx.x;
+  uint32_t row[DP_ITEMS];
+  int64_t q[DP_ITEMS];
+#pragma unroll
+  for (int u = 0; u < DP_ITEMS; ++u) {
+    const int64_t p = p0 + u * 256;
+    const bool op = p < n && key_is_op(keys[p]);
+    row[u] = op ? vals[p] : ~0u;
+    q[u] = op ? a.par[p] : -1;
+  }
+  // improper nesting: the op ends after its parent
   uint32_t imp = 0;
-  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < n; p += (int64_t)gridDim.x * 256) {
-    if (!key_is_op(keys[p])) continue;
-    const uint32_t row = vals[p];
-    int32_t d = 0;
-    int64_t q = a.par[p];
-    if (q >= 0 && a.te[row] > a.te[vals[q]]) ++imp;  // same process: raw ends compare like corrected
-    while (q >= 0 && in_range(a.ds, q, n)) {
-      ++d;
-      q = a.par[q];
+  uint32_t prow[DP_ITEMS];
+#pragma unroll
+  for (int u = 0; u < DP_ITEMS; ++u) prow[u] = q[u] >= 0 ? vals[q[u]] : ~0u;
+#pragma unroll
+  for (int u = 0; u < DP_ITEMS; ++u)
+    if (prow[u] != ~0u && a.te[row[u]] > a.te[prow[u]]) ++imp;  // one process: raw ends compare like corrected
+  int32_t d[DP_ITEMS];
+#pragma unroll
+  for (int u = 0; u < DP_ITEMS; ++u) d[u] = 0;
+  for (;;) {
+    bool any = false;
+#pragma unroll
+    for (int u = 0; u < DP_ITEMS; ++u) {
+      if (q[u] >= 0 && in_range(a.ds, q[u], n)) {
+        ++d[u];
+        q[u] = a.par[q[u]];
+        any = true;
+      }
     }
-    a.aux[row] = d;
-    a.op_nkern[row] = 0;
-    a.op_first[row] = I64MAX;
-    a.op_last[row] = I64MIN;
-    a.op_ksum[row] = 0;
+    if (!any) break;
+  }
+#pragma unroll
+  for (int u = 0; u < DP_ITEMS; ++u) {
+    if (row[u] == ~0u) continue;
+    a.aux[row[u]] = d[u];
+    a.op_nkern[row[u]] = 0;
+    a.op_first[row[u]] = I64MAX;
+    a.op_last[row[u]] = I64MIN;
+    a.op_ksum[row[u]] = 0;
   }
   const uint64_t w = wave_sum_u64(imp);
   if (lane_id() == 0 && w) atomicAdd(&s_imp, (unsigned long long)w);
@@ -652,10 +685,10 @@ void launch_contain(Ctx& c) {
   const int grid_stride = (int)std::max<int64_t>(cdiv(c.sC.n_max, 256), 1);
   hipLaunchKernelGGL(k_tiefix, dim3(grid_stride), dim3(256), 0, c.st, a);
   hipLaunchKernelGGL(k_tiefix_long, dim3(64), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_vbuild, dim3((unsigned)tiles), dim3(CT_THREADS), 0, c.st, a);
-  if (c.nlev > 3) hipLaunchKernelGGL(k_vlevels, dim3(1), dim3(1024), 0, c.st, a);
+  hipLaunchKernelGGL(k_vbuild, dim3((unsigned)tiles), dim3(VB_THREADS), 0, c.st, a);
   hipLaunchKernelGGL(k_query, dim3((unsigned)tiles), dim3(QY_THREADS), 0, c.st, a);
-  hipLaunchKernelGGL(k_depth, dim3(grid_stride), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_depth, dim3((unsigned)std::max<int64_t>(cdiv(c.sC.n_max, 256 * DP_ITEMS), 1)), dim3(256), 0,
+                     c.st, a);
 }
 
 void launch_opagg(Ctx& c) {
