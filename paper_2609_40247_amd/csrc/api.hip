@@ -73,6 +73,7 @@ size_t layout_workspace(Ctx& c, char* base) {
   }
   c.zero_bytes = align_up(b.off - z0);
   c.hist_part = b.take<uint32_t>((int64_t)N_SORTS * HIST_MAX_BLOCKS * 8 * 256);
+  c.k_rows = b.take<uint32_t>(n);
   if (c.P <= JT_PROCS) {
     // correlation table of the join: two slots per row bound every id range it accepts
     c.jt_cap = 2 * n;
@@ -376,12 +377,17 @@ static int enqueue(Ctx& c) {
   stage_end(c, HERSCHEL_STAGE_PREP);
   (void)hipEventRecord(dsx->e[3], s0);
 
-  // chain 2 starts here: the correlation-table join needs only prep's lists
+  // chain 2 starts here: the correlation-table join and the per-name tables
+  // need only prep's lists
   c.st = dsx->s[1];
   (void)hipStreamWaitEvent(c.st, dsx->e[3], 0);
   stage_begin(c, HERSCHEL_STAGE_JOIN);
   launch_join_table(c);
   stage_end(c, HERSCHEL_STAGE_JOIN);
+  stage_begin(c, HERSCHEL_STAGE_NAMES);
+  launch_names(c);
+  launch_names_reduce(c);
+  stage_end(c, HERSCHEL_STAGE_NAMES);
   c.st = s0;
 
   stage_begin(c, HERSCHEL_STAGE_HIST);
@@ -400,7 +406,7 @@ static int enqueue(Ctx& c) {
   stage_end(c, HERSCHEL_STAGE_SORT);
   (void)hipEventRecord(dsx->e[0], s0);
 
-  // chain 1: timeline, overlap, per-name tables
+  // chain 1: timeline and overlap
   c.st = dsx->s[0];
   (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
   stage_begin(c, HERSCHEL_STAGE_TIMELINE);
@@ -409,10 +415,6 @@ static int enqueue(Ctx& c) {
   stage_begin(c, HERSCHEL_STAGE_OVERLAP);
   if (c.overlap) launch_overlap(c);
   stage_end(c, HERSCHEL_STAGE_OVERLAP);
-  stage_begin(c, HERSCHEL_STAGE_NAMES);
-  launch_names(c);
-  launch_names_reduce(c);
-  stage_end(c, HERSCHEL_STAGE_NAMES);
   (void)hipEventRecord(dsx->e[1], c.st);
 
   // chain 2 continued: the sort-merge join (when the table was not used)

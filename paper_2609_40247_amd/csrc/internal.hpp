@@ -43,6 +43,7 @@ struct Ctx {
   int64_t vb_tiles = 0;
   int64_t* corr_min = nullptr;       // [P]
   SortBufs sK, sJ, sC;               // timeline, join, containment
+  uint32_t* k_rows = nullptr;        // [n] admitted kernels' rows in row order (per-name tables)
   uint32_t* hist_part = nullptr;     // [N_SORTS][HIST_MAX_BLOCKS][8 * 256] per-workgroup digit counts
   uint32_t* jt_tab = nullptr;        // [jt_cap] smallest launch row per correlation slot
   uint32_t* jt_own = nullptr;        // [jt_cap] one kernel row per slot

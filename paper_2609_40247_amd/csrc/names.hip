@@ -17,7 +17,7 @@ constexpr int NM_LDS_NAMES = 4096;  // 128 KB of LDS
 constexpr int NM_BATCH = 8;
 
 struct NamesArgs {
-  const uint32_t* rows[2];  // admitted kernels: the timeline sort's two buffers
+  const uint32_t* rows;  // admitted kernels' rows (prep's own copy: the sorts reuse their buffers)
   const int32_t* name;
   const int64_t* ts;
   const int64_t* te;
@@ -45,7 +45,7 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
     __syncthreads();
   }
   const int64_t n = a.ds->nK;
-  const uint32_t* rows = a.rows[a.ds->sort_parity[0]];  // the sorted list (any order would do)
+  const uint32_t* rows = a.rows;
   // NM_BATCH kernels per thread and round, their loads issued together
   const int64_t stride = (int64_t)gridDim.x * NM_THREADS;
   for (int64_t i0 = (int64_t)blockIdx.x * NM_THREADS + tid; i0 < n; i0 += NM_BATCH * stride) {
@@ -113,8 +113,7 @@ __global__ __launch_bounds__(256) void k_names_reduce(NamesArgs a) {
 
 static NamesArgs names_args(Ctx& c) {
   NamesArgs a;
-  a.rows[0] = c.sK.v[0];
-  a.rows[1] = c.sK.v[1];
+  a.rows = c.k_rows;
   a.name = c.ev.name;
   a.ts = c.ev.ts;
   a.te = c.ev.te;

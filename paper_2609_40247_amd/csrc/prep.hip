@@ -33,6 +33,7 @@ struct PrepArgs {
   uint64_t* status;  // [3][n_tiles]
   uint64_t* kK;
   uint32_t* vK;
+  uint32_t* kRows;  // the admitted kernels' rows again, for the per-name tables (not sorted)
   uint64_t* kC;
   uint32_t* vC;
   uint64_t* kJ;
@@ -196,6 +197,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
       if (in_range(a.ds, (int64_t)pos, a.n)) {
         a.kK[pos] = kA[j];
         a.vK[pos] = r;
+        a.kRows[pos] = r;
       }
     }
     if (fl & (2u << (3 * j))) {
@@ -240,6 +242,7 @@ void launch_prep(Ctx& c) {
   a.status = c.prep_status;
   a.kK = c.sK.k[0];
   a.vK = c.sK.v[0];
+  a.kRows = c.k_rows;
   a.kC = c.sC.k[0];
   a.vC = c.sC.v[0];
   a.kJ = c.sJ.k[0];
