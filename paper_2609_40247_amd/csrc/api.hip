@@ -2,7 +2,10 @@
 // of the stages on the caller's stream, and the return code.
 #include <string.h>
 
+#include <cstdio>
 #include <mutex>
+
+#include <stdlib.h>
 
 #include "internal.hpp"
 
@@ -338,6 +341,7 @@ static inline void stage_end(Ctx& c, int s) {
 // concurrent callers cannot interleave their event records.
 struct DeviceStreams {
   hipStream_t s[2] = {nullptr, nullptr};
+  hipStream_t cap = nullptr;  // graphs are captured here (the caller's stream may be the null stream)
   hipEvent_t e[4] = {nullptr, nullptr, nullptr, nullptr};  // sorts, timeline chain, join, prep done
   bool ok = false;
 };
@@ -351,6 +355,7 @@ static DeviceStreams* device_streams() {
   if (!d.ok) {
     for (auto& st : d.s)
       if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipStreamCreateWithFlags(&d.cap, hipStreamNonBlocking) != hipSuccess) return nullptr;
     for (auto& ev : d.e)
       if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return nullptr;
     d.ok = true;
@@ -358,15 +363,8 @@ static DeviceStreams* device_streams() {
   return &d;
 }
 
-static int enqueue(Ctx& c) {
-  std::lock_guard<std::mutex> lock(g_enqueue_mutex);
-  static bool lds_attr = false;
-  if (!lds_attr) {
-    names_set_lds_attr();
-    lds_attr = true;
-  }
-  DeviceStreams* dsx = device_streams();
-  if (!dsx) return HERSCHEL_EDEVICE;
+// Enqueues one call's kernels (the caller holds g_enqueue_mutex).
+static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   const hipStream_t s0 = c.st;
   stage_begin(c, HERSCHEL_STAGE_INIT);
   launch_init(c);
@@ -449,6 +447,125 @@ static int enqueue(Ctx& c) {
   launch_finalize(c);
   stage_end(c, HERSCHEL_STAGE_FINAL);
   return hipGetLastError() == hipSuccess ? HERSCHEL_OK : HERSCHEL_EDEVICE;
+}
+
+static DeviceStreams* enqueue_setup() {
+  static bool lds_attr = false;
+  if (!lds_attr) {
+    names_set_lds_attr();
+    lds_attr = true;
+  }
+  return device_streams();
+}
+
+static int enqueue(Ctx& c) {
+  std::lock_guard<std::mutex> lock(g_enqueue_mutex);
+  DeviceStreams* dsx = enqueue_setup();
+  if (!dsx) return HERSCHEL_EDEVICE;
+  return enqueue_locked(c, dsx);
+}
+
+// A call with exactly the arguments of the previous one on this device
+// (events, size, parameters except the stream, outputs) replays a HIP graph
+// of the previous call's launches: about 35 launches and the streams' event
+// edges become one graph launch on the caller's stream.  Each device keeps
+// the graphs of its last four distinct argument sets; any other call
+// captures a new graph in place of the oldest.  The graph is captured on a private
+// stream, so the caller's stream may be the null stream.  Not used while a
+// stage is being timed, nor after a capture has failed once in this process
+// (the calls then launch their kernels directly); HERSCHEL_GRAPHS=0 turns
+// it off and HERSCHEL_DEBUG=1 reports why a capture failed.
+struct GraphKey {
+  herschel_events ev;
+  int64_t n;
+  herschel_params p;
+  herschel_outputs out;
+};
+struct DeviceGraph {
+  bool valid = false;
+  GraphKey key;
+  hipGraphExec_t exec = nullptr;
+};
+constexpr int GRAPHS_PER_DEVICE = 4;
+static DeviceGraph g_graphs[64][GRAPHS_PER_DEVICE];
+static unsigned g_graph_next[64];
+static bool g_graphs_failed = false;
+static bool env_flag(const char* name, bool dflt) {
+  const char* e = getenv(name);
+  if (!e || !e[0]) return dflt;
+  return e[0] != '0';
+}
+static bool graphs_enabled() {
+  static const bool on = env_flag("HERSCHEL_GRAPHS", true);
+  return on && !g_graphs_failed;
+}
+static int graph_failed(const char* what, hipError_t e) {
+  static const bool dbg = env_flag("HERSCHEL_DEBUG", false);
+  if (dbg) fprintf(stderr, "herschel: graph capture off: %s: %s\n", what, hipGetErrorString(e));
+  g_graphs_failed = true;
+  return 0;
+}
+
+static int enqueue_cached(Ctx& c, const herschel_events* ev, int64_t n, const herschel_params* p,
+                          const herschel_outputs* out) {
+  if (g_stage >= 0 || !graphs_enabled()) return enqueue(c);
+  std::lock_guard<std::mutex> lock(g_enqueue_mutex);
+  DeviceStreams* dsx = enqueue_setup();
+  int dev = 0;
+  if (!dsx || hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return HERSCHEL_EDEVICE;
+  GraphKey key;
+  memset(&key, 0, sizeof(key));
+  key.ev = *ev;
+  key.n = n;
+  key.p = *p;
+  key.p.hip_stream = nullptr;
+  key.out = *out;
+  for (DeviceGraph& g : g_graphs[dev]) {
+    if (!g.valid || memcmp(&g.key, &key, sizeof(key)) != 0) continue;
+    const hipError_t e = hipGraphLaunch(g.exec, c.st);
+    if (e == hipSuccess) return HERSCHEL_OK;
+    graph_failed("hipGraphLaunch", e);
+    (void)hipGetLastError();
+    return enqueue_locked(c, dsx);
+  }
+  DeviceGraph& g = g_graphs[dev][g_graph_next[dev]++ % GRAPHS_PER_DEVICE];
+  if (g.valid) {
+    (void)hipGraphExecDestroy(g.exec);
+    g.valid = false;
+  }
+  Ctx cc = c;
+  cc.st = dsx->cap;
+  hipError_t e = hipStreamBeginCapture(cc.st, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) {
+    graph_failed("hipStreamBeginCapture", e);
+    (void)hipGetLastError();
+    return enqueue_locked(c, dsx);
+  }
+  const int code = enqueue_locked(cc, dsx);
+  hipGraph_t graph = nullptr;
+  e = hipStreamEndCapture(cc.st, &graph);
+  if (code != HERSCHEL_OK || e != hipSuccess || !graph) {
+    graph_failed("hipStreamEndCapture", e);
+    if (graph) (void)hipGraphDestroy(graph);
+    (void)hipGetLastError();
+    return code != HERSCHEL_OK ? code : enqueue_locked(c, dsx);
+  }
+  hipGraphExec_t exec = nullptr;
+  e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  if (e != hipSuccess || !exec) {
+    graph_failed("hipGraphInstantiate", e);
+    (void)hipGetLastError();
+    return enqueue_locked(c, dsx);
+  }
+  g.key = key;
+  g.exec = exec;
+  g.valid = true;
+  e = hipGraphLaunch(exec, c.st);
+  if (e == hipSuccess) return HERSCHEL_OK;
+  graph_failed("hipGraphLaunch", e);
+  (void)hipGetLastError();
+  return enqueue_locked(c, dsx);
 }
 
 static int code_from(const herschel_counters& h, int64_t gap_capacity) {
@@ -549,7 +666,7 @@ int herschel_trace_analyze(const herschel_events* ev, int64_t n, const herschel_
   Ctx c;
   int code = prepare(c, ev, n, p, out, p ? p->workspace : nullptr, p ? p->workspace_bytes : 0);
   if (code) return code;
-  code = enqueue(c);
+  code = enqueue_cached(c, ev, n, p, out);
   if (code) return code;
   herschel_counters h;
   if (hipMemcpyAsync(&h, out->counters, sizeof(h), hipMemcpyDeviceToHost, c.st) != hipSuccess) return HERSCHEL_EDEVICE;

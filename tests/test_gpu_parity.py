@@ -201,6 +201,39 @@ def test_sparse_correlation_ids(H, seed):
     check(H, cols, p, f"sparse corr seed {seed}")
 
 
+def test_graph_replays_follow_new_contents(H):
+    """Calls with the same buffers and parameters replay one captured graph;
+    between replays the buffers are refilled (eager copies, fills and
+    syncs), and every replay must match the oracle for the data it found.
+    A second analyzer with another gap threshold alternates with the first
+    (a graph of its own), and the stream is torch's null stream."""
+    traces = [synth.random_small(seed=9200 + s, n_rows=5000, window=6000, n_procs=2, n_streams=4, n_threads=2,
+                                 corr_range=700, edges=0) for s in range(3)]
+    n = 5000
+    assert all(t.n == n for t in traces)
+    p0 = dict(traces[0].params)
+    p1 = dict(p0, gap_threshold=int(p0["gap_threshold"]) * 2 + 1)
+    cap = n + p0["n_procs"] * p0["n_streams"]
+    ans = [H.Analyzer(p0, n, gap_capacity=cap), H.Analyzer(p1, n, gap_capacity=cap)]
+    dev = H.device_columns(traces[0].columns())
+    ev = H.events_struct(dev)
+    plan = [(0, 0), (0, 1), (0, 0), (1, 2), (0, 2), (1, 0), (1, 1), (0, 1)]
+    for k, (a, t) in enumerate(plan):
+        cols = dict(traces[t].columns())
+        shift = int(p0["window_begin"]) - int(traces[t].params["window_begin"])  # align the windows
+        cols["ts"] = cols["ts"] + shift
+        cols["te"] = cols["te"] + shift
+        for c, v in cols.items():
+            dev[c].copy_(torch.from_numpy(np.ascontiguousarray(v)).to(dev[c].device))
+        an, p = ans[a], (p0, p1)[a]
+        an.prefill()
+        torch.cuda.synchronize()
+        code = an.run(ev, n)
+        g = (code, an.results(n))
+        o = oracle.analyze(cols, p, gap_capacity=cap)
+        assert_same(g, o, p, f"call {k}: analyzer {a}, trace {t}")
+
+
 def test_4096_processes(H):
     tr = synth.random_small(seed=78, n_rows=20_000, window=5_000, n_procs=4096, n_streams=3, n_threads=2,
                             corr_range=50)
