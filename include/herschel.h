@@ -164,7 +164,14 @@ typedef struct {
 int herschel_workspace_size(int64_t n, const herschel_params *p, size_t *bytes);
 
 /* Reconstruct one window: n rows of ev under *p into *out.  Returns a
- * HERSCHEL_* code.  On EEVENT only counters->first_invalid is defined. */
+ * HERSCHEL_* code.  On EEVENT only counters->first_invalid is defined.
+ * The work is ordered on p->hip_stream (it also runs on two library
+ * streams that wait for, and are waited on by, that stream); the call
+ * returns after synchronising with it.  A call whose event columns, n,
+ * parameters (all but hip_stream) and output pointers equal those of one of
+ * the last four argument sets captured on the device replays that call's
+ * captured HIP graph; the buffers' contents may differ.  Calls overlapping
+ * from several host threads are serialised while they enqueue. */
 int herschel_trace_analyze(const herschel_events *ev, int64_t n, const herschel_params *p,
                            herschel_outputs *out);
 
@@ -182,7 +189,11 @@ int herschel_trace_analyze_batch(const herschel_events *ev, const int64_t *trace
 
 const char *herschel_strerror(int code);
 
-/* Diagnostics for benchmarks.  Stages of one analysis call, in launch order. */
+/* Diagnostics for benchmarks.  Stages of one analysis call.  INIT, PREP,
+ * HIST and SORT run in this order on params->hip_stream; after PREP the
+ * JOIN and NAMES stages run on a library stream, after SORT the TIMELINE and
+ * OVERLAP stages on another, while CONTAIN and OPAGG follow SORT on
+ * params->hip_stream; FINAL waits for all of them. */
 enum {
   HERSCHEL_STAGE_INIT = 0,     /* clear the workspace state and accumulating outputs */
   HERSCHEL_STAGE_PREP = 1,     /* validate, correct, admit, compact (one kernel) */
@@ -192,16 +203,18 @@ enum {
   HERSCHEL_STAGE_TIMELINE = 5, /* busy/idle, gaps, coverage runs (one kernel) */
   HERSCHEL_STAGE_OVERLAP = 6,  /* co-ranks of the coverage runs and the sweep */
   HERSCHEL_STAGE_CONTAIN = 7,  /* op nesting and launch -> op */
-  HERSCHEL_STAGE_JOIN = 8,     /* launch <-> kernel join, latency (one kernel) */
-  HERSCHEL_STAGE_OPAGG = 9,    /* inclusive per-op aggregates (one kernel) */
-  HERSCHEL_STAGE_EDGES = 10,
-  HERSCHEL_STAGE_FINAL = 11,
+  HERSCHEL_STAGE_JOIN = 8,     /* launch <-> kernel join by correlation table, latency */
+  HERSCHEL_STAGE_OPAGG = 9,    /* kernel -> op, inclusive per-op aggregates */
+  HERSCHEL_STAGE_EDGES = 10,   /* dependency waits */
+  HERSCHEL_STAGE_FINAL = 11,   /* counters and histogram totals */
   HERSCHEL_N_STAGES = 12
 };
 
 /* Record start_event / stop_event (hipEvent_t, created by the caller) on
- * params->hip_stream around stage `stage` of every following analysis call in
- * this process, for measuring one stage's device time live.  NULL events turn
+ * the stream that stage `stage` runs on, around that stage of every
+ * following analysis call in this process, for measuring one stage's device
+ * time live (such calls launch their kernels directly, not from a captured
+ * graph).  NULL events turn
  * the recording off.  Returns HERSCHEL_EINVAL for an unknown stage.  Not
  * thread-safe: meant for single-threaded benchmarks. */
 int herschel_time_stage(int stage, void *start_event, void *stop_event);
