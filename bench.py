@@ -81,6 +81,125 @@ def cpu_baseline(cols, params, n, budget_s=12.0, max_calls=30):
                       f"({dt:.1f} s on {os.cpu_count()} host cores, 1 used)"}
 
 
+def _config4_trace(t):
+    from paper_2609_40247_amd import synth
+    tr = synth.config4_trace(t)
+    return tr.columns(), tr.params
+
+
+def run_config4(args) -> int:
+    """One chunk of the 256-trace batch (traces 32c .. 32c+31, about 105M
+    rows) through the batch entry point, device-resident; then the same chunk
+    streamed from pinned host memory with double-buffered uploads."""
+    import multiprocessing as mp
+    import numpy as np
+    first = 32 * args.chunk
+    ids = list(range(first, first + 32))
+    with mp.get_context("fork").Pool(min(16, os.cpu_count() or 1)) as pool:  # before the GPU is touched
+        gen = pool.map(_config4_trace, ids)
+    cols_l = [c for c, _ in gen]
+    params_l = [p for _, p in gen]
+    ns = [len(c["ts"]) for c in cols_l]
+    n = int(sum(ns))
+    offs = np.cumsum([0] + ns).astype(np.int64)
+    keys = list(cols_l[0].keys())
+    cols = {k: np.concatenate([c[k] for c in cols_l]) for k in keys}
+    kernels = int(sum(int(np.count_nonzero(c["kind"] == 2)) for c in cols_l))
+
+    import torch
+    from paper_2609_40247_amd import herschel as H
+    big = int(np.argmax(ns))
+    ans = [H.Analyzer(p, ns[t], workspace=(t == big)) for t, p in enumerate(params_l)]
+    p0 = ans[0]._params_struct(ans[big].ws.data_ptr(), ans[big].ws_bytes)
+    plist = [p0] + [a.params for a in ans[1:]]
+    outs = [a.outs for a in ans]
+    dev = [H.device_columns(cols)]
+    ev = H.events_struct(dev[0])
+    torch.cuda.synchronize()
+
+    def call(e):
+        code = H.herschel_trace_analyze_batch(e, offs, plist, outs)
+        if code != 0:
+            raise RuntimeError(f"batch analysis failed: {H.herschel_strerror(code)}")
+
+    for _ in range(args.warmup):
+        call(ev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        call(ev)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    # streamed: chunk i+1 uploads on a copy stream while chunk i is analyzed
+    host = {k: torch.from_numpy(np.ascontiguousarray(v)).pin_memory() for k, v in cols.items()}
+    dev.append({k: torch.empty_like(v) for k, v in dev[0].items()})
+    evs = [H.events_struct(d) for d in dev]
+    cs = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    nbytes = sum(v.numel() * v.element_size() for v in host.values())
+    done = [torch.cuda.Event() for _ in range(2)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with torch.cuda.stream(cs):
+        for k in host:
+            dev[0][k].copy_(host[k], non_blocking=True)
+    done[0].record(cs)
+    torch.cuda.synchronize()
+    h2d_s = time.perf_counter() - t0
+    reps = max(args.steps, 2)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with torch.cuda.stream(cs):
+        for k in host:
+            dev[0][k].copy_(host[k], non_blocking=True)
+    done[0].record(cs)
+    for i in range(reps):
+        if i + 1 < reps:
+            b = (i + 1) % 2
+            with torch.cuda.stream(cs):
+                for k in host:
+                    dev[b][k].copy_(host[k], non_blocking=True)
+            done[b].record(cs)
+        main.wait_event(done[i % 2])
+        call(evs[i % 2])
+    torch.cuda.synchronize()
+    stream_ms = (time.perf_counter() - t0) * 1e3 / reps
+
+    out = {
+        "metric": METRIC, "value": round(n / (ms * 1e-3) / 1e6, 3), "unit": "M ev/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "config": {"workload": f"batch chunk {args.chunk} of the 256-trace set: traces {first}-{first + 31} "
+                               "(decode-step traces of 200k-2M kernels, windows of ceil(L/1000) x 30 ms), "
+                               "names, busy/idle, gaps, latency histogram",
+                   "rows": n, "kernels": kernels, "traces": 32,
+                   "kernel_records_per_s_M": round(kernels / (ms * 1e-3) / 1e6, 3),
+                   "est_ms_for_256_traces": round(ms * 8, 1)},
+        "streamed": {"value": round(n / (stream_ms * 1e-3) / 1e6, 3), "unit": "M ev/s", "ms_per_chunk":
+                     round(stream_ms, 3), "h2d_bytes_per_chunk": nbytes,
+                     "h2d_GBps": round(nbytes / h2d_s / 1e9, 2)},
+        "roofline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        oracle.analyze(cols_l[0], params_l[0])
+        t0, done_rows, used = time.perf_counter(), 0, 0
+        for c, p in zip(cols_l, params_l):
+            oracle.analyze(c, p)
+            done_rows += len(c["ts"])
+            used += 1
+            if time.perf_counter() - t0 >= 12.0:
+                break
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(done_rows / dt / 1e6, 3), "unit": "M ev/s", "cores": 1,
+                               "kind": "oracle", "sample": f"the first {used} traces of the chunk "
+                               f"({done_rows} rows) analyzed once each by the single-threaded C oracle "
+                               f"({dt:.1f} s)"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -91,11 +210,17 @@ def main() -> int:
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="first copy a buffer of this many MiB on the device (a plain copy kernel of known "
                          "size, for scaling rocprofv3 byte counters)")
+    ap.add_argument("--workload", choices=("config1", "config4"), default="config1",
+                    help="config1: the decode-step trace (the headline line); config4: one 32-trace chunk of "
+                         "the batch workload through the batch entry point")
+    ap.add_argument("--chunk", type=int, default=0, help="config4: which of the 8 chunks")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "run it with --gpus 1", file=sys.stderr)
         return 2
+    if args.workload == "config4":
+        return run_config4(args)
 
     import numpy as np
     import torch

@@ -177,7 +177,7 @@ class Analyzer:
     largest row count this analyzer will be called with."""
 
     def __init__(self, params: dict, n_max: int, gap_capacity: int | None = None, device="cuda",
-                 stream: torch.cuda.Stream | None = None, lib=None, op_fill: int = -3):
+                 stream: torch.cuda.Stream | None = None, lib=None, op_fill: int = -3, workspace: bool = True):
         self.lib = lib or load()
         self.device = device
         self.p = dict(params)
@@ -200,7 +200,11 @@ class Analyzer:
         self.op_fill = op_fill
         self.params = self._params_struct(None, 0)
         self.ws_bytes = herschel_workspace_size(self.n_max, self.params, self.lib)
-        self.ws = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
+        # outputs-only analyzers serve as the later traces of a batch call,
+        # which runs in the first trace's workspace
+        self.ws = torch.empty(max(self.ws_bytes, 256) if workspace else 256, dtype=torch.uint8, device=device)
+        if not workspace:
+            self.ws_bytes = 0
         n = max(self.n_max, 1)
         gc = max(self.gap_capacity, 1)
         z = lambda k, dt: torch.empty(k, dtype=dt, device=device)
