@@ -43,13 +43,16 @@ def source_hash(stage: str) -> str:
 
 
 def sort_units(stats):
-    """Key-passes the radix sorts must make: each sort moves its keys once
-    per digit on which they differ.  Also the number of pass launches (the
-    sorts share launches; one per digit of the widest key)."""
+    """Key-passes the radix passes of the sort stage must make: the timeline
+    and containment sorts (the join's own sort runs on the join stream, when
+    the correlation table cannot be used) each move their keys once per digit
+    on which they differ.  Also the number of pass launches of the stage (the
+    two sorts share launches; one per digit of the wider key)."""
+    stage = [stats[0], stats[2]]
     units = 0
-    for nkeys, skipped, nd in stats:
+    for nkeys, skipped, nd in stage:
         units += nkeys * sum(1 for d in range(nd) if not (skipped >> d) & 1)
-    return units, max(nd for _, _, nd in stats)
+    return units, max(nd for _, _, nd in stage)
 
 
 def profiled_traffic(stage: str, workload: str):

@@ -60,12 +60,14 @@ size_t layout_workspace(Ctx& c, char* base) {
   sort_plan(c.sK, 0, n, c.pb + c.sb + c.wb, true);
   sort_plan(c.sJ, 1, n, 49 + c.pb, true);
   sort_plan(c.sC, 2, n, c.pb + c.tb + c.wb + 1, true);
-  c.sK.status = b.take<uint32_t>((int64_t)c.sK.nd * c.sK.tiles_max * 256);
-  c.sJ.status = b.take<uint32_t>((int64_t)c.sJ.nd * c.sJ.tiles_max * 256);
+  // digit 0's look-back words are cleared here; each later digit's are
+  // cleared by the pass before it
+  c.sK.status0 = b.take<uint32_t>(c.sK.tiles_max * 256);
+  c.sJ.status0 = b.take<uint32_t>(c.sJ.tiles_max * 256);
   if (c.contain) {
     c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
     c.vb_status = b.take<uint64_t>(c.vb_tiles);
-    c.sC.status = b.take<uint32_t>((int64_t)c.sC.nd * c.sC.tiles_max * 256);
+    c.sC.status0 = b.take<uint32_t>(c.sC.tiles_max * 256);
     // pyramid levels above the tile maxima: built by atomic maxima, from zero
     c.nlev = 3;
     while (cdiv(n, (int64_t)1 << (6 * (c.nlev - 1))) > 64) ++c.nlev;
@@ -75,6 +77,8 @@ size_t layout_workspace(Ctx& c, char* base) {
     }
   }
   c.zero_bytes = align_up(b.off - z0);
+  for (SortBufs* s : {&c.sK, &c.sJ, &c.sC})
+    if (s != &c.sC || c.contain) s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * 256);
   c.hist_part = b.take<uint32_t>((int64_t)N_SORTS * HIST_MAX_BLOCKS * 8 * 256);
   c.k_rows = b.take<uint32_t>(n);
   if (c.P <= JT_PROCS) {
@@ -123,6 +127,9 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.lk_first = b.take<int64_t>(n);
     c.lk_last = b.take<int64_t>(n);
     c.lk_sum = b.take<int64_t>(n);
+    c.ag_tiles = cdiv(n, AG_TILE);
+    c.ag_chain = b.take<int32_t>(c.ag_tiles * AG_CHAIN);
+    c.ag_nchain = b.take<int32_t>(c.ag_tiles);
   }
   c.name_blocks = names_block_count(n, c.NN);
   if (c.NN <= names_lds_limit()) c.name_part = b.take<uint64_t>((int64_t)c.name_blocks * c.NN * 4);
@@ -342,7 +349,7 @@ static inline void stage_end(Ctx& c, int s) {
 struct DeviceStreams {
   hipStream_t s[2] = {nullptr, nullptr};
   hipStream_t cap = nullptr;  // graphs are captured here (the caller's stream may be the null stream)
-  hipEvent_t e[4] = {nullptr, nullptr, nullptr, nullptr};  // sorts, timeline chain, join, prep done
+  hipEvent_t e[3] = {};  // sorts, timeline chain, join
   bool ok = false;
 };
 static std::mutex g_enqueue_mutex;
@@ -363,9 +370,19 @@ static DeviceStreams* device_streams() {
   return &d;
 }
 
-// Enqueues one call's kernels (the caller holds g_enqueue_mutex).
+static bool env_flag(const char* name, bool dflt) {
+  const char* e = getenv(name);
+  if (!e || !e[0]) return dflt;
+  return e[0] != '0';
+}
+
+// Enqueues one call's kernels (the caller holds g_enqueue_mutex).  With
+// HERSCHEL_SERIAL=1 every chain runs on the caller's stream, one kernel
+// after another (for per-kernel profiles without concurrent neighbours).
 static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
+  static const bool serial = env_flag("HERSCHEL_SERIAL", false);
   const hipStream_t s0 = c.st;
+  const hipStream_t lib0 = serial ? s0 : dsx->s[0], lib1 = serial ? s0 : dsx->s[1];
   stage_begin(c, HERSCHEL_STAGE_INIT);
   launch_init(c);
   stage_end(c, HERSCHEL_STAGE_INIT);
@@ -373,59 +390,30 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   launch_prep(c);
   launch_join_plan(c);
   stage_end(c, HERSCHEL_STAGE_PREP);
-  (void)hipEventRecord(dsx->e[3], s0);
 
-  // chain 2 starts here: the correlation-table join and the per-name tables
-  // need only prep's lists
-  c.st = dsx->s[1];
-  (void)hipStreamWaitEvent(c.st, dsx->e[3], 0);
-  stage_begin(c, HERSCHEL_STAGE_JOIN);
-  launch_join_table(c);
-  stage_end(c, HERSCHEL_STAGE_JOIN);
-  stage_begin(c, HERSCHEL_STAGE_NAMES);
-  launch_names(c);
-  launch_names_reduce(c);
-  stage_end(c, HERSCHEL_STAGE_NAMES);
-  c.st = s0;
-
+  // The three sorts share their digit passes (blockIdx.y picks the sort; a
+  // sort whose digit is skipped leaves at once, as the join sort's do when
+  // the correlation table was used).  The join keys are wider than the
+  // others: the join sort's remaining digits run on the join stream.  Nothing
+  // else runs beside the sorts: a large grid on another stream would take
+  // the CUs first and hold up the passes, which every later stage waits for.
+  const int ks = c.contain ? 2 : 1;
+  SortBufs* ss[3] = {&c.sK, &c.sC, &c.sJ};
+  const int32_t* cc[3] = {&c.ds->nK, &c.ds->nCL, &c.ds->nJ};
+  ss[ks] = &c.sJ;
+  cc[ks] = &c.ds->nJ;
+  const int d_shared = c.contain ? std::max(c.sK.nd, c.sC.nd) : c.sK.nd;
   stage_begin(c, HERSCHEL_STAGE_HIST);
-  {
-    SortBufs* ss[3] = {&c.sK, &c.sJ, &c.sC};
-    const int32_t* cc[3] = {&c.ds->nK, &c.ds->nJ, &c.ds->nCL};
-    launch_hist_multi(c, ss, cc, c.contain ? 3 : 2);
-  }
+  launch_hist_multi(c, ss, cc, ks + 1);
   stage_end(c, HERSCHEL_STAGE_HIST);
   stage_begin(c, HERSCHEL_STAGE_SORT);
-  {
-    SortBufs* ss[3] = {&c.sK, &c.sJ, &c.sC};
-    const int32_t* cc[3] = {&c.ds->nK, &c.ds->nJ, &c.ds->nCL};
-    launch_sort_multi(c, ss, cc, c.contain ? 3 : 2);
-  }
+  launch_sort_multi(c, ss, cc, ks + 1, 0, d_shared);
   stage_end(c, HERSCHEL_STAGE_SORT);
   (void)hipEventRecord(dsx->e[0], s0);
 
-  // chain 1: timeline and overlap
-  c.st = dsx->s[0];
-  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
-  stage_begin(c, HERSCHEL_STAGE_TIMELINE);
-  launch_timeline(c);
-  stage_end(c, HERSCHEL_STAGE_TIMELINE);
-  stage_begin(c, HERSCHEL_STAGE_OVERLAP);
-  if (c.overlap) launch_overlap(c);
-  stage_end(c, HERSCHEL_STAGE_OVERLAP);
-  (void)hipEventRecord(dsx->e[1], c.st);
-
-  // chain 2 continued: the sort-merge join (when the table was not used)
-  // and the dependency waits
-  c.st = dsx->s[1];
-  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
-  launch_join(c);
-  stage_begin(c, HERSCHEL_STAGE_EDGES);
-  launch_edges(c);
-  stage_end(c, HERSCHEL_STAGE_EDGES);
-  (void)hipEventRecord(dsx->e[2], c.st);
-
-  // chain 3 on the caller's stream: containment, then what needs the join
+  // chain 3 on the caller's stream, enqueued first: containment is the
+  // longest of the three chains, and of work that becomes ready together
+  // the first enqueued takes the CUs first
   c.st = s0;
   if (c.contain) {
     stage_begin(c, HERSCHEL_STAGE_CONTAIN);
@@ -435,6 +423,38 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.n, 256 * 8), 1), 2048);
     hipLaunchKernelGGL(k_nocontain, dim3(grid), dim3(256), 0, c.st, c.sC.k[0], c.sC.v[0], c.ds, c.o.link, c.o.aux);
   }
+
+  // chain 1: timeline and overlap, then the per-name tables
+  c.st = lib0;
+  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
+  stage_begin(c, HERSCHEL_STAGE_TIMELINE);
+  launch_timeline(c);
+  stage_end(c, HERSCHEL_STAGE_TIMELINE);
+  stage_begin(c, HERSCHEL_STAGE_OVERLAP);
+  if (c.overlap) launch_overlap(c);
+  stage_end(c, HERSCHEL_STAGE_OVERLAP);
+  stage_begin(c, HERSCHEL_STAGE_NAMES);
+  launch_names(c);
+  launch_names_reduce(c);
+  stage_end(c, HERSCHEL_STAGE_NAMES);
+  (void)hipEventRecord(dsx->e[1], c.st);
+
+  // chain 2: the join (by the correlation table, else by the join sort's
+  // remaining digits and the sort-merge join) and the dependency waits
+  c.st = lib1;
+  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
+  stage_begin(c, HERSCHEL_STAGE_JOIN);
+  launch_join_table(c);
+  launch_sort_multi(c, &ss[ks], &cc[ks], 1, d_shared, c.sJ.nd);
+  launch_join(c);
+  stage_end(c, HERSCHEL_STAGE_JOIN);
+  stage_begin(c, HERSCHEL_STAGE_EDGES);
+  launch_edges(c);
+  stage_end(c, HERSCHEL_STAGE_EDGES);
+  (void)hipEventRecord(dsx->e[2], c.st);
+
+  // back on the caller's stream: what needs both containment and the join
+  c.st = s0;
   (void)hipStreamWaitEvent(c.st, dsx->e[2], 0);
   stage_begin(c, HERSCHEL_STAGE_OPAGG);
   if (c.contain) {
@@ -490,11 +510,6 @@ constexpr int GRAPHS_PER_DEVICE = 4;
 static DeviceGraph g_graphs[64][GRAPHS_PER_DEVICE];
 static unsigned g_graph_next[64];
 static bool g_graphs_failed = false;
-static bool env_flag(const char* name, bool dflt) {
-  const char* e = getenv(name);
-  if (!e || !e[0]) return dflt;
-  return e[0] != '0';
-}
 static bool graphs_enabled() {
   static const bool on = env_flag("HERSCHEL_GRAPHS", true);
   return on && !g_graphs_failed;

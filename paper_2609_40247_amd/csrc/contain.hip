@@ -55,6 +55,10 @@ struct ContainArgs {
   const int64_t* lk_first;
   const int64_t* lk_last;
   const int64_t* lk_sum;
+  // per aggregate tile: the ops open at its start (innermost first) and their number
+  int32_t* ag_chain;
+  int32_t* ag_nchain;
+  int64_t ag_tiles;
 };
 
 __device__ __forceinline__ int32_t key_pid(const ContainArgs& a, uint64_t key) {
@@ -194,26 +198,33 @@ __global__ __launch_bounds__(VB_THREADS) void k_vbuild(ContainArgs a) {
   uint64_t key[VB_ITEMS];
   uint32_t row[VB_ITEMS];
   int64_t te[VB_ITEMS];
+  // each round of loads is issued for all items together: indices are
+  // clamped (to the last position, or row 0), never branched on
 #pragma unroll
   for (int j = 0; j < VB_ITEMS; ++j) {
     const int64_t p = base + (int64_t)wv * (VB_ITEMS * WAVE) + j * WAVE + lane;
-    key[j] = p < n ? keys[p] : 0ull;
+    const int64_t pc = p < n ? p : n - 1;
+    key[j] = keys[pc];
+    row[j] = vals[pc];
   }
 #pragma unroll
   for (int j = 0; j < VB_ITEMS; ++j) {
     const int64_t p = base + (int64_t)wv * (VB_ITEMS * WAVE) + j * WAVE + lane;
-    row[j] = p < n && key_is_op(key[j]) ? vals[p] : ~0u;
+    if (!(p < n && key_is_op(key[j]))) row[j] = ~0u;
   }
+  int64_t offv[VB_ITEMS];
 #pragma unroll
-  for (int j = 0; j < VB_ITEMS; ++j) te[j] = row[j] != ~0u ? a.te[row[j]] : 0;
+  for (int j = 0; j < VB_ITEMS; ++j) {
+    te[j] = a.te[row[j] != ~0u ? row[j] : 0u];
+    offv[j] = a.off ? a.off[key_pid(a, key[j])] : 0;
+  }
   uint64_t wmax = 0;
 #pragma unroll
   for (int j = 0; j < VB_ITEMS; ++j) {
     const int64_t p = base + (int64_t)wv * (VB_ITEMS * WAVE) + j * WAVE + lane;
     uint64_t v = 0;
     if (row[j] != ~0u) {
-      const int32_t pid = key_pid(a, key[j]);
-      const int64_t tec = te[j] - (a.off ? a.off[pid] : 0);
+      const int64_t tec = te[j] - offv[j];
       const int64_t e = tec >= a.W1 ? a.W : tec - a.W0;
       v = (key_seg(a, key[j]) << a.vb) | (uint64_t)(e + 1);
     }
@@ -321,14 +332,24 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
   const int ng = (int)cdiv(tn, 64);
   uint64_t key[QY_ROUNDS];
   uint32_t row[QY_ROUNDS];
+  uint64_t vv[QY_ROUNDS];
+#pragma unroll
+  for (int r = 0; r < QY_ROUNDS; ++r) {
+    const int lp = (wv + r * (QY_THREADS / WAVE)) * 64 + lane;
+    const int64_t pc = base + (lp < tn ? lp : tn - 1);  // clamped: the loads stay in flight together
+    key[r] = keys[pc];
+    row[r] = vals[pc];
+    vv[r] = a.V[pc];
+  }
 #pragma unroll
   for (int r = 0; r < QY_ROUNDS; ++r) {
     const int lp = (wv + r * (QY_THREADS / WAVE)) * 64 + lane;
     const bool live = lp < tn;
-    key[r] = live ? keys[base + lp] : 0ull;
-    row[r] = live ? vals[base + lp] : 0u;
-    const uint64_t v = live ? a.V[base + lp] : 0ull;
-    s_v[lp] = v;
+    if (!live) {
+      key[r] = 0ull;
+      row[r] = 0u;
+    }
+    s_v[lp] = live ? vv[r] : 0ull;
     s_val[lp] = row[r];
   }
   if (tid == 0) s_nesc = 0;
@@ -340,7 +361,8 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
     s_sub[tid] = m;
   }
   if (wv == 0) {  // group-level window maxima and exclusive prefix maxima
-    const uint64_t m1 = lane < ng ? a.M[1][tile * QY_GROUPS + lane] : 0ull;
+    const uint64_t m1r = a.M[1][tile * QY_GROUPS + (lane < ng ? lane : 0)];
+    const uint64_t m1 = lane < ng ? m1r : 0ull;
     uint64_t w = m1;
     s_g[0][lane] = w;
 #pragma unroll
@@ -445,40 +467,63 @@ constexpr int DP_ITEMS = 4;
 
 __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
   __shared__ unsigned long long s_imp;
+  const int64_t n = a.ds->nCL;
+  // Positions past the end take the last entry (clamped loads); with no
+  // entry there is nothing to take, and nothing to do.
+  if (n == 0) return;
   if (threadIdx.x == 0) s_imp = 0;
   __syncthreads();
-  const int64_t n = a.ds->nCL;
   const int par = (int)a.ds->sort_parity[2];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
   const int64_t p0 = (int64_t)blockIdx.x * 256 * DP_ITEMS + threadIdx.x;
   uint32_t row[DP_ITEMS];
   int64_t q[DP_ITEMS];
+  // each round of loads is issued for all items together (clamped indices)
+  uint64_t kk[DP_ITEMS];
 #pragma unroll
   for (int u = 0; u < DP_ITEMS; ++u) {
     const int64_t p = p0 + u * 256;
-    const bool op = p < n && key_is_op(keys[p]);
-    row[u] = op ? vals[p] : ~0u;
-    q[u] = op ? a.par[p] : -1;
+    const int64_t pc = p < n ? p : n - 1;
+    kk[u] = keys[pc];
+    row[u] = vals[pc];
+    q[u] = a.par[pc];
+  }
+#pragma unroll
+  for (int u = 0; u < DP_ITEMS; ++u) {
+    const bool op = p0 + u * 256 < n && key_is_op(kk[u]);
+    if (!op) {
+      row[u] = ~0u;
+      q[u] = -1;
+    }
   }
   // improper nesting: the op ends after its parent
   uint32_t imp = 0;
   uint32_t prow[DP_ITEMS];
 #pragma unroll
-  for (int u = 0; u < DP_ITEMS; ++u) prow[u] = q[u] >= 0 ? vals[q[u]] : ~0u;
+  for (int u = 0; u < DP_ITEMS; ++u) prow[u] = vals[q[u] >= 0 ? q[u] : 0];
+  int64_t te_own[DP_ITEMS], te_par[DP_ITEMS];
+#pragma unroll
+  for (int u = 0; u < DP_ITEMS; ++u) {
+    te_own[u] = a.te[row[u] != ~0u ? row[u] : 0u];
+    te_par[u] = a.te[q[u] >= 0 ? prow[u] : 0u];
+  }
 #pragma unroll
   for (int u = 0; u < DP_ITEMS; ++u)
-    if (prow[u] != ~0u && a.te[row[u]] > a.te[prow[u]]) ++imp;  // one process: raw ends compare like corrected
+    if (q[u] >= 0 && te_own[u] > te_par[u]) ++imp;  // one process: raw ends compare like corrected
   int32_t d[DP_ITEMS];
 #pragma unroll
   for (int u = 0; u < DP_ITEMS; ++u) d[u] = 0;
   for (;;) {
     bool any = false;
+    int64_t nq[DP_ITEMS];
+#pragma unroll
+    for (int u = 0; u < DP_ITEMS; ++u) nq[u] = a.par[q[u] >= 0 && q[u] < n ? q[u] : 0];
 #pragma unroll
     for (int u = 0; u < DP_ITEMS; ++u) {
       if (q[u] >= 0 && in_range(a.ds, q[u], n)) {
         ++d[u];
-        q[u] = a.par[q[u]];
+        q[u] = nq[u];
         any = true;
       }
     }
@@ -493,6 +538,20 @@ __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
     a.op_last[row[u]] = I64MIN;
     a.op_ksum[row[u]] = 0;
   }
+  // The ops open at the start of aggregate tile b: the chain of answers from
+  // the position before it (that position first, if it is an op).
+  const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (b < cdiv(n, AG_TILE)) {
+    int nc = 0;
+    if (b > 0) {
+      const int64_t pe = b * AG_TILE - 1;
+      for (int64_t q = key_is_op(keys[pe]) ? pe : a.par[pe]; q >= 0 && in_range(a.ds, q, n); q = a.par[q]) {
+        if (nc < AG_CHAIN) a.ag_chain[b * AG_CHAIN + nc] = (int32_t)q;
+        ++nc;
+      }
+    }
+    a.ag_nchain[b] = nc;
+  }
   const uint64_t w = wave_sum_u64(imp);
   if (lane_id() == 0 && w) atomicAdd(&s_imp, (unsigned long long)w);
   __syncthreads();
@@ -500,22 +559,46 @@ __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
 }
 
 // ------------------------------------------------------ inclusive aggregates
-constexpr int AG_TILE = 1024;
-constexpr int AG_CHAIN = 64;
+constexpr int AG_THREADS = 256;
+constexpr int AG_ITEMS = AG_TILE / AG_THREADS;
 
-__global__ __launch_bounds__(256) void k_opagg(ContainArgs a) {
+// Adds (count, first, last, sum) to the op at sorted position q and every op
+// above it, in HBM: the part of a chain deeper than the table of ops open at
+// a tile start.
+__device__ void agg_add_global(const ContainArgs& a, int64_t q, uint32_t nk, int64_t f, int64_t l, uint64_t sm) {
+  const uint32_t* vals = a.v[(int)a.ds->sort_parity[2]];
+  for (int64_t r = q; r >= 0; r = a.par[r]) {
+    const uint32_t rr = vals[r];
+    atomicAdd(&a.op_nkern[rr], (int32_t)nk);
+    atomicMin((long long*)&a.op_first[rr], (long long)f);
+    atomicMax((long long*)&a.op_last[rr], (long long)l);
+    atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)sm);
+  }
+}
+
+// One workgroup per AG_TILE positions, AG_ITEMS per thread (striped).  The
+// answers form a forest whose preorder is the sorted order, and an op's
+// depth is its parent's plus one.  Every launch adds its kernels to its own
+// op; then, deepest level first, every op adds its totals to its parent, so
+// each op passes its totals up once (an op at the tile edge holds the part
+// of its subtree inside the tile).  Ops open at the tile start (found by the
+// depth pass) collect what reaches them in a table and take a prefix over
+// it, innermost first; ops still open at the tile end, and the open ops of
+// the start, add into HBM with atomics; the others are stored.
+__global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
   __shared__ int32_t s_par[AG_TILE];
+  __shared__ int32_t s_dep[AG_TILE];  // depth of an op; -1 for a launch
   __shared__ uint32_t s_nk[AG_TILE];
   __shared__ int64_t s_first[AG_TILE];
   __shared__ int64_t s_last[AG_TILE];
   __shared__ uint64_t s_sum[AG_TILE];
-  __shared__ int32_t s_chain[AG_CHAIN];      // ops open at the tile start, innermost first
+  __shared__ uint8_t s_open[AG_TILE];
+  __shared__ int32_t s_chain[AG_CHAIN];  // ops open at the tile start, innermost first
   __shared__ uint32_t c_nk[AG_CHAIN];
   __shared__ int64_t c_first[AG_CHAIN], c_last[AG_CHAIN];
   __shared__ uint64_t c_sum[AG_CHAIN];
-  __shared__ int s_nchain;
-  __shared__ uint8_t s_open[AG_TILE];
-  const int tid = threadIdx.x;
+  __shared__ int s_dmin, s_dmax;
+  const int tid = threadIdx.x, lane = lane_id();
   const int64_t n = a.ds->nCL;
   const int par = (int)a.ds->sort_parity[2];
   const uint64_t* keys = a.k[par];
@@ -523,95 +606,155 @@ __global__ __launch_bounds__(256) void k_opagg(ContainArgs a) {
   const int64_t base = (int64_t)blockIdx.x * AG_TILE;
   if (base >= n) return;
   const int64_t tn = min((int64_t)AG_TILE, n - base);
-  for (int64_t i = tid; i < tn; i += 256) {
-    s_par[i] = a.par[base + i];
-    s_nk[i] = 0;
-    s_first[i] = I64MAX;
-    s_last[i] = I64MIN;
-    s_sum[i] = 0;
-    s_open[i] = 0;
+
+  // round 1: keys, rows, answers; the open chain of the tile start
+  uint64_t key[AG_ITEMS];
+  uint32_t row[AG_ITEMS];
+  int32_t pr[AG_ITEMS];
+#pragma unroll
+  for (int u = 0; u < AG_ITEMS; ++u) {
+    const int i = tid + u * AG_THREADS;
+    const int64_t pc = base + (i < tn ? i : tn - 1);
+    key[u] = keys[pc];
+    row[u] = vals[pc];
+    pr[u] = a.par[pc];
+  }
+  const int32_t chv = tid < AG_CHAIN ? a.ag_chain[(int64_t)blockIdx.x * AG_CHAIN + tid] : -1;
+  const int32_t ncv = a.ag_nchain[blockIdx.x];
+  // round 2: an op's depth or a launch's kernel count (both in aux), and a
+  // launch's kernel aggregates (loaded for every row: the arrays span all
+  // rows, and one round of loads is shorter than two)
+  int32_t av[AG_ITEMS];
+  int64_t lf[AG_ITEMS], ll[AG_ITEMS];
+  uint64_t ls[AG_ITEMS];
+#pragma unroll
+  for (int u = 0; u < AG_ITEMS; ++u) {
+    av[u] = a.aux[row[u]];
+    lf[u] = a.lk_first[row[u]];
+    ll[u] = a.lk_last[row[u]];
+    ls[u] = (uint64_t)a.lk_sum[row[u]];
+  }
+  int dmin = INT32_MAX, dmax = -1;
+#pragma unroll
+  for (int u = 0; u < AG_ITEMS; ++u) {
+    const int i = tid + u * AG_THREADS;
+    if (i < tn) {
+      const bool op = key_is_op(key[u]);
+      s_par[i] = pr[u];
+      s_dep[i] = op ? av[u] : -1;
+      s_nk[i] = 0;
+      s_first[i] = I64MAX;
+      s_last[i] = I64MIN;
+      s_sum[i] = 0;
+      s_open[i] = 0;
+      if (op) {
+        dmin = av[u] < dmin ? av[u] : dmin;
+        dmax = av[u] > dmax ? av[u] : dmax;
+      }
+    }
   }
   if (tid < AG_CHAIN) {
+    s_chain[tid] = chv;
     c_nk[tid] = 0;
     c_first[tid] = I64MAX;
     c_last[tid] = I64MIN;
     c_sum[tid] = 0;
   }
   if (tid == 0) {
-    // stack after the element before the tile: that element (if an op) and
-    // its answer chain
-    int nc = 0;
-    if (base > 0) {
-      int64_t q = key_is_op(keys[base - 1]) ? base - 1 : a.par[base - 1];
-      while (q >= 0) {
-        if (nc < AG_CHAIN) s_chain[nc] = (int32_t)q;
-        ++nc;
-        q = a.par[q];
-      }
-    }
-    s_nchain = nc;
+    s_dmin = INT32_MAX;
+    s_dmax = -1;
+  }
+  for (int d = 1; d < WAVE; d <<= 1) {
+    const int o1 = __shfl_xor(dmin, d, WAVE), o2 = __shfl_xor(dmax, d, WAVE);
+    dmin = o1 < dmin ? o1 : dmin;
+    dmax = o2 > dmax ? o2 : dmax;
   }
   __syncthreads();
+  if (lane == 0) {
+    atomicMin(&s_dmin, dmin);
+    atomicMax(&s_dmax, dmax);
+  }
   if (tid == 0) {
     // ops of this tile still open at its end receive later contributions
     const int64_t last = tn - 1;
-    int64_t q = key_is_op(keys[base + last]) ? base + last : s_par[last];
+    int64_t q = s_dep[last] >= 0 ? base + last : s_par[last];
     while (q >= base) {
       s_open[q - base] = 1;
       q = s_par[q - base];
     }
   }
-  const int nc = s_nchain;
-  __syncthreads();
-  for (int64_t i = tid; i < tn; i += 256) {
-    const int64_t p = base + i;
-    const uint64_t key = keys[p];
-    if (key_is_op(key)) continue;
-    const uint32_t row = vals[p];
-    const int32_t nkl = a.aux[row];  // kernels joined to this launch
-    if (nkl <= 0) continue;
-    const int64_t f = a.lk_first[row], l = a.lk_last[row];
-    const uint64_t sm = (uint64_t)a.lk_sum[row];
-    int64_t q = s_par[i];
-    while (q >= base) {
-      const int64_t li = q - base;
-      atomicAdd(&s_nk[li], (uint32_t)nkl);
+  // Adds (count, first, last, sum) to the op at sorted position q: in LDS
+  // when q lies in the tile, to the table of ops open at the tile start when
+  // it lies before it, and to HBM beyond the table.  (The LDS arrays are
+  // named here, not passed by pointer, so that these stay LDS atomics.)
+  const int kn0 = ncv < AG_CHAIN ? ncv : AG_CHAIN;
+  auto add = [&](int64_t q, uint32_t nk, int64_t f, int64_t l, uint64_t sm) {
+    if (q >= base) {
+      const int li = (int)(q - base);
+      atomicAdd(&s_nk[li], nk);
       atomicMin((long long*)&s_first[li], (long long)f);
       atomicMax((long long*)&s_last[li], (long long)l);
       atomicAdd((unsigned long long*)&s_sum[li], (unsigned long long)sm);
-      q = s_par[li];
+      return;
     }
-    if (q >= 0) {
-      int k = 0;
-      while (k < nc && k < AG_CHAIN && s_chain[k] != q) ++k;
-      if (k < nc && k < AG_CHAIN) {
-        for (int c = k; c < nc && c < AG_CHAIN; ++c) {
-          atomicAdd(&c_nk[c], (uint32_t)nkl);
-          atomicMin((long long*)&c_first[c], (long long)f);
-          atomicMax((long long*)&c_last[c], (long long)l);
-          atomicAdd((unsigned long long*)&c_sum[c], (unsigned long long)sm);
-        }
-      }
-      if (nc > AG_CHAIN) {
-        // chain deeper than the table: walk the rest in HBM
-        int64_t r = k < nc && k < AG_CHAIN ? (int64_t)s_chain[AG_CHAIN - 1] : q;
-        if (k < nc && k < AG_CHAIN) r = a.par[r];
-        while (r >= 0) {
-          const uint32_t rr = vals[r];
-          atomicAdd(&a.op_nkern[rr], nkl);
-          atomicMin((long long*)&a.op_first[rr], (long long)f);
-          atomicMax((long long*)&a.op_last[rr], (long long)l);
-          atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)sm);
-          r = a.par[r];
-        }
+    if (q < 0) return;
+    int k = 0;
+    while (k < kn0 && s_chain[k] != q) ++k;
+    if (k < kn0) {
+      atomicAdd(&c_nk[k], nk);
+      atomicMin((long long*)&c_first[k], (long long)f);
+      atomicMax((long long*)&c_last[k], (long long)l);
+      atomicAdd((unsigned long long*)&c_sum[k], (unsigned long long)sm);
+      return;
+    }
+    agg_add_global(a, q, nk, f, l, sm);
+  };
+  // every launch to its own op
+#pragma unroll
+  for (int u = 0; u < AG_ITEMS; ++u) {
+    const int i = tid + u * AG_THREADS;
+    if (i < tn && !key_is_op(key[u]) && av[u] > 0) add(pr[u], (uint32_t)av[u], lf[u], ll[u], ls[u]);
+  }
+  __syncthreads();
+  // every op to its parent, deepest level first
+  const int d_lo = s_dmin, d_hi = s_dmax;
+  for (int L = d_hi; L >= d_lo && L >= 0; --L) {
+#pragma unroll
+    for (int u = 0; u < AG_ITEMS; ++u) {
+      const int i = tid + u * AG_THREADS;
+      if (i < tn && s_dep[i] == L && s_nk[i] > 0)
+        add(s_par[i], s_nk[i], s_first[i], s_last[i], s_sum[i]);
+    }
+    __syncthreads();
+  }
+  const int nc = ncv;
+  const int kn = nc < AG_CHAIN ? nc : AG_CHAIN;
+  if (tid == 0) {
+    // the open ops of the tile start, innermost first: each holds what
+    // reached it or any op inside it
+    for (int k = 1; k < kn; ++k) {
+      c_nk[k] += c_nk[k - 1];
+      c_first[k] = c_first[k - 1] < c_first[k] ? c_first[k - 1] : c_first[k];
+      c_last[k] = c_last[k - 1] > c_last[k] ? c_last[k - 1] : c_last[k];
+      c_sum[k] += c_sum[k - 1];
+    }
+    // chains deeper than the table: the ops above it take the table's total
+    if (nc > AG_CHAIN && c_nk[AG_CHAIN - 1]) {
+      for (int64_t r = a.par[s_chain[AG_CHAIN - 1]]; r >= 0; r = a.par[r]) {
+        const uint32_t rr = vals[r];
+        atomicAdd(&a.op_nkern[rr], (int32_t)c_nk[AG_CHAIN - 1]);
+        atomicMin((long long*)&a.op_first[rr], (long long)c_first[AG_CHAIN - 1]);
+        atomicMax((long long*)&a.op_last[rr], (long long)c_last[AG_CHAIN - 1]);
+        atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)c_sum[AG_CHAIN - 1]);
       }
     }
   }
   __syncthreads();
-  for (int64_t i = tid; i < tn; i += 256) {
-    const int64_t p = base + i;
-    if (!key_is_op(keys[p])) continue;
-    const uint32_t rr = vals[p];
+#pragma unroll
+  for (int u = 0; u < AG_ITEMS; ++u) {
+    const int i = tid + u * AG_THREADS;
+    if (!(i < tn && key_is_op(key[u]))) continue;
+    const uint32_t rr = row[u];
     if (s_open[i]) {
       if (s_nk[i]) {
         atomicAdd(&a.op_nkern[rr], (int32_t)s_nk[i]);
@@ -626,14 +769,12 @@ __global__ __launch_bounds__(256) void k_opagg(ContainArgs a) {
       a.op_ksum[rr] = (int64_t)s_sum[i];
     }
   }
-  for (int c = tid; c < nc && c < AG_CHAIN; c += 256) {
-    if (c_nk[c]) {
-      const uint32_t rr = vals[s_chain[c]];
-      atomicAdd(&a.op_nkern[rr], (int32_t)c_nk[c]);
-      atomicMin((long long*)&a.op_first[rr], (long long)c_first[c]);
-      atomicMax((long long*)&a.op_last[rr], (long long)c_last[c]);
-      atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)c_sum[c]);
-    }
+  if (tid < kn && c_nk[tid]) {
+    const uint32_t rr = vals[s_chain[tid]];
+    atomicAdd(&a.op_nkern[rr], (int32_t)c_nk[tid]);
+    atomicMin((long long*)&a.op_first[rr], (long long)c_first[tid]);
+    atomicMax((long long*)&a.op_last[rr], (long long)c_last[tid]);
+    atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)c_sum[tid]);
   }
 }
 
@@ -675,6 +816,9 @@ static ContainArgs contain_args(Ctx& c) {
   a.lk_first = c.lk_first;
   a.lk_last = c.lk_last;
   a.lk_sum = c.lk_sum;
+  a.ag_chain = c.ag_chain;
+  a.ag_nchain = c.ag_nchain;
+  a.ag_tiles = c.ag_tiles;
   return a;
 }
 
@@ -694,7 +838,7 @@ void launch_contain(Ctx& c) {
 void launch_opagg(Ctx& c) {
   ContainArgs a = contain_args(c);
   const int64_t tiles = std::max<int64_t>(cdiv(c.sC.n_max, AG_TILE), 1);
-  hipLaunchKernelGGL(k_opagg, dim3((unsigned)tiles), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_opagg, dim3((unsigned)tiles), dim3(AG_THREADS), 0, c.st, a);
 }
 
 }  // namespace hx

@@ -13,7 +13,8 @@ namespace hx {
 struct SortBufs {
   uint64_t* k[2] = {nullptr, nullptr};
   uint32_t* v[2] = {nullptr, nullptr};
-  uint32_t* status = nullptr;           // [8 passes][tiles_max * 256]
+  uint32_t* status0 = nullptr;          // [tiles_max * 256] look-back words of digit 0
+  uint32_t* status1 = nullptr;          // [nd - 1][tiles_max * 256] digits 1..nd-1
   int64_t n_max = 0;                    // capacity (host upper bound of the count)
   int64_t tiles_max = 0;
   int nd = 0;                           // digit passes to launch (8-bit digits)
@@ -67,6 +68,9 @@ struct Ctx {
   int64_t* lk_first = nullptr;       // [n] per launch row: first start of its kernels
   int64_t* lk_last = nullptr;        // [n] last end of its kernels
   int64_t* lk_sum = nullptr;         // [n] sum of its kernels' durations
+  int32_t* ag_chain = nullptr;       // [ag_tiles * AG_CHAIN] ops open at each aggregate tile's start
+  int32_t* ag_nchain = nullptr;      // [ag_tiles] their number (may exceed AG_CHAIN)
+  int64_t ag_tiles = 0;
   uint64_t* name_part = nullptr;     // [name_blocks * NN * 4] per-block name tables
   int name_blocks = 0;
   char* zero_begin = nullptr;        // region cleared at the start of a call
@@ -80,7 +84,7 @@ size_t layout_workspace(Ctx& c, char* base);
 void launch_init(Ctx& c);
 void launch_prep(Ctx& c);
 void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k);
-void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k);
+void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k, int d0, int d1);
 void launch_names(Ctx& c);
 void launch_timeline(Ctx& c);
 void launch_overlap(Ctx& c);
@@ -99,12 +103,17 @@ int64_t union_tile_elems();
 void names_set_lds_attr();
 
 // digit histograms: keys per workgroup (at least), most workgroups per sort
-constexpr int HIST_CHUNK = 32768;
-constexpr int HIST_MAX_BLOCKS = 64;
+constexpr int HIST_CHUNK = 8192;
+constexpr int HIST_MAX_BLOCKS = 256;
 
-constexpr int RS_THREADS = 1024;
+// per-op aggregates: positions per workgroup, open ops kept per tile start
+constexpr int AG_TILE = 1024;
+constexpr int AG_CHAIN = 64;
+
+constexpr int RS_THREADS = 512;
 constexpr int RS_ITEMS = 8;
-constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 8192 keys per tile
+constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 4096 keys per tile
+constexpr int RS_WAVES_PER_EU = 6;              // three workgroups of 8 waves per CU
 
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

@@ -52,6 +52,7 @@ struct JoinArgs {
   int64_t* kmax;
   int64_t* kmin;
   int64_t cap;
+  const uint32_t* k_rows;  // admitted kernels' rows (prep's list)
 };
 
 // Smallest index in [lo, hi) whose key is >= target (hi if none); galloping
@@ -271,8 +272,10 @@ __global__ __launch_bounds__(256) void k_jt_store(JoinArgs a) {
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
     const int64_t i = i0 + u * 256;
-    key[u] = i < n ? a.k[0][i] : ~0ull;  // unsorted: the join sort did not run
-    row[u] = i < n ? a.v[0][i] : 0u;
+    const int64_t ic = i < n ? i : (n > 0 ? n - 1 : 0);  // clamped: the loads stay in flight together
+    key[u] = a.k[0][ic];  // unsorted: the join sort did not run
+    row[u] = a.v[0][ic];
+    if (i >= n) key[u] = ~0ull;
   }
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
@@ -304,14 +307,18 @@ __global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
     const int64_t i = i0 + u * 256;
-    key[u] = i < n ? a.k[0][i] : ~0ull;
-    row[u] = i < n ? a.v[0][i] : 0u;
+    const int64_t ic = i < n ? i : (n > 0 ? n - 1 : 0);
+    key[u] = a.k[0][ic];
+    row[u] = a.v[0][ic];
+    if (i >= n) key[u] = ~0ull;
   }
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
     slot[u] = key[u] != ~0ull ? jt_slot(a.ds, key[u]) : -1;
     const bool ok = slot[u] >= 0 && in_range(a.ds, slot[u], a.cap);
-    w[u] = !ok ? row[u] : (key[u] & 1) ? a.own[slot[u]] : a.tab[slot[u]];
+    const int64_t sc = ok ? slot[u] : 0;
+    const uint32_t wo = a.own[sc], wt = a.tab[sc];
+    w[u] = !ok ? row[u] : (key[u] & 1) ? wo : wt;
   }
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
@@ -341,8 +348,10 @@ __global__ __launch_bounds__(256) void k_jt_fix(JoinArgs a) {
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
     const int64_t i = i0 + u * 256;
-    key[u] = i < n ? a.k[0][i] : 1ull;  // past the end: treated as a kernel
-    row[u] = i < n ? a.v[0][i] : 0u;
+    const int64_t ic = i < n ? i : (n > 0 ? n - 1 : 0);
+    key[u] = a.k[0][ic];
+    row[u] = a.v[0][ic];
+    if (i >= n) key[u] = 1ull;  // past the end: treated as a kernel
   }
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
@@ -364,6 +373,9 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
   __syncthreads();
   if (!a.ds->join_direct) return;
   const int64_t n = a.ds->nJ;
+  // Positions past the end take the last entry's row (clamped loads); with
+  // no entry there is no row to take, and nothing to do.
+  if (n == 0) return;
   const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + tid;
   uint32_t c[JC_N] = {};
   uint64_t key[JT_ITEMS];
@@ -371,8 +383,10 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
     const int64_t i = i0 + u * 256;
-    key[u] = i < n ? a.k[0][i] : 0ull;  // past the end: treated as a launch (skipped)
-    row[u] = i < n ? a.v[0][i] : 0u;
+    const int64_t ic = i < n ? i : n - 1;
+    key[u] = a.k[0][ic];
+    row[u] = a.v[0][ic];
+    if (i >= n) key[u] = 0ull;  // past the end: treated as a launch (skipped)
   }
   // round 2: the slot's launch and kernel count, the kernel's times
   int64_t slot[JT_ITEMS], ts[JT_ITEMS], te[JT_ITEMS];
@@ -383,15 +397,23 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
     const bool kern = (key[u] & 1) != 0;
     slot[u] = kern ? jt_slot(a.ds, key[u]) : -1;
     const bool ok = slot[u] >= 0 && in_range(a.ds, slot[u], a.cap);
-    l[u] = ok ? a.tab[slot[u]] : ~0u;
-    single[u] = ok && a.multi[slot[u]] == 0;
-    ts[u] = kern ? a.ts[row[u]] : 0;
-    te[u] = kern ? a.te[row[u]] : 0;
+    const int64_t sc = ok ? slot[u] : 0;
+    const uint32_t lt = a.tab[sc];
+    const uint8_t mu = a.multi[sc];
+    const int64_t t0 = a.ts[row[u]], t1 = a.te[row[u]];
+    l[u] = ok ? lt : ~0u;
+    single[u] = ok && mu == 0;
+    ts[u] = kern ? t0 : 0;
+    te[u] = kern ? t1 : 0;
   }
   // round 3: the launch's start
   int64_t lts[JT_ITEMS];
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) lts[u] = (key[u] & 1) && l[u] != ~0u ? a.ts[l[u]] : 0;
+  for (int u = 0; u < JT_ITEMS; ++u) {
+    const bool has = (key[u] & 1) && l[u] != ~0u;
+    const int64_t t = a.ts[has ? l[u] : 0u];
+    lts[u] = has ? t : 0;
+  }
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
     if (!(key[u] & 1)) continue;
@@ -438,33 +460,36 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
 }
 
 // Kernel -> op: the op of the kernel's launch (containment and the join run
-// concurrently; this pass follows both).  Counts matched kernels whose launch
-// has no op.
+// concurrently; this pass follows both).  Walks prep's list of the admitted
+// kernels' rows; counts matched kernels whose launch has no op.  Each round
+// of gathers is issued for all of a thread's kernels together.
 __global__ __launch_bounds__(256) void k_join_ops(JoinArgs a) {
   __shared__ unsigned long long s_c[JC_N];
   const int tid = threadIdx.x;
   if (tid < JC_N) s_c[tid] = 0;
   __syncthreads();
-  const int64_t n = a.ds->nJ;
-  const int par = (int)a.ds->sort_parity[1];
+  const int64_t n = a.ds->nK;
+  // Positions past the end take the last kernel's row (clamped loads); with
+  // no admitted kernel there is no row to take, and nothing to do.
+  if (n == 0) return;
   const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + tid;
   uint32_t c[JC_N] = {};
   uint32_t row[JT_ITEMS];
-  int32_t l[JT_ITEMS];
+  int32_t l[JT_ITEMS], op[JT_ITEMS];
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
     const int64_t i = i0 + u * 256;
-    const bool kern = i < n && (a.k[par][i] & 1);
-    row[u] = kern ? a.v[par][i] : ~0u;
+    row[u] = a.k_rows[i < n ? i : n - 1];
   }
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) l[u] = row[u] != ~0u ? a.link[row[u]] : -1;
+  for (int u = 0; u < JT_ITEMS; ++u) l[u] = a.link[row[u]];
+#pragma unroll
+  for (int u = 0; u < JT_ITEMS; ++u) op[u] = a.link[l[u] >= 0 ? l[u] : 0];
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
-    if (l[u] < 0) continue;
-    const int32_t op = a.link[l[u]];
-    a.aux[row[u]] = op;
-    if (op < 0) ++c[JC_UNATTR];
+    if (i0 + u * 256 >= n || l[u] < 0) continue;
+    a.aux[row[u]] = op[u];
+    if (op[u] < 0) ++c[JC_UNATTR];
   }
   jt_flush(a, c, s_c, nullptr);
 }
@@ -566,6 +591,7 @@ static JoinArgs join_args(Ctx& c) {
   a.kmax = c.jt_kmax;
   a.kmin = c.jt_kmin;
   a.cap = c.jt_cap;
+  a.k_rows = c.k_rows;
   return a;
 }
 

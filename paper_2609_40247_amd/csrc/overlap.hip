@@ -39,7 +39,7 @@ struct SweepArgs {
   int64_t* any_busy;
 };
 
-__device__ __forceinline__ void add_interval(const SweepArgs& a, uint64_t m, int64_t len, int pid, int pid0,
+__device__ __attribute__((always_inline)) inline void add_interval(const SweepArgs& a, uint64_t m, int64_t len, int pid, int pid0,
                                              const uint64_t* cmask, unsigned long long* s_pair,
                                              unsigned long long* s_cls) {
   if (len <= 0 || m == 0) return;
@@ -64,18 +64,19 @@ __device__ __forceinline__ void add_interval(const SweepArgs& a, uint64_t m, int
         if (present[c2]) atomicAdd((unsigned long long*)&a.class_overlap[(pid * 3 + c) * 3 + c2], (unsigned long long)len);
     }
   }
-  uint64_t mi = m;
-  while (mi) {
-    const int i = __ffsll((unsigned long long)mi) - 1;
-    mi &= mi - 1;
-    uint64_t mj = m;
-    while (mj) {
-      const int j = __ffsll((unsigned long long)mj) - 1;
-      mj &= mj - 1;
-      if (local)
-        atomicAdd(&s_pair[i * S + j], (unsigned long long)len);
-      else
-        atomicAdd((unsigned long long*)&a.pair[((int64_t)pid * S + i) * S + j], (unsigned long long)len);
+  // separate loops for LDS and HBM, so that neither becomes a flat atomic
+  if (local) {
+    for (uint64_t mi = m; mi; mi &= mi - 1) {
+      const int i = __ffsll((unsigned long long)mi) - 1;
+      for (uint64_t mj = m; mj; mj &= mj - 1)
+        atomicAdd(&s_pair[i * S + __ffsll((unsigned long long)mj) - 1], (unsigned long long)len);
+    }
+  } else {
+    for (uint64_t mi = m; mi; mi &= mi - 1) {
+      const int i = __ffsll((unsigned long long)mi) - 1;
+      for (uint64_t mj = m; mj; mj &= mj - 1)
+        atomicAdd((unsigned long long*)&a.pair[((int64_t)pid * S + i) * S + __ffsll((unsigned long long)mj) - 1],
+                  (unsigned long long)len);
     }
   }
 }

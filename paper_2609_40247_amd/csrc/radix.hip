@@ -1,9 +1,9 @@
 // LSD radix sort of 64-bit keys (optionally with a 32-bit payload) for CDNA4.
 //
-// One launch per 8-bit digit, shared by the independent sorts of a call.  Each workgroup ranks a tile of 8192 keys with
+// One launch per 8-bit digit, shared by the independent sorts of a call.  Each workgroup ranks a tile of 4096 keys with
 // wave64 ballots (a 64-lane match of the digit built from 8 ballots gives the
 // rank among equal digits in one step), publishes its 256 per-digit counts
-// through a decoupled look-back (one chain per digit, four lanes per digit),
+// through a decoupled look-back (one chain per digit, two lanes per digit),
 // reorders the tile in LDS and writes each digit's run contiguously.  The
 // global offset of each digit comes from a histogram of all digits taken in
 // one pass before the first digit pass.  A digit on which every key agrees
@@ -33,44 +33,52 @@ struct HistJobs {
 // and stores its table; the plan kernel that follows sums the tables.  No
 // global atomics and no fences: counters shared by many workgroups serialise
 // on their cache line, and a device-scope fence writes back the whole L2.
-constexpr int HIST_THREADS = 1024;
+// The grid is sized so that every CU holds a share (HIST_CHUNK keys at
+// least per workgroup, HIST_MAX_BLOCKS at most per sort).
+//
+// Each thread takes HIST_U consecutive keys per round.  Digits 0 and 1 of
+// these keys (nanoseconds, correlation ids) differ from key to key: every
+// key adds one to its bin.  Higher digits change rarely between neighbouring
+// records, and lanes adding to one LDS word are served one after another:
+// a thread adds each run of equal digits once, with the run's length.
+// Everything is vector code: the CU's one scalar unit would otherwise be
+// shared by all of its waves.
+constexpr int HIST_THREADS = 512;
+constexpr int HIST_U = 16;
 
-// Adds one key's ND digits to the LDS table.  Digits 0 and 1 of these keys
-// (nanoseconds, correlation ids) differ across a wave, so every lane adds;
-// for higher digits, when the whole wave agrees, one lane adds the count.
 template <int ND>
-__device__ __forceinline__ void hist_add(uint32_t* h, uint64_t k) {
-  const uint32_t lo = (uint32_t)k, hi = (uint32_t)(k >> 32);
-  const uint64_t active = ballot(true);
-  const bool leader = lane_id() == __ffsll((unsigned long long)active) - 1;
+__device__ __forceinline__ void hist_range(uint32_t* h, const uint64_t* __restrict__ keys, int64_t lo, int64_t hi) {
+  for (int64_t i0 = lo + (int64_t)threadIdx.x * HIST_U; i0 < hi; i0 += (int64_t)HIST_U * HIST_THREADS) {
+    // clamped, not branched on: every load of the round is in flight together
+    uint64_t k[HIST_U];
 #pragma unroll
-  for (int d = 0; d < ND; ++d) {
-    const uint32_t dg = ((d < 4 ? lo : hi) >> (8 * (d & 3))) & 255u;
-    if (d < 2) {
-      atomicAdd(&h[d * 256 + dg], 1u);
-    } else {
-      const uint32_t d0 = __builtin_amdgcn_readfirstlane(dg);
-      if (ballot(dg != d0) == 0) {
-        if (leader) atomicAdd(&h[d * 256 + d0], (uint32_t)popc(active));
+    for (int u = 0; u < HIST_U; ++u) k[u] = keys[min(i0 + u, hi - 1)];
+    const int nv = (int)min<int64_t>(HIST_U, hi - i0);  // valid keys of this thread
+#pragma unroll
+    for (int d = 0; d < ND; ++d) {
+      const int sh = 8 * d;
+      if (d < 2) {
+#pragma unroll
+        for (int u = 0; u < HIST_U; ++u)
+          if (u < nv) atomicAdd(&h[d * 256 + (uint32_t)((k[u] >> sh) & 255)], 1u);
       } else {
-        atomicAdd(&h[d * 256 + dg], 1u);
+        uint32_t cur = (uint32_t)((k[0] >> sh) & 255), run = 1;
+#pragma unroll
+        for (int u = 1; u < HIST_U; ++u) {
+          const uint32_t v = (uint32_t)((k[u] >> sh) & 255);
+          if (u < nv) {
+            if (v != cur) {
+              atomicAdd(&h[d * 256 + cur], run);
+              cur = v;
+              run = 0;
+            }
+            ++run;
+          }
+        }
+        atomicAdd(&h[d * 256 + cur], run);
       }
     }
   }
-}
-
-template <int ND>
-__device__ void hist_range(uint32_t* h, const uint64_t* __restrict__ keys, int64_t lo, int64_t hi) {
-  constexpr int U = 8;  // loads in flight per thread
-  int64_t i = lo + threadIdx.x;
-  for (; i + (U - 1) * HIST_THREADS < hi; i += U * HIST_THREADS) {
-    uint64_t k[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) k[u] = keys[i + u * HIST_THREADS];
-#pragma unroll
-    for (int u = 0; u < U; ++u) hist_add<ND>(h, k[u]);
-  }
-  for (; i < hi; i += HIST_THREADS) hist_add<ND>(h, keys[i]);
 }
 
 __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, const DevState* ds) {
@@ -102,34 +110,54 @@ __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, cons
 }
 
 // Plan of one digit of one sort (blockIdx.x = digit, blockIdx.y = sort):
-// the digit's counts summed over the workgroup tables, its trivial flag
-// (one bin holds every key) and each bin's exclusive offset.
-__global__ __launch_bounds__(256) void k_hist_plan(HistJobs jobs, DevState* ds) {
-  __shared__ uint32_t s_scan[256 / WAVE + 1];
+// the digit's counts summed over the workgroup tables (four threads per
+// bin, each summing every fourth table, 16 loads in flight), its trivial
+// flag (one bin holds every key) and each bin's exclusive offset.
+constexpr int PLAN_THREADS = 1024;
+constexpr int PLAN_GROUPS = PLAN_THREADS / 256;
+
+__global__ __launch_bounds__(PLAN_THREADS) void k_hist_plan(HistJobs jobs, DevState* ds) {
+  __shared__ uint32_t s_part[PLAN_GROUPS][256];
+  __shared__ uint32_t s_scan[PLAN_THREADS / WAVE + 1];
   const HistJob jb = jobs.j[blockIdx.y];
   const int d = blockIdx.x;
   if (d >= jb.nd || (jb.id == 1 && ds->join_direct)) return;
   const int64_t n = *jb.count;
   const int nblk = hist_blocks(n);
-  const uint32_t* src = jobs.part + (int64_t)jb.id * HIST_MAX_BLOCKS * 8 * 256 + d * 256 + threadIdx.x;
+  const int bin = threadIdx.x & 255, grp = threadIdx.x >> 8;
+  const uint32_t* src = jobs.part + (int64_t)jb.id * HIST_MAX_BLOCKS * 8 * 256 + d * 256 + bin;
   uint32_t c = 0;
-  for (int b0 = 0; b0 < nblk; b0 += 16) {
+  for (int b0 = grp; b0 < nblk; b0 += 16 * PLAN_GROUPS) {
     uint32_t v[16];
 #pragma unroll
-    for (int b = 0; b < 16; ++b) v[b] = b0 + b < nblk ? src[(int64_t)(b0 + b) * 8 * 256] : 0u;
+    for (int b = 0; b < 16; ++b) {
+      const int blk = b0 + b * PLAN_GROUPS;
+      v[b] = src[(int64_t)min(blk, nblk - 1) * 8 * 256];
+      v[b] = blk < nblk ? v[b] : 0u;
+    }
 #pragma unroll
     for (int b = 0; b < 16; ++b) c += v[b];
   }
-  if (__syncthreads_or(c == (uint32_t)n) && threadIdx.x == 0) atomicOr(&ds->sort_trivial[jb.id], 1u << d);
-  const uint32_t ex = block_excl_sum<256>(c, s_scan, nullptr);
-  ds->hist[jb.id][d][threadIdx.x] = ex;
+  s_part[grp][bin] = c;
+  __syncthreads();
+  if (threadIdx.x < 256) {
+    c = 0;
+#pragma unroll
+    for (int g = 0; g < PLAN_GROUPS; ++g) c += s_part[g][bin];
+  }
+  // every thread joins the barriers below; only the first 256 carry a bin
+  const bool full = threadIdx.x < 256 && c == (uint32_t)n;
+  if (__syncthreads_or(full) && threadIdx.x == 0) atomicOr(&ds->sort_trivial[jb.id], 1u << d);
+  const uint32_t ex = block_excl_sum<PLAN_THREADS>(threadIdx.x < 256 ? c : 0u, s_scan, nullptr);
+  if (threadIdx.x < 256) ds->hist[jb.id][d][bin] = ex;
 }
 
 struct SortJob {
   uint64_t* k[2];
   uint32_t* v[2];
   const int32_t* count;
-  uint32_t* status;  // [nd][tiles_max * 256]
+  uint32_t* status0;  // [tiles_max * 256] look-back words of digit 0 (cleared by the init kernel)
+  uint32_t* status1;  // [nd - 1][tiles_max * 256] digits 1.. (each cleared by the previous pass)
   int64_t tiles_max;
   int nd, id;
 };
@@ -138,37 +166,53 @@ struct SortJobs {
 };
 
 // One digit pass of up to N_SORTS independent sorts (blockIdx.y picks one).
-__global__ __launch_bounds__(RS_THREADS) void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
-  constexpr int NW = RS_THREADS / WAVE;     // waves per workgroup
-  constexpr int NSL = RS_THREADS / 256;     // look-back slices per digit
+// 512 threads rank a tile of 4096 keys; the tile (48 KB) and the per-wave
+// digit counts (8 KB, in the key area until the keys are placed) keep the
+// LDS of a workgroup under a third of the CU's (with the allocation
+// granularity), so three tiles share a CU and a launch of up to 768 tiles
+// has every tile resident at once.
+constexpr int RS_NW = RS_THREADS / WAVE;  // waves per workgroup
+constexpr int RS_NSL = RS_THREADS / 256;  // look-back slices per digit
+constexpr int RS_LB_WIN = 16;             // predecessors polled per slice and round trip
+
+__global__ __launch_bounds__(RS_THREADS) __attribute__((amdgpu_waves_per_eu(RS_WAVES_PER_EU)))
+void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
+  constexpr int NW = RS_NW, NSL = RS_NSL, LB_WIN = RS_LB_WIN;
   __shared__ uint64_t s_key[RS_TILE];
   __shared__ uint32_t s_val[RS_TILE];
-  __shared__ uint32_t s_wh[NW][256];
   __shared__ uint32_t s_local[256];
-  __shared__ uint32_t s_glob[256];
   __shared__ uint32_t s_scan[NW + 1];
   __shared__ uint32_t s_lb_sum[NSL][256];
   __shared__ uint8_t s_lb_state[NSL][256];
   __shared__ int s_tile;
+  static_assert(NW * 256 * 4 <= RS_TILE * 8, "per-wave counts must fit the key area");
+  uint32_t(*s_wh)[256] = reinterpret_cast<uint32_t(*)[256]>(s_key);
+  // the global offsets reuse the look-back's scratch once the look-back is over
+  uint32_t* s_glob = &s_lb_sum[0][0];
 
   const SortJob& jb = jobs.j[blockIdx.y];
   if (d >= jb.nd) return;
   const int id = jb.id;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int dgt = tid & 255, slice = tid >> 8;
+  const uint32_t n = (uint32_t)*jb.count;
+  const bool has_tile = (int64_t)blockIdx.x * RS_TILE < (int64_t)n;
+  // The next digit's look-back words of this workgroup's tile index are
+  // cleared here: the next pass starts only after this one has ended.
+  if (has_tile && d + 1 < jb.nd && tid < 256)
+    jb.status1[((int64_t)d * jb.tiles_max + blockIdx.x) * 256 + tid] = 0u;
   // The plan (trivial digits, offsets) was made by the histogram kernel.  A
   // digit is trivial iff one bin holds every key; the input buffer's parity
   // is the number of non-trivial digits below this one.  Workgroups with no
   // tile to sort leave before the ticket: the ticket counter is one address,
   // and every request to it is served in turn.  The first cdiv(n, tile)
   // workgroups stay, so they draw exactly the tickets of the real tiles.
-  const uint32_t n = (uint32_t)*jb.count;
   const uint32_t triv = ds->sort_trivial[id];
-  const uint32_t gexcl = ds->hist[id][d][dgt];
   // which buffer holds the result: parity of the digits that move data
   if (d == 0 && blockIdx.x == 0 && tid == 0)
     ds->sort_parity[id] = (uint32_t)(popc(~triv & ((jb.nd >= 32 ? 0u : 1u << jb.nd) - 1u)) & 1);
-  if (((triv >> d) & 1) || (int64_t)blockIdx.x * RS_TILE >= (int64_t)n) return;
+  if (((triv >> d) & 1) || !has_tile) return;
+  const uint32_t gexcl = ds->hist[id][d][dgt];
   if (tid == 0) s_tile = (int)atomicAdd(&ds->ticket[TK_RADIX + 8 * id + d], 1u);
   for (int i = tid; i < NW * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
   __syncthreads();
@@ -177,45 +221,47 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(SortJobs jobs, DevSta
   uint64_t* kout = jb.k[parity ^ 1];
   const uint32_t* vin = jb.v[parity];
   uint32_t* vout = jb.v[parity ^ 1];
-  uint32_t* status = jb.status + (int64_t)d * jb.tiles_max * 256;
+  uint32_t* status = d == 0 ? jb.status0 : jb.status1 + (int64_t)(d - 1) * jb.tiles_max * 256;
   const int tile = s_tile;
   const int64_t base = (int64_t)tile * RS_TILE;
 
   const int shift = 8 * d;
   uint64_t key[RS_ITEMS];
   uint32_t val[RS_ITEMS];
-  uint32_t rank[RS_ITEMS];
-  int dig[RS_ITEMS];
+  uint32_t rank[RS_ITEMS];  // rank among the wave's equal digits, then the tile position
   // each wave owns RS_ITEMS * 64 consecutive keys, item j of lane l at j*64+l
-  const int64_t wbase = base + (int64_t)wv * (RS_ITEMS * WAVE);
+  // 32-bit offsets from the uniform buffer bases (n < 2^30)
+  const uint32_t wbase = (uint32_t)base + (uint32_t)wv * (RS_ITEMS * WAVE) + (uint32_t)lane;
+  // Loads past the end read the last key instead (the index is clamped, not
+  // branched on, so that all of them are in flight together); such items
+  // carry digit 256 and are never placed.
 #pragma unroll
   for (int j = 0; j < RS_ITEMS; ++j) {
-    const int64_t idx = wbase + j * WAVE + lane;
-    const bool ok = idx < (int64_t)n;
-    key[j] = ok ? kin[idx] : 0ull;
-    val[j] = ok ? vin[idx] : 0u;
+    const uint32_t idx = min(wbase + j * WAVE, n - 1);
+    key[j] = kin[idx];
+    val[j] = vin[idx];
   }
-#pragma unroll
-  for (int j = 0; j < RS_ITEMS; ++j) {
-    const int64_t idx = wbase + j * WAVE + lane;
-    dig[j] = idx < (int64_t)n ? (int)((key[j] >> shift) & 255) : 256;
-  }
+  // an item's digit is re-derived from its key where needed (256: past the end)
+  auto digit_of = [&](int j) -> int {
+    return wbase + j * WAVE < n ? (int)((key[j] >> shift) & 255) : 256;
+  };
   // Wave-private ranking in input order: items in order, lanes in order.
   const uint64_t lt = lanemask_lt();
 #pragma unroll
   for (int j = 0; j < RS_ITEMS; ++j) {
-    const bool ok = dig[j] < 256;
+    const int dg = digit_of(j);
+    const bool ok = dg < 256;
     uint64_t peers = ballot(ok);
 #pragma unroll
     for (int b = 0; b < 8; ++b) {
-      const bool bit = (dig[j] >> b) & 1;
+      const bool bit = (dg >> b) & 1;
       const uint64_t bb = ballot(bit);
       peers &= bit ? bb : ~bb;
     }
-    const uint32_t before = ok ? s_wh[wv][dig[j]] : 0u;
+    const uint32_t before = ok ? s_wh[wv][dg] : 0u;
     rank[j] = before + (uint32_t)popc(peers & lt);
     __builtin_amdgcn_wave_barrier();
-    if (ok && (peers & lt) == 0) s_wh[wv][dig[j]] = before + (uint32_t)popc(peers);
+    if (ok && (peers & lt) == 0) s_wh[wv][dg] = before + (uint32_t)popc(peers);
     __builtin_amdgcn_wave_barrier();
   }
   __syncthreads();
@@ -230,10 +276,28 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(SortJobs jobs, DevSta
       cnt += c;
     }
   }
-  uint32_t* st = status + (int64_t)tile * 256;
+  uint32_t* st = status + (uint32_t)tile * 256u;
   if (tid < 256) st_agent(&st[tid], (tile == 0 ? RS_FLAG_P : RS_FLAG_A) | cnt);
   const uint32_t local_excl = block_excl_sum<RS_THREADS>(cnt, s_scan, nullptr);
   if (tid < 256) s_local[tid] = local_excl;
+  __syncthreads();
+
+  // Tile positions (the per-wave offsets still sit in the key area), then
+  // the tile is reordered in LDS before the look-back, so that no key or row
+  // stays in a register while the predecessors are polled.
+#pragma unroll
+  for (int j = 0; j < RS_ITEMS; ++j) {
+    const int dg = digit_of(j);
+    if (dg < 256) rank[j] += s_local[dg] + s_wh[wv][dg];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < RS_ITEMS; ++j) {
+    if (digit_of(j) < 256 && in_range(ds, rank[j], RS_TILE)) {
+      s_key[rank[j]] = key[j];
+      s_val[rank[j]] = val[j];
+    }
+  }
 
   // Look-back: every digit has NSL threads, each polling LB_WIN predecessors
   // per round trip (independent loads), so one round covers NSL * LB_WIN
@@ -242,7 +306,6 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(SortJobs jobs, DevSta
   // polled again.  The loop condition is uniform over the workgroup.
   uint32_t excl = 0;
   if (tile > 0) {
-    constexpr int LB_WIN = 16;
     int pred = tile - 1;  // newest predecessor not yet counted
     bool done = false;
     uint32_t spins = 0;
@@ -254,15 +317,15 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(SortJobs jobs, DevSta
         uint32_t sv[LB_WIN];
 #pragma unroll
         for (int i = 0; i < LB_WIN; ++i)
-          sv[i] = top - i >= 0 ? ld_agent(&status[(int64_t)(top - i) * 256 + dgt]) : RS_FLAG_P;
+          sv[i] = ld_agent(&status[(uint32_t)max(top - i, 0) * 256u + (uint32_t)dgt]);
 #pragma unroll
         for (int i = 0; i < LB_WIN; ++i) {
-          const uint32_t f = sv[i] >> 30;
+          const uint32_t f = top - i >= 0 ? sv[i] >> 30 : 2u;  // before tile 0: prefix 0
           if (state == 1) {
             if (f == 0) {
               state = 0;
             } else {
-              sum += sv[i] & RS_VAL;
+              sum += top - i >= 0 ? sv[i] & RS_VAL : 0u;
               if (f == 2) state = 2;
             }
           }
@@ -306,19 +369,8 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_pass(SortJobs jobs, DevSta
     }
     if (tid < 256) st_agent(&st[tid], RS_FLAG_P | ((excl + cnt) & RS_VAL));
   }
+  // the look-back loop ends on a barrier after its last read of s_lb_sum
   if (tid < 256) s_glob[tid] = gexcl + excl;
-  __syncthreads();
-
-#pragma unroll
-  for (int j = 0; j < RS_ITEMS; ++j) {
-    if (dig[j] < 256) {
-      const uint32_t pos = s_local[dig[j]] + s_wh[wv][dig[j]] + rank[j];
-      if (in_range(ds, pos, RS_TILE)) {
-        s_key[pos] = key[j];
-        s_val[pos] = val[j];
-      }
-    }
-  }
   __syncthreads();
 
   const uint32_t tile_n = (uint32_t)min((int64_t)RS_TILE, (int64_t)n - base);
@@ -347,21 +399,24 @@ void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
   if (m == 0) return;
   const int64_t grid = std::min<int64_t>(cdiv(n_max, HIST_CHUNK), HIST_MAX_BLOCKS);
   hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid, (unsigned)m), dim3(HIST_THREADS), 0, c.st, jobs, c.ds);
-  hipLaunchKernelGGL(k_hist_plan, dim3((unsigned)nd, (unsigned)m), dim3(256), 0, c.st, jobs, c.ds);
+  hipLaunchKernelGGL(k_hist_plan, dim3((unsigned)nd, (unsigned)m), dim3(PLAN_THREADS), 0, c.st, jobs, c.ds);
 }
 
-void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k) {
-  SortJobs jobs{};
-  int64_t grid = 1;
-  int nd = 0;
-  for (int i = 0; i < k; ++i) {
-    jobs.j[i] = SortJob{{s[i]->k[0], s[i]->k[1]}, {s[i]->v[0], s[i]->v[1]}, count[i], s[i]->status,
-                        s[i]->tiles_max, s[i]->nd, s[i]->id};
-    grid = std::max<int64_t>(grid, s[i]->tiles_max);
-    nd = std::max(nd, s[i]->nd);
+// Digit passes d0 .. d1-1 of up to N_SORTS sorts, one launch per digit.
+void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k, int d0, int d1) {
+  for (int d = d0; d < d1; ++d) {
+    SortJobs jobs{};
+    int64_t grid = 1;
+    int m = 0;
+    for (int i = 0; i < k; ++i) {
+      if (d >= s[i]->nd) continue;
+      jobs.j[m++] = SortJob{{s[i]->k[0], s[i]->k[1]}, {s[i]->v[0], s[i]->v[1]}, count[i], s[i]->status0,
+                            s[i]->status1, s[i]->tiles_max, s[i]->nd, s[i]->id};
+      grid = std::max<int64_t>(grid, s[i]->tiles_max);
+    }
+    if (m == 0) continue;
+    hipLaunchKernelGGL(k_radix_pass, dim3((unsigned)grid, (unsigned)m), dim3(RS_THREADS), 0, c.st, jobs, c.ds, d);
   }
-  for (int d = 0; d < nd; ++d)
-    hipLaunchKernelGGL(k_radix_pass, dim3((unsigned)grid, (unsigned)k), dim3(RS_THREADS), 0, c.st, jobs, c.ds, d);
 }
 
 }  // namespace hx

@@ -48,21 +48,6 @@ struct Elem {
   int64_t s, e;   // start and clipped end, relative to W0
 };
 
-__device__ __forceinline__ Elem load_elem(const UnionArgs& a, const uint64_t* keys, const uint32_t* vals, int64_t i) {
-  Elem x;
-  const uint64_t key = keys[i];
-  const uint32_t row = vals[i];
-  const uint64_t segbits = key >> a.wb;
-  const int32_t pid = (int32_t)(segbits >> a.sb);
-  const int32_t stream = (int32_t)(segbits & ((1u << a.sb) - 1));
-  x.seg = pid * a.S + stream;
-  x.s = (int64_t)(key & ((1ull << a.wb) - 1));
-  const int64_t o = a.off ? a.off[pid] : 0;
-  const int64_t tec = a.te[row] - o;  // corrected end; may lie far beyond W1
-  x.e = tec >= a.W1 ? a.W : tec - a.W0;
-  return x;
-}
-
 __device__ __forceinline__ int32_t seg_of_key(const UnionArgs& a, uint64_t key) {
   const uint64_t segbits = key >> a.wb;
   return (int32_t)(segbits >> a.sb) * a.S + (int32_t)(segbits & ((1u << a.sb) - 1));
@@ -210,22 +195,63 @@ __global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
   if (tid < 64) s_busy[tid] = 0;
   if (tid == 0) s_seg0 = seg_of_key(a, keys[base]);
 
+  // The thread's UN_ITEMS consecutive keys and rows (16-byte loads when the
+  // thread's group lies inside the list, clamped single loads at its end),
+  // then every end-time and clock-offset gather, so that each round of loads
+  // is in flight together.
   const int64_t i0 = base + (int64_t)tid * UN_ITEMS;
+  const int nv = nK - i0 >= UN_ITEMS ? UN_ITEMS : nK - i0 > 0 ? (int)(nK - i0) : 0;
+  uint64_t kv[UN_ITEMS];
+  uint32_t rv[UN_ITEMS];
+  if (nv == UN_ITEMS) {
+    const uint4* kp = reinterpret_cast<const uint4*>(keys + i0);
+    const uint4* rp = reinterpret_cast<const uint4*>(vals + i0);
+#pragma unroll
+    for (int h = 0; h < UN_ITEMS / 2; ++h) {
+      const uint4 w = kp[h];
+      kv[2 * h] = (uint64_t)w.x | ((uint64_t)w.y << 32);
+      kv[2 * h + 1] = (uint64_t)w.z | ((uint64_t)w.w << 32);
+    }
+#pragma unroll
+    for (int h = 0; h < UN_ITEMS / 4; ++h) {
+      const uint4 w = rp[h];
+      rv[4 * h] = w.x;
+      rv[4 * h + 1] = w.y;
+      rv[4 * h + 2] = w.z;
+      rv[4 * h + 3] = w.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < UN_ITEMS; ++j) {
+      const int64_t idx = i0 + j < nK ? i0 + j : nK - 1;
+      kv[j] = keys[idx];
+      rv[j] = vals[idx];
+    }
+  }
+  const bool has = nv > 0;
+  const int64_t iprev = i0 < nK ? i0 - 1 : nK - 1, inext = i0 + nv < nK ? i0 + nv : nK - 1;
+  const uint64_t kprev = keys[iprev > 0 ? iprev : 0];
+  const uint64_t knext = keys[inext];
+  int64_t tev[UN_ITEMS], offv[UN_ITEMS];
+#pragma unroll
+  for (int j = 0; j < UN_ITEMS; ++j) tev[j] = a.te[rv[j]];
+#pragma unroll
+  for (int j = 0; j < UN_ITEMS; ++j) offv[j] = a.off ? a.off[(int32_t)((kv[j] >> a.wb) >> a.sb)] : 0;
   Elem x[UN_ITEMS];
-  int nv = 0;
 #pragma unroll
   for (int j = 0; j < UN_ITEMS; ++j) {
-    if (i0 + j < nK) {
-      x[j] = load_elem(a, keys, vals, i0 + j);
-      nv = j + 1;
+    if (j < nv) {
+      x[j].seg = seg_of_key(a, kv[j]);
+      x[j].s = (int64_t)(kv[j] & ((1ull << a.wb) - 1));
+      const int64_t tec = tev[j] - offv[j];  // corrected end; may lie far beyond W1
+      x[j].e = tec >= a.W1 ? a.W : tec - a.W0;
     } else {
       x[j].seg = -1;
       x[j].s = x[j].e = 0;
     }
   }
-  const bool has = nv > 0;
-  const int32_t prev_seg = (has && i0 > 0) ? seg_of_key(a, keys[i0 - 1]) : -1;
-  const int32_t next_seg = (has && i0 + nv < nK) ? seg_of_key(a, keys[i0 + nv]) : -1;
+  const int32_t prev_seg = (has && i0 > 0) ? seg_of_key(a, kprev) : -1;
+  const int32_t next_seg = (has && i0 + nv < nK) ? seg_of_key(a, knext) : -1;
 
   // Thread aggregate for the segmented max-scan.
   uint64_t agg = 0;
