@@ -151,7 +151,6 @@ struct InitArgs {
   int64_t* class_overlap;
   int64_t* any_busy;
   int P, S;
-  bool names_direct;
   int NN;
   int64_t* name_count;
   int64_t* name_sum;
@@ -187,13 +186,15 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
     for (int64_t i = tid; i < (int64_t)a.P * 9; i += nth) a.class_overlap[i] = 0;
     for (int64_t i = tid; i < a.P; i += nth) a.any_busy[i] = 0;
   }
-  if (a.names_direct)
-    for (int64_t i = tid; i < a.NN; i += nth) {
-      a.name_count[i] = 0;
-      a.name_sum[i] = 0;
-      a.name_min[i] = I64MAX;
-      a.name_max[i] = I64MIN;
-    }
+  // the name outputs start as the identities: the per-block tables (or,
+  // with many names, the kernels themselves) are combined into them with
+  // atomics
+  for (int64_t i = tid; i < a.NN; i += nth) {
+    a.name_count[i] = 0;
+    a.name_sum[i] = 0;
+    a.name_min[i] = I64MAX;
+    a.name_max[i] = I64MIN;
+  }
 }
 
 void launch_init(Ctx& c) {
@@ -212,7 +213,6 @@ void launch_init(Ctx& c) {
   a.any_busy = c.o.any_busy;
   a.P = c.P;
   a.S = c.S;
-  a.names_direct = c.NN > names_lds_limit();
   a.NN = c.NN;
   a.name_count = c.o.name_count;
   a.name_sum = c.o.name_sum;

@@ -12,7 +12,7 @@
 
 namespace hx {
 
-constexpr int NM_THREADS = 256;
+constexpr int NM_THREADS = 512;
 constexpr int NM_LDS_NAMES = 4096;  // 128 KB of LDS
 constexpr int NM_BATCH = 8;
 
@@ -46,18 +46,22 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
   }
   const int64_t n = a.ds->nK;
   const uint32_t* rows = a.rows;
-  // NM_BATCH kernels per thread and round, their loads issued together
+  // NM_BATCH kernels per thread and round, each round of loads issued
+  // together (positions past the end take the last kernel: clamped, not
+  // branched on, and then skipped)
   const int64_t stride = (int64_t)gridDim.x * NM_THREADS;
   for (int64_t i0 = (int64_t)blockIdx.x * NM_THREADS + tid; i0 < n; i0 += NM_BATCH * stride) {
     uint32_t r[NM_BATCH];
 #pragma unroll
-    for (int u = 0; u < NM_BATCH; ++u) r[u] = i0 + u * stride < n ? rows[i0 + u * stride] : ~0u;
+    for (int u = 0; u < NM_BATCH; ++u) r[u] = rows[i0 + u * stride < n ? i0 + u * stride : n - 1];
     int32_t q[NM_BATCH];
     int64_t d[NM_BATCH];
 #pragma unroll
     for (int u = 0; u < NM_BATCH; ++u) {
-      q[u] = r[u] != ~0u ? a.name[r[u]] : -1;
-      d[u] = r[u] != ~0u ? a.te[r[u]] - a.ts[r[u]] : 0;
+      const int32_t nm = a.name[r[u]];
+      const int64_t e = a.te[r[u]], s = a.ts[r[u]];
+      q[u] = i0 + u * stride < n ? nm : -1;
+      d[u] = e - s;
     }
 #pragma unroll
     for (int u = 0; u < NM_BATCH; ++u) {
@@ -81,34 +85,43 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
   for (int i = tid; i < a.NN * 4; i += NM_THREADS) out[i] = tab[i];
 }
 
-// One thread per (name, statistic): the tables are read with independent,
-// coalesced loads (consecutive threads read consecutive words).
+// One thread per (name, statistic) and group of tables: group g folds the
+// tables g, g + NR_GROUPS, ... with independent, coalesced loads
+// (consecutive threads read consecutive words), 16 in flight, and combines
+// its result into the output with one atomic (the outputs start as the
+// identities, set by the init kernel).
+constexpr int NR_GROUPS = 8;
+
 __global__ __launch_bounds__(256) void k_names_reduce(NamesArgs a) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= (int64_t)a.NN * 4) return;
   const int q = (int)(t >> 2), stat = (int)(t & 3);
   const int64_t stride = (int64_t)a.NN * 4;
   uint64_t acc = stat == 2 ? (uint64_t)I64MAX : stat == 3 ? (uint64_t)I64MIN : 0;
-  int b = 0;
-  for (; b + 32 <= a.blocks; b += 32) {
-    uint64_t v[32];
+  for (int b0 = blockIdx.y; b0 < a.blocks; b0 += 16 * NR_GROUPS) {
+    uint64_t v[16];
 #pragma unroll
-    for (int i = 0; i < 32; ++i) v[i] = a.part[(int64_t)(b + i) * stride + t];
+    for (int i = 0; i < 16; ++i) {
+      const int b = b0 + i * NR_GROUPS;
+      v[i] = a.part[(int64_t)(b < a.blocks ? b : blockIdx.y) * stride + t];
+    }
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
+    for (int i = 0; i < 16; ++i) {
+      if (b0 + i * NR_GROUPS >= a.blocks) break;
       if (stat < 2) acc += v[i];
       else if (stat == 2) acc = (int64_t)v[i] < (int64_t)acc ? v[i] : acc;
       else acc = (int64_t)v[i] > (int64_t)acc ? v[i] : acc;
     }
   }
-  for (; b < a.blocks; ++b) {
-    const uint64_t v = a.part[(int64_t)b * stride + t];
-    if (stat < 2) acc += v;
-    else if (stat == 2) acc = (int64_t)v < (int64_t)acc ? v : acc;
-    else acc = (int64_t)v > (int64_t)acc ? v : acc;
+  if (stat == 0) {
+    if (acc) atomicAdd((unsigned long long*)&a.count[q], (unsigned long long)acc);
+  } else if (stat == 1) {
+    if (acc) atomicAdd((unsigned long long*)&a.sum[q], (unsigned long long)acc);
+  } else if (stat == 2) {
+    if ((int64_t)acc != I64MAX) atomicMin((long long*)&a.mn[q], (long long)acc);
+  } else {
+    if ((int64_t)acc != I64MIN) atomicMax((long long*)&a.mx[q], (long long)acc);
   }
-  int64_t* dst = stat == 0 ? a.count : stat == 1 ? a.sum : stat == 2 ? a.mn : a.mx;
-  dst[q] = (int64_t)acc;
 }
 
 static NamesArgs names_args(Ctx& c) {
@@ -130,7 +143,7 @@ static NamesArgs names_args(Ctx& c) {
 
 int names_block_count(int64_t n_max, int NN) {
   if (NN > NM_LDS_NAMES) return (int)std::min<int64_t>(std::max<int64_t>(cdiv(n_max, 4096), 1), 1024);
-  return (int)std::min<int64_t>(std::max<int64_t>(cdiv(n_max, 16384), 1), 128);
+  return (int)std::min<int64_t>(std::max<int64_t>(cdiv(n_max, 8192), 1), 256);
 }
 
 void launch_names(Ctx& c) {
@@ -142,7 +155,9 @@ void launch_names(Ctx& c) {
 void launch_names_reduce(Ctx& c) {
   if (c.NN > NM_LDS_NAMES) return;
   NamesArgs a = names_args(c);
-  hipLaunchKernelGGL(k_names_reduce, dim3((unsigned)cdiv((int64_t)c.NN * 4, 256)), dim3(256), 0, c.st, a);
+  const int groups = std::min(NR_GROUPS, std::max(c.name_blocks, 1));
+  hipLaunchKernelGGL(k_names_reduce, dim3((unsigned)cdiv((int64_t)c.NN * 4, 256), (unsigned)groups), dim3(256), 0, c.st,
+                     a);
 }
 
 int names_lds_limit() { return NM_LDS_NAMES; }

@@ -213,8 +213,11 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
     ds->sort_parity[id] = (uint32_t)(popc(~triv & ((jb.nd >= 32 ? 0u : 1u << jb.nd) - 1u)) & 1);
   if (((triv >> d) & 1) || !has_tile) return;
   const uint32_t gexcl = ds->hist[id][d][dgt];
+  // the tile's digit counts, in the row area until the rows are placed
+  uint32_t* s_cnt = s_val;
   if (tid == 0) s_tile = (int)atomicAdd(&ds->ticket[TK_RADIX + 8 * id + d], 1u);
   for (int i = tid; i < NW * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
+  if (tid < 256) s_cnt[tid] = 0;
   __syncthreads();
   const int parity = popc(~triv & ((1u << d) - 1u)) & 1;
   const uint64_t* kin = jb.k[parity];
@@ -245,6 +248,19 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   auto digit_of = [&](int j) -> int {
     return wbase + j * WAVE < n ? (int)((key[j] >> shift) & 255) : 256;
   };
+
+  // The tile's digit counts come first (LDS atomics) and are published
+  // before the ranking, so that a successor's look-back finds them ready.
+#pragma unroll
+  for (int j = 0; j < RS_ITEMS; ++j) {
+    const int dg = digit_of(j);
+    if (dg < 256) atomicAdd(&s_cnt[dg], 1u);
+  }
+  __syncthreads();
+  const uint32_t cnt = tid < 256 ? s_cnt[tid] : 0u;
+  uint32_t* st = status + (uint32_t)tile * 256u;
+  if (tid < 256) st_agent(&st[tid], (tile == 0 ? RS_FLAG_P : RS_FLAG_A) | cnt);
+
   // Wave-private ranking in input order: items in order, lanes in order.
   const uint64_t lt = lanemask_lt();
 #pragma unroll
@@ -266,25 +282,23 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   }
   __syncthreads();
 
-  // Threads 0..255 own one digit each: tile count, per-wave exclusive offsets.
-  uint32_t cnt = 0;
+  // Threads 0..255 own one digit each: per-wave exclusive offsets.
   if (tid < 256) {
+    uint32_t run = 0;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
       const uint32_t c = s_wh[w][tid];
-      s_wh[w][tid] = cnt;
-      cnt += c;
+      s_wh[w][tid] = run;
+      run += c;
     }
   }
-  uint32_t* st = status + (uint32_t)tile * 256u;
-  if (tid < 256) st_agent(&st[tid], (tile == 0 ? RS_FLAG_P : RS_FLAG_A) | cnt);
   const uint32_t local_excl = block_excl_sum<RS_THREADS>(cnt, s_scan, nullptr);
   if (tid < 256) s_local[tid] = local_excl;
   __syncthreads();
 
   // Tile positions (the per-wave offsets still sit in the key area), then
-  // the tile is reordered in LDS before the look-back, so that no key or row
-  // stays in a register while the predecessors are polled.
+  // the tile is reordered in LDS before the rest of the look-back, so that
+  // no key or row stays in a register while the predecessors are polled.
 #pragma unroll
   for (int j = 0; j < RS_ITEMS; ++j) {
     const int dg = digit_of(j);
