@@ -349,7 +349,7 @@ static inline void stage_end(Ctx& c, int s) {
 struct DeviceStreams {
   hipStream_t s[2] = {nullptr, nullptr};
   hipStream_t cap = nullptr;  // graphs are captured here (the caller's stream may be the null stream)
-  hipEvent_t e[3] = {};  // sorts, timeline chain, join
+  hipEvent_t e[4] = {};  // sorts, timeline chain, join, launches' ops
   bool ok = false;
 };
 static std::mutex g_enqueue_mutex;
@@ -418,26 +418,13 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   if (c.contain) {
     stage_begin(c, HERSCHEL_STAGE_CONTAIN);
     launch_contain(c);
+    (void)hipEventRecord(dsx->e[3], s0);  // each launch's op is known
+    launch_depth(c);
     stage_end(c, HERSCHEL_STAGE_CONTAIN);
   } else {
     const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.n, 256 * 8), 1), 2048);
     hipLaunchKernelGGL(k_nocontain, dim3(grid), dim3(256), 0, c.st, c.sC.k[0], c.sC.v[0], c.ds, c.o.link, c.o.aux);
   }
-
-  // chain 1: timeline and overlap, then the per-name tables
-  c.st = lib0;
-  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
-  stage_begin(c, HERSCHEL_STAGE_TIMELINE);
-  launch_timeline(c);
-  stage_end(c, HERSCHEL_STAGE_TIMELINE);
-  stage_begin(c, HERSCHEL_STAGE_OVERLAP);
-  if (c.overlap) launch_overlap(c);
-  stage_end(c, HERSCHEL_STAGE_OVERLAP);
-  stage_begin(c, HERSCHEL_STAGE_NAMES);
-  launch_names(c);
-  launch_names_reduce(c);
-  stage_end(c, HERSCHEL_STAGE_NAMES);
-  (void)hipEventRecord(dsx->e[1], c.st);
 
   // chain 2: the join (by the correlation table, else by the join sort's
   // remaining digits and the sort-merge join) and the dependency waits
@@ -453,14 +440,31 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_end(c, HERSCHEL_STAGE_EDGES);
   (void)hipEventRecord(dsx->e[2], c.st);
 
+  // chain 1: timeline and overlap, then the per-name tables (enqueued after
+  // the events it waits for have been recorded)
+  c.st = lib0;
+  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
+  stage_begin(c, HERSCHEL_STAGE_TIMELINE);
+  launch_timeline(c);
+  stage_end(c, HERSCHEL_STAGE_TIMELINE);
+  stage_begin(c, HERSCHEL_STAGE_OVERLAP);
+  if (c.overlap) launch_overlap(c);
+  stage_end(c, HERSCHEL_STAGE_OVERLAP);
+  // the name pass also gives each kernel its launch's op: after the join
+  // and after the launches' ops are known
+  if (c.contain) (void)hipStreamWaitEvent(c.st, dsx->e[3], 0);
+  (void)hipStreamWaitEvent(c.st, dsx->e[2], 0);
+  stage_begin(c, HERSCHEL_STAGE_NAMES);
+  launch_names(c);
+  launch_names_reduce(c);
+  stage_end(c, HERSCHEL_STAGE_NAMES);
+  (void)hipEventRecord(dsx->e[1], c.st);
+
   // back on the caller's stream: what needs both containment and the join
   c.st = s0;
   (void)hipStreamWaitEvent(c.st, dsx->e[2], 0);
   stage_begin(c, HERSCHEL_STAGE_OPAGG);
-  if (c.contain) {
-    launch_join_ops(c);
-    launch_opagg(c);
-  }
+  if (c.contain) launch_opagg(c);
   stage_end(c, HERSCHEL_STAGE_OPAGG);
   (void)hipStreamWaitEvent(c.st, dsx->e[1], 0);
   stage_begin(c, HERSCHEL_STAGE_FINAL);

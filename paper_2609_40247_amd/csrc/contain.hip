@@ -587,7 +587,6 @@ __device__ void agg_add_global(const ContainArgs& a, int64_t q, uint32_t nk, int
 // the start, add into HBM with atomics; the others are stored.
 __global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
   __shared__ int32_t s_par[AG_TILE];
-  __shared__ int32_t s_dep[AG_TILE];  // depth of an op; -1 for a launch
   __shared__ uint32_t s_nk[AG_TILE];
   __shared__ int64_t s_first[AG_TILE];
   __shared__ int64_t s_last[AG_TILE];
@@ -597,7 +596,7 @@ __global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
   __shared__ uint32_t c_nk[AG_CHAIN];
   __shared__ int64_t c_first[AG_CHAIN], c_last[AG_CHAIN];
   __shared__ uint64_t c_sum[AG_CHAIN];
-  __shared__ int s_dmin, s_dmax;
+  __shared__ int s_dmin, s_dmax, s_last_op;
   const int tid = threadIdx.x, lane = lane_id();
   const int64_t n = a.ds->nCL;
   const int par = (int)a.ds->sort_parity[2];
@@ -641,7 +640,7 @@ __global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
     if (i < tn) {
       const bool op = key_is_op(key[u]);
       s_par[i] = pr[u];
-      s_dep[i] = op ? av[u] : -1;
+      if (i == tn - 1) s_last_op = op;
       s_nk[i] = 0;
       s_first[i] = I64MAX;
       s_last[i] = I64MIN;
@@ -677,7 +676,7 @@ __global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
   if (tid == 0) {
     // ops of this tile still open at its end receive later contributions
     const int64_t last = tn - 1;
-    int64_t q = s_dep[last] >= 0 ? base + last : s_par[last];
+    int64_t q = s_last_op ? base + last : s_par[last];
     while (q >= base) {
       s_open[q - base] = 1;
       q = s_par[q - base];
@@ -722,8 +721,8 @@ __global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
 #pragma unroll
     for (int u = 0; u < AG_ITEMS; ++u) {
       const int i = tid + u * AG_THREADS;
-      if (i < tn && s_dep[i] == L && s_nk[i] > 0)
-        add(s_par[i], s_nk[i], s_first[i], s_last[i], s_sum[i]);
+      // the item's depth is in registers; only an op of this level reads LDS
+      if (i < tn && key_is_op(key[u]) && av[u] == L && s_nk[i] > 0) add(pr[u], s_nk[i], s_first[i], s_last[i], s_sum[i]);
     }
     __syncthreads();
   }
@@ -831,6 +830,10 @@ void launch_contain(Ctx& c) {
   hipLaunchKernelGGL(k_tiefix_long, dim3(64), dim3(256), 0, c.st, a);
   hipLaunchKernelGGL(k_vbuild, dim3((unsigned)tiles), dim3(VB_THREADS), 0, c.st, a);
   hipLaunchKernelGGL(k_query, dim3((unsigned)tiles), dim3(QY_THREADS), 0, c.st, a);
+}
+
+void launch_depth(Ctx& c) {
+  ContainArgs a = contain_args(c);
   hipLaunchKernelGGL(k_depth, dim3((unsigned)std::max<int64_t>(cdiv(c.sC.n_max, 256 * DP_ITEMS), 1)), dim3(256), 0,
                      c.st, a);
 }

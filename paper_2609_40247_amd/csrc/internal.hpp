@@ -89,11 +89,11 @@ void launch_names(Ctx& c);
 void launch_timeline(Ctx& c);
 void launch_overlap(Ctx& c);
 void launch_contain(Ctx& c);
+void launch_depth(Ctx& c);
 void launch_opagg(Ctx& c);
 void launch_names_reduce(Ctx& c);
 void launch_join(Ctx& c);
 void launch_join_plan(Ctx& c);
-void launch_join_ops(Ctx& c);
 void launch_join_table(Ctx& c);
 void launch_edges(Ctx& c);
 void launch_finalize(Ctx& c);

@@ -174,7 +174,7 @@ __global__ __launch_bounds__(256) void k_join(JoinArgs a) {
         if (x < 0) ++c[JC_NEG];
         const int bin = x <= 0 ? 0 : bits_of((uint64_t)x);
         atomicAdd(&s_h[bin], 1ull);
-        a.aux[row] = -1;  // the kernel's op comes later (k_join_ops)
+        a.aux[row] = -1;  // the kernel's op comes later (the name pass)
       } else {
         a.link[row] = -1;
         a.aux[row] = -1;
@@ -433,7 +433,7 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
       const int64_t x = ts[u] - lts[u];  // same process: the offset cancels
       if (x < 0) ++c[JC_NEG];
       atomicAdd(&s_h[x <= 0 ? 0 : bits_of((uint64_t)x)], 1ull);
-      a.aux[row[u]] = -1;  // the kernel's op comes later (k_join_ops)
+      a.aux[row[u]] = -1;  // the kernel's op comes later (the name pass)
       if (single[u]) {
         a.aux[l[u]] = 1;
         ++c[JC_MLAUNCH];
@@ -457,41 +457,6 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
     }
   }
   jt_flush(a, c, s_c, s_h);
-}
-
-// Kernel -> op: the op of the kernel's launch (containment and the join run
-// concurrently; this pass follows both).  Walks prep's list of the admitted
-// kernels' rows; counts matched kernels whose launch has no op.  Each round
-// of gathers is issued for all of a thread's kernels together.
-__global__ __launch_bounds__(256) void k_join_ops(JoinArgs a) {
-  __shared__ unsigned long long s_c[JC_N];
-  const int tid = threadIdx.x;
-  if (tid < JC_N) s_c[tid] = 0;
-  __syncthreads();
-  const int64_t n = a.ds->nK;
-  // Positions past the end take the last kernel's row (clamped loads); with
-  // no admitted kernel there is no row to take, and nothing to do.
-  if (n == 0) return;
-  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + tid;
-  uint32_t c[JC_N] = {};
-  uint32_t row[JT_ITEMS];
-  int32_t l[JT_ITEMS], op[JT_ITEMS];
-#pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
-    const int64_t i = i0 + u * 256;
-    row[u] = a.k_rows[i < n ? i : n - 1];
-  }
-#pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) l[u] = a.link[row[u]];
-#pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) op[u] = a.link[l[u] >= 0 ? l[u] : 0];
-#pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
-    if (i0 + u * 256 >= n || l[u] < 0) continue;
-    a.aux[row[u]] = op[u];
-    if (op[u] < 0) ++c[JC_UNATTR];
-  }
-  jt_flush(a, c, s_c, nullptr);
 }
 
 __global__ __launch_bounds__(256) void k_edges(JoinArgs a) {
@@ -622,11 +587,6 @@ void launch_join(Ctx& c) {
   hipLaunchKernelGGL(k_join, dim3((unsigned)grid), dim3(256), 0, c.st, a);
 }
 
-void launch_join_ops(Ctx& c) {
-  JoinArgs a = join_args(c);
-  const int64_t grid = std::max<int64_t>(cdiv(c.sJ.n_max, JT_TILE), 1);
-  hipLaunchKernelGGL(k_join_ops, dim3((unsigned)grid), dim3(256), 0, c.st, a);
-}
 
 void launch_edges(Ctx& c) {
   if (c.p.n_edges <= 0) return;

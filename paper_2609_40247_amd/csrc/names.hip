@@ -1,7 +1,9 @@
 // Per kernel-name aggregates: count, sum, min and max of the unclipped
 // kernel duration over all admitted kernels (Section 6.1 measures kernel
 // durations; grouping by kernel name is the per-name view of the same
-// records).
+// records).  With containment the same pass over the kernels also gives each
+// matched kernel the op of its launch (kernel composition, Section 6.1) and
+// counts the matched kernels whose launch has no op.
 //
 // Each workgroup keeps a private table of all names in LDS (32 bytes per
 // name) while it streams a slice of the admitted kernels, then writes the
@@ -29,6 +31,10 @@ struct NamesArgs {
   int64_t* sum;
   int64_t* mn;
   int64_t* mx;
+  // kernel -> op (with containment): the op of the kernel's launch
+  bool kernel_ops;
+  const int32_t* link;
+  int32_t* aux;
 };
 
 __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
@@ -46,6 +52,7 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
   }
   const int64_t n = a.ds->nK;
   const uint32_t* rows = a.rows;
+  uint32_t unattr = 0;  // matched kernels whose launch has no op
   // NM_BATCH kernels per thread and round, each round of loads issued
   // together (positions past the end take the last kernel: clamped, not
   // branched on, and then skipped)
@@ -54,14 +61,27 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
     uint32_t r[NM_BATCH];
 #pragma unroll
     for (int u = 0; u < NM_BATCH; ++u) r[u] = rows[i0 + u * stride < n ? i0 + u * stride : n - 1];
-    int32_t q[NM_BATCH];
+    int32_t q[NM_BATCH], l[NM_BATCH];
     int64_t d[NM_BATCH];
 #pragma unroll
     for (int u = 0; u < NM_BATCH; ++u) {
       const int32_t nm = a.name[r[u]];
       const int64_t e = a.te[r[u]], s = a.ts[r[u]];
+      l[u] = a.kernel_ops ? a.link[r[u]] : -1;
       q[u] = i0 + u * stride < n ? nm : -1;
       d[u] = e - s;
+    }
+    if (a.kernel_ops) {
+      // the op of each matched kernel's launch (one more round of gathers)
+      int32_t op[NM_BATCH];
+#pragma unroll
+      for (int u = 0; u < NM_BATCH; ++u) op[u] = a.link[l[u] >= 0 ? l[u] : 0];
+#pragma unroll
+      for (int u = 0; u < NM_BATCH; ++u) {
+        if (q[u] < 0 || l[u] < 0) continue;
+        a.aux[r[u]] = op[u];
+        if (op[u] < 0) ++unattr;
+      }
     }
 #pragma unroll
     for (int u = 0; u < NM_BATCH; ++u) {
@@ -78,6 +98,10 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
         atomicMax((long long*)&a.mx[q[u]], (long long)d[u]);
       }
     }
+  }
+  if (a.kernel_ops) {
+    const uint64_t w = wave_sum_u64(unattr);
+    if (lane_id() == 0 && w) atomicAdd(&a.ds->join_acc[blockIdx.x % JOIN_COPIES][JC_UNATTR], (unsigned long long)w);
   }
   if (!lds) return;
   __syncthreads();
@@ -138,6 +162,9 @@ static NamesArgs names_args(Ctx& c) {
   a.sum = c.o.name_sum;
   a.mn = c.o.name_min;
   a.mx = c.o.name_max;
+  a.kernel_ops = c.contain;
+  a.link = c.o.link;
+  a.aux = c.o.aux;
   return a;
 }
 
