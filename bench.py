@@ -43,16 +43,20 @@ def source_hash(stage: str) -> str:
 
 
 def sort_units(stats):
-    """Key-passes the radix passes of the sort stage must make: the timeline
-    and containment sorts (the join's own sort runs on the join stream, when
-    the correlation table cannot be used) each move their keys once per digit
-    on which they differ.  Also the number of pass launches of the stage (the
-    two sorts share launches; one per digit of the wider key)."""
+    """Key-passes the radix launches of the sort stage must make: the
+    timeline and containment sorts, and the join sort (which moves data only
+    when the correlation table cannot be used) for its digits in the same
+    range, each move their keys once per digit on which they differ.  Also
+    the number of pass launches of the stage: one per digit of the wider of
+    the timeline and containment keys, except a lowest digit that both leave
+    to the refine pass (bit 31 of the mask)."""
     stage = [stats[0], stats[2]]
+    first = 1 if all((skipped >> 31) & 1 for _, skipped, _ in stage) else 0
+    last = max(nd for _, _, nd in stage)
     units = 0
-    for nkeys, skipped, nd in stage:
-        units += nkeys * sum(1 for d in range(nd) if not (skipped >> d) & 1)
-    return units, max(nd for _, _, nd in stage)
+    for nkeys, skipped, nd in stats:  # the join sort's digits in the stage's range run in its launches
+        units += nkeys * sum(1 for d in range(first, min(nd, last)) if not (skipped >> d) & 1)
+    return units, last - first
 
 
 def profiled_traffic(stage: str, workload: str):

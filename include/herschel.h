@@ -190,16 +190,16 @@ int herschel_trace_analyze_batch(const herschel_events *ev, const int64_t *trace
 const char *herschel_strerror(int code);
 
 /* Diagnostics for benchmarks.  Stages of one analysis call.  INIT, PREP,
- * HIST and SORT run in this order on params->hip_stream; after PREP the
- * JOIN and NAMES stages run on a library stream, after SORT the TIMELINE and
- * OVERLAP stages on another, while CONTAIN and OPAGG follow SORT on
- * params->hip_stream; FINAL waits for all of them. */
+ * HIST and SORT (with the refine pass after it) run in this order on
+ * params->hip_stream; after SORT the JOIN and EDGES stages run on a library
+ * stream, the TIMELINE, OVERLAP and NAMES stages on another, while CONTAIN
+ * and OPAGG follow on params->hip_stream; FINAL waits for all of them. */
 enum {
   HERSCHEL_STAGE_INIT = 0,     /* clear the workspace state and accumulating outputs */
   HERSCHEL_STAGE_PREP = 1,     /* validate, correct, admit, compact (one kernel) */
-  HERSCHEL_STAGE_HIST = 2,     /* digit histograms and pass plans of the sorts */
+  HERSCHEL_STAGE_HIST = 2,     /* digit histograms and pass plans of the timeline and containment sorts */
   HERSCHEL_STAGE_NAMES = 3,    /* per-name partial tables */
-  HERSCHEL_STAGE_SORT = 4,     /* radix passes of the timeline, join and containment sorts */
+  HERSCHEL_STAGE_SORT = 4,     /* radix passes shared by the sorts (the timeline and containment digits) */
   HERSCHEL_STAGE_TIMELINE = 5, /* busy/idle, gaps, coverage runs (one kernel) */
   HERSCHEL_STAGE_OVERLAP = 6,  /* co-ranks of the coverage runs and the sweep */
   HERSCHEL_STAGE_CONTAIN = 7,  /* op nesting and launch -> op */
@@ -223,10 +223,12 @@ int herschel_time_stage(int stage, void *start_event, void *stop_event);
  * these params, for computing the bytes the radix passes must move: waits
  * for params->hip_stream, then writes, for s = 0 timeline, 1 join,
  * 2 containment sort: out[3 * s + 0] = its keys, out[3 * s + 1] = bit mask
- * of the 8-bit digits it skipped (every key agreed on them), out[3 * s + 2]
- * = its digits.  out must hold 9 entries (host memory).  Returns
- * HERSCHEL_EINVAL for NULL arguments, no workspace or an invalid window or
- * size, HERSCHEL_EDEVICE when the copy fails. */
+ * of the 8-bit digits that no pass moved (bit d: every key agreed on digit
+ * d, or digit d was left to the refine pass that orders keys equal above
+ * it; bit 31 is set in the second case), out[3 * s + 2] = its digits.  out
+ * must hold 9 entries (host memory).  Returns HERSCHEL_EINVAL for NULL
+ * arguments, no workspace or an invalid window or size, HERSCHEL_EDEVICE
+ * when the copy fails. */
 int herschel_sort_stats(const herschel_params *p, int32_t *out);
 
 #ifdef __cplusplus

@@ -37,12 +37,15 @@ struct Bump {
   }
 };
 
-static void sort_plan(SortBufs& s, int id, int64_t n_max, int key_bits, bool vals) {
+// refine: whether the lowest digit is left to the refine pass (keys wider
+// than 32 bits, whose low byte is nanoseconds: runs of keys equal above it
+// are short)
+static void sort_plan(SortBufs& s, int id, int64_t n_max, int key_bits, bool refine) {
   s.id = id;
   s.n_max = n_max;
   s.tiles_max = cdiv(std::max<int64_t>(n_max, 1), RS_TILE);
   s.nd = (key_bits + 7) / 8;
-  (void)vals;
+  s.first = refine && key_bits > 32 ? 1 : 0;
 }
 
 size_t layout_workspace(Ctx& c, char* base) {
@@ -58,7 +61,7 @@ size_t layout_workspace(Ctx& c, char* base) {
   c.union_status = b.take<uint64_t>(3 * c.union_tiles);
   // key widths (also reported by herschel_sort_stats)
   sort_plan(c.sK, 0, n, c.pb + c.sb + c.wb, true);
-  sort_plan(c.sJ, 1, n, 49 + c.pb, true);
+  sort_plan(c.sJ, 1, n, 49 + c.pb, false);  // low bits of dense ids: long runs
   sort_plan(c.sC, 2, n, c.pb + c.tb + c.wb + 1, true);
   // digit 0's look-back words are cleared here; each later digit's are
   // cleared by the pass before it
@@ -79,6 +82,9 @@ size_t layout_workspace(Ctx& c, char* base) {
   c.zero_bytes = align_up(b.off - z0);
   for (SortBufs* s : {&c.sK, &c.sJ, &c.sC})
     if (s != &c.sC || c.contain) s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * 256);
+  // long runs of the refine pass (each has more than RF_SHORT keys)
+  c.rf_cap = cdiv(n, RF_SHORT + 1) + 1;
+  c.rf_list = b.take<int32_t>(2 * c.rf_cap);
   c.hist_part = b.take<uint32_t>((int64_t)N_SORTS * HIST_MAX_BLOCKS * 8 * 256);
   c.k_rows = b.take<uint32_t>(n);
   if (c.P <= JT_PROCS) {
@@ -121,9 +127,6 @@ size_t layout_workspace(Ctx& c, char* base) {
     }
     c.pmt = b.take<uint64_t>(c.vb_tiles);
     c.par = b.take<int32_t>(n);
-    c.tie_cap = cdiv(n, 33) + 1;
-    c.tie_list = b.take<int32_t>(c.tie_cap);
-    c.tie_scratch = b.take<uint64_t>(4 * n);
     c.lk_first = b.take<int64_t>(n);
     c.lk_last = b.take<int64_t>(n);
     c.lk_sum = b.take<int64_t>(n);
@@ -393,22 +396,26 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
 
   // The three sorts share their digit passes (blockIdx.y picks the sort; a
   // sort whose digit is skipped leaves at once, as the join sort's do when
-  // the correlation table was used).  The join keys are wider than the
-  // others: the join sort's remaining digits run on the join stream.  Nothing
-  // else runs beside the sorts: a large grid on another stream would take
-  // the CUs first and hold up the passes, which every later stage waits for.
-  const int ks = c.contain ? 2 : 1;
+  // the correlation table is used).  The timeline and containment sorts leave
+  // their lowest digit to the refine pass; the join sort's digits beyond
+  // theirs run on the join stream.  Nothing else runs beside the sorts: a
+  // large grid on another stream would take the CUs first and hold up the
+  // passes, which every later stage waits for.
+  const int ks = c.contain ? 3 : 2;
   SortBufs* ss[3] = {&c.sK, &c.sC, &c.sJ};
   const int32_t* cc[3] = {&c.ds->nK, &c.ds->nCL, &c.ds->nJ};
-  ss[ks] = &c.sJ;
-  cc[ks] = &c.ds->nJ;
+  ss[ks - 1] = &c.sJ;
+  cc[ks - 1] = &c.ds->nJ;
   const int d_shared = c.contain ? std::max(c.sK.nd, c.sC.nd) : c.sK.nd;
+  const int d_first = c.contain ? std::min(c.sK.first, c.sC.first) : c.sK.first;
   stage_begin(c, HERSCHEL_STAGE_HIST);
-  launch_hist_multi(c, ss, cc, ks + 1);
+  launch_hist_multi(c, ss, cc, ks);
   stage_end(c, HERSCHEL_STAGE_HIST);
+  launch_sort_multi(c, ss, cc, ks, 0, d_first);  // the join sort's lowest digit alone
   stage_begin(c, HERSCHEL_STAGE_SORT);
-  launch_sort_multi(c, ss, cc, ks + 1, 0, d_shared);
+  launch_sort_multi(c, ss, cc, ks, d_first, d_shared);
   stage_end(c, HERSCHEL_STAGE_SORT);
+  launch_refine(c);
   (void)hipEventRecord(dsx->e[0], s0);
 
   // chain 3 on the caller's stream, enqueued first: containment is the
@@ -426,13 +433,13 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     hipLaunchKernelGGL(k_nocontain, dim3(grid), dim3(256), 0, c.st, c.sC.k[0], c.sC.v[0], c.ds, c.o.link, c.o.aux);
   }
 
-  // chain 2: the join (by the correlation table, else by the join sort's
-  // remaining digits and the sort-merge join) and the dependency waits
+  // chain 2: the join by the correlation table, or else by the rest of the
+  // join sort and the sort-merge join; then the dependency waits
   c.st = lib1;
   (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
   stage_begin(c, HERSCHEL_STAGE_JOIN);
   launch_join_table(c);
-  launch_sort_multi(c, &ss[ks], &cc[ks], 1, d_shared, c.sJ.nd);
+  launch_sort_multi(c, &ss[ks - 1], &cc[ks - 1], 1, d_shared, c.sJ.nd);
   launch_join(c);
   stage_end(c, HERSCHEL_STAGE_JOIN);
   stage_begin(c, HERSCHEL_STAGE_EDGES);
@@ -633,7 +640,7 @@ int herschel_sort_stats(const herschel_params* p, int32_t* out) {
   const int pb = bits_host((uint64_t)(p->n_procs - 1)), sb = bits_host((uint64_t)(p->n_streams - 1));
   const int tb = bits_host((uint64_t)(p->n_threads - 1));
   const int wb = bits_host((uint64_t)(p->window_end - p->window_begin - 1));
-  const int key_bits[N_SORTS] = {pb + sb + wb, 49 + pb, pb + tb + wb + 1};
+  const int key_bits[N_SORTS] = {pb + sb + wb, 49 + pb, pb + tb + wb + 1};  // as layout_workspace plans them
   const int32_t counts[N_SORTS] = {ds.nK, ds.nJ, ds.nCL};
   for (int i = 0; i < N_SORTS; ++i) {
     out[3 * i + 0] = counts[i];

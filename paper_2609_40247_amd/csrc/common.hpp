@@ -25,7 +25,7 @@ enum : uint32_t {
   DS_SPIN = 1u,      // a look-back wait exceeded its bound
   DS_OOB = 2u,       // checked build: an index left its buffer
   DS_PARAM = 4u,     // clock_offset or stream_class out of range
-  DS_TIES = 8u,      // more long runs of equal op starts than the list holds
+  DS_TIES = 8u,      // more long runs of equal keys than the refine list holds
   DS_CAPACITY = 16u, // an internal list overflowed its bound
   DS_LOGIC = 32u     // an internal consistency check failed
 };
@@ -57,11 +57,11 @@ struct DevState {
   int32_t nCL;  // admitted ops + launches (containment list)
   int32_t nJ;   // admitted launches + kernels (join list)
   int32_t nEv;  // overlap events (2 per coverage run)
-  int32_t n_long_ties;
-  int32_t pad0;
+  int32_t n_long[2];  // long runs listed by the refine pass (timeline, containment)
   int64_t first_invalid;  // smallest bad row (INT64_MAX = none)
   int64_t n_gaps;
-  uint32_t sort_trivial[N_SORTS];  // bit d: every key has the same digit d (pass skipped)
+  uint32_t sort_trivial[N_SORTS];  // bit d: digit d moves no data (every key agrees on it, or it is
+                                   // left to the refine pass: then bit 31 is set too)
   uint32_t join_direct;            // 1: the correlation table replaces the join sort
   uint32_t pad1;
   int64_t jt_slots;                // table slots in use

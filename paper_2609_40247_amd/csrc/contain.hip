@@ -23,7 +23,6 @@ namespace hx {
 constexpr int CT_THREADS = 256;
 constexpr int CT_ITEMS = 16;
 constexpr int CT_TILE = CT_THREADS * CT_ITEMS;  // 4096 positions = one M2 entry
-constexpr int TIE_SHORT = 32;
 
 struct ContainArgs {
   uint64_t* k[2];
@@ -48,9 +47,6 @@ struct ContainArgs {
   uint64_t* pmt;
   uint64_t* vb_status;
   int32_t* par;
-  int32_t* tie_list;
-  int64_t tie_cap;
-  uint64_t* tie_scratch;
   // per-launch kernel aggregates (by row), written by the join
   const int64_t* lk_first;
   const int64_t* lk_last;
@@ -69,108 +65,6 @@ __device__ __forceinline__ int64_t key_rel(const ContainArgs& a, uint64_t key) {
   return (int64_t)((key >> 1) & ((1ull << a.wb) - 1));
 }
 __device__ __forceinline__ bool key_is_op(uint64_t key) { return (key & 1) == 0; }
-
-// ----------------------------------------------------------------- ties
-// Ops of one thread starting at the same ns must be ordered by (te' down,
-// row up); the stable sort left them in row order.  Runs up to TIE_SHORT are
-// fixed in place by their first thread; longer runs are listed.
-__device__ __forceinline__ bool tie_before(int64_t te_a, uint32_t ra, int64_t te_b, uint32_t rb) {
-  return te_a > te_b || (te_a == te_b && ra < rb);
-}
-
-__global__ __launch_bounds__(256) void k_tiefix(ContainArgs a) {
-  const int64_t n = a.ds->nCL;
-  const int par = (int)a.ds->sort_parity[2];
-  const uint64_t* keys = a.k[par];
-  uint32_t* vals = a.v[par];
-  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < n; p += (int64_t)gridDim.x * 256) {
-    const uint64_t key = keys[p];
-    if (!key_is_op(key)) continue;
-    if (p + 1 >= n || keys[p + 1] != key) continue;
-    if (p > 0 && keys[p - 1] == key) continue;
-    int64_t e = p + 1;
-    while (e < n && keys[e] == key && e - p <= TIE_SHORT) ++e;
-    const int64_t len = e - p;
-    if (len > TIE_SHORT) {
-      const int slot = atomicAdd(&a.ds->n_long_ties, 1);
-      if (slot < a.tie_cap) a.tie_list[slot] = (int32_t)p;
-      else set_status(a.ds, DS_TIES);
-      continue;
-    }
-    // insertion sort of the run by (te down, row up); one process, so the
-    // raw end times order like the corrected ones
-    for (int64_t i = p + 1; i < e; ++i) {
-      const uint32_t r = vals[i];
-      const int64_t t = a.te[r];
-      int64_t j = i - 1;
-      while (j >= p) {
-        const uint32_t rj = vals[j];
-        if (!tie_before(t, r, a.te[rj], rj)) break;
-        vals[j + 1] = rj;
-        --j;
-      }
-      vals[j + 1] = r;
-    }
-  }
-}
-
-// Long runs: one workgroup per run, bitonic sort in a scratch region that
-// belongs to the run alone ([2p, 2p + m) with m <= 2 * len).
-__global__ __launch_bounds__(256) void k_tiefix_long(ContainArgs a) {
-  const int64_t n = a.ds->nCL;
-  const int64_t nl = min((int64_t)a.ds->n_long_ties, a.tie_cap);
-  const int par = (int)a.ds->sort_parity[2];
-  const uint64_t* keys = a.k[par];
-  uint32_t* vals = a.v[par];
-  __shared__ int64_t s_len;
-  for (int64_t r = blockIdx.x; r < nl; r += gridDim.x) {
-    const int64_t p = a.tie_list[r];
-    if (threadIdx.x == 0) {
-      int64_t e = p + 1;
-      while (e < n && keys[e] == keys[p]) ++e;
-      s_len = e - p;
-    }
-    __syncthreads();
-    const int64_t len = s_len;
-    int64_t m = 1;
-    while (m < len) m <<= 1;
-    int64_t* ste = (int64_t*)a.tie_scratch + 2 * p;
-    uint64_t* srow = a.tie_scratch + 2 * n + 2 * p;
-    for (int64_t i = threadIdx.x; i < m; i += 256) {
-      if (i < len) {
-        const uint32_t rr = vals[p + i];
-        ste[i] = a.te[rr];
-        srow[i] = rr;
-      } else {
-        ste[i] = I64MIN;
-        srow[i] = 0xffffffffull;
-      }
-    }
-    __syncthreads();
-    for (int64_t k = 2; k <= m; k <<= 1) {
-      for (int64_t j = k >> 1; j > 0; j >>= 1) {
-        for (int64_t i = threadIdx.x; i < m; i += 256) {
-          const int64_t l = i ^ j;
-          if (l > i) {
-            const bool up = (i & k) == 0;
-            const bool lb = tie_before(ste[l], (uint32_t)srow[l], ste[i], (uint32_t)srow[i]);
-            if (up ? lb : !lb) {
-              const int64_t t0 = ste[i];
-              ste[i] = ste[l];
-              ste[l] = t0;
-              const uint64_t r0 = srow[i];
-              srow[i] = srow[l];
-              srow[l] = r0;
-            }
-          }
-        }
-        __syncthreads();
-      }
-    }
-    for (int64_t i = threadIdx.x; i < len; i += 256) vals[p + i] = (uint32_t)srow[i];
-    __syncthreads();
-  }
-}
 
 // ------------------------------------------------------- encoding, pyramid
 // V and the first pyramid levels of one 4096-position tile: 16 waves, each
@@ -809,9 +703,6 @@ static ContainArgs contain_args(Ctx& c) {
   a.pmt = c.pmt;
   a.vb_status = c.vb_status;
   a.par = c.par;
-  a.tie_list = c.tie_list;
-  a.tie_cap = c.tie_cap;
-  a.tie_scratch = c.tie_scratch;
   a.lk_first = c.lk_first;
   a.lk_last = c.lk_last;
   a.lk_sum = c.lk_sum;
@@ -824,10 +715,6 @@ static ContainArgs contain_args(Ctx& c) {
 void launch_contain(Ctx& c) {
   ContainArgs a = contain_args(c);
   const int64_t tiles = std::max<int64_t>(cdiv(c.sC.n_max, CT_TILE), 1);
-  // one position per thread: these kernels are chains of dependent loads
-  const int grid_stride = (int)std::max<int64_t>(cdiv(c.sC.n_max, 256), 1);
-  hipLaunchKernelGGL(k_tiefix, dim3(grid_stride), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_tiefix_long, dim3(64), dim3(256), 0, c.st, a);
   hipLaunchKernelGGL(k_vbuild, dim3((unsigned)tiles), dim3(VB_THREADS), 0, c.st, a);
   hipLaunchKernelGGL(k_query, dim3((unsigned)tiles), dim3(QY_THREADS), 0, c.st, a);
 }

@@ -17,8 +17,9 @@ struct SortBufs {
   uint32_t* status1 = nullptr;          // [nd - 1][tiles_max * 256] digits 1..nd-1
   int64_t n_max = 0;                    // capacity (host upper bound of the count)
   int64_t tiles_max = 0;
-  int nd = 0;                           // digit passes to launch (8-bit digits)
+  int nd = 0;                           // 8-bit digits of the key
   int id = 0;                           // sort index: histogram, parity, tickets
+  int first = 0;                        // first digit sorted by passes (1: digit 0 left to the refine pass)
 };
 
 struct Ctx {
@@ -62,9 +63,8 @@ struct Ctx {
   int nlev = 0;
   uint64_t* pmt = nullptr;           // [vb_tiles] exclusive prefix max before each tile
   int32_t* par = nullptr;            // [n] answer position per sorted position
-  int32_t* tie_list = nullptr;       // [tie_cap * 2] long runs of equal op starts
-  int64_t tie_cap = 0;
-  uint64_t* tie_scratch = nullptr;   // [4n] end times and rows of long tie runs
+  int32_t* rf_list = nullptr;        // [2][rf_cap] long runs found by the refine pass
+  int64_t rf_cap = 0;
   int64_t* lk_first = nullptr;       // [n] per launch row: first start of its kernels
   int64_t* lk_last = nullptr;        // [n] last end of its kernels
   int64_t* lk_sum = nullptr;         // [n] sum of its kernels' durations
@@ -85,6 +85,7 @@ void launch_init(Ctx& c);
 void launch_prep(Ctx& c);
 void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k);
 void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k, int d0, int d1);
+void launch_refine(Ctx& c);
 void launch_names(Ctx& c);
 void launch_timeline(Ctx& c);
 void launch_overlap(Ctx& c);
@@ -114,6 +115,10 @@ constexpr int RS_THREADS = 512;
 constexpr int RS_ITEMS = 8;
 constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 4096 keys per tile
 constexpr int RS_WAVES_PER_EU = 6;              // three workgroups of 8 waves per CU
+// Keys wider than 32 bits leave their lowest digit to the refine pass, which
+// orders the runs of keys equal above it; runs up to RF_SHORT are fixed in
+// place, longer ones listed.
+constexpr int RF_SHORT = 32;
 
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

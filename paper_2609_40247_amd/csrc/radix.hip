@@ -22,6 +22,7 @@ struct HistJob {
   const int32_t* count;
   int nd;
   int id;
+  int first;  // 1: digit 0 is left to the refine pass
 };
 struct HistJobs {
   HistJob j[N_SORTS];
@@ -148,6 +149,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void k_hist_plan(HistJobs jobs, DevSt
   // every thread joins the barriers below; only the first 256 carry a bin
   const bool full = threadIdx.x < 256 && c == (uint32_t)n;
   if (__syncthreads_or(full) && threadIdx.x == 0) atomicOr(&ds->sort_trivial[jb.id], 1u << d);
+  if (d < jb.first && threadIdx.x == 0) atomicOr(&ds->sort_trivial[jb.id], (1u << d) | (1u << 31));
   const uint32_t ex = block_excl_sum<PLAN_THREADS>(threadIdx.x < 256 ? c : 0u, s_scan, nullptr);
   if (threadIdx.x < 256) ds->hist[jb.id][d][bin] = ex;
 }
@@ -156,10 +158,10 @@ struct SortJob {
   uint64_t* k[2];
   uint32_t* v[2];
   const int32_t* count;
-  uint32_t* status0;  // [tiles_max * 256] look-back words of digit 0 (cleared by the init kernel)
-  uint32_t* status1;  // [nd - 1][tiles_max * 256] digits 1.. (each cleared by the previous pass)
+  uint32_t* status0;  // [tiles_max * 256] look-back words of the first digit (cleared by the init kernel)
+  uint32_t* status1;  // [nd - 1][tiles_max * 256] later digits (each cleared by the previous pass)
   int64_t tiles_max;
-  int nd, id;
+  int nd, id, first;
 };
 struct SortJobs {
   SortJob j[N_SORTS];
@@ -191,7 +193,7 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   uint32_t* s_glob = &s_lb_sum[0][0];
 
   const SortJob& jb = jobs.j[blockIdx.y];
-  if (d >= jb.nd) return;
+  if (d >= jb.nd || d < jb.first) return;
   const int id = jb.id;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int dgt = tid & 255, slice = tid >> 8;
@@ -200,7 +202,7 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   // The next digit's look-back words of this workgroup's tile index are
   // cleared here: the next pass starts only after this one has ended.
   if (has_tile && d + 1 < jb.nd && tid < 256)
-    jb.status1[((int64_t)d * jb.tiles_max + blockIdx.x) * 256 + tid] = 0u;
+    jb.status1[((int64_t)(d - jb.first) * jb.tiles_max + blockIdx.x) * 256 + tid] = 0u;
   // The plan (trivial digits, offsets) was made by the histogram kernel.  A
   // digit is trivial iff one bin holds every key; the input buffer's parity
   // is the number of non-trivial digits below this one.  Workgroups with no
@@ -209,7 +211,7 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   // workgroups stay, so they draw exactly the tickets of the real tiles.
   const uint32_t triv = ds->sort_trivial[id];
   // which buffer holds the result: parity of the digits that move data
-  if (d == 0 && blockIdx.x == 0 && tid == 0)
+  if (d == jb.first && blockIdx.x == 0 && tid == 0)
     ds->sort_parity[id] = (uint32_t)(popc(~triv & ((jb.nd >= 32 ? 0u : 1u << jb.nd) - 1u)) & 1);
   if (((triv >> d) & 1) || !has_tile) return;
   const uint32_t gexcl = ds->hist[id][d][dgt];
@@ -224,7 +226,7 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   uint64_t* kout = jb.k[parity ^ 1];
   const uint32_t* vin = jb.v[parity];
   uint32_t* vout = jb.v[parity ^ 1];
-  uint32_t* status = d == 0 ? jb.status0 : jb.status1 + (int64_t)(d - 1) * jb.tiles_max * 256;
+  uint32_t* status = d == jb.first ? jb.status0 : jb.status1 + (int64_t)(d - jb.first - 1) * jb.tiles_max * 256;
   const int tile = s_tile;
   const int64_t base = (int64_t)tile * RS_TILE;
 
@@ -406,7 +408,7 @@ void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
   int64_t n_max = 1;
   for (int i = 0; i < k; ++i) {
     if (s[i]->nd == 0) continue;
-    jobs.j[m++] = HistJob{s[i]->k[0], count[i], s[i]->nd, s[i]->id};
+    jobs.j[m++] = HistJob{s[i]->k[0], count[i], s[i]->nd, s[i]->id, s[i]->first};
     n_max = std::max<int64_t>(n_max, s[i]->n_max);
     nd = std::max(nd, s[i]->nd);
   }
@@ -416,21 +418,256 @@ void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
   hipLaunchKernelGGL(k_hist_plan, dim3((unsigned)nd, (unsigned)m), dim3(PLAN_THREADS), 0, c.st, jobs, c.ds);
 }
 
-// Digit passes d0 .. d1-1 of up to N_SORTS sorts, one launch per digit.
+// Digit passes d0 .. d1-1 of up to N_SORTS sorts, one launch per digit
+// (none for a digit that every sort leaves to the refine pass).
 void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k, int d0, int d1) {
   for (int d = d0; d < d1; ++d) {
     SortJobs jobs{};
     int64_t grid = 1;
     int m = 0;
     for (int i = 0; i < k; ++i) {
-      if (d >= s[i]->nd) continue;
+      if (d >= s[i]->nd || d < s[i]->first) continue;
       jobs.j[m++] = SortJob{{s[i]->k[0], s[i]->k[1]}, {s[i]->v[0], s[i]->v[1]}, count[i], s[i]->status0,
-                            s[i]->status1, s[i]->tiles_max, s[i]->nd, s[i]->id};
+                            s[i]->status1, s[i]->tiles_max, s[i]->nd, s[i]->id, s[i]->first};
       grid = std::max<int64_t>(grid, s[i]->tiles_max);
     }
     if (m == 0) continue;
     hipLaunchKernelGGL(k_radix_pass, dim3((unsigned)grid, (unsigned)m), dim3(RS_THREADS), 0, c.st, jobs, c.ds, d);
   }
+}
+
+// ------------------------------------------------------------------ refine
+// After passes over digits 1.. only, a sort is ordered by key >> 8; keys
+// equal above bit 8 still sit in row order (the passes are stable).  The
+// refine pass orders each such run by the full key, and keys that are
+// equal by the sort's own tie rule: the row (stable) for the timeline; for
+// the containment list, ops of equal key by end time down, then row (the
+// rule that nests an op that starts with its parent inside it).  The
+// containment list is refined even when every digit was sorted (runs of
+// equal keys, shift 0), for that tie rule.  Runs up to RF_SHORT are ordered
+// in place by their first thread (insertion sort); longer runs are listed
+// and each is sorted by one workgroup.
+struct RefineJob {
+  uint64_t* k[2];
+  uint32_t* v[2];
+  const int32_t* count;
+  int id;        // sort index (parity)
+  int contain;   // 1: containment tie rule
+  int slot;      // list index (0 timeline, 1 containment)
+  int shift;     // runs are keys equal above this bit (8, or 0 when every digit was sorted)
+};
+struct RefineJobs {
+  RefineJob j[2];
+  const int64_t* te;
+  int32_t* list;  // [2][cap]
+  int64_t cap;
+};
+
+// a before b in the refined order (a and b from one run)
+__device__ __forceinline__ bool rf_before(const RefineJob& jb, const int64_t* te, uint64_t ka, uint32_t ra, uint64_t kb,
+                                          uint32_t rb) {
+  if (ka != kb) return ka < kb;
+  if (jb.contain && (ka & 1) == 0) {  // two ops starting together: the longer first
+    const int64_t ta = te[ra], tb = te[rb];  // one process: raw ends compare like corrected
+    if (ta != tb) return ta > tb;
+  }
+  return ra < rb;
+}
+
+constexpr int RF_THREADS = 256;
+constexpr int RF_ITEMS = 4;
+constexpr int RF_NET = 8;  // runs up to this length are sorted in registers
+
+__global__ __launch_bounds__(RF_THREADS) void k_refine(RefineJobs jobs, DevState* ds) {
+  __shared__ int32_t s_run[RF_THREADS * RF_ITEMS];  // run starts of this workgroup's positions
+  __shared__ int s_nrun;
+  const RefineJob& jb = jobs.j[blockIdx.y];
+  const int64_t n = *jb.count;
+  if (n < 2) return;
+  const int par = (int)ds->sort_parity[jb.id];
+  uint64_t* keys = jb.k[par];
+  uint32_t* vals = jb.v[par];
+  const int64_t p0 = (int64_t)blockIdx.x * RF_THREADS * RF_ITEMS + threadIdx.x;
+  if (threadIdx.x == 0) s_nrun = 0;
+  // each position with its neighbours, loads clamped and issued together
+  uint64_t kp[RF_ITEMS], kc[RF_ITEMS], kn[RF_ITEMS];
+#pragma unroll
+  for (int u = 0; u < RF_ITEMS; ++u) {
+    const int64_t p = p0 + u * RF_THREADS;
+    const int64_t pc = p < n ? p : n - 1;
+    kp[u] = keys[pc > 0 ? pc - 1 : 0];
+    kc[u] = keys[pc];
+    kn[u] = keys[pc + 1 < n ? pc + 1 : pc];
+  }
+  __syncthreads();
+  const int sh = jb.shift;
+  // the first positions of runs of two or more keys equal above the shift,
+  // gathered so that each is then ordered by a thread of its own (a run
+  // start is rare: ordering it where it was found would hold up its wave)
+#pragma unroll
+  for (int u = 0; u < RF_ITEMS; ++u) {
+    const int64_t p = p0 + u * RF_THREADS;
+    const bool start = p < n && p + 1 < n && (kn[u] >> sh) == (kc[u] >> sh) && !(p > 0 && (kp[u] >> sh) == (kc[u] >> sh));
+    const uint64_t b = ballot(start);
+    if (b == 0) continue;
+    int at = 0;
+    if (lane_id() == __ffsll((unsigned long long)b) - 1) at = atomicAdd(&s_nrun, popc(b));
+    at = __shfl(at, __ffsll((unsigned long long)b) - 1, WAVE);
+    if (start) s_run[at + popc(b & lanemask_lt())] = (int32_t)p;
+  }
+  __syncthreads();
+  const int nrun = s_nrun;
+  for (int ri = threadIdx.x; ri < nrun; ri += RF_THREADS) {
+    const int64_t p = s_run[ri];
+    const uint64_t hi = keys[p] >> sh;
+    // runs up to RF_NET: loaded at once and ordered by a sorting network
+    // in registers; longer ones by insertion sort in place, or listed
+    uint64_t rk[RF_NET];
+    uint32_t rr[RF_NET];
+#pragma unroll
+    for (int t = 0; t < RF_NET; ++t) {
+      const int64_t q = p + t < n ? p + t : n - 1;
+      rk[t] = keys[q];
+      rr[t] = vals[q];
+    }
+    int len = 0;
+#pragma unroll
+    for (int t = 0; t < RF_NET; ++t)
+      if (len == t && p + t < n && (rk[t] >> sh) == hi) len = t + 1;
+    if (len < RF_NET || p + RF_NET >= n || (keys[p + RF_NET] >> sh) != hi) {
+      // odd-even transposition network over the run's first len entries
+      // (entries past it compare as greater and never move)
+#pragma unroll
+      for (int round = 0; round < RF_NET; ++round) {
+#pragma unroll
+        for (int t = round & 1; t + 1 < RF_NET; t += 2) {
+          if (t + 1 < len && rf_before(jb, jobs.te, rk[t + 1], rr[t + 1], rk[t], rr[t])) {
+            const uint64_t k0 = rk[t];
+            const uint32_t r0 = rr[t];
+            rk[t] = rk[t + 1];
+            rr[t] = rr[t + 1];
+            rk[t + 1] = k0;
+            rr[t + 1] = r0;
+          }
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < RF_NET; ++t) {
+        if (t < len) {
+          keys[p + t] = rk[t];
+          vals[p + t] = rr[t];
+        }
+      }
+      continue;
+    }
+    int64_t e = p + RF_NET;
+    while (e < n && (keys[e] >> sh) == hi && e - p <= RF_SHORT) ++e;
+    if (e - p > RF_SHORT) {
+      const int at = atomicAdd(&ds->n_long[jb.slot], 1);
+      if (at < jobs.cap) jobs.list[(int64_t)jb.slot * jobs.cap + at] = (int32_t)p;
+      else set_status(ds, DS_TIES);
+      continue;
+    }
+    for (int64_t i = p + 1; i < e; ++i) {
+      const uint64_t k = keys[i];
+      const uint32_t r = vals[i];
+      int64_t j = i - 1;
+      while (j >= p) {
+        const uint64_t kj = keys[j];
+        const uint32_t rj = vals[j];
+        if (!rf_before(jb, jobs.te, k, r, kj, rj)) break;
+        keys[j + 1] = kj;
+        vals[j + 1] = rj;
+        --j;
+      }
+      keys[j + 1] = k;
+      vals[j + 1] = r;
+    }
+  }
+}
+
+// One workgroup per long run: the run is copied into the sort's other
+// buffer (free once the passes are done) at the same positions, sorted there
+// by a bitonic network that only compares pairs inside the run (the
+// positions past its end act as +infinity, and every comparator puts the
+// smaller element first), and copied back.
+__global__ __launch_bounds__(256) void k_refine_long(RefineJobs jobs, DevState* ds) {
+  const RefineJob& jb = jobs.j[blockIdx.y];
+  const int64_t nl = min((int64_t)ds->n_long[jb.slot], jobs.cap);
+  if (nl == 0) return;
+  const int64_t n = *jb.count;
+  const int par = (int)ds->sort_parity[jb.id];
+  uint64_t* keys = jb.k[par];
+  uint32_t* vals = jb.v[par];
+  uint64_t* sk = jb.k[par ^ 1];
+  uint32_t* sv = jb.v[par ^ 1];
+  __shared__ int64_t s_len;
+  for (int64_t q = blockIdx.x; q < nl; q += gridDim.x) {
+    const int64_t p = jobs.list[(int64_t)jb.slot * jobs.cap + q];
+    const uint64_t hi = keys[p] >> jb.shift;
+    if (threadIdx.x == 0) s_len = n - p;
+    __syncthreads();
+    // the run's end: the first position past it, found 256 at a time
+    for (int64_t b = p; b < n; b += 256) {
+      const int64_t i = b + threadIdx.x;
+      if (i < n && (keys[i] >> jb.shift) != hi) atomicMin((unsigned long long*)&s_len, (unsigned long long)(i - p));
+      __syncthreads();
+      if (s_len < n - p) break;
+      __syncthreads();
+    }
+    const int64_t len = s_len;
+    for (int64_t i = threadIdx.x; i < len; i += 256) {
+      sk[p + i] = keys[p + i];
+      sv[p + i] = vals[p + i];
+    }
+    __syncthreads();
+    int64_t m = 1;
+    while (m < len) m <<= 1;
+    for (int64_t size = 2; size <= m; size <<= 1) {
+      for (int64_t stride = size >> 1; stride > 0; stride >>= 1) {
+        for (int64_t i = threadIdx.x; i < len; i += 256) {
+          // first step of a merge: the mirror in the block; then halvings
+          const int64_t l = stride == (size >> 1) ? (i ^ (size - 1)) : (i ^ stride);
+          if (l > i && l < len) {
+            const uint64_t ki = sk[p + i], kl = sk[p + l];
+            const uint32_t ri = sv[p + i], rl = sv[p + l];
+            if (rf_before(jb, jobs.te, kl, rl, ki, ri)) {
+              sk[p + i] = kl;
+              sv[p + i] = rl;
+              sk[p + l] = ki;
+              sv[p + l] = ri;
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
+    for (int64_t i = threadIdx.x; i < len; i += 256) {
+      keys[p + i] = sk[p + i];
+      vals[p + i] = sv[p + i];
+    }
+    __syncthreads();
+  }
+}
+
+void launch_refine(Ctx& c) {
+  RefineJobs jobs{};
+  int m = 0;
+  int64_t n_max = 1;
+  for (SortBufs* s : {&c.sK, &c.sC}) {
+    const bool con = s == &c.sC;
+    if (con ? !c.contain : s->first == 0) continue;
+    jobs.j[m++] = RefineJob{{s->k[0], s->k[1]}, {s->v[0], s->v[1]}, con ? &c.ds->nCL : &c.ds->nK, s->id, con ? 1 : 0,
+                            con ? 1 : 0, 8 * s->first};
+    n_max = std::max<int64_t>(n_max, s->n_max);
+  }
+  if (m == 0) return;
+  jobs.te = c.ev.te;
+  jobs.list = c.rf_list;
+  jobs.cap = c.rf_cap;
+  const int64_t grid = cdiv(n_max, RF_THREADS * RF_ITEMS);
+  hipLaunchKernelGGL(k_refine, dim3((unsigned)grid, (unsigned)m), dim3(RF_THREADS), 0, c.st, jobs, c.ds);
+  hipLaunchKernelGGL(k_refine_long, dim3(64, (unsigned)m), dim3(256), 0, c.st, jobs, c.ds);
 }
 
 }  // namespace hx
