@@ -213,6 +213,7 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
   __shared__ uint64_t s_g[6][QY_GROUPS];    // window maxima over the tile's groups
   __shared__ uint64_t s_gpre[QY_GROUPS];    // max over the tile's earlier groups and all earlier tiles
   __shared__ uint16_t s_esc[CT_TILE];
+  __shared__ uint64_t s_prev[QY_GROUPS];    // group maxima of the previous tile (its M1 entries)
   __shared__ int s_nesc;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int64_t n = a.ds->nCL;
@@ -253,6 +254,10 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) m = s_v[tid * 8 + i] > m ? s_v[tid * 8 + i] : m;
     s_sub[tid] = m;
+  }
+  if (wv == 1) {  // the previous tile's group maxima: most escaping answers lie there
+    const uint64_t pm = a.M[1][tile > 0 ? (tile - 1) * QY_GROUPS + lane : lane];
+    s_prev[lane] = tile > 0 ? pm : 0ull;
   }
   if (wv == 0) {  // group-level window maxima and exclusive prefix maxima
     const uint64_t m1r = a.M[1][tile * QY_GROUPS + (lane < ng ? lane : 0)];
@@ -345,7 +350,18 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
     const int64_t p = base + lp;
     const uint64_t kk = keys[p];
     const uint64_t q = (key_seg(a, kk) << a.vb) | (uint64_t)(key_rel(a, kk) + 1);
-    const int64_t ans = wave_escape(a, tile, q, n);
+    // the last group of the previous tile holding a value above q, then its
+    // last position above q (one load); else the general climb
+    int64_t ans = -1;
+    const uint64_t gb = ballot(s_prev[lane] > q);
+    if (gb) {
+      const int g = 63 - __clzll((long long)gb);
+      const int64_t e0 = (tile - 1) * CT_TILE + (int64_t)g * 64;
+      const uint64_t v = a.V[e0 + lane];
+      const uint64_t vb = ballot(v > q);
+      if (vb) ans = e0 + 63 - __clzll((long long)vb);
+    }
+    if (!gb) ans = wave_escape(a, tile, q, n);
     if (lane == 0) {
       if (ans < 0) set_status(a.ds, DS_LOGIC);
       a.par[p] = (int32_t)ans;
