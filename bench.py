@@ -43,20 +43,22 @@ def source_hash(stage: str) -> str:
 
 
 def sort_units(stats):
-    """Key-passes the radix launches of the sort stage must make: the
-    timeline and containment sorts, and the join sort (which moves data only
-    when the correlation table cannot be used) for its digits in the same
-    range, each move their keys once per digit on which they differ.  Also
-    the number of pass launches of the stage: one per digit of the wider of
-    the timeline and containment keys, except a lowest digit that both leave
-    to the refine pass (bit 31 of the mask)."""
-    stage = [stats[0], stats[2]]
-    first = 1 if all((skipped >> 31) & 1 for _, skipped, _ in stage) else 0
-    last = max(nd for _, _, nd in stage)
+    """Key-passes the radix launches of the sort stage must make, and the
+    number of those launches.  Pass p of a sort is its digit first + p, where
+    first is 1 when the sort leaves its lowest digit to the refine pass (bit
+    31 of its skipped-digit mask).  The stage makes as many passes as the
+    timeline and containment sorts need; the join sort (which moves data only
+    when the correlation table cannot be used) runs its passes in the same
+    launches.  A sort moves its keys once per pass whose digit is not
+    skipped."""
+    def first(skipped):
+        return 1 if (skipped >> 31) & 1 else 0
+    passes = max(nd - first(skipped) for _, skipped, nd in (stats[0], stats[2]))
     units = 0
-    for nkeys, skipped, nd in stats:  # the join sort's digits in the stage's range run in its launches
-        units += nkeys * sum(1 for d in range(first, min(nd, last)) if not (skipped >> d) & 1)
-    return units, last - first
+    for nkeys, skipped, nd in stats:
+        f = first(skipped)
+        units += nkeys * sum(1 for d in range(f, min(nd, f + passes)) if not (skipped >> d) & 1)
+    return units, passes
 
 
 def profiled_traffic(stage: str, workload: str):

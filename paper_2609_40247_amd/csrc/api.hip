@@ -394,26 +394,26 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   launch_join_plan(c);
   stage_end(c, HERSCHEL_STAGE_PREP);
 
-  // The three sorts share their digit passes (blockIdx.y picks the sort; a
-  // sort whose digit is skipped leaves at once, as the join sort's do when
-  // the correlation table is used).  The timeline and containment sorts leave
-  // their lowest digit to the refine pass; the join sort's digits beyond
-  // theirs run on the join stream.  Nothing else runs beside the sorts: a
-  // large grid on another stream would take the CUs first and hold up the
-  // passes, which every later stage waits for.
+  // The three sorts share their digit passes, pass p of a sort being its
+  // digit first + p (a sort whose digit is skipped has no tiles in the
+  // launch, as the join sort has none when the correlation table is used).
+  // The timeline and containment sorts leave their lowest digit to the
+  // refine pass; the join sort's passes beyond theirs run on the join
+  // stream.  Nothing else runs beside the sorts: a large grid on another
+  // stream would take the CUs first and hold up the passes, which every
+  // later stage waits for.
   const int ks = c.contain ? 3 : 2;
   SortBufs* ss[3] = {&c.sK, &c.sC, &c.sJ};
   const int32_t* cc[3] = {&c.ds->nK, &c.ds->nCL, &c.ds->nJ};
   ss[ks - 1] = &c.sJ;
   cc[ks - 1] = &c.ds->nJ;
-  const int d_shared = c.contain ? std::max(c.sK.nd, c.sC.nd) : c.sK.nd;
-  const int d_first = c.contain ? std::min(c.sK.first, c.sC.first) : c.sK.first;
+  int p_shared = c.sK.nd - c.sK.first;
+  if (c.contain) p_shared = std::max(p_shared, c.sC.nd - c.sC.first);
   stage_begin(c, HERSCHEL_STAGE_HIST);
   launch_hist_multi(c, ss, cc, ks);
   stage_end(c, HERSCHEL_STAGE_HIST);
-  launch_sort_multi(c, ss, cc, ks, 0, d_first);  // the join sort's lowest digit alone
   stage_begin(c, HERSCHEL_STAGE_SORT);
-  launch_sort_multi(c, ss, cc, ks, d_first, d_shared);
+  launch_sort_multi(c, ss, cc, ks, 0, p_shared);
   stage_end(c, HERSCHEL_STAGE_SORT);
   launch_refine(c);
   (void)hipEventRecord(dsx->e[0], s0);
@@ -439,7 +439,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
   stage_begin(c, HERSCHEL_STAGE_JOIN);
   launch_join_table(c);
-  launch_sort_multi(c, &ss[ks - 1], &cc[ks - 1], 1, d_shared, c.sJ.nd);
+  launch_sort_multi(c, &ss[ks - 1], &cc[ks - 1], 1, p_shared, c.sJ.nd - c.sJ.first);
   launch_join(c);
   stage_end(c, HERSCHEL_STAGE_JOIN);
   stage_begin(c, HERSCHEL_STAGE_EDGES);

@@ -35,9 +35,8 @@ enum : int {
   TK_PREP = 0,
   TK_UNION = 1,
   TK_VBUILD = 2,
-  TK_RADIX = 8  // + 8 * sort + pass
+  N_TICKETS = 3
 };
-constexpr int N_TICKETS = TK_RADIX + 8 * 3;
 
 constexpr int N_SORTS = 3;  // 0 timeline, 1 join, 2 containment
 // join counters; the correlation table path keeps JC_MLAUNCH (launches with a

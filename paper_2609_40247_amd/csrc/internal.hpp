@@ -84,7 +84,7 @@ size_t layout_workspace(Ctx& c, char* base);
 void launch_init(Ctx& c);
 void launch_prep(Ctx& c);
 void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k);
-void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k, int d0, int d1);
+void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k, int p0, int p1);
 void launch_refine(Ctx& c);
 void launch_names(Ctx& c);
 void launch_timeline(Ctx& c);

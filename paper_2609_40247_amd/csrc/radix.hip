@@ -162,23 +162,35 @@ struct SortJob {
   uint32_t* status1;  // [nd - 1][tiles_max * 256] later digits (each cleared by the previous pass)
   int64_t tiles_max;
   int nd, id, first;
+  int d;  // the digit this launch sorts on
 };
 struct SortJobs {
   SortJob j[N_SORTS];
+  int m;  // sorts in the launch
 };
 
-// One digit pass of up to N_SORTS independent sorts (blockIdx.y picks one).
+// One digit pass of up to N_SORTS independent sorts (each on its own digit).
 // 512 threads rank a tile of 4096 keys; the tile (48 KB) and the per-wave
 // digit counts (8 KB, in the key area until the keys are placed) keep the
 // LDS of a workgroup under a third of the CU's (with the allocation
-// granularity), so three tiles share a CU and a launch of up to 768 tiles
-// has every tile resident at once.
+// granularity), so three tiles share a CU.
+//
+// The grid is one-dimensional and sized for every sort's largest input.
+// The tiles whose digit moves data are numbered sort after sort, and
+// workgroup b sorts tile b; the workgroups past the last tile leave at
+// once, after the real tiles have been dispatched.  A tile's look-back waits
+// only for tiles of lower number, whose workgroups have lower indices: the
+// dispatcher starts workgroups in index order, so the lowest unfinished
+// tile always has its workgroup running and every wait ends (a wait that
+// exceeds its bound gives up with an error all the same).  No tile ticket:
+// a counter that every workgroup increments is one address, served one
+// request at a time, and it held the last tiles back by microseconds.
 constexpr int RS_NW = RS_THREADS / WAVE;  // waves per workgroup
 constexpr int RS_NSL = RS_THREADS / 256;  // look-back slices per digit
 constexpr int RS_LB_WIN = 16;             // predecessors polled per slice and round trip
 
 __global__ __launch_bounds__(RS_THREADS) __attribute__((amdgpu_waves_per_eu(RS_WAVES_PER_EU)))
-void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
+void k_radix_pass(SortJobs jobs, DevState* ds) {
   constexpr int NW = RS_NW, NSL = RS_NSL, LB_WIN = RS_LB_WIN;
   __shared__ uint64_t s_key[RS_TILE];
   __shared__ uint32_t s_val[RS_TILE];
@@ -186,38 +198,53 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   __shared__ uint32_t s_scan[NW + 1];
   __shared__ uint32_t s_lb_sum[NSL][256];
   __shared__ uint8_t s_lb_state[NSL][256];
-  __shared__ int s_tile;
   static_assert(NW * 256 * 4 <= RS_TILE * 8, "per-wave counts must fit the key area");
   uint32_t(*s_wh)[256] = reinterpret_cast<uint32_t(*)[256]>(s_key);
   // the global offsets reuse the look-back's scratch once the look-back is over
   uint32_t* s_glob = &s_lb_sum[0][0];
 
-  const SortJob& jb = jobs.j[blockIdx.y];
-  if (d >= jb.nd || d < jb.first) return;
-  const int id = jb.id;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int dgt = tid & 255, slice = tid >> 8;
+  const uint32_t b = blockIdx.x;
+  // Per sort: the next digit's look-back words of tile index b are cleared
+  // here (the next pass starts only after this one has ended), the first
+  // pass records which buffer will hold the result (the parity of the
+  // digits that move data), and the tiles of a digit on which every key
+  // agrees (plan of the histogram kernel) are not sorted at all.
+  uint32_t nt[N_SORTS];
+#pragma unroll
+  for (int i = 0; i < N_SORTS; ++i) {
+    nt[i] = 0;
+    if (i >= jobs.m) continue;
+    const SortJob& jb = jobs.j[i];
+    const uint32_t n = (uint32_t)*jb.count;
+    const uint32_t tiles = (n + RS_TILE - 1) / RS_TILE;
+    const uint32_t triv = ds->sort_trivial[jb.id];
+    if (b < tiles && jb.d + 1 < jb.nd && tid < 256)
+      jb.status1[((int64_t)(jb.d - jb.first) * jb.tiles_max + b) * 256 + tid] = 0u;
+    if (jb.d == jb.first && b == 0 && tid == 0)
+      ds->sort_parity[jb.id] = (uint32_t)(popc(~triv & ((jb.nd >= 32 ? 0u : 1u << jb.nd) - 1u)) & 1);
+    nt[i] = ((triv >> jb.d) & 1) ? 0u : tiles;
+  }
+  int sel = -1;
+  uint32_t t = b;
+#pragma unroll
+  for (int i = 0; i < N_SORTS; ++i) {
+    if (sel < 0) {
+      if (t < nt[i])
+        sel = i;
+      else
+        t -= nt[i];
+    }
+  }
+  if (sel < 0) return;
+  const SortJob& jb = jobs.j[sel];
+  const int d = jb.d, id = jb.id;
   const uint32_t n = (uint32_t)*jb.count;
-  const bool has_tile = (int64_t)blockIdx.x * RS_TILE < (int64_t)n;
-  // The next digit's look-back words of this workgroup's tile index are
-  // cleared here: the next pass starts only after this one has ended.
-  if (has_tile && d + 1 < jb.nd && tid < 256)
-    jb.status1[((int64_t)(d - jb.first) * jb.tiles_max + blockIdx.x) * 256 + tid] = 0u;
-  // The plan (trivial digits, offsets) was made by the histogram kernel.  A
-  // digit is trivial iff one bin holds every key; the input buffer's parity
-  // is the number of non-trivial digits below this one.  Workgroups with no
-  // tile to sort leave before the ticket: the ticket counter is one address,
-  // and every request to it is served in turn.  The first cdiv(n, tile)
-  // workgroups stay, so they draw exactly the tickets of the real tiles.
   const uint32_t triv = ds->sort_trivial[id];
-  // which buffer holds the result: parity of the digits that move data
-  if (d == jb.first && blockIdx.x == 0 && tid == 0)
-    ds->sort_parity[id] = (uint32_t)(popc(~triv & ((jb.nd >= 32 ? 0u : 1u << jb.nd) - 1u)) & 1);
-  if (((triv >> d) & 1) || !has_tile) return;
   const uint32_t gexcl = ds->hist[id][d][dgt];
   // the tile's digit counts, in the row area until the rows are placed
   uint32_t* s_cnt = s_val;
-  if (tid == 0) s_tile = (int)atomicAdd(&ds->ticket[TK_RADIX + 8 * id + d], 1u);
   for (int i = tid; i < NW * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
   if (tid < 256) s_cnt[tid] = 0;
   __syncthreads();
@@ -227,7 +254,7 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   const uint32_t* vin = jb.v[parity];
   uint32_t* vout = jb.v[parity ^ 1];
   uint32_t* status = d == jb.first ? jb.status0 : jb.status1 + (int64_t)(d - jb.first - 1) * jb.tiles_max * 256;
-  const int tile = s_tile;
+  const int tile = (int)t;
   const int64_t base = (int64_t)tile * RS_TILE;
 
   const int shift = 8 * d;
@@ -264,22 +291,30 @@ void k_radix_pass(SortJobs jobs, DevState* ds, int d) {
   if (tid < 256) st_agent(&st[tid], (tile == 0 ? RS_FLAG_P : RS_FLAG_A) | cnt);
 
   // Wave-private ranking in input order: items in order, lanes in order.
-  const uint64_t lt = lanemask_lt();
+  // A lane's peers (the lanes with its digit) are found bit by bit: for each
+  // digit bit, the lanes whose bit differs from this lane's are marked
+  // mismatched (m is 0 or all ones, the lane's bit; the ballot holds every
+  // lane's), one three-input bit operation per 32-lane half.
+  constexpr int OR_XOR = 0xF0 | (0xCC ^ 0xAA);  // truth table of a | (b ^ c)
 #pragma unroll
   for (int j = 0; j < RS_ITEMS; ++j) {
     const int dg = digit_of(j);
     const bool ok = dg < 256;
-    uint64_t peers = ballot(ok);
+    const uint64_t okm = ballot(ok);  // lanes past the end are nobody's peers
+    uint32_t mis_lo = ~(uint32_t)okm, mis_hi = ~(uint32_t)(okm >> 32);
 #pragma unroll
     for (int b = 0; b < 8; ++b) {
-      const bool bit = (dg >> b) & 1;
-      const uint64_t bb = ballot(bit);
-      peers &= bit ? bb : ~bb;
+      const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe(dg, b, 1);
+      const uint64_t bb = __builtin_amdgcn_uicmp(m, 0u, 33);  // ballot(m != 0)
+      mis_lo = __builtin_amdgcn_bitop3_b32(mis_lo, (uint32_t)bb, m, OR_XOR);
+      mis_hi = __builtin_amdgcn_bitop3_b32(mis_hi, (uint32_t)(bb >> 32), m, OR_XOR);
     }
+    // peers in lower lanes, and all peers
+    const uint32_t below = __builtin_amdgcn_mbcnt_hi(~mis_hi, __builtin_amdgcn_mbcnt_lo(~mis_lo, 0u));
     const uint32_t before = ok ? s_wh[wv][dg] : 0u;
-    rank[j] = before + (uint32_t)popc(peers & lt);
+    rank[j] = before + below;
     __builtin_amdgcn_wave_barrier();
-    if (ok && (peers & lt) == 0) s_wh[wv][dg] = before + (uint32_t)popc(peers);
+    if (ok && below == 0) s_wh[wv][dg] = before + (uint32_t)(__builtin_popcount(~mis_lo) + __builtin_popcount(~mis_hi));
     __builtin_amdgcn_wave_barrier();
   }
   __syncthreads();
@@ -418,21 +453,24 @@ void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
   hipLaunchKernelGGL(k_hist_plan, dim3((unsigned)nd, (unsigned)m), dim3(PLAN_THREADS), 0, c.st, jobs, c.ds);
 }
 
-// Digit passes d0 .. d1-1 of up to N_SORTS sorts, one launch per digit
-// (none for a digit that every sort leaves to the refine pass).
-void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k, int d0, int d1) {
-  for (int d = d0; d < d1; ++d) {
+// Passes p0 .. p1-1 of up to N_SORTS sorts, one launch per pass: pass p of
+// a sort is its digit first + p (its lowest digit is left to the refine
+// pass when first is 1).  The grid covers every sort's largest input.
+void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, int k, int p0, int p1) {
+  for (int p = p0; p < p1; ++p) {
     SortJobs jobs{};
-    int64_t grid = 1;
+    int64_t grid = 0;
     int m = 0;
     for (int i = 0; i < k; ++i) {
-      if (d >= s[i]->nd || d < s[i]->first) continue;
+      const int d = s[i]->first + p;
+      if (d >= s[i]->nd) continue;
       jobs.j[m++] = SortJob{{s[i]->k[0], s[i]->k[1]}, {s[i]->v[0], s[i]->v[1]}, count[i], s[i]->status0,
-                            s[i]->status1, s[i]->tiles_max, s[i]->nd, s[i]->id, s[i]->first};
-      grid = std::max<int64_t>(grid, s[i]->tiles_max);
+                            s[i]->status1, s[i]->tiles_max, s[i]->nd, s[i]->id, s[i]->first, d};
+      grid += s[i]->tiles_max;
     }
     if (m == 0) continue;
-    hipLaunchKernelGGL(k_radix_pass, dim3((unsigned)grid, (unsigned)m), dim3(RS_THREADS), 0, c.st, jobs, c.ds, d);
+    jobs.m = m;
+    hipLaunchKernelGGL(k_radix_pass, dim3((unsigned)grid), dim3(RS_THREADS), 0, c.st, jobs, c.ds);
   }
 }
 
