@@ -65,12 +65,12 @@ size_t layout_workspace(Ctx& c, char* base) {
   sort_plan(c.sC, 2, n, c.pb + c.tb + c.wb + 1, true);
   // digit 0's look-back words are cleared here; each later digit's are
   // cleared by the pass before it
-  c.sK.status0 = b.take<uint32_t>(c.sK.tiles_max * 256);
-  c.sJ.status0 = b.take<uint32_t>(c.sJ.tiles_max * 256);
+  c.sK.status0 = b.take<uint32_t>(c.sK.tiles_max * RS_LB_WORDS);
+  c.sJ.status0 = b.take<uint32_t>(c.sJ.tiles_max * RS_LB_WORDS);
   if (c.contain) {
     c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
     c.vb_status = b.take<uint64_t>(c.vb_tiles);
-    c.sC.status0 = b.take<uint32_t>(c.sC.tiles_max * 256);
+    c.sC.status0 = b.take<uint32_t>(c.sC.tiles_max * RS_LB_WORDS);
     // pyramid levels above the tile maxima: built by atomic maxima, from zero
     c.nlev = 3;
     while (cdiv(n, (int64_t)1 << (6 * (c.nlev - 1))) > 64) ++c.nlev;
@@ -81,7 +81,7 @@ size_t layout_workspace(Ctx& c, char* base) {
   }
   c.zero_bytes = align_up(b.off - z0);
   for (SortBufs* s : {&c.sK, &c.sJ, &c.sC})
-    if (s != &c.sC || c.contain) s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * 256);
+    if (s != &c.sC || c.contain) s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * RS_LB_WORDS);
   // long runs of the refine pass (each has more than RF_SHORT keys)
   c.rf_cap = cdiv(n, RF_SHORT + 1) + 1;
   c.rf_list = b.take<int32_t>(2 * c.rf_cap);

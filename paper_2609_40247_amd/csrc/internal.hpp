@@ -13,8 +13,8 @@ namespace hx {
 struct SortBufs {
   uint64_t* k[2] = {nullptr, nullptr};
   uint32_t* v[2] = {nullptr, nullptr};
-  uint32_t* status0 = nullptr;          // [tiles_max * 256] look-back words of digit 0
-  uint32_t* status1 = nullptr;          // [nd - 1][tiles_max * 256] digits 1..nd-1
+  uint32_t* status0 = nullptr;          // [tiles_max * RS_LB_WORDS] look-back words of the first digit
+  uint32_t* status1 = nullptr;          // [nd - 1][tiles_max * RS_LB_WORDS] the later digits
   int64_t n_max = 0;                    // capacity (host upper bound of the count)
   int64_t tiles_max = 0;
   int nd = 0;                           // 8-bit digits of the key
@@ -114,6 +114,7 @@ constexpr int AG_CHAIN = 64;
 constexpr int RS_THREADS = 512;
 constexpr int RS_ITEMS = 8;
 constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 4096 keys per tile
+constexpr int RS_LB_WORDS = 512;                // look-back words per tile: 256 counts, 256 window sums
 constexpr int RS_WAVES_PER_EU = 6;              // three workgroups of 8 waves per CU
 // Keys wider than 32 bits leave their lowest digit to the refine pass, which
 // orders the runs of keys equal above it; runs up to RF_SHORT are fixed in

@@ -158,15 +158,15 @@ struct SortJob {
   uint64_t* k[2];
   uint32_t* v[2];
   const int32_t* count;
-  uint32_t* status0;  // [tiles_max * 256] look-back words of the first digit (cleared by the init kernel)
-  uint32_t* status1;  // [nd - 1][tiles_max * 256] later digits (each cleared by the previous pass)
+  uint32_t* status0;  // [tiles_max][RS_LB_WORDS] look-back words of the first digit (cleared by the init kernel)
+  uint32_t* status1;  // [nd - 1][tiles_max][RS_LB_WORDS] later digits (each cleared by the previous pass)
   int64_t tiles_max;
   int nd, id, first;
   int d;  // the digit this launch sorts on
 };
 struct SortJobs {
-  SortJob j[N_SORTS];
-  int m;  // sorts in the launch
+  SortJob j[N_SORTS];  // slots m.. repeat slot 0
+  int m;               // sorts in the launch
 };
 
 // One digit pass of up to N_SORTS independent sorts (each on its own digit).
@@ -187,7 +187,7 @@ struct SortJobs {
 // request at a time, and it held the last tiles back by microseconds.
 constexpr int RS_NW = RS_THREADS / WAVE;  // waves per workgroup
 constexpr int RS_NSL = RS_THREADS / 256;  // look-back slices per digit
-constexpr int RS_LB_WIN = 16;             // predecessors polled per slice and round trip
+constexpr int RS_LB_WIN = 16;             // positions polled per slice and round trip
 
 __global__ __launch_bounds__(RS_THREADS) __attribute__((amdgpu_waves_per_eu(RS_WAVES_PER_EU)))
 void k_radix_pass(SortJobs jobs, DevState* ds) {
@@ -211,20 +211,32 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   // pass records which buffer will hold the result (the parity of the
   // digits that move data), and the tiles of a digit on which every key
   // agrees (plan of the histogram kernel) are not sorted at all.
-  uint32_t nt[N_SORTS];
+  // The counts and plans of all sorts are loaded together (one round trip;
+  // the slots past the launch's sorts repeat its first).
+  uint32_t nn[N_SORTS], tr[N_SORTS], nt[N_SORTS];
+  const int32_t* cp[N_SORTS];
+  int ids[N_SORTS];
+#pragma unroll
+  for (int i = 0; i < N_SORTS; ++i) {
+    cp[i] = jobs.j[i].count;
+    ids[i] = jobs.j[i].id;
+  }
+#pragma unroll
+  for (int i = 0; i < N_SORTS; ++i) {
+    nn[i] = (uint32_t)*cp[i];
+    tr[i] = ds->sort_trivial[ids[i]];
+  }
 #pragma unroll
   for (int i = 0; i < N_SORTS; ++i) {
     nt[i] = 0;
     if (i >= jobs.m) continue;
     const SortJob& jb = jobs.j[i];
-    const uint32_t n = (uint32_t)*jb.count;
-    const uint32_t tiles = (n + RS_TILE - 1) / RS_TILE;
-    const uint32_t triv = ds->sort_trivial[jb.id];
-    if (b < tiles && jb.d + 1 < jb.nd && tid < 256)
-      jb.status1[((int64_t)(jb.d - jb.first) * jb.tiles_max + b) * 256 + tid] = 0u;
+    const uint32_t tiles = (nn[i] + RS_TILE - 1) / RS_TILE;
+    if (b < tiles && jb.d + 1 < jb.nd && tid < RS_LB_WORDS)
+      jb.status1[((int64_t)(jb.d - jb.first) * jb.tiles_max + b) * RS_LB_WORDS + tid] = 0u;
     if (jb.d == jb.first && b == 0 && tid == 0)
-      ds->sort_parity[jb.id] = (uint32_t)(popc(~triv & ((jb.nd >= 32 ? 0u : 1u << jb.nd) - 1u)) & 1);
-    nt[i] = ((triv >> jb.d) & 1) ? 0u : tiles;
+      ds->sort_parity[jb.id] = (uint32_t)(popc(~tr[i] & ((jb.nd >= 32 ? 0u : 1u << jb.nd) - 1u)) & 1);
+    nt[i] = ((tr[i] >> jb.d) & 1) ? 0u : tiles;
   }
   int sel = -1;
   uint32_t t = b;
@@ -240,20 +252,17 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   if (sel < 0) return;
   const SortJob& jb = jobs.j[sel];
   const int d = jb.d, id = jb.id;
-  const uint32_t n = (uint32_t)*jb.count;
-  const uint32_t triv = ds->sort_trivial[id];
+  static_assert(N_SORTS == 3, "the selects below name every sort");
+  const uint32_t n = sel == 0 ? nn[0] : sel == 1 ? nn[1] : nn[2];
+  const uint32_t triv = sel == 0 ? tr[0] : sel == 1 ? tr[1] : tr[2];
   const uint32_t gexcl = ds->hist[id][d][dgt];
-  // the tile's digit counts, in the row area until the rows are placed
-  uint32_t* s_cnt = s_val;
-  for (int i = tid; i < NW * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
-  if (tid < 256) s_cnt[tid] = 0;
-  __syncthreads();
   const int parity = popc(~triv & ((1u << d) - 1u)) & 1;
   const uint64_t* kin = jb.k[parity];
   uint64_t* kout = jb.k[parity ^ 1];
   const uint32_t* vin = jb.v[parity];
   uint32_t* vout = jb.v[parity ^ 1];
-  uint32_t* status = d == jb.first ? jb.status0 : jb.status1 + (int64_t)(d - jb.first - 1) * jb.tiles_max * 256;
+  uint32_t* status =
+      d == jb.first ? jb.status0 : jb.status1 + (int64_t)(d - jb.first - 1) * jb.tiles_max * RS_LB_WORDS;
   const int tile = (int)t;
   const int64_t base = (int64_t)tile * RS_TILE;
 
@@ -273,6 +282,12 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
     key[j] = kin[idx];
     val[j] = vin[idx];
   }
+  // the counters are cleared while the loads are in flight; the tile's
+  // digit counts sit in the row area until the rows are placed
+  uint32_t* s_cnt = s_val;
+  for (int i = tid; i < NW * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
+  if (tid < 256) s_cnt[tid] = 0;
+  __syncthreads();
   // an item's digit is re-derived from its key where needed (256: past the end)
   auto digit_of = [&](int j) -> int {
     return wbase + j * WAVE < n ? (int)((key[j] >> shift) & 255) : 256;
@@ -287,8 +302,10 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   }
   __syncthreads();
   const uint32_t cnt = tid < 256 ? s_cnt[tid] : 0u;
-  uint32_t* st = status + (uint32_t)tile * 256u;
+  // this tile's words: its own counts (then its prefix) and its window sums
+  uint32_t* st = status + (uint32_t)tile * RS_LB_WORDS;
   if (tid < 256) st_agent(&st[tid], (tile == 0 ? RS_FLAG_P : RS_FLAG_A) | cnt);
+  if (tile == 0 && tid < 256) st_agent(&st[256 + tid], RS_FLAG_P | cnt);
 
   // Wave-private ranking in input order: items in order, lanes in order.
   // A lane's peers (the lanes with its digit) are found bit by bit: for each
@@ -350,33 +367,42 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
     }
   }
 
-  // Look-back: every digit has NSL threads, each polling LB_WIN predecessors
-  // per round trip (independent loads), so one round covers NSL * LB_WIN
-  // tiles.  A round is used up to the nearest tile that published its
-  // inclusive prefix; a round with an unpublished tile before that is
-  // polled again.  The loop condition is uniform over the workgroup.
+  // Look-back: every digit has NSL threads, each polling LB_WIN positions
+  // per round trip (independent loads), WIN = NSL * LB_WIN per round.  The
+  // first round polls the WIN nearest predecessors' own counts.  If none of
+  // them has published its inclusive prefix, the tile publishes the sum of
+  // its window (its count and those WIN), and the later rounds poll the
+  // window sums ending WIN + 1, 2 (WIN + 1), ... tiles before it, which
+  // tile into the rest: WIN (WIN + 1) tiles per round instead of WIN.  A
+  // round is used up to the nearest position that published a prefix; a
+  // round with an unpublished position before that is polled again.  The
+  // loop condition is uniform over the workgroup.
   uint32_t excl = 0;
   if (tile > 0) {
-    int pred = tile - 1;  // newest predecessor not yet counted
+    constexpr int WIN = NSL * LB_WIN;
+    int pred = tile - 1;  // newest position not yet counted
+    int stride = 1;       // 1: own counts, WIN + 1: window sums
     bool done = false;
     uint32_t spins = 0;
     for (;;) {
-      const int top = pred - slice * LB_WIN;
+      const uint32_t* src = status + (stride == 1 ? 0 : 256) + dgt;
+      const int top = pred - stride * slice * LB_WIN;
       uint32_t sum = 0;
-      int state = 1;  // 0: not ready, 1: all aggregates, 2: reached a prefix
+      int state = 1;  // 0: not ready, 1: all partial sums, 2: reached a prefix
       if (!done) {
         uint32_t sv[LB_WIN];
 #pragma unroll
         for (int i = 0; i < LB_WIN; ++i)
-          sv[i] = ld_agent(&status[(uint32_t)max(top - i, 0) * 256u + (uint32_t)dgt]);
+          sv[i] = ld_agent(&src[(uint32_t)max(top - stride * i, 0) * RS_LB_WORDS]);
 #pragma unroll
         for (int i = 0; i < LB_WIN; ++i) {
-          const uint32_t f = top - i >= 0 ? sv[i] >> 30 : 2u;  // before tile 0: prefix 0
+          const bool real = top - stride * i >= 0;
+          const uint32_t f = real ? sv[i] >> 30 : 2u;  // before tile 0: prefix 0
           if (state == 1) {
             if (f == 0) {
               state = 0;
             } else {
-              sum += top - i >= 0 ? sv[i] & RS_VAL : 0u;
+              sum += real ? sv[i] & RS_VAL : 0u;
               if (f == 2) state = 2;
             }
           }
@@ -411,14 +437,25 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
           }
         } else {
           excl += add;
-          pred -= NSL * LB_WIN;
-          if (res == 2 || pred < 0) done = true;
+          if (res == 2) {
+            done = true;
+          } else if (stride == 1) {
+            if (tid < 256) st_agent(&st[256 + tid], RS_FLAG_A | ((excl + cnt) & RS_VAL));
+            pred -= WIN;
+            stride = WIN + 1;
+          } else {
+            pred -= stride * WIN;
+          }
+          if (pred < 0) done = true;
         }
       }
       if (!__syncthreads_or(!done)) break;
       if (again) __builtin_amdgcn_s_sleep(1);
     }
-    if (tid < 256) st_agent(&st[tid], RS_FLAG_P | ((excl + cnt) & RS_VAL));
+    if (tid < 256) {
+      st_agent(&st[tid], RS_FLAG_P | ((excl + cnt) & RS_VAL));
+      st_agent(&st[256 + tid], RS_FLAG_P | ((excl + cnt) & RS_VAL));
+    }
   }
   // the look-back loop ends on a barrier after its last read of s_lb_sum
   if (tid < 256) s_glob[tid] = gexcl + excl;
@@ -470,6 +507,7 @@ void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
     }
     if (m == 0) continue;
     jobs.m = m;
+    for (int i = m; i < N_SORTS; ++i) jobs.j[i] = jobs.j[0];
     hipLaunchKernelGGL(k_radix_pass, dim3((unsigned)grid), dim3(RS_THREADS), 0, c.st, jobs, c.ds);
   }
 }
