@@ -30,12 +30,12 @@ enum : uint32_t {
   DS_LOGIC = 32u     // an internal consistency check failed
 };
 
-// Ticket slots: one per look-back kernel launch in a call.
+// Ticket slots: look-back kernels whose tiles are numbered in arrival order.
+// (The others number them by workgroup index: a tile waits only for tiles of
+// lower index, whose workgroups the dispatcher started first.)
 enum : int {
-  TK_PREP = 0,
-  TK_UNION = 1,
-  TK_VBUILD = 2,
-  N_TICKETS = 3
+  TK_UNION = 0,
+  N_TICKETS = 1
 };
 
 constexpr int N_SORTS = 3;  // 0 timeline, 1 join, 2 containment

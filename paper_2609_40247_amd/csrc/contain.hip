@@ -77,7 +77,6 @@ constexpr int VB_THREADS = 1024;
 constexpr int VB_ITEMS = CT_TILE / VB_THREADS;
 
 __global__ __launch_bounds__(VB_THREADS) void k_vbuild(ContainArgs a) {
-  __shared__ int s_tile;
   __shared__ uint64_t s_w[VB_THREADS / WAVE];
   __shared__ uint64_t s_tmax;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
@@ -85,8 +84,8 @@ __global__ __launch_bounds__(VB_THREADS) void k_vbuild(ContainArgs a) {
   const int par = (int)a.ds->sort_parity[2];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
-  if ((int64_t)blockIdx.x * CT_TILE >= n) return;  // no tile: stay off the ticket counter
-  const int tile = take_ticket(a.ds, TK_VBUILD, &s_tile);
+  if ((int64_t)blockIdx.x * CT_TILE >= n) return;
+  const int tile = blockIdx.x;
   const int64_t base = (int64_t)tile * CT_TILE;
   // item j of lane covers position base + wv*256 + j*64 + lane
   uint64_t key[VB_ITEMS];

@@ -18,7 +18,7 @@ struct SortBufs {
   int64_t n_max = 0;                    // capacity (host upper bound of the count)
   int64_t tiles_max = 0;
   int nd = 0;                           // 8-bit digits of the key
-  int id = 0;                           // sort index: histogram, parity, tickets
+  int id = 0;                           // sort index: histogram, parity
   int first = 0;                        // first digit sorted by passes (1: digit 0 left to the refine pass)
 };
 

@@ -40,75 +40,107 @@ struct PrepArgs {
   uint32_t* vJ;
 };
 
+// Rows are loaded PREP_BATCH per thread at a time, every column of every row
+// of a batch in flight together: no load waits for another (the correlation
+// id is loaded for every kind, the clock offsets are read from LDS).
+constexpr int PREP_BATCH = 4;
+constexpr int PREP_OFF_LDS = 512;  // processes whose clock offsets are staged in LDS
+
+// Tiles are taken by workgroup index: a tile's look-back waits only for
+// tiles of lower index, whose workgroups the dispatcher started first.
 __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
-  __shared__ int s_tile;
   __shared__ uint64_t s_bal[PREP_ITEMS][PREP_THREADS / WAVE][3];
   __shared__ uint32_t s_off[PREP_ITEMS][PREP_THREADS / WAVE][3];
   __shared__ uint32_t s_tot[3];
   __shared__ uint64_t s_base[3];
   __shared__ unsigned long long s_bad;
   __shared__ unsigned long long s_jr[2 * JT_PROCS];  // per process: max of ~key, max of key
+  __shared__ int64_t s_clk[PREP_OFF_LDS];
 
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
-  const int tile = take_ticket(a.ds, TK_PREP, &s_tile);
+  const int tile = blockIdx.x;
   const int64_t base = (int64_t)tile * PREP_TILE;
+  const bool clk_lds = a.off && a.P <= PREP_OFF_LDS;
   if (tid == 0) s_bad = ~0ull;
   if (tid < 2 * JT_PROCS) s_jr[tid] = 0;
+  if (clk_lds)
+    for (int i = tid; i < a.P; i += PREP_THREADS) s_clk[i] = a.off[i];
+  __syncthreads();
 
   uint64_t kA[PREP_ITEMS], kB[PREP_ITEMS];  // kA: timeline or containment key, kB: join key
   uint32_t fl = 0;                          // per item: bit 3j list K, 3j+1 list C, 3j+2 list J
   uint64_t bad = ~0ull;
   const uint64_t lt = lanemask_lt();
 #pragma unroll
-  for (int j = 0; j < PREP_ITEMS; ++j) {
-    const int64_t r = base + (int64_t)j * PREP_THREADS + tid;
-    bool fK = false, fC = false, fJ = false;
-    kA[j] = 0;
-    kB[j] = 0;
-    if (r < a.n) {
-      const int kind = a.ev.kind[r];
-      const int32_t pid = a.ev.pid[r], lane_ = a.ev.lane[r], name = a.ev.name[r];
-      const int64_t ts = a.ev.ts[r], te = a.ev.te[r];
-      const int64_t corr = kind != HERSCHEL_CPU_OP ? a.ev.corr[r] : 0;
-      constexpr int64_t LIM = HERSCHEL_MAX_ABS_TIME;
-      bool ok = kind <= 2 && pid >= 0 && pid < a.P;
-      if (kind == HERSCHEL_KERNEL)
-        ok = ok && lane_ >= 0 && lane_ < a.S && name >= 0 && name < a.NN;
-      else
-        ok = ok && lane_ >= 0 && lane_ < a.T && name >= 0 && (kind != HERSCHEL_CPU_OP || name < a.NOP);
-      ok = ok && (kind == HERSCHEL_CPU_OP || (corr >= 0 && corr < HERSCHEL_CORR_LIMIT));
-      ok = ok && ts > -LIM && ts < LIM && te > -LIM && te < LIM && te >= ts;
-      bool adm = false;
-      int64_t rel = 0;
-      if (ok) {
-        const int64_t o = a.off ? a.off[pid] : 0;
-        const int64_t tsc = ts - o;
-        adm = tsc >= a.W0 && tsc < a.W1;
-        rel = tsc - a.W0;
-      } else {
-        bad = (uint64_t)r < bad ? (uint64_t)r : bad;
-      }
-      if (!adm) {
-        a.link[r] = -2;
-        a.aux[r] = -2;
-      } else {
-        fK = kind == HERSCHEL_KERNEL;
-        fC = !fK;
-        fJ = kind != HERSCHEL_CPU_OP;
-        if (fK)
-          kA[j] = ((uint64_t)pid << (a.sb + a.wb)) | ((uint64_t)lane_ << a.wb) | (uint64_t)rel;
-        else
-          kA[j] = ((uint64_t)pid << (a.tb + a.wb + 1)) | ((uint64_t)lane_ << (a.wb + 1)) | ((uint64_t)rel << 1) |
-                  (uint64_t)(kind == HERSCHEL_LAUNCH);
-        kB[j] = ((uint64_t)pid << 49) | ((uint64_t)corr << 1) | (uint64_t)(kind == HERSCHEL_KERNEL);
-      }
+  for (int j0 = 0; j0 < PREP_ITEMS; j0 += PREP_BATCH) {
+    // rows past the end load the last row (clamped index) and are ignored
+    int kind_[PREP_BATCH];
+    int32_t pid_[PREP_BATCH], lane_[PREP_BATCH], name_[PREP_BATCH];
+    int64_t ts_[PREP_BATCH], te_[PREP_BATCH], corr_[PREP_BATCH];
+#pragma unroll
+    for (int u = 0; u < PREP_BATCH; ++u) {
+      const int64_t r = base + (int64_t)(j0 + u) * PREP_THREADS + tid;
+      const int64_t rc = r < a.n ? r : a.n - 1;
+      kind_[u] = a.ev.kind[rc];
+      pid_[u] = a.ev.pid[rc];
+      lane_[u] = a.ev.lane[rc];
+      name_[u] = a.ev.name[rc];
+      ts_[u] = a.ev.ts[rc];
+      te_[u] = a.ev.te[rc];
+      corr_[u] = a.ev.corr[rc];
     }
-    fl |= (fK ? 1u : 0u) << (3 * j) | (fC ? 1u : 0u) << (3 * j + 1) | (fJ ? 1u : 0u) << (3 * j + 2);
-    const uint64_t b0 = ballot(fK), b1 = ballot(fC), b2 = ballot(fJ);
-    if (lane == 0) {
-      s_bal[j][wv][0] = b0;
-      s_bal[j][wv][1] = b1;
-      s_bal[j][wv][2] = b2;
+#pragma unroll
+    for (int u = 0; u < PREP_BATCH; ++u) {
+      const int j = j0 + u;
+      const int64_t r = base + (int64_t)j * PREP_THREADS + tid;
+      bool fK = false, fC = false, fJ = false;
+      kA[j] = 0;
+      kB[j] = 0;
+      if (r < a.n) {
+        const int kind = kind_[u];
+        const int32_t pid = pid_[u], ln = lane_[u], name = name_[u];
+        const int64_t ts = ts_[u], te = te_[u];
+        const int64_t corr = kind != HERSCHEL_CPU_OP ? corr_[u] : 0;
+        constexpr int64_t LIM = HERSCHEL_MAX_ABS_TIME;
+        bool ok = kind <= 2 && pid >= 0 && pid < a.P;
+        if (kind == HERSCHEL_KERNEL)
+          ok = ok && ln >= 0 && ln < a.S && name >= 0 && name < a.NN;
+        else
+          ok = ok && ln >= 0 && ln < a.T && name >= 0 && (kind != HERSCHEL_CPU_OP || name < a.NOP);
+        ok = ok && (kind == HERSCHEL_CPU_OP || (corr >= 0 && corr < HERSCHEL_CORR_LIMIT));
+        ok = ok && ts > -LIM && ts < LIM && te > -LIM && te < LIM && te >= ts;
+        bool adm = false;
+        int64_t rel = 0;
+        if (ok) {
+          const int64_t o = !a.off ? 0 : clk_lds ? s_clk[pid] : a.off[pid];
+          const int64_t tsc = ts - o;
+          adm = tsc >= a.W0 && tsc < a.W1;
+          rel = tsc - a.W0;
+        } else {
+          bad = (uint64_t)r < bad ? (uint64_t)r : bad;
+        }
+        if (!adm) {
+          a.link[r] = -2;
+          a.aux[r] = -2;
+        } else {
+          fK = kind == HERSCHEL_KERNEL;
+          fC = !fK;
+          fJ = kind != HERSCHEL_CPU_OP;
+          if (fK)
+            kA[j] = ((uint64_t)pid << (a.sb + a.wb)) | ((uint64_t)ln << a.wb) | (uint64_t)rel;
+          else
+            kA[j] = ((uint64_t)pid << (a.tb + a.wb + 1)) | ((uint64_t)ln << (a.wb + 1)) | ((uint64_t)rel << 1) |
+                    (uint64_t)(kind == HERSCHEL_LAUNCH);
+          kB[j] = ((uint64_t)pid << 49) | ((uint64_t)corr << 1) | (uint64_t)(kind == HERSCHEL_KERNEL);
+        }
+      }
+      fl |= (fK ? 1u : 0u) << (3 * j) | (fC ? 1u : 0u) << (3 * j + 1) | (fJ ? 1u : 0u) << (3 * j + 2);
+      const uint64_t b0 = ballot(fK), b1 = ballot(fC), b2 = ballot(fJ);
+      if (lane == 0) {
+        s_bal[j][wv][0] = b0;
+        s_bal[j][wv][1] = b1;
+        s_bal[j][wv][2] = b2;
+      }
     }
   }
   if (bad != ~0ull) atomicMin(&s_bad, (unsigned long long)bad);
