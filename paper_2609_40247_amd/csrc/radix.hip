@@ -207,7 +207,8 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   const int dgt = tid & 255, slice = tid >> 8;
   const uint32_t b = blockIdx.x;
   // Per sort: the next digit's look-back words of tile index b are cleared
-  // here (the next pass starts only after this one has ended), the first
+  // here (the next pass starts only after this one has ended; the words of
+  // a digit are used by that digit's pass alone), the first
   // pass records which buffer will hold the result (the parity of the
   // digits that move data), and the tiles of a digit on which every key
   // agrees (plan of the histogram kernel) are not sorted at all.
@@ -232,7 +233,8 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
     if (i >= jobs.m) continue;
     const SortJob& jb = jobs.j[i];
     const uint32_t tiles = (nn[i] + RS_TILE - 1) / RS_TILE;
-    if (b < tiles && jb.d + 1 < jb.nd && tid < RS_LB_WORDS)
+    // (only for a next digit that moves data: a skipped digit's words are never read)
+    if (b < tiles && jb.d + 1 < jb.nd && !((tr[i] >> (jb.d + 1)) & 1) && tid < RS_LB_WORDS)
       jb.status1[((int64_t)(jb.d - jb.first) * jb.tiles_max + b) * RS_LB_WORDS + tid] = 0u;
     if (jb.d == jb.first && b == 0 && tid == 0)
       ds->sort_parity[jb.id] = (uint32_t)(popc(~tr[i] & ((jb.nd >= 32 ? 0u : 1u << jb.nd) - 1u)) & 1);
@@ -288,9 +290,14 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   for (int i = tid; i < NW * 256; i += RS_THREADS) (&s_wh[0][0])[i] = 0;
   if (tid < 256) s_cnt[tid] = 0;
   __syncthreads();
-  // an item's digit is re-derived from its key where needed (256: past the end)
+  // The items' digits, four to a register; the thread's first nv items lie
+  // before the end of the input (an item past it has digit 256).
+  uint32_t dpk[RS_ITEMS / 4] = {};
+#pragma unroll
+  for (int j = 0; j < RS_ITEMS; ++j) dpk[j >> 2] |= (uint32_t)((key[j] >> shift) & 255) << (8 * (j & 3));
+  const int nv = wbase < n ? (int)min((n - wbase + WAVE - 1) / WAVE, (uint32_t)RS_ITEMS) : 0;
   auto digit_of = [&](int j) -> int {
-    return wbase + j * WAVE < n ? (int)((key[j] >> shift) & 255) : 256;
+    return j < nv ? (int)__builtin_amdgcn_ubfe(dpk[j >> 2], 8 * (j & 3), 8) : 256;
   };
 
   // The tile's digit counts come first (LDS atomics) and are published
@@ -336,9 +343,13 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   }
   __syncthreads();
 
-  // Threads 0..255 own one digit each: per-wave exclusive offsets.
+  // Threads 0..255 own one digit each: the digit's first tile position
+  // (exclusive sum over digits), then each wave's (plus the exclusive sum
+  // over waves), in the key area.
+  const uint32_t local_excl = block_excl_sum<RS_THREADS>(cnt, s_scan, nullptr);
   if (tid < 256) {
-    uint32_t run = 0;
+    s_local[tid] = local_excl;
+    uint32_t run = local_excl;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
       const uint32_t c = s_wh[w][tid];
@@ -346,17 +357,15 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
       run += c;
     }
   }
-  const uint32_t local_excl = block_excl_sum<RS_THREADS>(cnt, s_scan, nullptr);
-  if (tid < 256) s_local[tid] = local_excl;
   __syncthreads();
 
-  // Tile positions (the per-wave offsets still sit in the key area), then
-  // the tile is reordered in LDS before the rest of the look-back, so that
-  // no key or row stays in a register while the predecessors are polled.
+  // Tile positions, then the tile is reordered in LDS before the rest of
+  // the look-back, so that no key or row stays in a register while the
+  // predecessors are polled.
 #pragma unroll
   for (int j = 0; j < RS_ITEMS; ++j) {
     const int dg = digit_of(j);
-    if (dg < 256) rank[j] += s_local[dg] + s_wh[wv][dg];
+    if (dg < 256) rank[j] += s_wh[wv][dg];
   }
   __syncthreads();
 #pragma unroll
