@@ -63,14 +63,9 @@ size_t layout_workspace(Ctx& c, char* base) {
   sort_plan(c.sK, 0, n, c.pb + c.sb + c.wb, true);
   sort_plan(c.sJ, 1, n, 49 + c.pb, false);  // low bits of dense ids: long runs
   sort_plan(c.sC, 2, n, c.pb + c.tb + c.wb + 1, true);
-  // digit 0's look-back words are cleared here; each later digit's are
-  // cleared by the pass before it
-  c.sK.status0 = b.take<uint32_t>(c.sK.tiles_max * RS_LB_WORDS);
-  c.sJ.status0 = b.take<uint32_t>(c.sJ.tiles_max * RS_LB_WORDS);
   if (c.contain) {
     c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
     c.vb_status = b.take<uint64_t>(c.vb_tiles);
-    c.sC.status0 = b.take<uint32_t>(c.sC.tiles_max * RS_LB_WORDS);
     // pyramid levels above the tile maxima: built by atomic maxima, from zero
     c.nlev = 3;
     while (cdiv(n, (int64_t)1 << (6 * (c.nlev - 1))) > 64) ++c.nlev;
@@ -80,6 +75,11 @@ size_t layout_workspace(Ctx& c, char* base) {
     }
   }
   c.zero_bytes = align_up(b.off - z0);
+  // the first digit's look-back words are cleared by the histogram kernel
+  // (for the tiles of the call), each later digit's by the pass before it
+  c.sK.status0 = b.take<uint32_t>(c.sK.tiles_max * RS_LB_WORDS);
+  c.sJ.status0 = b.take<uint32_t>(c.sJ.tiles_max * RS_LB_WORDS);
+  if (c.contain) c.sC.status0 = b.take<uint32_t>(c.sC.tiles_max * RS_LB_WORDS);
   for (SortBufs* s : {&c.sK, &c.sJ, &c.sC})
     if (s != &c.sC || c.contain) s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * RS_LB_WORDS);
   // long runs of the refine pass (each has more than RF_SHORT keys)
@@ -352,7 +352,7 @@ static inline void stage_end(Ctx& c, int s) {
 struct DeviceStreams {
   hipStream_t s[2] = {nullptr, nullptr};
   hipStream_t cap = nullptr;  // graphs are captured here (the caller's stream may be the null stream)
-  hipEvent_t e[4] = {};  // sorts, timeline chain, join, launches' ops
+  hipEvent_t e[5] = {};  // sorts, timeline chain, join, launches' ops, name tables
   bool ok = false;
 };
 static std::mutex g_enqueue_mutex;
@@ -446,9 +446,16 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   launch_edges(c);
   stage_end(c, HERSCHEL_STAGE_EDGES);
   (void)hipEventRecord(dsx->e[2], c.st);
+  // the name pass also gives each kernel its launch's op: after the join
+  // and after the launches' ops are known
+  if (c.contain) (void)hipStreamWaitEvent(c.st, dsx->e[3], 0);
+  stage_begin(c, HERSCHEL_STAGE_NAMES);
+  launch_names(c);
+  launch_names_reduce(c);
+  stage_end(c, HERSCHEL_STAGE_NAMES);
+  (void)hipEventRecord(dsx->e[4], c.st);
 
-  // chain 1: timeline and overlap, then the per-name tables (enqueued after
-  // the events it waits for have been recorded)
+  // chain 1: timeline and overlap
   c.st = lib0;
   (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
   stage_begin(c, HERSCHEL_STAGE_TIMELINE);
@@ -457,14 +464,6 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_OVERLAP);
   if (c.overlap) launch_overlap(c);
   stage_end(c, HERSCHEL_STAGE_OVERLAP);
-  // the name pass also gives each kernel its launch's op: after the join
-  // and after the launches' ops are known
-  if (c.contain) (void)hipStreamWaitEvent(c.st, dsx->e[3], 0);
-  (void)hipStreamWaitEvent(c.st, dsx->e[2], 0);
-  stage_begin(c, HERSCHEL_STAGE_NAMES);
-  launch_names(c);
-  launch_names_reduce(c);
-  stage_end(c, HERSCHEL_STAGE_NAMES);
   (void)hipEventRecord(dsx->e[1], c.st);
 
   // back on the caller's stream: what needs both containment and the join
@@ -474,6 +473,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   if (c.contain) launch_opagg(c);
   stage_end(c, HERSCHEL_STAGE_OPAGG);
   (void)hipStreamWaitEvent(c.st, dsx->e[1], 0);
+  (void)hipStreamWaitEvent(c.st, dsx->e[4], 0);
   stage_begin(c, HERSCHEL_STAGE_FINAL);
   launch_finalize(c);
   stage_end(c, HERSCHEL_STAGE_FINAL);

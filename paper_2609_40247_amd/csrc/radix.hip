@@ -20,6 +20,7 @@ constexpr uint32_t RS_VAL = (1u << 30) - 1;
 struct HistJob {
   const uint64_t* keys;
   const int32_t* count;
+  uint32_t* status0;  // the first digit pass's look-back words, cleared here
   int nd;
   int id;
   int first;  // 1: digit 0 is left to the refine pass
@@ -88,6 +89,14 @@ __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, cons
   const int nd = jb.nd, nbins = nd * 256;
   __shared__ uint32_t h[8 * 256];
   const int64_t n = *jb.count;
+  // the first digit pass's look-back words of this call's tiles (the passes
+  // follow on the same stream)
+  {
+    const int64_t words = cdiv(n, (int64_t)RS_TILE) * RS_LB_WORDS / 4;
+    uint4* st = reinterpret_cast<uint4*>(jb.status0);
+    for (int64_t w = (int64_t)blockIdx.x * HIST_THREADS + threadIdx.x; w < words; w += (int64_t)gridDim.x * HIST_THREADS)
+      st[w] = make_uint4(0u, 0u, 0u, 0u);
+  }
   const int nblk = hist_blocks(n);
   const int blk = blockIdx.x;
   if (blk >= nblk) return;
@@ -489,7 +498,7 @@ void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
   int64_t n_max = 1;
   for (int i = 0; i < k; ++i) {
     if (s[i]->nd == 0) continue;
-    jobs.j[m++] = HistJob{s[i]->k[0], count[i], s[i]->nd, s[i]->id, s[i]->first};
+    jobs.j[m++] = HistJob{s[i]->k[0], count[i], s[i]->status0, s[i]->nd, s[i]->id, s[i]->first};
     n_max = std::max<int64_t>(n_max, s[i]->n_max);
     nd = std::max(nd, s[i]->nd);
   }

@@ -177,6 +177,40 @@ def test_deep_nesting(H):
     assert g["aux"][D - 1] == D - 1
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_bursty_streams_overlap(H, seed):
+    """Streams of very different density over a large window: one with all
+    its kernels packed into 40 us at the window's end (a leading gap spanning
+    most of its buckets, and buckets holding hundreds of events), one spread
+    evenly, one with a single kernel, one with none, one with clusters in the
+    middle; two processes, classes over the streams, gaps and overlap."""
+    rng = np.random.default_rng(700 + seed)
+    W = 50_000_000
+    rows = []
+    corr = 0
+
+    def kern(pid, s, t, d):
+        nonlocal corr
+        rows.append((2, pid, s, int(t), int(t + d), corr, corr % 4))
+        corr += 1
+
+    for pid in range(2):
+        t = W - 40_000 + rng.integers(0, 5, 4000).cumsum()            # stream 0: packed at the end
+        for x in t:
+            kern(pid, 0, x, rng.integers(1, 30))
+        for x in np.sort(rng.integers(0, W - 100, 3000)):               # stream 1: spread
+            kern(pid, 1, x, rng.integers(1, 20_000))
+        kern(pid, 2, W // 3 + pid, 5_000_000)                            # stream 3: nothing
+        for c0 in (W // 4, W // 2 + 17):                                 # streams 4, 5: clusters
+            for x in c0 + rng.integers(0, 300_000, 1500):
+                kern(pid, 4, x, rng.integers(1, 2_000))
+                kern(pid, 5, x + rng.integers(0, 50), rng.integers(1, 500))
+    perm = rng.permutation(len(rows))
+    rows = [rows[i] for i in perm]
+    cols, p = _rows(rows, P=2, S=6, W=W, thr=1_000, cls=np.array([0, 1, 2, 0, 1, 2], np.uint8))
+    check(H, cols, p, f"bursty streams seed{seed}")
+
+
 def test_64_streams_overlap(H):
     tr = synth.random_small(seed=77, n_rows=6000, window=20_000, n_procs=2, n_streams=64, n_threads=2,
                             corr_range=3000)
