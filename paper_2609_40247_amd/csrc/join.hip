@@ -291,7 +291,7 @@ __global__ __launch_bounds__(256) void k_jt_store(JoinArgs a) {
 
 // Pass 2: a launch that lost its slot is a duplicate; a kernel that lost its
 // owner word marks the slot as holding several kernels.  Launches start with
-// no kernels.
+// no kernels (their kernel aggregates are read only when they have some).
 __global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
   __shared__ unsigned long long s_c[JC_N];
   const int tid = threadIdx.x;
@@ -328,17 +328,15 @@ __global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
     } else {
       if (w[u] != row[u]) ++c[JC_DUP];
       a.aux[row[u]] = 0;
-      if (a.contain) {
-        a.lk_first[row[u]] = I64MAX;
-        a.lk_last[row[u]] = I64MIN;
-        a.lk_sum[row[u]] = 0;
-      }
     }
   }
   jt_flush(a, c, s_c, nullptr);
 }
 
-// Pass 3: duplicates put the smallest row into their slot (rare: atomics).
+// Pass 3: duplicates put the smallest row into their slot (rare: atomics),
+// and the launches of slots with several kernels start their kernel
+// aggregates at the identities (the kernels add to them with atomics; a
+// launch with one kernel gets plain stores).
 __global__ __launch_bounds__(256) void k_jt_fix(JoinArgs a) {
   if (!a.ds->join_direct) return;
   const int64_t n = a.ds->nJ;
@@ -357,7 +355,15 @@ __global__ __launch_bounds__(256) void k_jt_fix(JoinArgs a) {
   for (int u = 0; u < JT_ITEMS; ++u) {
     if (key[u] & 1) continue;
     const int64_t slot = jt_slot(a.ds, key[u]);
-    if (in_range(a.ds, slot, a.cap) && a.tab[slot] != row[u]) atomicMin(&a.tab[slot], row[u]);
+    if (!in_range(a.ds, slot, a.cap)) continue;
+    const uint32_t t = a.tab[slot];
+    const uint8_t mu = a.multi[slot];
+    if (t != row[u]) atomicMin(&a.tab[slot], row[u]);
+    if (a.contain && mu) {
+      a.lk_first[row[u]] = I64MAX;
+      a.lk_last[row[u]] = I64MIN;
+      a.lk_sum[row[u]] = 0;
+    }
   }
 }
 
