@@ -442,24 +442,35 @@ __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
   for (int u = 0; u < DP_ITEMS; ++u) {
     if (row[u] == ~0u) continue;
     a.aux[row[u]] = d[u];
-    a.op_nkern[row[u]] = 0;
-    a.op_first[row[u]] = I64MAX;
-    a.op_last[row[u]] = I64MIN;
-    a.op_ksum[row[u]] = 0;
   }
   // The ops open at the start of aggregate tile b: the chain of answers from
-  // the position before it (that position first, if it is an op).
+  // the position before it (that position first, if it is an op).  They, and
+  // the ops open at the end of the last tile, are the only ops whose
+  // aggregates are summed with atomics (the others are stored whole by the
+  // aggregate pass): their aggregates start here at the identities.
   const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (b < cdiv(n, AG_TILE)) {
+  const int64_t ntl = cdiv(n, AG_TILE);
+  auto init_op = [&](int64_t q) {
+    const uint32_t rr = vals[q];
+    a.op_nkern[rr] = 0;
+    a.op_first[rr] = I64MAX;
+    a.op_last[rr] = I64MIN;
+    a.op_ksum[rr] = 0;
+  };
+  if (b < ntl) {
     int nc = 0;
     if (b > 0) {
       const int64_t pe = b * AG_TILE - 1;
       for (int64_t q = key_is_op(keys[pe]) ? pe : a.par[pe]; q >= 0 && in_range(a.ds, q, n); q = a.par[q]) {
         if (nc < AG_CHAIN) a.ag_chain[b * AG_CHAIN + nc] = (int32_t)q;
         ++nc;
+        init_op(q);
       }
     }
     a.ag_nchain[b] = nc;
+  } else if (b == ntl) {
+    const int64_t pe = n - 1;
+    for (int64_t q = key_is_op(keys[pe]) ? pe : a.par[pe]; q >= 0 && in_range(a.ds, q, n); q = a.par[q]) init_op(q);
   }
   const uint64_t w = wave_sum_u64(imp);
   if (lane_id() == 0 && w) atomicAdd(&s_imp, (unsigned long long)w);
@@ -530,17 +541,19 @@ __global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
   const int32_t chv = tid < AG_CHAIN ? a.ag_chain[(int64_t)blockIdx.x * AG_CHAIN + tid] : -1;
   const int32_t ncv = a.ag_nchain[blockIdx.x];
   // round 2: an op's depth or a launch's kernel count (both in aux), and a
-  // launch's kernel aggregates (loaded for every row: the arrays span all
-  // rows, and one round of loads is shorter than two)
+  // launch's kernel aggregates (one round of loads: an op reads the
+  // aggregates of row 0 instead of branching around the loads, so that its
+  // reads hit one cached line and the loads need no wait of their own)
   int32_t av[AG_ITEMS];
   int64_t lf[AG_ITEMS], ll[AG_ITEMS];
   uint64_t ls[AG_ITEMS];
 #pragma unroll
   for (int u = 0; u < AG_ITEMS; ++u) {
+    const uint32_t lr = key_is_op(key[u]) ? 0u : row[u];
     av[u] = a.aux[row[u]];
-    lf[u] = a.lk_first[row[u]];
-    ll[u] = a.lk_last[row[u]];
-    ls[u] = (uint64_t)a.lk_sum[row[u]];
+    lf[u] = a.lk_first[lr];
+    ll[u] = a.lk_last[lr];
+    ls[u] = (uint64_t)a.lk_sum[lr];
   }
   int dmin = INT32_MAX, dmax = -1;
 #pragma unroll
