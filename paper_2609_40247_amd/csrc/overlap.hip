@@ -81,27 +81,34 @@ __device__ __attribute__((always_inline)) inline void add_interval(const SweepAr
   }
 }
 
-// First event of every (pid, stream) group, by binary search over the group
-// order of the events; entry P * S is the event count.
+// First event of every (pid, stream) group; entry P * S is the event count.
+// One wave per group boundary searches the events 64-ary: each round every
+// lane tests one point of the remaining stretch and a ballot keeps the part
+// where the boundary lies (four rounds for a million events).
 __global__ __launch_bounds__(256) void k_segoff(SweepArgs a) {
   const int32_t n = a.ds->nEv;
   const int nseg = a.P * a.S;
   const int pshift = a.wb1 + a.sb;
   const uint64_t smask = (1ull << a.sb) - 1;
-  for (int g = blockIdx.x * 256 + threadIdx.x; g <= nseg; g += gridDim.x * 256) {
-    int32_t lo = 0, len = n;
-    while (len > 0) {
-      const int32_t half = len >> 1;
-      const uint64_t k = a.ev[lo + half];
-      const int sg = (int)(k >> pshift) * a.S + (int)(k & smask);
-      if (sg < g) {
-        lo += half + 1;
-        len -= half + 1;
-      } else {
-        len = half;
+  const int lane = lane_id();
+  const int waves = gridDim.x * (256 / WAVE);
+  for (int g = blockIdx.x * (256 / WAVE) + threadIdx.x / WAVE; g <= nseg; g += waves) {
+    int32_t lo = 0, hi = n;  // the first event of group >= g lies in [lo, hi]
+    while (lo < hi) {
+      const int32_t step = (hi - lo + WAVE - 1) / WAVE;
+      const int32_t x = lo + lane * step;
+      bool below = false;
+      if (x < hi) {
+        const uint64_t k = a.ev[x];
+        below = (int)(k >> pshift) * a.S + (int)(k & smask) < g;
       }
+      const int c = popc(ballot(below));  // lanes 0..c-1 test points below the boundary
+      const int32_t nlo = c > 0 ? lo + (c - 1) * step + 1 : lo;
+      const int32_t xc = lo + c * step;
+      hi = xc < hi ? xc : hi;
+      lo = nlo;
     }
-    a.seg_off[g] = lo;
+    if (lane == 0) a.seg_off[g] = lo;
   }
 }
 
@@ -503,7 +510,7 @@ void launch_overlap(Ctx& c) {
   a.corank = c.corank;
   a.ev_cap = c.ev_cap;
   const int64_t nseg = (int64_t)c.P * c.S + 1;
-  hipLaunchKernelGGL(k_segoff, dim3((unsigned)std::min<int64_t>(cdiv(nseg, 256), 1024)), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_segoff, dim3((unsigned)std::min<int64_t>(cdiv(nseg, 256 / WAVE), 1024)), dim3(256), 0, c.st, a);
   const dim3 grid((unsigned)std::max<int64_t>(cdiv(c.ev_cap, SW_TILE), 1));
   if (c.S > 1 && c.S <= CR_SMAX) {
     const int64_t steps = (int64_t)(c.S - 1) * c.ev_cap;
