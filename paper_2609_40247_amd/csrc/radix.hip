@@ -48,8 +48,10 @@ struct HistJobs {
 constexpr int HIST_THREADS = 512;
 constexpr int HIST_U = 16;
 
+// Digits below `first` (left to the refine pass) are not counted.
 template <int ND>
-__device__ __forceinline__ void hist_range(uint32_t* h, const uint64_t* __restrict__ keys, int64_t lo, int64_t hi) {
+__device__ __forceinline__ void hist_range(uint32_t* h, const uint64_t* __restrict__ keys, int64_t lo, int64_t hi,
+                                           int first) {
   for (int64_t i0 = lo + (int64_t)threadIdx.x * HIST_U; i0 < hi; i0 += (int64_t)HIST_U * HIST_THREADS) {
     // clamped, not branched on: every load of the round is in flight together
     uint64_t k[HIST_U];
@@ -59,6 +61,7 @@ __device__ __forceinline__ void hist_range(uint32_t* h, const uint64_t* __restri
 #pragma unroll
     for (int d = 0; d < ND; ++d) {
       const int sh = 8 * d;
+      if (d < first) continue;
       if (d < 2) {
 #pragma unroll
         for (int u = 0; u < HIST_U; ++u)
@@ -105,14 +108,14 @@ __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, cons
   const int64_t per = cdiv(n, nblk);
   const int64_t lo = min<int64_t>(n, (int64_t)blk * per), hi = min<int64_t>(n, lo + per);
   switch (nd) {
-    case 1: hist_range<1>(h, jb.keys, lo, hi); break;
-    case 2: hist_range<2>(h, jb.keys, lo, hi); break;
-    case 3: hist_range<3>(h, jb.keys, lo, hi); break;
-    case 4: hist_range<4>(h, jb.keys, lo, hi); break;
-    case 5: hist_range<5>(h, jb.keys, lo, hi); break;
-    case 6: hist_range<6>(h, jb.keys, lo, hi); break;
-    case 7: hist_range<7>(h, jb.keys, lo, hi); break;
-    default: hist_range<8>(h, jb.keys, lo, hi); break;
+    case 1: hist_range<1>(h, jb.keys, lo, hi, jb.first); break;
+    case 2: hist_range<2>(h, jb.keys, lo, hi, jb.first); break;
+    case 3: hist_range<3>(h, jb.keys, lo, hi, jb.first); break;
+    case 4: hist_range<4>(h, jb.keys, lo, hi, jb.first); break;
+    case 5: hist_range<5>(h, jb.keys, lo, hi, jb.first); break;
+    case 6: hist_range<6>(h, jb.keys, lo, hi, jb.first); break;
+    case 7: hist_range<7>(h, jb.keys, lo, hi, jb.first); break;
+    default: hist_range<8>(h, jb.keys, lo, hi, jb.first); break;
   }
   __syncthreads();
   uint32_t* part = jobs.part + ((int64_t)jb.id * HIST_MAX_BLOCKS + blk) * 8 * 256;
