@@ -63,10 +63,12 @@ __device__ __forceinline__ void put_gap(const UnionArgs& a, int64_t pos, int32_t
   }
 }
 
-__device__ __forceinline__ void put_event(const UnionArgs& a, int64_t pos, int32_t seg, int64_t t) {
-  if (in_range(a.ds, pos, a.ev_cap)) {
+// Events are staged in LDS at their position within the tile (the tile
+// then writes them out whole, coalesced).
+__device__ __forceinline__ void put_event(const UnionArgs& a, uint64_t* s_ev, int64_t pos, int32_t seg, int64_t t) {
+  if (in_range(a.ds, pos, 2 * UN_TILE)) {
     const uint64_t pid = (uint64_t)(seg / a.S), stream = (uint64_t)(seg % a.S);
-    a.ev_keys[pos] = (pid << (a.wb1 + a.sb)) | ((uint64_t)t << a.sb) | stream;
+    s_ev[pos] = (pid << (a.wb1 + a.sb)) | ((uint64_t)t << a.sb) | stream;
   }
 }
 
@@ -75,7 +77,7 @@ __device__ __forceinline__ void put_event(const UnionArgs& a, int64_t pos, int32
 template <int MODE>
 __device__ __forceinline__ void walk(const UnionArgs& a, const Elem* x, int nv, int32_t prev_seg, int32_t next_seg, uint64_t m_in,
                      int64_t i0, int64_t nK, uint32_t* ngap, uint32_t* nev, int64_t gbase, int64_t ebase,
-                     int64_t* s_busy, int32_t seg0) {
+                     int64_t* s_busy, int32_t seg0, uint64_t* s_ev) {
   const int nseg = a.P * a.S;
   const bool full_gap = a.W > a.thr;
   uint64_t m = m_in;  // 0 none, else (max covered end) + 1
@@ -105,10 +107,10 @@ __device__ __forceinline__ void walk(const UnionArgs& a, const Elem* x, int nv, 
       }
       if (a.overlap && (m == 0 || q.s > C)) {
         if (m != 0) {
-          if (MODE == 1) put_event(a, ebase + v, q.seg, C);
+          if (MODE == 1) put_event(a, s_ev, ebase + v, q.seg, C);
           ++v;
         }
-        if (MODE == 1) put_event(a, ebase + v, q.seg, q.s);
+        if (MODE == 1) put_event(a, s_ev, ebase + v, q.seg, q.s);
         ++v;
       }
       if (MODE == 0) {
@@ -136,7 +138,7 @@ __device__ __forceinline__ void walk(const UnionArgs& a, const Elem* x, int nv, 
         ++g;
       }
       if (a.overlap && m != 0) {
-        if (MODE == 1) put_event(a, ebase + v, q.seg, Cl);
+        if (MODE == 1) put_event(a, s_ev, ebase + v, q.seg, Cl);
         ++v;
       }
       if (i0 + j == nK - 1) {
@@ -168,6 +170,7 @@ __global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
   __shared__ uint32_t s_scan[UN_THREADS / WAVE + 1];
   __shared__ uint32_t s_tot[2];
   __shared__ uint64_t s_base[2];
+  __shared__ uint64_t s_ev[2 * UN_TILE];  // the tile's coverage-run endpoints, in order
 
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int64_t nK = a.ds->nK;
@@ -333,7 +336,7 @@ __global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
   const uint64_t m_in = (has && pre_has && (int32_t)OpSegMax::seg(pre) == x[0].seg) ? OpSegMax::m(pre) : 0;
 
   uint32_t ngap = 0, nev = 0;
-  if (has) walk<0>(a, x, nv, prev_seg, next_seg, m_in, i0, nK, &ngap, &nev, 0, 0, s_busy, s_seg0);
+  if (has) walk<0>(a, x, nv, prev_seg, next_seg, m_in, i0, nK, &ngap, &nev, 0, 0, s_busy, s_seg0, s_ev);
   uint32_t gtot, etot;
   const uint32_t gex = block_excl_sum<UN_THREADS>(ngap, s_scan, &gtot);
   const uint32_t eex = block_excl_sum<UN_THREADS>(nev, s_scan, &etot);
@@ -356,9 +359,14 @@ __global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
   }
   if (has && (ngap || nev)) {
     uint32_t g2, e2;
-    walk<1>(a, x, nv, prev_seg, next_seg, m_in, i0, nK, &g2, &e2, (int64_t)s_base[0] + gex, (int64_t)s_base[1] + eex,
-            s_busy, s_seg0);
+    walk<1>(a, x, nv, prev_seg, next_seg, m_in, i0, nK, &g2, &e2, (int64_t)s_base[0] + gex, (int64_t)eex, s_busy, s_seg0,
+            s_ev);
   }
+  __syncthreads();
+  const uint32_t ne = s_tot[1];
+  const int64_t eb = (int64_t)s_base[1];
+  for (uint32_t i = tid; i < ne; i += UN_THREADS)
+    if (in_range(a.ds, eb + i, a.ev_cap)) a.ev_keys[eb + i] = s_ev[i];
 }
 
 void launch_timeline(Ctx& c) {
