@@ -317,8 +317,9 @@ __global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
     slot[u] = key[u] != ~0ull ? jt_slot(a.ds, key[u]) : -1;
     const bool ok = slot[u] >= 0 && in_range(a.ds, slot[u], a.cap);
     const int64_t sc = ok ? slot[u] : 0;
-    const uint32_t wo = a.own[sc], wt = a.tab[sc];
-    w[u] = !ok ? row[u] : (key[u] & 1) ? wo : wt;
+    // one load: the owner word for a kernel, the slot for a launch
+    const uint32_t ws = ((key[u] & 1) ? a.own : a.tab)[sc];
+    w[u] = !ok ? row[u] : ws;
   }
 #pragma unroll
   for (int u = 0; u < JT_ITEMS; ++u) {
