@@ -52,7 +52,7 @@ enum {
   HERSCHEL_EINVAL = -1,     /* a required pointer is NULL or a parameter is out of range */
   HERSCHEL_EEVENT = -2,     /* an input row is invalid; counters->first_invalid = smallest such row */
   HERSCHEL_ECAPACITY = -3,  /* more gaps than gap_capacity; the first gap_capacity are written */
-  HERSCHEL_EWORKSPACE = -4, /* workspace is NULL or smaller than herschel_workspace_size() */
+  HERSCHEL_EWORKSPACE = -4, /* workspace is NULL, not 256-byte aligned, or smaller than herschel_workspace_size() */
   HERSCHEL_EDEVICE = -5     /* a HIP call failed or a device-side consistency check tripped */
 };
 
@@ -107,7 +107,7 @@ typedef struct {
   int64_t n_edges;
   uint32_t flags;               /* HERSCHEL_OUT_* */
   void *hip_stream;             /* hipStream_t to enqueue on; NULL = the null stream */
-  void *workspace;              /* device scratch owned by the caller */
+  void *workspace;              /* device scratch owned by the caller, 256-byte aligned (hipMalloc's are) */
   size_t workspace_bytes;
 } herschel_params;
 

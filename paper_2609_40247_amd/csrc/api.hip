@@ -614,7 +614,7 @@ const char* herschel_strerror(int code) {
     case HERSCHEL_EINVAL: return "invalid argument";
     case HERSCHEL_EEVENT: return "invalid input row (see counters.first_invalid)";
     case HERSCHEL_ECAPACITY: return "gap list capacity exceeded (see counters.n_gaps_total)";
-    case HERSCHEL_EWORKSPACE: return "workspace missing or too small";
+    case HERSCHEL_EWORKSPACE: return "workspace missing, misaligned or too small";
     case HERSCHEL_EDEVICE: return "device error";
     default: return "unknown error";
   }
@@ -683,7 +683,8 @@ static int prepare(Ctx& c, const herschel_events* ev, int64_t n, const herschel_
   int code = check_and_plan(c, ev, n, p, out);
   if (code) return code;
   const size_t need = layout_workspace(c, nullptr);
-  if (!ws || ws_bytes < need) return HERSCHEL_EWORKSPACE;
+  // the layout aligns every buffer to 256 bytes from the base (16-byte loads)
+  if (!ws || ((uintptr_t)ws & 255) != 0 || ws_bytes < need) return HERSCHEL_EWORKSPACE;
   layout_workspace(c, (char*)ws);
   return HERSCHEL_OK;
 }

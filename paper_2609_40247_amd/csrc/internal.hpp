@@ -104,7 +104,7 @@ int64_t union_tile_elems();
 void names_set_lds_attr();
 
 // digit histograms: keys per workgroup (at least), most workgroups per sort
-constexpr int HIST_CHUNK = 8192;
+constexpr int HIST_CHUNK = 4096;
 constexpr int HIST_MAX_BLOCKS = 256;
 
 // per-op aggregates: positions per workgroup, open ops kept per tile start

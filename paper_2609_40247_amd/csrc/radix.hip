@@ -38,123 +38,220 @@ struct HistJobs {
 // The grid is sized so that every CU holds a share (HIST_CHUNK keys at
 // least per workgroup, HIST_MAX_BLOCKS at most per sort).
 //
-// Each thread takes HIST_U consecutive keys per round.  Digits 0 and 1 of
-// these keys (nanoseconds, correlation ids) differ from key to key: every
-// key adds one to its bin.  Higher digits change rarely between neighbouring
-// records, and lanes adding to one LDS word are served one after another:
-// a thread adds each run of equal digits once, with the run's length.
-// Everything is vector code: the CU's one scalar unit would otherwise be
-// shared by all of its waves.
+// A round takes HIST_ROUND keys: the workgroup loads them coalesced (16
+// bytes a lane) into LDS, then each thread reads back HIST_U consecutive
+// keys (one row, padded so that the 16-byte reads of a wave meet distinct
+// banks).  The next round's loads are in flight while a round is counted.
 constexpr int HIST_THREADS = 512;
-constexpr int HIST_U = 16;
+constexpr int HIST_U = 8;                           // consecutive keys per thread and round
+constexpr int HIST_ROUND = HIST_THREADS * HIST_U;  // keys per round
+constexpr int HIST_ROW = HIST_U + 2;                // u64 words per thread row (16 bytes of padding)
 
-// Digits below `first` (left to the refine pass) are not counted.
+// Counts one thread's keys.  Digits below `first` (left to the refine pass)
+// are not counted.
+//
+// A full wave (every lane holds HIST_U valid keys, the usual case) runs
+// without branches per key.  Digits 0 and 1 (nanoseconds, correlation ids)
+// differ from key to key: every key adds one to its bin.  A higher digit
+// that all of the wave's keys share is added once for the wave (the 64
+// lanes would otherwise add to one LDS word one after another); otherwise
+// each lane adds each run of equal digits once, at its last key, and the
+// other keys add to a word of the lane's own (s_spare), which costs an LDS
+// access but neither a conflict nor a branch.
+//
+// A partial wave (the end of the range; nv valid keys, 0 past the end)
+// takes the same counts with a branch per key.
 template <int ND>
-__device__ __forceinline__ void hist_range(uint32_t* h, const uint64_t* __restrict__ keys, int64_t lo, int64_t hi,
-                                           int first) {
-  for (int64_t i0 = lo + (int64_t)threadIdx.x * HIST_U; i0 < hi; i0 += (int64_t)HIST_U * HIST_THREADS) {
-    // clamped, not branched on: every load of the round is in flight together
-    uint64_t k[HIST_U];
+__device__ __forceinline__ void hist_count(uint32_t* h, uint32_t* s_spare, const uint64_t* k, int nv, int first,
+                                           bool full) {
+  const int lane = threadIdx.x & (WAVE - 1);
+  if (full) {
+    // bits that differ between any two keys of the wave
+    const uint32_t f_lo = __builtin_amdgcn_readfirstlane((uint32_t)k[0]);
+    const uint32_t f_hi = __builtin_amdgcn_readfirstlane((uint32_t)(k[0] >> 32));
+    uint64_t x = k[0] ^ (((uint64_t)f_hi << 32) | f_lo);
 #pragma unroll
-    for (int u = 0; u < HIST_U; ++u) k[u] = keys[min(i0 + u, hi - 1)];
-    const int nv = (int)min<int64_t>(HIST_U, hi - i0);  // valid keys of this thread
+    for (int u = 1; u < HIST_U; ++u) x |= k[u] ^ k[0];
 #pragma unroll
     for (int d = 0; d < ND; ++d) {
       const int sh = 8 * d;
       if (d < first) continue;
       if (d < 2) {
 #pragma unroll
-        for (int u = 0; u < HIST_U; ++u)
-          if (u < nv) atomicAdd(&h[d * 256 + (uint32_t)((k[u] >> sh) & 255)], 1u);
+        for (int u = 0; u < HIST_U; ++u) atomicAdd(&h[d * 256 + (uint32_t)((k[u] >> sh) & 255)], 1u);
+      } else if (!__any((uint32_t)((x >> sh) & 255) != 0)) {
+        if (lane == 0) atomicAdd(&h[d * 256 + (uint32_t)((k[0] >> sh) & 255)], (uint32_t)(WAVE * HIST_U));
       } else {
-        uint32_t cur = (uint32_t)((k[0] >> sh) & 255), run = 1;
+        uint32_t run = 1, v = (uint32_t)((k[0] >> sh) & 255);
 #pragma unroll
-        for (int u = 1; u < HIST_U; ++u) {
-          const uint32_t v = (uint32_t)((k[u] >> sh) & 255);
-          if (u < nv) {
-            if (v != cur) {
-              atomicAdd(&h[d * 256 + cur], run);
-              cur = v;
-              run = 0;
-            }
-            ++run;
-          }
+        for (int u = 0; u < HIST_U; ++u) {
+          const uint32_t nx = u + 1 < HIST_U ? (uint32_t)((k[u + 1] >> sh) & 255) : 256u;
+          const bool end = nx != v;
+          atomicAdd(end ? &h[d * 256 + v] : &s_spare[lane], run);
+          run = end ? 1u : run + 1u;
+          v = nx;
         }
-        atomicAdd(&h[d * 256 + cur], run);
       }
+    }
+    return;
+  }
+#pragma unroll
+  for (int d = 0; d < ND; ++d) {
+    const int sh = 8 * d;
+    if (d < first) continue;
+    if (d < 2) {
+#pragma unroll
+      for (int u = 0; u < HIST_U; ++u)
+        if (u < nv) atomicAdd(&h[d * 256 + (uint32_t)((k[u] >> sh) & 255)], 1u);
+    } else {
+      uint32_t cur = (uint32_t)((k[0] >> sh) & 255), run = 1;
+#pragma unroll
+      for (int u = 1; u < HIST_U; ++u) {
+        const uint32_t v = (uint32_t)((k[u] >> sh) & 255);
+        if (u < nv) {
+          if (v != cur) {
+            atomicAdd(&h[d * 256 + cur], run);
+            cur = v;
+            run = 0;
+          }
+          ++run;
+        }
+      }
+      if (nv > 0) atomicAdd(&h[d * 256 + cur], run);
     }
   }
 }
 
+// Round loads: pair q of the round starting at r0 is keys r0 + 2q and
+// r0 + 2q + 1 (16-byte loads; r0 is even).
+__device__ __forceinline__ void hist_load(uint4* v, const uint64_t* __restrict__ keys, int64_t r0, int64_t hi) {
+#pragma unroll
+  for (int i = 0; i < HIST_U / 2; ++i) {
+    const int64_t g = r0 + 2 * (int64_t)(i * HIST_THREADS + threadIdx.x);
+    v[i] = make_uint4(0u, 0u, 0u, 0u);
+    if (g + 1 < hi) {
+      v[i] = *reinterpret_cast<const uint4*>(keys + g);
+    } else if (g < hi) {
+      const uint64_t x = keys[g];
+      v[i].x = (uint32_t)x;
+      v[i].y = (uint32_t)(x >> 32);
+    }
+  }
+}
+
+// The next round's loads are in flight while a round is counted.
+template <int ND>
+__device__ __forceinline__ void hist_range(uint32_t* h, uint32_t* s_spare, uint64_t* s_row, const uint64_t* __restrict__ keys,
+                                           int64_t lo, int64_t hi, int first) {
+  const int t = threadIdx.x;
+  uint4 v[HIST_U / 2];
+  hist_load(v, keys, lo, hi);
+  for (int64_t r0 = lo; r0 < hi; r0 += HIST_ROUND) {
+    // pair q goes to row q / (HIST_U / 2)
+#pragma unroll
+    for (int i = 0; i < HIST_U / 2; ++i) {
+      const int q = i * HIST_THREADS + t;
+      *reinterpret_cast<uint4*>(s_row + (q / (HIST_U / 2)) * HIST_ROW + 2 * (q % (HIST_U / 2))) = v[i];
+    }
+    __syncthreads();
+    uint64_t k[HIST_U];
+#pragma unroll
+    for (int i = 0; i < HIST_U / 2; ++i) {
+      const uint4 w = *reinterpret_cast<const uint4*>(s_row + t * HIST_ROW + 2 * i);
+      k[2 * i] = (uint64_t)w.x | ((uint64_t)w.y << 32);
+      k[2 * i + 1] = (uint64_t)w.z | ((uint64_t)w.w << 32);
+    }
+    if (r0 + HIST_ROUND < hi) hist_load(v, keys, r0 + HIST_ROUND, hi);
+    const int nv = (int)max<int64_t>(0, min<int64_t>(HIST_U, hi - (r0 + (int64_t)t * HIST_U)));
+    const int wv = __builtin_amdgcn_readfirstlane(t / WAVE);
+    const bool full = r0 + (int64_t)(wv + 1) * WAVE * HIST_U <= hi;  // the wave's keys are all valid
+    hist_count<ND>(h, s_spare, k, nv, first, full);
+    __syncthreads();  // the rows are rewritten by the next round
+  }
+}
+
 __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, const DevState* ds) {
+  __shared__ uint32_t h[8 * 256];
+  __shared__ uint32_t s_spare[WAVE];  // adds that count nothing (never read)
+  __shared__ __align__(16) uint64_t s_row[HIST_THREADS * HIST_ROW];
   const HistJob jb = jobs.j[blockIdx.y];
   if (jb.id == 1 && ds->join_direct) return;  // the correlation table replaces the join sort
-  const int nd = jb.nd, nbins = nd * 256;
-  __shared__ uint32_t h[8 * 256];
   const int64_t n = *jb.count;
-  // the first digit pass's look-back words of this call's tiles (the passes
-  // follow on the same stream)
-  {
-    const int64_t words = cdiv(n, (int64_t)RS_TILE) * RS_LB_WORDS / 4;
-    uint4* st = reinterpret_cast<uint4*>(jb.status0);
-    for (int64_t w = (int64_t)blockIdx.x * HIST_THREADS + threadIdx.x; w < words; w += (int64_t)gridDim.x * HIST_THREADS)
-      st[w] = make_uint4(0u, 0u, 0u, 0u);
-  }
   const int nblk = hist_blocks(n);
   const int blk = blockIdx.x;
-  if (blk >= nblk) return;
+  // the first digit pass's look-back words of this call's tiles (the passes
+  // follow on the same stream), after the counting: its loads go first
+  auto clear_status = [&]() {
+    const int64_t words = cdiv(n, (int64_t)RS_TILE) * RS_LB_WORDS / 4;
+    uint4* st = reinterpret_cast<uint4*>(jb.status0);
+    for (int64_t w = (int64_t)blk * HIST_THREADS + threadIdx.x; w < words; w += (int64_t)gridDim.x * HIST_THREADS)
+      st[w] = make_uint4(0u, 0u, 0u, 0u);
+  };
+  if (blk >= nblk) {
+    clear_status();
+    return;
+  }
+  // (the first barrier of the count orders these before any add)
   for (int i = threadIdx.x; i < 8 * 256; i += HIST_THREADS) h[i] = 0;
-  __syncthreads();
-  const int64_t per = cdiv(n, nblk);
+  // shares are whole multiples of 64 keys (the 16-byte loads stay aligned)
+  const int64_t per = cdiv(cdiv(n, nblk), 64) * 64;
   const int64_t lo = min<int64_t>(n, (int64_t)blk * per), hi = min<int64_t>(n, lo + per);
-  switch (nd) {
-    case 1: hist_range<1>(h, jb.keys, lo, hi, jb.first); break;
-    case 2: hist_range<2>(h, jb.keys, lo, hi, jb.first); break;
-    case 3: hist_range<3>(h, jb.keys, lo, hi, jb.first); break;
-    case 4: hist_range<4>(h, jb.keys, lo, hi, jb.first); break;
-    case 5: hist_range<5>(h, jb.keys, lo, hi, jb.first); break;
-    case 6: hist_range<6>(h, jb.keys, lo, hi, jb.first); break;
-    case 7: hist_range<7>(h, jb.keys, lo, hi, jb.first); break;
-    default: hist_range<8>(h, jb.keys, lo, hi, jb.first); break;
+  switch (jb.nd) {
+    case 1: hist_range<1>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
+    case 2: hist_range<2>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
+    case 3: hist_range<3>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
+    case 4: hist_range<4>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
+    case 5: hist_range<5>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
+    case 6: hist_range<6>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
+    case 7: hist_range<7>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
+    default: hist_range<8>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
   }
   __syncthreads();
   uint32_t* part = jobs.part + ((int64_t)jb.id * HIST_MAX_BLOCKS + blk) * 8 * 256;
-  for (int j = threadIdx.x; j < nbins; j += HIST_THREADS) part[j] = h[j];
+  for (int j = threadIdx.x; j < jb.nd * 256; j += HIST_THREADS) part[j] = h[j];
+  clear_status();
 }
 
 // Plan of one digit of one sort (blockIdx.x = digit, blockIdx.y = sort):
-// the digit's counts summed over the workgroup tables (four threads per
-// bin, each summing every fourth table, 16 loads in flight), its trivial
-// flag (one bin holds every key) and each bin's exclusive offset.
+// the digit's counts summed over the workgroup tables, its trivial flag
+// (one bin holds every key) and each bin's exclusive offset.  A wave reads a
+// table's 256 counts as 16-byte loads (four bins a lane); the 16 waves take
+// every 16th table, PLAN_LOADS tables in flight per lane.
 constexpr int PLAN_THREADS = 1024;
-constexpr int PLAN_GROUPS = PLAN_THREADS / 256;
+constexpr int PLAN_GROUPS = PLAN_THREADS / WAVE;
+constexpr int PLAN_LOADS = 16;
 
 __global__ __launch_bounds__(PLAN_THREADS) void k_hist_plan(HistJobs jobs, DevState* ds) {
-  __shared__ uint32_t s_part[PLAN_GROUPS][256];
+  __shared__ __align__(16) uint32_t s_part[PLAN_GROUPS][256];
   __shared__ uint32_t s_scan[PLAN_THREADS / WAVE + 1];
   const HistJob jb = jobs.j[blockIdx.y];
   const int d = blockIdx.x;
   if (d >= jb.nd || (jb.id == 1 && ds->join_direct)) return;
   const int64_t n = *jb.count;
   const int nblk = hist_blocks(n);
-  const int bin = threadIdx.x & 255, grp = threadIdx.x >> 8;
-  const uint32_t* src = jobs.part + (int64_t)jb.id * HIST_MAX_BLOCKS * 8 * 256 + d * 256 + bin;
-  uint32_t c = 0;
-  for (int b0 = grp; b0 < nblk; b0 += 16 * PLAN_GROUPS) {
-    uint32_t v[16];
+  const int lane = threadIdx.x & (WAVE - 1), grp = threadIdx.x / WAVE;
+  const uint4* src = reinterpret_cast<const uint4*>(jobs.part + (int64_t)jb.id * HIST_MAX_BLOCKS * 8 * 256 + d * 256) + lane;
+  uint4 c4 = make_uint4(0u, 0u, 0u, 0u);
+  for (int b0 = grp; b0 < nblk; b0 += PLAN_LOADS * PLAN_GROUPS) {
+    uint4 v[PLAN_LOADS];
 #pragma unroll
-    for (int b = 0; b < 16; ++b) {
+    for (int b = 0; b < PLAN_LOADS; ++b) {
       const int blk = b0 + b * PLAN_GROUPS;
-      v[b] = src[(int64_t)min(blk, nblk - 1) * 8 * 256];
-      v[b] = blk < nblk ? v[b] : 0u;
+      v[b] = blk < nblk ? src[(int64_t)blk * 8 * 256 / 4] : make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
-    for (int b = 0; b < 16; ++b) c += v[b];
+    for (int b = 0; b < PLAN_LOADS; ++b) {
+      c4.x += v[b].x;
+      c4.y += v[b].y;
+      c4.z += v[b].z;
+      c4.w += v[b].w;
+    }
   }
-  s_part[grp][bin] = c;
+  *reinterpret_cast<uint4*>(&s_part[grp][4 * lane]) = c4;
   __syncthreads();
+  const int bin = threadIdx.x & 255;
+  uint32_t c = 0;
   if (threadIdx.x < 256) {
-    c = 0;
 #pragma unroll
     for (int g = 0; g < PLAN_GROUPS; ++g) c += s_part[g][bin];
   }

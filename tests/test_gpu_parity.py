@@ -355,6 +355,12 @@ def test_workspace_too_small(H):
     assert H.herschel_trace_analyze(ev, len(cols["ts"]), params, an.outs) == -4
     params = an._params_struct(None, 0)
     assert H.herschel_trace_analyze(ev, len(cols["ts"]), params, an.outs) == -4
+    # a workspace that is large enough but not 256-byte aligned
+    import torch
+
+    big = torch.empty(an.ws_bytes + 512, dtype=torch.uint8, device="cuda")
+    params = an._params_struct(big.data_ptr() + 16, an.ws_bytes)
+    assert H.herschel_trace_analyze(ev, len(cols["ts"]), params, an.outs) == -4
     assert an.run(ev, len(cols["ts"])) == 0
 
 
