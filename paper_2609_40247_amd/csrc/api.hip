@@ -37,15 +37,14 @@ struct Bump {
   }
 };
 
-// refine: whether the lowest digit is left to the refine pass (keys wider
-// than 32 bits, whose low byte is nanoseconds: runs of keys equal above it
-// are short)
+// refine: whether the lowest bits are left to the refine pass (keys wider
+// than 32 bits, whose low bits are nanoseconds: runs of keys equal above
+// them are short)
 static void sort_plan(SortBufs& s, int id, int64_t n_max, int key_bits, bool refine) {
   s.id = id;
   s.n_max = n_max;
   s.tiles_max = cdiv(std::max<int64_t>(n_max, 1), RS_TILE);
-  s.nd = (key_bits + 7) / 8;
-  s.first = refine && key_bits > 32 ? 1 : 0;
+  sort_digits(key_bits, refine, &s.nd, &s.first, &s.sh1);
 }
 
 size_t layout_workspace(Ctx& c, char* base) {
@@ -391,7 +390,6 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_end(c, HERSCHEL_STAGE_INIT);
   stage_begin(c, HERSCHEL_STAGE_PREP);
   launch_prep(c);
-  launch_join_plan(c);
   stage_end(c, HERSCHEL_STAGE_PREP);
 
   // The three sorts share their digit passes, pass p of a sort being its
@@ -641,11 +639,14 @@ int herschel_sort_stats(const herschel_params* p, int32_t* out) {
   const int tb = bits_host((uint64_t)(p->n_threads - 1));
   const int wb = bits_host((uint64_t)(p->window_end - p->window_begin - 1));
   const int key_bits[N_SORTS] = {pb + sb + wb, 49 + pb, pb + tb + wb + 1};  // as layout_workspace plans them
+  const bool refine[N_SORTS] = {true, false, true};
   const int32_t counts[N_SORTS] = {ds.nK, ds.nJ, ds.nCL};
   for (int i = 0; i < N_SORTS; ++i) {
+    int nd, first, sh1;
+    sort_digits(key_bits[i], refine[i], &nd, &first, &sh1);
     out[3 * i + 0] = counts[i];
     out[3 * i + 1] = (int32_t)ds.sort_trivial[i];
-    out[3 * i + 2] = (key_bits[i] + 7) / 8;
+    out[3 * i + 2] = nd;
   }
   return HERSCHEL_OK;
 }

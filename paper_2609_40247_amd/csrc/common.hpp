@@ -70,8 +70,8 @@ struct DevState {
   int64_t jt_base[JT_PROCS];       // first table slot of each process
   // join counts (JC_* order) and latency bins, in copies summed at the end
   unsigned long long join_acc[JOIN_COPIES][JC_N + 64];
-  // radix digit histograms; the last histogram workgroup turns each into the
-  // exclusive prefix over digit values (the global offset of every bin)
+  // radix digit offsets: each digit's exclusive prefix over its values (the
+  // global offset of every bin), from the plan kernel
   uint32_t hist[N_SORTS][8][256];
 };
 
@@ -95,6 +95,41 @@ template <class T>
 __device__ __forceinline__ T shfl_down(T v, unsigned d) { return __shfl_down(v, d, WAVE); }
 template <class T>
 __device__ __forceinline__ T shfl_xor(T v, int m) { return __shfl_xor(v, m, WAVE); }
+
+// The correlation-table plan, by one wave (lane p is process p of P <=
+// JT_PROCS): the table replaces the join sort when the processes' id ranges,
+// from prep's per-process smallest and largest join keys, fit `cap` slots
+// together; process p's ids then start at slot jt_base[p].  With `write` the
+// lanes store the plan (one wave of the call does); every caller gets the
+// decision.
+__device__ __forceinline__ bool jt_plan_wave(DevState* ds, int P, int64_t cap, bool write) {
+  const int p = threadIdx.x & (WAVE - 1);
+  const uint64_t lo = p < P ? ds->jt_key_lo[p] : 0ull, hi = p < P ? ds->jt_key_hi[p] : 0ull;
+  constexpr uint64_t CORR_MASK = (1ull << 48) - 1;
+  const bool present = lo != 0;  // lo holds ~(smallest key); keys never reach ~0
+  const int64_t cmin = present ? (int64_t)((~lo >> 1) & CORR_MASK) : 0;
+  const int64_t cmax = present ? (int64_t)((hi >> 1) & CORR_MASK) : -1;
+  // ranges beyond the capacity saturate, so the sum cannot overflow
+  int64_t range = cmax - cmin + 1;
+  range = range > cap ? cap + 1 : range;
+  int64_t inc = range;
+  for (int d = 1; d < WAVE; d <<= 1) {
+    const int64_t o = (int64_t)__shfl_up((uint64_t)inc, d, WAVE);
+    if (p >= d) inc += o;
+  }
+  const int64_t total = (int64_t)__shfl((uint64_t)inc, WAVE - 1, WAVE);
+  const bool direct = total <= cap;
+  if (write) {
+    ds->jt_cmin[p] = cmin;
+    ds->jt_base[p] = inc - range;
+    if (p == 0) {
+      ds->join_direct = direct ? 1u : 0u;
+      ds->jt_slots = direct ? total : 0;
+      if (direct) ds->sort_trivial[1] = 0xFFu;  // no join sort: every digit pass skipped
+    }
+  }
+  return direct;
+}
 
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
   for (int d = 32; d >= 1; d >>= 1) v += shfl_down(v, d);

@@ -17,10 +17,32 @@ struct SortBufs {
   uint32_t* status1 = nullptr;          // [nd - 1][tiles_max * RS_LB_WORDS] the later digits
   int64_t n_max = 0;                    // capacity (host upper bound of the count)
   int64_t tiles_max = 0;
-  int nd = 0;                           // 8-bit digits of the key
+  int nd = 0;                           // digits of the key: digit 0 below bit sh1, 8-bit digits above
   int id = 0;                           // sort index: histogram, parity
   int first = 0;                        // first digit sorted by passes (1: digit 0 left to the refine pass)
+  int sh1 = 8;                          // lowest bit of digit 1 (digit d >= 1 is bits sh1 + 8(d-1) ..)
 };
+
+// Digits of a key_bits-bit sort key.  With `refine` (keys wider than 32
+// bits), the passes take 8-bit digits from the top down and leave the bits
+// below them to the refine pass: as few passes as leave it at most
+// RF_LOW_MAX bits (8 at least).  Otherwise every digit is 8 bits, from bit 0.
+constexpr int RF_LOW_MAX = 14;
+inline void sort_digits(int key_bits, bool refine, int* nd, int* first, int* sh1) {
+  if (refine && key_bits > 32) {
+    int passes = (key_bits - RF_LOW_MAX + 7) / 8;
+    if (passes < 1) passes = 1;
+    int lo = key_bits - 8 * passes;
+    if (lo < 8) lo = 8;
+    *first = 1;
+    *sh1 = lo;
+    *nd = 1 + (key_bits - lo + 7) / 8;
+  } else {
+    *first = 0;
+    *sh1 = 8;
+    *nd = (key_bits + 7) / 8;
+  }
+}
 
 struct Ctx {
   hipStream_t st = nullptr;
@@ -94,7 +116,6 @@ void launch_depth(Ctx& c);
 void launch_opagg(Ctx& c);
 void launch_names_reduce(Ctx& c);
 void launch_join(Ctx& c);
-void launch_join_plan(Ctx& c);
 void launch_join_table(Ctx& c);
 void launch_edges(Ctx& c);
 void launch_finalize(Ctx& c);

@@ -196,32 +196,6 @@ __global__ __launch_bounds__(256) void k_join(JoinArgs a) {
 // Correlation-table plan: each process's id range (from the key range prep
 // found), slot bases by an exclusive scan, and the decision.  One wave, one
 // lane per process.
-__global__ __launch_bounds__(64) void k_jt_plan(JoinArgs a) {
-  const int p = threadIdx.x;
-  const uint64_t lo = p < a.P ? a.ds->jt_key_lo[p] : 0ull, hi = p < a.P ? a.ds->jt_key_hi[p] : 0ull;
-  constexpr uint64_t CORR_MASK = (1ull << 48) - 1;
-  const bool present = lo != 0;  // lo holds ~(smallest key); keys never reach ~0
-  const int64_t cmin = present ? (int64_t)((~lo >> 1) & CORR_MASK) : 0;
-  const int64_t cmax = present ? (int64_t)((hi >> 1) & CORR_MASK) : -1;
-  // ranges beyond the capacity saturate, so the sum cannot overflow
-  int64_t range = cmax - cmin + 1;
-  range = range > a.cap ? a.cap + 1 : range;
-  int64_t inc = range;
-  for (int d = 1; d < WAVE; d <<= 1) {
-    const int64_t o = (int64_t)shfl_up((uint64_t)inc, d);
-    if (p >= d) inc += o;
-  }
-  const int64_t total = (int64_t)shfl((uint64_t)inc, WAVE - 1);
-  const bool direct = total <= a.cap;
-  a.ds->jt_cmin[p] = cmin;
-  a.ds->jt_base[p] = inc - range;
-  if (p == 0) {
-    a.ds->join_direct = direct ? 1u : 0u;
-    a.ds->jt_slots = direct ? total : 0;
-    if (direct) a.ds->sort_trivial[1] = 0xFFu;  // no join sort: every digit pass skipped
-  }
-}
-
 __device__ __forceinline__ int64_t jt_slot(const DevState* ds, uint64_t key) {
   const int p = (int)(key >> 49);
   return ds->jt_base[p] + (int64_t)((key >> 1) & ((1ull << 48) - 1)) - ds->jt_cmin[p];
@@ -565,12 +539,6 @@ static JoinArgs join_args(Ctx& c) {
   a.cap = c.jt_cap;
   a.k_rows = c.k_rows;
   return a;
-}
-
-void launch_join_plan(Ctx& c) {
-  if (c.P > JT_PROCS) return;  // join_direct stays 0: the sort path
-  JoinArgs a = join_args(c);
-  hipLaunchKernelGGL(k_jt_plan, dim3(1), dim3(64), 0, c.st, a);
 }
 
 // The correlation-table join (no-ops unless the plan chose it); it needs only

@@ -24,15 +24,20 @@ struct HistJob {
   int nd;
   int id;
   int first;  // 1: digit 0 is left to the refine pass
+  int sh1;    // lowest bit of digit 1
 };
 struct HistJobs {
   HistJob j[N_SORTS];
   uint32_t* part;  // [N_SORTS][HIST_MAX_BLOCKS][8 * 256] per-workgroup counts
+  int jt_P;        // processes of the correlation-table plan (0: no table, the join sorts)
+  int64_t jt_cap;  // table slots
 };
 
 // Digit histograms of several sort inputs in one launch (blockIdx.y picks
 // the sort).  Each workgroup counts a contiguous share of the keys in LDS
-// and stores its table; the plan kernel that follows sums the tables.  No
+// and stores its table; the plan kernel that follows sums the tables.  The
+// join sort's workgroups first take the correlation-table plan, which
+// decides whether that sort runs at all.  No
 // global atomics and no fences: counters shared by many workgroups serialise
 // on their cache line, and a device-scope fence writes back the whole L2.
 // The grid is sized so that every CU holds a share (HIST_CHUNK keys at
@@ -139,10 +144,13 @@ __device__ __forceinline__ void hist_load(uint4* v, const uint64_t* __restrict__
   }
 }
 
-// The next round's loads are in flight while a round is counted.
+// The next round's loads are in flight while a round is counted.  Keys are
+// shifted right by `pre` (sh1 - 8) as they are read, so that digit d >= 1
+// is bits 8d .. 8d+7 of the shifted key.
 template <int ND>
-__device__ __forceinline__ void hist_range(uint32_t* h, uint32_t* s_spare, uint64_t* s_row, const uint64_t* __restrict__ keys,
-                                           int64_t lo, int64_t hi, int first) {
+__device__ __forceinline__ void hist_range(uint32_t* h, uint32_t* s_spare, uint64_t* s_row,
+                                           const uint64_t* __restrict__ keys, int64_t lo, int64_t hi, int first,
+                                           int pre) {
   const int t = threadIdx.x;
   uint4 v[HIST_U / 2];
   hist_load(v, keys, lo, hi);
@@ -158,8 +166,8 @@ __device__ __forceinline__ void hist_range(uint32_t* h, uint32_t* s_spare, uint6
 #pragma unroll
     for (int i = 0; i < HIST_U / 2; ++i) {
       const uint4 w = *reinterpret_cast<const uint4*>(s_row + t * HIST_ROW + 2 * i);
-      k[2 * i] = (uint64_t)w.x | ((uint64_t)w.y << 32);
-      k[2 * i + 1] = (uint64_t)w.z | ((uint64_t)w.w << 32);
+      k[2 * i] = ((uint64_t)w.x | ((uint64_t)w.y << 32)) >> pre;
+      k[2 * i + 1] = ((uint64_t)w.z | ((uint64_t)w.w << 32)) >> pre;
     }
     if (r0 + HIST_ROUND < hi) hist_load(v, keys, r0 + HIST_ROUND, hi);
     const int nv = (int)max<int64_t>(0, min<int64_t>(HIST_U, hi - (r0 + (int64_t)t * HIST_U)));
@@ -170,12 +178,22 @@ __device__ __forceinline__ void hist_range(uint32_t* h, uint32_t* s_spare, uint6
   }
 }
 
-__global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, const DevState* ds) {
+__global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, DevState* ds) {
   __shared__ uint32_t h[8 * 256];
   __shared__ uint32_t s_spare[WAVE];  // adds that count nothing (never read)
   __shared__ __align__(16) uint64_t s_row[HIST_THREADS * HIST_ROW];
+  __shared__ uint32_t s_direct;
   const HistJob jb = jobs.j[blockIdx.y];
-  if (jb.id == 1 && ds->join_direct) return;  // the correlation table replaces the join sort
+  if (jb.id == 1 && jobs.jt_P > 0) {
+    // the join sort's workgroups take the correlation-table plan (the first
+    // stores it): when the table replaces the sort they have nothing to count
+    if (threadIdx.x < WAVE) {
+      const bool direct = jt_plan_wave(ds, jobs.jt_P, jobs.jt_cap, blockIdx.x == 0);
+      if (threadIdx.x == 0) s_direct = direct ? 1u : 0u;
+    }
+    __syncthreads();
+    if (s_direct) return;
+  }
   const int64_t n = *jb.count;
   const int nblk = hist_blocks(n);
   const int blk = blockIdx.x;
@@ -197,14 +215,14 @@ __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, cons
   const int64_t per = cdiv(cdiv(n, nblk), 64) * 64;
   const int64_t lo = min<int64_t>(n, (int64_t)blk * per), hi = min<int64_t>(n, lo + per);
   switch (jb.nd) {
-    case 1: hist_range<1>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
-    case 2: hist_range<2>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
-    case 3: hist_range<3>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
-    case 4: hist_range<4>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
-    case 5: hist_range<5>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
-    case 6: hist_range<6>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
-    case 7: hist_range<7>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
-    default: hist_range<8>(h, s_spare, s_row, jb.keys, lo, hi, jb.first); break;
+    case 1: hist_range<1>(h, s_spare, s_row, jb.keys, lo, hi, jb.first, jb.sh1 - 8); break;
+    case 2: hist_range<2>(h, s_spare, s_row, jb.keys, lo, hi, jb.first, jb.sh1 - 8); break;
+    case 3: hist_range<3>(h, s_spare, s_row, jb.keys, lo, hi, jb.first, jb.sh1 - 8); break;
+    case 4: hist_range<4>(h, s_spare, s_row, jb.keys, lo, hi, jb.first, jb.sh1 - 8); break;
+    case 5: hist_range<5>(h, s_spare, s_row, jb.keys, lo, hi, jb.first, jb.sh1 - 8); break;
+    case 6: hist_range<6>(h, s_spare, s_row, jb.keys, lo, hi, jb.first, jb.sh1 - 8); break;
+    case 7: hist_range<7>(h, s_spare, s_row, jb.keys, lo, hi, jb.first, jb.sh1 - 8); break;
+    default: hist_range<8>(h, s_spare, s_row, jb.keys, lo, hi, jb.first, jb.sh1 - 8); break;
   }
   __syncthreads();
   uint32_t* part = jobs.part + ((int64_t)jb.id * HIST_MAX_BLOCKS + blk) * 8 * 256;
@@ -271,7 +289,8 @@ struct SortJob {
   uint32_t* status1;  // [nd - 1][tiles_max][RS_LB_WORDS] later digits (each cleared by the previous pass)
   int64_t tiles_max;
   int nd, id, first;
-  int d;  // the digit this launch sorts on
+  int sh1;  // lowest bit of digit 1 (digit d >= 1 is bits sh1 + 8(d-1) ..)
+  int d;    // the digit this launch sorts on
 };
 struct SortJobs {
   SortJob j[N_SORTS];  // slots m.. repeat slot 0
@@ -377,7 +396,7 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   const int tile = (int)t;
   const int64_t base = (int64_t)tile * RS_TILE;
 
-  const int shift = 8 * d;
+  const int shift = d == 0 ? 0 : jb.sh1 + 8 * (d - 1);
   uint64_t key[RS_ITEMS];
   uint32_t val[RS_ITEMS];
   uint32_t rank[RS_ITEMS];  // rank among the wave's equal digits, then the tile position
@@ -598,11 +617,13 @@ void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
   int64_t n_max = 1;
   for (int i = 0; i < k; ++i) {
     if (s[i]->nd == 0) continue;
-    jobs.j[m++] = HistJob{s[i]->k[0], count[i], s[i]->status0, s[i]->nd, s[i]->id, s[i]->first};
+    jobs.j[m++] = HistJob{s[i]->k[0], count[i], s[i]->status0, s[i]->nd, s[i]->id, s[i]->first, s[i]->sh1};
     n_max = std::max<int64_t>(n_max, s[i]->n_max);
     nd = std::max(nd, s[i]->nd);
   }
   if (m == 0) return;
+  jobs.jt_P = c.P <= JT_PROCS ? c.P : 0;
+  jobs.jt_cap = c.jt_cap;
   const int64_t grid = std::min<int64_t>(cdiv(n_max, HIST_CHUNK), HIST_MAX_BLOCKS);
   hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid, (unsigned)m), dim3(HIST_THREADS), 0, c.st, jobs, c.ds);
   hipLaunchKernelGGL(k_hist_plan, dim3((unsigned)nd, (unsigned)m), dim3(PLAN_THREADS), 0, c.st, jobs, c.ds);
@@ -620,7 +641,7 @@ void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
       const int d = s[i]->first + p;
       if (d >= s[i]->nd) continue;
       jobs.j[m++] = SortJob{{s[i]->k[0], s[i]->k[1]}, {s[i]->v[0], s[i]->v[1]}, count[i], s[i]->status0,
-                            s[i]->status1, s[i]->tiles_max, s[i]->nd, s[i]->id, s[i]->first, d};
+                            s[i]->status1, s[i]->tiles_max, s[i]->nd, s[i]->id, s[i]->first, s[i]->sh1, d};
       grid += s[i]->tiles_max;
     }
     if (m == 0) continue;
@@ -631,16 +652,17 @@ void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
 }
 
 // ------------------------------------------------------------------ refine
-// After passes over digits 1.. only, a sort is ordered by key >> 8; keys
-// equal above bit 8 still sit in row order (the passes are stable).  The
+// After passes over digits 1.. only, a sort is ordered by key >> sh1 (the
+// passes' lowest bit, 8 to RF_LOW_MAX); keys equal above it still sit in
+// row order (the passes are stable).  The
 // refine pass orders each such run by the full key, and keys that are
 // equal by the sort's own tie rule: the row (stable) for the timeline; for
 // the containment list, ops of equal key by end time down, then row (the
 // rule that nests an op that starts with its parent inside it).  The
 // containment list is refined even when every digit was sorted (runs of
 // equal keys, shift 0), for that tie rule.  Runs up to RF_SHORT are ordered
-// in place by their first thread (insertion sort); longer runs are listed
-// and each is sorted by one workgroup.
+// by one thread; longer runs are listed and each is sorted by one
+// workgroup.
 struct RefineJob {
   uint64_t* k[2];
   uint32_t* v[2];
@@ -648,7 +670,7 @@ struct RefineJob {
   int id;        // sort index (parity)
   int contain;   // 1: containment tie rule
   int slot;      // list index (0 timeline, 1 containment)
-  int shift;     // runs are keys equal above this bit (8, or 0 when every digit was sorted)
+  int shift;     // runs are keys equal above this bit (the passes' lowest, or 0 when every digit was sorted)
 };
 struct RefineJobs {
   RefineJob j[2];
@@ -670,112 +692,106 @@ __device__ __forceinline__ bool rf_before(const RefineJob& jb, const int64_t* te
 
 constexpr int RF_THREADS = 256;
 constexpr int RF_ITEMS = 4;
-constexpr int RF_NET = 8;  // runs up to this length are sorted in registers
+constexpr int RF_TILE = RF_THREADS * RF_ITEMS;  // positions whose runs a workgroup orders
+constexpr int RF_SPAN = 1 + RF_TILE + RF_SHORT;  // the position before the tile, the tile, and its runs' reach
 
+// A workgroup stages its tile's keys and rows in LDS (coalesced), with the
+// position before the tile and the RF_SHORT after it, and finds the tile's
+// run starts there.  A thread per run orders it in LDS (insertion sort:
+// the runs are short, and many are in order already) and marks the
+// positions that moved; the workgroup then writes those back, coalesced.
+// A run longer than RF_SHORT is listed instead.
 __global__ __launch_bounds__(RF_THREADS) void k_refine(RefineJobs jobs, DevState* ds) {
-  __shared__ int32_t s_run[RF_THREADS * RF_ITEMS];  // run starts of this workgroup's positions
+  __shared__ uint64_t s_k[RF_SPAN];
+  __shared__ uint32_t s_v[RF_SPAN];
+  __shared__ uint8_t s_chg[RF_SPAN];       // 1: the position moved
+  __shared__ int32_t s_run[RF_TILE / 2];  // span indices of the tile's run starts (a run has two keys or more)
   __shared__ int s_nrun;
   const RefineJob& jb = jobs.j[blockIdx.y];
   const int64_t n = *jb.count;
-  if (n < 2) return;
+  const int64_t t0 = (int64_t)blockIdx.x * RF_TILE;
+  if (n < 2 || t0 >= n) return;
   const int par = (int)ds->sort_parity[jb.id];
   uint64_t* keys = jb.k[par];
   uint32_t* vals = jb.v[par];
-  const int64_t p0 = (int64_t)blockIdx.x * RF_THREADS * RF_ITEMS + threadIdx.x;
   if (threadIdx.x == 0) s_nrun = 0;
-  // each position with its neighbours, loads clamped and issued together
-  uint64_t kp[RF_ITEMS], kc[RF_ITEMS], kn[RF_ITEMS];
+  // span index i holds position t0 - 1 + i (clamped to the list); the
+  // loads are issued together (the span's last few are loaded twice)
+  constexpr int RF_LD = (RF_SPAN + RF_THREADS - 1) / RF_THREADS;
+  uint64_t lk[RF_LD];
+  uint32_t lv[RF_LD];
 #pragma unroll
-  for (int u = 0; u < RF_ITEMS; ++u) {
-    const int64_t p = p0 + u * RF_THREADS;
-    const int64_t pc = p < n ? p : n - 1;
-    kp[u] = keys[pc > 0 ? pc - 1 : 0];
-    kc[u] = keys[pc];
-    kn[u] = keys[pc + 1 < n ? pc + 1 : pc];
+  for (int u = 0; u < RF_LD; ++u) {
+    const int i = min(u * RF_THREADS + (int)threadIdx.x, RF_SPAN - 1);
+    int64_t q = t0 - 1 + i;
+    q = q < 0 ? 0 : q >= n ? n - 1 : q;
+    lk[u] = keys[q];
+    lv[u] = vals[q];
+  }
+#pragma unroll
+  for (int u = 0; u < RF_LD; ++u) {
+    const int i = min(u * RF_THREADS + (int)threadIdx.x, RF_SPAN - 1);
+    s_k[i] = lk[u];
+    s_v[i] = lv[u];
+    s_chg[i] = 0;
   }
   __syncthreads();
   const int sh = jb.shift;
-  // the first positions of runs of two or more keys equal above the shift,
-  // gathered so that each is then ordered by a thread of its own (a run
-  // start is rare: ordering it where it was found would hold up its wave)
+  // the first positions of runs of two or more keys equal above the shift
 #pragma unroll
   for (int u = 0; u < RF_ITEMS; ++u) {
-    const int64_t p = p0 + u * RF_THREADS;
-    const bool start = p < n && p + 1 < n && (kn[u] >> sh) == (kc[u] >> sh) && !(p > 0 && (kp[u] >> sh) == (kc[u] >> sh));
+    const int i = 1 + u * RF_THREADS + (int)threadIdx.x;
+    const int64_t p = t0 - 1 + i;
+    const uint64_t hk = s_k[i] >> sh;
+    const bool start = p + 1 < n && (s_k[i + 1] >> sh) == hk && !(p > 0 && (s_k[i - 1] >> sh) == hk);
     const uint64_t b = ballot(start);
     if (b == 0) continue;
     int at = 0;
     if (lane_id() == __ffsll((unsigned long long)b) - 1) at = atomicAdd(&s_nrun, popc(b));
     at = __shfl(at, __ffsll((unsigned long long)b) - 1, WAVE);
-    if (start) s_run[at + popc(b & lanemask_lt())] = (int32_t)p;
+    if (start) s_run[at + popc(b & lanemask_lt())] = i;
   }
   __syncthreads();
   const int nrun = s_nrun;
   for (int ri = threadIdx.x; ri < nrun; ri += RF_THREADS) {
-    const int64_t p = s_run[ri];
-    const uint64_t hi = keys[p] >> sh;
-    // runs up to RF_NET: loaded at once and ordered by a sorting network
-    // in registers; longer ones by insertion sort in place, or listed
-    uint64_t rk[RF_NET];
-    uint32_t rr[RF_NET];
-#pragma unroll
-    for (int t = 0; t < RF_NET; ++t) {
-      const int64_t q = p + t < n ? p + t : n - 1;
-      rk[t] = keys[q];
-      rr[t] = vals[q];
-    }
-    int len = 0;
-#pragma unroll
-    for (int t = 0; t < RF_NET; ++t)
-      if (len == t && p + t < n && (rk[t] >> sh) == hi) len = t + 1;
-    if (len < RF_NET || p + RF_NET >= n || (keys[p + RF_NET] >> sh) != hi) {
-      // odd-even transposition network over the run's first len entries
-      // (entries past it compare as greater and never move)
-#pragma unroll
-      for (int round = 0; round < RF_NET; ++round) {
-#pragma unroll
-        for (int t = round & 1; t + 1 < RF_NET; t += 2) {
-          if (t + 1 < len && rf_before(jb, jobs.te, rk[t + 1], rr[t + 1], rk[t], rr[t])) {
-            const uint64_t k0 = rk[t];
-            const uint32_t r0 = rr[t];
-            rk[t] = rk[t + 1];
-            rr[t] = rr[t + 1];
-            rk[t + 1] = k0;
-            rr[t + 1] = r0;
-          }
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < RF_NET; ++t) {
-        if (t < len) {
-          keys[p + t] = rk[t];
-          vals[p + t] = rr[t];
-        }
-      }
-      continue;
-    }
-    int64_t e = p + RF_NET;
-    while (e < n && (keys[e] >> sh) == hi && e - p <= RF_SHORT) ++e;
-    if (e - p > RF_SHORT) {
+    const int i = s_run[ri];
+    const int64_t p = t0 - 1 + i;
+    const uint64_t hk = s_k[i] >> sh;
+    // the run's length (a run that reaches the span's end is longer than RF_SHORT)
+    int len = 2;
+    while (i + len < RF_SPAN && p + len < n && (s_k[i + len] >> sh) == hk) ++len;
+    if (len > RF_SHORT || (i + len == RF_SPAN && p + len < n)) {
       const int at = atomicAdd(&ds->n_long[jb.slot], 1);
       if (at < jobs.cap) jobs.list[(int64_t)jb.slot * jobs.cap + at] = (int32_t)p;
       else set_status(ds, DS_TIES);
       continue;
     }
-    for (int64_t i = p + 1; i < e; ++i) {
-      const uint64_t k = keys[i];
-      const uint32_t r = vals[i];
-      int64_t j = i - 1;
-      while (j >= p) {
-        const uint64_t kj = keys[j];
-        const uint32_t rj = vals[j];
-        if (!rf_before(jb, jobs.te, k, r, kj, rj)) break;
-        keys[j + 1] = kj;
-        vals[j + 1] = rj;
-        --j;
+    // insertion sort in LDS; `lo` is the first position that moved
+    int lo = len;
+    for (int x = i + 1; x < i + len; ++x) {
+      const uint64_t k = s_k[x];
+      const uint32_t r = s_v[x];
+      int y = x - 1;
+      while (y >= i && rf_before(jb, jobs.te, k, r, s_k[y], s_v[y])) {
+        s_k[y + 1] = s_k[y];
+        s_v[y + 1] = s_v[y];
+        --y;
       }
-      keys[j + 1] = k;
-      vals[j + 1] = r;
+      if (y + 1 != x) {
+        s_k[y + 1] = k;
+        s_v[y + 1] = r;
+        lo = min(lo, y + 1 - i);
+      }
+    }
+    for (int j = lo; j < len; ++j) s_chg[i + j] = 1;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < RF_LD; ++u) {
+    const int i = u * RF_THREADS + (int)threadIdx.x;
+    if (i < RF_SPAN && s_chg[i]) {
+      keys[t0 - 1 + i] = s_k[i];
+      vals[t0 - 1 + i] = s_v[i];
     }
   }
 }
@@ -852,14 +868,14 @@ void launch_refine(Ctx& c) {
     const bool con = s == &c.sC;
     if (con ? !c.contain : s->first == 0) continue;
     jobs.j[m++] = RefineJob{{s->k[0], s->k[1]}, {s->v[0], s->v[1]}, con ? &c.ds->nCL : &c.ds->nK, s->id, con ? 1 : 0,
-                            con ? 1 : 0, 8 * s->first};
+                            con ? 1 : 0, s->first ? s->sh1 : 0};
     n_max = std::max<int64_t>(n_max, s->n_max);
   }
   if (m == 0) return;
   jobs.te = c.ev.te;
   jobs.list = c.rf_list;
   jobs.cap = c.rf_cap;
-  const int64_t grid = cdiv(n_max, RF_THREADS * RF_ITEMS);
+  const int64_t grid = cdiv(n_max, RF_TILE);
   hipLaunchKernelGGL(k_refine, dim3((unsigned)grid, (unsigned)m), dim3(RF_THREADS), 0, c.st, jobs, c.ds);
   hipLaunchKernelGGL(k_refine_long, dim3(64, (unsigned)m), dim3(256), 0, c.st, jobs, c.ds);
 }
