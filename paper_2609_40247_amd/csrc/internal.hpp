@@ -129,7 +129,7 @@ constexpr int HIST_CHUNK = 4096;
 constexpr int HIST_MAX_BLOCKS = 256;
 
 // per-op aggregates: positions per workgroup, open ops kept per tile start
-constexpr int AG_TILE = 1024;
+constexpr int AG_TILE = 512;
 constexpr int AG_CHAIN = 64;
 
 constexpr int RS_THREADS = 512;
