@@ -372,7 +372,7 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
 // Depth by walking the parents; improper nesting; op aggregates reset.  Each
 // thread walks DP_ITEMS positions' parent chains side by side, so the loads
 // of one step of all chains are in flight together.
-constexpr int DP_ITEMS = 4;
+constexpr int DP_ITEMS = 2;
 
 __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
   __shared__ unsigned long long s_imp;

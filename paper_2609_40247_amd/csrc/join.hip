@@ -228,23 +228,25 @@ __device__ __forceinline__ void jt_flush(const JoinArgs& a, uint32_t (&c)[JC_N],
   if (s_h && threadIdx.x < 64 && s_h[threadIdx.x]) atomicAdd(&acc[JC_N + threadIdx.x], s_h[threadIdx.x]);
 }
 
-// The table passes give each thread JT_ITEMS positions (striped over the
+// The table passes give each thread IT positions (striped over the
 // workgroup) and issue each round of their loads together: a pass is a
 // short chain of dependent loads, and batching positions per thread keeps
-// the number of waves the chip must cycle through low.
-constexpr int JT_ITEMS = 4;
-constexpr int JT_TILE = 256 * JT_ITEMS;
+// the number of waves the chip must cycle through low.  The check and
+// kernel passes, whose chains are longest, take 8 positions a thread; the
+// store and fix passes 2 (each measured best).
+constexpr int JT_IT_STORE = 2, JT_IT_CHECK = 8, JT_IT_FIX = 2, JT_IT_KERNEL = 8;
 
 // Pass 1: every launch stores its row in its slot and every kernel in its
 // slot's owner word, with plain stores (one writer of each wins).
+template <int IT>
 __global__ __launch_bounds__(256) void k_jt_store(JoinArgs a) {
   if (!a.ds->join_direct) return;
   const int64_t n = a.ds->nJ;
-  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + threadIdx.x;
-  uint64_t key[JT_ITEMS];
-  uint32_t row[JT_ITEMS];
+  const int64_t i0 = (int64_t)blockIdx.x * (256 * IT) + threadIdx.x;
+  uint64_t key[IT];
+  uint32_t row[IT];
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     const int64_t i = i0 + u * 256;
     const int64_t ic = i < n ? i : (n > 0 ? n - 1 : 0);  // clamped: the loads stay in flight together
     key[u] = a.k[0][ic];  // unsorted: the join sort did not run
@@ -252,7 +254,7 @@ __global__ __launch_bounds__(256) void k_jt_store(JoinArgs a) {
     if (i >= n) key[u] = ~0ull;
   }
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     if (key[u] == ~0ull) continue;
     const int64_t slot = jt_slot(a.ds, key[u]);
     if (!in_range(a.ds, slot, a.cap)) continue;
@@ -266,6 +268,7 @@ __global__ __launch_bounds__(256) void k_jt_store(JoinArgs a) {
 // Pass 2: a launch that lost its slot is a duplicate; a kernel that lost its
 // owner word marks the slot as holding several kernels.  Launches start with
 // no kernels (their kernel aggregates are read only when they have some).
+template <int IT>
 __global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
   __shared__ unsigned long long s_c[JC_N];
   const int tid = threadIdx.x;
@@ -273,13 +276,13 @@ __global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
   __syncthreads();
   if (!a.ds->join_direct) return;
   const int64_t n = a.ds->nJ;
-  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + tid;
+  const int64_t i0 = (int64_t)blockIdx.x * (256 * IT) + tid;
   uint32_t c[JC_N] = {};
-  uint64_t key[JT_ITEMS];
-  uint32_t row[JT_ITEMS], w[JT_ITEMS];
-  int64_t slot[JT_ITEMS];
+  uint64_t key[IT];
+  uint32_t row[IT], w[IT];
+  int64_t slot[IT];
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     const int64_t i = i0 + u * 256;
     const int64_t ic = i < n ? i : (n > 0 ? n - 1 : 0);
     key[u] = a.k[0][ic];
@@ -287,7 +290,7 @@ __global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
     if (i >= n) key[u] = ~0ull;
   }
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     slot[u] = key[u] != ~0ull ? jt_slot(a.ds, key[u]) : -1;
     const bool ok = slot[u] >= 0 && in_range(a.ds, slot[u], a.cap);
     const int64_t sc = ok ? slot[u] : 0;
@@ -296,7 +299,7 @@ __global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
     w[u] = !ok ? row[u] : ws;
   }
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     if (key[u] == ~0ull) continue;
     if (key[u] & 1) {
       if (w[u] != row[u]) a.multi[slot[u]] = 1;
@@ -312,14 +315,15 @@ __global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
 // and the launches of slots with several kernels start their kernel
 // aggregates at the identities (the kernels add to them with atomics; a
 // launch with one kernel gets plain stores).
+template <int IT>
 __global__ __launch_bounds__(256) void k_jt_fix(JoinArgs a) {
   if (!a.ds->join_direct) return;
   const int64_t n = a.ds->nJ;
-  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + threadIdx.x;
-  uint64_t key[JT_ITEMS];
-  uint32_t row[JT_ITEMS];
+  const int64_t i0 = (int64_t)blockIdx.x * (256 * IT) + threadIdx.x;
+  uint64_t key[IT];
+  uint32_t row[IT];
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     const int64_t i = i0 + u * 256;
     const int64_t ic = i < n ? i : (n > 0 ? n - 1 : 0);
     key[u] = a.k[0][ic];
@@ -327,7 +331,7 @@ __global__ __launch_bounds__(256) void k_jt_fix(JoinArgs a) {
     if (i >= n) key[u] = 1ull;  // past the end: treated as a kernel
   }
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     if (key[u] & 1) continue;
     const int64_t slot = jt_slot(a.ds, key[u]);
     if (!in_range(a.ds, slot, a.cap)) continue;
@@ -345,6 +349,7 @@ __global__ __launch_bounds__(256) void k_jt_fix(JoinArgs a) {
 // Pass 4: each kernel reads its launch, records the latency, and adds itself
 // to the launch's counts: with plain stores when it is its slot's only kernel
 // (the usual case), with atomics otherwise.
+template <int IT>
 __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
   __shared__ unsigned long long s_c[JC_N];
   __shared__ unsigned long long s_h[64];
@@ -357,12 +362,12 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
   // Positions past the end take the last entry's row (clamped loads); with
   // no entry there is no row to take, and nothing to do.
   if (n == 0) return;
-  const int64_t i0 = (int64_t)blockIdx.x * JT_TILE + tid;
+  const int64_t i0 = (int64_t)blockIdx.x * (256 * IT) + tid;
   uint32_t c[JC_N] = {};
-  uint64_t key[JT_ITEMS];
-  uint32_t row[JT_ITEMS];
+  uint64_t key[IT];
+  uint32_t row[IT];
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     const int64_t i = i0 + u * 256;
     const int64_t ic = i < n ? i : n - 1;
     key[u] = a.k[0][ic];
@@ -370,11 +375,11 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
     if (i >= n) key[u] = 0ull;  // past the end: treated as a launch (skipped)
   }
   // round 2: the slot's launch and kernel count, the kernel's times
-  int64_t slot[JT_ITEMS], ts[JT_ITEMS], te[JT_ITEMS];
-  uint32_t l[JT_ITEMS];
-  bool single[JT_ITEMS];
+  int64_t slot[IT], ts[IT], te[IT];
+  uint32_t l[IT];
+  bool single[IT];
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     const bool kern = (key[u] & 1) != 0;
     slot[u] = kern ? jt_slot(a.ds, key[u]) : -1;
     const bool ok = slot[u] >= 0 && in_range(a.ds, slot[u], a.cap);
@@ -388,15 +393,15 @@ __global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
     te[u] = kern ? t1 : 0;
   }
   // round 3: the launch's start
-  int64_t lts[JT_ITEMS];
+  int64_t lts[IT];
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     const bool has = (key[u] & 1) && l[u] != ~0u;
     const int64_t t = a.ts[has ? l[u] : 0u];
     lts[u] = has ? t : 0;
   }
 #pragma unroll
-  for (int u = 0; u < JT_ITEMS; ++u) {
+  for (int u = 0; u < IT; ++u) {
     if (!(key[u] & 1)) continue;
     const int64_t o = a.off ? a.off[(int32_t)(key[u] >> 49)] : 0;
     if (a.kmax && slot[u] >= 0) {
@@ -547,12 +552,12 @@ void launch_join_table(Ctx& c) {
   if (c.P > JT_PROCS) return;
   JoinArgs a = join_args(c);
   const int64_t cgrid = std::min<int64_t>(std::max<int64_t>(cdiv(c.jt_cap, 256 * 8), 1), 4096);
-  const int64_t tgrid = std::max<int64_t>(cdiv(c.sJ.n_max, JT_TILE), 1);
+  auto tgrid = [&](int it) { return dim3((unsigned)std::max<int64_t>(cdiv(c.sJ.n_max, 256 * it), 1)); };
   hipLaunchKernelGGL(k_jt_clear, dim3((unsigned)cgrid), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_jt_store, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_jt_check, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_jt_fix, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_jt_kernel, dim3((unsigned)tgrid), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_store<JT_IT_STORE>, tgrid(JT_IT_STORE), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_check<JT_IT_CHECK>, tgrid(JT_IT_CHECK), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_fix<JT_IT_FIX>, tgrid(JT_IT_FIX), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_kernel<JT_IT_KERNEL>, tgrid(JT_IT_KERNEL), dim3(256), 0, c.st, a);
 }
 
 // The sort-merge join (a no-op when the table did the join); after the sorts.
