@@ -160,6 +160,33 @@ def test_long_runs_of_equal_op_starts(H):
     check(H, cols, p, "long tie runs")
 
 
+def test_wide_keys_short_runs_across_tiles(H):
+    """Keys wider than 32 bits (a 30 s window): the digit passes stop at bit
+    12 or 13 and the refine pass orders the runs of keys equal above it.
+    Bursts of 1 to 40 kernels of one stream, and of ops and launches of one
+    thread, start within 4 us of each other in random row order, so runs of
+    every length up to past the short limit (32 keys) fall on every offset
+    of the refine pass's 1024-position tiles."""
+    rng = np.random.default_rng(11)
+    rows = []
+    corr = 0
+    for g in range(700):
+        L = int(rng.choice([1, 2, 3, 5, 8, 17, 31, 32, 33, 40]))
+        base = 5_000_000_000 + g * 60_000 + int(rng.integers(0, 8192))
+        s, th = g % 2, (g // 2) % 2
+        for i in range(L):
+            ts = base + int(rng.integers(0, 4000))
+            rows.append((2, 0, s, ts, ts + 50 + int(rng.integers(0, 2000)), corr, i % 4))
+            rows.append((1, 0, th, ts - 500, ts - 480, corr, 0))
+            corr += 1
+            to = base + int(rng.integers(0, 4000))
+            rows.append((0, 0, th, to, to + 100 + int(rng.integers(0, 5000)), 0, i % 4))
+    perm = rng.permutation(len(rows))
+    rows = [rows[i] for i in perm]
+    cols, p = _rows(rows, S=2, T=2, W=30_000_000_000, thr=20_000)
+    check(H, cols, p, "wide keys, short runs")
+
+
 def test_deep_nesting(H):
     """A chain of 300 nested ops with thousands of launches inside: the
     stack open at a tile edge is deeper than the per-tile table."""
