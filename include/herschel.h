@@ -223,9 +223,11 @@ int herschel_time_stage(int stage, void *start_event, void *stop_event);
  * these params, for computing the bytes the radix passes must move: waits
  * for params->hip_stream, then writes, for s = 0 timeline, 1 join,
  * 2 containment sort: out[3 * s + 0] = its keys, out[3 * s + 1] = bit mask
- * of the 8-bit digits that no pass moved (bit d: every key agreed on digit
- * d, or digit d was left to the refine pass that orders keys equal above
- * it; bit 31 is set in the second case), out[3 * s + 2] = its digits.  out
+ * of the digits that no pass moved (bit d: every key agreed on digit d, or
+ * digit d was left to the refine pass that orders keys equal above it; bit
+ * 31 is set in the second case), out[3 * s + 2] = its digits.  Digits above
+ * digit 0 are 8 bits wide; digit 0 is 8 bits, or, when it is left to the
+ * refine pass, the 8 to 14 bits below the passes' 8-bit digits.  out
  * must hold 9 entries (host memory).  Returns HERSCHEL_EINVAL for NULL
  * arguments, no workspace or an invalid window or size, HERSCHEL_EDEVICE
  * when the copy fails. */
