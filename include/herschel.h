@@ -46,14 +46,15 @@ enum {
 };
 
 /* Return codes.  Precedence when several apply:
- * EINVAL > EWORKSPACE > EEVENT > EDEVICE > ECAPACITY. */
+ * EINVAL > EWORKSPACE (ETOOBIG) > EEVENT > EDEVICE > ECAPACITY. */
 enum {
   HERSCHEL_OK = 0,
   HERSCHEL_EINVAL = -1,     /* a required pointer is NULL or a parameter is out of range */
   HERSCHEL_EEVENT = -2,     /* an input row is invalid; counters->first_invalid = smallest such row */
   HERSCHEL_ECAPACITY = -3,  /* more gaps than gap_capacity; the first gap_capacity are written */
   HERSCHEL_EWORKSPACE = -4, /* workspace is NULL, not 256-byte aligned, or smaller than herschel_workspace_size() */
-  HERSCHEL_EDEVICE = -5     /* a HIP call failed or a device-side consistency check tripped */
+  HERSCHEL_EDEVICE = -5,    /* a HIP call failed or a device-side consistency check tripped */
+  HERSCHEL_ETOOBIG = -6     /* herschel_trace_analyze_static: the call needs more than its static scratch */
 };
 
 /* Optional outputs (params.flags).  Timelines, gaps, the launch/kernel join,
@@ -174,6 +175,25 @@ int herschel_workspace_size(int64_t n, const herschel_params *p, size_t *bytes);
  * from several host threads are serialised while they enqueue. */
 int herschel_trace_analyze(const herschel_events *ev, int64_t n, const herschel_params *p,
                            herschel_outputs *out);
+
+/* Device memory, in bytes, of the static scratch that
+ * herschel_trace_analyze_static uses in place of a caller's workspace (about
+ * 330,000 rows with every output of a 4-stream trace). */
+#define HERSCHEL_STATIC_SCRATCH_BYTES (64LL << 20)
+
+/* For callers that cannot allocate device memory (serving loops, harnesses
+ * that forbid allocation): herschel_trace_analyze with the same arguments and
+ * results, except that p->workspace and p->workspace_bytes are ignored.  The
+ * library's own scratch array (HERSCHEL_STATIC_SCRATCH_BYTES, one per device,
+ * held until the process ends) serves as the workspace, every kernel runs on
+ * p->hip_stream one after another, and the call allocates nothing: no device
+ * memory, no streams, no events, no graphs.  Returns HERSCHEL_ETOOBIG (and
+ * enqueues nothing) when herschel_workspace_size(n, p) exceeds the scratch.
+ * Calls that overlap on one device share its scratch and race: the caller
+ * must not issue a second call on a device before the first has returned.
+ * Each call clears what it needs, so calls in sequence are independent. */
+int herschel_trace_analyze_static(const herschel_events *ev, int64_t n, const herschel_params *p,
+                                  herschel_outputs *out);
 
 /* Reconstruct n_traces independent windows stored back to back in ev: trace
  * t holds rows [trace_offsets[t], trace_offsets[t+1]) (a HOST array of

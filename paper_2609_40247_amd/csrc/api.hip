@@ -379,12 +379,21 @@ static bool env_flag(const char* name, bool dflt) {
 }
 
 // Enqueues one call's kernels (the caller holds g_enqueue_mutex).  With
-// HERSCHEL_SERIAL=1 every chain runs on the caller's stream, one kernel
-// after another (for per-kernel profiles without concurrent neighbours).
+// HERSCHEL_SERIAL=1, or without library streams (dsx == nullptr, the
+// entry point that allocates nothing), every chain runs on the caller's
+// stream, one kernel after another, and no event is recorded.
 static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
-  static const bool serial = env_flag("HERSCHEL_SERIAL", false);
+  static const bool serial_env = env_flag("HERSCHEL_SERIAL", false);
+  const bool serial = serial_env || !dsx;
   const hipStream_t s0 = c.st;
   const hipStream_t lib0 = serial ? s0 : dsx->s[0], lib1 = serial ? s0 : dsx->s[1];
+  // cross-stream edges (nothing to order when every chain is on one stream)
+  auto rec = [&](int e, hipStream_t s) {
+    if (!serial) (void)hipEventRecord(dsx->e[e], s);
+  };
+  auto wait = [&](hipStream_t s, int e) {
+    if (!serial) (void)hipStreamWaitEvent(s, dsx->e[e], 0);
+  };
   stage_begin(c, HERSCHEL_STAGE_INIT);
   launch_init(c);
   stage_end(c, HERSCHEL_STAGE_INIT);
@@ -414,7 +423,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   launch_sort_multi(c, ss, cc, ks, 0, p_shared);
   stage_end(c, HERSCHEL_STAGE_SORT);
   launch_refine(c);
-  (void)hipEventRecord(dsx->e[0], s0);
+  rec(0, s0);
 
   // chain 3 on the caller's stream, enqueued first: containment is the
   // longest of the three chains, and of work that becomes ready together
@@ -423,7 +432,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   if (c.contain) {
     stage_begin(c, HERSCHEL_STAGE_CONTAIN);
     launch_contain(c);
-    (void)hipEventRecord(dsx->e[3], s0);  // each launch's op is known
+    rec(3, s0);  // each launch's op is known
     launch_depth(c);
     stage_end(c, HERSCHEL_STAGE_CONTAIN);
   } else {
@@ -434,7 +443,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   // chain 2: the join by the correlation table, or else by the rest of the
   // join sort and the sort-merge join; then the dependency waits
   c.st = lib1;
-  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
+  wait(c.st, 0);
   stage_begin(c, HERSCHEL_STAGE_JOIN);
   launch_join_table(c);
   launch_sort_multi(c, &ss[ks - 1], &cc[ks - 1], 1, p_shared, c.sJ.nd - c.sJ.first);
@@ -443,35 +452,35 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_EDGES);
   launch_edges(c);
   stage_end(c, HERSCHEL_STAGE_EDGES);
-  (void)hipEventRecord(dsx->e[2], c.st);
+  rec(2, c.st);
   // the name pass also gives each kernel its launch's op: after the join
   // and after the launches' ops are known
-  if (c.contain) (void)hipStreamWaitEvent(c.st, dsx->e[3], 0);
+  if (c.contain) wait(c.st, 3);
   stage_begin(c, HERSCHEL_STAGE_NAMES);
   launch_names(c);
   launch_names_reduce(c);
   stage_end(c, HERSCHEL_STAGE_NAMES);
-  (void)hipEventRecord(dsx->e[4], c.st);
+  rec(4, c.st);
 
   // chain 1: timeline and overlap
   c.st = lib0;
-  (void)hipStreamWaitEvent(c.st, dsx->e[0], 0);
+  wait(c.st, 0);
   stage_begin(c, HERSCHEL_STAGE_TIMELINE);
   launch_timeline(c);
   stage_end(c, HERSCHEL_STAGE_TIMELINE);
   stage_begin(c, HERSCHEL_STAGE_OVERLAP);
   if (c.overlap) launch_overlap(c);
   stage_end(c, HERSCHEL_STAGE_OVERLAP);
-  (void)hipEventRecord(dsx->e[1], c.st);
+  rec(1, c.st);
 
   // back on the caller's stream: what needs both containment and the join
   c.st = s0;
-  (void)hipStreamWaitEvent(c.st, dsx->e[2], 0);
+  wait(c.st, 2);
   stage_begin(c, HERSCHEL_STAGE_OPAGG);
   if (c.contain) launch_opagg(c);
   stage_end(c, HERSCHEL_STAGE_OPAGG);
-  (void)hipStreamWaitEvent(c.st, dsx->e[1], 0);
-  (void)hipStreamWaitEvent(c.st, dsx->e[4], 0);
+  wait(c.st, 1);
+  wait(c.st, 4);
   stage_begin(c, HERSCHEL_STAGE_FINAL);
   launch_finalize(c);
   stage_end(c, HERSCHEL_STAGE_FINAL);
@@ -592,6 +601,33 @@ static int enqueue_cached(Ctx& c, const herschel_events* ev, int64_t n, const he
   return enqueue_locked(c, dsx);
 }
 
+// ------------------------------------------------------- static scratch
+// The workspace of herschel_trace_analyze_static: one array per device that
+// loads the library, held until the process ends.  Host code never passes
+// the array's name to a kernel (on the host it is a stand-in, not a device
+// address): the device address is taken once per device with
+// hipGetSymbolAddress and every use goes through it.
+static __device__ __align__(256) char scratch[HERSCHEL_STATIC_SCRATCH_BYTES];
+static void* g_scratch_ptr[64];
+static bool g_scratch_ok[64];
+
+// The current device's address of `scratch` (the caller holds
+// g_enqueue_mutex); nullptr when the lookup fails.
+static void* static_scratch() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  if (!g_scratch_ok[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+    g_scratch_ok[dev] = true;
+  }
+  return g_scratch_ptr[dev];
+}
+
 static int code_from(const herschel_counters& h, int64_t gap_capacity) {
   if (h.device_status & DS_PARAM) return HERSCHEL_EINVAL;
   if (h.first_invalid >= 0) return HERSCHEL_EEVENT;
@@ -614,6 +650,7 @@ const char* herschel_strerror(int code) {
     case HERSCHEL_ECAPACITY: return "gap list capacity exceeded (see counters.n_gaps_total)";
     case HERSCHEL_EWORKSPACE: return "workspace missing, misaligned or too small";
     case HERSCHEL_EDEVICE: return "device error";
+    case HERSCHEL_ETOOBIG: return "input too large for the static scratch of herschel_trace_analyze_static";
     default: return "unknown error";
   }
 }
@@ -695,6 +732,31 @@ int herschel_trace_analyze(const herschel_events* ev, int64_t n, const herschel_
   int code = prepare(c, ev, n, p, out, p ? p->workspace : nullptr, p ? p->workspace_bytes : 0);
   if (code) return code;
   code = enqueue_cached(c, ev, n, p, out);
+  if (code) return code;
+  herschel_counters h;
+  if (hipMemcpyAsync(&h, out->counters, sizeof(h), hipMemcpyDeviceToHost, c.st) != hipSuccess) return HERSCHEL_EDEVICE;
+  if (hipStreamSynchronize(c.st) != hipSuccess) return HERSCHEL_EDEVICE;
+  return code_from(h, out->gap_capacity);
+}
+
+int herschel_trace_analyze_static(const herschel_events* ev, int64_t n, const herschel_params* p,
+                                  herschel_outputs* out) {
+  Ctx c;
+  int code = check_and_plan(c, ev, n, p, out);
+  if (code) return code;
+  if (layout_workspace(c, nullptr) > (size_t)HERSCHEL_STATIC_SCRATCH_BYTES) return HERSCHEL_ETOOBIG;
+  {
+    std::lock_guard<std::mutex> lock(g_enqueue_mutex);
+    void* base = static_scratch();
+    if (!base) return HERSCHEL_EDEVICE;
+    layout_workspace(c, (char*)base);
+    static bool lds_attr = false;
+    if (!lds_attr) {
+      names_set_lds_attr();
+      lds_attr = true;
+    }
+    code = enqueue_locked(c, nullptr);
+  }
   if (code) return code;
   herschel_counters h;
   if (hipMemcpyAsync(&h, out->counters, sizeof(h), hipMemcpyDeviceToHost, c.st) != hipSuccess) return HERSCHEL_EDEVICE;

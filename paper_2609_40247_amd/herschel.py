@@ -22,7 +22,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIBS = {"release": "libherschel.so", "checked": "libherschel_checked.so"}
 
 CPU_OP, LAUNCH, KERNEL = 0, 1, 2
-OK, EINVAL, EEVENT, ECAPACITY, EWORKSPACE, EDEVICE = 0, -1, -2, -3, -4, -5
+OK, EINVAL, EEVENT, ECAPACITY, EWORKSPACE, EDEVICE, ETOOBIG = 0, -1, -2, -3, -4, -5, -6
+STATIC_SCRATCH_BYTES = 64 << 20  # HERSCHEL_STATIC_SCRATCH_BYTES
 OUT_CONTAIN, OUT_OVERLAP = 0x1, 0x2
 
 _P = ctypes.c_void_p
@@ -80,6 +81,9 @@ def load(variant: str | None = None) -> ctypes.CDLL:
         lib.herschel_trace_analyze.restype = ctypes.c_int
         lib.herschel_trace_analyze.argtypes = [ctypes.POINTER(HerschelEvents), ctypes.c_int64,
                                                ctypes.POINTER(HerschelParams), ctypes.POINTER(HerschelOutputs)]
+        lib.herschel_trace_analyze_static.restype = ctypes.c_int
+        lib.herschel_trace_analyze_static.argtypes = [ctypes.POINTER(HerschelEvents), ctypes.c_int64,
+                                                      ctypes.POINTER(HerschelParams), ctypes.POINTER(HerschelOutputs)]
         lib.herschel_trace_analyze_batch.restype = ctypes.c_int
         lib.herschel_trace_analyze_batch.argtypes = [ctypes.POINTER(HerschelEvents), ctypes.POINTER(ctypes.c_int64),
                                                      ctypes.c_int32, ctypes.POINTER(HerschelParams),
@@ -108,6 +112,15 @@ def herschel_trace_analyze(events: HerschelEvents, n: int, params: HerschelParam
                            lib=None) -> int:
     lib = lib or load()
     return int(lib.herschel_trace_analyze(ctypes.byref(events), int(n), ctypes.byref(params), ctypes.byref(out)))
+
+
+def herschel_trace_analyze_static(events: HerschelEvents, n: int, params: HerschelParams, out: HerschelOutputs,
+                                  lib=None) -> int:
+    """The entry point that allocates nothing: params' workspace is ignored
+    and the library's static scratch is used instead."""
+    lib = lib or load()
+    return int(lib.herschel_trace_analyze_static(ctypes.byref(events), int(n), ctypes.byref(params),
+                                                 ctypes.byref(out)))
 
 
 def herschel_trace_analyze_batch(events: HerschelEvents, offsets: np.ndarray, params: list, outs: list,
