@@ -12,12 +12,12 @@
  *    and device kernel records located by device stream and linked to their
  *    launch by the same correlation id.
  *  - Records are admitted to the window by their start time (Section 5.2,
- *    "Session transitions": start-time filtering separates windows).
+ *    "Session transitions").
  *  - The results are the observations of Section 6.1 ("Operator execution and
  *    efficiency", "Execution progress and state") and of Figure "Key
  *    performance observations": kernel composition of each operator from
- *    call-to-kernel links, the operator span T_op from the first kernel start
- *    to the last completion, idle intervals of the GPU activity (the idle
+ *    call-to-kernel links, the operator span T_op (from the earliest start
+ *    to the latest end of the op's kernels), idle intervals of the GPU activity (the idle
  *    evidence of the case study in Section 9.1), communication overlapped
  *    with computation measured as interval coverage, and cross-process waits.
  *

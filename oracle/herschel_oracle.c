@@ -13,10 +13,10 @@
  * prose that the paper leaves open are marked READING.
  *
  *   1. validate rows                      (record schema, Section 5.2)
- *   2. correct clocks, 3. admit by start   (start-time filtering, Section 5.2)
+ *   2. correct clocks, 3. admit by start   (session transitions, Section 5.2)
  *   4-6. per-stream coverage, busy/idle, gaps (idle intervals, Section 9.1)
  *   7-8. launch/kernel join by correlation id, launch latency
- *        (call-to-kernel links, Section 6.1; "CPU submission time" and
+ *        (call-to-kernel links, Section 6.1; the submission-time and
  *        "correlation id" in panel "Operator execution and efficiency")
  *   9-12. op nesting, launch -> op, kernel -> op, inclusive T_op aggregates
  *        (kernel composition and T_op, Section 6.1; nested calls, Section 5.2)
@@ -319,8 +319,8 @@ int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p
       out->link[i] = (int32_t)l;
       out->aux[l]++;
       c->n_matched++;
-      /* 8. Launch latency: kernel start minus the launch's start (the "CPU
-       *    submission time" of the operator figure).  Signed.  Bin 0 for
+      /* 8. Launch latency: kernel start minus the launch's start (the host
+       *    submission time of the operator panel).  Signed.  Bin 0 for
        *    x <= 0, else floor(log2 x) + 1. */
       int64_t x = ts[i] - ts[l];
       if (x < 0) c->n_negative_latency++;
@@ -403,7 +403,7 @@ int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p
       }
     }
     /* 12. Inclusive per-op aggregates: every kernel counts for its op and
-     *     for each ancestor.  T_op spans the first kernel start to the last
+     *     for each ancestor.  T_op runs from the earliest kernel start to the latest
      *     kernel end (Section 6.1), unclipped. */
     for (int64_t q = 0; q < nc; ++q) {
       int64_t r = cr[q].row;

@@ -203,9 +203,24 @@ __device__ __forceinline__ bool in_range(DevState* ds, int64_t i, int64_t n) {
   return true;
 }
 
-// Bound on look-back waits: ~2^22 sleeps of 64 cycles (about 0.1 s).  A wait
-// that runs out sets DS_SPIN and gives up, so a logic error can never hang.
-constexpr uint32_t SPIN_LIMIT = 1u << 22;
+// Release-build bounds check of an index that one kernel derives from
+// another kernel's results (a scatter position): a violation sets DS_OOB and
+// the caller skips the access, so a disagreement between two kernels ends in
+// HERSCHEL_EDEVICE instead of a stray store.
+__device__ __forceinline__ bool in_bounds(DevState* ds, int64_t i, int64_t n) {
+  if ((uint64_t)i >= (uint64_t)n) {
+    set_status(ds, DS_OOB);
+    return false;
+  }
+  return true;
+}
+
+// Bound on look-back waits, in device time: s_memrealtime counts a constant
+// 100 MHz clock, and a wait that has lasted SPIN_TICKS (50 ms, thousands of
+// times a kernel's run time here) sets DS_SPIN and gives up, so a logic
+// error can never hang a queue.
+constexpr uint64_t SPIN_TICKS = 5000000;
+__device__ __forceinline__ uint64_t spin_clock() { return wall_clock64(); }
 
 // ------------------------------------------------------ decoupled look-back
 // 64-bit status words: bits 62-63 flag (0 empty, 1 aggregate, 2 prefix),
@@ -264,10 +279,12 @@ __device__ uint64_t wave_lookback(uint64_t* status, int tile, uint64_t agg, DevS
   while (true) {
     int idx = pred - lane;
     uint64_t s = idx >= 0 ? ld_agent(&status[idx]) : (LB_PRE | Op::identity());
-    uint32_t spins = 0;
+    uint64_t t0 = 0;
     while (ballot((s >> 62) == 0)) {
       if ((s >> 62) == 0) s = ld_agent(&status[idx]);
-      if (++spins > SPIN_LIMIT) {
+      const uint64_t now = spin_clock();
+      if (t0 == 0) t0 = now;
+      if (now - t0 > SPIN_TICKS) {
         give_up = true;
         break;
       }

@@ -23,6 +23,7 @@ namespace hx {
 constexpr int CT_THREADS = 256;
 constexpr int CT_ITEMS = 16;
 constexpr int CT_TILE = CT_THREADS * CT_ITEMS;  // 4096 positions = one M2 entry
+static_assert(CT_TILE == 64 * 64, "a containment tile is one entry of pyramid level 2");
 
 struct ContainArgs {
   uint64_t* k[2];
@@ -204,6 +205,8 @@ __device__ __forceinline__ int wave_lift(const uint64_t (&w)[6], int pos, uint64
 constexpr int QY_THREADS = 1024;
 constexpr int QY_GROUPS = CT_TILE / 64;                  // 64 groups per tile
 constexpr int QY_ROUNDS = QY_GROUPS / (QY_THREADS / WAVE);  // groups per wave
+static_assert(QY_GROUPS == WAVE && QY_GROUPS % (QY_THREADS / WAVE) == 0, "one lane per group of the tile");
+static_assert(CT_TILE <= 65536, "escaping positions are kept as 16-bit tile offsets");
 
 __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
   __shared__ uint64_t s_v[CT_TILE];
@@ -481,6 +484,7 @@ __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
 // ------------------------------------------------------ inclusive aggregates
 constexpr int AG_THREADS = 256;
 constexpr int AG_ITEMS = AG_TILE / AG_THREADS;
+static_assert(AG_TILE % AG_THREADS == 0 && AG_CHAIN <= AG_THREADS, "aggregate tile layout");
 
 // Adds (count, first, last, sum) to the op at sorted position q and every op
 // above it, in HBM: the part of a chain deeper than the table of ops open at

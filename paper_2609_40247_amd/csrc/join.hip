@@ -7,8 +7,8 @@
 // its launches first: a kernel's launch is the head of its run (the smallest
 // row, the sort being stable), extra launches are duplicates.  Run bounds are
 // found by galloping searches, which cost O(log run length).  The latency is
-// the kernel start minus the launch start (the "CPU submission time" of the
-// operator figure) binned by floor(log2)+1.  Dependency edges (panel
+// the kernel start minus the launch start (the host submission time of the
+// operator panel) binned by floor(log2)+1.  Dependency edges (panel
 // "Cross-process blocking") are binary searches into the same sorted runs.
 //
 // When a call has at most JT_PROCS processes and their correlation ids span

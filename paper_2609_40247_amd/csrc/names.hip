@@ -17,6 +17,7 @@ namespace hx {
 constexpr int NM_THREADS = 512;
 constexpr int NM_LDS_NAMES = 4096;  // 128 KB of LDS
 constexpr int NM_BATCH = 8;
+static_assert(NM_LDS_NAMES * 32 <= 160 * 1024, "the per-block name table must fit the LDS of a CU");
 
 struct NamesArgs {
   const uint32_t* rows;  // admitted kernels' rows (prep's own copy: the sorts reuse their buffers)

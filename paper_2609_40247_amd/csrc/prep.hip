@@ -1,8 +1,7 @@
 // Prep: one pass over the raw records (37 bytes per row).
 //
 // Validates each row (record schema of Section 5.2), moves it onto the
-// common clock, admits it by its start time (start-time filtering, Section
-// 5.2), marks rows outside the window, and compacts the admitted rows, in
+// common clock, admits it by its start time (Section 5.2, session transitions), marks rows outside the window, and compacts the admitted rows, in
 // row order, into the inputs of the three sorts:
 //   timeline    (pid, stream, ts'-W0)            kernels
 //   containment (pid, thread, ts'-W0, is_launch) ops and launches
@@ -45,6 +44,10 @@ struct PrepArgs {
 // id is loaded for every kind, the clock offsets are read from LDS).
 constexpr int PREP_BATCH = 4;
 constexpr int PREP_OFF_LDS = 512;  // processes whose clock offsets are staged in LDS
+// the three list flags of every item are packed into one 32-bit word
+static_assert(3 * PREP_ITEMS <= 32, "list flags of all items must fit the 32-bit flag word");
+static_assert(PREP_ITEMS % PREP_BATCH == 0, "items are loaded in whole batches");
+static_assert(PREP_THREADS % WAVE == 0 && 2 * JT_PROCS <= PREP_THREADS, "one thread per id-range word");
 
 // Tiles are taken by workgroup index: a tile's look-back waits only for
 // tiles of lower index, whose workgroups the dispatcher started first.

@@ -277,8 +277,12 @@ __global__ __launch_bounds__(PLAN_THREADS) void k_hist_plan(HistJobs jobs, DevSt
   const bool full = threadIdx.x < 256 && c == (uint32_t)n;
   if (__syncthreads_or(full) && threadIdx.x == 0) atomicOr(&ds->sort_trivial[jb.id], 1u << d);
   if (d < jb.first && threadIdx.x == 0) atomicOr(&ds->sort_trivial[jb.id], (1u << d) | (1u << 31));
-  const uint32_t ex = block_excl_sum<PLAN_THREADS>(threadIdx.x < 256 ? c : 0u, s_scan, nullptr);
+  uint32_t total = 0;
+  const uint32_t ex = block_excl_sum<PLAN_THREADS>(threadIdx.x < 256 ? c : 0u, s_scan, &total);
   if (threadIdx.x < 256) ds->hist[jb.id][d][bin] = ex;
+  // every key lies in one bin of a counted digit: a total other than n means
+  // the histogram and the passes disagree, and the passes must not scatter
+  if (d >= jb.first && total != (uint32_t)n && threadIdx.x == 0) set_status(ds, DS_LOGIC);
 }
 
 struct SortJob {
@@ -313,6 +317,9 @@ struct SortJobs {
 // exceeds its bound gives up with an error all the same).  No tile ticket:
 // a counter that every workgroup increments is one address, served one
 // request at a time, and it held the last tiles back by microseconds.
+static_assert(RS_ITEMS % 4 == 0, "digits are packed four to a register");
+static_assert(RS_THREADS % 256 == 0 && RS_LB_WORDS == 512, "look-back slices: 256 digits per slice, counts + window sums");
+static_assert(HIST_U % 2 == 0, "histogram keys are loaded in 16-byte pairs");
 constexpr int RS_NW = RS_THREADS / WAVE;  // waves per workgroup
 constexpr int RS_NSL = RS_THREADS / 256;  // look-back slices per digit
 constexpr int RS_LB_WIN = 16;             // positions polled per slice and round trip
@@ -344,6 +351,7 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   // the slots past the launch's sorts repeat its first).
   uint32_t nn[N_SORTS], tr[N_SORTS], nt[N_SORTS];
   const int32_t* cp[N_SORTS];
+  if (ds->status & DS_LOGIC) return;  // a digit plan did not add up: nothing is moved
   int ids[N_SORTS];
 #pragma unroll
   for (int i = 0; i < N_SORTS; ++i) {
@@ -520,7 +528,7 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
     int pred = tile - 1;  // newest position not yet counted
     int stride = 1;       // 1: own counts, WIN + 1: window sums
     bool done = false;
-    uint32_t spins = 0;
+    uint64_t t0 = 0;
     for (;;) {
       const uint32_t* src = status + (stride == 1 ? 0 : 256) + dgt;
       const int top = pred - stride * slice * LB_WIN;
@@ -566,7 +574,9 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
           }
         }
         if (res == 0) {
-          if (++spins > SPIN_LIMIT) {
+          const uint64_t now = spin_clock();
+          if (t0 == 0) t0 = now;
+          if (now - t0 > SPIN_TICKS) {
             set_status(ds, DS_SPIN);
             done = true;
           } else {
@@ -603,7 +613,7 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
     const uint64_t kk = s_key[i];
     const int dg = (int)((kk >> shift) & 255);
     const uint32_t gpos = s_glob[dg] + (i - s_local[dg]);
-    if (in_range(ds, gpos, n)) {
+    if (in_bounds(ds, gpos, n)) {
       kout[gpos] = kk;
       vout[gpos] = s_val[i];
     }

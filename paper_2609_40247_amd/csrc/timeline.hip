@@ -18,6 +18,7 @@ namespace hx {
 constexpr int UN_THREADS = 512;
 constexpr int UN_ITEMS = 8;
 constexpr int UN_TILE = UN_THREADS * UN_ITEMS;
+static_assert(UN_ITEMS % 4 == 0, "a thread's keys and rows are loaded 16 bytes at a time");
 
 struct UnionArgs {
   const uint64_t* k[2];

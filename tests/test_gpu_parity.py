@@ -30,8 +30,8 @@ def H():
     return herschel
 
 
-def check(H, cols, p, label, cap=None):
-    g = H.analyze(cols, p, gap_capacity=cap)
+def check(H, cols, p, label, cap=None, variant=None):
+    g = H.analyze(cols, p, gap_capacity=cap, variant=variant)
     o = oracle.analyze(cols, p, gap_capacity=cap)
     assert g[1]["counters"]["device_status"] == 0, f"{label}: device status {g[1]['counters']['device_status']}"
     assert_same(g, o, p, label)
@@ -438,3 +438,33 @@ def test_batch_matches_single_calls(H):
     for t, a in zip(traces, ans):
         o = oracle.analyze(t.columns(), t.params, gap_capacity=a.gap_capacity)
         assert_same((0, a.results(t.n)), o, t.params, t.label)
+
+
+# --------------------------------------------------------------- bounds-checked build
+@pytest.mark.parametrize("case", ["config0", "medium", "sparse", "config1_short"])
+def test_checked_library(H, case):
+    """The bounds-checked library (every data-dependent index tested against
+    its buffer; a violation sets a device status bit) on workloads that reach
+    every kernel: no violation, and the same results as the oracle."""
+    if case == "config0":
+        tr = synth.config0()
+        cols, p = tr.columns(), tr.params
+    elif case == "medium":
+        tr = synth.random_small(seed=9300, n_rows=60_000, window=400_000, n_procs=3, n_streams=5, n_threads=2,
+                                corr_range=20_000, edges=300)
+        cols, p = tr.columns(), tr.params
+    elif case == "sparse":
+        tr = synth.random_small(seed=9301, n_rows=20_000, window=30_000, n_procs=3, n_streams=4, n_threads=3,
+                                corr_range=3_000, edges=100)
+        cols = tr.columns()
+        cols["corr"] = cols["corr"] << 30
+        p = dict(tr.params)
+        e = p["edges"].copy()
+        e["prod_corr"] = e["prod_corr"] << 30
+        e["cons_corr"] = e["cons_corr"] << 30
+        p["edges"] = e
+    else:
+        tr = synth.config1(n_steps=40)
+        cols, p = tr.columns(), tr.params
+    check(H, cols, p, f"checked library: {case}", variant="checked")
+
