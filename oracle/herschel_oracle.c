@@ -44,7 +44,6 @@
 #define I64_MAX ((int64_t)0x7fffffffffffffffLL)
 #define I64_MIN ((int64_t)(-0x7fffffffffffffffLL - 1))
 #define ABS_LIMIT (1LL << 62)
-#define CORR_LIMIT (1LL << 48)
 
 static int64_t wrap_add(int64_t a, int64_t b) { return (int64_t)((uint64_t)a + (uint64_t)b); }
 static int64_t wrap_sub(int64_t a, int64_t b) { return (int64_t)((uint64_t)a - (uint64_t)b); }
@@ -63,7 +62,6 @@ static int row_is_valid(const hro_events *ev, int64_t i, const hro_params *p) {
     if (k == K_CPU && (ev->name[i] < 0 || ev->name[i] >= p->n_op_names)) return 0;
     if (k == K_LAUNCH && ev->name[i] < 0) return 0;
   }
-  if (k != K_CPU && (ev->corr[i] < 0 || ev->corr[i] >= CORR_LIMIT)) return 0;
   if (!in_abs(ev->ts[i]) || !in_abs(ev->te[i])) return 0;
   if (ev->te[i] < ev->ts[i]) return 0;
   return 1;
@@ -75,7 +73,7 @@ static int params_ok(int64_t n, const hro_params *p) {
   if (p->w1 - p->w0 > (1LL << 40)) return 0;
   if (p->n_procs < 1 || p->n_procs > 4096) return 0;
   if (p->n_streams < 1 || p->n_streams > 64) return 0;
-  if (p->n_threads < 1 || p->n_threads > 512) return 0;
+  if (p->n_threads < 1 || p->n_threads > 2048) return 0;
   if (p->n_names < 1 || p->n_names > (1 << 24)) return 0;
   if (p->n_op_names < 1) return 0;
   if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return 0;

@@ -13,7 +13,6 @@ import numpy as np
 
 I64_MAX = (1 << 63) - 1
 I64_MIN = -(1 << 63)
-CORR_LIMIT = 1 << 48
 ABS = 1 << 62
 
 
@@ -37,8 +36,6 @@ def _valid(k, pid, lane, name, ts, te, corr, p) -> bool:
             return False
         if k == 1 and name < 0:
             return False
-    if k != 0 and not 0 <= corr < CORR_LIMIT:
-        return False
     if not (-ABS < ts < ABS and -ABS < te < ABS):
         return False
     return te >= ts

@@ -379,7 +379,7 @@ def _t1():
 
 @pytest.mark.parametrize("field,row,value", [
     ("kind", 3, 3), ("pid", 5, 1), ("pid", 5, -1), ("lane", 12, 2), ("lane", 4, 1), ("name", 12, 3),
-    ("name", 2, 4), ("name", 6, -1), ("te", 7, 12), ("corr", 9, -1), ("corr", 9, 1 << 48),
+    ("name", 2, 4), ("name", 6, -1), ("te", 7, 12),
     ("ts", 0, -(1 << 62)), ("te", 0, 1 << 62),
 ])
 def test_invalid_row(field, row, value):
@@ -408,9 +408,62 @@ def test_cpu_op_corr_is_not_validated():
     assert code == 0
 
 
+def _remap_ids(cols, p, f):
+    """Apply the id map f (numpy, elementwise) to every launch / kernel id
+    and to both ids of every edge."""
+    c = {k: v.copy() for k, v in cols.items()}
+    jk = c["kind"] != 0
+    c["corr"][jk] = f(c["corr"][jk])
+    q = dict(p)
+    if p.get("edges") is not None and len(p["edges"]):
+        e = p["edges"].copy()
+        e["prod_corr"] = f(e["prod_corr"])
+        e["cons_corr"] = f(e["cons_corr"])
+        q["edges"] = e
+    return c, q
+
+
+ID_MAPS = {
+    "negate": lambda x: -x - 1,
+    "extremes": lambda x: np.where(x % 2 == 0, np.int64(-(1 << 63)) + x, np.int64((1 << 63) - 1) - x),
+    "spread": lambda x: (x * np.int64(1 << 40)) ^ np.int64(0x5555),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ID_MAPS))
+def test_any_int64_correlation_id(name):
+    """The correlation id is an opaque per-process identifier (any int64,
+    Section 5.2): a one-to-one map of the ids, applied to the rows and the
+    edges alike, leaves every result unchanged (the join and the edges only
+    compare ids), whether the ids come out negative, at the int64 limits or
+    spread far apart."""
+    for tr in (synth.random_small(seed=71, n_rows=400, window=3000, n_procs=3, n_streams=4, n_threads=3,
+                                  corr_range=60, edges=20),
+               synth.random_small(seed=72, n_rows=60, window=400, n_procs=2, n_streams=2, n_threads=2,
+                                  corr_range=8, edges=6)):
+        cols, p = tr.columns(), tr.params
+        ref = oracle.analyze(cols, p)
+        c2, p2 = _remap_ids(cols, p, ID_MAPS[name])
+        assert len(np.unique(c2["corr"][c2["kind"] != 0])) == len(np.unique(cols["corr"][cols["kind"] != 0]))
+        got = oracle.analyze(c2, p2)
+        assert_same(got, ref, p, f"ids {name}")
+        if tr.n <= 100:
+            bcode, b = bruteforce.analyze(c2, p2)
+            assert bcode == ref[0]
+            _bf_compare(c2, p2, ref[1], b, f"brute force, ids {name}")
+
+
+def test_thread_limit():
+    """Up to 2048 threads per process are accepted (the containment key then
+    fills 64 bits at the largest process count and window)."""
+    cols, p = _t1()
+    p["n_threads"] = 2048
+    assert oracle.analyze(cols, p)[0] == 0
+
+
 @pytest.mark.parametrize("change", [
     dict(window_end=0), dict(window_end=-5), dict(window_end=(1 << 40) + 1), dict(n_procs=0),
-    dict(n_procs=4097), dict(n_streams=65), dict(n_streams=0), dict(n_threads=513), dict(n_names=0),
+    dict(n_procs=4097), dict(n_streams=65), dict(n_streams=0), dict(n_threads=2049), dict(n_names=0),
     dict(n_op_names=0), dict(clock_offset=np.array([1 << 62])), dict(stream_class=np.array([0, 3], np.uint8)),
     dict(window_begin=-(1 << 62), window_end=-(1 << 62) + 100),
 ])
