@@ -49,7 +49,8 @@ enum {
  * EINVAL > EWORKSPACE (ETOOBIG) > EEVENT > EDEVICE > ECAPACITY. */
 enum {
   HERSCHEL_OK = 0,
-  HERSCHEL_EINVAL = -1,     /* a required pointer is NULL or a parameter is out of range */
+  HERSCHEL_EINVAL = -1,     /* a required pointer (events, params, outputs, counters) is NULL or a
+                               parameter is out of range */
   HERSCHEL_EEVENT = -2,     /* an input row is invalid; counters->first_invalid = smallest such row */
   HERSCHEL_ECAPACITY = -3,  /* more gaps than gap_capacity; the first gap_capacity are written */
   HERSCHEL_EWORKSPACE = -4, /* workspace is NULL, not 256-byte aligned, or smaller than herschel_workspace_size() */
@@ -65,12 +66,12 @@ enum {
 /* Implementation limits (checked; EINVAL when exceeded). */
 #define HERSCHEL_MAX_PROCS 4096
 #define HERSCHEL_MAX_STREAMS 64
-#define HERSCHEL_MAX_THREADS 512
+#define HERSCHEL_MAX_THREADS 2048
 #define HERSCHEL_MAX_WINDOW (1LL << 40)  /* W1 - W0 in ns (about 18 minutes) */
 #define HERSCHEL_MAX_ABS_TIME (1LL << 62) /* |ts|, |te|, |W0|, |W1|, |clock offset| must be below */
-#define HERSCHEL_CORR_LIMIT (1LL << 48)   /* LAUNCH/KERNEL corr must lie in [0, 2^48) */
 #define HERSCHEL_MAX_NAMES (1 << 24)
-#define HERSCHEL_MAX_ROWS (1LL << 30)      /* n must be below */
+#define HERSCHEL_MAX_ROWS (1LL << 30)      /* n must be below: overlap endpoints (two per kernel) are
+                                              indexed with int32, radix look-back words hold 30-bit prefixes */
 
 /* Input records as a structure of arrays, n rows, in any order (delivery
  * order).  37 bytes per row.  Row i is valid iff
@@ -78,12 +79,12 @@ enum {
  *   KERNEL: 0 <= lane < n_streams and 0 <= name < n_names,
  *   CPU_OP: 0 <= lane < n_threads and 0 <= name < n_op_names,
  *   LAUNCH: 0 <= lane < n_threads and name >= 0 (an API id),
- *   LAUNCH/KERNEL: 0 <= corr < 2^48,
- *   -2^62 < ts <= te < 2^62. */
+ *   -2^62 < ts <= te < 2^62.
+ * corr may be any int64 (an opaque per-process id, Section 5.2). */
 typedef struct {
   const int64_t *ts;   /* start, ns on the process clock */
   const int64_t *te;   /* end, ns on the process clock */
-  const int64_t *corr; /* correlation id, per process; ignored for CPU_OP */
+  const int64_t *corr; /* correlation id, per process, any value; ignored for CPU_OP */
   const int32_t *pid;  /* process index */
   const int32_t *lane; /* KERNEL: device stream; CPU_OP / LAUNCH: native thread */
   const int32_t *name; /* KERNEL: kernel-name id; CPU_OP: op-name id; LAUNCH: API id */
@@ -137,7 +138,11 @@ typedef struct {
  * KERNEL aux are -1 and the op_* arrays are not touched.
  * op_* are written at admitted CPU_OP rows only: the inclusive aggregates of
  * the kernels attributed to the op or to any of its descendants; an op with
- * none gets (0, INT64_MAX, INT64_MIN, 0).  T_op = op_last - op_first. */
+ * none gets (0, INT64_MAX, INT64_MIN, 0).  T_op = op_last - op_first.
+ * Every pointer but counters may be NULL: that output is not written (and
+ * the work only it needs is skipped), as are outputs whose HERSCHEL_OUT_*
+ * flag is clear.  The batch workload of many traces, for example, wants
+ * only the per-name aggregates, busy / idle, gaps and the latency histogram. */
 typedef struct {
   int32_t *link, *aux;               /* [n] */
   int32_t *op_nkern;                 /* [n] */

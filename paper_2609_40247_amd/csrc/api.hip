@@ -60,8 +60,7 @@ size_t layout_workspace(Ctx& c, char* base) {
   c.union_status = b.take<uint64_t>(3 * c.union_tiles);
   // key widths (also reported by herschel_sort_stats)
   sort_plan(c.sK, 0, n, c.pb + c.sb + c.wb, true);
-  sort_plan(c.sJ, 1, n, 49 + c.pb, false);  // low bits of dense ids: long runs
-  sort_plan(c.sC, 2, n, c.pb + c.tb + c.wb + 1, true);
+  sort_plan(c.sC, 1, n, c.pb + c.tb + c.wb + 1, true);
   if (c.contain) {
     c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
     c.vb_status = b.take<uint64_t>(c.vb_tiles);
@@ -77,28 +76,34 @@ size_t layout_workspace(Ctx& c, char* base) {
   // the first digit's look-back words are cleared by the histogram kernel
   // (for the tiles of the call), each later digit's by the pass before it
   c.sK.status0 = b.take<uint32_t>(c.sK.tiles_max * RS_LB_WORDS);
-  c.sJ.status0 = b.take<uint32_t>(c.sJ.tiles_max * RS_LB_WORDS);
   if (c.contain) c.sC.status0 = b.take<uint32_t>(c.sC.tiles_max * RS_LB_WORDS);
-  for (SortBufs* s : {&c.sK, &c.sJ, &c.sC})
+  for (SortBufs* s : {&c.sK, &c.sC})
     if (s != &c.sC || c.contain) s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * RS_LB_WORDS);
   // long runs of the refine pass (each has more than RF_SHORT keys)
   c.rf_cap = cdiv(n, RF_SHORT + 1) + 1;
   c.rf_list = b.take<int32_t>(2 * c.rf_cap);
   c.hist_part = b.take<uint32_t>((int64_t)N_SORTS * HIST_MAX_BLOCKS * 8 * 256);
   c.k_rows = b.take<uint32_t>(n);
-  if (c.P <= JT_PROCS) {
-    // correlation table of the join: two slots per row bound every id range it accepts
-    c.jt_cap = 2 * n;
-    c.jt_tab = b.take<uint32_t>(c.jt_cap);
-    c.jt_own = b.take<uint32_t>(c.jt_cap);
-    c.jt_multi = b.take<uint8_t>(c.jt_cap);
-    if (c.p.n_edges > 0) {
-      c.jt_kmax = b.take<int64_t>(c.jt_cap);
-      c.jt_kmin = b.take<int64_t>(c.jt_cap);
-    }
+  // the join: prep's list, the correlation table (two slots per row bound
+  // every dense id range it accepts; hashed slots use the power of two
+  // above), each entry's hashed slot and the fix-up list
+  c.jkey = b.take<uint64_t>(n);
+  c.jrow = b.take<uint32_t>(n);
+  c.jslot = b.take<uint32_t>(n);
+  c.jt_cap = 2 * n;
+  c.jt_hsize = 64;
+  while (c.jt_hsize < c.jt_cap) c.jt_hsize <<= 1;
+  c.jt_L = b.take<uint32_t>(c.jt_hsize);
+  c.jt_K = b.take<uint32_t>(c.jt_hsize);
+  c.jt_C = b.take<uint32_t>(c.jt_hsize);
+  if (c.p.n_edges > 0) {
+    c.jt_kmax = b.take<int64_t>(c.jt_hsize);
+    c.jt_kmin = b.take<int64_t>(c.jt_hsize);
   }
+  c.jt_fix_cap = n;
+  c.jt_fix = b.take<uint32_t>(3 * c.jt_fix_cap);
   // sort buffers
-  for (SortBufs* s : {&c.sK, &c.sJ, &c.sC}) {
+  for (SortBufs* s : {&c.sK, &c.sC}) {
     if (s == &c.sC && !c.contain) {
       // the containment list is still compacted by prep (ops and launches)
       s->k[0] = b.take<uint64_t>(n);
@@ -132,7 +137,11 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.ag_tiles = cdiv(n, AG_TILE);
     c.ag_chain = b.take<int32_t>(c.ag_tiles * AG_CHAIN);
     c.ag_nchain = b.take<int32_t>(c.ag_tiles);
+    // the per-row links stand in for NULL link / aux outputs: containment reads them back
+    c.link_ws = b.take<int32_t>(n);
+    c.aux_ws = b.take<int32_t>(n);
   }
+  c.busy_ws = b.take<int64_t>((int64_t)c.P * c.S);
   c.name_blocks = names_block_count(n, c.NN);
   if (c.NN <= names_lds_limit()) c.name_part = b.take<uint64_t>((int64_t)c.name_blocks * c.NN * 4);
   return b.off;
@@ -172,7 +181,7 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
     if (threadIdx.x == 0) a.ds->first_invalid = I64MAX;
     int64_t* cz = (int64_t*)a.cnt;
     for (int i = threadIdx.x; i < (int)(sizeof(herschel_counters) / 8); i += 256) cz[i] = 0;
-    if (threadIdx.x < 64) a.lat_hist[threadIdx.x] = 0;
+    if (a.lat_hist && threadIdx.x < 64) a.lat_hist[threadIdx.x] = 0;
     bool bad = false;
     if (a.off)
       for (int q = threadIdx.x; q < a.P; q += 256)
@@ -183,19 +192,23 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
   }
   for (int64_t i = tid; i < a.nps; i += nth) a.busy[i] = 0;
   if (a.overlap) {
-    for (int64_t i = tid; i < (int64_t)a.nps * a.S; i += nth) a.pair[i] = 0;
-    for (int64_t i = tid; i < (int64_t)a.P * 3; i += nth) a.class_busy[i] = 0;
-    for (int64_t i = tid; i < (int64_t)a.P * 9; i += nth) a.class_overlap[i] = 0;
-    for (int64_t i = tid; i < a.P; i += nth) a.any_busy[i] = 0;
+    if (a.pair)
+      for (int64_t i = tid; i < (int64_t)a.nps * a.S; i += nth) a.pair[i] = 0;
+    if (a.class_busy)
+      for (int64_t i = tid; i < (int64_t)a.P * 3; i += nth) a.class_busy[i] = 0;
+    if (a.class_overlap)
+      for (int64_t i = tid; i < (int64_t)a.P * 9; i += nth) a.class_overlap[i] = 0;
+    if (a.any_busy)
+      for (int64_t i = tid; i < a.P; i += nth) a.any_busy[i] = 0;
   }
   // the name outputs start as the identities: the per-block tables (or,
   // with many names, the kernels themselves) are combined into them with
   // atomics
   for (int64_t i = tid; i < a.NN; i += nth) {
-    a.name_count[i] = 0;
-    a.name_sum[i] = 0;
-    a.name_min[i] = I64MAX;
-    a.name_max[i] = I64MIN;
+    if (a.name_count) a.name_count[i] = 0;
+    if (a.name_sum) a.name_sum[i] = 0;
+    if (a.name_min) a.name_min[i] = I64MAX;
+    if (a.name_max) a.name_max[i] = I64MIN;
   }
 }
 
@@ -205,7 +218,7 @@ void launch_init(Ctx& c) {
   a.zero = (uint4*)c.zero_begin;
   a.zero_n = (int64_t)(c.zero_bytes / 16);
   a.cnt = c.o.counters;
-  a.busy = c.o.busy;
+  a.busy = c.o.busy ? c.o.busy : c.busy_ws;
   a.nps = c.P * c.S;
   a.lat_hist = c.o.lat_hist;
   a.overlap = c.overlap;
@@ -227,42 +240,43 @@ void launch_init(Ctx& c) {
   hipLaunchKernelGGL(k_init, dim3(std::max(grid, 1)), dim3(256), 0, c.st, a);
 }
 
-// Without containment, admitted ops and launches have no op links.
+// Without containment, admitted ops and launches have no op links (either
+// output may be NULL).
 __global__ __launch_bounds__(256) void k_nocontain(const uint64_t* keys, const uint32_t* rows, DevState* ds,
                                                     int32_t* link, int32_t* aux) {
   const int64_t n = ds->nCL;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
     const uint32_t r = rows[i];
-    link[r] = -1;
-    if ((keys[i] & 1) == 0) aux[r] = -1;
+    if (link) link[r] = -1;
+    if (aux && (keys[i] & 1) == 0) aux[r] = -1;
   }
 }
 
-__global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counters* cnt, int64_t* lat_hist, int64_t* busy,
-                                                  int64_t* idle, int nps, int64_t W) {
-  for (int i = threadIdx.x; i < nps; i += 256) idle[i] = W - busy[i];
+__global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counters* cnt, int64_t* lat_hist,
+                                                  const int64_t* busy, int64_t* idle, int nps, int64_t W) {
+  if (idle)
+    for (int i = threadIdx.x; i < nps; i += 256) idle[i] = W - busy[i];
   // join counts and latency bins from their accumulator copies
   if (threadIdx.x < JC_N + 64) {
     unsigned long long v = 0;
     for (int k = 0; k < JOIN_COPIES; ++k) v += ds->join_acc[k][threadIdx.x];
     if (threadIdx.x >= JC_N) {
-      if (v) lat_hist[threadIdx.x - JC_N] += (int64_t)v;
+      if (v && lat_hist) lat_hist[threadIdx.x - JC_N] += (int64_t)v;
     } else {
       int64_t* dst = nullptr;
+      int64_t val = (int64_t)v;
       switch (threadIdx.x) {
         case JC_MATCHED: dst = &cnt->n_matched; break;
         case JC_UNM_K: dst = &cnt->n_unmatched_kernels; break;
-        case JC_UNM_L: dst = &cnt->n_unmatched_launches; break;
         case JC_DUP: dst = &cnt->n_dup_launch_corr; break;
         case JC_NEG: dst = &cnt->n_negative_latency; break;
         case JC_UNATTR: dst = &cnt->n_unattributed_kernels; break;
-        default: dst = &cnt->n_unmatched_launches; break;  // JC_MLAUNCH
+        default:  // JC_MLAUNCH: the unmatched launches are the others
+          dst = &cnt->n_unmatched_launches;
+          val = cnt->n_admitted[HERSCHEL_LAUNCH] - val;
+          break;
       }
-      // two threads may add to one counter (the table path derives the
-      // unmatched launches from the launches with a kernel)
-      int64_t add = (int64_t)v;
-      if (threadIdx.x == JC_MLAUNCH) add = ds->join_direct ? cnt->n_admitted[HERSCHEL_LAUNCH] - (int64_t)v : 0;
-      if (add) atomicAdd((unsigned long long*)dst, (unsigned long long)add);
+      *dst = val;
     }
   }
   if (threadIdx.x == 0) {
@@ -272,8 +286,8 @@ __global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counter
 }
 
 void launch_finalize(Ctx& c) {
-  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, c.st, c.ds, c.o.counters, c.o.lat_hist, c.o.busy, c.o.idle,
-                     c.P * c.S, c.W);
+  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, c.st, c.ds, c.o.counters, c.o.lat_hist,
+                     c.o.busy ? c.o.busy : c.busy_ws, c.o.idle, c.P * c.S, c.W);
 }
 
 // ------------------------------------------------------------- the call
@@ -295,17 +309,9 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return HERSCHEL_EINVAL;
   if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP)) return HERSCHEL_EINVAL;
   const bool contain = (p->flags & HERSCHEL_OUT_CONTAIN) != 0, overlap = (p->flags & HERSCHEL_OUT_OVERLAP) != 0;
-  if (!out->counters || !out->link || !out->aux || !out->busy || !out->idle || !out->name_count ||
-      !out->name_sum || !out->name_min || !out->name_max || !out->lat_hist)
-    return HERSCHEL_EINVAL;
+  // every output but the counters may be NULL: that output is skipped
+  if (!out->counters) return HERSCHEL_EINVAL;
   if (out->gap_capacity < 0) return HERSCHEL_EINVAL;
-  if (out->gap_capacity > 0 &&
-      (!out->gap_pid || !out->gap_stream || !out->gap_begin || !out->gap_end || !out->gap_flags))
-    return HERSCHEL_EINVAL;
-  if (contain && (!out->op_nkern || !out->op_first || !out->op_last || !out->op_ksum)) return HERSCHEL_EINVAL;
-  if (overlap && (!out->pair_overlap || !out->class_busy || !out->class_overlap || !out->any_busy))
-    return HERSCHEL_EINVAL;
-  if (p->n_edges > 0 && (!out->edge_wait || !out->edge_status)) return HERSCHEL_EINVAL;
 
   c.st = (hipStream_t)p->hip_stream;
   c.ev = *ev;
@@ -401,19 +407,16 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   launch_prep(c);
   stage_end(c, HERSCHEL_STAGE_PREP);
 
-  // The three sorts share their digit passes, pass p of a sort being its
-  // digit first + p (a sort whose digit is skipped has no tiles in the
-  // launch, as the join sort has none when the correlation table is used).
-  // The timeline and containment sorts leave their lowest digit to the
-  // refine pass; the join sort's passes beyond theirs run on the join
-  // stream.  Nothing else runs beside the sorts: a large grid on another
+  // The timeline and containment sorts share their digit passes, pass p of
+  // a sort being its digit first + p (a sort whose digit is skipped has no
+  // tiles in the launch); both leave their lowest digit to the refine pass.
+  // The histogram launch also takes the correlation table's plan and empties
+  // the table.  Nothing else runs beside the sorts: a large grid on another
   // stream would take the CUs first and hold up the passes, which every
   // later stage waits for.
-  const int ks = c.contain ? 3 : 2;
-  SortBufs* ss[3] = {&c.sK, &c.sC, &c.sJ};
-  const int32_t* cc[3] = {&c.ds->nK, &c.ds->nCL, &c.ds->nJ};
-  ss[ks - 1] = &c.sJ;
-  cc[ks - 1] = &c.ds->nJ;
+  const int ks = c.contain ? 2 : 1;
+  SortBufs* ss[2] = {&c.sK, &c.sC};
+  const int32_t* cc[2] = {&c.ds->nK, &c.ds->nCL};
   int p_shared = c.sK.nd - c.sK.first;
   if (c.contain) p_shared = std::max(p_shared, c.sC.nd - c.sC.first);
   stage_begin(c, HERSCHEL_STAGE_HIST);
@@ -435,19 +438,16 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     rec(3, s0);  // each launch's op is known
     launch_depth(c);
     stage_end(c, HERSCHEL_STAGE_CONTAIN);
-  } else {
+  } else if (c.o.link || c.o.aux) {
     const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.n, 256 * 8), 1), 2048);
     hipLaunchKernelGGL(k_nocontain, dim3(grid), dim3(256), 0, c.st, c.sC.k[0], c.sC.v[0], c.ds, c.o.link, c.o.aux);
   }
 
-  // chain 2: the join by the correlation table, or else by the rest of the
-  // join sort and the sort-merge join; then the dependency waits
+  // chain 2: the join by the correlation table, then the dependency waits
   c.st = lib1;
   wait(c.st, 0);
   stage_begin(c, HERSCHEL_STAGE_JOIN);
   launch_join_table(c);
-  launch_sort_multi(c, &ss[ks - 1], &cc[ks - 1], 1, p_shared, c.sJ.nd - c.sJ.first);
-  launch_join(c);
   stage_end(c, HERSCHEL_STAGE_JOIN);
   stage_begin(c, HERSCHEL_STAGE_EDGES);
   launch_edges(c);
@@ -671,19 +671,23 @@ int herschel_sort_stats(const herschel_params* p, int32_t* out) {
   if (hipStreamSynchronize((hipStream_t)p->hip_stream) != hipSuccess ||
       hipMemcpy(&ds, p->workspace, sizeof(DevState), hipMemcpyDeviceToHost) != hipSuccess)
     return HERSCHEL_EDEVICE;
-  // digit passes per sort, as layout_workspace plans them
+  // digit passes per sort, as layout_workspace plans them; the join has no
+  // sort (the correlation table serves it), so its entries are zero
   const int pb = bits_host((uint64_t)(p->n_procs - 1)), sb = bits_host((uint64_t)(p->n_streams - 1));
   const int tb = bits_host((uint64_t)(p->n_threads - 1));
   const int wb = bits_host((uint64_t)(p->window_end - p->window_begin - 1));
-  const int key_bits[N_SORTS] = {pb + sb + wb, 49 + pb, pb + tb + wb + 1};  // as layout_workspace plans them
-  const bool refine[N_SORTS] = {true, false, true};
-  const int32_t counts[N_SORTS] = {ds.nK, ds.nJ, ds.nCL};
+  const int key_bits[N_SORTS] = {pb + sb + wb, pb + tb + wb + 1};
+  const int32_t counts[N_SORTS] = {ds.nK, ds.nCL};
+  const int slot_of[N_SORTS] = {0, 2};  // timeline, containment in the reported order
+  for (int i = 0; i < 3; ++i) out[i] = 0;
+  for (int i = 3; i < 9; ++i) out[i] = 0;
   for (int i = 0; i < N_SORTS; ++i) {
     int nd, first, sh1;
-    sort_digits(key_bits[i], refine[i], &nd, &first, &sh1);
-    out[3 * i + 0] = counts[i];
-    out[3 * i + 1] = (int32_t)ds.sort_trivial[i];
-    out[3 * i + 2] = nd;
+    sort_digits(key_bits[i], true, &nd, &first, &sh1);
+    const int o = 3 * slot_of[i];
+    out[o + 0] = counts[i];
+    out[o + 1] = (int32_t)ds.sort_trivial[i];
+    out[o + 2] = nd;
   }
   return HERSCHEL_OK;
 }
@@ -716,6 +720,14 @@ int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) 
   return HERSCHEL_OK;
 }
 
+// Containment reads the per-row links back (each launch's op, each op's
+// depth): NULL link / aux outputs are then served by workspace arrays.
+static void redirect_outputs(Ctx& c) {
+  if (!c.contain) return;
+  if (!c.o.link) c.o.link = c.link_ws;
+  if (!c.o.aux) c.o.aux = c.aux_ws;
+}
+
 static int prepare(Ctx& c, const herschel_events* ev, int64_t n, const herschel_params* p, const herschel_outputs* out,
                    void* ws, size_t ws_bytes) {
   int code = check_and_plan(c, ev, n, p, out);
@@ -724,6 +736,7 @@ static int prepare(Ctx& c, const herschel_events* ev, int64_t n, const herschel_
   // the layout aligns every buffer to 256 bytes from the base (16-byte loads)
   if (!ws || ((uintptr_t)ws & 255) != 0 || ws_bytes < need) return HERSCHEL_EWORKSPACE;
   layout_workspace(c, (char*)ws);
+  redirect_outputs(c);
   return HERSCHEL_OK;
 }
 
@@ -750,6 +763,7 @@ int herschel_trace_analyze_static(const herschel_events* ev, int64_t n, const he
     void* base = static_scratch();
     if (!base) return HERSCHEL_EDEVICE;
     layout_workspace(c, (char*)base);
+    redirect_outputs(c);
     static bool lds_attr = false;
     if (!lds_attr) {
       names_set_lds_attr();

@@ -38,14 +38,21 @@ enum : int {
   N_TICKETS = 1
 };
 
-constexpr int N_SORTS = 3;  // 0 timeline, 1 join, 2 containment
-// join counters; the correlation table path keeps JC_MLAUNCH (launches with a
-// kernel) instead of JC_UNM_L and derives the unmatched launches at the end
-enum { JC_MATCHED, JC_UNM_K, JC_UNM_L, JC_DUP, JC_NEG, JC_UNATTR, JC_MLAUNCH, JC_N };
+constexpr int N_SORTS = 2;  // 0 timeline, 1 containment
+// join counters (JC_MLAUNCH: launches with at least one kernel; the
+// unmatched launches are the admitted ones without)
+enum { JC_MATCHED, JC_UNM_K, JC_DUP, JC_NEG, JC_UNATTR, JC_MLAUNCH, JC_N };
 constexpr int JOIN_COPIES = 16;
-// The join uses a table indexed by correlation id when the call has at most
-// JT_PROCS processes and their id ranges fit the table (2 slots per row).
+// The correlation table takes dense slots (process base + id - smallest id)
+// when the call has at most JT_PROCS processes and their id ranges fit two
+// slots per row; otherwise hashed slots.
 constexpr int JT_PROCS = 64;
+// Join keys: (pid << 52) | ((corr mod 2^51) << 1) | is_kernel.  Dense slots
+// subtract ids modulo 2^51, exact since a dense range is far below 2^51.
+constexpr int JK_PID_SHIFT = 52;
+constexpr uint64_t JK_CORR_MASK = (1ull << 51) - 1;
+constexpr uint32_t JT_EMPTY = ~0u;
+constexpr uint64_t SIGN64 = 1ull << 63;
 
 // Per-call device state, zeroed by the init kernel.
 struct DevState {
@@ -61,11 +68,12 @@ struct DevState {
   int64_t n_gaps;
   uint32_t sort_trivial[N_SORTS];  // bit d: digit d moves no data (every key agrees on it, or it is
                                    // left to the refine pass: then bit 31 is set too)
-  uint32_t join_direct;            // 1: the correlation table replaces the join sort
-  uint32_t pad1;
-  int64_t jt_slots;                // table slots in use
-  uint64_t jt_key_lo[JT_PROCS];    // bitwise complement of each process's smallest join key (0: none)
-  uint64_t jt_key_hi[JT_PROCS];    // each process's largest join key
+  uint32_t join_direct;            // 1: dense correlation slots, 0: hashed slots
+  uint32_t jt_nfix;                // entries of the join's fix-up list
+  int64_t jt_slots;                // table slots in use (dense: the ids' ranges; hashed: the table)
+  uint64_t jt_present;             // bit p: process p has an admitted launch or kernel
+  uint64_t jt_lo[JT_PROCS];        // per process: max of ~(corr ^ 2^63), the smallest id
+  uint64_t jt_hi[JT_PROCS];        // per process: max of corr ^ 2^63, the largest id
   int64_t jt_cmin[JT_PROCS];       // smallest correlation id of each process
   int64_t jt_base[JT_PROCS];       // first table slot of each process
   // join counts (JC_* order) and latency bins, in copies summed at the end
@@ -96,39 +104,60 @@ __device__ __forceinline__ T shfl_down(T v, unsigned d) { return __shfl_down(v, 
 template <class T>
 __device__ __forceinline__ T shfl_xor(T v, int m) { return __shfl_xor(v, m, WAVE); }
 
-// The correlation-table plan, by one wave (lane p is process p of P <=
-// JT_PROCS): the table replaces the join sort when the processes' id ranges,
-// from prep's per-process smallest and largest join keys, fit `cap` slots
-// together; process p's ids then start at slot jt_base[p].  With `write` the
+// The correlation-table plan, by one wave (lane p is process p): dense
+// slots when the call has at most JT_PROCS processes (P > 0 here) and their
+// id ranges, from prep's per-process smallest and largest ids, fit `cap`
+// slots together (process p's ids then start at slot jt_base[p]); hashed
+// slots over the whole table of `hsize` slots otherwise.  With `write` the
 // lanes store the plan (one wave of the call does); every caller gets the
-// decision.
-__device__ __forceinline__ bool jt_plan_wave(DevState* ds, int P, int64_t cap, bool write) {
+// decision and the number of slots in use.
+__device__ __forceinline__ bool jt_plan_wave(DevState* ds, int P, int64_t cap, int64_t hsize, bool write,
+                                             int64_t* slots) {
   const int p = threadIdx.x & (WAVE - 1);
-  const uint64_t lo = p < P ? ds->jt_key_lo[p] : 0ull, hi = p < P ? ds->jt_key_hi[p] : 0ull;
-  constexpr uint64_t CORR_MASK = (1ull << 48) - 1;
-  const bool present = lo != 0;  // lo holds ~(smallest key); keys never reach ~0
-  const int64_t cmin = present ? (int64_t)((~lo >> 1) & CORR_MASK) : 0;
-  const int64_t cmax = present ? (int64_t)((hi >> 1) & CORR_MASK) : -1;
-  // ranges beyond the capacity saturate, so the sum cannot overflow
-  int64_t range = cmax - cmin + 1;
-  range = range > cap ? cap + 1 : range;
+  const bool present = P > 0 && p < P && ((ds->jt_present >> p) & 1);
+  const uint64_t ulo = present ? ~ds->jt_lo[p] : 0ull, uhi = present ? ds->jt_hi[p] : 0ull;
+  const int64_t cmin = (int64_t)(ulo ^ SIGN64);
+  // largest - smallest id, exact in unsigned arithmetic; ranges beyond the
+  // capacity saturate, so the sum cannot overflow
+  const uint64_t span = uhi - ulo;
+  const int64_t range = !present ? 0 : span >= (uint64_t)cap ? cap + 1 : (int64_t)span + 1;
   int64_t inc = range;
   for (int d = 1; d < WAVE; d <<= 1) {
     const int64_t o = (int64_t)__shfl_up((uint64_t)inc, d, WAVE);
     if (p >= d) inc += o;
   }
   const int64_t total = (int64_t)__shfl((uint64_t)inc, WAVE - 1, WAVE);
-  const bool direct = total <= cap;
+  const bool direct = P > 0 && total <= cap;
+  *slots = direct ? total : hsize;
   if (write) {
-    ds->jt_cmin[p] = cmin;
+    ds->jt_cmin[p] = present ? cmin : 0;
     ds->jt_base[p] = inc - range;
     if (p == 0) {
       ds->join_direct = direct ? 1u : 0u;
-      ds->jt_slots = direct ? total : 0;
-      if (direct) ds->sort_trivial[1] = 0xFFu;  // no join sort: every digit pass skipped
+      ds->jt_slots = direct ? total : hsize;
     }
   }
   return direct;
+}
+
+// Dense slot of a join key (the plan chose dense slots).
+__device__ __forceinline__ int64_t jt_dense_slot(const DevState* ds, uint64_t key) {
+  const int p = (int)(key >> JK_PID_SHIFT);
+  const uint64_t rel = (((key >> 1) & JK_CORR_MASK) - ((uint64_t)ds->jt_cmin[p] & JK_CORR_MASK)) & JK_CORR_MASK;
+  return ds->jt_base[p] + (int64_t)rel;
+}
+
+// First probe of a join key's hashed slot: the SplitMix64 finalizer (Steele,
+// Lea and Flood, "Fast splittable pseudorandom number generators", 2014) of
+// the key without its kind bit.
+__device__ __forceinline__ uint64_t jt_hash(uint64_t key) {
+  uint64_t x = key >> 1;
+  x ^= x >> 30;
+  x *= 0xbf58476d1ce4e5b9ull;
+  x ^= x >> 27;
+  x *= 0x94d049bb133111ebull;
+  x ^= x >> 31;
+  return x;
 }
 
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {

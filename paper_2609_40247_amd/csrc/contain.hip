@@ -67,6 +67,23 @@ __device__ __forceinline__ int64_t key_rel(const ContainArgs& a, uint64_t key) {
 }
 __device__ __forceinline__ bool key_is_op(uint64_t key) { return (key & 1) == 0; }
 
+// Per-op outputs (each may be NULL): a plain store of whole aggregates, or
+// atomic combination into ones that start at the identities.
+__device__ __forceinline__ void op_store(const ContainArgs& a, uint32_t rr, int32_t nk, int64_t f, int64_t l,
+                                         int64_t sm) {
+  if (a.op_nkern) a.op_nkern[rr] = nk;
+  if (a.op_first) a.op_first[rr] = f;
+  if (a.op_last) a.op_last[rr] = l;
+  if (a.op_ksum) a.op_ksum[rr] = sm;
+}
+__device__ __forceinline__ void op_combine(const ContainArgs& a, uint32_t rr, uint32_t nk, int64_t f, int64_t l,
+                                           uint64_t sm) {
+  if (a.op_nkern) atomicAdd(&a.op_nkern[rr], (int32_t)nk);
+  if (a.op_first) atomicMin((long long*)&a.op_first[rr], (long long)f);
+  if (a.op_last) atomicMax((long long*)&a.op_last[rr], (long long)l);
+  if (a.op_ksum) atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)sm);
+}
+
 // ------------------------------------------------------- encoding, pyramid
 // V and the first pyramid levels of one 4096-position tile: 16 waves, each
 // wave four 64-position groups (one M1 entry each), every round of loads
@@ -82,7 +99,7 @@ __global__ __launch_bounds__(VB_THREADS) void k_vbuild(ContainArgs a) {
   __shared__ uint64_t s_tmax;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int64_t n = a.ds->nCL;
-  const int par = (int)a.ds->sort_parity[2];
+  const int par = (int)a.ds->sort_parity[1];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
   if ((int64_t)blockIdx.x * CT_TILE >= n) return;
@@ -219,7 +236,7 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
   __shared__ int s_nesc;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int64_t n = a.ds->nCL;
-  const int par = (int)a.ds->sort_parity[2];
+  const int par = (int)a.ds->sort_parity[1];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
   const int64_t tile = blockIdx.x;
@@ -385,7 +402,7 @@ __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
   if (n == 0) return;
   if (threadIdx.x == 0) s_imp = 0;
   __syncthreads();
-  const int par = (int)a.ds->sort_parity[2];
+  const int par = (int)a.ds->sort_parity[1];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
   const int64_t p0 = (int64_t)blockIdx.x * 256 * DP_ITEMS + threadIdx.x;
@@ -455,10 +472,7 @@ __global__ __launch_bounds__(256) void k_depth(ContainArgs a) {
   const int64_t ntl = cdiv(n, AG_TILE);
   auto init_op = [&](int64_t q) {
     const uint32_t rr = vals[q];
-    a.op_nkern[rr] = 0;
-    a.op_first[rr] = I64MAX;
-    a.op_last[rr] = I64MIN;
-    a.op_ksum[rr] = 0;
+    op_store(a, rr, 0, I64MAX, I64MIN, 0);
   };
   if (b < ntl) {
     int nc = 0;
@@ -490,13 +504,10 @@ static_assert(AG_TILE % AG_THREADS == 0 && AG_CHAIN <= AG_THREADS, "aggregate ti
 // above it, in HBM: the part of a chain deeper than the table of ops open at
 // a tile start.
 __device__ void agg_add_global(const ContainArgs& a, int64_t q, uint32_t nk, int64_t f, int64_t l, uint64_t sm) {
-  const uint32_t* vals = a.v[(int)a.ds->sort_parity[2]];
+  const uint32_t* vals = a.v[(int)a.ds->sort_parity[1]];
   for (int64_t r = q; r >= 0; r = a.par[r]) {
     const uint32_t rr = vals[r];
-    atomicAdd(&a.op_nkern[rr], (int32_t)nk);
-    atomicMin((long long*)&a.op_first[rr], (long long)f);
-    atomicMax((long long*)&a.op_last[rr], (long long)l);
-    atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)sm);
+    op_combine(a, rr, nk, f, l, sm);
   }
 }
 
@@ -523,7 +534,7 @@ __global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
   __shared__ int s_dmin, s_dmax, s_last_op;
   const int tid = threadIdx.x, lane = lane_id();
   const int64_t n = a.ds->nCL;
-  const int par = (int)a.ds->sort_parity[2];
+  const int par = (int)a.ds->sort_parity[1];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
   const int64_t base = (int64_t)blockIdx.x * AG_TILE;
@@ -667,10 +678,7 @@ __global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
     if (nc > AG_CHAIN && c_nk[AG_CHAIN - 1]) {
       for (int64_t r = a.par[s_chain[AG_CHAIN - 1]]; r >= 0; r = a.par[r]) {
         const uint32_t rr = vals[r];
-        atomicAdd(&a.op_nkern[rr], (int32_t)c_nk[AG_CHAIN - 1]);
-        atomicMin((long long*)&a.op_first[rr], (long long)c_first[AG_CHAIN - 1]);
-        atomicMax((long long*)&a.op_last[rr], (long long)c_last[AG_CHAIN - 1]);
-        atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)c_sum[AG_CHAIN - 1]);
+        op_combine(a, rr, c_nk[AG_CHAIN - 1], c_first[AG_CHAIN - 1], c_last[AG_CHAIN - 1], c_sum[AG_CHAIN - 1]);
       }
     }
   }
@@ -682,24 +690,15 @@ __global__ __launch_bounds__(AG_THREADS) void k_opagg(ContainArgs a) {
     const uint32_t rr = row[u];
     if (s_open[i]) {
       if (s_nk[i]) {
-        atomicAdd(&a.op_nkern[rr], (int32_t)s_nk[i]);
-        atomicMin((long long*)&a.op_first[rr], (long long)s_first[i]);
-        atomicMax((long long*)&a.op_last[rr], (long long)s_last[i]);
-        atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)s_sum[i]);
+        op_combine(a, rr, s_nk[i], s_first[i], s_last[i], s_sum[i]);
       }
     } else {
-      a.op_nkern[rr] = (int32_t)s_nk[i];
-      a.op_first[rr] = s_first[i];
-      a.op_last[rr] = s_last[i];
-      a.op_ksum[rr] = (int64_t)s_sum[i];
+      op_store(a, rr, (int32_t)s_nk[i], s_first[i], s_last[i], (int64_t)s_sum[i]);
     }
   }
   if (tid < kn && c_nk[tid]) {
     const uint32_t rr = vals[s_chain[tid]];
-    atomicAdd(&a.op_nkern[rr], (int32_t)c_nk[tid]);
-    atomicMin((long long*)&a.op_first[rr], (long long)c_first[tid]);
-    atomicMax((long long*)&a.op_last[rr], (long long)c_last[tid]);
-    atomicAdd((unsigned long long*)&a.op_ksum[rr], (unsigned long long)c_sum[tid]);
+    op_combine(a, rr, c_nk[tid], c_first[tid], c_last[tid], c_sum[tid]);
   }
 }
 

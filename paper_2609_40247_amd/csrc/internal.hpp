@@ -66,15 +66,24 @@ struct Ctx {
   uint64_t* vb_status = nullptr;     // [vb_tiles]
   int64_t vb_tiles = 0;
   int64_t* corr_min = nullptr;       // [P]
-  SortBufs sK, sJ, sC;               // timeline, join, containment
+  SortBufs sK, sC;                   // timeline, containment
   uint32_t* k_rows = nullptr;        // [n] admitted kernels' rows in row order (per-name tables)
   uint32_t* hist_part = nullptr;     // [N_SORTS][HIST_MAX_BLOCKS][8 * 256] per-workgroup digit counts
-  uint32_t* jt_tab = nullptr;        // [jt_cap] smallest launch row per correlation slot
-  uint32_t* jt_own = nullptr;        // [jt_cap] one kernel row per slot
-  uint8_t* jt_multi = nullptr;       // [jt_cap] 1: the slot has several kernels
-  int64_t* jt_kmax = nullptr;        // [jt_cap] latest kernel end per slot (edges only)
-  int64_t* jt_kmin = nullptr;        // [jt_cap] earliest kernel start per slot (edges only)
-  int64_t jt_cap = 0;
+  uint64_t* jkey = nullptr;          // [n] join list (prep): admitted launches and kernels in row order
+  uint32_t* jrow = nullptr;          // [n] their rows
+  uint32_t* jslot = nullptr;         // [n] their hashed slots
+  uint32_t* jt_L = nullptr;          // [jt_hsize] launch word per correlation slot
+  uint32_t* jt_K = nullptr;          // [jt_hsize] kernel word per slot
+  uint32_t* jt_C = nullptr;          // [jt_hsize] claiming row per slot (hashed slots)
+  int64_t* jt_kmax = nullptr;        // [jt_hsize] latest kernel end per slot (edges only)
+  int64_t* jt_kmin = nullptr;        // [jt_hsize] earliest kernel start per slot (edges only)
+  uint32_t* jt_fix = nullptr;        // [jt_fix_cap][3] the join's fix-up list
+  int64_t jt_fix_cap = 0;
+  int64_t jt_cap = 0;                // most dense slots (two per row)
+  int64_t jt_hsize = 0;              // hashed table size: a power of two of at least jt_cap
+  int64_t* busy_ws = nullptr;        // [P * S] busy time when the busy output is NULL
+  int32_t* link_ws = nullptr;        // [n] link when the output is NULL (containment reads it)
+  int32_t* aux_ws = nullptr;         // [n] aux likewise
   uint64_t* ev_keys = nullptr;       // [ev_cap] coverage run endpoints, grouped by (pid, stream)
   int64_t ev_cap = 0;
   int32_t* seg_off = nullptr;        // [P * S + 1] first endpoint of each (pid, stream)
@@ -115,7 +124,6 @@ void launch_contain(Ctx& c);
 void launch_depth(Ctx& c);
 void launch_opagg(Ctx& c);
 void launch_names_reduce(Ctx& c);
-void launch_join(Ctx& c);
 void launch_join_table(Ctx& c);
 void launch_edges(Ctx& c);
 void launch_finalize(Ctx& c);

@@ -2,40 +2,52 @@
 //
 // The correlation id associates a submission with its device activity
 // (Section 5.2); kernel composition is recovered from these call-to-kernel
-// links (Section 6.1), and a graph launch may own many kernels.  Launches and
-// kernels are sorted by (pid, corr, is_kernel), so each id is one run with
-// its launches first: a kernel's launch is the head of its run (the smallest
-// row, the sort being stable), extra launches are duplicates.  Run bounds are
-// found by galloping searches, which cost O(log run length).  The latency is
-// the kernel start minus the launch start (the host submission time of the
-// operator panel) binned by floor(log2)+1.  Dependency edges (panel
-// "Cross-process blocking") are binary searches into the same sorted runs.
+// links (Section 6.1), and a graph launch may own many kernels.  A kernel
+// joins the admitted launch with its (pid, corr) and the smallest row;
+// further launches with that id are duplicates.  The latency is the kernel
+// start minus the launch start (the host submission time of the operator
+// panel) binned by floor(log2)+1.  Dependency edges (panel "Cross-process
+// blocking") look their two ids up in the same table.
 //
-// When a call has at most JT_PROCS processes and their correlation ids span
-// at most two slots per row (ids are dense per process: every API call takes
-// the next one), a table indexed by (process, id) replaces the sort.  Bulk
-// global atomics are slow on this GPU, so the table is built with plain
-// stores and checked: launches store their rows (one writer wins), those
-// that lost are the duplicates and put the smallest row in (atomics, rare);
-// kernels store their rows in an owner word, and only kernels sharing a slot
-// (graph replays) add to their launch's counts with atomics.  The decision
-// is taken on the device right after prep, which finds each process's id
-// range; the join sort's histogram and digit passes are then skipped.
+// The join is a table of (pid, corr) slots, each with a launch word and a
+// kernel word, built with plain stores: bulk global atomics are slow on this
+// GPU, and in real traces nearly every id has one launch and one kernel.
+// Slots are dense (process base + id - the process's smallest id) when the
+// call has at most JT_PROCS processes whose ids span at most two slots per
+// row, as ids that every API call takes in turn do; otherwise hashed, by
+// linear probing over a power-of-two table in which the first row of a key
+// claims the slot with a compare-and-swap.  The table is emptied by the
+// histogram kernel, which takes the plan.
+//
+//   store:   every launch writes its row to its slot's launch word, every
+//            kernel to the kernel word (one writer of each wins);
+//   resolve: a launch that won its word is the slot's launch for now; it
+//            joins the kernel that won the kernel word (the usual case: one
+//            launch, one kernel, all plain stores).  A launch that lost is a
+//            duplicate, a kernel that lost shares its slot with others: both
+//            go to a short fix-up list;
+//   dups:    duplicates put the smallest row into the launch word (atomics);
+//   fix:     a duplicate that ends up in the word takes the slot's kernel
+//            over from the launch that held it, and every kernel of the
+//            list joins the final launch with atomics.
+// The fix-up passes are short grids that leave at once when the list is
+// empty.
 #include "internal.hpp"
 
 namespace hx {
 
 struct JoinArgs {
-  const uint64_t* k[2];
-  const uint32_t* v[2];
+  const uint64_t* jkey;  // prep's join list: launches and kernels in row order
+  const uint32_t* jrow;
+  uint32_t* jslot;       // [n] each entry's slot (hashed slots only)
   const int64_t* ts;
   const int64_t* te;
+  const int64_t* corr;
+  const int32_t* pid;
   const int64_t* off;
   DevState* ds;
-  herschel_counters* cnt;
-  int32_t* link;
-  int32_t* aux;
-  int64_t* lat_hist;
+  int32_t* link;  // may be NULL (no containment, output not wanted)
+  int32_t* aux;   // may be NULL (likewise)
   int64_t* lk_first;
   int64_t* lk_last;
   int64_t* lk_sum;
@@ -45,181 +57,68 @@ struct JoinArgs {
   int P;
   int64_t* edge_wait;
   int32_t* edge_status;
-  // correlation table (processes <= JT_PROCS)
-  uint32_t* tab;
-  uint32_t* own;
-  uint8_t* multi;
-  int64_t* kmax;
-  int64_t* kmin;
-  int64_t cap;
-  const uint32_t* k_rows;  // admitted kernels' rows (prep's list)
+  uint32_t* L;     // [cap] launch word per slot
+  uint32_t* K;     // [cap] kernel word per slot
+  uint32_t* C;     // [cap] claiming row per slot (hashed slots)
+  int64_t* kmax;   // [cap] latest kernel end per slot (edges only)
+  int64_t* kmin;   // [cap] earliest kernel start per slot (edges only)
+  uint64_t hmask;  // hashed table size - 1 (a power of two)
+  uint32_t* fix;   // [fix_cap][3]: slot, row | FIX_DUP, launch row seen by the resolve pass
+  int64_t fix_cap;
 };
 
-// Smallest index in [lo, hi) whose key is >= target (hi if none); galloping
-// from lo.
-__device__ int64_t gallop_ge(const uint64_t* keys, int64_t lo, int64_t hi, uint64_t target) {
-  if (lo >= hi || keys[lo] >= target) return lo;
-  int64_t a = lo, b = lo + 1, step = 1;
-  while (b < hi && keys[b] < target) {
-    a = b;
-    step <<= 1;
-    b = a + step;
-  }
-  if (b > hi) b = hi;
-  while (b - a > 1) {
-    const int64_t mid = a + (b - a) / 2;
-    if (keys[mid] < target)
-      a = mid;
-    else
-      b = mid;
-  }
-  return b;
-}
+constexpr uint32_t FIX_DUP = 1u << 31;  // the entry is a duplicate launch (else a kernel sharing its slot)
 
-// Smallest index <= i whose key is >= target, given keys[i] >= target;
-// galloping backwards from i.
-__device__ int64_t gallop_back_ge(const uint64_t* keys, int64_t i, uint64_t target) {
-  if (i == 0 || keys[i - 1] < target) return i;
-  int64_t b = i - 1, step = 1, a = b - 1;
-  while (a >= 0 && keys[a] >= target) {
-    b = a;
-    step <<= 1;
-    a = b - step;
-  }
-  if (a < -1) a = -1;
-  while (b - a > 1) {
-    const int64_t mid = a + (b - a) / 2;
-    if (keys[mid] < target)
-      a = mid;
-    else
-      b = mid;
-  }
-  return b;
-}
-
-// One sorted position per thread.  The neighbours i-2 .. i+2 are
-// loaded with the position itself: they settle the usual groups (one launch
-// and its kernel) without a search, and the gallops handle the rest.  Counts
-// and latency bins go to one of JOIN_COPIES accumulator copies (spread so
-// that few workgroups add to one address); the final kernel sums them.
-__global__ __launch_bounds__(256) void k_join(JoinArgs a) {
-  __shared__ unsigned long long s_c[JC_N];
-  __shared__ unsigned long long s_h[64];
-  const int tid = threadIdx.x;
-  if (tid < JC_N) s_c[tid] = 0;
-  if (tid < 64) s_h[tid] = 0;
-  __syncthreads();
-  if (a.ds->join_direct) return;  // the correlation table did the join
-  const int64_t n = a.ds->nJ;
-  const int par = (int)a.ds->sort_parity[1];
-  const uint64_t* keys = a.k[par];
-  const uint32_t* vals = a.v[par];
-  const int64_t i = (int64_t)blockIdx.x * 256 + tid;
-  uint32_t c[JC_N] = {};
-  if (i < n) {
-    const uint64_t key = keys[i];
-    const uint32_t row = vals[i];
-    const uint64_t kprev = i > 0 ? keys[i - 1] : ~0ull;
-    const uint64_t kprev2 = i > 1 ? keys[i - 2] : ~0ull;
-    const uint64_t knext = i + 1 < n ? keys[i + 1] : ~0ull;
-    const uint64_t knext2 = i + 2 < n ? keys[i + 2] : ~0ull;
-    const uint64_t g = key >> 1;
-    if ((key & 1) == 0) {  // launch
-      if ((kprev >> 1) != g) {  // the group's head
-        int64_t fk, end;
-        if (knext == ((g << 1) | 1)) {
-          fk = i + 1;
-          end = (knext2 >> 1) != g ? i + 2 : gallop_ge(keys, i + 2, n, (g + 1) << 1);
-        } else if ((knext >> 1) != g) {
-          fk = end = i + 1;
-        } else {
-          fk = gallop_ge(keys, i + 1, n, (g << 1) | 1);
-          end = gallop_ge(keys, fk, n, (g + 1) << 1);
-        }
-        const int64_t nk = end - fk;
-        a.aux[row] = (int32_t)nk;
-        if (nk == 0) ++c[JC_UNM_L];
-        if (a.contain && nk > 0) {
-          const int64_t o = a.off ? a.off[(int32_t)(key >> 49)] : 0;
-          int64_t first = I64MAX, last = I64MIN;
-          uint64_t sum = 0;
-          for (int64_t q = fk; q < end; ++q) {
-            const uint32_t kr = vals[q];
-            const int64_t s = a.ts[kr] - o, e = a.te[kr] - o;
-            first = s < first ? s : first;
-            last = e > last ? e : last;
-            sum += (uint64_t)(e - s);
-          }
-          a.lk_first[row] = first;
-          a.lk_last[row] = last;
-          a.lk_sum[row] = (int64_t)sum;
-        }
-      } else {
-        a.aux[row] = 0;
-        ++c[JC_DUP];
-        ++c[JC_UNM_L];
-      }
-    } else {  // kernel: the group's head decides
-      // the first position of the group: i, i - 1 (one launch before), or
-      // found by galloping back (several launches, or kernels before i)
-      const int64_t f = (kprev >> 1) != g                          ? i
-                        : (kprev & 1) == 0 && (kprev2 >> 1) != g ? i - 1
-                                                                 : gallop_back_ge(keys, i, g << 1);
-      const uint64_t kf = f == i ? key : f == i - 1 ? kprev : keys[f];
-      if ((kf & 1) == 0) {
-        const uint32_t lrow = vals[f];
-        a.link[row] = (int32_t)lrow;
-        ++c[JC_MATCHED];
-        const int64_t x = a.ts[row] - a.ts[lrow];  // same process: the offset cancels
-        if (x < 0) ++c[JC_NEG];
-        const int bin = x <= 0 ? 0 : bits_of((uint64_t)x);
-        atomicAdd(&s_h[bin], 1ull);
-        a.aux[row] = -1;  // the kernel's op comes later (the name pass)
-      } else {
-        a.link[row] = -1;
-        a.aux[row] = -1;
-        ++c[JC_UNM_K];
-      }
+// Hashed slot of (key, pid, corr): probe from the key's hash; an empty slot
+// is claimed with a compare-and-swap (a claimed slot never changes within a
+// call, so a stale read of an empty slot only sends the thread to the
+// compare-and-swap, which returns the current claimer); a claimed slot is
+// this key's when its claiming row has the same process and id.
+__device__ __forceinline__ int64_t jt_claim(const JoinArgs& a, uint64_t key, uint32_t row, int32_t pid,
+                                            int64_t corr) {
+  uint64_t s = jt_hash(key) & a.hmask;
+  for (uint64_t probe = 0; probe <= a.hmask; ++probe) {
+    uint32_t c = a.C[s];
+    if (c == JT_EMPTY) {
+      c = atomicCAS(&a.C[s], JT_EMPTY, row);
+      if (c == JT_EMPTY) return (int64_t)s;
     }
+    if (a.pid[c] == pid && a.corr[c] == corr) return (int64_t)s;
+    s = (s + 1) & a.hmask;
   }
-#pragma unroll
-  for (int q = 0; q < JC_N; ++q) {
-    const uint64_t w = wave_sum_u64(c[q]);
-    if (lane_id() == 0 && w) atomicAdd(&s_c[q], (unsigned long long)w);
-  }
-  __syncthreads();
-  unsigned long long* acc = &a.ds->join_acc[blockIdx.x % JOIN_COPIES][0];
-  if (tid < JC_N && s_c[tid]) atomicAdd(&acc[tid], s_c[tid]);
-  if (tid < 64 && s_h[tid]) atomicAdd(&acc[JC_N + tid], s_h[tid]);
+  set_status(a.ds, DS_CAPACITY);  // unreachable: the table has twice the rows' slots
+  return -1;
 }
 
-// Correlation-table plan: each process's id range (from the key range prep
-// found), slot bases by an exclusive scan, and the decision.  One wave, one
-// lane per process.
-__device__ __forceinline__ int64_t jt_slot(const DevState* ds, uint64_t key) {
-  const int p = (int)(key >> 49);
-  return ds->jt_base[p] + (int64_t)((key >> 1) & ((1ull << 48) - 1)) - ds->jt_cmin[p];
-}
-
-// Empty every slot in use (and the kernel-time tables when there are edges).
-__global__ __launch_bounds__(256) void k_jt_clear(JoinArgs a) {
-  if (!a.ds->join_direct) return;
-  const int64_t R = a.ds->jt_slots;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < R; i += (int64_t)gridDim.x * 256) {
-    a.tab[i] = ~0u;
-    a.multi[i] = 0;
-    if (a.kmax) {
-      a.kmax[i] = I64MIN;
-      a.kmin[i] = I64MAX;
-    }
+// Slot of (pid, corr) without claiming; -1 when no admitted launch or kernel
+// has that id.
+__device__ __forceinline__ int64_t jt_find(const JoinArgs& a, int32_t pid, int64_t corr) {
+  if (pid < 0 || pid >= a.P) return -1;
+  const uint64_t key = ((uint64_t)pid << JK_PID_SHIFT) | (((uint64_t)corr & JK_CORR_MASK) << 1);
+  if (a.ds->join_direct) {
+    if (!((a.ds->jt_present >> pid) & 1)) return -1;
+    const uint64_t rel = (uint64_t)corr - (uint64_t)a.ds->jt_cmin[pid];
+    const int64_t lim = (pid + 1 < a.P ? a.ds->jt_base[pid + 1] : a.ds->jt_slots) - a.ds->jt_base[pid];
+    if (rel >= (uint64_t)lim) return -1;
+    return a.ds->jt_base[pid] + (int64_t)rel;
   }
+  uint64_t s = jt_hash(key) & a.hmask;
+  for (uint64_t probe = 0; probe <= a.hmask; ++probe) {
+    const uint32_t c = a.C[s];
+    if (c == JT_EMPTY) return -1;
+    if (a.pid[c] == pid && a.corr[c] == corr) return (int64_t)s;
+    s = (s + 1) & a.hmask;
+  }
+  return -1;
 }
 
-__device__ __forceinline__ void jt_flush(const JoinArgs& a, uint32_t (&c)[JC_N], unsigned long long* s_c,
+// Adds each thread's counts (signed: the fix-up moves latencies between
+// bins) to the workgroup's and then to one of the accumulator copies.
+__device__ __forceinline__ void jt_flush(const JoinArgs& a, int64_t (&c)[JC_N], unsigned long long* s_c,
                                          unsigned long long* s_h) {
 #pragma unroll
   for (int q = 0; q < JC_N; ++q) {
-    const uint64_t w = wave_sum_u64(c[q]);
+    const uint64_t w = wave_sum_u64((uint64_t)c[q]);
     if (lane_id() == 0 && w) atomicAdd(&s_c[q], (unsigned long long)w);
   }
   __syncthreads();
@@ -228,305 +127,308 @@ __device__ __forceinline__ void jt_flush(const JoinArgs& a, uint32_t (&c)[JC_N],
   if (s_h && threadIdx.x < 64 && s_h[threadIdx.x]) atomicAdd(&acc[JC_N + threadIdx.x], s_h[threadIdx.x]);
 }
 
-// The table passes give each thread IT positions (striped over the
-// workgroup) and issue each round of their loads together: a pass is a
-// short chain of dependent loads, and batching positions per thread keeps
-// the number of waves the chip must cycle through low.  The check and
-// kernel passes, whose chains are longest, take 8 positions a thread; the
-// store and fix passes 2 (each measured best).
-constexpr int JT_IT_STORE = 2, JT_IT_CHECK = 8, JT_IT_FIX = 2, JT_IT_KERNEL = 8;
+__device__ __forceinline__ int lat_bin(int64_t x) { return x <= 0 ? 0 : bits_of((uint64_t)x); }
 
-// Pass 1: every launch stores its row in its slot and every kernel in its
-// slot's owner word, with plain stores (one writer of each wins).
+// The passes give each thread IT entries (striped over the workgroup) and
+// issue each round of their loads together: a pass is a short chain of
+// dependent loads, and batching entries per thread keeps the number of waves
+// the chip must cycle through low.
+constexpr int JT_IT_STORE = 4, JT_IT_RESOLVE = 8;
+
+// Pass 1: every launch writes its row to its slot's launch word, every kernel
+// to the kernel word (plain stores; one writer of each wins).
 template <int IT>
 __global__ __launch_bounds__(256) void k_jt_store(JoinArgs a) {
-  if (!a.ds->join_direct) return;
   const int64_t n = a.ds->nJ;
+  if (n == 0) return;
+  const bool dense = a.ds->join_direct != 0;
+  const int64_t cap = a.ds->jt_slots;
   const int64_t i0 = (int64_t)blockIdx.x * (256 * IT) + threadIdx.x;
   uint64_t key[IT];
   uint32_t row[IT];
 #pragma unroll
   for (int u = 0; u < IT; ++u) {
     const int64_t i = i0 + u * 256;
-    const int64_t ic = i < n ? i : (n > 0 ? n - 1 : 0);  // clamped: the loads stay in flight together
-    key[u] = a.k[0][ic];  // unsorted: the join sort did not run
-    row[u] = a.v[0][ic];
-    if (i >= n) key[u] = ~0ull;
+    const int64_t ic = i < n ? i : n - 1;  // clamped: the loads stay in flight together
+    key[u] = a.jkey[ic];
+    row[u] = a.jrow[ic];
   }
+  if (dense) {
+#pragma unroll
+    for (int u = 0; u < IT; ++u) {
+      if (i0 + u * 256 >= n) continue;
+      const int64_t slot = jt_dense_slot(a.ds, key[u]);
+      if (!in_bounds(a.ds, slot, cap)) continue;
+      ((key[u] & 1) ? a.K : a.L)[slot] = row[u];
+    }
+    return;
+  }
+  // hashed: the entries' own process and full id, then the probes
+  int32_t pd[IT];
+  int64_t cr[IT];
 #pragma unroll
   for (int u = 0; u < IT; ++u) {
-    if (key[u] == ~0ull) continue;
-    const int64_t slot = jt_slot(a.ds, key[u]);
-    if (!in_range(a.ds, slot, a.cap)) continue;
-    if (key[u] & 1)
-      a.own[slot] = row[u];
-    else
-      a.tab[slot] = row[u];
+    pd[u] = a.pid[row[u]];
+    cr[u] = a.corr[row[u]];
   }
-}
-
-// Pass 2: a launch that lost its slot is a duplicate; a kernel that lost its
-// owner word marks the slot as holding several kernels.  Launches start with
-// no kernels (their kernel aggregates are read only when they have some).
-template <int IT>
-__global__ __launch_bounds__(256) void k_jt_check(JoinArgs a) {
-  __shared__ unsigned long long s_c[JC_N];
-  const int tid = threadIdx.x;
-  if (tid < JC_N) s_c[tid] = 0;
-  __syncthreads();
-  if (!a.ds->join_direct) return;
-  const int64_t n = a.ds->nJ;
-  const int64_t i0 = (int64_t)blockIdx.x * (256 * IT) + tid;
-  uint32_t c[JC_N] = {};
-  uint64_t key[IT];
-  uint32_t row[IT], w[IT];
-  int64_t slot[IT];
 #pragma unroll
   for (int u = 0; u < IT; ++u) {
     const int64_t i = i0 + u * 256;
-    const int64_t ic = i < n ? i : (n > 0 ? n - 1 : 0);
-    key[u] = a.k[0][ic];
-    row[u] = a.v[0][ic];
-    if (i >= n) key[u] = ~0ull;
-  }
-#pragma unroll
-  for (int u = 0; u < IT; ++u) {
-    slot[u] = key[u] != ~0ull ? jt_slot(a.ds, key[u]) : -1;
-    const bool ok = slot[u] >= 0 && in_range(a.ds, slot[u], a.cap);
-    const int64_t sc = ok ? slot[u] : 0;
-    // one load: the owner word for a kernel, the slot for a launch
-    const uint32_t ws = ((key[u] & 1) ? a.own : a.tab)[sc];
-    w[u] = !ok ? row[u] : ws;
-  }
-#pragma unroll
-  for (int u = 0; u < IT; ++u) {
-    if (key[u] == ~0ull) continue;
-    if (key[u] & 1) {
-      if (w[u] != row[u]) a.multi[slot[u]] = 1;
-    } else {
-      if (w[u] != row[u]) ++c[JC_DUP];
-      a.aux[row[u]] = 0;
-    }
-  }
-  jt_flush(a, c, s_c, nullptr);
-}
-
-// Pass 3: duplicates put the smallest row into their slot (rare: atomics),
-// and the launches of slots with several kernels start their kernel
-// aggregates at the identities (the kernels add to them with atomics; a
-// launch with one kernel gets plain stores).
-template <int IT>
-__global__ __launch_bounds__(256) void k_jt_fix(JoinArgs a) {
-  if (!a.ds->join_direct) return;
-  const int64_t n = a.ds->nJ;
-  const int64_t i0 = (int64_t)blockIdx.x * (256 * IT) + threadIdx.x;
-  uint64_t key[IT];
-  uint32_t row[IT];
-#pragma unroll
-  for (int u = 0; u < IT; ++u) {
-    const int64_t i = i0 + u * 256;
-    const int64_t ic = i < n ? i : (n > 0 ? n - 1 : 0);
-    key[u] = a.k[0][ic];
-    row[u] = a.v[0][ic];
-    if (i >= n) key[u] = 1ull;  // past the end: treated as a kernel
-  }
-#pragma unroll
-  for (int u = 0; u < IT; ++u) {
-    if (key[u] & 1) continue;
-    const int64_t slot = jt_slot(a.ds, key[u]);
-    if (!in_range(a.ds, slot, a.cap)) continue;
-    const uint32_t t = a.tab[slot];
-    const uint8_t mu = a.multi[slot];
-    if (t != row[u]) atomicMin(&a.tab[slot], row[u]);
-    if (a.contain && mu) {
-      a.lk_first[row[u]] = I64MAX;
-      a.lk_last[row[u]] = I64MIN;
-      a.lk_sum[row[u]] = 0;
-    }
+    if (i >= n) continue;
+    const int64_t slot = jt_claim(a, key[u], row[u], pd[u], cr[u]);
+    if (slot < 0) continue;
+    a.jslot[i] = (uint32_t)slot;
+    ((key[u] & 1) ? a.K : a.L)[slot] = row[u];
   }
 }
 
-// Pass 4: each kernel reads its launch, records the latency, and adds itself
-// to the launch's counts: with plain stores when it is its slot's only kernel
-// (the usual case), with atomics otherwise.
+// Appends (slot, row | flag, w) to the fix-up list: one atomic per wave.
+__device__ __forceinline__ void fix_append(const JoinArgs& a, bool want, int64_t slot, uint32_t rowf, uint32_t w) {
+  const uint64_t b = ballot(want);
+  if (!b) return;
+  const int leader = __ffsll((unsigned long long)b) - 1;
+  uint32_t base = 0;
+  if (lane_id() == leader) base = atomicAdd(&a.ds->jt_nfix, (uint32_t)popc(b));
+  base = __shfl(base, leader, WAVE);
+  if (!want) return;
+  const int64_t at = (int64_t)base + popc(b & lanemask_lt());
+  if (!in_bounds(a.ds, at, a.fix_cap)) return;
+  a.fix[3 * at + 0] = (uint32_t)slot;
+  a.fix[3 * at + 1] = rowf;
+  a.fix[3 * at + 2] = w;
+}
+
+// Pass 2.  A launch that holds its slot's launch word joins the kernel that
+// holds the kernel word: it writes the kernel's link, the latency, its own
+// kernel count (1) and kernel aggregates.  A launch that lost is a duplicate
+// (count 0; listed).  A kernel that holds the kernel word records its times
+// for the edges, or, with no launch in the slot, is unmatched; a kernel that
+// lost shares the slot (listed).
 template <int IT>
-__global__ __launch_bounds__(256) void k_jt_kernel(JoinArgs a) {
+__global__ __launch_bounds__(256) void k_jt_resolve(JoinArgs a) {
   __shared__ unsigned long long s_c[JC_N];
   __shared__ unsigned long long s_h[64];
   const int tid = threadIdx.x;
   if (tid < JC_N) s_c[tid] = 0;
   if (tid < 64) s_h[tid] = 0;
   __syncthreads();
-  if (!a.ds->join_direct) return;
   const int64_t n = a.ds->nJ;
-  // Positions past the end take the last entry's row (clamped loads); with
-  // no entry there is no row to take, and nothing to do.
   if (n == 0) return;
+  const bool dense = a.ds->join_direct != 0;
+  const int64_t cap = a.ds->jt_slots;
   const int64_t i0 = (int64_t)blockIdx.x * (256 * IT) + tid;
-  uint32_t c[JC_N] = {};
+  int64_t c[JC_N] = {};
+  // round 1: the entries
   uint64_t key[IT];
-  uint32_t row[IT];
+  uint32_t row[IT], hs[IT];
 #pragma unroll
   for (int u = 0; u < IT; ++u) {
     const int64_t i = i0 + u * 256;
     const int64_t ic = i < n ? i : n - 1;
-    key[u] = a.k[0][ic];
-    row[u] = a.v[0][ic];
-    if (i >= n) key[u] = 0ull;  // past the end: treated as a launch (skipped)
+    key[u] = a.jkey[ic];
+    row[u] = a.jrow[ic];
+    hs[u] = dense ? 0u : a.jslot[ic];
   }
-  // round 2: the slot's launch and kernel count, the kernel's times
-  int64_t slot[IT], ts[IT], te[IT];
-  uint32_t l[IT];
-  bool single[IT];
+  // round 2: the slot's words
+  int64_t slot[IT];
+  uint32_t lw[IT], kw[IT];
+#pragma unroll
+  for (int u = 0; u < IT; ++u) {
+    const bool live = i0 + u * 256 < n;
+    slot[u] = dense ? jt_dense_slot(a.ds, key[u]) : (int64_t)hs[u];
+    if (!live || !in_bounds(a.ds, slot[u], cap)) slot[u] = -1;
+    const int64_t sc = slot[u] >= 0 ? slot[u] : 0;
+    lw[u] = a.L[sc];
+    kw[u] = a.K[sc];
+  }
+  // round 3: times (a launch that joins a kernel: the kernel's start and end
+  // and its own start; a kernel with edges: its start and end)
+  int64_t t0[IT], t1[IT], t2[IT];
 #pragma unroll
   for (int u = 0; u < IT; ++u) {
     const bool kern = (key[u] & 1) != 0;
-    slot[u] = kern ? jt_slot(a.ds, key[u]) : -1;
-    const bool ok = slot[u] >= 0 && in_range(a.ds, slot[u], a.cap);
-    const int64_t sc = ok ? slot[u] : 0;
-    const uint32_t lt = a.tab[sc];
-    const uint8_t mu = a.multi[sc];
-    const int64_t t0 = a.ts[row[u]], t1 = a.te[row[u]];
-    l[u] = ok ? lt : ~0u;
-    single[u] = ok && mu == 0;
-    ts[u] = kern ? t0 : 0;
-    te[u] = kern ? t1 : 0;
-  }
-  // round 3: the launch's start
-  int64_t lts[IT];
-#pragma unroll
-  for (int u = 0; u < IT; ++u) {
-    const bool has = (key[u] & 1) && l[u] != ~0u;
-    const int64_t t = a.ts[has ? l[u] : 0u];
-    lts[u] = has ? t : 0;
+    const bool joins = !kern && slot[u] >= 0 && lw[u] == row[u] && kw[u] != JT_EMPTY;
+    const uint32_t kr = kern ? row[u] : joins ? kw[u] : 0u;
+    t0[u] = a.ts[kr];
+    t1[u] = a.te[kr];
+    t2[u] = a.ts[joins ? row[u] : 0u];
   }
 #pragma unroll
   for (int u = 0; u < IT; ++u) {
-    if (!(key[u] & 1)) continue;
-    const int64_t o = a.off ? a.off[(int32_t)(key[u] >> 49)] : 0;
-    if (a.kmax && slot[u] >= 0) {
-      if (single[u]) {
-        a.kmax[slot[u]] = te[u] - o;
-        a.kmin[slot[u]] = ts[u] - o;
+    const bool kern = (key[u] & 1) != 0;
+    const bool live = slot[u] >= 0;
+    const int64_t o = a.off ? a.off[(int32_t)(key[u] >> JK_PID_SHIFT)] : 0;
+    if (live && !kern) {
+      if (lw[u] != row[u]) {  // a duplicate: no kernels (unless the fix-up hands it the slot's)
+        if (a.aux) a.aux[row[u]] = 0;
+        ++c[JC_DUP];
+      } else if (kw[u] == JT_EMPTY) {
+        if (a.aux) a.aux[row[u]] = 0;
       } else {
-        atomicMax((long long*)&a.kmax[slot[u]], (long long)(te[u] - o));
-        atomicMin((long long*)&a.kmin[slot[u]], (long long)(ts[u] - o));
+        const uint32_t kr = kw[u];
+        if (a.link) a.link[kr] = (int32_t)row[u];
+        if (a.aux) {
+          a.aux[kr] = -1;  // the kernel's op comes later (the name pass)
+          a.aux[row[u]] = 1;
+        }
+        ++c[JC_MATCHED];
+        ++c[JC_MLAUNCH];
+        const int64_t x = t0[u] - t2[u];  // same process: the offset cancels
+        if (x < 0) ++c[JC_NEG];
+        atomicAdd(&s_h[lat_bin(x)], 1ull);
+        if (a.contain) {
+          a.lk_first[row[u]] = t0[u] - o;
+          a.lk_last[row[u]] = t1[u] - o;
+          a.lk_sum[row[u]] = t1[u] - t0[u];
+        }
       }
     }
-    if (l[u] != ~0u) {
-      a.link[row[u]] = (int32_t)l[u];
-      ++c[JC_MATCHED];
-      const int64_t x = ts[u] - lts[u];  // same process: the offset cancels
-      if (x < 0) ++c[JC_NEG];
-      atomicAdd(&s_h[x <= 0 ? 0 : bits_of((uint64_t)x)], 1ull);
-      a.aux[row[u]] = -1;  // the kernel's op comes later (the name pass)
-      if (single[u]) {
-        a.aux[l[u]] = 1;
-        ++c[JC_MLAUNCH];
-        if (a.contain) {
-          a.lk_first[l[u]] = ts[u] - o;
-          a.lk_last[l[u]] = te[u] - o;
-          a.lk_sum[l[u]] = te[u] - ts[u];
-        }
-      } else {
-        if (atomicAdd(&a.aux[l[u]], 1) == 0) ++c[JC_MLAUNCH];
-        if (a.contain) {
-          atomicMin((long long*)&a.lk_first[l[u]], (long long)(ts[u] - o));
-          atomicMax((long long*)&a.lk_last[l[u]], (long long)(te[u] - o));
-          atomicAdd((unsigned long long*)&a.lk_sum[l[u]], (unsigned long long)(te[u] - ts[u]));
-        }
+    if (live && kern && kw[u] == row[u]) {
+      if (a.kmax) {
+        a.kmax[slot[u]] = t1[u] - o;
+        a.kmin[slot[u]] = t0[u] - o;
       }
-    } else {
-      a.link[row[u]] = -1;
-      a.aux[row[u]] = -1;
+      if (lw[u] == JT_EMPTY) {
+        if (a.link) a.link[row[u]] = -1;
+        if (a.aux) a.aux[row[u]] = -1;
+        ++c[JC_UNM_K];
+      }
+    }
+    const bool dup = live && !kern && lw[u] != row[u];
+    const bool shared = live && kern && kw[u] != row[u];
+    fix_append(a, dup || shared, slot[u], row[u] | (dup ? FIX_DUP : 0u), lw[u]);
+  }
+  jt_flush(a, c, s_c, s_h);
+}
+
+constexpr int JT_FIX_BLOCKS = 256;
+
+// Fix-up 1: duplicates put the smallest row into the launch word, and start
+// their kernel aggregates at the identities (the one that ends up in the
+// word receives its kernels with atomics).
+__global__ __launch_bounds__(256) void k_jt_dups(JoinArgs a) {
+  const int64_t nf = min((int64_t)a.ds->jt_nfix, a.fix_cap);
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nf; i += (int64_t)gridDim.x * 256) {
+    const uint32_t rf = a.fix[3 * i + 1];
+    if (!(rf & FIX_DUP)) continue;
+    const uint32_t slot = a.fix[3 * i], row = rf & ~FIX_DUP;
+    atomicMin(&a.L[slot], row);
+    if (a.contain) {
+      a.lk_first[row] = I64MAX;
+      a.lk_last[row] = I64MIN;
+      a.lk_sum[row] = 0;
+    }
+  }
+}
+
+// Fix-up 2: the duplicate now in its slot's launch word takes over the slot's
+// kernel from the launch that joined it in the resolve pass (link, latency
+// bin, kernel count and aggregates move); every kernel that shares a slot
+// joins the slot's final launch with atomics (or is unmatched) and adds its
+// times to the slot's edge extremes.
+__global__ __launch_bounds__(256) void k_jt_fix(JoinArgs a) {
+  __shared__ unsigned long long s_c[JC_N];
+  __shared__ unsigned long long s_h[64];
+  const int tid = threadIdx.x;
+  if (tid < JC_N) s_c[tid] = 0;
+  if (tid < 64) s_h[tid] = 0;
+  __syncthreads();
+  const int64_t nf = min((int64_t)a.ds->jt_nfix, a.fix_cap);
+  if ((int64_t)blockIdx.x * 256 >= nf) return;  // uniform: no entry for this workgroup
+  int64_t c[JC_N] = {};
+  for (int64_t i = (int64_t)blockIdx.x * 256 + tid; i < nf; i += (int64_t)gridDim.x * 256) {
+    const uint32_t slot = a.fix[3 * i], rf = a.fix[3 * i + 1], w = a.fix[3 * i + 2];
+    const uint32_t row = rf & ~FIX_DUP;
+    const uint32_t l = a.L[slot];
+    if (rf & FIX_DUP) {
+      const uint32_t kr = a.K[slot];
+      if (l != row || kr == JT_EMPTY) continue;
+      // row < w: the kernel of the resolve pass moves from launch w to row
+      const int64_t o = a.off ? a.off[a.pid[row]] : 0;
+      const int64_t ks = a.ts[kr], ke = a.te[kr];
+      const int64_t x_old = ks - a.ts[w], x_new = ks - a.ts[row];
+      if (a.link) a.link[kr] = (int32_t)row;
+      if (a.aux) {
+        a.aux[w] = 0;
+        atomicAdd(&a.aux[row], 1);
+      }
+      atomicAdd(&s_h[lat_bin(x_old)], ~0ull);  // minus one
+      atomicAdd(&s_h[lat_bin(x_new)], 1ull);
+      c[JC_NEG] += (x_new < 0 ? 1 : 0) - (x_old < 0 ? 1 : 0);
+      if (a.contain) {
+        atomicMin((long long*)&a.lk_first[row], (long long)(ks - o));
+        atomicMax((long long*)&a.lk_last[row], (long long)(ke - o));
+        atomicAdd((unsigned long long*)&a.lk_sum[row], (unsigned long long)(ke - ks));
+      }
+      continue;
+    }
+    // a kernel that shares its slot
+    const int64_t o = a.off ? a.off[a.pid[row]] : 0;
+    const int64_t ks = a.ts[row], ke = a.te[row];
+    if (a.kmax) {
+      atomicMax((long long*)&a.kmax[slot], (long long)(ke - o));
+      atomicMin((long long*)&a.kmin[slot], (long long)(ks - o));
+    }
+    if (l == JT_EMPTY) {
+      if (a.link) a.link[row] = -1;
+      if (a.aux) a.aux[row] = -1;
       ++c[JC_UNM_K];
+      continue;
+    }
+    if (a.link) a.link[row] = (int32_t)l;
+    if (a.aux) {
+      a.aux[row] = -1;
+      atomicAdd(&a.aux[l], 1);
+    }
+    ++c[JC_MATCHED];
+    const int64_t x = ks - a.ts[l];
+    if (x < 0) ++c[JC_NEG];
+    atomicAdd(&s_h[lat_bin(x)], 1ull);
+    if (a.contain) {
+      atomicMin((long long*)&a.lk_first[l], (long long)(ks - o));
+      atomicMax((long long*)&a.lk_last[l], (long long)(ke - o));
+      atomicAdd((unsigned long long*)&a.lk_sum[l], (unsigned long long)(ke - ks));
     }
   }
   jt_flush(a, c, s_c, s_h);
 }
 
+// Dependency waits: each edge's producer and consumer ids looked up in the
+// table; the slot's kernel extremes give the producer's last end and the
+// consumer's first start.
 __global__ __launch_bounds__(256) void k_edges(JoinArgs a) {
-  if (a.ds->join_direct) {
-    // table path: the kernels' latest end and earliest start per slot
-    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < a.n_edges; e += (int64_t)gridDim.x * 256) {
-      const herschel_edge ed = a.edges[e];
-      int found[2] = {0, 0};
-      int64_t prod_end = I64MIN, cons_start = I64MAX;
-      for (int side = 0; side < 2; ++side) {
-        const int32_t pid = side == 0 ? ed.prod_pid : ed.cons_pid;
-        const int64_t corr = side == 0 ? ed.prod_corr : ed.cons_corr;
-        if (pid < 0 || pid >= a.P || corr < 0 || corr >= HERSCHEL_CORR_LIMIT) continue;
-        const int64_t rel = corr - a.ds->jt_cmin[pid];
-        const int64_t lim = (pid + 1 < a.P ? a.ds->jt_base[pid + 1] : a.ds->jt_slots) - a.ds->jt_base[pid];
-        if (rel < 0 || rel >= lim) continue;
-        const int64_t slot = a.ds->jt_base[pid] + rel;
-        if (side == 0 && a.kmax[slot] != I64MIN) {
-          found[0] = 1;
-          prod_end = a.kmax[slot];
-        }
-        if (side == 1 && a.kmin[slot] != I64MAX) {
-          found[1] = 1;
-          cons_start = a.kmin[slot];
-        }
-      }
-      a.edge_status[e] = (found[0] ? 0 : 1) | (found[1] ? 0 : 2);
-      a.edge_wait[e] = (found[0] && found[1]) ? (int64_t)((uint64_t)cons_start - (uint64_t)prod_end) : I64MIN;
-    }
-    return;
-  }
-  const int64_t n = a.ds->nJ;
-  const int par = (int)a.ds->sort_parity[1];
-  const uint64_t* keys = a.k[par];
-  const uint32_t* vals = a.v[par];
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < a.n_edges; e += (int64_t)gridDim.x * 256) {
     const herschel_edge ed = a.edges[e];
     int found[2] = {0, 0};
     int64_t prod_end = I64MIN, cons_start = I64MAX;
     for (int side = 0; side < 2; ++side) {
-      const int32_t pid = side == 0 ? ed.prod_pid : ed.cons_pid;
-      const int64_t corr = side == 0 ? ed.prod_corr : ed.cons_corr;
-      if (pid < 0 || pid >= a.P || corr < 0 || corr >= HERSCHEL_CORR_LIMIT) continue;
-      const uint64_t target = ((uint64_t)pid << 49) | ((uint64_t)corr << 1) | 1;
-      int64_t lo = 0, hi = n;
-      while (lo < hi) {
-        const int64_t mid = lo + (hi - lo) / 2;
-        if (keys[mid] < target)
-          lo = mid + 1;
-        else
-          hi = mid;
-      }
-      const int64_t o = a.off ? a.off[pid] : 0;
-      for (int64_t q = lo; q < n && keys[q] == target; ++q) {
-        const uint32_t r = vals[q];
-        found[side] = 1;
-        if (side == 0) {
-          const int64_t t = a.te[r] - o;
-          prod_end = t > prod_end ? t : prod_end;
-        } else {
-          const int64_t t = a.ts[r] - o;
-          cons_start = t < cons_start ? t : cons_start;
-        }
-      }
+      const int64_t slot = side == 0 ? jt_find(a, ed.prod_pid, ed.prod_corr) : jt_find(a, ed.cons_pid, ed.cons_corr);
+      if (slot < 0 || a.K[slot] == JT_EMPTY) continue;
+      found[side] = 1;
+      if (side == 0)
+        prod_end = a.kmax[slot];
+      else
+        cons_start = a.kmin[slot];
     }
-    a.edge_status[e] = (found[0] ? 0 : 1) | (found[1] ? 0 : 2);
-    a.edge_wait[e] = (found[0] && found[1]) ? (int64_t)((uint64_t)cons_start - (uint64_t)prod_end) : I64MIN;
+    if (a.edge_status) a.edge_status[e] = (found[0] ? 0 : 1) | (found[1] ? 0 : 2);
+    if (a.edge_wait)
+      a.edge_wait[e] = (found[0] && found[1]) ? (int64_t)((uint64_t)cons_start - (uint64_t)prod_end) : I64MIN;
   }
 }
 
 static JoinArgs join_args(Ctx& c) {
   JoinArgs a;
-  a.k[0] = c.sJ.k[0];
-  a.k[1] = c.sJ.k[1];
-  a.v[0] = c.sJ.v[0];
-  a.v[1] = c.sJ.v[1];
+  a.jkey = c.jkey;
+  a.jrow = c.jrow;
+  a.jslot = c.jslot;
   a.ts = c.ev.ts;
   a.te = c.ev.te;
+  a.corr = c.ev.corr;
+  a.pid = c.ev.pid;
   a.off = c.p.clock_offset;
   a.ds = c.ds;
-  a.cnt = c.o.counters;
   a.link = c.o.link;
   a.aux = c.o.aux;
-  a.lat_hist = c.o.lat_hist;
   a.lk_first = c.lk_first;
   a.lk_last = c.lk_last;
   a.lk_sum = c.lk_sum;
@@ -536,37 +438,29 @@ static JoinArgs join_args(Ctx& c) {
   a.P = c.P;
   a.edge_wait = c.o.edge_wait;
   a.edge_status = c.o.edge_status;
-  a.tab = c.jt_tab;
-  a.own = c.jt_own;
-  a.multi = c.jt_multi;
+  a.L = c.jt_L;
+  a.K = c.jt_K;
+  a.C = c.jt_C;
   a.kmax = c.jt_kmax;
   a.kmin = c.jt_kmin;
-  a.cap = c.jt_cap;
-  a.k_rows = c.k_rows;
+  a.hmask = (uint64_t)c.jt_hsize - 1;
+  a.fix = c.jt_fix;
+  a.fix_cap = c.jt_fix_cap;
   return a;
 }
 
-// The correlation-table join (no-ops unless the plan chose it); it needs only
-// prep's lists, so it can run beside the sorts.
+// The join after the plan and the emptied table (both from the histogram
+// kernel): store, resolve and the two fix-up passes.
 void launch_join_table(Ctx& c) {
-  if (c.P > JT_PROCS) return;
+  if (c.n == 0) return;
   JoinArgs a = join_args(c);
-  const int64_t cgrid = std::min<int64_t>(std::max<int64_t>(cdiv(c.jt_cap, 256 * 8), 1), 4096);
-  auto tgrid = [&](int it) { return dim3((unsigned)std::max<int64_t>(cdiv(c.sJ.n_max, 256 * it), 1)); };
-  hipLaunchKernelGGL(k_jt_clear, dim3((unsigned)cgrid), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_jt_store<JT_IT_STORE>, tgrid(JT_IT_STORE), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_jt_check<JT_IT_CHECK>, tgrid(JT_IT_CHECK), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_jt_fix<JT_IT_FIX>, tgrid(JT_IT_FIX), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_jt_kernel<JT_IT_KERNEL>, tgrid(JT_IT_KERNEL), dim3(256), 0, c.st, a);
+  auto grid = [&](int it) { return dim3((unsigned)std::max<int64_t>(cdiv(c.n, 256 * it), 1)); };
+  hipLaunchKernelGGL(k_jt_store<JT_IT_STORE>, grid(JT_IT_STORE), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_resolve<JT_IT_RESOLVE>, grid(JT_IT_RESOLVE), dim3(256), 0, c.st, a);
+  const unsigned fb = (unsigned)std::min<int64_t>(std::max<int64_t>(cdiv(c.n, 256), 1), JT_FIX_BLOCKS);
+  hipLaunchKernelGGL(k_jt_dups, dim3(fb), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_jt_fix, dim3(fb), dim3(256), 0, c.st, a);
 }
-
-// The sort-merge join (a no-op when the table did the join); after the sorts.
-void launch_join(Ctx& c) {
-  JoinArgs a = join_args(c);
-  const int64_t grid = std::max<int64_t>(cdiv(c.sJ.n_max, 256), 1);
-  hipLaunchKernelGGL(k_join, dim3((unsigned)grid), dim3(256), 0, c.st, a);
-}
-
 
 void launch_edges(Ctx& c) {
   if (c.p.n_edges <= 0) return;

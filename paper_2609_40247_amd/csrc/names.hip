@@ -34,6 +34,7 @@ struct NamesArgs {
   int64_t* mx;
   // kernel -> op (with containment): the op of the kernel's launch
   bool kernel_ops;
+  bool tables;  // some name output is wanted
   const int32_t* link;
   int32_t* aux;
 };
@@ -41,7 +42,7 @@ struct NamesArgs {
 __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
   extern __shared__ unsigned long long tab[];  // [NN][4]: count, sum, min, max
   const int tid = threadIdx.x;
-  const bool lds = a.NN <= NM_LDS_NAMES;
+  const bool lds = a.tables && a.NN <= NM_LDS_NAMES;
   if (lds) {
     for (int q = tid; q < a.NN; q += NM_THREADS) {
       tab[q * 4 + 0] = 0;
@@ -86,17 +87,17 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
     }
 #pragma unroll
     for (int u = 0; u < NM_BATCH; ++u) {
-      if (q[u] < 0) continue;
+      if (q[u] < 0 || !a.tables) continue;
       if (lds) {
         atomicAdd(&tab[q[u] * 4 + 0], 1ull);
         atomicAdd(&tab[q[u] * 4 + 1], (unsigned long long)d[u]);
         atomicMin((long long*)&tab[q[u] * 4 + 2], (long long)d[u]);
         atomicMax((long long*)&tab[q[u] * 4 + 3], (long long)d[u]);
       } else {
-        atomicAdd((unsigned long long*)&a.count[q[u]], 1ull);
-        atomicAdd((unsigned long long*)&a.sum[q[u]], (unsigned long long)d[u]);
-        atomicMin((long long*)&a.mn[q[u]], (long long)d[u]);
-        atomicMax((long long*)&a.mx[q[u]], (long long)d[u]);
+        if (a.count) atomicAdd((unsigned long long*)&a.count[q[u]], 1ull);
+        if (a.sum) atomicAdd((unsigned long long*)&a.sum[q[u]], (unsigned long long)d[u]);
+        if (a.mn) atomicMin((long long*)&a.mn[q[u]], (long long)d[u]);
+        if (a.mx) atomicMax((long long*)&a.mx[q[u]], (long long)d[u]);
       }
     }
   }
@@ -121,6 +122,8 @@ __global__ __launch_bounds__(256) void k_names_reduce(NamesArgs a) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= (int64_t)a.NN * 4) return;
   const int q = (int)(t >> 2), stat = (int)(t & 3);
+  int64_t* const dst[4] = {a.count, a.sum, a.mn, a.mx};
+  if (!dst[stat]) return;  // that output is not wanted
   const int64_t stride = (int64_t)a.NN * 4;
   uint64_t acc = stat == 2 ? (uint64_t)I64MAX : stat == 3 ? (uint64_t)I64MIN : 0;
   for (int b0 = blockIdx.y; b0 < a.blocks; b0 += 16 * NR_GROUPS) {
@@ -164,6 +167,7 @@ static NamesArgs names_args(Ctx& c) {
   a.mn = c.o.name_min;
   a.mx = c.o.name_max;
   a.kernel_ops = c.contain;
+  a.tables = c.o.name_count || c.o.name_sum || c.o.name_min || c.o.name_max;
   a.link = c.o.link;
   a.aux = c.o.aux;
   return a;
@@ -174,14 +178,23 @@ int names_block_count(int64_t n_max, int NN) {
   return (int)std::min<int64_t>(std::max<int64_t>(cdiv(n_max, 8192), 1), 256);
 }
 
+// Names are wanted, or the pass gives kernels their ops (containment).
+static bool names_needed(const Ctx& c) {
+  return c.contain || c.o.name_count || c.o.name_sum || c.o.name_min || c.o.name_max;
+}
+static bool names_tables(const Ctx& c) {
+  return c.o.name_count || c.o.name_sum || c.o.name_min || c.o.name_max;
+}
+
 void launch_names(Ctx& c) {
+  if (!names_needed(c)) return;
   NamesArgs a = names_args(c);
-  const size_t lds = c.NN <= NM_LDS_NAMES ? (size_t)c.NN * 32 : 0;
+  const size_t lds = a.tables && c.NN <= NM_LDS_NAMES ? (size_t)c.NN * 32 : 0;
   hipLaunchKernelGGL(k_names_partial, dim3(c.name_blocks), dim3(NM_THREADS), lds, c.st, a);
 }
 
 void launch_names_reduce(Ctx& c) {
-  if (c.NN > NM_LDS_NAMES) return;
+  if (c.NN > NM_LDS_NAMES || !names_tables(c)) return;
   NamesArgs a = names_args(c);
   const int groups = std::min(NR_GROUPS, std::max(c.name_blocks, 1));
   hipLaunchKernelGGL(k_names_reduce, dim3((unsigned)cdiv((int64_t)c.NN * 4, 256), (unsigned)groups), dim3(256), 0, c.st,

@@ -56,12 +56,14 @@ __device__ __attribute__((always_inline)) inline void add_interval(const SweepAr
         if (present[c2]) atomicAdd(&s_cls[3 + c * 3 + c2], (unsigned long long)len);
     }
   } else {
-    atomicAdd((unsigned long long*)&a.any_busy[pid], (unsigned long long)len);
+    if (a.any_busy) atomicAdd((unsigned long long*)&a.any_busy[pid], (unsigned long long)len);
     for (int c = 0; c < 3; ++c) {
       if (!present[c]) continue;
-      atomicAdd((unsigned long long*)&a.class_busy[pid * 3 + c], (unsigned long long)len);
-      for (int c2 = 0; c2 < 3; ++c2)
-        if (present[c2]) atomicAdd((unsigned long long*)&a.class_overlap[(pid * 3 + c) * 3 + c2], (unsigned long long)len);
+      if (a.class_busy) atomicAdd((unsigned long long*)&a.class_busy[pid * 3 + c], (unsigned long long)len);
+      if (a.class_overlap)
+        for (int c2 = 0; c2 < 3; ++c2)
+          if (present[c2])
+            atomicAdd((unsigned long long*)&a.class_overlap[(pid * 3 + c) * 3 + c2], (unsigned long long)len);
     }
   }
   // separate loops for LDS and HBM, so that neither becomes a flat atomic
@@ -71,7 +73,7 @@ __device__ __attribute__((always_inline)) inline void add_interval(const SweepAr
       for (uint64_t mj = m; mj; mj &= mj - 1)
         atomicAdd(&s_pair[i * S + __ffsll((unsigned long long)mj) - 1], (unsigned long long)len);
     }
-  } else {
+  } else if (a.pair) {
     for (uint64_t mi = m; mi; mi &= mi - 1) {
       const int i = __ffsll((unsigned long long)mi) - 1;
       for (uint64_t mj = m; mj; mj &= mj - 1)
@@ -464,7 +466,7 @@ __global__ __launch_bounds__(SW_THREADS) void k_sweep(SweepArgs a) {
       unsigned long long v = 0;
       for (int mk = 1; mk < nm; ++mk)
         if (((uint64_t)mk & need) == need) v += s_mlen[mk];
-      if (v) atomicAdd((unsigned long long*)&a.pair[((int64_t)pid0 * S + i) * S + jj], v);
+      if (v && a.pair) atomicAdd((unsigned long long*)&a.pair[((int64_t)pid0 * S + i) * S + jj], v);
     } else if (tid >= 64 && tid < 64 + 13) {
       const int e = tid - 64;  // 0..2 class busy, 3..11 class pairs, 12 any
       unsigned long long v = 0;
@@ -483,14 +485,15 @@ __global__ __launch_bounds__(SW_THREADS) void k_sweep(SweepArgs a) {
     }
     __syncthreads();
   }
-  if (!SMALL) {
+  if (!SMALL && a.pair) {
     for (int i = tid; i < S * S; i += SW_THREADS)
       if (s_pair[i]) atomicAdd((unsigned long long*)&a.pair[(int64_t)pid0 * S * S + i], s_pair[i]);
   }
-  if (tid < 3 && s_cls[tid]) atomicAdd((unsigned long long*)&a.class_busy[pid0 * 3 + tid], s_cls[tid]);
-  if (tid >= 3 && tid < 12 && s_cls[tid])
+  if (a.class_busy && tid < 3 && s_cls[tid])
+    atomicAdd((unsigned long long*)&a.class_busy[pid0 * 3 + tid], s_cls[tid]);
+  if (a.class_overlap && tid >= 3 && tid < 12 && s_cls[tid])
     atomicAdd((unsigned long long*)&a.class_overlap[pid0 * 9 + (tid - 3)], s_cls[tid]);
-  if (tid == 12 && s_cls[12]) atomicAdd((unsigned long long*)&a.any_busy[pid0], s_cls[12]);
+  if (a.any_busy && tid == 12 && s_cls[12]) atomicAdd((unsigned long long*)&a.any_busy[pid0], s_cls[12]);
 }
 
 void launch_overlap(Ctx& c) {

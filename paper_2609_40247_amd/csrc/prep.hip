@@ -5,7 +5,8 @@
 // row order, into the inputs of the three sorts:
 //   timeline    (pid, stream, ts'-W0)            kernels
 //   containment (pid, thread, ts'-W0, is_launch) ops and launches
-//   join        (pid, corr, is_kernel)            launches and kernels
+//   join        (pid, corr mod 2^51, is_kernel)   launches and kernels (not sorted: the
+//                                                 correlation table takes them in row order)
 // Compaction offsets come from a decoupled look-back per list; the last
 // tile's prefixes are the admitted counts.
 #include "internal.hpp"
@@ -24,7 +25,7 @@ struct PrepArgs {
   int P, S, T, NN, NOP;
   int sb, tb, wb;
   int64_t n_tiles;
-  bool jt_range;  // find each process's join key range (at most JT_PROCS processes)
+  bool jt_range;  // find each process's id range (at most JT_PROCS processes)
   DevState* ds;
   herschel_counters* cnt;
   int32_t* link;
@@ -57,14 +58,18 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
   __shared__ uint32_t s_tot[3];
   __shared__ uint64_t s_base[3];
   __shared__ unsigned long long s_bad;
-  __shared__ unsigned long long s_jr[2 * JT_PROCS];  // per process: max of ~key, max of key
+  __shared__ unsigned long long s_jr[2 * JT_PROCS];  // per process: max of ~u, max of u (u = corr ^ 2^63)
+  __shared__ unsigned long long s_jp;                 // processes with an admitted launch or kernel
   __shared__ int64_t s_clk[PREP_OFF_LDS];
 
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
   const int tile = blockIdx.x;
   const int64_t base = (int64_t)tile * PREP_TILE;
   const bool clk_lds = a.off && a.P <= PREP_OFF_LDS;
-  if (tid == 0) s_bad = ~0ull;
+  if (tid == 0) {
+    s_bad = ~0ull;
+    s_jp = 0;
+  }
   if (tid < 2 * JT_PROCS) s_jr[tid] = 0;
   if (clk_lds)
     for (int i = tid; i < a.P; i += PREP_THREADS) s_clk[i] = a.off[i];
@@ -73,6 +78,10 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
   uint64_t kA[PREP_ITEMS], kB[PREP_ITEMS];  // kA: timeline or containment key, kB: join key
   uint32_t fl = 0;                          // per item: bit 3j list K, 3j+1 list C, 3j+2 list J
   uint64_t bad = ~0ull;
+  // id range of the thread's current process (the join items of a thread
+  // mostly share one): tp the process, ulo / uhi the max of ~u and of u
+  int tp = -1;
+  uint64_t ulo = 0, uhi = 0;
   const uint64_t lt = lanemask_lt();
 #pragma unroll
   for (int j0 = 0; j0 < PREP_ITEMS; j0 += PREP_BATCH) {
@@ -110,7 +119,6 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
           ok = ok && ln >= 0 && ln < a.S && name >= 0 && name < a.NN;
         else
           ok = ok && ln >= 0 && ln < a.T && name >= 0 && (kind != HERSCHEL_CPU_OP || name < a.NOP);
-        ok = ok && (kind == HERSCHEL_CPU_OP || (corr >= 0 && corr < HERSCHEL_CORR_LIMIT));
         ok = ok && ts > -LIM && ts < LIM && te > -LIM && te < LIM && te >= ts;
         bool adm = false;
         int64_t rel = 0;
@@ -123,8 +131,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
           bad = (uint64_t)r < bad ? (uint64_t)r : bad;
         }
         if (!adm) {
-          a.link[r] = -2;
-          a.aux[r] = -2;
+          if (a.link) a.link[r] = -2;
+          if (a.aux) a.aux[r] = -2;
         } else {
           fK = kind == HERSCHEL_KERNEL;
           fC = !fK;
@@ -134,7 +142,24 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
           else
             kA[j] = ((uint64_t)pid << (a.tb + a.wb + 1)) | ((uint64_t)ln << (a.wb + 1)) | ((uint64_t)rel << 1) |
                     (uint64_t)(kind == HERSCHEL_LAUNCH);
-          kB[j] = ((uint64_t)pid << 49) | ((uint64_t)corr << 1) | (uint64_t)(kind == HERSCHEL_KERNEL);
+          kB[j] = ((uint64_t)pid << JK_PID_SHIFT) | (((uint64_t)corr & JK_CORR_MASK) << 1) |
+                  (uint64_t)(kind == HERSCHEL_KERNEL);
+          if (a.jt_range && fJ) {
+            const uint64_t u = (uint64_t)corr ^ SIGN64;  // unsigned order = signed order of the ids
+            if (pid != tp) {
+              if (tp >= 0) {
+                atomicMax(&s_jr[2 * tp], (unsigned long long)ulo);
+                atomicMax(&s_jr[2 * tp + 1], (unsigned long long)uhi);
+                atomicOr(&s_jp, 1ull << tp);
+              }
+              tp = pid;
+              ulo = ~u;
+              uhi = u;
+            } else {
+              ulo = ~u > ulo ? ~u : ulo;
+              uhi = u > uhi ? u : uhi;
+            }
+          }
         }
       }
       fl |= (fK ? 1u : 0u) << (3 * j) | (fC ? 1u : 0u) << (3 * j + 1) | (fJ ? 1u : 0u) << (3 * j + 2);
@@ -149,28 +174,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
   if (bad != ~0ull) atomicMin(&s_bad, (unsigned long long)bad);
   __syncthreads();
   if (a.jt_range) {
-    // each process's smallest and largest join key (the correlation table's
-    // id ranges): a thread's keys of one process are combined in registers,
-    // a wave whose keys all belong to one process combines them by shuffles
-    int tp = -1;
-    uint64_t lo = 0, hi = 0;  // lo: max of ~key
-#pragma unroll
-    for (int j = 0; j < PREP_ITEMS; ++j) {
-      if (!(fl & (4u << (3 * j)))) continue;
-      const int pj = (int)(kB[j] >> 49);
-      if (pj != tp) {
-        if (tp >= 0) {
-          atomicMax(&s_jr[2 * tp], (unsigned long long)lo);
-          atomicMax(&s_jr[2 * tp + 1], (unsigned long long)hi);
-        }
-        tp = pj;
-        lo = ~kB[j];
-        hi = kB[j];
-      } else {
-        lo = ~kB[j] > lo ? ~kB[j] : lo;
-        hi = kB[j] > hi ? kB[j] : hi;
-      }
-    }
+    // each process's smallest and largest id: a wave whose items all belong
+    // to one process combines them by shuffles, others add per thread
     int pm = tp;
     for (int d = 1; d < WAVE; d <<= 1) {
       const int o = __shfl_xor(pm, d, WAVE);
@@ -178,17 +183,19 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
     }
     if (pm >= 0 && ballot(tp >= 0 && tp != pm) == 0) {
       for (int d = 1; d < WAVE; d <<= 1) {
-        const uint64_t ol = shfl_xor(lo, d), oh = shfl_xor(hi, d);
-        lo = ol > lo ? ol : lo;
-        hi = oh > hi ? oh : hi;
+        const uint64_t ol = shfl_xor(ulo, d), oh = shfl_xor(uhi, d);
+        ulo = ol > ulo ? ol : ulo;
+        uhi = oh > uhi ? oh : uhi;
       }
       if (lane == 0) {
-        atomicMax(&s_jr[2 * pm], (unsigned long long)lo);
-        atomicMax(&s_jr[2 * pm + 1], (unsigned long long)hi);
+        atomicMax(&s_jr[2 * pm], (unsigned long long)ulo);
+        atomicMax(&s_jr[2 * pm + 1], (unsigned long long)uhi);
+        atomicOr(&s_jp, 1ull << pm);
       }
     } else if (tp >= 0) {
-      atomicMax(&s_jr[2 * tp], (unsigned long long)lo);
-      atomicMax(&s_jr[2 * tp + 1], (unsigned long long)hi);
+      atomicMax(&s_jr[2 * tp], (unsigned long long)ulo);
+      atomicMax(&s_jr[2 * tp + 1], (unsigned long long)uhi);
+      atomicOr(&s_jp, 1ull << tp);
     }
   }
   if (tid < 3) {
@@ -202,10 +209,11 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
   }
   if (tid == 0 && s_bad != ~0ull) atomicMin((unsigned long long*)&a.ds->first_invalid, s_bad);
   __syncthreads();
-  if (a.jt_range && tid < 2 * JT_PROCS && s_jr[tid]) {
-    unsigned long long* dst = (unsigned long long*)(tid & 1 ? &a.ds->jt_key_hi[tid >> 1] : &a.ds->jt_key_lo[tid >> 1]);
+  if (a.jt_range && tid < 2 * JT_PROCS && ((s_jp >> (tid >> 1)) & 1)) {
+    unsigned long long* dst = (unsigned long long*)(tid & 1 ? &a.ds->jt_hi[tid >> 1] : &a.ds->jt_lo[tid >> 1]);
     atomicMax(dst, s_jr[tid]);
   }
+  if (a.jt_range && tid == 0 && s_jp) atomicOr((unsigned long long*)&a.ds->jt_present, s_jp);
   if (wv < 3) {
     const uint64_t ex = wave_lookback<OpSum>(a.status + (int64_t)wv * a.n_tiles, tile, s_tot[wv], a.ds);
     if (lane == 0) s_base[wv] = ex;
@@ -280,8 +288,8 @@ void launch_prep(Ctx& c) {
   a.kRows = c.k_rows;
   a.kC = c.sC.k[0];
   a.vC = c.sC.v[0];
-  a.kJ = c.sJ.k[0];
-  a.vJ = c.sJ.v[0];
+  a.kJ = c.jkey;
+  a.vJ = c.jrow;
   hipLaunchKernelGGL(k_prep, dim3((unsigned)c.prep_tiles), dim3(PREP_THREADS), 0, c.st, a);
 }
 

@@ -29,15 +29,22 @@ struct HistJob {
 struct HistJobs {
   HistJob j[N_SORTS];
   uint32_t* part;  // [N_SORTS][HIST_MAX_BLOCKS][8 * 256] per-workgroup counts
-  int jt_P;        // processes of the correlation-table plan (0: no table, the join sorts)
-  int64_t jt_cap;  // table slots
+  // the correlation table's plan and emptying, by the workgroups of slice
+  // blockIdx.y == jt_slice
+  int jt_slice;
+  int jt_P;          // processes (0: more than JT_PROCS, hashed slots)
+  int64_t jt_cap;    // most dense slots
+  int64_t jt_hsize;  // hashed table size (a power of two, a multiple of 4)
+  uint32_t* jt_L;
+  uint32_t* jt_K;
+  uint32_t* jt_C;
 };
 
 // Digit histograms of several sort inputs in one launch (blockIdx.y picks
 // the sort).  Each workgroup counts a contiguous share of the keys in LDS
-// and stores its table; the plan kernel that follows sums the tables.  The
-// join sort's workgroups first take the correlation-table plan, which
-// decides whether that sort runs at all.  No
+// and stores its table; the plan kernel that follows sums the tables.  One
+// more slice of workgroups takes the correlation-table plan and empties the
+// table's slots in use, beside the counting.  No
 // global atomics and no fences: counters shared by many workgroups serialise
 // on their cache line, and a device-scope fence writes back the whole L2.
 // The grid is sized so that every CU holds a share (HIST_CHUNK keys at
@@ -183,17 +190,31 @@ __global__ __launch_bounds__(HIST_THREADS) void k_digit_hist(HistJobs jobs, DevS
   __shared__ uint32_t s_spare[WAVE];  // adds that count nothing (never read)
   __shared__ __align__(16) uint64_t s_row[HIST_THREADS * HIST_ROW];
   __shared__ uint32_t s_direct;
-  const HistJob jb = jobs.j[blockIdx.y];
-  if (jb.id == 1 && jobs.jt_P > 0) {
-    // the join sort's workgroups take the correlation-table plan (the first
-    // stores it): when the table replaces the sort they have nothing to count
+  __shared__ int64_t s_slots;
+  if ((int)blockIdx.y == jobs.jt_slice) {
+    // every workgroup takes the plan (the first stores it), then they empty
+    // the slots in use: launch and kernel words, and with hashed slots the
+    // claim words
     if (threadIdx.x < WAVE) {
-      const bool direct = jt_plan_wave(ds, jobs.jt_P, jobs.jt_cap, blockIdx.x == 0);
-      if (threadIdx.x == 0) s_direct = direct ? 1u : 0u;
+      int64_t slots = 0;
+      const bool direct = jt_plan_wave(ds, jobs.jt_P, jobs.jt_cap, jobs.jt_hsize, blockIdx.x == 0, &slots);
+      if (threadIdx.x == 0) {
+        s_direct = direct ? 1u : 0u;
+        s_slots = slots;
+      }
     }
     __syncthreads();
-    if (s_direct) return;
+    const int64_t q4 = cdiv(s_slots, 4);  // 16-byte words (the table is a multiple of 4 slots)
+    const bool claims = !s_direct;
+    const uint4 e4 = make_uint4(JT_EMPTY, JT_EMPTY, JT_EMPTY, JT_EMPTY);
+    for (int64_t w = (int64_t)blockIdx.x * HIST_THREADS + threadIdx.x; w < q4; w += (int64_t)gridDim.x * HIST_THREADS) {
+      reinterpret_cast<uint4*>(jobs.jt_L)[w] = e4;
+      reinterpret_cast<uint4*>(jobs.jt_K)[w] = e4;
+      if (claims) reinterpret_cast<uint4*>(jobs.jt_C)[w] = e4;
+    }
+    return;
   }
+  const HistJob jb = jobs.j[blockIdx.y];
   const int64_t n = *jb.count;
   const int nblk = hist_blocks(n);
   const int blk = blockIdx.x;
@@ -244,7 +265,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void k_hist_plan(HistJobs jobs, DevSt
   __shared__ uint32_t s_scan[PLAN_THREADS / WAVE + 1];
   const HistJob jb = jobs.j[blockIdx.y];
   const int d = blockIdx.x;
-  if (d >= jb.nd || (jb.id == 1 && ds->join_direct)) return;
+  if (d >= jb.nd) return;
   const int64_t n = *jb.count;
   const int nblk = hist_blocks(n);
   const int lane = threadIdx.x & (WAVE - 1), grp = threadIdx.x / WAVE;
@@ -390,9 +411,9 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   if (sel < 0) return;
   const SortJob& jb = jobs.j[sel];
   const int d = jb.d, id = jb.id;
-  static_assert(N_SORTS == 3, "the selects below name every sort");
-  const uint32_t n = sel == 0 ? nn[0] : sel == 1 ? nn[1] : nn[2];
-  const uint32_t triv = sel == 0 ? tr[0] : sel == 1 ? tr[1] : tr[2];
+  static_assert(N_SORTS == 2, "the selects below name every sort");
+  const uint32_t n = sel == 0 ? nn[0] : nn[1];
+  const uint32_t triv = sel == 0 ? tr[0] : tr[1];
   const uint32_t gexcl = ds->hist[id][d][dgt];
   const int parity = popc(~triv & ((1u << d) - 1u)) & 1;
   const uint64_t* kin = jb.k[parity];
@@ -631,12 +652,18 @@ void launch_hist_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
     n_max = std::max<int64_t>(n_max, s[i]->n_max);
     nd = std::max(nd, s[i]->nd);
   }
-  if (m == 0) return;
+  jobs.jt_slice = m;
   jobs.jt_P = c.P <= JT_PROCS ? c.P : 0;
   jobs.jt_cap = c.jt_cap;
-  const int64_t grid = std::min<int64_t>(cdiv(n_max, HIST_CHUNK), HIST_MAX_BLOCKS);
-  hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid, (unsigned)m), dim3(HIST_THREADS), 0, c.st, jobs, c.ds);
-  hipLaunchKernelGGL(k_hist_plan, dim3((unsigned)nd, (unsigned)m), dim3(PLAN_THREADS), 0, c.st, jobs, c.ds);
+  jobs.jt_hsize = c.jt_hsize;
+  jobs.jt_L = c.jt_L;
+  jobs.jt_K = c.jt_K;
+  jobs.jt_C = c.jt_C;
+  const int64_t grid = std::min<int64_t>(cdiv(std::max<int64_t>(n_max, 2 * c.n), HIST_CHUNK), HIST_MAX_BLOCKS);
+  hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)grid, (unsigned)(m + 1)), dim3(HIST_THREADS), 0, c.st, jobs,
+                     c.ds);
+  if (m > 0)
+    hipLaunchKernelGGL(k_hist_plan, dim3((unsigned)nd, (unsigned)m), dim3(PLAN_THREADS), 0, c.st, jobs, c.ds);
 }
 
 // Passes p0 .. p1-1 of up to N_SORTS sorts, one launch per pass: pass p of

@@ -55,12 +55,12 @@ __device__ __forceinline__ int32_t seg_of_key(const UnionArgs& a, uint64_t key) 
 }
 
 __device__ __forceinline__ void put_gap(const UnionArgs& a, int64_t pos, int32_t seg, int64_t b, int64_t e) {
-  if (pos < a.gap_cap) {
-    a.gap_pid[pos] = seg / a.S;
-    a.gap_stream[pos] = seg % a.S;
-    a.gap_begin[pos] = a.W0 + b;
-    a.gap_end[pos] = a.W0 + e;
-    a.gap_flags[pos] = (uint8_t)((b == 0 ? 1 : 0) | (e == a.W ? 2 : 0));
+  if (pos < a.gap_cap) {  // each gap array may be NULL
+    if (a.gap_pid) a.gap_pid[pos] = seg / a.S;
+    if (a.gap_stream) a.gap_stream[pos] = seg % a.S;
+    if (a.gap_begin) a.gap_begin[pos] = a.W0 + b;
+    if (a.gap_end) a.gap_end[pos] = a.W0 + e;
+    if (a.gap_flags) a.gap_flags[pos] = (uint8_t)((b == 0 ? 1 : 0) | (e == a.W ? 2 : 0));
   }
 }
 
@@ -392,7 +392,7 @@ void launch_timeline(Ctx& c) {
   a.overlap = c.overlap;
   a.ds = c.ds;
   a.cnt = c.o.counters;
-  a.busy = c.o.busy;
+  a.busy = c.o.busy ? c.o.busy : c.busy_ws;
   a.gap_cap = c.o.gap_capacity;
   a.gap_pid = c.o.gap_pid;
   a.gap_stream = c.o.gap_stream;

@@ -333,8 +333,7 @@ def test_single_kernel_covering_window(H):
 # --------------------------------------------------------------- errors
 def test_invalid_rows(H):
     cols, p, _ = load_golden("t1_worked_timeline.json")
-    for field, row, val in (("kind", 3, 3), ("pid", 5, 1), ("lane", 12, 2), ("te", 7, 12), ("corr", 9, -1),
-                            ("name", 2, 4)):
+    for field, row, val in (("kind", 3, 3), ("pid", 5, 1), ("lane", 12, 2), ("te", 7, 12), ("name", 2, 4)):
         c = {k: v.copy() for k, v in cols.items()}
         c[field][row] = val
         c["kind"][16] = 7  # a second, later invalid row
@@ -347,7 +346,7 @@ def test_invalid_params(H):
     n = len(cols["ts"])
     an = H.Analyzer(p, n)
     ev = H.events_struct(H.device_columns(cols))
-    for change in (dict(window_end=0), dict(n_streams=65), dict(n_threads=513), dict(n_procs=0),
+    for change in (dict(window_end=0), dict(n_streams=65), dict(n_threads=2049), dict(n_procs=0),
                    dict(flags=8), dict(n_names=0)):
         an.p = dict(p, **change)
         params = an._params_struct(an.ws.data_ptr(), an.ws_bytes)
@@ -467,4 +466,135 @@ def test_checked_library(H, case):
         tr = synth.config1(n_steps=40)
         cols, p = tr.columns(), tr.params
     check(H, cols, p, f"checked library: {case}", variant="checked")
+
+
+# --------------------------------------------------------------- correlation table
+def _remap_ids(cols, p, f):
+    c = {k: v.copy() for k, v in cols.items()}
+    jk = c["kind"] != 0
+    c["corr"][jk] = f(c["corr"][jk])
+    q = dict(p)
+    if p.get("edges") is not None and len(p["edges"]):
+        e = p["edges"].copy()
+        e["prod_corr"] = f(e["prod_corr"])
+        e["cons_corr"] = f(e["cons_corr"])
+        q["edges"] = e
+    return c, q
+
+
+def test_sparse_ids_full_size(H):
+    """The decode-step trace at full size (2.99M rows) with every id spread
+    by 2^20, so that no process's ids fit two slots per row: the join takes
+    hashed slots."""
+    tr = synth.config1()
+    cols, p = _remap_ids(tr.columns(), tr.params, lambda x: x << 20)
+    (code, g), _ = check(H, cols, p, "config1, sparse ids")
+    assert code == 0 and g["counters"]["n_matched"] > 980_000
+
+
+def test_sparse_ids_node_trace(H):
+    """Eight processes with edges and clock offsets, ids spread so that the
+    table takes hashed slots (and the edges look their ids up by hashing)."""
+    tr = synth.config3(n_procs=8, n_steps=60, n_edges=3000)
+    cols, p = _remap_ids(tr.columns(), tr.params, lambda x: (x << 18) ^ 0x2a5)
+    (code, g), _ = check(H, cols, p, "config3 small, sparse ids")
+    assert (g["edge_status"] == 0).mean() > 0.9
+
+
+@pytest.mark.parametrize("name", ["negate", "extremes", "spread"])
+def test_any_int64_ids(H, name):
+    """Ids anywhere in int64 (negative, at the limits, far apart): dense and
+    hashed slots, duplicates and shared launches, edges."""
+    maps = {
+        "negate": lambda x: -x - 1,
+        "extremes": lambda x: np.where(x % 2 == 0, np.int64(-(1 << 63)) + x, np.int64((1 << 63) - 1) - x),
+        "spread": lambda x: (x * np.int64(1 << 40)) ^ np.int64(0x5555),
+    }
+    for seed, (rows, corr_range) in enumerate(((3000, 300), (20_000, 20_000), (400, 60))):
+        tr = synth.random_small(seed=9400 + seed, n_rows=rows, window=4 * rows, n_procs=3, n_streams=4,
+                                n_threads=3, corr_range=corr_range, edges=40)
+        cols, p = _remap_ids(tr.columns(), tr.params, maps[name])
+        check(H, cols, p, f"ids {name}, {rows} rows")
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_duplicates_and_shared_launches_at_scale(H, seed):
+    """50k ids, each with 1 to 3 launches (the smallest row wins; the others
+    are duplicates) and 0 to 6 kernels (graph launches), rows shuffled: the
+    fix-up list carries tens of thousands of entries, and a duplicate with a
+    smaller row than the launch that first held the slot takes its kernels
+    over."""
+    rng = np.random.default_rng(9500 + seed)
+    W = 50_000_000
+    rows = []
+    for i in range(50_000):
+        pid = int(rng.integers(0, 2))
+        corr = int(rng.integers(0, 1 << 20)) * 50_000 + i if seed == 2 else i
+        t = int(rng.integers(0, W - 10_000))
+        for _ in range(int(rng.integers(1, 4))):
+            ts = t + int(rng.integers(0, 1000))
+            rows.append((1, pid, int(rng.integers(0, 2)), ts, ts + 500, corr, 0))
+        for _ in range(int(rng.choice([0, 1, 1, 1, 2, 6]))):
+            ks = t + int(rng.integers(-200, 3000))
+            rows.append((2, pid, int(rng.integers(0, 3)), ks, ks + int(rng.integers(0, 900)), corr,
+                         int(rng.integers(0, 4))))
+        if i % 7 == 0:
+            rows.append((0, pid, int(rng.integers(0, 2)), t - 100, t + 5000, 0, int(rng.integers(0, 4))))
+    perm = rng.permutation(len(rows))
+    rows = [rows[i] for i in perm]
+    e = np.zeros(500, synth.EDGE_DTYPE)
+    e["prod_pid"] = rng.integers(0, 2, 500)
+    e["cons_pid"] = rng.integers(0, 2, 500)
+    ids = np.array([r[5] for r in rows], np.int64)
+    e["prod_corr"] = rng.choice(ids, 500)
+    e["cons_corr"] = rng.choice(ids, 500)
+    cols, p = _rows(rows, P=2, S=3, T=2, W=W, thr=1000, edges=e)
+    (code, g), _ = check(H, cols, p, f"duplicates and shared launches, seed {seed}")
+    assert g["counters"]["n_dup_launch_corr"] > 10_000
+
+
+# --------------------------------------------------------------- optional outputs
+OUTPUT_SETS = {
+    "batch set": ("name_count", "name_sum", "name_min", "name_max", "busy", "idle", "gap_pid", "gap_stream",
+                  "gap_begin", "gap_end", "gap_flags", "lat_hist"),
+    "no per-row links": ("op_nkern", "op_first", "op_last", "op_ksum", "busy", "pair_overlap", "class_busy",
+                         "any_busy", "edge_wait", "lat_hist"),
+    "only idle and one name column": ("idle", "name_max", "gap_end", "class_overlap", "edge_status"),
+}
+
+
+@pytest.mark.parametrize("which", sorted(OUTPUT_SETS))
+@pytest.mark.parametrize("flags", [0, 3])
+def test_null_outputs(H, which, flags):
+    """Outputs left NULL are not written and change nothing in the others:
+    containment and the per-row links it reads back still work when the link
+    and aux outputs are NULL."""
+    tr = synth.config3(n_procs=3, n_steps=20, n_edges=300)
+    cols, p = tr.columns(), dict(tr.params, flags=flags)
+    n = tr.n
+    cap = n + p["n_procs"] * p["n_streams"]
+    an = H.Analyzer(p, n, gap_capacity=cap)
+    keep = set(OUTPUT_SETS[which])
+    ptrs = {k: (v.data_ptr() if k in keep or k == "counters" else None) for k, v in an.o.items()}
+    outs = H.HerschelOutputs(gap_capacity=cap, **ptrs)
+    for v in an.o.values():  # the oracle's mark of entries it does not write (op_* at other rows)
+        v.fill_(oracle.UNWRITTEN_I64 if v.dtype != torch.uint8 else 7)
+    d = H.device_columns(cols)
+    code = H.herschel_trace_analyze(H.events_struct(d), n, an.params, outs)
+    torch.cuda.synchronize()
+    res = an.results(n)
+    ocode, o = oracle.analyze(cols, p, gap_capacity=cap)
+    assert code == ocode == 0
+    assert res["counters"] == {**o["counters"], "device_status": 0}
+    for k in an.o:
+        if k == "counters":
+            continue
+        if k in keep:
+            if k.startswith("op_") and not flags & 1 or k in ("pair_overlap", "class_busy", "class_overlap",
+                                                                 "any_busy") and not flags & 2:
+                continue
+            assert np.array_equal(res[k], o[k]), (which, k)
+        else:  # untouched
+            raw = an.o[k].cpu().numpy()
+            assert (raw == (7 if raw.dtype == np.uint8 else oracle.UNWRITTEN_I64)).all(), (which, k)
 
