@@ -1,14 +1,21 @@
 #!/usr/bin/env python3
 """Benchmark of the trace analyzer on one MI355X.
 
-One step = one full analysis (every output: timelines, gaps, join and
-latency histogram, containment with per-op aggregates, per-name
-aggregates, cross-stream overlap) of the decode-step trace: 1 process,
-4 streams, a 30 s window, 1,000 steps of 1,000 kernels (about 1M kernel
-records, 1M launches, 1M CPU ops: 2.99M rows).  The input is resident in
-HBM before timing.  Prints one JSON line: events (all input rows) per
-second, the roofline of the dominant kernel measured live with HIP events
-on the library's stream (the radix-sort passes), and the CPU oracle timed
+One step = one full analysis of one synthetic profiling window (every output:
+timelines, gaps, join and latency histogram, containment with per-op
+aggregates, per-name aggregates, cross-stream overlap, dependency waits).
+The default workload is the decode-step trace: 1 process, 4 streams, a 30 s
+window, 1,000 steps of 1,000 kernels (about 1M kernel records, 1M launches,
+1M CPU ops: 2.99M rows).  ``--workload`` picks another: the tiny trace, the
+mixed prefill/decode trace, the 8-process node trace, or one 32-trace chunk
+of the 256-trace batch through the batch entry point.  The input is resident
+in HBM before timing.
+
+Prints one JSON line: events (all input rows) per second; the roofline of the
+dominant kernel (the radix digit passes) measured live with HIP events on the
+stream they run on; the whole call's algorithmic bytes over its wall time,
+warm and with a cold cache, beside the HBM traffic the committed rocprofv3
+counter profile measured over all analysis kernels; and the CPU oracle timed
 on this host.
 """
 from __future__ import annotations
@@ -18,61 +25,106 @@ import hashlib
 import json
 import os
 import re
+import statistics
 import sys
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 METRIC = "trace events analyzed/sec (M ev/s) at 1 MI355X + achieved HBM GB/s % peak"
 HBM_PEAK_GBS = 8000.0
-# Stage used for the roofline (the radix passes: the largest share of the
-# device time) and the sources that define its kernels (the profiled traffic
-# is only trusted while these files are unchanged).
 ROOFLINE_STAGE = "sort"
 ROOFLINE_KERNEL = "k_radix_pass"
-STAGE_SOURCES = {"sort": ["paper_2609_40247_amd/csrc/radix.hip", "paper_2609_40247_amd/csrc/common.hpp",
-                          "paper_2609_40247_amd/csrc/internal.hpp"]}
 BYTES_PER_KEY_PASS = 24  # a digit pass reads and writes one 8-byte key and one 4-byte row index
+CSRC = os.path.join(ROOT, "paper_2609_40247_amd", "csrc")
+
+WORKLOADS = {
+    "config0": "tiny trace: 1 process, 2 streams, 10 s window, 20k kernels, 20k launches, 20k CPU ops",
+    "config1": "decode-step trace: 1 process, 4 streams, 30 s window, 1000 steps x 1000 kernels",
+    "config2": "mixed prefill/decode trace: 1 process, 8 streams (compute, comm, copy), 30 s window, 5M rows",
+    "config3": "node trace: 8 decode-step processes with clock offsets, 20k cross-process dependency edges",
+}
 
 
-def source_hash(stage: str) -> str:
+def sources_hash() -> str:
+    """Hash of every library source: a counter profile is trusted only while
+    the kernels it measured are unchanged."""
     h = hashlib.sha256()
-    for f in STAGE_SOURCES[stage]:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+    for d, pat in ((CSRC, (".hip", ".hpp")), (os.path.join(ROOT, "include"), (".h",))):
+        for f in sorted(os.listdir(d)):
+            if f.endswith(pat):
+                with open(os.path.join(d, f), "rb") as fh:
+                    h.update(f.encode())
+                    h.update(fh.read())
     return h.hexdigest()[:16]
+
+
+def profile_fields(workload: str):
+    """Per-call HBM traffic and summed kernel time of the analysis from the
+    committed rocprofv3 summary of this workload, if taken on the current
+    sources."""
+    path = os.path.join(ROOT, "profiles", f"pipeline_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    want = {"sources_sha256": r"sources_sha256:\s*([0-9a-f]+)", "hbm_bytes_per_call": r"hbm_bytes_per_call:\s*([0-9]+)",
+            "kernel_us_per_call": r"kernel_us_per_call:\s*([0-9.]+)",
+            "radix_hbm_bytes_per_launch": r"radix_hbm_bytes_per_launch:\s*([0-9]+)"}
+    got = {}
+    for k, pat in want.items():
+        m = re.search(pat, txt)
+        if not m:
+            return None
+        got[k] = m.group(1)
+    if got["sources_sha256"] != sources_hash():
+        return None
+    return {"hbm_bytes_per_call": int(got["hbm_bytes_per_call"]), "kernel_us_per_call": float(got["kernel_us_per_call"]),
+            "radix_hbm_bytes_per_launch": int(got["radix_hbm_bytes_per_launch"])}
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def algorithmic_bytes(n: int, counters: dict, params: dict, n_gaps: int) -> int:
+    """Bytes the analysis must read and write once: every input column
+    (37 B a row), the per-row links (8 B a row), the per-op aggregates
+    (28 B an admitted op, with containment), and the per-stream, per-name,
+    gap, overlap, histogram and edge outputs."""
+    flags = int(params.get("flags", 3))
+    P, S, NN = int(params["n_procs"]), int(params["n_streams"]), int(params["n_names"])
+    edges = params.get("edges")
+    E = 0 if edges is None else len(edges)
+    b = 37 * n + 8 * n
+    if flags & 1:
+        b += 28 * counters["n_admitted_cpu"]
+    b += 16 * P * S + 32 * NN + 64 * 8 + 25 * n_gaps + 8 * P + S + 112
+    if flags & 2:
+        b += 8 * (P * S * S + 12 * P)
+    b += 36 * E  # each edge read (24 B) and its wait and status written
+    return b
 
 
 def sort_units(stats):
     """Key-passes the radix launches of the sort stage must make, and the
     number of those launches.  Pass p of a sort is its digit first + p, where
     first is 1 when the sort leaves its lowest digit to the refine pass (bit
-    31 of its skipped-digit mask).  The stage makes as many passes as the
-    timeline and containment sorts need; the join sort (which moves data only
-    when the correlation table cannot be used) runs its passes in the same
-    launches.  A sort moves its keys once per pass whose digit is not
-    skipped."""
+    31 of its skipped-digit mask); a sort moves its keys once per pass whose
+    digit is not skipped."""
     def first(skipped):
         return 1 if (skipped >> 31) & 1 else 0
-    passes = max(nd - first(skipped) for _, skipped, nd in (stats[0], stats[2]))
+    sorts = [s for s in (stats[0], stats[2]) if s[2] > 0]
+    passes = max(nd - first(skipped) for _, skipped, nd in sorts)
     units = 0
-    for nkeys, skipped, nd in stats:
+    for nkeys, skipped, nd in sorts:
         f = first(skipped)
         units += nkeys * sum(1 for d in range(f, min(nd, f + passes)) if not (skipped >> d) & 1)
     return units, passes
-
-
-def profiled_traffic(stage: str, workload: str):
-    """HBM bytes per call of the stage from the committed rocprofv3 counter
-    summary, if it was taken on the current sources."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{ROOFLINE_KERNEL}_{workload}.md")
-    if not os.path.exists(path):
-        return None
-    txt = open(path).read()
-    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", txt)
-    m_b = re.search(r"hbm_bytes_per_call:\s*([0-9]+)", txt)
-    if not m_sha or not m_b or m_sha.group(1) != source_hash(stage):
-        return None
-    return int(m_b.group(1))
 
 
 def cpu_baseline(cols, params, n, budget_s=12.0, max_calls=30):
@@ -86,26 +138,32 @@ def cpu_baseline(cols, params, n, budget_s=12.0, max_calls=30):
             break
     dt = time.perf_counter() - t0
     return {"value": round(n * calls / dt / 1e6, 3), "unit": "M ev/s", "cores": 1, "kind": "oracle",
-            "sample": f"the same 2.99M-row trace analyzed {calls} times by the single-threaded C oracle "
-                      f"({dt:.1f} s on {os.cpu_count()} host cores, 1 used)"}
+            "cpu_model": cpu_model(), "host_cores": os.cpu_count(),
+            "sample": f"the same {n}-row trace analyzed {calls} times by the single-threaded C oracle "
+                      f"({dt:.1f} s, 1 of {os.cpu_count()} host cores used)"}
 
 
-def _config4_trace(t):
+def make_trace(workload: str):
     from paper_2609_40247_amd import synth
-    tr = synth.config4_trace(t)
-    return tr.columns(), tr.params
+    return {"config0": synth.config0, "config1": synth.config1, "config2": synth.config2,
+            "config3": synth.config3}[workload]()
+
+
+BATCH_OUTPUTS = ("name_count", "name_sum", "name_min", "name_max", "busy", "idle", "gap_pid", "gap_stream",
+                 "gap_begin", "gap_end", "gap_flags", "lat_hist", "counters")
 
 
 def run_config4(args) -> int:
     """One chunk of the 256-trace batch (traces 32c .. 32c+31, about 105M
-    rows) through the batch entry point, device-resident; then the same chunk
-    streamed from pinned host memory with double-buffered uploads."""
-    import multiprocessing as mp
+    rows) through the batch entry point with the batch output set (per-name
+    aggregates, busy / idle, gaps, latency histogram; the other outputs NULL),
+    device-resident; then the same chunk streamed from pinned host memory
+    with double-buffered uploads."""
     import numpy as np
+    from paper_2609_40247_amd import synth
     first = 32 * args.chunk
     ids = list(range(first, first + 32))
-    with mp.get_context("fork").Pool(min(16, os.cpu_count() or 1)) as pool:  # before the GPU is touched
-        gen = pool.map(_config4_trace, ids)
+    gen = synth.config4_chunk(ids)  # spawned workers, before the GPU is touched
     cols_l = [c for c, _ in gen]
     params_l = [p for _, p in gen]
     ns = [len(c["ts"]) for c in cols_l]
@@ -121,7 +179,9 @@ def run_config4(args) -> int:
     ans = [H.Analyzer(p, ns[t], workspace=(t == big)) for t, p in enumerate(params_l)]
     p0 = ans[0]._params_struct(ans[big].ws.data_ptr(), ans[big].ws_bytes)
     plist = [p0] + [a.params for a in ans[1:]]
-    outs = [a.outs for a in ans]
+    outs = [H.HerschelOutputs(gap_capacity=a.gap_capacity,
+                              **{k: (v.data_ptr() if k in BATCH_OUTPUTS else None) for k, v in a.o.items()})
+            for a in ans]
     dev = [H.device_columns(cols)]
     ev = H.events_struct(dev[0])
     torch.cuda.synchronize()
@@ -139,6 +199,15 @@ def run_config4(args) -> int:
         call(ev)
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    gaps, alg = 0, 0
+    for t, a in enumerate(ans):
+        c = {k: int(v) for k, v in zip(H.COUNTERS, a.o["counters"].cpu().tolist())}
+        g = min(c["n_gaps_total"], a.gap_capacity)
+        p = params_l[t]
+        gaps += g
+        # the batch set: every input column once, then busy / idle, the names,
+        # the gap list, the histogram and the counters
+        alg += 37 * ns[t] + 16 * p["n_procs"] * p["n_streams"] + 32 * p["n_names"] + 25 * g + 512 + 112
 
     # streamed: chunk i+1 uploads on a copy stream while chunk i is analyzed
     host = {k: torch.from_numpy(np.ascontiguousarray(v)).pin_memory() for k, v in cols.items()}
@@ -181,10 +250,12 @@ def run_config4(args) -> int:
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": {"workload": f"batch chunk {args.chunk} of the 256-trace set: traces {first}-{first + 31} "
                                "(decode-step traces of 200k-2M kernels, windows of ceil(L/1000) x 30 ms), "
-                               "names, busy/idle, gaps, latency histogram",
-                   "rows": n, "kernels": kernels, "traces": 32,
+                               "outputs: per-name aggregates, busy/idle, gaps, latency histogram",
+                   "rows": n, "kernels": kernels, "traces": 32, "gaps": int(gaps),
                    "kernel_records_per_s_M": round(kernels / (ms * 1e-3) / 1e6, 3),
                    "est_ms_for_256_traces": round(ms * 8, 1)},
+        "whole_call": {"algorithmic_bytes": alg, "algorithmic_GBps": round(alg / (ms * 1e-3) / 1e9, 1),
+                       "frac": round(alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
         "streamed": {"value": round(n / (stream_ms * 1e-3) / 1e6, 3), "unit": "M ev/s", "ms_per_chunk":
                      round(stream_ms, 3), "h2d_bytes_per_chunk": nbytes,
                      "h2d_GBps": round(nbytes / h2d_s / 1e9, 2)},
@@ -202,9 +273,9 @@ def run_config4(args) -> int:
                 break
         dt = time.perf_counter() - t0
         out["cpu_baseline"] = {"value": round(done_rows / dt / 1e6, 3), "unit": "M ev/s", "cores": 1,
-                               "kind": "oracle", "sample": f"the first {used} traces of the chunk "
-                               f"({done_rows} rows) analyzed once each by the single-threaded C oracle "
-                               f"({dt:.1f} s)"}
+                               "kind": "oracle", "cpu_model": cpu_model(), "host_cores": os.cpu_count(),
+                               "sample": f"the first {used} traces of the chunk ({done_rows} rows) analyzed once "
+                                         f"each by the single-threaded C oracle ({dt:.1f} s)"}
     print(json.dumps(out), flush=True)
     return 0
 
@@ -215,13 +286,14 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache timing")
     ap.add_argument("--stages", action="store_true", help="also print a per-stage breakdown to stderr")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="first copy a buffer of this many MiB on the device (a plain copy kernel of known "
                          "size, for scaling rocprofv3 byte counters)")
-    ap.add_argument("--workload", choices=("config1", "config4"), default="config1",
-                    help="config1: the decode-step trace (the headline line); config4: one 32-trace chunk of "
-                         "the batch workload through the batch entry point")
+    ap.add_argument("--workload", choices=tuple(WORKLOADS) + ("config4",), default="config1",
+                    help="config1: the decode-step trace (the headline line); config0, config2, config3: the "
+                         "other single-window workloads; config4: one 32-trace chunk of the batch workload")
     ap.add_argument("--chunk", type=int, default=0, help="config4: which of the 8 chunks")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -231,10 +303,9 @@ def main() -> int:
     if args.workload == "config4":
         return run_config4(args)
 
-    import numpy as np
+    tr = make_trace(args.workload)  # generated before the GPU is touched
     import torch
     from paper_2609_40247_amd import herschel as H
-    from paper_2609_40247_amd import synth
 
     if args.copy_mb > 0:
         src = torch.empty(args.copy_mb << 20, dtype=torch.uint8, device="cuda").fill_(1)
@@ -244,17 +315,21 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    tr = synth.config1()
     n = tr.n
     an = H.Analyzer(tr.params, n)
     dcols = H.device_columns(tr.columns())
     ev = H.events_struct(dcols)
     torch.cuda.synchronize()
-    for _ in range(args.warmup):
+
+    def run():
         code = an.run(ev, n)
         if code != 0:
             raise RuntimeError(f"analysis failed: {H.herschel_strerror(code)}")
-    c = an.results(n)["counters"]
+
+    for _ in range(args.warmup):
+        run()
+    res = an.results(n)
+    c = res["counters"]
     units, launches = sort_units(H.herschel_sort_stats(an.params))
 
     # the timed region: K calls as a user makes them (repeated calls with the
@@ -262,12 +337,28 @@ def main() -> int:
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        code = an.run(ev, n)
-        if code != 0:
-            raise RuntimeError(f"analysis failed: {H.herschel_strerror(code)}")
+        run()
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms = (t1 - t0) * 1e3 / args.steps
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    # cold cache: before each call a 1 GiB fill evicts the caches (the 256 MB
+    # last-level cache included); each call is timed on its own, and so are
+    # warm calls the same way for comparison
+    cold = None
+    if not args.no_cold:
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        cold_ms, warm_ms = [], []
+        for i in range(min(args.steps, 20)):
+            flush.fill_(i & 0xFF)
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            run()
+            cold_ms.append((time.perf_counter() - t) * 1e3)
+            t = time.perf_counter()
+            run()
+            warm_ms.append((time.perf_counter() - t) * 1e3)
+        del flush
+        cold = (statistics.median(cold_ms), statistics.median(warm_ms))
 
     # the roofline kernel: HIP events around the sort stage, recorded on the
     # stream its passes run on, over another K calls (launched directly, since
@@ -281,9 +372,7 @@ def main() -> int:
     torch.cuda.synchronize()
     for a, b in pairs:
         H.herschel_time_stage(stage_id, a, b)
-        code = an.run(ev, n)
-        if code != 0:
-            raise RuntimeError(f"analysis failed: {H.herschel_strerror(code)}")
+        run()
     torch.cuda.synchronize()
     H.herschel_time_stage(stage_id, None, None)
     stage_ms = sum(a.elapsed_time(b) for a, b in pairs) / args.steps
@@ -306,19 +395,31 @@ def main() -> int:
     alg = BYTES_PER_KEY_PASS * units / launches
     launch_s = stage_ms * 1e-3 / launches
     achieved = alg / launch_s / 1e9
-    traffic = profiled_traffic(ROOFLINE_STAGE, "config1")
-    traffic = None if traffic is None else round(traffic / launches)
+    prof = profile_fields(args.workload)
+    gaps = min(c["n_gaps_total"], an.gap_capacity)
+    call_bytes = algorithmic_bytes(n, c, tr.params, gaps)
+    whole = {"algorithmic_bytes": call_bytes, "algorithmic_GBps": round(call_bytes / (ms * 1e-3) / 1e9, 1),
+             "frac": round(call_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+             "traffic_bytes": None, "kernel_us": None, "traffic_GBps": None, "traffic_frac": None}
+    if cold is not None:
+        whole.update({"cold_ms_per_call": round(cold[0], 4), "warm_ms_per_call_same_timing": round(cold[1], 4),
+                      "cold_algorithmic_GBps": round(call_bytes / (cold[0] * 1e-3) / 1e9, 1)})
+    if prof is not None:
+        tb, ku = prof["hbm_bytes_per_call"], prof["kernel_us_per_call"]
+        whole.update({"traffic_bytes": tb, "kernel_us": ku, "traffic_GBps": round(tb / (ku * 1e-6) / 1e9, 1),
+                      "traffic_frac": round(tb / (ku * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
     out = {
         "metric": METRIC, "value": round(n / (ms * 1e-3) / 1e6, 3), "unit": "M ev/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
-        "config": {"workload": "decode-step trace: 1 process, 4 streams, 30 s window, 1000 steps x 1000 kernels",
-                   "rows": n, "kernels": c["n_admitted_kernel"], "launches": c["n_admitted_launch"],
-                   "cpu_ops": c["n_admitted_cpu"], "outputs": "all"},
+        "config": {"workload": WORKLOADS[args.workload], "rows": n, "kernels": c["n_admitted_kernel"],
+                   "launches": c["n_admitted_launch"], "cpu_ops": c["n_admitted_cpu"], "outputs": "all"},
         "roofline": {"kernel": ROOFLINE_KERNEL, "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "algorithmic_bytes": round(alg), "launch_us": round(launch_s * 1e6, 2),
+                     "traffic": None if prof is None else prof["radix_hbm_bytes_per_launch"],
+                     "algorithmic_bytes": round(alg), "launch_us": round(launch_s * 1e6, 2),
                      "launches_per_step": launches, "key_passes_per_step": units},
+        "whole_call": whole,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(tr.columns(), tr.params, n)

@@ -33,6 +33,8 @@ from __future__ import annotations
 import dataclasses
 import math
 
+import os
+
 import numpy as np
 
 CPU_OP, LAUNCH, KERNEL = 0, 1, 2
@@ -472,6 +474,24 @@ def config4_trace(t: int, kernels: int | None = None) -> Trace:
     params = empty_params(window_begin=w0, window_end=w0 + n_steps * period, gap_threshold=20 * US,
                           n_procs=1, n_streams=4, n_threads=1, n_names=2000, n_op_names=100, flags=0)
     return _assemble(rng, [pr], [0], params, f"config4[{t}]")
+
+
+def _config4_columns(t: int):
+    tr = config4_trace(t)
+    return tr.columns(), tr.params
+
+
+def config4_chunk(ids, workers: int = 16):
+    """Columns and params of the batch traces `ids`, generated by a pool of
+    fresh worker processes (spawned, so that a parent that already uses the
+    GPU forks nothing)."""
+    import multiprocessing as mp
+    ids = [int(t) for t in ids]
+    workers = max(1, min(workers, len(ids), os.cpu_count() or 1))
+    if workers == 1:
+        return [_config4_columns(t) for t in ids]
+    with mp.get_context("spawn").Pool(workers) as pool:
+        return pool.map(_config4_columns, ids)
 
 
 def config4_lengths(n_traces: int = 256) -> np.ndarray:

@@ -598,3 +598,51 @@ def test_null_outputs(H, which, flags):
             raw = an.o[k].cpu().numpy()
             assert (raw == (7 if raw.dtype == np.uint8 else oracle.UNWRITTEN_I64)).all(), (which, k)
 
+
+# --------------------------------------------------------------- batch at full size
+BATCH_OUTPUTS = ("name_count", "name_sum", "name_min", "name_max", "busy", "idle", "gap_pid", "gap_stream",
+                 "gap_begin", "gap_end", "gap_flags", "lat_hist")
+
+
+@pytest.mark.slow
+def test_config4_chunk_full_size(H):
+    """One chunk of the 256-trace batch at its stated size through the batch
+    entry point with the batch output set (every other output NULL, flags 0):
+    32 traces including the shortest (trace 234, 0.21M kernels) and the
+    longest (trace 44, 1.99M kernels), about 110M rows; every trace compared
+    with the oracle element by element."""
+    lengths = synth.config4_lengths()
+    shortest, longest = int(np.argmin(lengths)), int(np.argmax(lengths))
+    ids = [longest, shortest] + [t for t in range(32, 64) if t not in (longest, shortest)][:30]
+    print(f"generating traces {ids}", flush=True)
+    gen = synth.config4_chunk(ids)
+    ns = [len(c["ts"]) for c, _ in gen]
+    offs = np.cumsum([0] + ns).astype(np.int64)
+    cols = {k: np.concatenate([c[k] for c, _ in gen]) for k in gen[0][0]}
+    print(f"{len(ids)} traces, {int(offs[-1])} rows", flush=True)
+    d = H.device_columns(cols)
+    del cols
+    big = int(np.argmax(ns))
+    ans, outs = [], []
+    for t, (c, p) in enumerate(gen):
+        cap = int(np.count_nonzero(c["kind"] == 2)) + p["n_procs"] * p["n_streams"]
+        an = H.Analyzer(p, ns[t], gap_capacity=cap, workspace=(t == big))
+        ans.append(an)
+        outs.append(H.HerschelOutputs(gap_capacity=cap, **{k: (v.data_ptr() if k in BATCH_OUTPUTS or
+                                                                 k == "counters" else None)
+                                                             for k, v in an.o.items()}))
+    p0 = ans[0]._params_struct(ans[big].ws.data_ptr(), ans[big].ws_bytes)
+    torch.cuda.synchronize()
+    print("batch call", flush=True)
+    code = H.herschel_trace_analyze_batch(H.events_struct(d), offs, [p0] + [a.params for a in ans[1:]], outs)
+    torch.cuda.synchronize()
+    assert code == 0, H.herschel_strerror(code)
+    for t, ((c, p), an) in enumerate(zip(gen, ans)):
+        res = an.results(ns[t])
+        ocode, o = oracle.analyze(c, p, gap_capacity=an.gap_capacity)
+        assert ocode == 0
+        assert res["counters"] == {**o["counters"], "device_status": 0}, ids[t]
+        for k in BATCH_OUTPUTS:
+            assert np.array_equal(res[k], o[k]), (ids[t], k)
+        print(f"trace {ids[t]}: {ns[t]} rows identical", flush=True)
+
