@@ -79,7 +79,7 @@ class _Outputs(ctypes.Structure):
                 ("name_sum", _P), ("name_min", _P), ("name_max", _P), ("lat_hist", _P),
                 ("edge_wait", _P), ("edge_status", _P), ("gap_capacity", ctypes.c_int64),
                 ("gap_pid", _P), ("gap_stream", _P), ("gap_begin", _P), ("gap_end", _P),
-                ("gap_flags", _P), ("counters", _P)]
+                ("gap_flags", _P), ("counters", _P), ("dev_idle", _P), ("op_span", _P), ("op_idle", _P)]
 
 
 def _ptr(a):
@@ -122,6 +122,8 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
         gap_pid=np.zeros(max(gap_capacity, 1), np.int32), gap_stream=np.zeros(max(gap_capacity, 1), np.int32),
         gap_begin=np.zeros(max(gap_capacity, 1), np.int64), gap_end=np.zeros(max(gap_capacity, 1), np.int64),
         gap_flags=np.zeros(max(gap_capacity, 1), np.uint8),
+        dev_idle=np.zeros(P, np.int64), op_span=np.zeros(P * int(params["n_op_names"]), np.int64),
+        op_idle=np.zeros(P * int(params["n_op_names"]), np.int64),
     )
     counters = np.zeros(len(COUNTER_NAMES), np.int64)
     ev = _Events(**{k: _ptr(v) for k, v in c.items()})

@@ -24,6 +24,7 @@
  *   14. cross-stream overlap as interval coverage (panel "Overlap and exposed
  *       work"; Section 6.1 "Execution progress and state")
  *   15. cross-process dependency waits (panel "Cross-process blocking")
+ *   16. GPU idle coinciding with CPU ops, by op name (Section 9.1)
  *
  * Sorting uses the C library's qsort with comparators that end in the row
  * index, so every order is total and the result does not depend on qsort's
@@ -77,6 +78,9 @@ static int params_ok(int64_t n, const hro_params *p) {
   if (p->n_names < 1 || p->n_names > (1 << 24)) return 0;
   if (p->n_op_names < 1) return 0;
   if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return 0;
+  /* implementation limit shared with the library, for error parity: with
+   * the idle-coincidence outputs, at most 2048 op names */
+  if ((p->flags & 4u) != 0 && p->n_op_names > 2048) return 0;
   if (p->clock_offset)
     for (int q = 0; q < p->n_procs; ++q)
       if (!in_abs(p->clock_offset[q])) return 0;
@@ -528,6 +532,78 @@ int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p
       out->edge_wait[e] = (found[0] && found[1]) ? wrap_sub(cons_start, prod_end) : I64_MIN;
     }
     free(kc);
+  }
+
+  /* 16. GPU idle coinciding with CPU ops, by op name (the evidence of the
+   *     case study in Section 9.1: idle intervals of the GPU activity that
+   *     coincide with the Worker's waits in one Python call).  READING: the
+   *     GPU of process p is idle where none of its streams' kernels covers
+   *     the time; its idle intervals are the maximal such sub-intervals of
+   *     [W0, W1), kept when longer than the gap threshold (as gaps are).
+   *     Per op name o of process p, U = the union of its admitted ops'
+   *     ranges [ts', min(te', W1)); op_span = |U|, op_idle = |U and the kept
+   *     idle intervals|, dev_idle[p] = their total length. */
+  if ((p->flags & 4u) != 0) {
+    const int NOP = p->n_op_names;
+    /* the admitted ops' non-empty clipped ranges, by (process, name, start) */
+    int64_t nc = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (adm[i] && ev->kind[i] == K_CPU) ++nc;
+    rec4 *orc = (rec4 *)malloc(sizeof(rec4) * (size_t)(nc > 0 ? nc : 1));
+    int64_t no = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (adm[i] && ev->kind[i] == K_CPU) {
+        int64_t e = te[i] < W1 ? te[i] : W1;
+        if (e > ts[i]) {
+          orc[no].a = (int64_t)ev->pid[i] * NOP + ev->name[i];
+          orc[no].b = ts[i];
+          orc[no].c = e;
+          orc[no].row = i;
+          ++no;
+        }
+      }
+    qsort(orc, (size_t)no, sizeof(rec4), cmp_rec4);
+    for (int64_t q = 0; q < (int64_t)P * NOP; ++q) {
+      out->op_span[q] = 0;
+      out->op_idle[q] = 0;
+    }
+    ival *u = (ival *)malloc(sizeof(ival) * (size_t)(no > 0 ? no : 1));
+    int64_t at = 0;
+    for (int pp = 0; pp < P; ++pp) {
+      ival *all;
+      int64_t nall = union_of(runs + (int64_t)pp * S, nruns + (int64_t)pp * S, S, &all);
+      /* the complement of the busy runs in [W0, W1), long ones only */
+      ival *idle = (ival *)malloc(sizeof(ival) * (size_t)(nall + 1));
+      int64_t ni = 0, prev = W0, tot = 0;
+      for (int64_t q = 0; q <= nall; ++q) {
+        int64_t gb = prev, ge = q < nall ? all[q].s : W1;
+        if (ge > gb && ge - gb > p->thr) {
+          idle[ni].s = gb;
+          idle[ni].e = ge;
+          tot += ge - gb;
+          ++ni;
+        }
+        if (q < nall) prev = all[q].e;
+      }
+      out->dev_idle[pp] = tot;
+      /* each op name of this process: union of its ranges, then the idle part */
+      while (at < no && orc[at].a / NOP == pp) {
+        int64_t seg = orc[at].a, w = 0;
+        while (at < no && orc[at].a == seg) {
+          u[w].s = orc[at].b;
+          u[w].e = orc[at].c;
+          ++w;
+          ++at;
+        }
+        int64_t r = merge_runs(u, w);
+        out->op_span[seg] = runs_length(u, r);
+        out->op_idle[seg] = runs_intersection(u, r, idle, ni);
+      }
+      free(idle);
+      free(all);
+    }
+    free(u);
+    free(orc);
   }
 
   for (int64_t ps = 0; ps < (int64_t)P * S; ++ps) free(runs[ps]);

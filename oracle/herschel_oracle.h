@@ -38,7 +38,7 @@ typedef struct {
   const uint8_t *stream_class; /* may be NULL */
   const hro_edge *edges;
   int64_t n_edges;
-  uint32_t flags; /* bit0: containment, bit1: overlap */
+  uint32_t flags; /* bit0: containment, bit1: overlap, bit2: idle coincidence */
 } hro_params;
 
 typedef struct {
@@ -60,6 +60,8 @@ typedef struct {
   int64_t *gap_begin, *gap_end;
   uint8_t *gap_flags;
   hro_counters *counters;
+  int64_t *dev_idle;        /* [n_procs] (flags bit 2) */
+  int64_t *op_span, *op_idle; /* [n_procs * n_op_names] (flags bit 2) */
 } hro_outputs;
 
 /* Same return codes as the product: 0 ok, -1 bad parameter, -2 invalid row,

@@ -211,6 +211,31 @@ def analyze(cols: dict, p: dict):
         ov = dict(pair_overlap=pair.reshape(-1), class_busy=cb.reshape(-1),
                   class_overlap=co.reshape(-1), any_busy=anyb)
 
+    waits = None
+    if p["flags"] & 4:
+        # GPU idle: no stream of the process covers the ns; runs of idle ns
+        # longer than the threshold count; per op name, the ns covered by any
+        # of its admitted ops (clipped at W1)
+        nop = p["n_op_names"]
+        dev_idle = np.zeros(P, np.int64)
+        span = np.zeros((P, nop), np.int64)
+        oidle = np.zeros((P, nop), np.int64)
+        for q in range(P):
+            idle_ns = np.zeros(W, bool)
+            for a, b in _runs(~cov[q].any(axis=0)):
+                if b - a > p["gap_threshold"]:
+                    idle_ns[a:b] = True
+            dev_idle[q] = idle_ns.sum()
+            for o in range(nop):
+                m = np.zeros(W, bool)
+                for i in ops:
+                    r = rows[i]
+                    if r["pid"] == q and r["name"] == o:
+                        m[r["t0"] - W0:min(r["t1"], W1) - W0] = True
+                span[q, o] = m.sum()
+                oidle[q, o] = np.count_nonzero(m & idle_ns)
+        waits = dict(dev_idle=dev_idle, op_span=span.reshape(-1), op_idle=oidle.reshape(-1))
+
     edges = p.get("edges")
     ew, es = [], []
     for e in ([] if edges is None else edges):
@@ -227,6 +252,6 @@ def analyze(cols: dict, p: dict):
                busy=busy, idle=idle, gaps=gaps, lat_hist=np.array(hist, np.int64),
                name_count=np.array(ncount, np.int64), name_sum=np.array(nsum, np.int64),
                name_min=np.array(nmin, np.int64), name_max=np.array(nmax, np.int64),
-               op=op_arrays, overlap=ov, edge_wait=np.array(ew, np.int64),
+               op=op_arrays, overlap=ov, waits=waits, edge_wait=np.array(ew, np.int64),
                edge_status=np.array(es, np.int32))
     return 0, out

@@ -37,6 +37,12 @@ MUTANTS = [
     ("zero-length rows invalid", "if (ev->te[i] < ev->ts[i]) return 0;", "if (ev->te[i] <= ev->ts[i]) return 0;"),
     ("row tie-break reversed", "if (u->row != v->row) return u->row < v->row ? -1 : 1;",
      "if (u->row != v->row) return u->row > v->row ? -1 : 1;"),
+    ("idle threshold inclusive", "if (ge > gb && ge - gb > p->thr) {", "if (ge > gb && ge - gb >= p->thr) {"),
+    ("GPU idle from one stream", "union_of(runs + (int64_t)pp * S, nruns + (int64_t)pp * S, S, &all);",
+     "union_of(runs + (int64_t)pp * S, nruns + (int64_t)pp * S, 1, &all);"),
+    ("op ranges unclipped", "int64_t e = te[i] < W1 ? te[i] : W1;", "int64_t e = te[i];"),
+    ("op time intersected with busy", "runs_intersection(u, r, idle, ni);", "runs_intersection(u, r, all, nall);"),
+    ("op ranges not merged", "int64_t r = merge_runs(u, w);\n        out->op_span", "int64_t r = w;\n        out->op_span"),
     ("join ignores pid", "if (lo < nl && lr[lo].a == ev->pid[i] && lr[lo].b == ev->corr[i]) {",
      "if (lo < nl && lr[lo].b == ev->corr[i]) {"),
     ("latency sign", "int64_t x = ts[i] - ts[l];", "int64_t x = ts[l] - ts[i];"),
@@ -87,7 +93,9 @@ def _battery(lib) -> None:
         code, o = oracle.analyze(cols, p, lib=lib)
         assert code == g["expect"]["code"]
         pins._check_expect(o, cols, g["expect"])
-    for case in pins.BF_CASES[::4] + pins.BF_CASES[-40:]:
+    many_procs = [c for c in pins.BF_CASES if 4000 <= c["seed"] < 4100]
+    waits = [c for c in pins.BF_CASES if c["seed"] >= 5000][::2]
+    for case in pins.BF_CASES[::4] + many_procs + waits:
         tr = synth.random_small(**case)
         code, o = oracle.analyze(tr.columns(), tr.params, lib=lib)
         bcode, b = bruteforce.analyze(tr.columns(), tr.params)
@@ -98,6 +106,12 @@ def _battery(lib) -> None:
     code, o = oracle.analyze(tr.columns(), tr.params, lib=lib)
     pins._invariants(tr, o)
     pins._truth_check(tr, o)
+    cols, p, g = load_golden("t1_worked_timeline.json")
+    exp = g["expect_waits"]
+    p["flags"] = exp["flags"]
+    code, o = oracle.analyze(cols, p, lib=lib)
+    for k in ("dev_idle", "op_span", "op_idle"):
+        assert o[k].tolist() == exp[k], k
 
 
 @pytest.fixture(scope="module")

@@ -97,6 +97,9 @@ def _bf_compare(cols, p, o, b, ctx):
     if p["flags"] & 2:
         for k, v in b["overlap"].items():
             assert o[k].tolist() == v.tolist(), f"{ctx}: {k}"
+    if p["flags"] & 4:
+        for k, v in b["waits"].items():
+            assert o[k].tolist() == v.tolist(), f"{ctx}: {k}"
 
 
 BF_CASES = [dict(seed=s) for s in range(120)] + [
@@ -106,7 +109,11 @@ BF_CASES = [dict(seed=s) for s in range(120)] + [
     # many processes sharing few correlation ids: a join that forgets the
     # process would find another process's launch
     dict(seed=4000 + s, n_rows=30, window=200, n_procs=4, n_streams=2, n_threads=2, corr_range=3)
-    for s in range(40)]
+    for s in range(40)] + [
+    # GPU idle coinciding with ops, with every other output and alone
+    dict(seed=5000 + s, flags=7 if s % 2 else 4) for s in range(40)] + [
+    dict(seed=5100 + s, n_rows=150, window=700, n_procs=2, n_streams=3, n_threads=3, n_op_names=3, flags=7)
+    for s in range(20)]
 
 
 @pytest.mark.parametrize("case", BF_CASES, ids=lambda c: f"seed{c['seed']}")
@@ -498,3 +505,61 @@ def test_empty_trace():
     assert o["counters"]["n_gaps_total"] == 6 and (o["gap_flags"] == 3).all()
     assert (o["name_min"] == I64_MAX).all() and (o["name_max"] == I64_MIN).all()
     assert (o["any_busy"] == 0).all() and o["lat_hist"].sum() == 0
+
+
+# --------------------------------------------------------------------------- GPU idle x CPU ops
+
+def test_t1_idle_coincidence():
+    """Hand-worked values of GPU idle coinciding with op names on T1, and the
+    strict threshold (an idle interval as long as the threshold is dropped)."""
+    cols, p, g = load_golden("t1_worked_timeline.json")
+    exp = g["expect_waits"]
+    p["flags"] = exp["flags"]
+    code, o = oracle.analyze(cols, p)
+    assert code == 0
+    for k in ("dev_idle", "op_span", "op_idle"):
+        assert o[k].tolist() == exp[k], k
+    p["gap_threshold"] = 10
+    code, o = oracle.analyze(cols, p)
+    for k in ("dev_idle", "op_span", "op_idle"):
+        assert o[k].tolist() == exp["thr10"][k], k
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_idle_coincidence_invariants(seed):
+    """op_idle <= op_span and <= dev_idle; with threshold -1 the GPU idle is
+    the window minus the time any stream is busy; an op spanning the whole
+    window of every process sees all of its GPU idle."""
+    tr = synth.random_small(seed=5200 + seed, n_rows=400, window=3000, n_procs=3, n_streams=4, n_threads=3,
+                            corr_range=60, flags=7)
+    cols, p = tr.columns(), dict(tr.params)
+    code, o = oracle.analyze(cols, p)
+    nop = p["n_op_names"]
+    span, idle = o["op_span"].reshape(-1, nop), o["op_idle"].reshape(-1, nop)
+    assert (idle <= span).all() and (idle <= o["dev_idle"][:, None]).all()
+    p["gap_threshold"] = -1
+    code, o = oracle.analyze(cols, p)
+    W = p["window_end"] - p["window_begin"]
+    assert (o["dev_idle"] == W - o["any_busy"]).all()
+    # one more op per process covering the window, with its own name
+    P = p["n_procs"]
+    off = p["clock_offset"] if p["clock_offset"] is not None else np.zeros(P, np.int64)
+    extra = dict(kind=np.zeros(P, np.uint8), pid=np.arange(P, dtype=np.int32), lane=np.zeros(P, np.int32),
+                 ts=(p["window_begin"] + off).astype(np.int64), te=(p["window_end"] + off).astype(np.int64),
+                 corr=np.zeros(P, np.int64), name=np.full(P, nop, np.int32))
+    c2 = {k: np.concatenate([cols[k], extra[k]]) for k in cols}
+    p2 = dict(p, n_op_names=nop + 1, gap_threshold=int(tr.params["gap_threshold"]))
+    code, o2 = oracle.analyze(c2, p2)
+    whole = o2["op_idle"].reshape(-1, nop + 1)[:, nop]
+    assert (whole == o2["dev_idle"]).all()
+    assert (o2["op_span"].reshape(-1, nop + 1)[:, nop] == W).all()
+
+
+def test_idle_coincidence_name_limit():
+    cols, p = _t1()
+    p["flags"] = 7
+    p["n_op_names"] = 2048
+    assert oracle.analyze(cols, p)[0] == 0
+    p["n_op_names"] = 2049
+    assert oracle.analyze(cols, p)[0] == -1
+
