@@ -62,6 +62,7 @@ enum {
  * the latency histogram and the per-name aggregates are always produced. */
 #define HERSCHEL_OUT_CONTAIN 0x1u /* op nesting, launch->op, kernel->op, per-op aggregates */
 #define HERSCHEL_OUT_OVERLAP 0x2u /* cross-stream overlap and class coverage */
+#define HERSCHEL_OUT_WAITS 0x4u   /* GPU idle coinciding with CPU ops, by op name (Section 9.1) */
 
 /* Implementation limits (checked; EINVAL when exceeded). */
 #define HERSCHEL_MAX_PROCS 4096
@@ -70,6 +71,7 @@ enum {
 #define HERSCHEL_MAX_WINDOW (1LL << 40)  /* W1 - W0 in ns (about 18 minutes) */
 #define HERSCHEL_MAX_ABS_TIME (1LL << 62) /* |ts|, |te|, |W0|, |W1|, |clock offset| must be below */
 #define HERSCHEL_MAX_NAMES (1 << 24)
+#define HERSCHEL_MAX_WAIT_OP_NAMES 2048   /* n_op_names with HERSCHEL_OUT_WAITS */
 #define HERSCHEL_MAX_ROWS (1LL << 30)      /* n must be below: overlap endpoints (two per kernel) are
                                               indexed with int32, radix look-back words hold 30-bit prefixes */
 
@@ -163,6 +165,14 @@ typedef struct {
   int64_t *gap_begin, *gap_end;      /* [gap_capacity] */
   uint8_t *gap_flags;                /* [gap_capacity] bit0 leading (at W0), bit1 trailing (at W1) */
   herschel_counters *counters;       /* device pointer */
+  /* HERSCHEL_OUT_WAITS (the idle evidence of the case study in Section 9.1):
+   * the GPU of process p is idle where no kernel of any of its streams covers
+   * the time; its idle intervals are the maximal ones in [W0, W1) longer
+   * than gap_threshold.  For op name o of process p, U(p, o) is the union of
+   * its admitted ops' ranges [ts', min(te', W1)). */
+  int64_t *dev_idle;                 /* [n_procs] total length of the idle intervals */
+  int64_t *op_span;                  /* [n_procs * n_op_names] |U(p, o)| */
+  int64_t *op_idle;                  /* [n_procs * n_op_names] |U(p, o) within the idle intervals| */
 } herschel_outputs;
 
 /* Bytes of device workspace that herschel_trace_analyze needs for n rows
@@ -232,7 +242,8 @@ enum {
   HERSCHEL_STAGE_OPAGG = 9,    /* kernel -> op, inclusive per-op aggregates */
   HERSCHEL_STAGE_EDGES = 10,   /* dependency waits */
   HERSCHEL_STAGE_FINAL = 11,   /* counters and histogram totals */
-  HERSCHEL_N_STAGES = 12
+  HERSCHEL_STAGE_WAITS = 12,   /* device-lane and op-name unions, idle coincidence (OUT_WAITS) */
+  HERSCHEL_N_STAGES = 13
 };
 
 /* Record start_event / stop_event (hipEvent_t, created by the caller) on

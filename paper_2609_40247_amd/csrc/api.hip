@@ -37,6 +37,14 @@ struct Bump {
   }
 };
 
+// Sorts the call runs: the timeline always, containment and the two
+// idle-coincidence sorts with their outputs.
+static bool sort_used(const Ctx& c, const SortBufs* s) {
+  if (s == &c.sK) return true;
+  if (s == &c.sC) return c.contain;
+  return c.waits;
+}
+
 // refine: whether the lowest bits are left to the refine pass (keys wider
 // than 32 bits, whose low bits are nanoseconds: runs of keys equal above
 // them are short)
@@ -55,12 +63,22 @@ size_t layout_workspace(Ctx& c, char* base) {
   c.zero_begin = base ? base + b.off : nullptr;
   const size_t z0 = b.off;
   c.prep_tiles = cdiv(c.n, prep_tile_rows());
-  c.prep_status = b.take<uint64_t>(3 * std::max<int64_t>(c.prep_tiles, 1));
+  c.prep_status = b.take<uint64_t>(4 * std::max<int64_t>(c.prep_tiles, 1));
   c.union_tiles = std::max<int64_t>(cdiv(n, union_tile_elems()), 1);
   c.union_status = b.take<uint64_t>(3 * c.union_tiles);
   // key widths (also reported by herschel_sort_stats)
-  sort_plan(c.sK, 0, n, c.pb + c.sb + c.wb, true);
-  sort_plan(c.sC, 1, n, c.pb + c.tb + c.wb + 1, true);
+  sort_plan(c.sK, SORT_K, n, c.pb + c.sb + c.wb, true);
+  sort_plan(c.sC, SORT_C, n, c.pb + c.tb + c.wb + 1, true);
+  if (c.waits) {
+    sort_plan(c.sD, SORT_D, n, c.pb + c.wb, true);
+    sort_plan(c.sO, SORT_O, n, c.pb + c.nob + c.wb, true);
+    c.union_status_d = b.take<uint64_t>(3 * c.union_tiles);
+    c.union_status_o = b.take<uint64_t>(3 * c.union_tiles);
+    c.dg_cap = n + c.P;  // idle intervals: at most one more per process than kernels
+    c.dg_tiles = std::max<int64_t>(cdiv(c.dg_cap, 4096), 1);
+    c.dg_status = b.take<uint64_t>(c.dg_tiles);
+    c.dbusy_ws = b.take<int64_t>(c.P);
+  }
   if (c.contain) {
     c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
     c.vb_status = b.take<uint64_t>(c.vb_tiles);
@@ -75,13 +93,14 @@ size_t layout_workspace(Ctx& c, char* base) {
   c.zero_bytes = align_up(b.off - z0);
   // the first digit's look-back words are cleared by the histogram kernel
   // (for the tiles of the call), each later digit's by the pass before it
-  c.sK.status0 = b.take<uint32_t>(c.sK.tiles_max * RS_LB_WORDS);
-  if (c.contain) c.sC.status0 = b.take<uint32_t>(c.sC.tiles_max * RS_LB_WORDS);
-  for (SortBufs* s : {&c.sK, &c.sC})
-    if (s != &c.sC || c.contain) s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * RS_LB_WORDS);
+  for (SortBufs* s : {&c.sK, &c.sC, &c.sD, &c.sO}) {
+    if (!sort_used(c, s)) continue;
+    s->status0 = b.take<uint32_t>(s->tiles_max * RS_LB_WORDS);
+    s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * RS_LB_WORDS);
+  }
   // long runs of the refine pass (each has more than RF_SHORT keys)
   c.rf_cap = cdiv(n, RF_SHORT + 1) + 1;
-  c.rf_list = b.take<int32_t>(2 * c.rf_cap);
+  c.rf_list = b.take<int32_t>(N_SORTS * c.rf_cap);
   c.hist_part = b.take<uint32_t>((int64_t)N_SORTS * HIST_MAX_BLOCKS * 8 * 256);
   c.k_rows = b.take<uint32_t>(n);
   // the join: prep's list, the correlation table (two slots per row bound
@@ -103,7 +122,8 @@ size_t layout_workspace(Ctx& c, char* base) {
   c.jt_fix_cap = n;
   c.jt_fix = b.take<uint32_t>(3 * c.jt_fix_cap);
   // sort buffers
-  for (SortBufs* s : {&c.sK, &c.sC}) {
+  for (SortBufs* s : {&c.sK, &c.sC, &c.sD, &c.sO}) {
+    if ((s == &c.sD || s == &c.sO) && !c.waits) continue;
     if (s == &c.sC && !c.contain) {
       // the containment list is still compacted by prep (ops and launches)
       s->k[0] = b.take<uint64_t>(n);
@@ -142,6 +162,15 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.aux_ws = b.take<int32_t>(n);
   }
   c.busy_ws = b.take<int64_t>((int64_t)c.P * c.S);
+  if (c.waits) {
+    c.dg_pid = b.take<int32_t>(c.dg_cap);
+    c.dg_begin = b.take<int64_t>(c.dg_cap);
+    c.dg_end = b.take<int64_t>(c.dg_cap);
+    c.dg_pre = b.take<int64_t>(c.dg_cap);
+    c.oev_cap = 2 * n;
+    c.oev = b.take<uint64_t>(c.oev_cap);
+    c.op_span_ws = b.take<int64_t>((int64_t)c.P * c.NOP);
+  }
   c.name_blocks = names_block_count(n, c.NN);
   if (c.NN <= names_lds_limit()) c.name_part = b.take<uint64_t>((int64_t)c.name_blocks * c.NN * 4);
   return b.off;
@@ -169,6 +198,9 @@ struct InitArgs {
   int64_t* name_max;
   const int64_t* off;
   const uint8_t* cls;
+  int64_t n_opn;      // P * n_op_names with the idle-coincidence outputs, else 0
+  int64_t* op_span;
+  int64_t* op_idle;
 };
 
 __global__ __launch_bounds__(256) void k_init(InitArgs a) {
@@ -204,6 +236,10 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
   // the name outputs start as the identities: the per-block tables (or,
   // with many names, the kernels themselves) are combined into them with
   // atomics
+  for (int64_t i = tid; i < a.n_opn; i += nth) {  // accumulated with atomics
+    if (a.op_span) a.op_span[i] = 0;
+    if (a.op_idle) a.op_idle[i] = 0;
+  }
   for (int64_t i = tid; i < a.NN; i += nth) {
     if (a.name_count) a.name_count[i] = 0;
     if (a.name_sum) a.name_sum[i] = 0;
@@ -235,7 +271,10 @@ void launch_init(Ctx& c) {
   a.name_max = c.o.name_max;
   a.off = c.p.clock_offset;
   a.cls = c.p.stream_class;
-  const int64_t work = std::max<int64_t>({a.zero_n, (int64_t)a.nps * (c.overlap ? c.S : 1), (int64_t)c.NN, 1});
+  a.n_opn = c.waits ? (int64_t)c.P * c.NOP : 0;
+  a.op_span = c.o.op_span ? c.o.op_span : c.op_span_ws;
+  a.op_idle = c.o.op_idle;
+  const int64_t work = std::max<int64_t>({a.zero_n, (int64_t)a.nps * (c.overlap ? c.S : 1), (int64_t)c.NN, a.n_opn, 1});
   const int grid = (int)std::min<int64_t>(cdiv(work, 256 * 4), 2048);
   hipLaunchKernelGGL(k_init, dim3(std::max(grid, 1)), dim3(256), 0, c.st, a);
 }
@@ -307,7 +346,9 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   if (p->n_names < 1 || p->n_names > HERSCHEL_MAX_NAMES) return HERSCHEL_EINVAL;
   if (p->n_op_names < 1) return HERSCHEL_EINVAL;
   if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return HERSCHEL_EINVAL;
-  if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP)) return HERSCHEL_EINVAL;
+  if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP | HERSCHEL_OUT_WAITS)) return HERSCHEL_EINVAL;
+  // the op-name key (pid, name, ts') and its run endpoints must fit 64 bits
+  if ((p->flags & HERSCHEL_OUT_WAITS) && p->n_op_names > HERSCHEL_MAX_WAIT_OP_NAMES) return HERSCHEL_EINVAL;
   const bool contain = (p->flags & HERSCHEL_OUT_CONTAIN) != 0, overlap = (p->flags & HERSCHEL_OUT_OVERLAP) != 0;
   // every output but the counters may be NULL: that output is skipped
   if (!out->counters) return HERSCHEL_EINVAL;
@@ -329,6 +370,8 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   c.NOP = p->n_op_names;
   c.contain = contain;
   c.overlap = overlap;
+  c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
+  c.nob = bits_host((uint64_t)(c.NOP - 1));
   c.pb = bits_host((uint64_t)(c.P - 1));
   c.sb = bits_host((uint64_t)(c.S - 1));
   c.tb = bits_host((uint64_t)(c.T - 1));
@@ -414,11 +457,23 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   // the table.  Nothing else runs beside the sorts: a large grid on another
   // stream would take the CUs first and hold up the passes, which every
   // later stage waits for.
-  const int ks = c.contain ? 2 : 1;
-  SortBufs* ss[2] = {&c.sK, &c.sC};
-  const int32_t* cc[2] = {&c.ds->nK, &c.ds->nCL};
-  int p_shared = c.sK.nd - c.sK.first;
-  if (c.contain) p_shared = std::max(p_shared, c.sC.nd - c.sC.first);
+  SortBufs* ss[N_SORTS];
+  const int32_t* cc[N_SORTS];
+  int ks = 0;
+  ss[ks] = &c.sK;
+  cc[ks++] = &c.ds->nK;
+  if (c.contain) {
+    ss[ks] = &c.sC;
+    cc[ks++] = &c.ds->nCL;
+  }
+  if (c.waits) {  // the device lane and the op-name lanes
+    ss[ks] = &c.sD;
+    cc[ks++] = &c.ds->nK;
+    ss[ks] = &c.sO;
+    cc[ks++] = &c.ds->nO;
+  }
+  int p_shared = 0;
+  for (int i = 0; i < ks; ++i) p_shared = std::max(p_shared, ss[i]->nd - ss[i]->first);
   stage_begin(c, HERSCHEL_STAGE_HIST);
   launch_hist_multi(c, ss, cc, ks);
   stage_end(c, HERSCHEL_STAGE_HIST);
@@ -471,6 +526,12 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_OVERLAP);
   if (c.overlap) launch_overlap(c);
   stage_end(c, HERSCHEL_STAGE_OVERLAP);
+  stage_begin(c, HERSCHEL_STAGE_WAITS);
+  if (c.waits) {
+    launch_union_waits(c);
+    launch_waits(c);
+  }
+  stage_end(c, HERSCHEL_STAGE_WAITS);
   rec(1, c.st);
 
   // back on the caller's stream: what needs both containment and the join
@@ -676,12 +737,12 @@ int herschel_sort_stats(const herschel_params* p, int32_t* out) {
   const int pb = bits_host((uint64_t)(p->n_procs - 1)), sb = bits_host((uint64_t)(p->n_streams - 1));
   const int tb = bits_host((uint64_t)(p->n_threads - 1));
   const int wb = bits_host((uint64_t)(p->window_end - p->window_begin - 1));
-  const int key_bits[N_SORTS] = {pb + sb + wb, pb + tb + wb + 1};
-  const int32_t counts[N_SORTS] = {ds.nK, ds.nCL};
-  const int slot_of[N_SORTS] = {0, 2};  // timeline, containment in the reported order
-  for (int i = 0; i < 3; ++i) out[i] = 0;
-  for (int i = 3; i < 9; ++i) out[i] = 0;
-  for (int i = 0; i < N_SORTS; ++i) {
+  // the timeline and containment sorts, reported as s = 0 and s = 2
+  const int key_bits[2] = {pb + sb + wb, pb + tb + wb + 1};
+  const int32_t counts[2] = {ds.nK, ds.nCL};
+  const int slot_of[2] = {0, 2};
+  for (int i = 0; i < 9; ++i) out[i] = 0;
+  for (int i = 0; i < 2; ++i) {
     int nd, first, sh1;
     sort_digits(key_bits[i], true, &nd, &first, &sh1);
     const int o = 3 * slot_of[i];
@@ -700,6 +761,8 @@ int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) 
       p->n_streams > HERSCHEL_MAX_STREAMS || p->n_threads < 1 || p->n_threads > HERSCHEL_MAX_THREADS ||
       p->n_names < 1 || p->n_names > HERSCHEL_MAX_NAMES)
     return HERSCHEL_EINVAL;
+  if ((p->flags & HERSCHEL_OUT_WAITS) && (p->n_op_names < 1 || p->n_op_names > HERSCHEL_MAX_WAIT_OP_NAMES))
+    return HERSCHEL_EINVAL;
   Ctx c;
   c.p = *p;
   c.n = n;
@@ -709,6 +772,9 @@ int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) 
   c.NN = p->n_names;
   c.W = p->window_end - p->window_begin;
   c.contain = (p->flags & HERSCHEL_OUT_CONTAIN) != 0;
+  c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
+  c.NOP = p->n_op_names;
+  c.nob = bits_host((uint64_t)(c.NOP > 0 ? c.NOP - 1 : 0));
   c.overlap = (p->flags & HERSCHEL_OUT_OVERLAP) != 0;
   c.pb = bits_host((uint64_t)(c.P - 1));
   c.sb = bits_host((uint64_t)(c.S - 1));

@@ -34,11 +34,16 @@ enum : uint32_t {
 // (The others number them by workgroup index: a tile waits only for tiles of
 // lower index, whose workgroups the dispatcher started first.)
 enum : int {
-  TK_UNION = 0,
-  N_TICKETS = 1
+  TK_UNION = 0,    // the timeline (per stream)
+  TK_UNION_D = 1,  // the device lane (all streams of a process)
+  TK_UNION_O = 2,  // the op-name lanes
+  N_TICKETS = 3
 };
 
-constexpr int N_SORTS = 2;  // 0 timeline, 1 containment
+// 0 timeline (pid, stream, ts'), 1 containment, and with the idle-coincidence
+// outputs 2 device lane (pid, ts') and 3 op names (pid, op name, ts')
+constexpr int N_SORTS = 4;
+enum : int { SORT_K = 0, SORT_C = 1, SORT_D = 2, SORT_O = 3 };
 // join counters (JC_MLAUNCH: launches with at least one kernel; the
 // unmatched launches are the admitted ones without)
 enum { JC_MATCHED, JC_UNM_K, JC_DUP, JC_NEG, JC_UNATTR, JC_MLAUNCH, JC_N };
@@ -63,7 +68,13 @@ struct DevState {
   int32_t nCL;  // admitted ops + launches (containment list)
   int32_t nJ;   // admitted launches + kernels (join list)
   int32_t nEv;  // overlap events (2 per coverage run)
-  int32_t n_long[2];  // long runs listed by the refine pass (timeline, containment)
+  int32_t n_long[N_SORTS];  // long runs listed by the refine pass, per sort
+  int32_t nO;          // admitted CPU ops (op-name list, idle coincidence)
+  int32_t nOev;        // op-name run endpoints
+  int64_t nDgap;       // device idle intervals
+  int64_t nOgap;       // gaps of the op-name lanes (not used)
+  int32_t nDev;        // endpoints of the device lane (none)
+  int32_t pad2;
   int64_t first_invalid;  // smallest bad row (INT64_MAX = none)
   int64_t n_gaps;
   uint32_t sort_trivial[N_SORTS];  // bit d: digit d moves no data (every key agrees on it, or it is

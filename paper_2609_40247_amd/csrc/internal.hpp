@@ -52,7 +52,8 @@ struct Ctx {
   herschel_outputs o{};
   int64_t W0 = 0, W1 = 0, W = 0, thr = 0;
   int P = 0, S = 0, T = 0, NN = 0, NOP = 0;
-  bool contain = false, overlap = false;
+  bool contain = false, overlap = false, waits = false;
+  int nob = 0;                         // bits of an op name (idle coincidence)
   int pb = 0, sb = 0, tb = 0, wb = 0;  // key field widths: pid, stream, thread, ts'-W0
   int wb1 = 0;                         // bits of W (values 0..W)
   int vb = 0;                          // bits of W+1 (containment encoding)
@@ -62,11 +63,25 @@ struct Ctx {
   uint64_t* prep_status = nullptr;   // [prep_tiles * 3]
   int64_t prep_tiles = 0;
   uint64_t* union_status = nullptr;  // [union_tiles * 3]
+  uint64_t* union_status_d = nullptr;  // [union_tiles * 3] the device-lane union
+  uint64_t* union_status_o = nullptr;  // [union_tiles * 3] the op-name union
+  uint64_t* dg_status = nullptr;     // [dg_tiles] look-back of the idle-length scan
+  int64_t dg_tiles = 0;
+  int32_t* dg_pid = nullptr;         // [dg_cap] device idle intervals, in (pid, begin) order
+  int64_t* dg_begin = nullptr;
+  int64_t* dg_end = nullptr;
+  int64_t* dg_pre = nullptr;         // [dg_cap] idle length before each interval (exclusive prefix)
+  int64_t dg_cap = 0;
+  uint64_t* oev = nullptr;           // [oev_cap] op-name run endpoints
+  int64_t oev_cap = 0;
+  int64_t* op_span_ws = nullptr;     // [P * NOP] when the op_span output is NULL
+  int64_t* dbusy_ws = nullptr;       // [P] busy time of the device lane (zeroed with the state)
   int64_t union_tiles = 0;
   uint64_t* vb_status = nullptr;     // [vb_tiles]
   int64_t vb_tiles = 0;
   int64_t* corr_min = nullptr;       // [P]
   SortBufs sK, sC;                   // timeline, containment
+  SortBufs sD, sO;                   // device lane, op names (idle coincidence)
   uint32_t* k_rows = nullptr;        // [n] admitted kernels' rows in row order (per-name tables)
   uint32_t* hist_part = nullptr;     // [N_SORTS][HIST_MAX_BLOCKS][8 * 256] per-workgroup digit counts
   uint64_t* jkey = nullptr;          // [n] join list (prep): admitted launches and kernels in row order
@@ -119,6 +134,8 @@ void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
 void launch_refine(Ctx& c);
 void launch_names(Ctx& c);
 void launch_timeline(Ctx& c);
+void launch_union_waits(Ctx& c);
+void launch_waits(Ctx& c);
 void launch_overlap(Ctx& c);
 void launch_contain(Ctx& c);
 void launch_depth(Ctx& c);

@@ -7,6 +7,9 @@
 //   containment (pid, thread, ts'-W0, is_launch) ops and launches
 //   join        (pid, corr mod 2^51, is_kernel)   launches and kernels (not sorted: the
 //                                                 correlation table takes them in row order)
+// and, with the idle-coincidence outputs, the op-name list
+//   (pid, op name, ts'-W0) of the CPU ops, and for every kernel at its
+//   timeline position the device-lane key (pid, ts'-W0).
 // Compaction offsets come from a decoupled look-back per list; the last
 // tile's prefixes are the admitted counts.
 #include "internal.hpp"
@@ -26,11 +29,13 @@ struct PrepArgs {
   int sb, tb, wb;
   int64_t n_tiles;
   bool jt_range;  // find each process's id range (at most JT_PROCS processes)
+  bool waits;     // the op-name list and device-lane keys (idle coincidence)
+  int nob;        // bits of an op name
   DevState* ds;
   herschel_counters* cnt;
   int32_t* link;
   int32_t* aux;
-  uint64_t* status;  // [3][n_tiles]
+  uint64_t* status;  // [4][n_tiles]
   uint64_t* kK;
   uint32_t* vK;
   uint32_t* kRows;  // the admitted kernels' rows again, for the per-name tables (not sorted)
@@ -38,25 +43,31 @@ struct PrepArgs {
   uint32_t* vC;
   uint64_t* kJ;
   uint32_t* vJ;
+  uint64_t* kD;  // device-lane keys at the timeline positions
+  uint32_t* vD;
+  uint64_t* kO;  // op-name list
+  uint32_t* vO;
 };
+constexpr int PREP_LISTS = 4;  // timeline, containment, join, op names
 
 // Rows are loaded PREP_BATCH per thread at a time, every column of every row
 // of a batch in flight together: no load waits for another (the correlation
 // id is loaded for every kind, the clock offsets are read from LDS).
 constexpr int PREP_BATCH = 4;
 constexpr int PREP_OFF_LDS = 512;  // processes whose clock offsets are staged in LDS
-// the three list flags of every item are packed into one 32-bit word
-static_assert(3 * PREP_ITEMS <= 32, "list flags of all items must fit the 32-bit flag word");
+// the four list flags of every item are packed into one 32-bit word
+static_assert(PREP_LISTS * PREP_ITEMS <= 32, "list flags of all items must fit the 32-bit flag word");
+static_assert(PREP_LISTS <= PREP_THREADS / WAVE, "one wave per list's look-back");
 static_assert(PREP_ITEMS % PREP_BATCH == 0, "items are loaded in whole batches");
 static_assert(PREP_THREADS % WAVE == 0 && 2 * JT_PROCS <= PREP_THREADS, "one thread per id-range word");
 
 // Tiles are taken by workgroup index: a tile's look-back waits only for
 // tiles of lower index, whose workgroups the dispatcher started first.
 __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
-  __shared__ uint64_t s_bal[PREP_ITEMS][PREP_THREADS / WAVE][3];
-  __shared__ uint32_t s_off[PREP_ITEMS][PREP_THREADS / WAVE][3];
-  __shared__ uint32_t s_tot[3];
-  __shared__ uint64_t s_base[3];
+  __shared__ uint64_t s_bal[PREP_ITEMS][PREP_THREADS / WAVE][PREP_LISTS];
+  __shared__ uint32_t s_off[PREP_ITEMS][PREP_THREADS / WAVE][PREP_LISTS];
+  __shared__ uint32_t s_tot[PREP_LISTS];
+  __shared__ uint64_t s_base[PREP_LISTS];
   __shared__ unsigned long long s_bad;
   __shared__ unsigned long long s_jr[2 * JT_PROCS];  // per process: max of ~u, max of u (u = corr ^ 2^63)
   __shared__ unsigned long long s_jp;                 // processes with an admitted launch or kernel
@@ -76,7 +87,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
   __syncthreads();
 
   uint64_t kA[PREP_ITEMS], kB[PREP_ITEMS];  // kA: timeline or containment key, kB: join key
-  uint32_t fl = 0;                          // per item: bit 3j list K, 3j+1 list C, 3j+2 list J
+  uint32_t fl = 0;                          // per item: bit 4j list K, 4j+1 C, 4j+2 J, 4j+3 O
   uint64_t bad = ~0ull;
   // id range of the thread's current process (the join items of a thread
   // mostly share one): tp the process, ulo / uhi the max of ~u and of u
@@ -105,7 +116,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
     for (int u = 0; u < PREP_BATCH; ++u) {
       const int j = j0 + u;
       const int64_t r = base + (int64_t)j * PREP_THREADS + tid;
-      bool fK = false, fC = false, fJ = false;
+      bool fK = false, fC = false, fJ = false, fO = false;
       kA[j] = 0;
       kB[j] = 0;
       if (r < a.n) {
@@ -144,6 +155,9 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
                     (uint64_t)(kind == HERSCHEL_LAUNCH);
           kB[j] = ((uint64_t)pid << JK_PID_SHIFT) | (((uint64_t)corr & JK_CORR_MASK) << 1) |
                   (uint64_t)(kind == HERSCHEL_KERNEL);
+          fO = a.waits && kind == HERSCHEL_CPU_OP;
+          if (fO)  // an op takes no join key: its slot holds the op-name key
+            kB[j] = ((uint64_t)pid << (a.nob + a.wb)) | ((uint64_t)name << a.wb) | (uint64_t)rel;
           if (a.jt_range && fJ) {
             const uint64_t u = (uint64_t)corr ^ SIGN64;  // unsigned order = signed order of the ids
             if (pid != tp) {
@@ -162,12 +176,14 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
           }
         }
       }
-      fl |= (fK ? 1u : 0u) << (3 * j) | (fC ? 1u : 0u) << (3 * j + 1) | (fJ ? 1u : 0u) << (3 * j + 2);
-      const uint64_t b0 = ballot(fK), b1 = ballot(fC), b2 = ballot(fJ);
+      fl |= (fK ? 1u : 0u) << (4 * j) | (fC ? 1u : 0u) << (4 * j + 1) | (fJ ? 1u : 0u) << (4 * j + 2) |
+            (fO ? 1u : 0u) << (4 * j + 3);
+      const uint64_t b0 = ballot(fK), b1 = ballot(fC), b2 = ballot(fJ), b3 = ballot(fO);
       if (lane == 0) {
         s_bal[j][wv][0] = b0;
         s_bal[j][wv][1] = b1;
         s_bal[j][wv][2] = b2;
+        s_bal[j][wv][3] = b3;
       }
     }
   }
@@ -198,7 +214,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
       atomicOr(&s_jp, 1ull << tp);
     }
   }
-  if (tid < 3) {
+  const int nlists = a.waits ? PREP_LISTS : PREP_LISTS - 1;  // the op-name list only with its outputs
+  if (tid < nlists) {
     uint32_t run = 0;
     for (int j = 0; j < PREP_ITEMS; ++j)
       for (int w = 0; w < PREP_THREADS / WAVE; ++w) {
@@ -214,7 +231,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
     atomicMax(dst, s_jr[tid]);
   }
   if (a.jt_range && tid == 0 && s_jp) atomicOr((unsigned long long*)&a.ds->jt_present, s_jp);
-  if (wv < 3) {
+  if (wv < nlists) {
     const uint64_t ex = wave_lookback<OpSum>(a.status + (int64_t)wv * a.n_tiles, tile, s_tot[wv], a.ds);
     if (lane == 0) s_base[wv] = ex;
   }
@@ -226,6 +243,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
     a.ds->nK = (int32_t)nK;
     a.ds->nCL = (int32_t)nC;
     a.ds->nJ = (int32_t)nJ;
+    a.ds->nO = a.waits ? (int32_t)(s_base[3] + s_tot[3]) : 0;
     const int64_t nLaunch = nJ - nK;
     a.cnt->n_admitted[HERSCHEL_KERNEL] = nK;
     a.cnt->n_admitted[HERSCHEL_LAUNCH] = nLaunch;
@@ -235,26 +253,37 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
 #pragma unroll
   for (int j = 0; j < PREP_ITEMS; ++j) {
     const uint32_t r = (uint32_t)(base + (int64_t)j * PREP_THREADS + tid);
-    if (fl & (1u << (3 * j))) {
+    if (fl & (1u << (4 * j))) {
       const uint64_t pos = s_base[0] + s_off[j][wv][0] + popc(s_bal[j][wv][0] & lt);
       if (in_range(a.ds, (int64_t)pos, a.n)) {
         a.kK[pos] = kA[j];
         a.vK[pos] = r;
         a.kRows[pos] = r;
+        if (a.waits) {  // the device lane: the timeline key without its stream
+          a.kD[pos] = ((kA[j] >> (a.sb + a.wb)) << a.wb) | (kA[j] & ((1ull << a.wb) - 1));
+          a.vD[pos] = r;
+        }
       }
     }
-    if (fl & (2u << (3 * j))) {
+    if (fl & (2u << (4 * j))) {
       const uint64_t pos = s_base[1] + s_off[j][wv][1] + popc(s_bal[j][wv][1] & lt);
       if (in_range(a.ds, (int64_t)pos, a.n)) {
         a.kC[pos] = kA[j];
         a.vC[pos] = r;
       }
     }
-    if (fl & (4u << (3 * j))) {
+    if (fl & (4u << (4 * j))) {
       const uint64_t pos = s_base[2] + s_off[j][wv][2] + popc(s_bal[j][wv][2] & lt);
       if (in_range(a.ds, (int64_t)pos, a.n)) {
         a.kJ[pos] = kB[j];
         a.vJ[pos] = r;
+      }
+    }
+    if (fl & (8u << (4 * j))) {
+      const uint64_t pos = s_base[3] + s_off[j][wv][3] + popc(s_bal[j][wv][3] & lt);
+      if (in_range(a.ds, (int64_t)pos, a.n)) {
+        a.kO[pos] = kB[j];
+        a.vO[pos] = r;
       }
     }
   }
@@ -278,6 +307,8 @@ void launch_prep(Ctx& c) {
   a.wb = c.wb;
   a.n_tiles = c.prep_tiles;
   a.jt_range = c.P <= JT_PROCS;
+  a.waits = c.waits;
+  a.nob = c.nob;
   a.ds = c.ds;
   a.cnt = c.o.counters;
   a.link = c.o.link;
@@ -290,6 +321,10 @@ void launch_prep(Ctx& c) {
   a.vC = c.sC.v[0];
   a.kJ = c.jkey;
   a.vJ = c.jrow;
+  a.kD = c.sD.k[0];
+  a.vD = c.sD.v[0];
+  a.kO = c.sO.k[0];
+  a.vO = c.sO.v[0];
   hipLaunchKernelGGL(k_prep, dim3((unsigned)c.prep_tiles), dim3(PREP_THREADS), 0, c.st, a);
 }
 

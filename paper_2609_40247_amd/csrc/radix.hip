@@ -411,9 +411,9 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   if (sel < 0) return;
   const SortJob& jb = jobs.j[sel];
   const int d = jb.d, id = jb.id;
-  static_assert(N_SORTS == 2, "the selects below name every sort");
-  const uint32_t n = sel == 0 ? nn[0] : nn[1];
-  const uint32_t triv = sel == 0 ? tr[0] : tr[1];
+  static_assert(N_SORTS == 4, "the selects below name every sort");
+  const uint32_t n = sel == 0 ? nn[0] : sel == 1 ? nn[1] : sel == 2 ? nn[2] : nn[3];
+  const uint32_t triv = sel == 0 ? tr[0] : sel == 1 ? tr[1] : sel == 2 ? tr[2] : tr[3];
   const uint32_t gexcl = ds->hist[id][d][dgt];
   const int parity = popc(~triv & ((1u << d) - 1u)) & 1;
   const uint64_t* kin = jb.k[parity];
@@ -706,11 +706,11 @@ struct RefineJob {
   const int32_t* count;
   int id;        // sort index (parity)
   int contain;   // 1: containment tie rule
-  int slot;      // list index (0 timeline, 1 containment)
+  int slot;      // list index (the sort's id)
   int shift;     // runs are keys equal above this bit (the passes' lowest, or 0 when every digit was sorted)
 };
 struct RefineJobs {
-  RefineJob j[2];
+  RefineJob j[N_SORTS];
   const int64_t* te;
   int32_t* list;  // [2][cap]
   int64_t cap;
@@ -901,11 +901,17 @@ void launch_refine(Ctx& c) {
   RefineJobs jobs{};
   int m = 0;
   int64_t n_max = 1;
-  for (SortBufs* s : {&c.sK, &c.sC}) {
+  // the containment list always (its tie rule orders ops that start
+  // together); the others when a digit was left to this pass; the device and
+  // op-name lists with the idle-coincidence outputs (row order breaks ties)
+  const int32_t* counts[N_SORTS] = {&c.ds->nK, &c.ds->nCL, &c.ds->nK, &c.ds->nO};
+  for (SortBufs* s : {&c.sK, &c.sC, &c.sD, &c.sO}) {
     const bool con = s == &c.sC;
-    if (con ? !c.contain : s->first == 0) continue;
-    jobs.j[m++] = RefineJob{{s->k[0], s->k[1]}, {s->v[0], s->v[1]}, con ? &c.ds->nCL : &c.ds->nK, s->id, con ? 1 : 0,
-                            con ? 1 : 0, s->first ? s->sh1 : 0};
+    if (con && !c.contain) continue;
+    if ((s == &c.sD || s == &c.sO) && !c.waits) continue;
+    if (!con && s->first == 0) continue;
+    jobs.j[m++] = RefineJob{{s->k[0], s->k[1]}, {s->v[0], s->v[1]}, counts[s->id], s->id, con ? 1 : 0,
+                            s->id, s->first ? s->sh1 : 0};
     n_max = std::max<int64_t>(n_max, s->n_max);
   }
   if (m == 0) return;

@@ -42,6 +42,13 @@ struct UnionArgs {
   int64_t ev_cap;
   uint64_t* status;   // [3][tiles_max]: segmax, gap count, event count
   int64_t tiles_max;
+  // which list: its count, sort, tile ticket, and where its totals go
+  const int32_t* count;
+  int sort_id;
+  int ticket;
+  bool want_gaps;     // the op-name lanes need no gaps
+  int64_t* gaps_out;  // the gap count
+  int32_t* ev_out;    // the endpoint count
 };
 
 struct Elem {
@@ -80,7 +87,7 @@ __device__ __forceinline__ void walk(const UnionArgs& a, const Elem* x, int nv, 
                      int64_t i0, int64_t nK, uint32_t* ngap, uint32_t* nev, int64_t gbase, int64_t ebase,
                      int64_t* s_busy, int32_t seg0, uint64_t* s_ev) {
   const int nseg = a.P * a.S;
-  const bool full_gap = a.W > a.thr;
+  const bool full_gap = a.want_gaps && a.W > a.thr;
   uint64_t m = m_in;  // 0 none, else (max covered end) + 1
   int32_t prev = prev_seg;
   uint32_t g = 0, v = 0;
@@ -91,9 +98,8 @@ __device__ __forceinline__ void walk(const UnionArgs& a, const Elem* x, int nv, 
     if (j >= nv) continue;
     const Elem& q = x[j];
     if (q.seg != prev) {
-      const int32_t from = prev + 1;  // empty streams strictly between
-      for (int32_t s = from; s < q.seg; ++s) {
-        if (full_gap) {
+      if (full_gap) {  // empty streams strictly between
+        for (int32_t s = prev + 1; s < q.seg; ++s) {
           if (MODE == 1) put_gap(a, gbase + g, s, 0, a.W);
           ++g;
         }
@@ -102,7 +108,7 @@ __device__ __forceinline__ void walk(const UnionArgs& a, const Elem* x, int nv, 
     }
     const int64_t C = m ? (int64_t)m - 1 : 0;
     if (q.e > q.s) {
-      if (q.s > C && q.s - C > a.thr) {
+      if (a.want_gaps && q.s > C && q.s - C > a.thr) {
         if (MODE == 1) put_gap(a, gbase + g, q.seg, C, q.s);
         ++g;
       }
@@ -134,7 +140,7 @@ __device__ __forceinline__ void walk(const UnionArgs& a, const Elem* x, int nv, 
     const int32_t nxt = (j + 1 < nv) ? x[j + 1].seg : next_seg;
     if (nxt != q.seg) {
       const int64_t Cl = m ? (int64_t)m - 1 : 0;
-      if (Cl < a.W && a.W - Cl > a.thr) {
+      if (a.want_gaps && Cl < a.W && a.W - Cl > a.thr) {
         if (MODE == 1) put_gap(a, gbase + g, q.seg, Cl, a.W);
         ++g;
       }
@@ -142,12 +148,10 @@ __device__ __forceinline__ void walk(const UnionArgs& a, const Elem* x, int nv, 
         if (MODE == 1) put_event(a, s_ev, ebase + v, q.seg, Cl);
         ++v;
       }
-      if (i0 + j == nK - 1) {
+      if (full_gap && i0 + j == nK - 1) {
         for (int32_t s = q.seg + 1; s < nseg; ++s) {
-          if (full_gap) {
-            if (MODE == 1) put_gap(a, gbase + g, s, 0, a.W);
-            ++g;
-          }
+          if (MODE == 1) put_gap(a, gbase + g, s, 0, a.W);
+          ++g;
         }
       }
     }
@@ -174,24 +178,24 @@ __global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
   __shared__ uint64_t s_ev[2 * UN_TILE];  // the tile's coverage-run endpoints, in order
 
   const int tid = threadIdx.x, lane = lane_id(), wv = tid / WAVE;
-  const int64_t nK = a.ds->nK;
-  const int par = (int)a.ds->sort_parity[0];
+  const int64_t nK = *a.count;
+  const int par = (int)a.ds->sort_parity[a.sort_id];
   const uint64_t* keys = a.k[par];
   const uint32_t* vals = a.v[par];
   const int64_t ntiles = nK > 0 ? cdiv(nK, UN_TILE) : 1;
   if ((int64_t)blockIdx.x >= ntiles) return;  // no tile: stay off the ticket counter
-  const int tile = take_ticket(a.ds, TK_UNION, &s_tile);
+  const int tile = take_ticket(a.ds, a.ticket, &s_tile);
   const int64_t base = (int64_t)tile * UN_TILE;
   const int nseg = a.P * a.S;
 
   if (nK == 0) {  // no kernels: one full-window gap per stream
-    const bool full_gap = a.W > a.thr;
+    const bool full_gap = a.want_gaps && a.W > a.thr;
     for (int s = tid; s < nseg; s += UN_THREADS)
       if (full_gap) put_gap(a, s, s, 0, a.W);
     if (tid == 0) {
-      a.ds->n_gaps = full_gap ? nseg : 0;
-      a.cnt->n_gaps_total = full_gap ? nseg : 0;
-      a.ds->nEv = 0;
+      *a.gaps_out = full_gap ? nseg : 0;
+      if (a.cnt) a.cnt->n_gaps_total = full_gap ? nseg : 0;
+      *a.ev_out = 0;
     }
     return;
   }
@@ -354,9 +358,9 @@ __global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
   __syncthreads();
   if (tile == ntiles - 1 && tid == 0) {
     const int64_t g = (int64_t)(s_base[0] + s_tot[0]);
-    a.ds->n_gaps = g;
-    a.cnt->n_gaps_total = g;
-    a.ds->nEv = (int32_t)(s_base[1] + s_tot[1]);
+    *a.gaps_out = g;
+    if (a.cnt) a.cnt->n_gaps_total = g;
+    *a.ev_out = (int32_t)(s_base[1] + s_tot[1]);
   }
   if (has && (ngap || nev)) {
     uint32_t g2, e2;
@@ -370,12 +374,12 @@ __global__ __launch_bounds__(UN_THREADS) void k_union(UnionArgs a) {
     if (in_range(a.ds, eb + i, a.ev_cap)) a.ev_keys[eb + i] = s_ev[i];
 }
 
-void launch_timeline(Ctx& c) {
+static UnionArgs union_args(Ctx& c, const SortBufs& sb_, int S, int sbits) {
   UnionArgs a;
-  a.k[0] = c.sK.k[0];
-  a.k[1] = c.sK.k[1];
-  a.v[0] = c.sK.v[0];
-  a.v[1] = c.sK.v[1];
+  a.k[0] = sb_.k[0];
+  a.k[1] = sb_.k[1];
+  a.v[0] = sb_.v[0];
+  a.v[1] = sb_.v[1];
   a.te = c.ev.te;
   a.pid_col = c.ev.pid;
   a.off = c.p.clock_offset;
@@ -384,13 +388,22 @@ void launch_timeline(Ctx& c) {
   a.W = c.W;
   a.thr = c.thr;
   a.P = c.P;
-  a.S = c.S;
-  a.sb = c.sb;
+  a.S = S;
+  a.sb = sbits;
   a.wb = c.wb;
   a.wb1 = c.wb1;
   a.pb = c.pb;
-  a.overlap = c.overlap;
   a.ds = c.ds;
+  a.tiles_max = c.union_tiles;
+  a.sort_id = sb_.id;
+  a.want_gaps = true;
+  return a;
+}
+
+// Busy time, gaps and coverage-run endpoints of every (pid, stream).
+void launch_timeline(Ctx& c) {
+  UnionArgs a = union_args(c, c.sK, c.S, c.sb);
+  a.overlap = c.overlap;
   a.cnt = c.o.counters;
   a.busy = c.o.busy ? c.o.busy : c.busy_ws;
   a.gap_cap = c.o.gap_capacity;
@@ -402,8 +415,55 @@ void launch_timeline(Ctx& c) {
   a.ev_keys = c.ev_keys;
   a.ev_cap = c.ev_cap;
   a.status = c.union_status;
-  a.tiles_max = c.union_tiles;
+  a.count = &c.ds->nK;
+  a.ticket = TK_UNION;
+  a.gaps_out = &c.ds->n_gaps;
+  a.ev_out = &c.ds->nEv;
   hipLaunchKernelGGL(k_union, dim3((unsigned)c.union_tiles), dim3(UN_THREADS), 0, c.st, a);
+}
+
+// The same scan over the device lane (every stream of a process at once):
+// its gaps above the threshold are the GPU's idle intervals, in (pid, begin)
+// order; and over the op-name lanes, whose busy time is each op name's span
+// and whose coverage-run endpoints bound its union.
+void launch_union_waits(Ctx& c) {
+  UnionArgs d = union_args(c, c.sD, 1, 0);
+  d.overlap = false;
+  d.cnt = nullptr;
+  d.busy = c.dbusy_ws;
+  d.gap_cap = c.dg_cap;
+  d.gap_pid = c.dg_pid;
+  d.gap_stream = nullptr;
+  d.gap_begin = c.dg_begin;
+  d.gap_end = c.dg_end;
+  d.gap_flags = nullptr;
+  d.ev_keys = nullptr;
+  d.ev_cap = 0;
+  d.status = c.union_status_d;
+  d.count = &c.ds->nK;
+  d.ticket = TK_UNION_D;
+  d.gaps_out = &c.ds->nDgap;
+  d.ev_out = &c.ds->nDev;
+  hipLaunchKernelGGL(k_union, dim3((unsigned)c.union_tiles), dim3(UN_THREADS), 0, c.st, d);
+  UnionArgs o = union_args(c, c.sO, c.NOP, c.nob);
+  o.overlap = true;
+  o.want_gaps = false;
+  o.cnt = nullptr;
+  o.busy = c.o.op_span ? c.o.op_span : c.op_span_ws;
+  o.gap_cap = 0;
+  o.gap_pid = nullptr;
+  o.gap_stream = nullptr;
+  o.gap_begin = nullptr;
+  o.gap_end = nullptr;
+  o.gap_flags = nullptr;
+  o.ev_keys = c.oev;
+  o.ev_cap = c.oev_cap;
+  o.status = c.union_status_o;
+  o.count = &c.ds->nO;
+  o.ticket = TK_UNION_O;
+  o.gaps_out = &c.ds->nOgap;
+  o.ev_out = &c.ds->nOev;
+  hipLaunchKernelGGL(k_union, dim3((unsigned)c.union_tiles), dim3(UN_THREADS), 0, c.st, o);
 }
 
 int64_t union_tile_elems() { return UN_TILE; }

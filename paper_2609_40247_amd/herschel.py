@@ -24,7 +24,7 @@ _LIBS = {"release": "libherschel.so", "checked": "libherschel_checked.so"}
 CPU_OP, LAUNCH, KERNEL = 0, 1, 2
 OK, EINVAL, EEVENT, ECAPACITY, EWORKSPACE, EDEVICE, ETOOBIG = 0, -1, -2, -3, -4, -5, -6
 STATIC_SCRATCH_BYTES = 64 << 20  # HERSCHEL_STATIC_SCRATCH_BYTES
-OUT_CONTAIN, OUT_OVERLAP = 0x1, 0x2
+OUT_CONTAIN, OUT_OVERLAP, OUT_WAITS = 0x1, 0x2, 0x4
 
 _P = ctypes.c_void_p
 
@@ -53,7 +53,8 @@ class HerschelOutputs(ctypes.Structure):
                                   "pair_overlap", "class_busy", "class_overlap", "any_busy", "name_count",
                                   "name_sum", "name_min", "name_max", "lat_hist", "edge_wait", "edge_status")] + [
         ("gap_capacity", ctypes.c_int64)] + [(k, _P) for k in ("gap_pid", "gap_stream", "gap_begin", "gap_end",
-                                                               "gap_flags", "counters")]
+                                                               "gap_flags", "counters", "dev_idle", "op_span",
+                                                               "op_idle")]
 
 
 _lib = {}
@@ -136,7 +137,7 @@ def herschel_trace_analyze_batch(events: HerschelEvents, offsets: np.ndarray, pa
 
 
 STAGES = ("init", "prep", "hist", "names", "sort", "timeline", "overlap", "contain", "join", "opagg", "edges",
-          "final")
+          "final", "waits")
 
 
 def herschel_time_stage(stage: int, start_event, stop_event, lib=None) -> int:
@@ -231,6 +232,8 @@ class Analyzer:
             edge_wait=z(max(self.n_edges, 1), torch.int64), edge_status=z(max(self.n_edges, 1), torch.int32),
             gap_pid=z(gc, torch.int32), gap_stream=z(gc, torch.int32), gap_begin=z(gc, torch.int64),
             gap_end=z(gc, torch.int64), gap_flags=z(gc, torch.uint8), counters=z(len(COUNTERS), torch.int64),
+            dev_idle=z(P, torch.int64), op_span=z(P * int(params["n_op_names"]), torch.int64),
+            op_idle=z(P * int(params["n_op_names"]), torch.int64),
         )
         self.params = self._params_struct(self.ws.data_ptr(), self.ws_bytes)
         self.outs = HerschelOutputs(gap_capacity=self.gap_capacity,
@@ -264,7 +267,7 @@ class Analyzer:
         c = dict(zip(COUNTERS, (int(x) for x in h.pop("counters"))))
         res = {k: h[k][:n] for k in ("link", "aux", "op_nkern", "op_first", "op_last", "op_ksum")}
         for k in ("busy", "idle", "pair_overlap", "class_busy", "class_overlap", "any_busy", "name_count",
-                  "name_sum", "name_min", "name_max", "lat_hist"):
+                  "name_sum", "name_min", "name_max", "lat_hist", "dev_idle", "op_span", "op_idle"):
             res[k] = h[k]
         res["edge_wait"] = h["edge_wait"][:self.n_edges]
         res["edge_status"] = h["edge_status"][:self.n_edges]

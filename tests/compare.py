@@ -40,5 +40,7 @@ def assert_same(got: tuple, want: tuple, params: dict, ctx: str = "") -> None:
         keys += ["op_nkern", "op_first", "op_last", "op_ksum"]
     if params.get("flags", 3) & 2:
         keys += ["pair_overlap", "class_busy", "class_overlap", "any_busy"]
+    if params.get("flags", 3) & 4:
+        keys += ["dev_idle", "op_span", "op_idle"]
     for k in keys:
         _eq(k, g[k], w[k], ctx)

@@ -64,7 +64,10 @@ SMALL = [dict(seed=s) for s in range(60)] + [
     for s in range(20)] + [
     dict(seed=2000 + s, n_rows=40, window=60, n_procs=1, n_streams=2, n_threads=1, corr_range=6, offsets=False)
     for s in range(20)] + [dict(seed=3000 + s, flags=s % 4) for s in range(12)] + [
-    dict(seed=4000 + s, n_rows=30, window=200, n_procs=4, n_streams=2, n_threads=2, corr_range=3) for s in range(12)]
+    dict(seed=4000 + s, n_rows=30, window=200, n_procs=4, n_streams=2, n_threads=2, corr_range=3) for s in range(12)] + [
+    dict(seed=5000 + s, flags=4 + s % 4) for s in range(24)] + [
+    dict(seed=5100 + s, n_rows=400, window=3000, n_procs=3, n_streams=4, n_threads=3, corr_range=60, n_op_names=3,
+         flags=7) for s in range(12)]
 
 
 @pytest.mark.parametrize("case", SMALL, ids=lambda c: f"seed{c['seed']}")
@@ -645,4 +648,60 @@ def test_config4_chunk_full_size(H):
         for k in BATCH_OUTPUTS:
             assert np.array_equal(res[k], o[k]), (ids[t], k)
         print(f"trace {ids[t]}: {ns[t]} rows identical", flush=True)
+
+
+# --------------------------------------------------------------- GPU idle x CPU ops
+def test_worked_timeline_idle_coincidence(H):
+    cols, p, g = load_golden("t1_worked_timeline.json")
+    exp = g["expect_waits"]
+    p["flags"] = exp["flags"]
+    (code, o), _ = check(H, cols, p, "T1 idle coincidence")
+    for k in ("dev_idle", "op_span", "op_idle"):
+        assert o[k].tolist() == exp[k], k
+
+
+@pytest.mark.parametrize("which", ["config0", "config1", "config2", "config3", "medium"])
+def test_idle_coincidence_workloads(H, which):
+    """Every output with the idle coincidence, on the workload shapes (the
+    decode-step trace at full size)."""
+    if which == "config0":
+        tr = synth.config0()
+    elif which == "config1":
+        tr = synth.config1()
+    elif which == "config2":
+        tr = synth.config2(scale=0.2)
+    elif which == "config3":
+        tr = synth.config3(n_procs=8, n_steps=40, n_edges=2000)
+    else:
+        tr = synth.random_small(seed=9600, n_rows=60_000, window=400_000, n_procs=3, n_streams=5, n_threads=2,
+                                corr_range=20_000, edges=300, n_op_names=7)
+    p = dict(tr.params, flags=7)
+    (code, g), _ = check(H, tr.columns(), p, f"{which} with idle coincidence")
+    assert (g["op_idle"] <= g["op_span"]).all()
+
+
+def test_idle_coincidence_limits(H):
+    """The widest keys the op-name lanes take: 4096 processes, 2048 op names
+    and a window of 2^40 ns; one more op name is rejected by both."""
+    W0 = (1 << 62) - (1 << 41)
+    W = 1 << 40
+    rng = np.random.default_rng(12)
+    rows = []
+    for j in range(3000):
+        pid = int(rng.integers(0, 4096))
+        t = W0 + int(rng.integers(0, W))
+        rows.append((2, pid, j % 2, t, t + int(rng.integers(1, 1 << 30)), j, j % 4))
+        rows.append((0, pid, 0, t - int(rng.integers(0, 1 << 31)), t + int(rng.integers(0, 1 << 31)), 0,
+                     int(rng.integers(0, 2048))))
+    cols, p = _rows(rows, P=4096, S=2, W0=W0, W=W, thr=1 << 20, NOP=2048, flags=7)
+    check(H, cols, p, "idle coincidence at the key limits")
+    n = len(cols["ts"])
+    an = H.Analyzer(p, n)
+    ev = H.events_struct(H.device_columns(cols))
+    an.p = dict(p, n_op_names=2049)
+    params = an._params_struct(an.ws.data_ptr(), an.ws_bytes)
+    assert H.herschel_trace_analyze(ev, n, params, an.outs) == -1
+    with pytest.raises(ValueError):
+        H.herschel_workspace_size(n, params)
+    assert oracle.analyze(cols, an.p)[0] == -1
 

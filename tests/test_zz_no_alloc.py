@@ -46,8 +46,9 @@ def _run_both(H, tr, label):
     r_ref, r_st = ref.results(n), st.results(n)
     assert c_st == c_ref == 0, (label, c_st, c_ref)
     assert r_st["counters"] == r_ref["counters"], label
+    unwritten = () if p.get("flags", 3) & 4 else ("dev_idle", "op_span", "op_idle")  # outputs of another flag
     for k in r_ref:
-        if k != "counters":
+        if k != "counters" and k not in unwritten:
             assert np.array_equal(r_st[k], r_ref[k]), (label, k)
     assert_same((c_st, r_st), oracle.analyze(cols, p, gap_capacity=cap), p, label + " vs oracle")
 
