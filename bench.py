@@ -107,6 +107,8 @@ def algorithmic_bytes(n: int, counters: dict, params: dict, n_gaps: int) -> int:
     if flags & 2:
         b += 8 * (P * S * S + 12 * P)
     b += 36 * E  # each edge read (24 B) and its wait and status written
+    if flags & 4:
+        b += 8 * P + 16 * P * int(params["n_op_names"])  # GPU idle, op-name span and idle
     return b
 
 
@@ -295,6 +297,8 @@ def main() -> int:
                     help="config1: the decode-step trace (the headline line); config0, config2, config3: the "
                          "other single-window workloads; config4: one 32-trace chunk of the batch workload")
     ap.add_argument("--chunk", type=int, default=0, help="config4: which of the 8 chunks")
+    ap.add_argument("--waits", action="store_true",
+                    help="also compute the GPU idle coinciding with CPU ops, by op name")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -316,6 +320,8 @@ def main() -> int:
         del src, dst
 
     n = tr.n
+    if args.waits:
+        tr.params["flags"] = int(tr.params.get("flags", 3)) | H.OUT_WAITS
     an = H.Analyzer(tr.params, n)
     dcols = H.device_columns(tr.columns())
     ev = H.events_struct(dcols)
@@ -395,7 +401,7 @@ def main() -> int:
     alg = BYTES_PER_KEY_PASS * units / launches
     launch_s = stage_ms * 1e-3 / launches
     achieved = alg / launch_s / 1e9
-    prof = profile_fields(args.workload)
+    prof = profile_fields(args.workload + ("_waits" if args.waits else ""))
     gaps = min(c["n_gaps_total"], an.gap_capacity)
     call_bytes = algorithmic_bytes(n, c, tr.params, gaps)
     whole = {"algorithmic_bytes": call_bytes, "algorithmic_GBps": round(call_bytes / (ms * 1e-3) / 1e9, 1),
@@ -413,7 +419,8 @@ def main() -> int:
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": {"workload": WORKLOADS[args.workload], "rows": n, "kernels": c["n_admitted_kernel"],
-                   "launches": c["n_admitted_launch"], "cpu_ops": c["n_admitted_cpu"], "outputs": "all"},
+                   "launches": c["n_admitted_launch"], "cpu_ops": c["n_admitted_cpu"],
+                   "outputs": "all, with the idle coincidence by op name" if args.waits else "all"},
         "roofline": {"kernel": ROOFLINE_KERNEL, "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": None if prof is None else prof["radix_hbm_bytes_per_launch"],
