@@ -55,7 +55,7 @@ _P = ctypes.c_void_p
 
 
 class _Events(ctypes.Structure):
-    _fields_ = [(k, _P) for k in ("ts", "te", "corr", "pid", "lane", "name", "kind")]
+    _fields_ = [(k, _P) for k in ("ts", "te", "corr", "pid", "lane", "name", "kind", "flops", "bytes")]
 
 
 class _Params(ctypes.Structure):
@@ -63,7 +63,8 @@ class _Params(ctypes.Structure):
                 ("n_procs", ctypes.c_int32), ("n_streams", ctypes.c_int32),
                 ("n_threads", ctypes.c_int32), ("n_names", ctypes.c_int32),
                 ("n_op_names", ctypes.c_int32), ("clock_offset", _P), ("stream_class", _P),
-                ("edges", _P), ("n_edges", ctypes.c_int64), ("flags", ctypes.c_uint32)]
+                ("edges", _P), ("n_edges", ctypes.c_int64), ("flags", ctypes.c_uint32),
+                ("peak_flops", ctypes.c_int64), ("peak_bytes", ctypes.c_int64), ("ref_sol_ppm", _P)]
 
 
 COUNTER_NAMES = ("n_admitted_cpu", "n_admitted_launch", "n_admitted_kernel", "n_outside_window",
@@ -79,7 +80,9 @@ class _Outputs(ctypes.Structure):
                 ("name_sum", _P), ("name_min", _P), ("name_max", _P), ("lat_hist", _P),
                 ("edge_wait", _P), ("edge_status", _P), ("gap_capacity", ctypes.c_int64),
                 ("gap_pid", _P), ("gap_stream", _P), ("gap_begin", _P), ("gap_end", _P),
-                ("gap_flags", _P), ("counters", _P), ("dev_idle", _P), ("op_span", _P), ("op_idle", _P)]
+                ("gap_flags", _P), ("counters", _P), ("dev_idle", _P), ("op_span", _P), ("op_idle", _P),
+                ("op_mfu", _P), ("op_mbu", _P), ("op_sol", _P), ("opn_flops", _P), ("opn_bytes", _P),
+                ("opn_time", _P), ("opn_sol", _P), ("opn_hot", _P)]
 
 
 def _ptr(a):
@@ -98,6 +101,9 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
          (("ts", np.int64), ("te", np.int64), ("corr", np.int64), ("pid", np.int32),
           ("lane", np.int32), ("name", np.int32), ("kind", np.uint8))}
     n = int(c["ts"].shape[0])
+    for k in ("flops", "bytes"):  # per-op operation counts and logical bytes (SOL outputs)
+        if cols.get(k) is not None:
+            c[k] = np.ascontiguousarray(cols[k], dtype=np.int64)
     P, S = int(params["n_procs"]), int(params["n_streams"])
     edges = params.get("edges")
     n_edges = 0 if edges is None else int(len(edges))
@@ -105,6 +111,8 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
     off = None if off is None else np.ascontiguousarray(off, dtype=np.int64)
     cls = params.get("stream_class")
     cls = None if cls is None else np.ascontiguousarray(cls, dtype=np.uint8)
+    ref = params.get("ref_sol_ppm")
+    ref = None if ref is None else np.ascontiguousarray(ref, dtype=np.int64)
     edges = None if n_edges == 0 else np.ascontiguousarray(edges)
     if gap_capacity is None:
         gap_capacity = int(np.count_nonzero(c["kind"] == 2)) + P * S
@@ -124,6 +132,10 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
         gap_flags=np.zeros(max(gap_capacity, 1), np.uint8),
         dev_idle=np.zeros(P, np.int64), op_span=np.zeros(P * int(params["n_op_names"]), np.int64),
         op_idle=np.zeros(P * int(params["n_op_names"]), np.int64),
+        op_mfu=np.full(n, UNWRITTEN_I64, np.int64), op_mbu=np.full(n, UNWRITTEN_I64, np.int64),
+        op_sol=np.full(n, UNWRITTEN_I64, np.int64),
+        **{k: np.zeros(int(params["n_op_names"]), np.int64)
+           for k in ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot")},
     )
     counters = np.zeros(len(COUNTER_NAMES), np.int64)
     ev = _Events(**{k: _ptr(v) for k, v in c.items()})
@@ -131,7 +143,9 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
                  thr=int(params["gap_threshold"]), n_procs=P, n_streams=S,
                  n_threads=int(params["n_threads"]), n_names=int(params["n_names"]),
                  n_op_names=int(params["n_op_names"]), clock_offset=_ptr(off), stream_class=_ptr(cls),
-                 edges=_ptr(edges), n_edges=n_edges, flags=int(params.get("flags", 3)))
+                 edges=_ptr(edges), n_edges=n_edges, flags=int(params.get("flags", 3)),
+                 peak_flops=int(params.get("peak_flops", 0)), peak_bytes=int(params.get("peak_bytes", 0)),
+                 ref_sol_ppm=_ptr(ref))
     out = _Outputs(gap_capacity=gap_capacity, counters=counters.ctypes.data,
                    **{k: v.ctypes.data for k, v in o.items()})
     code = lib.herschel_oracle_analyze(ctypes.byref(ev), n, ctypes.byref(pr), ctypes.byref(out))

@@ -25,6 +25,8 @@
  *       work"; Section 6.1 "Execution progress and state")
  *   15. cross-process dependency waits (panel "Cross-process blocking")
  *   16. GPU idle coinciding with CPU ops, by op name (Section 9.1)
+ *   17. operator MFU, MBU and SOL, per op name and Hotness (Section 6.1,
+ *       "Operator execution and efficiency"; Section 6.2)
  *
  * Sorting uses the C library's qsort with comparators that end in the row
  * index, so every order is total and the result does not depend on qsort's
@@ -65,6 +67,8 @@ static int row_is_valid(const hro_events *ev, int64_t i, const hro_params *p) {
   }
   if (!in_abs(ev->ts[i]) || !in_abs(ev->te[i])) return 0;
   if (ev->te[i] < ev->ts[i]) return 0;
+  /* with the SOL outputs, an op's operation count and logical bytes */
+  if ((p->flags & 8u) != 0 && k == K_CPU && (ev->flops[i] < 0 || ev->bytes[i] < 0)) return 0;
   return 1;
 }
 
@@ -81,6 +85,13 @@ static int params_ok(int64_t n, const hro_params *p) {
   /* implementation limit shared with the library, for error parity: with
    * the idle-coincidence outputs, at most 2048 op names */
   if ((p->flags & 4u) != 0 && p->n_op_names > 2048) return 0;
+  /* SOL needs T_op (containment), positive peaks */
+  if ((p->flags & 8u) != 0) {
+    if ((p->flags & 1u) == 0 || p->peak_flops <= 0 || p->peak_bytes <= 0) return 0;
+    if (p->ref_sol_ppm)
+      for (int o = 0; o < p->n_op_names; ++o)
+        if (p->ref_sol_ppm[o] < 0) return 0;
+  }
   if (p->clock_offset)
     for (int q = 0; q < p->n_procs; ++q)
       if (!in_abs(p->clock_offset[q])) return 0;
@@ -164,6 +175,15 @@ static int64_t union_of(ival *const *lists, const int64_t *lens, int nl, ival **
   return r;
 }
 
+/* floor(10^15 x / (t peak)) in parts per million: x per t ns against a peak
+ * per second (step 17), exact in 128 bits; saturates at INT64_MAX. */
+static int64_t ppm_of(uint64_t x, uint64_t t, uint64_t peak) {
+  unsigned __int128 num = (unsigned __int128)x * 1000000000000000ull;
+  unsigned __int128 den = (unsigned __int128)t * peak;
+  unsigned __int128 q = num / den;
+  return q > (unsigned __int128)I64_MAX ? I64_MAX : (int64_t)q;
+}
+
 /* floor(log2 x) + 1 for x > 0, 0 otherwise (step 8's histogram bin). */
 static int latency_bin(int64_t x) {
   int b = 0;
@@ -178,6 +198,7 @@ int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p
                             hro_outputs *out) {
   if (!ev || !p || !out || !out->counters) return -1;
   if (!params_ok(n, p)) return -1;
+  if ((p->flags & 8u) != 0 && n > 0 && (!ev->flops || !ev->bytes)) return -1;
   const int P = p->n_procs, S = p->n_streams;
   const int64_t W0 = p->w0, W1 = p->w1, W = W1 - W0;
   const int contain = (p->flags & 1u) != 0, overlap = (p->flags & 2u) != 0;
@@ -604,6 +625,56 @@ int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p
     }
     free(u);
     free(orc);
+  }
+
+  /* 17. Operator efficiency (Section 6.1, "Operator execution and
+   *     efficiency"): the op's operation count F and logical bytes B,
+   *     normalized by T_op = op_last - op_first and the device peaks, give
+   *     MFU and MBU; SOL = max(MFU, MBU).  READING: parts per million,
+   *     floor(10^15 F / (T_op[ns] peak_flops[/s])), exact in 128 bits; an op
+   *     without kernels or with T_op = 0 is unmeasured (-1).  Per op name,
+   *     over its measured ops: the sums of F, B and T_op (wrapping), SOL of
+   *     the sums, and Hotness, the time recoverable at the name's reference
+   *     SOL: sum of floor(T_op (ref - SOL) / ref) over ops below it
+   *     (Section 6.2 weights that fraction by time). */
+  if ((p->flags & 8u) != 0) {
+    const int NOP = p->n_op_names;
+    for (int o = 0; o < NOP; ++o) {
+      out->opn_flops[o] = 0;
+      out->opn_bytes[o] = 0;
+      out->opn_time[o] = 0;
+      out->opn_hot[o] = 0;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+      if (!adm[i] || ev->kind[i] != K_CPU) continue;
+      int64_t T = out->op_nkern[i] > 0 ? wrap_sub(out->op_last[i], out->op_first[i]) : 0;
+      if (T <= 0) {
+        out->op_mfu[i] = out->op_mbu[i] = out->op_sol[i] = -1;
+        continue;
+      }
+      out->op_mfu[i] = ppm_of((uint64_t)ev->flops[i], (uint64_t)T, (uint64_t)p->peak_flops);
+      out->op_mbu[i] = ppm_of((uint64_t)ev->bytes[i], (uint64_t)T, (uint64_t)p->peak_bytes);
+      out->op_sol[i] = out->op_mfu[i] > out->op_mbu[i] ? out->op_mfu[i] : out->op_mbu[i];
+      int o = ev->name[i];
+      out->opn_flops[o] = wrap_add(out->opn_flops[o], ev->flops[i]);
+      out->opn_bytes[o] = wrap_add(out->opn_bytes[o], ev->bytes[i]);
+      out->opn_time[o] = wrap_add(out->opn_time[o], T);
+      int64_t ref = p->ref_sol_ppm ? p->ref_sol_ppm[o] : 0;
+      if (ref > 0 && out->op_sol[i] < ref) {
+        unsigned __int128 x = (unsigned __int128)(uint64_t)T * (uint64_t)(ref - out->op_sol[i]);
+        out->opn_hot[o] = wrap_add(out->opn_hot[o], (int64_t)(uint64_t)(x / (uint64_t)ref));
+      }
+    }
+    for (int o = 0; o < NOP; ++o) {
+      uint64_t t = (uint64_t)out->opn_time[o];
+      if (t == 0) {
+        out->opn_sol[o] = -1;
+      } else {
+        int64_t f = ppm_of((uint64_t)out->opn_flops[o], t, (uint64_t)p->peak_flops);
+        int64_t b = ppm_of((uint64_t)out->opn_bytes[o], t, (uint64_t)p->peak_bytes);
+        out->opn_sol[o] = f > b ? f : b;
+      }
+    }
   }
 
   for (int64_t ps = 0; ps < (int64_t)P * S; ++ps) free(runs[ps]);

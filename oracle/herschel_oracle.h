@@ -24,6 +24,7 @@ typedef struct {
   const int64_t *ts, *te, *corr;
   const int32_t *pid, *lane, *name;
   const uint8_t *kind;
+  const int64_t *flops, *bytes; /* per CPU op (flags bit 3); may be NULL otherwise */
 } hro_events;
 
 typedef struct {
@@ -38,7 +39,9 @@ typedef struct {
   const uint8_t *stream_class; /* may be NULL */
   const hro_edge *edges;
   int64_t n_edges;
-  uint32_t flags; /* bit0: containment, bit1: overlap, bit2: idle coincidence */
+  uint32_t flags; /* bit0: containment, bit1: overlap, bit2: idle coincidence, bit3: SOL */
+  int64_t peak_flops, peak_bytes;   /* per second (bit 3) */
+  const int64_t *ref_sol_ppm;       /* [n_op_names] or NULL (bit 3) */
 } hro_params;
 
 typedef struct {
@@ -62,6 +65,8 @@ typedef struct {
   hro_counters *counters;
   int64_t *dev_idle;        /* [n_procs] (flags bit 2) */
   int64_t *op_span, *op_idle; /* [n_procs * n_op_names] (flags bit 2) */
+  int64_t *op_mfu, *op_mbu, *op_sol; /* [n] ppm at CPU_OP rows (flags bit 3) */
+  int64_t *opn_flops, *opn_bytes, *opn_time, *opn_sol, *opn_hot; /* [n_op_names] (flags bit 3) */
 } hro_outputs;
 
 /* Same return codes as the product: 0 ok, -1 bad parameter, -2 invalid row,

@@ -494,6 +494,27 @@ def config4_chunk(ids, workers: int = 16):
         return pool.map(_config4_columns, ids)
 
 
+def add_op_costs(cols: dict, params: dict, seed: int, ref: bool = True, flops_median: float = 2e9,
+                 bytes_median: float = 5e8, peak_flops: int = 2_500_000_000_000_000,
+                 peak_bytes: int = 8_000_000_000_000):
+    """Columns of per-op operation counts and logical bytes (the shapes an
+    analyzer recovers from Python object fields), device peaks and a
+    reference SOL per op name, for the operator-efficiency outputs.  Counts
+    are LogNormal (sigma 1.5) around 2 GFLOP and 0.5 GB per op by default,
+    peaks those of a device of 2.5 PFLOP/s and 8 TB/s; rows other than ops
+    get zeros."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    n = len(cols["ts"])
+    ops = np.asarray(cols["kind"]) == CPU_OP
+    flops = np.where(ops, np.rint(rng.lognormal(np.log(flops_median), 1.5, n)), 0).astype(np.int64)
+    nbytes = np.where(ops, np.rint(rng.lognormal(np.log(bytes_median), 1.5, n)), 0).astype(np.int64)
+    c = dict(cols, flops=flops, bytes=nbytes)
+    q = dict(params, peak_flops=int(peak_flops), peak_bytes=int(peak_bytes),
+             flags=int(params.get("flags", 3)) | 8 | 1)
+    q["ref_sol_ppm"] = rng.integers(0, 400_000, int(params["n_op_names"])).astype(np.int64) if ref else None
+    return c, q
+
+
 def config4_lengths(n_traces: int = 256) -> np.ndarray:
     return np.array([int(np.random.Generator(np.random.PCG64(4000 + t)).integers(200_000, 2_000_001))
                      for t in range(n_traces)], np.int64)

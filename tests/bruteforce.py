@@ -21,7 +21,7 @@ def _wrap(x: int) -> int:
     return x - (1 << 64) if x >= (1 << 63) else x
 
 
-def _valid(k, pid, lane, name, ts, te, corr, p) -> bool:
+def _valid(k, pid, lane, name, ts, te, corr, p, flops=0, nbytes=0) -> bool:
     if k not in (0, 1, 2):
         return False
     if not 0 <= pid < p["n_procs"]:
@@ -35,6 +35,8 @@ def _valid(k, pid, lane, name, ts, te, corr, p) -> bool:
         if k == 0 and not 0 <= name < p["n_op_names"]:
             return False
         if k == 1 and name < 0:
+            return False
+        if k == 0 and p["flags"] & 8 and (flops < 0 or nbytes < 0):
             return False
     if not (-ABS < ts < ABS and -ABS < te < ABS):
         return False
@@ -67,7 +69,8 @@ def analyze(cols: dict, p: dict):
                  name=int(cols["name"][i]), ts=int(cols["ts"][i]), te=int(cols["te"][i]),
                  corr=int(cols["corr"][i])) for i in range(n)]
     for i, r in enumerate(rows):
-        if not _valid(r["kind"], r["pid"], r["lane"], r["name"], r["ts"], r["te"], r["corr"], p):
+        fb = (int(cols["flops"][i]), int(cols["bytes"][i])) if p["flags"] & 8 else (0, 0)
+        if not _valid(r["kind"], r["pid"], r["lane"], r["name"], r["ts"], r["te"], r["corr"], p, *fb):
             return -2, dict(counters=dict(first_invalid=i))
     off = p.get("clock_offset")
     for r in rows:
@@ -236,6 +239,46 @@ def analyze(cols: dict, p: dict):
                 oidle[q, o] = np.count_nonzero(m & idle_ns)
         waits = dict(dev_idle=dev_idle, op_span=span.reshape(-1), op_idle=oidle.reshape(-1))
 
+    sol = None
+    if p["flags"] & 8:
+        # operator efficiency in parts per million with Python's exact
+        # integers: 10^15 * count / (T_op * peak), T_op from the op's
+        # inclusive kernel span; per op name over the measured ops
+        nop = p["n_op_names"]
+        PF, PB = int(p["peak_flops"]), int(p["peak_bytes"])
+        ref = p.get("ref_sol_ppm")
+        mfu, mbu, so = {}, {}, {}
+        nf, nb, nt, nh = [0] * nop, [0] * nop, [0] * nop, [0] * nop
+        for i in ops:
+            nk, first, last, _ = op_arrays[i]
+            T = last - first if nk > 0 else 0
+            if T <= 0:
+                mfu[i] = mbu[i] = so[i] = -1
+                continue
+            F, B = int(cols["flops"][i]), int(cols["bytes"][i])
+            mfu[i] = min(10**15 * F // (T * PF), I64_MAX)
+            mbu[i] = min(10**15 * B // (T * PB), I64_MAX)
+            so[i] = max(mfu[i], mbu[i])
+            o = rows[i]["name"]
+            nf[o] += F
+            nb[o] += B
+            nt[o] += T
+            r = 0 if ref is None else int(ref[o])
+            if r > 0 and so[i] < r:
+                nh[o] += T * (r - so[i]) // r
+        nsol = []
+        for o in range(nop):
+            t = nt[o] % (1 << 64)
+            if t == 0:
+                nsol.append(-1)
+            else:
+                f, b2 = nf[o] % (1 << 64), nb[o] % (1 << 64)
+                nsol.append(max(min(10**15 * f // (t * PF), I64_MAX), min(10**15 * b2 // (t * PB), I64_MAX)))
+        sol = dict(op_mfu=mfu, op_mbu=mbu, op_sol=so, opn_flops=np.array([_wrap(x) for x in nf], np.int64),
+                   opn_bytes=np.array([_wrap(x) for x in nb], np.int64),
+                   opn_time=np.array([_wrap(x) for x in nt], np.int64), opn_sol=np.array(nsol, np.int64),
+                   opn_hot=np.array([_wrap(x) for x in nh], np.int64))
+
     edges = p.get("edges")
     ew, es = [], []
     for e in ([] if edges is None else edges):
@@ -252,6 +295,6 @@ def analyze(cols: dict, p: dict):
                busy=busy, idle=idle, gaps=gaps, lat_hist=np.array(hist, np.int64),
                name_count=np.array(ncount, np.int64), name_sum=np.array(nsum, np.int64),
                name_min=np.array(nmin, np.int64), name_max=np.array(nmax, np.int64),
-               op=op_arrays, overlap=ov, waits=waits, edge_wait=np.array(ew, np.int64),
+               op=op_arrays, overlap=ov, waits=waits, sol=sol, edge_wait=np.array(ew, np.int64),
                edge_status=np.array(es, np.int32))
     return 0, out

@@ -40,3 +40,9 @@ def load_golden(name: str):
     exp["edge_wait"] = [_val(x) for x in exp["edge_wait"]]
     exp["op"] = {int(k): [_val(x) for x in v] for k, v in exp["op"].items()}
     return cols, p, g
+
+
+def load_golden_raw(name: str) -> dict:
+    """A golden fixture's JSON as written (fixtures that are not row tables)."""
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)

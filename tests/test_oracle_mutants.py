@@ -82,6 +82,20 @@ MUTANTS = [
     ("consumer latest", "if (side == 1 && ts[r] < cons_start) cons_start = ts[r];",
      "if (side == 1 && (cons_start == I64_MAX || ts[r] > cons_start)) cons_start = ts[r];"),
     ("wait sign", "wrap_sub(cons_start, prod_end)", "wrap_sub(prod_end, cons_start)"),
+    ("SOL as the smaller", "out->op_sol[i] = out->op_mfu[i] > out->op_mbu[i]",
+     "out->op_sol[i] = out->op_mfu[i] < out->op_mbu[i]"),
+    ("MBU over the compute peak", "out->op_mbu[i] = ppm_of((uint64_t)ev->bytes[i], (uint64_t)T, (uint64_t)p->peak_bytes);",
+     "out->op_mbu[i] = ppm_of((uint64_t)ev->bytes[i], (uint64_t)T, (uint64_t)p->peak_flops);"),
+    ("T_op as kernel time", "int64_t T = out->op_nkern[i] > 0 ? wrap_sub(out->op_last[i], out->op_first[i]) : 0;",
+     "int64_t T = out->op_nkern[i] > 0 ? out->op_ksum[i] : 0;"),
+    ("ppm scale off by ten", "(unsigned __int128)x * 1000000000000000ull;", "(unsigned __int128)x * 100000000000000ull;"),
+    ("ppm not saturated", "return q > (unsigned __int128)I64_MAX ? I64_MAX : (int64_t)q;", "return (int64_t)q;"),
+    ("hotness at or above reference", "if (ref > 0 && out->op_sol[i] < ref) {", "if (ref > 0) {"),
+    ("hotness over SOL", "(int64_t)(uint64_t)(x / (uint64_t)ref)", "(int64_t)(uint64_t)(x / (uint64_t)out->op_sol[i])"),
+    ("name MFU dropped", "int64_t f = ppm_of((uint64_t)out->opn_flops[o], t, (uint64_t)p->peak_flops);",
+     "int64_t f = 0;"),
+    ("hotness overwritten", "out->opn_hot[o] = wrap_add(out->opn_hot[o], (int64_t)(uint64_t)(x / (uint64_t)ref));",
+     "out->opn_hot[o] = (int64_t)(uint64_t)(x / (uint64_t)ref);"),
     ("edge status bits swapped", "(found[0] ? 0 : 1) | (found[1] ? 0 : 2)", "(found[0] ? 0 : 2) | (found[1] ? 0 : 1)"),
 ]
 
@@ -112,6 +126,14 @@ def _battery(lib) -> None:
     code, o = oracle.analyze(cols, p, lib=lib)
     for k in ("dev_idle", "op_span", "op_idle"):
         assert o[k].tolist() == exp[k], k
+    pins.check_pa_case(lib)
+    for seed in pins.SOL_BF_SEEDS[::3] + [4, 5, 29]:  # 4, 5, 29: two ops of one name below its reference
+        cols, p = pins.sol_case(seed)
+        code, o = oracle.analyze(cols, p, lib=lib)
+        bcode, b = bruteforce.analyze(cols, p)
+        assert code == bcode
+        if code == 0:
+            pins._bf_compare(cols, p, o, b, f"sol seed {seed}")
 
 
 @pytest.fixture(scope="module")

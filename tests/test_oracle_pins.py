@@ -16,7 +16,7 @@ import pytest
 import bruteforce
 import oracle
 from compare import COUNTERS, assert_same
-from fixtures import I64_MAX, I64_MIN, load_golden
+from fixtures import I64_MAX, I64_MIN, load_golden, load_golden_raw
 from paper_2609_40247_amd import synth
 
 GOLDEN = ["t1_worked_timeline.json", "t2_worked_timeline.json"]
@@ -100,6 +100,12 @@ def _bf_compare(cols, p, o, b, ctx):
     if p["flags"] & 4:
         for k, v in b["waits"].items():
             assert o[k].tolist() == v.tolist(), f"{ctx}: {k}"
+    if p["flags"] & 8:
+        for k in ("op_mfu", "op_mbu", "op_sol"):
+            for r, v in b["sol"][k].items():
+                assert int(o[k][r]) == v, f"{ctx}: {k} row {r}"
+        for k in ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot"):
+            assert o[k].tolist() == b["sol"][k].tolist(), f"{ctx}: {k}"
 
 
 BF_CASES = [dict(seed=s) for s in range(120)] + [
@@ -114,6 +120,31 @@ BF_CASES = [dict(seed=s) for s in range(120)] + [
     dict(seed=5000 + s, flags=7 if s % 2 else 4) for s in range(40)] + [
     dict(seed=5100 + s, n_rows=150, window=700, n_procs=2, n_streams=3, n_threads=3, n_op_names=3, flags=7)
     for s in range(20)]
+
+
+SOL_BF_SEEDS = list(range(40))
+
+
+def sol_case(seed):
+    """A tiny adversarial trace with per-op counts scaled to its nanosecond
+    ops, so that SOL falls on both sides of the reference; every fourth case
+    saturates the ppm at INT64_MAX with peaks of 1 /s."""
+    tr = synth.random_small(seed=6000 + seed, n_rows=80 if seed % 2 else 40, window=500)
+    tiny = seed % 4 == 3
+    return synth.add_op_costs(tr.columns(), tr.params, seed, ref=seed % 3 != 0, flops_median=1e7,
+                              bytes_median=3e4, peak_flops=1 if tiny else 2_500_000_000_000_000,
+                              peak_bytes=1 if tiny else 8_000_000_000_000)
+
+
+@pytest.mark.parametrize("seed", SOL_BF_SEEDS)
+def test_bruteforce_sol(seed):
+    """Operator efficiency against Python's exact integers on tiny traces."""
+    cols, p = sol_case(seed)
+    code, o = oracle.analyze(cols, p)
+    bcode, b = bruteforce.analyze(cols, p)
+    assert code == bcode
+    if code == 0:
+        _bf_compare(cols, p, o, b, f"sol seed {seed}")
 
 
 @pytest.mark.parametrize("case", BF_CASES, ids=lambda c: f"seed{c['seed']}")
@@ -561,5 +592,81 @@ def test_idle_coincidence_name_limit():
     p["n_op_names"] = 2048
     assert oracle.analyze(cols, p)[0] == 0
     p["n_op_names"] = 2049
+    assert oracle.analyze(cols, p)[0] == -1
+
+
+# --------------------------------------------------------------------------- operator efficiency
+
+def pa_trace(T):
+    """One op, one launch and one kernel of T ns: T_op = T."""
+    g = load_golden_raw("pa_sol_case.json")
+    rows = [(0, 0, 0, 0, T + 2000, 0, 0), (1, 0, 0, 100, 200, 7, 0), (2, 0, 0, 1000, 1000 + T, 7, 0)]
+    a = np.array(rows, dtype=np.int64)
+    cols = dict(kind=a[:, 0].astype(np.uint8), pid=a[:, 1].astype(np.int32), lane=a[:, 2].astype(np.int32),
+                ts=a[:, 3], te=a[:, 4], corr=a[:, 5], name=a[:, 6].astype(np.int32),
+                flops=np.array([g["flops"], 0, 0], np.int64), bytes=np.array([g["bytes"], 0, 0], np.int64))
+    p = synth.empty_params(window_begin=0, window_end=2 * 10**9, gap_threshold=0, flags=1 | 8,
+                           peak_flops=g["peak_flops"], peak_bytes=g["peak_bytes"],
+                           ref_sol_ppm=np.array([g["ref_sol_ppm"]], np.int64))
+    return cols, p, g
+
+
+def test_pa_case_arithmetic():
+    """The printed PagedAttention figures: SOL is the larger of MFU and MBU,
+    it scales with 1/T_op (a 60.9% cut takes 7.32% to 18.7%, +155%), and the
+    recoverable time against a 17% reference."""
+    check_pa_case()
+
+
+def check_pa_case(lib=None):
+    res = {}
+    for phase in ("before", "after"):
+        cols, p, g = pa_trace(load_golden_raw("pa_sol_case.json")[phase]["T_op"])
+        code, o = oracle.analyze(cols, p, lib=lib)
+        assert code == 0
+        e = g[phase]
+        assert [int(o["op_mfu"][0]), int(o["op_mbu"][0]), int(o["op_sol"][0])] == [e["mfu"], e["mbu"], e["sol"]]
+        assert int(o["opn_hot"][0]) == e["hot"] and int(o["opn_sol"][0]) == e["sol"]
+        assert int(o["opn_time"][0]) == e["T_op"]
+        assert o["op_sol"][1:].tolist() == [oracle.UNWRITTEN_I64] * 2  # launch and kernel rows
+        res[phase] = e["sol"]
+    assert round(res["before"] / 1e4, 1) == 7.3 and round(res["after"] / 1e4, 1) == 18.7
+    assert int(100 * (res["after"] / res["before"] - 1)) == 155
+
+
+def test_sol_unmeasured_and_invariants():
+    """An op without kernels, or whose kernels span no time, is unmeasured
+    (-1); SOL is the larger of MFU and MBU; per-name sums cover the measured
+    ops only; Hotness never exceeds the measured time."""
+    tr = synth.config0()
+    cols, p = synth.add_op_costs(tr.columns(), tr.params, 3)
+    code, o = oracle.analyze(cols, p)
+    assert code == 0
+    ops = np.flatnonzero((cols["kind"] == 0) & (o["link"] != -2))
+    meas = ops[o["op_nkern"][ops] > 0]
+    meas = meas[o["op_last"][meas] > o["op_first"][meas]]
+    un = np.setdiff1d(ops, meas)
+    assert len(un) and (o["op_sol"][un] == -1).all() and (o["op_mfu"][un] == -1).all()
+    assert (o["op_sol"][meas] == np.maximum(o["op_mfu"][meas], o["op_mbu"][meas])).all()
+    T = o["op_last"][meas] - o["op_first"][meas]
+    nm = cols["name"][meas]
+    assert (np.bincount(nm, weights=T, minlength=p["n_op_names"]).astype(np.int64) == o["opn_time"]).all()
+    assert (o["opn_hot"] <= o["opn_time"]).all() and (o["opn_hot"] >= 0).all()
+
+
+@pytest.mark.parametrize("change", ["no containment", "zero peak", "negative reference", "negative flops"])
+def test_sol_errors(change):
+    cols, p, g = pa_trace(10**9)
+    if change == "no containment":
+        p["flags"] = 8
+    elif change == "zero peak":
+        p["peak_bytes"] = 0
+    elif change == "negative reference":
+        p["ref_sol_ppm"] = np.array([-1], np.int64)
+    else:
+        cols["flops"][0] = -5
+        code, o = oracle.analyze(cols, p)
+        assert code == -2 and o["counters"]["first_invalid"] == 0
+        return
     assert oracle.analyze(cols, p)[0] == -1
 
