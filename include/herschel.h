@@ -20,6 +20,10 @@
  *    to the latest end of the op's kernels), idle intervals of the GPU activity (the idle
  *    evidence of the case study in Section 9.1), communication overlapped
  *    with computation measured as interval coverage, and cross-process waits.
+ *  - Operator efficiency (Section 6.1): MFU, MBU and SOL = max(MFU, MBU) of
+ *    each op from its operation count and logical bytes over T_op and the
+ *    device peaks, and per op name the time that reaching a reference SOL
+ *    would save (the time-weighted gap to the reference of Section 6.2).
  *
  * Every entry point takes DEVICE pointers for all arrays (events, params
  * arrays, outputs, workspace), enqueues its kernels on params->hip_stream,
@@ -63,6 +67,8 @@ enum {
 #define HERSCHEL_OUT_CONTAIN 0x1u /* op nesting, launch->op, kernel->op, per-op aggregates */
 #define HERSCHEL_OUT_OVERLAP 0x2u /* cross-stream overlap and class coverage */
 #define HERSCHEL_OUT_WAITS 0x4u   /* GPU idle coinciding with CPU ops, by op name (Section 9.1) */
+#define HERSCHEL_OUT_SOL 0x8u     /* operator efficiency: MFU, MBU, SOL, per-name hotness (Section 6.1);
+                                     needs HERSCHEL_OUT_CONTAIN */
 
 /* Implementation limits (checked; EINVAL when exceeded). */
 #define HERSCHEL_MAX_PROCS 4096
@@ -76,10 +82,11 @@ enum {
                                               indexed with int32, radix look-back words hold 30-bit prefixes */
 
 /* Input records as a structure of arrays, n rows, in any order (delivery
- * order).  37 bytes per row.  Row i is valid iff
+ * order).  37 bytes per row (53 with HERSCHEL_OUT_SOL).  Row i is valid iff
  *   kind[i] in {CPU_OP, LAUNCH, KERNEL}, 0 <= pid[i] < n_procs,
  *   KERNEL: 0 <= lane < n_streams and 0 <= name < n_names,
  *   CPU_OP: 0 <= lane < n_threads and 0 <= name < n_op_names,
+ *           and with HERSCHEL_OUT_SOL flops >= 0 and bytes >= 0,
  *   LAUNCH: 0 <= lane < n_threads and name >= 0 (an API id),
  *   -2^62 < ts <= te < 2^62.
  * corr may be any int64 (an opaque per-process id, Section 5.2). */
@@ -91,6 +98,12 @@ typedef struct {
   const int32_t *lane; /* KERNEL: device stream; CPU_OP / LAUNCH: native thread */
   const int32_t *name; /* KERNEL: kernel-name id; CPU_OP: op-name id; LAUNCH: API id */
   const uint8_t *kind; /* HERSCHEL_CPU_OP / _LAUNCH / _KERNEL */
+  /* HERSCHEL_OUT_SOL only (else may be NULL): per CPU_OP row, the op's
+   * floating-point operation count F and the logical bytes B it must move,
+   * as the analyzer derives them from the call's arguments (Section 5.2,
+   * "Python calls and object fields"); read at CPU_OP rows only. */
+  const int64_t *flops;
+  const int64_t *bytes;
 } herschel_events;
 
 /* A cross-process dependency edge (Figure "Key performance observations",
@@ -113,6 +126,12 @@ typedef struct {
   void *hip_stream;             /* hipStream_t to enqueue on; NULL = the null stream */
   void *workspace;              /* device scratch owned by the caller, 256-byte aligned (hipMalloc's are) */
   size_t workspace_bytes;
+  /* HERSCHEL_OUT_SOL only: the device's peak compute (FLOP/s) and memory
+   * bandwidth (B/s), both > 0, and per op name a reference SOL in parts per
+   * million (>= 0; the SOL the same op reaches elsewhere, Section 9.4), or
+   * NULL for no reference. */
+  int64_t peak_flops, peak_bytes;
+  const int64_t *ref_sol_ppm;   /* [n_op_names] or NULL */
 } herschel_params;
 
 typedef struct {
@@ -173,6 +192,21 @@ typedef struct {
   int64_t *dev_idle;                 /* [n_procs] total length of the idle intervals */
   int64_t *op_span;                  /* [n_procs * n_op_names] |U(p, o)| */
   int64_t *op_idle;                  /* [n_procs * n_op_names] |U(p, o) within the idle intervals| */
+  /* HERSCHEL_OUT_SOL (Section 6.1, "Operator execution and efficiency"): an
+   * admitted op is measured when it has kernels and T_op = op_last - op_first
+   * > 0.  In parts per million, exact (integer arithmetic in 128 bits),
+   * saturating at INT64_MAX:
+   *   MFU = floor(10^15 F / (T_op peak_flops)), MBU = floor(10^15 B / (T_op peak_bytes)),
+   *   SOL = max(MFU, MBU);
+   * an unmeasured op gets -1 in all three.  Per op name o, over its measured
+   * ops: the sums of F, B and T_op (wrapping), the SOL of those sums (-1
+   * with no measured op), and the hotness, the sum over ops below the
+   * name's reference ref of floor(T_op (ref - SOL) / ref): the time the
+   * name's ops would save at the reference SOL. */
+  int64_t *op_mfu, *op_mbu, *op_sol; /* [n], written at admitted CPU_OP rows only */
+  int64_t *opn_flops, *opn_bytes;    /* [n_op_names] */
+  int64_t *opn_time, *opn_sol;       /* [n_op_names] */
+  int64_t *opn_hot;                  /* [n_op_names] ns */
 } herschel_outputs;
 
 /* Bytes of device workspace that herschel_trace_analyze needs for n rows
@@ -243,7 +277,8 @@ enum {
   HERSCHEL_STAGE_EDGES = 10,   /* dependency waits */
   HERSCHEL_STAGE_FINAL = 11,   /* counters and histogram totals */
   HERSCHEL_STAGE_WAITS = 12,   /* device-lane and op-name unions, idle coincidence (OUT_WAITS) */
-  HERSCHEL_N_STAGES = 13
+  HERSCHEL_STAGE_SOL = 13,     /* operator efficiency and per-name hotness (OUT_SOL), after OPAGG */
+  HERSCHEL_N_STAGES = 14
 };
 
 /* Record start_event / stop_event (hipEvent_t, created by the caller) on

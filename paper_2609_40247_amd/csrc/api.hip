@@ -79,6 +79,7 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.dg_status = b.take<uint64_t>(c.dg_tiles);
     c.dbusy_ws = b.take<int64_t>(c.P);
   }
+  if (c.sol) c.sol_tot = b.take<uint64_t>((int64_t)c.NOP * 4);
   if (c.contain) {
     c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
     c.vb_status = b.take<uint64_t>(c.vb_tiles);
@@ -173,6 +174,13 @@ size_t layout_workspace(Ctx& c, char* base) {
   }
   c.name_blocks = names_block_count(n, c.NN);
   if (c.NN <= names_lds_limit()) c.name_part = b.take<uint64_t>((int64_t)c.name_blocks * c.NN * 4);
+  if (c.sol) {
+    c.sol_blocks = sol_block_count(n, c.NOP);
+    if (sol_uses_tables(c.NOP)) c.sol_part = b.take<uint64_t>((int64_t)c.sol_blocks * c.NOP * 4);
+    c.op_nkern_ws = b.take<int32_t>(n);
+    c.op_first_ws = b.take<int64_t>(n);
+    c.op_last_ws = b.take<int64_t>(n);
+  }
   return b.off;
 }
 
@@ -346,7 +354,15 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   if (p->n_names < 1 || p->n_names > HERSCHEL_MAX_NAMES) return HERSCHEL_EINVAL;
   if (p->n_op_names < 1) return HERSCHEL_EINVAL;
   if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return HERSCHEL_EINVAL;
-  if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP | HERSCHEL_OUT_WAITS)) return HERSCHEL_EINVAL;
+  if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP | HERSCHEL_OUT_WAITS | HERSCHEL_OUT_SOL))
+    return HERSCHEL_EINVAL;
+  // operator efficiency reads the per-op aggregates of containment, the
+  // ops' counts and the device's peaks
+  if (p->flags & HERSCHEL_OUT_SOL) {
+    if (!(p->flags & HERSCHEL_OUT_CONTAIN)) return HERSCHEL_EINVAL;
+    if (p->peak_flops <= 0 || p->peak_bytes <= 0) return HERSCHEL_EINVAL;
+    if (n > 0 && (!ev->flops || !ev->bytes)) return HERSCHEL_EINVAL;
+  }
   // the op-name key (pid, name, ts') and its run endpoints must fit 64 bits
   if ((p->flags & HERSCHEL_OUT_WAITS) && p->n_op_names > HERSCHEL_MAX_WAIT_OP_NAMES) return HERSCHEL_EINVAL;
   const bool contain = (p->flags & HERSCHEL_OUT_CONTAIN) != 0, overlap = (p->flags & HERSCHEL_OUT_OVERLAP) != 0;
@@ -371,6 +387,7 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   c.contain = contain;
   c.overlap = overlap;
   c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
+  c.sol = (p->flags & HERSCHEL_OUT_SOL) != 0;
   c.nob = bits_host((uint64_t)(c.NOP - 1));
   c.pb = bits_host((uint64_t)(c.P - 1));
   c.sb = bits_host((uint64_t)(c.S - 1));
@@ -540,6 +557,9 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_OPAGG);
   if (c.contain) launch_opagg(c);
   stage_end(c, HERSCHEL_STAGE_OPAGG);
+  stage_begin(c, HERSCHEL_STAGE_SOL);
+  if (c.sol) launch_sol(c);
+  stage_end(c, HERSCHEL_STAGE_SOL);
   wait(c.st, 1);
   wait(c.st, 4);
   stage_begin(c, HERSCHEL_STAGE_FINAL);
@@ -763,6 +783,7 @@ int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) 
     return HERSCHEL_EINVAL;
   if ((p->flags & HERSCHEL_OUT_WAITS) && (p->n_op_names < 1 || p->n_op_names > HERSCHEL_MAX_WAIT_OP_NAMES))
     return HERSCHEL_EINVAL;
+  if ((p->flags & HERSCHEL_OUT_SOL) && p->n_op_names < 1) return HERSCHEL_EINVAL;
   Ctx c;
   c.p = *p;
   c.n = n;
@@ -773,6 +794,7 @@ int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) 
   c.W = p->window_end - p->window_begin;
   c.contain = (p->flags & HERSCHEL_OUT_CONTAIN) != 0;
   c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
+  c.sol = (p->flags & HERSCHEL_OUT_SOL) != 0;
   c.NOP = p->n_op_names;
   c.nob = bits_host((uint64_t)(c.NOP > 0 ? c.NOP - 1 : 0));
   c.overlap = (p->flags & HERSCHEL_OUT_OVERLAP) != 0;
@@ -792,6 +814,11 @@ static void redirect_outputs(Ctx& c) {
   if (!c.contain) return;
   if (!c.o.link) c.o.link = c.link_ws;
   if (!c.o.aux) c.o.aux = c.aux_ws;
+  // operator efficiency reads the per-op aggregates back
+  if (!c.sol) return;
+  if (!c.o.op_nkern) c.o.op_nkern = c.op_nkern_ws;
+  if (!c.o.op_first) c.o.op_first = c.op_first_ws;
+  if (!c.o.op_last) c.o.op_last = c.op_last_ws;
 }
 
 static int prepare(Ctx& c, const herschel_events* ev, int64_t n, const herschel_params* p, const herschel_outputs* out,
@@ -863,6 +890,8 @@ int herschel_trace_analyze_batch(const herschel_events* ev, const int64_t* trace
       e.lane += o;
       e.name += o;
       e.kind += o;
+      if (e.flops) e.flops += o;
+      if (e.bytes) e.bytes += o;
     }
     herschel_params pt = p[t];
     pt.hip_stream = p[0].hip_stream;

@@ -52,7 +52,7 @@ struct Ctx {
   herschel_outputs o{};
   int64_t W0 = 0, W1 = 0, W = 0, thr = 0;
   int P = 0, S = 0, T = 0, NN = 0, NOP = 0;
-  bool contain = false, overlap = false, waits = false;
+  bool contain = false, overlap = false, waits = false, sol = false;
   int nob = 0;                         // bits of an op name (idle coincidence)
   int pb = 0, sb = 0, tb = 0, wb = 0;  // key field widths: pid, stream, thread, ts'-W0
   int wb1 = 0;                         // bits of W (values 0..W)
@@ -119,6 +119,12 @@ struct Ctx {
   int64_t ag_tiles = 0;
   uint64_t* name_part = nullptr;     // [name_blocks * NN * 4] per-block name tables
   int name_blocks = 0;
+  uint64_t* sol_part = nullptr;      // [sol_blocks * NOP * 4] per-block op-name tables (operator efficiency)
+  uint64_t* sol_tot = nullptr;       // [NOP * 4] their totals (zeroed with the state)
+  int sol_blocks = 0;
+  int32_t* op_nkern_ws = nullptr;    // [n] per-op aggregates when those outputs are NULL
+  int64_t* op_first_ws = nullptr;    //     (operator efficiency reads them back)
+  int64_t* op_last_ws = nullptr;
   char* zero_begin = nullptr;        // region cleared at the start of a call
   size_t zero_bytes = 0;
 };
@@ -144,6 +150,9 @@ void launch_names_reduce(Ctx& c);
 void launch_join_table(Ctx& c);
 void launch_edges(Ctx& c);
 void launch_finalize(Ctx& c);
+void launch_sol(Ctx& c);
+int sol_block_count(int64_t n_max, int NOP);
+bool sol_uses_tables(int NOP);
 
 int64_t prep_tile_rows();
 int64_t union_tile_elems();

@@ -31,6 +31,7 @@ struct PrepArgs {
   bool jt_range;  // find each process's id range (at most JT_PROCS processes)
   bool waits;     // the op-name list and device-lane keys (idle coincidence)
   int nob;        // bits of an op name
+  bool sol;       // ops carry operation counts and bytes (operator efficiency), which must be >= 0
   DevState* ds;
   herschel_counters* cnt;
   int32_t* link;
@@ -99,7 +100,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
     // rows past the end load the last row (clamped index) and are ignored
     int kind_[PREP_BATCH];
     int32_t pid_[PREP_BATCH], lane_[PREP_BATCH], name_[PREP_BATCH];
-    int64_t ts_[PREP_BATCH], te_[PREP_BATCH], corr_[PREP_BATCH];
+    int64_t ts_[PREP_BATCH], te_[PREP_BATCH], corr_[PREP_BATCH], cost_[PREP_BATCH];
 #pragma unroll
     for (int u = 0; u < PREP_BATCH; ++u) {
       const int64_t r = base + (int64_t)(j0 + u) * PREP_THREADS + tid;
@@ -111,6 +112,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
       ts_[u] = a.ev.ts[rc];
       te_[u] = a.ev.te[rc];
       corr_[u] = a.ev.corr[rc];
+      // an op's counts: negative iff either is (loaded for every kind)
+      cost_[u] = a.sol ? a.ev.flops[rc] | a.ev.bytes[rc] : 0;
     }
 #pragma unroll
     for (int u = 0; u < PREP_BATCH; ++u) {
@@ -129,7 +132,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
         if (kind == HERSCHEL_KERNEL)
           ok = ok && ln >= 0 && ln < a.S && name >= 0 && name < a.NN;
         else
-          ok = ok && ln >= 0 && ln < a.T && name >= 0 && (kind != HERSCHEL_CPU_OP || name < a.NOP);
+          ok = ok && ln >= 0 && ln < a.T && name >= 0 &&
+               (kind != HERSCHEL_CPU_OP || (name < a.NOP && cost_[u] >= 0));
         ok = ok && ts > -LIM && ts < LIM && te > -LIM && te < LIM && te >= ts;
         bool adm = false;
         int64_t rel = 0;
@@ -309,6 +313,7 @@ void launch_prep(Ctx& c) {
   a.jt_range = c.P <= JT_PROCS;
   a.waits = c.waits;
   a.nob = c.nob;
+  a.sol = c.sol;
   a.ds = c.ds;
   a.cnt = c.o.counters;
   a.link = c.o.link;

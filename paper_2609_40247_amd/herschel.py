@@ -24,13 +24,13 @@ _LIBS = {"release": "libherschel.so", "checked": "libherschel_checked.so"}
 CPU_OP, LAUNCH, KERNEL = 0, 1, 2
 OK, EINVAL, EEVENT, ECAPACITY, EWORKSPACE, EDEVICE, ETOOBIG = 0, -1, -2, -3, -4, -5, -6
 STATIC_SCRATCH_BYTES = 64 << 20  # HERSCHEL_STATIC_SCRATCH_BYTES
-OUT_CONTAIN, OUT_OVERLAP, OUT_WAITS = 0x1, 0x2, 0x4
+OUT_CONTAIN, OUT_OVERLAP, OUT_WAITS, OUT_SOL = 0x1, 0x2, 0x4, 0x8
 
 _P = ctypes.c_void_p
 
 
 class HerschelEvents(ctypes.Structure):
-    _fields_ = [(k, _P) for k in ("ts", "te", "corr", "pid", "lane", "name", "kind")]
+    _fields_ = [(k, _P) for k in ("ts", "te", "corr", "pid", "lane", "name", "kind", "flops", "bytes")]
 
 
 class HerschelParams(ctypes.Structure):
@@ -40,7 +40,8 @@ class HerschelParams(ctypes.Structure):
                 ("n_names", ctypes.c_int32), ("n_op_names", ctypes.c_int32),
                 ("clock_offset", _P), ("stream_class", _P), ("edges", _P),
                 ("n_edges", ctypes.c_int64), ("flags", ctypes.c_uint32), ("hip_stream", _P),
-                ("workspace", _P), ("workspace_bytes", ctypes.c_size_t)]
+                ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
+                ("peak_flops", ctypes.c_int64), ("peak_bytes", ctypes.c_int64), ("ref_sol_ppm", _P)]
 
 
 COUNTERS = ("n_admitted_cpu", "n_admitted_launch", "n_admitted_kernel", "n_outside_window", "n_matched",
@@ -54,7 +55,11 @@ class HerschelOutputs(ctypes.Structure):
                                   "name_sum", "name_min", "name_max", "lat_hist", "edge_wait", "edge_status")] + [
         ("gap_capacity", ctypes.c_int64)] + [(k, _P) for k in ("gap_pid", "gap_stream", "gap_begin", "gap_end",
                                                                "gap_flags", "counters", "dev_idle", "op_span",
-                                                               "op_idle")]
+                                                               "op_idle", "op_mfu", "op_mbu", "op_sol",
+                                                               "opn_flops", "opn_bytes", "opn_time", "opn_sol",
+                                                               "opn_hot")]
+SOL_ROW_OUTPUTS = ("op_mfu", "op_mbu", "op_sol")
+SOL_NAME_OUTPUTS = ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot")
 
 
 _lib = {}
@@ -137,7 +142,7 @@ def herschel_trace_analyze_batch(events: HerschelEvents, offsets: np.ndarray, pa
 
 
 STAGES = ("init", "prep", "hist", "names", "sort", "timeline", "overlap", "contain", "join", "opagg", "edges",
-          "final", "waits")
+          "final", "waits", "sol")
 
 
 def herschel_time_stage(stage: int, start_event, stop_event, lib=None) -> int:
@@ -173,9 +178,12 @@ def _ptr(t) -> int | None:
 
 
 def device_columns(cols: dict, device="cuda") -> dict:
-    """Host numpy columns -> contiguous device tensors of the ABI's types."""
-    dt = dict(ts=np.int64, te=np.int64, corr=np.int64, pid=np.int32, lane=np.int32, name=np.int32, kind=np.uint8)
-    return {k: torch.from_numpy(np.ascontiguousarray(cols[k], dtype=dt[k])).to(device) for k in dt}
+    """Host numpy columns -> contiguous device tensors of the ABI's types
+    (flops and bytes only when the columns hold them)."""
+    dt = dict(ts=np.int64, te=np.int64, corr=np.int64, pid=np.int32, lane=np.int32, name=np.int32, kind=np.uint8,
+              flops=np.int64, bytes=np.int64)
+    return {k: torch.from_numpy(np.ascontiguousarray(cols[k], dtype=dt[k])).to(device)
+            for k in dt if cols.get(k) is not None}
 
 
 def events_struct(dcols: dict, offset: int = 0) -> HerschelEvents:
@@ -203,6 +211,8 @@ class Analyzer:
         self.n_edges = 0 if edges is None else len(edges)
         self.d_off = None if off is None else torch.from_numpy(np.ascontiguousarray(off, np.int64)).to(device)
         self.d_cls = None if cls is None else torch.from_numpy(np.ascontiguousarray(cls, np.uint8)).to(device)
+        ref = params.get("ref_sol_ppm")
+        self.d_ref = None if ref is None else torch.from_numpy(np.ascontiguousarray(ref, np.int64)).to(device)
         self.d_edges = None
         if self.n_edges:
             raw = np.ascontiguousarray(edges).view(np.uint8).reshape(-1)
@@ -234,6 +244,8 @@ class Analyzer:
             gap_end=z(gc, torch.int64), gap_flags=z(gc, torch.uint8), counters=z(len(COUNTERS), torch.int64),
             dev_idle=z(P, torch.int64), op_span=z(P * int(params["n_op_names"]), torch.int64),
             op_idle=z(P * int(params["n_op_names"]), torch.int64),
+            **{k: z(n, torch.int64) for k in SOL_ROW_OUTPUTS},
+            **{k: z(int(params["n_op_names"]), torch.int64) for k in SOL_NAME_OUTPUTS},
         )
         self.params = self._params_struct(self.ws.data_ptr(), self.ws_bytes)
         self.outs = HerschelOutputs(gap_capacity=self.gap_capacity,
@@ -248,12 +260,13 @@ class Analyzer:
             n_threads=int(p["n_threads"]), n_names=int(p["n_names"]), n_op_names=int(p["n_op_names"]),
             clock_offset=_ptr(self.d_off), stream_class=_ptr(self.d_cls), edges=_ptr(self.d_edges),
             n_edges=self.n_edges, flags=int(p.get("flags", 3)), hip_stream=st, workspace=ws,
-            workspace_bytes=ws_bytes)
+            workspace_bytes=ws_bytes, peak_flops=int(p.get("peak_flops", 0)), peak_bytes=int(p.get("peak_bytes", 0)),
+            ref_sol_ppm=_ptr(self.d_ref))
 
     def prefill(self) -> None:
         """Fill the op arrays with a marker so rows the library must not write
         can be checked."""
-        for k in ("op_nkern", "op_first", "op_last", "op_ksum"):
+        for k in ("op_nkern", "op_first", "op_last", "op_ksum") + SOL_ROW_OUTPUTS:
             self.o[k].fill_(self.op_fill)
 
     def run(self, events: HerschelEvents, n: int) -> int:
@@ -265,9 +278,9 @@ class Analyzer:
         """Copy the outputs of the last call to host numpy (oracle layout)."""
         h = {k: v.cpu().numpy() for k, v in self.o.items()}
         c = dict(zip(COUNTERS, (int(x) for x in h.pop("counters"))))
-        res = {k: h[k][:n] for k in ("link", "aux", "op_nkern", "op_first", "op_last", "op_ksum")}
+        res = {k: h[k][:n] for k in ("link", "aux", "op_nkern", "op_first", "op_last", "op_ksum") + SOL_ROW_OUTPUTS}
         for k in ("busy", "idle", "pair_overlap", "class_busy", "class_overlap", "any_busy", "name_count",
-                  "name_sum", "name_min", "name_max", "lat_hist", "dev_idle", "op_span", "op_idle"):
+                  "name_sum", "name_min", "name_max", "lat_hist", "dev_idle", "op_span", "op_idle") + SOL_NAME_OUTPUTS:
             res[k] = h[k]
         res["edge_wait"] = h["edge_wait"][:self.n_edges]
         res["edge_status"] = h["edge_status"][:self.n_edges]

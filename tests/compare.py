@@ -42,5 +42,7 @@ def assert_same(got: tuple, want: tuple, params: dict, ctx: str = "") -> None:
         keys += ["pair_overlap", "class_busy", "class_overlap", "any_busy"]
     if params.get("flags", 3) & 4:
         keys += ["dev_idle", "op_span", "op_idle"]
+    if params.get("flags", 3) & 8:
+        keys += ["op_mfu", "op_mbu", "op_sol", "opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot"]
     for k in keys:
         _eq(k, g[k], w[k], ctx)

@@ -64,3 +64,62 @@ def test_host_only_entry_points(libs):
     assert lib.herschel_time_stage(1, None, None) == 0
     lib.herschel_sort_stats.restype = ctypes.c_int
     assert lib.herschel_sort_stats(None, None) == -1
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The binding's ctypes structures (and the edge record's numpy dtype)
+    have the header's sizes and field offsets, as the host C compiler lays
+    them out."""
+    from paper_2609_40247_amd import herschel as H
+    from paper_2609_40247_amd import synth
+    structs = {"herschel_events": H.HerschelEvents, "herschel_params": H.HerschelParams,
+               "herschel_outputs": H.HerschelOutputs}
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "herschel.h"', "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append(f'  printf("{cname} %zu\\n", sizeof({cname}));')
+        for f, _ in cls._fields_:
+            lines.append(f'  printf("{cname}.{f} %zu\\n", offsetof({cname}, {f}));')
+    lines.append('  printf("herschel_edge %zu\\n", sizeof(herschel_edge));')
+    for f in synth.EDGE_DTYPE.names:
+        lines.append(f'  printf("herschel_edge.{f} %zu\\n", offsetof(herschel_edge, {f}));')
+    lines.append('  printf("herschel_counters %zu\\n", sizeof(herschel_counters));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    import subprocess
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(src)], check=True)
+    got = dict(line.rsplit(" ", 1) for line in subprocess.run([str(exe)], check=True, capture_output=True,
+                                                                 text=True).stdout.splitlines())
+    for cname, cls in structs.items():
+        assert int(got[cname]) == ctypes.sizeof(cls), cname
+        for f, _ in cls._fields_:
+            assert int(got[f"{cname}.{f}"]) == getattr(cls, f).offset, f"{cname}.{f}"
+    assert int(got["herschel_edge"]) == synth.EDGE_DTYPE.itemsize
+    for f in synth.EDGE_DTYPE.names:
+        assert int(got[f"herschel_edge.{f}"]) == synth.EDGE_DTYPE.fields[f][1], f
+    assert int(got["herschel_counters"]) == 8 * len(H.COUNTERS)
+
+
+def test_oracle_struct_layouts(tmp_path):
+    """The oracle wrapper's ctypes structures match the oracle's header."""
+    import subprocess
+
+    import oracle
+    structs = {"hro_events": oracle._Events, "hro_params": oracle._Params, "hro_outputs": oracle._Outputs}
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "herschel_oracle.h"', "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append(f'  printf("{cname} %zu\\n", sizeof({cname}));')
+        for f, _ in cls._fields_:
+            lines.append(f'  printf("{cname}.{f} %zu\\n", offsetof({cname}, {f}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "oracle"), "-o", str(exe), str(src)], check=True)
+    got = dict(line.rsplit(" ", 1) for line in subprocess.run([str(exe)], check=True, capture_output=True,
+                                                                 text=True).stdout.splitlines())
+    for cname, cls in structs.items():
+        assert int(got[cname]) == ctypes.sizeof(cls), cname
+        for f, _ in cls._fields_:
+            assert int(got[f"{cname}.{f}"]) == getattr(cls, f).offset, f"{cname}.{f}"
