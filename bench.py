@@ -109,6 +109,8 @@ def algorithmic_bytes(n: int, counters: dict, params: dict, n_gaps: int) -> int:
     b += 36 * E  # each edge read (24 B) and its wait and status written
     if flags & 4:
         b += 8 * P + 16 * P * int(params["n_op_names"])  # GPU idle, op-name span and idle
+    if flags & 8:  # each admitted op's counts read, its MFU, MBU and SOL written; per op name 5 sums and a reference
+        b += 40 * counters["n_admitted_cpu"] + 48 * int(params["n_op_names"])
     return b
 
 
@@ -299,6 +301,9 @@ def main() -> int:
     ap.add_argument("--chunk", type=int, default=0, help="config4: which of the 8 chunks")
     ap.add_argument("--waits", action="store_true",
                     help="also compute the GPU idle coinciding with CPU ops, by op name")
+    ap.add_argument("--sol", action="store_true",
+                    help="also compute operator efficiency (MFU, MBU, SOL per op; per op name sums and hotness) "
+                         "from synthetic per-op counts")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -320,10 +325,14 @@ def main() -> int:
         del src, dst
 
     n = tr.n
+    cols, params = tr.columns(), dict(tr.params)
     if args.waits:
-        tr.params["flags"] = int(tr.params.get("flags", 3)) | H.OUT_WAITS
-    an = H.Analyzer(tr.params, n)
-    dcols = H.device_columns(tr.columns())
+        params["flags"] = int(params.get("flags", 3)) | H.OUT_WAITS
+    if args.sol:
+        from paper_2609_40247_amd import synth
+        cols, params = synth.add_op_costs(cols, params, 7)
+    an = H.Analyzer(params, n)
+    dcols = H.device_columns(cols)
     ev = H.events_struct(dcols)
     torch.cuda.synchronize()
 
@@ -401,9 +410,9 @@ def main() -> int:
     alg = BYTES_PER_KEY_PASS * units / launches
     launch_s = stage_ms * 1e-3 / launches
     achieved = alg / launch_s / 1e9
-    prof = profile_fields(args.workload + ("_waits" if args.waits else ""))
+    prof = profile_fields(args.workload + ("_waits" if args.waits else "") + ("_sol" if args.sol else ""))
     gaps = min(c["n_gaps_total"], an.gap_capacity)
-    call_bytes = algorithmic_bytes(n, c, tr.params, gaps)
+    call_bytes = algorithmic_bytes(n, c, params, gaps)
     whole = {"algorithmic_bytes": call_bytes, "algorithmic_GBps": round(call_bytes / (ms * 1e-3) / 1e9, 1),
              "frac": round(call_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
              "traffic_bytes": None, "kernel_us": None, "traffic_GBps": None, "traffic_frac": None}
@@ -420,7 +429,8 @@ def main() -> int:
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": {"workload": WORKLOADS[args.workload], "rows": n, "kernels": c["n_admitted_kernel"],
                    "launches": c["n_admitted_launch"], "cpu_ops": c["n_admitted_cpu"],
-                   "outputs": "all, with the idle coincidence by op name" if args.waits else "all"},
+                   "outputs": "all" + (", with the idle coincidence by op name" if args.waits else "") +
+                              (", with operator efficiency" if args.sol else "")},
         "roofline": {"kernel": ROOFLINE_KERNEL, "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": None if prof is None else prof["radix_hbm_bytes_per_launch"],
@@ -429,7 +439,7 @@ def main() -> int:
         "whole_call": whole,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(tr.columns(), tr.params, n)
+        out["cpu_baseline"] = cpu_baseline(cols, params, n)
     print(json.dumps(out), flush=True)
     return 0
 

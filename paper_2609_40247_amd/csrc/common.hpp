@@ -74,7 +74,7 @@ struct DevState {
   int64_t nDgap;       // device idle intervals
   int64_t nOgap;       // gaps of the op-name lanes (not used)
   int32_t nDev;        // endpoints of the device lane (none)
-  uint32_t sol_done;   // workgroups of the SOL fold that have finished
+  uint32_t pad2;
   int64_t first_invalid;  // smallest bad row (INT64_MAX = none)
   int64_t n_gaps;
   uint32_t sort_trivial[N_SORTS];  // bit d: digit d moves no data (every key agrees on it, or it is

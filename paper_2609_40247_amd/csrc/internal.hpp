@@ -120,7 +120,7 @@ struct Ctx {
   uint64_t* name_part = nullptr;     // [name_blocks * NN * 4] per-block name tables
   int name_blocks = 0;
   uint64_t* sol_part = nullptr;      // [sol_blocks * NOP * 4] per-block op-name tables (operator efficiency)
-  uint64_t* sol_tot = nullptr;       // [NOP * 4] their totals (zeroed with the state)
+  uint64_t* sol_tot = nullptr;       // [NOP * 4] per-name totals (zeroed with the state)
   int sol_blocks = 0;
   int32_t* op_nkern_ws = nullptr;    // [n] per-op aggregates when those outputs are NULL
   int64_t* op_first_ws = nullptr;    //     (operator efficiency reads them back)

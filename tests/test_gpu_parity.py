@@ -327,6 +327,14 @@ def test_empty_and_all_outside(H):
     check(H, cols, p, "empty")
     cols, p = _rows([(2, 0, 0, -50, -10, 1, 0), (1, 0, 0, 200_000, 200_010, 1, 0)], S=2)
     check(H, cols, p, "all outside")
+    # with every optional output: the per-name outputs of no op (SOL -1)
+    cols, p = _rows([], P=3, S=2, NOP=5, flags=15)
+    cols, p = synth.add_op_costs(cols, p, 1)
+    (code, g), _ = check(H, cols, p, "empty, all outputs")
+    assert g["opn_sol"].tolist() == [-1] * 5 and g["opn_time"].tolist() == [0] * 5
+    cols, p = _rows([(0, 0, 0, -50, -10, 0, 1), (0, 0, 0, 200_000, 200_010, 0, 2)], S=2, NOP=5, flags=15)
+    cols, p = synth.add_op_costs(cols, p, 1)
+    check(H, cols, p, "all outside, all outputs")
 
 
 def test_single_kernel_covering_window(H):
