@@ -347,8 +347,8 @@ def main() -> int:
     c = res["counters"]
     units, launches = sort_units(H.herschel_sort_stats(an.params))
 
-    # the timed region: K calls as a user makes them (repeated calls with the
-    # same arguments replay the library's captured graph of the launches)
+    # the timed region: K calls as a user makes them (each launches its
+    # kernels directly: graph replay is the library's opt-in)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -376,8 +376,7 @@ def main() -> int:
         cold = (statistics.median(cold_ms), statistics.median(warm_ms))
 
     # the roofline kernel: HIP events around the sort stage, recorded on the
-    # stream its passes run on, over another K calls (launched directly, since
-    # a call with stage events is not replayed from the graph)
+    # stream its passes run on, over another K calls
     stage_id = H.STAGES.index(ROOFLINE_STAGE)
     pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     stream = torch.cuda.current_stream()

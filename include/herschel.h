@@ -69,6 +69,9 @@ enum {
 #define HERSCHEL_OUT_WAITS 0x4u   /* GPU idle coinciding with CPU ops, by op name (Section 9.1) */
 #define HERSCHEL_OUT_SOL 0x8u     /* operator efficiency: MFU, MBU, SOL, per-name hotness (Section 6.1);
                                      needs HERSCHEL_OUT_CONTAIN */
+/* Not an output: repeated calls with equal arguments replay a captured HIP
+ * graph of their launches (herschel_trace_analyze).  Off by default. */
+#define HERSCHEL_REPLAY 0x100u
 
 /* Implementation limits (checked; EINVAL when exceeded). */
 #define HERSCHEL_MAX_PROCS 4096
@@ -217,11 +220,13 @@ int herschel_workspace_size(int64_t n, const herschel_params *p, size_t *bytes);
  * HERSCHEL_* code.  On EEVENT only counters->first_invalid is defined.
  * The work is ordered on p->hip_stream (it also runs on two library
  * streams that wait for, and are waited on by, that stream); the call
- * returns after synchronising with it.  A call whose event columns, n,
- * parameters (all but hip_stream) and output pointers equal those of one of
- * the last four argument sets captured on the device replays that call's
- * captured HIP graph; the buffers' contents may differ.  Calls overlapping
- * from several host threads are serialised while they enqueue. */
+ * returns after synchronising with it.  With HERSCHEL_REPLAY in
+ * params->flags, a call whose event columns, n, parameters (all but
+ * hip_stream) and output pointers equal those of one of the last four such
+ * argument sets captured on the device replays that call's captured HIP
+ * graph (the buffers' contents may differ); without it every call launches
+ * its kernels directly.  Calls overlapping from several host threads are
+ * serialised while they enqueue. */
 int herschel_trace_analyze(const herschel_events *ev, int64_t n, const herschel_params *p,
                            herschel_outputs *out);
 

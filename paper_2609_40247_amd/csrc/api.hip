@@ -354,7 +354,8 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   if (p->n_names < 1 || p->n_names > HERSCHEL_MAX_NAMES) return HERSCHEL_EINVAL;
   if (p->n_op_names < 1) return HERSCHEL_EINVAL;
   if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return HERSCHEL_EINVAL;
-  if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP | HERSCHEL_OUT_WAITS | HERSCHEL_OUT_SOL))
+  if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP | HERSCHEL_OUT_WAITS | HERSCHEL_OUT_SOL |
+                   HERSCHEL_REPLAY))
     return HERSCHEL_EINVAL;
   // operator efficiency reads the per-op aggregates of containment, the
   // ops' counts and the device's peaks
@@ -584,16 +585,19 @@ static int enqueue(Ctx& c) {
   return enqueue_locked(c, dsx);
 }
 
-// A call with exactly the arguments of the previous one on this device
-// (events, size, parameters except the stream, outputs) replays a HIP graph
-// of the previous call's launches: about 35 launches and the streams' event
-// edges become one graph launch on the caller's stream.  Each device keeps
-// the graphs of its last four distinct argument sets; any other call
-// captures a new graph in place of the oldest.  The graph is captured on a private
-// stream, so the caller's stream may be the null stream.  Not used while a
-// stage is being timed, nor after a capture has failed once in this process
-// (the calls then launch their kernels directly); HERSCHEL_GRAPHS=0 turns
-// it off and HERSCHEL_DEBUG=1 reports why a capture failed.
+// With HERSCHEL_REPLAY in the flags, a call with exactly the arguments of
+// an earlier one on this device (events, size, parameters except the
+// stream, outputs) replays a HIP graph of that call's launches: about 35
+// launches and the streams' event edges become one graph launch on the
+// caller's stream.  Each device keeps the graphs of its last four distinct
+// argument sets; any other call captures a new graph in place of the
+// oldest.  The graph is captured on a private stream, so the caller's stream
+// may be the null stream.  Not used while a stage is being timed, nor after
+// a capture has failed once in this process (the calls then launch their
+// kernels directly); HERSCHEL_GRAPHS=0 turns it off and HERSCHEL_DEBUG=1
+// reports why a capture failed.  Replay is opt-in: it saves about 1.5% of a
+// call on the decode-step trace, and stream capture across three streams is
+// the part of the runtime this library leans on least in tested volume.
 struct GraphKey {
   herschel_events ev;
   int64_t n;
@@ -622,7 +626,7 @@ static int graph_failed(const char* what, hipError_t e) {
 
 static int enqueue_cached(Ctx& c, const herschel_events* ev, int64_t n, const herschel_params* p,
                           const herschel_outputs* out) {
-  if (g_stage >= 0 || !graphs_enabled()) return enqueue(c);
+  if (g_stage >= 0 || !graphs_enabled() || !(c.p.flags & HERSCHEL_REPLAY)) return enqueue(c);
   std::lock_guard<std::mutex> lock(g_enqueue_mutex);
   DeviceStreams* dsx = enqueue_setup();
   int dev = 0;

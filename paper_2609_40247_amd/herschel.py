@@ -25,6 +25,7 @@ CPU_OP, LAUNCH, KERNEL = 0, 1, 2
 OK, EINVAL, EEVENT, ECAPACITY, EWORKSPACE, EDEVICE, ETOOBIG = 0, -1, -2, -3, -4, -5, -6
 STATIC_SCRATCH_BYTES = 64 << 20  # HERSCHEL_STATIC_SCRATCH_BYTES
 OUT_CONTAIN, OUT_OVERLAP, OUT_WAITS, OUT_SOL = 0x1, 0x2, 0x4, 0x8
+REPLAY = 0x100  # not an output: repeated equal calls replay a captured HIP graph
 
 _P = ctypes.c_void_p
 

@@ -267,11 +267,12 @@ def test_sparse_correlation_ids(H, seed):
 
 
 def test_graph_replays_follow_new_contents(H):
-    """Calls with the same buffers and parameters replay one captured graph;
-    between replays the buffers are refilled (eager copies, fills and
-    syncs), and every replay must match the oracle for the data it found.
-    A second analyzer with another gap threshold alternates with the first
-    (a graph of its own), and the stream is torch's null stream."""
+    """With the replay flag, calls with the same buffers and parameters
+    replay one captured graph; between replays the buffers are refilled
+    (eager copies, fills and syncs), and every replay must match the oracle
+    for the data it found.  A second analyzer with another gap threshold
+    alternates with the first (a graph of its own), and the stream is
+    torch's null stream."""
     traces = [synth.random_small(seed=9200 + s, n_rows=5000, window=6000, n_procs=2, n_streams=4, n_threads=2,
                                  corr_range=700, edges=0) for s in range(3)]
     n = 5000
@@ -279,7 +280,7 @@ def test_graph_replays_follow_new_contents(H):
     p0 = dict(traces[0].params)
     p1 = dict(p0, gap_threshold=int(p0["gap_threshold"]) * 2 + 1)
     cap = n + p0["n_procs"] * p0["n_streams"]
-    ans = [H.Analyzer(p0, n, gap_capacity=cap), H.Analyzer(p1, n, gap_capacity=cap)]
+    ans = [H.Analyzer(dict(q, flags=int(q["flags"]) | H.REPLAY), n, gap_capacity=cap) for q in (p0, p1)]
     dev = H.device_columns(traces[0].columns())
     ev = H.events_struct(dev)
     plan = [(0, 0), (0, 1), (0, 0), (1, 2), (0, 2), (1, 0), (1, 1), (0, 1)]
