@@ -21,6 +21,7 @@ _SO = os.path.join(_HERE, "libherschel_oracle.so")
 # Values the oracle leaves in rows it does not write (tests compare whole arrays).
 UNWRITTEN_I32 = -3
 UNWRITTEN_I64 = -3
+UNWRITTEN_U8 = 0xFD
 
 
 def build() -> str:
@@ -82,7 +83,8 @@ class _Outputs(ctypes.Structure):
                 ("gap_pid", _P), ("gap_stream", _P), ("gap_begin", _P), ("gap_end", _P),
                 ("gap_flags", _P), ("counters", _P), ("dev_idle", _P), ("op_span", _P), ("op_idle", _P),
                 ("op_mfu", _P), ("op_mbu", _P), ("op_sol", _P), ("opn_flops", _P), ("opn_bytes", _P),
-                ("opn_time", _P), ("opn_sol", _P), ("opn_hot", _P)]
+                ("opn_time", _P), ("opn_sol", _P), ("opn_hot", _P), ("crit_time", _P), ("crit_flags", _P),
+                ("crit_proc", _P)]
 
 
 def _ptr(a):
@@ -136,6 +138,8 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
         op_sol=np.full(n, UNWRITTEN_I64, np.int64),
         **{k: np.zeros(int(params["n_op_names"]), np.int64)
            for k in ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot")},
+        crit_time=np.full(n, UNWRITTEN_I64, np.int64), crit_flags=np.full(n, UNWRITTEN_U8, np.uint8),
+        crit_proc=np.zeros(P * 8, np.int64),
     )
     counters = np.zeros(len(COUNTER_NAMES), np.int64)
     ev = _Events(**{k: _ptr(v) for k, v in c.items()})

@@ -92,6 +92,8 @@ static int params_ok(int64_t n, const hro_params *p) {
       for (int o = 0; o < p->n_op_names; ++o)
         if (p->ref_sol_ppm[o] < 0) return 0;
   }
+  /* the critical path walks the host nesting (containment) */
+  if ((p->flags & 16u) != 0 && (p->flags & 1u) == 0) return 0;
   if (p->clock_offset)
     for (int q = 0; q < p->n_procs; ++q)
       if (!in_abs(p->clock_offset[q])) return 0;
@@ -675,6 +677,188 @@ int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p
         out->opn_sol[o] = f > b ? f : b;
       }
     }
+  }
+
+  /* 18. Critical path (Section 6.1, "Execution progress and state"; the
+   *     figure of the critical path: submission, execution-order and
+   *     synchronization dependencies).  READING: every admitted record x has
+   *     a start event S(x) at ts' and an end event E(x) at min(te', W1).
+   *     Walking back from the end event of the process's last-ending record
+   *     (largest end, then largest row), each event steps to the one event
+   *     that released it:
+   *       E(kernel)        <- its own S (it ran);
+   *       E(launch)        <- E(g) when the launch has no kernels of its own
+   *                           and g, the process's kernel ending last strictly
+   *                           inside the call (largest end, then row), exists
+   *                           (a synchronizing call returns when g completes);
+   *                           else its own S;
+   *       E(op)            <- E(last child) if that child ends no later than
+   *                           the op, else its own S;
+   *       S(kernel)        <- of E(previous kernel on its stream), if it ended
+   *                           by the kernel's start, and its launch (E(launch)
+   *                           if the launch ended by then, else S(launch),
+   *                           if it started by then): the later release,
+   *                           the launch on a tie;
+   *       S(op or launch)  <- of E(previous sibling), if it ended by the
+   *                           start, and S(parent): the later, the sibling on
+   *                           a tie; none: the path starts here.
+   *     Children and siblings are ordered by the containment order of the
+   *     thread (ts' up, ops before launches, ops by te' down, row up).  Each
+   *     step's time difference is attributed: kernel run, launch API time
+   *     (its own interval, or the part before its kernel started), the sync
+   *     tail after the releasing kernel, op self time (the part after its
+   *     last child or before a child's start, or all of a leaf op), and the
+   *     unattributed gaps (launch gap: launch end to kernel start; queue gap:
+   *     previous kernel end to kernel start; host gap: previous sibling end
+   *     to start).  A strictly earlier release makes the steps acyclic. */
+  if ((p->flags & 16u) != 0) {
+    const int T = p->n_threads;
+    int64_t *tS = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *tE = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *kprev = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *sib = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *lastc = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *gate = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *pos = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    rec4 *hr = (rec4 *)malloc(sizeof(rec4) * (size_t)(n > 0 ? n : 1));
+    rec4 *ke = (rec4 *)malloc(sizeof(rec4) * (size_t)(n > 0 ? n : 1));
+    int64_t nh = 0, nk = 0, nke = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      kprev[i] = sib[i] = lastc[i] = gate[i] = pos[i] = -1;
+      if (!adm[i]) continue;
+      tS[i] = ts[i];
+      tE[i] = te[i] < W1 ? te[i] : W1;
+      out->crit_time[i] = 0;
+      out->crit_flags[i] = 0;
+    }
+    for (int64_t q = 0; q < (int64_t)P * 8; ++q) out->crit_proc[q] = 0;
+    /* stream order of the kernels: (pid, stream, ts', row) */
+    for (int64_t i = 0; i < n; ++i)
+      if (adm[i] && ev->kind[i] == K_KERNEL) {
+        hr[nk].a = (int64_t)ev->pid[i] * S + ev->lane[i];
+        hr[nk].b = ts[i];
+        hr[nk].c = 0;
+        hr[nk].row = i;
+        ++nk;
+        ke[nke].a = ev->pid[i];
+        ke[nke].b = tE[i];
+        ke[nke].c = 0;
+        ke[nke].row = i;
+        ++nke;
+      }
+    qsort(hr, (size_t)nk, sizeof(rec4), cmp_rec4);
+    for (int64_t q = 1; q < nk; ++q)
+      if (hr[q].a == hr[q - 1].a) kprev[hr[q].row] = hr[q - 1].row;
+    /* kernels by (pid, end, row), for the synchronizing calls */
+    qsort(ke, (size_t)nke, sizeof(rec4), cmp_rec4);
+    for (int64_t i = 0; i < n; ++i) {
+      if (!adm[i] || ev->kind[i] != K_LAUNCH || out->aux[i] != 0) continue;
+      /* last kernel with (pid, end) < (pid, E(L)) */
+      int64_t lo = 0, hi = nke;
+      while (lo < hi) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (ke[mid].a < ev->pid[i] || (ke[mid].a == ev->pid[i] && ke[mid].b < tE[i]))
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      if (lo > 0 && ke[lo - 1].a == ev->pid[i] && ke[lo - 1].b > tS[i]) {
+        /* the largest row among the kernels with that end */
+        int64_t j = lo - 1;
+        gate[i] = ke[j].row;
+      }
+    }
+    /* host order of a thread: ops and launches, (thread, ts', ops before
+     * launches, ops by te' down, row) */
+    nh = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (adm[i] && ev->kind[i] != K_KERNEL) {
+        hr[nh].a = (int64_t)ev->pid[i] * T + ev->lane[i];
+        hr[nh].b = ts[i];
+        hr[nh].c = ev->kind[i] == K_LAUNCH ? I64_MAX : -te[i];
+        hr[nh].row = i;
+        ++nh;
+      }
+    qsort(hr, (size_t)nh, sizeof(rec4), cmp_rec4);
+    for (int64_t q = 0; q < nh; ++q) pos[hr[q].row] = q;
+    for (int64_t q = 0; q < nh; ++q) {
+      const int64_t x = hr[q].row, par = out->link[x];
+      /* previous sibling: the nearest earlier record of the thread with the
+       * same parent, not passing the parent itself */
+      for (int64_t j = q - 1; j >= 0 && hr[j].a == hr[q].a; --j) {
+        const int64_t y = hr[j].row;
+        if (y == par) break;
+        if (out->link[y] == par) {
+          sib[x] = y;
+          break;
+        }
+      }
+      if (par >= 0) lastc[par] = x; /* later children overwrite earlier */
+    }
+    /* the walk, per process from its last-ending record */
+    int64_t *zrow = (int64_t *)malloc(sizeof(int64_t) * (size_t)P);
+    for (int q = 0; q < P; ++q) zrow[q] = -1;
+    for (int64_t i = 0; i < n; ++i) {
+      if (!adm[i]) continue;
+      int64_t z = zrow[ev->pid[i]];
+      if (z < 0 || tE[i] > tE[z] || (tE[i] == tE[z] && i > z)) zrow[ev->pid[i]] = i;
+    }
+    for (int q = 0; q < P; ++q) {
+      if (zrow[q] < 0) continue;
+      int64_t *cp = out->crit_proc + (int64_t)q * 8;
+      int64_t x = zrow[q];
+      int side = 1; /* 0: S(x), 1: E(x) */
+      const int64_t tend = tE[x];
+      for (;;) {
+        out->crit_flags[x] |= (uint8_t)(side ? 2 : 1);
+        const int64_t t = side ? tE[x] : tS[x];
+        int64_t y = -1;
+        int ys = 0, cat = -1;
+        int64_t who = -1; /* the row an attributed step is charged to */
+        const int k = ev->kind[x];
+        if (side == 1) {
+          if (k == K_LAUNCH && gate[x] >= 0 && tE[gate[x]] < tE[x]) {
+            y = gate[x], ys = 1, cat = 3, who = x;
+          } else if (k == K_CPU && lastc[x] >= 0 && tE[lastc[x]] <= tE[x]) {
+            y = lastc[x], ys = 1, cat = 4, who = x;
+          } else {
+            y = x, ys = 0, cat = k == K_KERNEL ? 1 : k == K_LAUNCH ? 2 : 4, who = x;
+          }
+        } else if (k == K_KERNEL) {
+          int64_t rel = I64_MIN;
+          const int64_t kp = kprev[x], l = out->link[x];
+          if (kp >= 0 && tE[kp] <= t) y = kp, ys = 1, rel = tE[kp], cat = 6, who = -1;
+          if (l >= 0) {
+            if (tE[l] <= t && tE[l] >= rel) y = l, ys = 1, rel = tE[l], cat = 5, who = -1;
+            else if (tE[l] > t && tS[l] <= t && tS[l] >= rel) y = l, ys = 0, rel = tS[l], cat = 2, who = l;
+          }
+        } else {
+          int64_t rel = I64_MIN;
+          const int64_t par = out->link[x], sb = sib[x];
+          if (par >= 0) y = par, ys = 0, rel = tS[par], cat = 4, who = par;
+          if (sb >= 0 && tE[sb] <= t && tE[sb] >= rel) y = sb, ys = 1, rel = tE[sb], cat = 7, who = -1;
+        }
+        if (y < 0) {
+          cp[0] = tend - t;
+          break;
+        }
+        const int64_t ty = ys ? tE[y] : tS[y];
+        cp[cat] += t - ty;
+        if (who >= 0) out->crit_time[who] += t - ty;
+        x = y;
+        side = ys;
+      }
+    }
+    free(zrow);
+    free(tS);
+    free(tE);
+    free(kprev);
+    free(sib);
+    free(lastc);
+    free(gate);
+    free(pos);
+    free(hr);
+    free(ke);
   }
 
   for (int64_t ps = 0; ps < (int64_t)P * S; ++ps) free(runs[ps]);

@@ -67,6 +67,9 @@ typedef struct {
   int64_t *op_span, *op_idle; /* [n_procs * n_op_names] (flags bit 2) */
   int64_t *op_mfu, *op_mbu, *op_sol; /* [n] ppm at CPU_OP rows (flags bit 3) */
   int64_t *opn_flops, *opn_bytes, *opn_time, *opn_sol, *opn_hot; /* [n_op_names] (flags bit 3) */
+  int64_t *crit_time;    /* [n] critical-path time attributed to each admitted row (flags bit 4) */
+  uint8_t *crit_flags;   /* [n] bit0: the row's start event on the path, bit1: its end event (bit 4) */
+  int64_t *crit_proc;    /* [n_procs * 8] length, kernel, api, sync, op, launch gap, queue gap, host gap */
 } hro_outputs;
 
 /* Same return codes as the product: 0 ok, -1 bad parameter, -2 invalid row,

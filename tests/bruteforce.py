@@ -291,10 +291,97 @@ def analyze(cols: dict, p: dict):
         else:
             ew.append(_wrap(min(rows[k]["t0"] for k in cons) - max(rows[k]["t1"] for k in prod)))
 
+    crit = None
+    if p["flags"] & 16 and contain:
+        # critical path: every release candidate of every event is an explicit
+        # edge (release time, priority, target event, category, charged row);
+        # the released-by edge is the maximum by (release, priority); the
+        # structures come from all-pairs scans over this brute force's own
+        # join and containment
+        adm = [i for i, r in enumerate(rows) if r["in"]]
+        tS = {i: rows[i]["t0"] for i in adm}
+        tE = {i: min(rows[i]["t1"], W1) for i in adm}
+
+        def hkey(i):  # containment order within a thread
+            r = rows[i]
+            return (r["t0"], 0 if r["kind"] == 0 else 1, -r["t1"] if r["kind"] == 0 else 0, i)
+
+        host = [i for i in adm if rows[i]["kind"] != 2]
+        cands = {}
+        for i in adm:
+            r = rows[i]
+            ce, cs = [], []
+            if r["kind"] == 2:
+                ce.append((tS[i], 0, (i, 0), 1, i))
+                prev = [j for j in ker if rows[j]["pid"] == r["pid"] and rows[j]["lane"] == r["lane"]
+                        and (rows[j]["t0"], j) < (r["t0"], i)]
+                if prev:
+                    j = max(prev, key=lambda j: (rows[j]["t0"], j))
+                    if tE[j] <= tS[i]:
+                        cs.append((tE[j], 0, (j, 1), 6, -1))
+                L = link[i]
+                if L >= 0:
+                    if tE[L] <= tS[i]:
+                        cs.append((tE[L], 1, (L, 1), 5, -1))
+                    elif tS[L] <= tS[i]:
+                        cs.append((tS[L], 1, (L, 0), 2, L))
+            else:
+                same = [j for j in host if (rows[j]["pid"], rows[j]["lane"]) == (r["pid"], r["lane"])
+                        and link[j] == link[i]]
+                before = [j for j in same if hkey(j) < hkey(i)]
+                if r["kind"] == 1:
+                    g = [k for k in ker if rows[k]["pid"] == r["pid"] and tS[i] < tE[k] < tE[i]]
+                    if aux[i] == 0 and g:
+                        k = max(g, key=lambda k: (tE[k], k))
+                        ce.append((tE[k], 1, (k, 1), 3, i))
+                    ce.append((tS[i], 0, (i, 0), 2, i))
+                else:
+                    kids = [j for j in host if link[j] == i]
+                    if kids:
+                        c = max(kids, key=hkey)
+                        if tE[c] <= tE[i]:
+                            ce.append((tE[c], 1, (c, 1), 4, i))
+                    ce.append((tS[i], 0, (i, 0), 4, i))
+                if before:
+                    j = max(before, key=hkey)
+                    if tE[j] <= tS[i]:
+                        cs.append((tE[j], 1, (j, 1), 7, -1))
+                if link[i] >= 0:
+                    cs.append((tS[link[i]], 0, (link[i], 0), 4, link[i]))
+            # an end event prefers its priority-1 edge when it has one
+            cands[(i, 1)] = max(ce, key=lambda c: (c[1], c[0])) if ce else None
+            cands[(i, 0)] = max(cs, key=lambda c: (c[0], c[1])) if cs else None
+        ctime = {i: 0 for i in adm}
+        cflag = {i: 0 for i in adm}
+        cproc = np.zeros((P, 8), np.int64)
+        for q in range(P):
+            mine = [i for i in adm if rows[i]["pid"] == q]
+            if not mine:
+                continue
+            z = max(mine, key=lambda i: (tE[i], i))
+            ev_, seen = (z, 1), set()
+            while True:
+                assert ev_ not in seen, "a cycle"
+                seen.add(ev_)
+                cflag[ev_[0]] |= 2 if ev_[1] else 1
+                t = tE[ev_[0]] if ev_[1] else tS[ev_[0]]
+                c = cands[ev_]
+                if c is None:
+                    cproc[q, 0] = tE[z] - t
+                    break
+                tgt = c[2]
+                d = t - (tE[tgt[0]] if tgt[1] else tS[tgt[0]])
+                assert d >= 0
+                cproc[q, c[3]] += d
+                if c[4] >= 0:
+                    ctime[c[4]] += d
+                ev_ = tgt
+        crit = dict(crit_time=ctime, crit_flags=cflag, crit_proc=cproc.reshape(-1))
+
     out = dict(counters=cnt, link=np.array(link, np.int32), aux=np.array(aux, np.int32),
                busy=busy, idle=idle, gaps=gaps, lat_hist=np.array(hist, np.int64),
                name_count=np.array(ncount, np.int64), name_sum=np.array(nsum, np.int64),
                name_min=np.array(nmin, np.int64), name_max=np.array(nmax, np.int64),
-               op=op_arrays, overlap=ov, waits=waits, sol=sol, edge_wait=np.array(ew, np.int64),
+               op=op_arrays, overlap=ov, waits=waits, sol=sol, crit=crit, edge_wait=np.array(ew, np.int64),
                edge_status=np.array(es, np.int32))
     return 0, out

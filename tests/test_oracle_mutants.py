@@ -96,6 +96,20 @@ MUTANTS = [
      "int64_t f = 0;"),
     ("hotness overwritten", "out->opn_hot[o] = wrap_add(out->opn_hot[o], (int64_t)(uint64_t)(x / (uint64_t)ref));",
      "out->opn_hot[o] = (int64_t)(uint64_t)(x / (uint64_t)ref);"),
+    ("kernel tie to the stream", "if (tE[l] <= t && tE[l] >= rel) y = l, ys = 1, rel = tE[l], cat = 5, who = -1;",
+     "if (tE[l] <= t && tE[l] > rel) y = l, ys = 1, rel = tE[l], cat = 5, who = -1;"),
+    ("sync gate ignored", "if (k == K_LAUNCH && gate[x] >= 0 && tE[gate[x]] < tE[x]) {",
+     "if (0 && k == K_LAUNCH && gate[x] >= 0 && tE[gate[x]] < tE[x]) {"),
+    ("first child as last", "if (par >= 0) lastc[par] = x; /* later children overwrite earlier */",
+     "if (par >= 0 && lastc[par] < 0) lastc[par] = x;"),
+    ("path ends unclipped", "tE[i] = te[i] < W1 ? te[i] : W1;", "tE[i] = te[i];"),
+    ("last record by smallest row", "if (z < 0 || tE[i] > tE[z] || (tE[i] == tE[z] && i > z)) zrow[ev->pid[i]] = i;",
+     "if (z < 0 || tE[i] > tE[z] || (tE[i] == tE[z] && i < z)) zrow[ev->pid[i]] = i;"),
+    ("launch gap as queue gap", "y = l, ys = 1, rel = tE[l], cat = 5, who = -1;", "y = l, ys = 1, rel = tE[l], cat = 6, who = -1;"),
+    ("parent released at its end", "if (par >= 0) y = par, ys = 0, rel = tS[par], cat = 4, who = par;",
+     "if (par >= 0) y = par, ys = 0, rel = tE[par], cat = 4, who = par;"),
+    ("api charged to the kernel", "y = l, ys = 0, rel = tS[l], cat = 2, who = l;", "y = l, ys = 0, rel = tS[l], cat = 2, who = x;"),
+    ("op tail charged to the child", "y = lastc[x], ys = 1, cat = 4, who = x;", "y = lastc[x], ys = 1, cat = 4, who = lastc[x];"),
     ("edge status bits swapped", "(found[0] ? 0 : 1) | (found[1] ? 0 : 2)", "(found[0] ? 0 : 2) | (found[1] ? 0 : 1)"),
 ]
 
@@ -127,6 +141,18 @@ def _battery(lib) -> None:
     for k in ("dev_idle", "op_span", "op_idle"):
         assert o[k].tolist() == exp[k], k
     pins.check_pa_case(lib)
+    pins.check_crit_golden(lib)
+    for case in [c for c in pins.BF_CASES if c.get("flags", 3) & 16][::3]:
+        tr = synth.random_small(**case)
+        code, o = oracle.analyze(tr.columns(), tr.params, lib=lib)
+        bcode, b = bruteforce.analyze(tr.columns(), tr.params)
+        assert code == bcode
+        if code == 0:
+            pins._bf_compare(tr.columns(), tr.params, o, b, tr.label)
+    tr = synth.config1(n_steps=12)
+    tr.params["flags"] = 17
+    code, o = oracle.analyze(tr.columns(), tr.params, lib=lib)
+    pins.crit_invariants(tr, o)
     for seed in pins.SOL_BF_SEEDS[::3] + [4, 5, 29]:  # 4, 5, 29: two ops of one name below its reference
         cols, p = pins.sol_case(seed)
         code, o = oracle.analyze(cols, p, lib=lib)

@@ -106,6 +106,12 @@ def _bf_compare(cols, p, o, b, ctx):
                 assert int(o[k][r]) == v, f"{ctx}: {k} row {r}"
         for k in ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot"):
             assert o[k].tolist() == b["sol"][k].tolist(), f"{ctx}: {k}"
+    if p["flags"] & 16:
+        for r, v in b["crit"]["crit_time"].items():
+            assert int(o["crit_time"][r]) == v, f"{ctx}: crit_time row {r}"
+        for r, v in b["crit"]["crit_flags"].items():
+            assert int(o["crit_flags"][r]) == v, f"{ctx}: crit_flags row {r}"
+        assert o["crit_proc"].tolist() == b["crit"]["crit_proc"].tolist(), f"{ctx}: crit_proc"
 
 
 BF_CASES = [dict(seed=s) for s in range(120)] + [
@@ -119,7 +125,14 @@ BF_CASES = [dict(seed=s) for s in range(120)] + [
     # GPU idle coinciding with ops, with every other output and alone
     dict(seed=5000 + s, flags=7 if s % 2 else 4) for s in range(40)] + [
     dict(seed=5100 + s, n_rows=150, window=700, n_procs=2, n_streams=3, n_threads=3, n_op_names=3, flags=7)
-    for s in range(20)]
+    for s in range(20)] + [
+    # the critical path, alone with containment and with every other output
+    dict(seed=7000 + s, flags=17 if s % 2 else 23) for s in range(40)] + [
+    dict(seed=7100 + s, n_rows=150, window=900, n_procs=3, n_streams=3, n_threads=2, corr_range=40, flags=17)
+    for s in range(20)] + [
+    # few distinct times: ties between releases everywhere
+    dict(seed=7200 + s, n_rows=50, window=30, n_procs=1, n_streams=2, n_threads=1, corr_range=8, offsets=False,
+         flags=17) for s in range(20)]
 
 
 SOL_BF_SEEDS = list(range(40))
@@ -669,4 +682,96 @@ def test_sol_errors(change):
         assert code == -2 and o["counters"]["first_invalid"] == 0
         return
     assert oracle.analyze(cols, p)[0] == -1
+
+
+# --------------------------------------------------------------- critical path
+
+def crit_golden_cases():
+    g = load_golden_raw("crit_path_cases.json")
+    out = []
+    for c in g["cases"]:
+        a = np.array(c["rows"], np.int64)
+        cols = dict(kind=a[:, 0].astype(np.uint8), pid=a[:, 1].astype(np.int32), lane=a[:, 2].astype(np.int32),
+                    ts=a[:, 3], te=a[:, 4], corr=a[:, 5], name=a[:, 6].astype(np.int32))
+        out.append((c["name"], cols, synth.empty_params(**c["params"]), c["expect"]))
+    return out
+
+
+def check_crit_golden(lib=None):
+    for name, cols, p, exp in crit_golden_cases():
+        code, o = oracle.analyze(cols, p, lib=lib)
+        assert code == 0, name
+        for k in ("crit_time", "crit_flags", "crit_proc"):
+            assert o[k].tolist() == exp[k], (name, k)
+
+
+def test_crit_path_worked_cases():
+    """Two hand-worked cases: the scenario of the paper's critical-path figure
+    (a synchronizing call makes the kernel it waited for part of the path;
+    the other stream's kernel is off it) and nested ops with a queued kernel,
+    launch and queue gaps and an op's tail after its last child."""
+    check_crit_golden()
+
+
+def crit_invariants(tr, o):
+    cols, p = tr.columns(), tr.params
+    cp = o["crit_proc"].reshape(-1, 8)
+    assert (cp >= 0).all()
+    assert (cp[:, 0] == cp[:, 1:].sum(axis=1)).all(), "length = sum of the parts"
+    adm = o["link"] != -2
+    ct, cf = o["crit_time"], o["crit_flags"]
+    assert (ct[adm] >= 0).all() and (cf[adm] <= 3).all()
+    assert (ct[~adm] == oracle.UNWRITTEN_I64).all() and (cf[~adm] == oracle.UNWRITTEN_U8).all()
+    pid = cols["pid"]
+    for q in range(p["n_procs"]):
+        m = adm & (pid == q)
+        assert ct[m].sum() == cp[q, 1:5].sum(), "attributed time = kernel + api + sync + op"
+        assert cp[q, 0] <= int(p["window_end"]) - int(p["window_begin"])
+        # time is charged only to records on the path
+        assert ((ct[m] == 0) | (cf[m] != 0)).all()
+        # kernels are charged their whole run exactly when their end event is on the path
+        ker = m & (cols["kind"] == 2)
+        run = np.minimum(cols["te"] - _off(p, pid), int(p["window_end"])) - (cols["ts"] - _off(p, pid))
+        assert (ct[ker & ((cf & 2) != 0)] == run[ker & ((cf & 2) != 0)]).all()
+        assert (ct[ker & ((cf & 2) == 0)] == 0).all()
+
+
+def _off(p, pid):
+    off = p.get("clock_offset")
+    return np.zeros(len(pid), np.int64) if off is None else np.asarray(off, np.int64)[pid]
+
+
+@pytest.mark.parametrize("which", ["config0", "config1_short", "config3_small"])
+def test_crit_path_invariants(which):
+    tr = {"config0": lambda: synth.config0(), "config1_short": lambda: synth.config1(n_steps=20),
+          "config3_small": lambda: synth.config3(n_procs=3, n_steps=10, n_edges=50)}[which]()
+    tr.params["flags"] = 17
+    code, o = oracle.analyze(tr.columns(), tr.params)
+    assert code == 0
+    crit_invariants(tr, o)
+    # a decode step is GPU-bound: most of the path is kernel time
+    cp = o["crit_proc"].reshape(-1, 8)
+    assert cp[:, 0].min() > 0
+
+
+def test_crit_path_time_shift():
+    """A global shift of every time and of the window leaves the path and its
+    parts unchanged."""
+    tr = synth.config1(n_steps=10)
+    tr.params["flags"] = 17
+    code, a = oracle.analyze(tr.columns(), tr.params)
+    cols = dict(tr.columns())
+    d = 123_456_789
+    cols["ts"] = cols["ts"] + d
+    cols["te"] = cols["te"] + d
+    q = dict(tr.params, window_begin=int(tr.params["window_begin"]) + d, window_end=int(tr.params["window_end"]) + d)
+    code2, b = oracle.analyze(cols, q)
+    assert code == code2 == 0
+    for k in ("crit_time", "crit_flags", "crit_proc"):
+        assert a[k].tolist() == b[k].tolist(), k
+
+
+def test_crit_path_needs_containment():
+    name, cols, p, _ = crit_golden_cases()[0]
+    assert oracle.analyze(cols, dict(p, flags=16))[0] == -1
 
