@@ -111,6 +111,8 @@ def algorithmic_bytes(n: int, counters: dict, params: dict, n_gaps: int) -> int:
         b += 8 * P + 16 * P * int(params["n_op_names"])  # GPU idle, op-name span and idle
     if flags & 8:  # each admitted op's counts read, its MFU, MBU and SOL written; per op name 5 sums and a reference
         b += 40 * counters["n_admitted_cpu"] + 48 * int(params["n_op_names"])
+    if flags & 16:  # each admitted row's time charged and path flags written; per process 8 parts
+        b += 9 * sum(counters[k] for k in ("n_admitted_cpu", "n_admitted_launch", "n_admitted_kernel")) + 64 * P
     return b
 
 
@@ -301,6 +303,7 @@ def main() -> int:
     ap.add_argument("--chunk", type=int, default=0, help="config4: which of the 8 chunks")
     ap.add_argument("--waits", action="store_true",
                     help="also compute the GPU idle coinciding with CPU ops, by op name")
+    ap.add_argument("--crit", action="store_true", help="also compute the critical path")
     ap.add_argument("--sol", action="store_true",
                     help="also compute operator efficiency (MFU, MBU, SOL per op; per op name sums and hotness) "
                          "from synthetic per-op counts")
@@ -331,6 +334,8 @@ def main() -> int:
     if args.sol:
         from paper_2609_40247_amd import synth
         cols, params = synth.add_op_costs(cols, params, 7)
+    if args.crit:
+        params["flags"] = int(params.get("flags", 3)) | H.OUT_CRIT | H.OUT_CONTAIN
     an = H.Analyzer(params, n)
     dcols = H.device_columns(cols)
     ev = H.events_struct(dcols)
@@ -409,7 +414,8 @@ def main() -> int:
     alg = BYTES_PER_KEY_PASS * units / launches
     launch_s = stage_ms * 1e-3 / launches
     achieved = alg / launch_s / 1e9
-    prof = profile_fields(args.workload + ("_waits" if args.waits else "") + ("_sol" if args.sol else ""))
+    prof = profile_fields(args.workload + ("_waits" if args.waits else "") + ("_sol" if args.sol else "") +
+                          ("_crit" if args.crit else ""))
     gaps = min(c["n_gaps_total"], an.gap_capacity)
     call_bytes = algorithmic_bytes(n, c, params, gaps)
     whole = {"algorithmic_bytes": call_bytes, "algorithmic_GBps": round(call_bytes / (ms * 1e-3) / 1e9, 1),
@@ -429,7 +435,8 @@ def main() -> int:
         "config": {"workload": WORKLOADS[args.workload], "rows": n, "kernels": c["n_admitted_kernel"],
                    "launches": c["n_admitted_launch"], "cpu_ops": c["n_admitted_cpu"],
                    "outputs": "all" + (", with the idle coincidence by op name" if args.waits else "") +
-                              (", with operator efficiency" if args.sol else "")},
+                              (", with operator efficiency" if args.sol else "") +
+                              (", with the critical path" if args.crit else "")},
         "roofline": {"kernel": ROOFLINE_KERNEL, "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": None if prof is None else prof["radix_hbm_bytes_per_launch"],

@@ -69,6 +69,8 @@ enum {
 #define HERSCHEL_OUT_WAITS 0x4u   /* GPU idle coinciding with CPU ops, by op name (Section 9.1) */
 #define HERSCHEL_OUT_SOL 0x8u     /* operator efficiency: MFU, MBU, SOL, per-name hotness (Section 6.1);
                                      needs HERSCHEL_OUT_CONTAIN */
+#define HERSCHEL_OUT_CRIT 0x10u   /* critical path (Section 6.1, execution progress and state);
+                                     needs HERSCHEL_OUT_CONTAIN */
 /* Not an output: repeated calls with equal arguments replay a captured HIP
  * graph of their launches (herschel_trace_analyze).  Off by default. */
 #define HERSCHEL_REPLAY 0x100u
@@ -210,6 +212,34 @@ typedef struct {
   int64_t *opn_flops, *opn_bytes;    /* [n_op_names] */
   int64_t *opn_time, *opn_sol;       /* [n_op_names] */
   int64_t *opn_hot;                  /* [n_op_names] ns */
+  /* HERSCHEL_OUT_CRIT (Section 6.1, "Execution progress and state": the
+   * submission, execution-order and synchronization dependencies that
+   * identify the critical path).  Each admitted record x has a start event
+   * at ts' and an end event at min(te', W1); each event is released by one
+   * other event:
+   *   a kernel's end by its start; a launch's end by the end of g, when the
+   *   launch has no kernel of its own and g, the process's kernel ending last
+   *   strictly inside the call (then the largest row), exists (a
+   *   synchronizing call), else by its start; an op's end by its last
+   *   child's end if that child ends no later, else by its start;
+   *   a kernel's start by the later of the previous kernel of its stream's
+   *   end (if by then) and its launch (its end if by then, else its start if
+   *   by then), the launch on a tie; an op's or launch's start by the later
+   *   of its previous sibling's end (if by then) and its parent's start, the
+   *   sibling on a tie.
+   * Children and siblings are ordered as the thread's containment (ts' up,
+   * ops before launches, ops by te' down, row up).  A process's path runs
+   * back from the end event of its last-ending record (largest end, then
+   * row) to an event nothing releases; each step's time is charged to one
+   * part and, for the first four parts, to one record. */
+  int64_t *crit_time;                /* [n] time charged to each admitted row (0 off the path) */
+  uint8_t *crit_flags;               /* [n] admitted rows: bit0 start on the path, bit1 end on the path */
+  int64_t *crit_proc;                /* [n_procs * 8] per process: length, then kernel run, API time
+                                        (a launch's interval, or the part before its kernel started),
+                                        sync tail (after the releasing kernel), op self time, launch gap
+                                        (launch end to kernel start), queue gap (previous kernel end to
+                                        kernel start), host gap (sibling end to start); all zero for a
+                                        process without admitted rows */
 } herschel_outputs;
 
 /* Bytes of device workspace that herschel_trace_analyze needs for n rows
@@ -283,7 +313,8 @@ enum {
   HERSCHEL_STAGE_FINAL = 11,   /* counters and histogram totals */
   HERSCHEL_STAGE_WAITS = 12,   /* device-lane and op-name unions, idle coincidence (OUT_WAITS) */
   HERSCHEL_STAGE_SOL = 13,     /* operator efficiency and per-name hotness (OUT_SOL), after OPAGG */
-  HERSCHEL_N_STAGES = 14
+  HERSCHEL_STAGE_CRIT = 14,    /* critical path (OUT_CRIT), after SOL */
+  HERSCHEL_N_STAGES = 15
 };
 
 /* Record start_event / stop_event (hipEvent_t, created by the caller) on

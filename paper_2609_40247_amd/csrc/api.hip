@@ -42,6 +42,7 @@ struct Bump {
 static bool sort_used(const Ctx& c, const SortBufs* s) {
   if (s == &c.sK) return true;
   if (s == &c.sC) return c.contain;
+  if (s == &c.sE) return c.crit;
   return c.waits;
 }
 
@@ -80,6 +81,14 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.dbusy_ws = b.take<int64_t>(c.P);
   }
   if (c.sol) c.sol_tot = b.take<uint64_t>((int64_t)c.NOP * 4);
+  if (c.crit) {
+    sort_plan(c.sE, SORT_E, n, c.pb + c.wb1, true);
+    c.crit_mark = b.take<uint8_t>(2 * n);
+    c.crit_lastc1 = b.take<uint32_t>(n);
+    c.crit_hasnext = b.take<uint8_t>(n);
+    c.crit_zmax = b.take<uint64_t>(c.P);
+    c.crit_zrow1 = b.take<uint32_t>(c.P);
+  }
   if (c.contain) {
     c.vb_tiles = std::max<int64_t>(cdiv(n, 4096), 1);
     c.vb_status = b.take<uint64_t>(c.vb_tiles);
@@ -94,7 +103,7 @@ size_t layout_workspace(Ctx& c, char* base) {
   c.zero_bytes = align_up(b.off - z0);
   // the first digit's look-back words are cleared by the histogram kernel
   // (for the tiles of the call), each later digit's by the pass before it
-  for (SortBufs* s : {&c.sK, &c.sC, &c.sD, &c.sO}) {
+  for (SortBufs* s : {&c.sK, &c.sC, &c.sD, &c.sO, &c.sE}) {
     if (!sort_used(c, s)) continue;
     s->status0 = b.take<uint32_t>(s->tiles_max * RS_LB_WORDS);
     s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * RS_LB_WORDS);
@@ -123,8 +132,9 @@ size_t layout_workspace(Ctx& c, char* base) {
   c.jt_fix_cap = n;
   c.jt_fix = b.take<uint32_t>(3 * c.jt_fix_cap);
   // sort buffers
-  for (SortBufs* s : {&c.sK, &c.sC, &c.sD, &c.sO}) {
+  for (SortBufs* s : {&c.sK, &c.sC, &c.sD, &c.sO, &c.sE}) {
     if ((s == &c.sD || s == &c.sO) && !c.waits) continue;
+    if (s == &c.sE && !c.crit) continue;
     if (s == &c.sC && !c.contain) {
       // the containment list is still compacted by prep (ops and launches)
       s->k[0] = b.take<uint64_t>(n);
@@ -181,6 +191,12 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.op_first_ws = b.take<int64_t>(n);
     c.op_last_ws = b.take<int64_t>(n);
   }
+  if (c.crit) {
+    c.crit_pred = b.take<int32_t>(2 * n);
+    c.crit_code = b.take<uint8_t>(2 * n);
+    c.crit_ptr[0] = b.take<int32_t>(2 * n);
+    c.crit_ptr[1] = b.take<int32_t>(2 * n);
+  }
   return b.off;
 }
 
@@ -207,6 +223,8 @@ struct InitArgs {
   const int64_t* off;
   const uint8_t* cls;
   int64_t n_opn;      // P * n_op_names with the idle-coincidence outputs, else 0
+  int64_t n_crit;     // P * 8 with the critical path, else 0
+  int64_t* crit_proc;
   int64_t* op_span;
   int64_t* op_idle;
 };
@@ -244,6 +262,7 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
   // the name outputs start as the identities: the per-block tables (or,
   // with many names, the kernels themselves) are combined into them with
   // atomics
+  for (int64_t i = tid; i < a.n_crit; i += nth) a.crit_proc[i] = 0;  // accumulated with atomics
   for (int64_t i = tid; i < a.n_opn; i += nth) {  // accumulated with atomics
     if (a.op_span) a.op_span[i] = 0;
     if (a.op_idle) a.op_idle[i] = 0;
@@ -280,6 +299,8 @@ void launch_init(Ctx& c) {
   a.off = c.p.clock_offset;
   a.cls = c.p.stream_class;
   a.n_opn = c.waits ? (int64_t)c.P * c.NOP : 0;
+  a.n_crit = c.crit && c.o.crit_proc ? (int64_t)c.P * 8 : 0;
+  a.crit_proc = c.o.crit_proc;
   a.op_span = c.o.op_span ? c.o.op_span : c.op_span_ws;
   a.op_idle = c.o.op_idle;
   const int64_t work = std::max<int64_t>({a.zero_n, (int64_t)a.nps * (c.overlap ? c.S : 1), (int64_t)c.NN, a.n_opn, 1});
@@ -355,8 +376,10 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   if (p->n_op_names < 1) return HERSCHEL_EINVAL;
   if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return HERSCHEL_EINVAL;
   if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP | HERSCHEL_OUT_WAITS | HERSCHEL_OUT_SOL |
-                   HERSCHEL_REPLAY))
+                   HERSCHEL_OUT_CRIT | HERSCHEL_REPLAY))
     return HERSCHEL_EINVAL;
+  // the critical path walks the host nesting
+  if ((p->flags & HERSCHEL_OUT_CRIT) && !(p->flags & HERSCHEL_OUT_CONTAIN)) return HERSCHEL_EINVAL;
   // operator efficiency reads the per-op aggregates of containment, the
   // ops' counts and the device's peaks
   if (p->flags & HERSCHEL_OUT_SOL) {
@@ -389,6 +412,7 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   c.overlap = overlap;
   c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
   c.sol = (p->flags & HERSCHEL_OUT_SOL) != 0;
+  c.crit = (p->flags & HERSCHEL_OUT_CRIT) != 0;
   c.nob = bits_host((uint64_t)(c.NOP - 1));
   c.pb = bits_host((uint64_t)(c.P - 1));
   c.sb = bits_host((uint64_t)(c.S - 1));
@@ -466,6 +490,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_end(c, HERSCHEL_STAGE_INIT);
   stage_begin(c, HERSCHEL_STAGE_PREP);
   launch_prep(c);
+  if (c.crit) launch_crit_elist(c);  // the kernel-end list joins the sorts
   stage_end(c, HERSCHEL_STAGE_PREP);
 
   // The timeline and containment sorts share their digit passes, pass p of
@@ -489,6 +514,10 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     cc[ks++] = &c.ds->nK;
     ss[ks] = &c.sO;
     cc[ks++] = &c.ds->nO;
+  }
+  if (c.crit) {  // kernel ends, for the synchronizing calls of the critical path
+    ss[ks] = &c.sE;
+    cc[ks++] = &c.ds->nK;
   }
   int p_shared = 0;
   for (int i = 0; i < ks; ++i) p_shared = std::max(p_shared, ss[i]->nd - ss[i]->first);
@@ -561,6 +590,9 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_SOL);
   if (c.sol) launch_sol(c);
   stage_end(c, HERSCHEL_STAGE_SOL);
+  stage_begin(c, HERSCHEL_STAGE_CRIT);
+  if (c.crit) launch_crit(c);
+  stage_end(c, HERSCHEL_STAGE_CRIT);
   wait(c.st, 1);
   wait(c.st, 4);
   stage_begin(c, HERSCHEL_STAGE_FINAL);
@@ -799,6 +831,7 @@ int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) 
   c.contain = (p->flags & HERSCHEL_OUT_CONTAIN) != 0;
   c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
   c.sol = (p->flags & HERSCHEL_OUT_SOL) != 0;
+  c.crit = (p->flags & HERSCHEL_OUT_CRIT) != 0;
   c.NOP = p->n_op_names;
   c.nob = bits_host((uint64_t)(c.NOP > 0 ? c.NOP - 1 : 0));
   c.overlap = (p->flags & HERSCHEL_OUT_OVERLAP) != 0;

@@ -40,10 +40,13 @@ enum : int {
   N_TICKETS = 3
 };
 
-// 0 timeline (pid, stream, ts'), 1 containment, and with the idle-coincidence
-// outputs 2 device lane (pid, ts') and 3 op names (pid, op name, ts')
-constexpr int N_SORTS = 4;
-enum : int { SORT_K = 0, SORT_C = 1, SORT_D = 2, SORT_O = 3 };
+// 0 timeline (pid, stream, ts'), 1 containment, with the idle-coincidence
+// outputs 2 device lane (pid, ts') and 3 op names (pid, op name, ts'), with
+// the critical path 4 kernel ends (pid, min(te', W1))
+constexpr int N_SORTS = 5;
+enum : int { SORT_K = 0, SORT_C = 1, SORT_D = 2, SORT_O = 3, SORT_E = 4 };
+// Rounds of the critical path's pointer doubling (its events number 2n < 2^31).
+constexpr int CRIT_MAX_ROUNDS = 32;
 // join counters (JC_MLAUNCH: launches with at least one kernel; the
 // unmatched launches are the admitted ones without)
 enum { JC_MATCHED, JC_UNM_K, JC_DUP, JC_NEG, JC_UNATTR, JC_MLAUNCH, JC_N };
@@ -75,6 +78,7 @@ struct DevState {
   int64_t nOgap;       // gaps of the op-name lanes (not used)
   int32_t nDev;        // endpoints of the device lane (none)
   uint32_t pad2;
+  uint32_t crit_new[CRIT_MAX_ROUNDS];  // critical path: events newly marked in each doubling round
   int64_t first_invalid;  // smallest bad row (INT64_MAX = none)
   int64_t n_gaps;
   uint32_t sort_trivial[N_SORTS];  // bit d: digit d moves no data (every key agrees on it, or it is

@@ -52,7 +52,7 @@ struct Ctx {
   herschel_outputs o{};
   int64_t W0 = 0, W1 = 0, W = 0, thr = 0;
   int P = 0, S = 0, T = 0, NN = 0, NOP = 0;
-  bool contain = false, overlap = false, waits = false, sol = false;
+  bool contain = false, overlap = false, waits = false, sol = false, crit = false;
   int nob = 0;                         // bits of an op name (idle coincidence)
   int pb = 0, sb = 0, tb = 0, wb = 0;  // key field widths: pid, stream, thread, ts'-W0
   int wb1 = 0;                         // bits of W (values 0..W)
@@ -82,6 +82,7 @@ struct Ctx {
   int64_t* corr_min = nullptr;       // [P]
   SortBufs sK, sC;                   // timeline, containment
   SortBufs sD, sO;                   // device lane, op names (idle coincidence)
+  SortBufs sE;                       // kernel ends (critical path)
   uint32_t* k_rows = nullptr;        // [n] admitted kernels' rows in row order (per-name tables)
   uint32_t* hist_part = nullptr;     // [N_SORTS][HIST_MAX_BLOCKS][8 * 256] per-workgroup digit counts
   uint64_t* jkey = nullptr;          // [n] join list (prep): admitted launches and kernels in row order
@@ -125,6 +126,14 @@ struct Ctx {
   int32_t* op_nkern_ws = nullptr;    // [n] per-op aggregates when those outputs are NULL
   int64_t* op_first_ws = nullptr;    //     (operator efficiency reads them back)
   int64_t* op_last_ws = nullptr;
+  int32_t* crit_pred = nullptr;      // [2n] critical path: each event's release
+  uint8_t* crit_code = nullptr;      // [2n] its part and charged record
+  uint8_t* crit_mark = nullptr;      // [2n] on the path (zeroed)
+  int32_t* crit_ptr[2] = {nullptr, nullptr};  // [2n] doubling pointers
+  uint32_t* crit_lastc1 = nullptr;   // [n] by containment position (zeroed)
+  uint8_t* crit_hasnext = nullptr;   // [n] by containment position (zeroed)
+  uint64_t* crit_zmax = nullptr;     // [P] (zeroed)
+  uint32_t* crit_zrow1 = nullptr;    // [P] (zeroed)
   char* zero_begin = nullptr;        // region cleared at the start of a call
   size_t zero_bytes = 0;
 };
@@ -151,6 +160,8 @@ void launch_join_table(Ctx& c);
 void launch_edges(Ctx& c);
 void launch_finalize(Ctx& c);
 void launch_sol(Ctx& c);
+void launch_crit_elist(Ctx& c);
+void launch_crit(Ctx& c);
 int sol_block_count(int64_t n_max, int NOP);
 bool sol_uses_tables(int NOP);
 

@@ -411,9 +411,15 @@ void k_radix_pass(SortJobs jobs, DevState* ds) {
   if (sel < 0) return;
   const SortJob& jb = jobs.j[sel];
   const int d = jb.d, id = jb.id;
-  static_assert(N_SORTS == 4, "the selects below name every sort");
-  const uint32_t n = sel == 0 ? nn[0] : sel == 1 ? nn[1] : sel == 2 ? nn[2] : nn[3];
-  const uint32_t triv = sel == 0 ? tr[0] : sel == 1 ? tr[1] : sel == 2 ? tr[2] : tr[3];
+  // selects, not a dynamically indexed array: the values stay in registers
+  uint32_t n = nn[0], triv = tr[0];
+#pragma unroll
+  for (int i = 1; i < N_SORTS; ++i) {
+    if (sel == i) {
+      n = nn[i];
+      triv = tr[i];
+    }
+  }
   const uint32_t gexcl = ds->hist[id][d][dgt];
   const int parity = popc(~triv & ((1u << d) - 1u)) & 1;
   const uint64_t* kin = jb.k[parity];
@@ -904,11 +910,13 @@ void launch_refine(Ctx& c) {
   // the containment list always (its tie rule orders ops that start
   // together); the others when a digit was left to this pass; the device and
   // op-name lists with the idle-coincidence outputs (row order breaks ties)
-  const int32_t* counts[N_SORTS] = {&c.ds->nK, &c.ds->nCL, &c.ds->nK, &c.ds->nO};
-  for (SortBufs* s : {&c.sK, &c.sC, &c.sD, &c.sO}) {
+  const int32_t* counts[N_SORTS] = {&c.ds->nK, &c.ds->nCL, &c.ds->nK, &c.ds->nO, &c.ds->nK};
+  static_assert(N_SORTS == 5, "a count for every sort");
+  for (SortBufs* s : {&c.sK, &c.sC, &c.sD, &c.sO, &c.sE}) {
     const bool con = s == &c.sC;
     if (con && !c.contain) continue;
     if ((s == &c.sD || s == &c.sO) && !c.waits) continue;
+    if (s == &c.sE && !c.crit) continue;
     if (!con && s->first == 0) continue;
     jobs.j[m++] = RefineJob{{s->k[0], s->k[1]}, {s->v[0], s->v[1]}, counts[s->id], s->id, con ? 1 : 0,
                             s->id, s->first ? s->sh1 : 0};

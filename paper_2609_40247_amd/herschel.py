@@ -24,7 +24,7 @@ _LIBS = {"release": "libherschel.so", "checked": "libherschel_checked.so"}
 CPU_OP, LAUNCH, KERNEL = 0, 1, 2
 OK, EINVAL, EEVENT, ECAPACITY, EWORKSPACE, EDEVICE, ETOOBIG = 0, -1, -2, -3, -4, -5, -6
 STATIC_SCRATCH_BYTES = 64 << 20  # HERSCHEL_STATIC_SCRATCH_BYTES
-OUT_CONTAIN, OUT_OVERLAP, OUT_WAITS, OUT_SOL = 0x1, 0x2, 0x4, 0x8
+OUT_CONTAIN, OUT_OVERLAP, OUT_WAITS, OUT_SOL, OUT_CRIT = 0x1, 0x2, 0x4, 0x8, 0x10
 REPLAY = 0x100  # not an output: repeated equal calls replay a captured HIP graph
 
 _P = ctypes.c_void_p
@@ -58,7 +58,7 @@ class HerschelOutputs(ctypes.Structure):
                                                                "gap_flags", "counters", "dev_idle", "op_span",
                                                                "op_idle", "op_mfu", "op_mbu", "op_sol",
                                                                "opn_flops", "opn_bytes", "opn_time", "opn_sol",
-                                                               "opn_hot")]
+                                                               "opn_hot", "crit_time", "crit_flags", "crit_proc")]
 SOL_ROW_OUTPUTS = ("op_mfu", "op_mbu", "op_sol")
 SOL_NAME_OUTPUTS = ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot")
 
@@ -143,7 +143,7 @@ def herschel_trace_analyze_batch(events: HerschelEvents, offsets: np.ndarray, pa
 
 
 STAGES = ("init", "prep", "hist", "names", "sort", "timeline", "overlap", "contain", "join", "opagg", "edges",
-          "final", "waits", "sol")
+          "final", "waits", "sol", "crit")
 
 
 def herschel_time_stage(stage: int, start_event, stop_event, lib=None) -> int:
@@ -247,6 +247,7 @@ class Analyzer:
             op_idle=z(P * int(params["n_op_names"]), torch.int64),
             **{k: z(n, torch.int64) for k in SOL_ROW_OUTPUTS},
             **{k: z(int(params["n_op_names"]), torch.int64) for k in SOL_NAME_OUTPUTS},
+            crit_time=z(n, torch.int64), crit_flags=z(n, torch.uint8), crit_proc=z(P * 8, torch.int64),
         )
         self.params = self._params_struct(self.ws.data_ptr(), self.ws_bytes)
         self.outs = HerschelOutputs(gap_capacity=self.gap_capacity,
@@ -267,8 +268,9 @@ class Analyzer:
     def prefill(self) -> None:
         """Fill the op arrays with a marker so rows the library must not write
         can be checked."""
-        for k in ("op_nkern", "op_first", "op_last", "op_ksum") + SOL_ROW_OUTPUTS:
+        for k in ("op_nkern", "op_first", "op_last", "op_ksum", "crit_time") + SOL_ROW_OUTPUTS:
             self.o[k].fill_(self.op_fill)
+        self.o["crit_flags"].fill_(0xFD)
 
     def run(self, events: HerschelEvents, n: int) -> int:
         if n > self.n_max:
@@ -279,9 +281,11 @@ class Analyzer:
         """Copy the outputs of the last call to host numpy (oracle layout)."""
         h = {k: v.cpu().numpy() for k, v in self.o.items()}
         c = dict(zip(COUNTERS, (int(x) for x in h.pop("counters"))))
-        res = {k: h[k][:n] for k in ("link", "aux", "op_nkern", "op_first", "op_last", "op_ksum") + SOL_ROW_OUTPUTS}
+        res = {k: h[k][:n] for k in ("link", "aux", "op_nkern", "op_first", "op_last", "op_ksum", "crit_time",
+                                     "crit_flags") + SOL_ROW_OUTPUTS}
         for k in ("busy", "idle", "pair_overlap", "class_busy", "class_overlap", "any_busy", "name_count",
-                  "name_sum", "name_min", "name_max", "lat_hist", "dev_idle", "op_span", "op_idle") + SOL_NAME_OUTPUTS:
+                  "name_sum", "name_min", "name_max", "lat_hist", "dev_idle", "op_span", "op_idle",
+                  "crit_proc") + SOL_NAME_OUTPUTS:
             res[k] = h[k]
         res["edge_wait"] = h["edge_wait"][:self.n_edges]
         res["edge_status"] = h["edge_status"][:self.n_edges]

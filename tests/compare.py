@@ -44,5 +44,7 @@ def assert_same(got: tuple, want: tuple, params: dict, ctx: str = "") -> None:
         keys += ["dev_idle", "op_span", "op_idle"]
     if params.get("flags", 3) & 8:
         keys += ["op_mfu", "op_mbu", "op_sol", "opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot"]
+    if params.get("flags", 3) & 16:
+        keys += ["crit_time", "crit_flags", "crit_proc"]
     for k in keys:
         _eq(k, g[k], w[k], ctx)

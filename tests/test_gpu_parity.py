@@ -852,3 +852,69 @@ def test_sol_batch(H):
         o = oracle.analyze(c, q, gap_capacity=a.gap_capacity)
         assert_same((0, a.results(t.n)), o, q, t.label)
 
+
+
+# --------------------------------------------------------------- critical path
+@pytest.mark.parametrize("case", [0, 1, 2], ids=["figure", "nested", "ties"])
+def test_crit_worked_cases(H, case):
+    name, cols, p, exp = pins.crit_golden_cases()[case]
+    (code, g), _ = check(H, cols, p, f"critical path, {name}")
+    for k in ("crit_time", "crit_flags", "crit_proc"):
+        assert g[k].tolist() == exp[k], k
+
+
+CRIT_SMALL = [c for c in pins.BF_CASES if c.get("flags", 3) & 16] + [
+    dict(seed=7300 + s, n_rows=400, window=2000, n_procs=100, n_streams=2, n_threads=2, corr_range=50, flags=17)
+    for s in range(4)]
+
+
+@pytest.mark.parametrize("case", CRIT_SMALL, ids=lambda c: f"seed{c['seed']}")
+def test_crit_random_small(H, case):
+    tr = synth.random_small(**case)
+    check(H, tr.columns(), tr.params, tr.label)
+
+
+@pytest.mark.parametrize("which", ["config0", "config1", "config2", "config3", "medium", "all outputs"])
+def test_crit_workloads(H, which):
+    """The critical path on the workload shapes (the decode-step trace at
+    full size), alone with containment and with every other output."""
+    if which == "config0":
+        tr = synth.config0()
+    elif which in ("config1", "all outputs"):
+        tr = synth.config1()
+    elif which == "config2":
+        tr = synth.config2(scale=0.2)
+    elif which == "config3":
+        tr = synth.config3(n_procs=8, n_steps=40, n_edges=2000)
+    else:
+        tr = synth.random_small(seed=9900, n_rows=60_000, window=400_000, n_procs=3, n_streams=5, n_threads=2,
+                                corr_range=20_000, edges=300, n_op_names=7)
+    cols, p = tr.columns(), dict(tr.params, flags=17)
+    if which == "all outputs":
+        cols, p = synth.add_op_costs(cols, dict(p, flags=31), 3)
+    (code, g), _ = check(H, cols, p, f"{which} with the critical path")
+    cp = g["crit_proc"].reshape(-1, 8)
+    assert (cp[:, 0] == cp[:, 1:].sum(axis=1)).all() and cp[:, 0].max() > 0
+
+
+def test_crit_null_outputs_and_errors(H):
+    """Any of the three outputs may be NULL; the path needs containment."""
+    tr = synth.config3(n_procs=3, n_steps=10, n_edges=50)
+    cols, p = tr.columns(), dict(tr.params, flags=17)
+    n = tr.n
+    cap = n + p["n_procs"] * p["n_streams"]
+    ocode, o = oracle.analyze(cols, p, gap_capacity=cap)
+    for keep in (("crit_proc",), ("crit_time", "busy"), ("crit_flags", "link")):
+        an = H.Analyzer(p, n, gap_capacity=cap)
+        ptrs = {k: (v.data_ptr() if k in keep or k == "counters" else None) for k, v in an.o.items()}
+        outs = H.HerschelOutputs(gap_capacity=cap, **ptrs)
+        for k, v in an.o.items():  # the oracle's marks of rows it does not write
+            v.fill_(oracle.UNWRITTEN_U8 if k == "crit_flags" else 7 if v.dtype == torch.uint8 else oracle.UNWRITTEN_I64)
+        code = H.herschel_trace_analyze(H.events_struct(H.device_columns(cols)), n, an.params, outs)
+        torch.cuda.synchronize()
+        res = an.results(n)
+        assert code == ocode == 0
+        for k in keep:
+            assert np.array_equal(res[k], o[k]), k
+    code, _ = H.analyze(cols, dict(p, flags=16))
+    assert code == -1

@@ -46,7 +46,11 @@ def _run_both(H, tr, label):
     r_ref, r_st = ref.results(n), st.results(n)
     assert c_st == c_ref == 0, (label, c_st, c_ref)
     assert r_st["counters"] == r_ref["counters"], label
-    unwritten = () if p.get("flags", 3) & 4 else ("dev_idle", "op_span", "op_idle")  # outputs of another flag
+    # outputs of flags this call does not set are never written
+    flags = p.get("flags", 3)
+    unwritten = (() if flags & 4 else ("dev_idle", "op_span", "op_idle")) + \
+        (() if flags & 8 else H.SOL_ROW_OUTPUTS + H.SOL_NAME_OUTPUTS) + \
+        (() if flags & 16 else ("crit_time", "crit_flags", "crit_proc"))
     for k in r_ref:
         if k != "counters" and k not in unwritten:
             assert np.array_equal(r_st[k], r_ref[k]), (label, k)
