@@ -56,7 +56,8 @@ _P = ctypes.c_void_p
 
 
 class _Events(ctypes.Structure):
-    _fields_ = [(k, _P) for k in ("ts", "te", "corr", "pid", "lane", "name", "kind", "flops", "bytes")]
+    _fields_ = [(k, _P) for k in ("ts", "te", "corr", "pid", "lane", "name", "kind", "flops", "bytes",
+                                  "graph_node")]
 
 
 class _Params(ctypes.Structure):
@@ -65,7 +66,8 @@ class _Params(ctypes.Structure):
                 ("n_threads", ctypes.c_int32), ("n_names", ctypes.c_int32),
                 ("n_op_names", ctypes.c_int32), ("clock_offset", _P), ("stream_class", _P),
                 ("edges", _P), ("n_edges", ctypes.c_int64), ("flags", ctypes.c_uint32),
-                ("peak_flops", ctypes.c_int64), ("peak_bytes", ctypes.c_int64), ("ref_sol_ppm", _P)]
+                ("peak_flops", ctypes.c_int64), ("peak_bytes", ctypes.c_int64), ("ref_sol_ppm", _P),
+                ("n_graph_nodes", ctypes.c_int32)]
 
 
 COUNTER_NAMES = ("n_admitted_cpu", "n_admitted_launch", "n_admitted_kernel", "n_outside_window",
@@ -84,7 +86,8 @@ class _Outputs(ctypes.Structure):
                 ("gap_flags", _P), ("counters", _P), ("dev_idle", _P), ("op_span", _P), ("op_idle", _P),
                 ("op_mfu", _P), ("op_mbu", _P), ("op_sol", _P), ("opn_flops", _P), ("opn_bytes", _P),
                 ("opn_time", _P), ("opn_sol", _P), ("opn_hot", _P), ("crit_time", _P), ("crit_flags", _P),
-                ("crit_proc", _P)]
+                ("crit_proc", _P), ("launch_first", _P), ("launch_last", _P), ("gn_count", _P), ("gn_sum", _P),
+                ("gn_min", _P), ("gn_max", _P), ("gn_offset", _P)]
 
 
 def _ptr(a):
@@ -106,6 +109,8 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
     for k in ("flops", "bytes"):  # per-op operation counts and logical bytes (SOL outputs)
         if cols.get(k) is not None:
             c[k] = np.ascontiguousarray(cols[k], dtype=np.int64)
+    if cols.get("graph_node") is not None:  # per-kernel graph nodes (graph replay outputs)
+        c["graph_node"] = np.ascontiguousarray(cols["graph_node"], dtype=np.int32)
     P, S = int(params["n_procs"]), int(params["n_streams"])
     edges = params.get("edges")
     n_edges = 0 if edges is None else int(len(edges))
@@ -140,6 +145,9 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
            for k in ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot")},
         crit_time=np.full(n, UNWRITTEN_I64, np.int64), crit_flags=np.full(n, UNWRITTEN_U8, np.uint8),
         crit_proc=np.zeros(P * 8, np.int64),
+        launch_first=np.full(n, UNWRITTEN_I64, np.int64), launch_last=np.full(n, UNWRITTEN_I64, np.int64),
+        **{k: np.zeros(max(int(params.get("n_graph_nodes", 1)), 1), np.int64)
+           for k in ("gn_count", "gn_sum", "gn_min", "gn_max", "gn_offset")},
     )
     counters = np.zeros(len(COUNTER_NAMES), np.int64)
     ev = _Events(**{k: _ptr(v) for k, v in c.items()})
@@ -149,7 +157,7 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
                  n_op_names=int(params["n_op_names"]), clock_offset=_ptr(off), stream_class=_ptr(cls),
                  edges=_ptr(edges), n_edges=n_edges, flags=int(params.get("flags", 3)),
                  peak_flops=int(params.get("peak_flops", 0)), peak_bytes=int(params.get("peak_bytes", 0)),
-                 ref_sol_ppm=_ptr(ref))
+                 ref_sol_ppm=_ptr(ref), n_graph_nodes=int(params.get("n_graph_nodes", 0)))
     out = _Outputs(gap_capacity=gap_capacity, counters=counters.ctypes.data,
                    **{k: v.ctypes.data for k, v in o.items()})
     code = lib.herschel_oracle_analyze(ctypes.byref(ev), n, ctypes.byref(pr), ctypes.byref(out))

@@ -69,6 +69,9 @@ static int row_is_valid(const hro_events *ev, int64_t i, const hro_params *p) {
   if (ev->te[i] < ev->ts[i]) return 0;
   /* with the SOL outputs, an op's operation count and logical bytes */
   if ((p->flags & 8u) != 0 && k == K_CPU && (ev->flops[i] < 0 || ev->bytes[i] < 0)) return 0;
+  /* with graph replay separation, a kernel's graph node */
+  if ((p->flags & 32u) != 0 && k == K_KERNEL && (ev->graph_node[i] < -1 || ev->graph_node[i] >= p->n_graph_nodes))
+    return 0;
   return 1;
 }
 
@@ -94,6 +97,8 @@ static int params_ok(int64_t n, const hro_params *p) {
   }
   /* the critical path walks the host nesting (containment) */
   if ((p->flags & 16u) != 0 && (p->flags & 1u) == 0) return 0;
+  /* graph replay separation uses the per-launch kernel spans of containment */
+  if ((p->flags & 32u) != 0 && ((p->flags & 1u) == 0 || p->n_graph_nodes < 1)) return 0;
   if (p->clock_offset)
     for (int q = 0; q < p->n_procs; ++q)
       if (!in_abs(p->clock_offset[q])) return 0;
@@ -201,6 +206,7 @@ int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p
   if (!ev || !p || !out || !out->counters) return -1;
   if (!params_ok(n, p)) return -1;
   if ((p->flags & 8u) != 0 && n > 0 && (!ev->flops || !ev->bytes)) return -1;
+  if ((p->flags & 32u) != 0 && n > 0 && !ev->graph_node) return -1;
   const int P = p->n_procs, S = p->n_streams;
   const int64_t W0 = p->w0, W1 = p->w1, W = W1 - W0;
   const int contain = (p->flags & 1u) != 0, overlap = (p->flags & 2u) != 0;
@@ -859,6 +865,49 @@ int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p
     free(pos);
     free(hr);
     free(ke);
+  }
+
+  /* 19. Graph replay separation (Section 6.1: graph replay hides the
+   *     operator calls; graph identities and launch correlations separate
+   *     the replays).  READING: a replay is one admitted launch and the
+   *     kernels joined to it; its span runs from their first start to their
+   *     last end (corrected, unclipped; INT64_MAX / INT64_MIN with none),
+   *     reported for every admitted launch.  A kernel's graph node (a dense
+   *     id the caller gives to each node of each captured graph, -1 for a
+   *     kernel launched on its own) identifies the same operator across
+   *     replays: per node, over admitted kernels joined to a launch, the
+   *     count, sum, minimum and maximum of the duration te' - ts', and the
+   *     sum of the offsets ts' - the replay's first start (its place along
+   *     the replayed layer sequence). */
+  if ((p->flags & 32u) != 0) {
+    for (int64_t i = 0; i < n; ++i) {
+      if (!adm[i] || ev->kind[i] != K_LAUNCH) continue;
+      out->launch_first[i] = I64_MAX;
+      out->launch_last[i] = I64_MIN;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+      if (!adm[i] || ev->kind[i] != K_KERNEL || out->link[i] < 0) continue;
+      const int64_t l = out->link[i];
+      if (ts[i] < out->launch_first[l]) out->launch_first[l] = ts[i];
+      if (te[i] > out->launch_last[l]) out->launch_last[l] = te[i];
+    }
+    for (int q = 0; q < p->n_graph_nodes; ++q) {
+      out->gn_count[q] = 0;
+      out->gn_sum[q] = 0;
+      out->gn_min[q] = I64_MAX;
+      out->gn_max[q] = I64_MIN;
+      out->gn_offset[q] = 0;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+      if (!adm[i] || ev->kind[i] != K_KERNEL || out->link[i] < 0 || ev->graph_node[i] < 0) continue;
+      const int q = ev->graph_node[i];
+      const int64_t d = te[i] - ts[i];
+      out->gn_count[q]++;
+      out->gn_sum[q] = wrap_add(out->gn_sum[q], d);
+      if (d < out->gn_min[q]) out->gn_min[q] = d;
+      if (d > out->gn_max[q]) out->gn_max[q] = d;
+      out->gn_offset[q] = wrap_add(out->gn_offset[q], ts[i] - out->launch_first[out->link[i]]);
+    }
   }
 
   for (int64_t ps = 0; ps < (int64_t)P * S; ++ps) free(runs[ps]);

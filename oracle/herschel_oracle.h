@@ -25,6 +25,7 @@ typedef struct {
   const int32_t *pid, *lane, *name;
   const uint8_t *kind;
   const int64_t *flops, *bytes; /* per CPU op (flags bit 3); may be NULL otherwise */
+  const int32_t *graph_node;    /* per kernel (flags bit 5): node of a captured graph, -1 none */
 } hro_events;
 
 typedef struct {
@@ -42,6 +43,7 @@ typedef struct {
   uint32_t flags; /* bit0: containment, bit1: overlap, bit2: idle coincidence, bit3: SOL */
   int64_t peak_flops, peak_bytes;   /* per second (bit 3) */
   const int64_t *ref_sol_ppm;       /* [n_op_names] or NULL (bit 3) */
+  int32_t n_graph_nodes;            /* (bit 5) */
 } hro_params;
 
 typedef struct {
@@ -70,6 +72,8 @@ typedef struct {
   int64_t *crit_time;    /* [n] critical-path time attributed to each admitted row (flags bit 4) */
   uint8_t *crit_flags;   /* [n] bit0: the row's start event on the path, bit1: its end event (bit 4) */
   int64_t *crit_proc;    /* [n_procs * 8] length, kernel, api, sync, op, launch gap, queue gap, host gap */
+  int64_t *launch_first, *launch_last; /* [n] at admitted launches: span of their kernels (bit 5) */
+  int64_t *gn_count, *gn_sum, *gn_min, *gn_max, *gn_offset; /* [n_graph_nodes] (bit 5) */
 } hro_outputs;
 
 /* Same return codes as the product: 0 ok, -1 bad parameter, -2 invalid row,

@@ -515,6 +515,69 @@ def add_op_costs(cols: dict, params: dict, seed: int, ref: bool = True, flops_me
     return c, q
 
 
+def graph_replay_trace(seed: int = 21, n_steps: int = 200, n_nodes: int = 1000, n_streams: int = 2,
+                       drop_p: float = 0.01, eager: int = 3, period: int = 30 * MS):
+    """Decode steps replayed from one captured graph (the case where graph
+    replay hides the operator calls): per step a CPU op holds one graph
+    launch whose n_nodes kernels carry their node id (node i runs on stream
+    i % n_streams, back to back per stream after the launch, each node with
+    its own LogNormal median around 6 us and 20% spread per replay), and
+    `eager` kernels launched one by one (graph node -1) under ops of their
+    own.  Graph kernels are dropped with probability drop_p.  One process,
+    one thread; the window cuts the first and the last step.  Returns
+    (columns with graph_node, params)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    w0 = EPOCH
+    med = _lognormal_ns(rng, 6 * US, 1.0, n_nodes)
+    node_name = _zipf(rng, 2000, 1.1, n_nodes)
+    rows = []  # kind, lane, ts, te, corr, name, node
+    corr = int(rng.integers(0, 1 << 20))
+    for s_ in range(-1, n_steps + 1):
+        t = w0 + s_ * period + int(rng.integers(0, 200 * US))
+        step_rows = []
+        lat = int(rng.integers(3 * US, 9 * US))
+        l_end = t + int(rng.integers(10 * US, 20 * US))
+        step_rows.append((1, 0, t, l_end, corr, 1, -1))
+        ends = [t + lat] * n_streams
+        dur = np.maximum(1, np.rint(med * rng.lognormal(0.0, 0.2, n_nodes))).astype(np.int64)
+        keep = rng.random(n_nodes) >= drop_p
+        for i in range(n_nodes):
+            st = i % n_streams
+            a = ends[st] + int(rng.integers(0, 2 * US))
+            b = a + int(dur[i])
+            ends[st] = b
+            if keep[i]:
+                step_rows.append((2, st, a, b, corr, int(node_name[i]), i))
+        corr += 1
+        g_end = max(ends)
+        # eager kernels after the graph, each under its own op
+        te_ = g_end + int(rng.integers(2 * US, 10 * US))
+        for e in range(eager):
+            o0 = te_
+            l0 = o0 + int(rng.integers(1 * US, 3 * US))
+            l1 = l0 + int(rng.integers(3 * US, 8 * US))
+            k0 = max(l1, ends[0]) + int(rng.integers(1 * US, 5 * US))
+            k1 = k0 + int(rng.integers(2 * US, 20 * US))
+            ends[0] = k1
+            step_rows.append((1, 0, l0, l1, corr, 0, -1))
+            step_rows.append((2, 0, k0, k1, corr, int(rng.integers(0, 2000)), -1))
+            step_rows.append((0, 0, o0, l1 + int(rng.integers(1 * US, 3 * US)), 0, 1 + e, -1))
+            corr += 1
+            te_ = l1 + int(rng.integers(4 * US, 8 * US))
+        step_rows.append((0, 0, t - int(rng.integers(20 * US, 60 * US)), te_ + 5 * US, 0, 0, -1))
+        rows.extend(step_rows)
+    a = np.array(rows, np.int64)
+    order = rng.permutation(len(a))
+    a = a[order]
+    cols = dict(kind=a[:, 0].astype(np.uint8), pid=np.zeros(len(a), np.int32), lane=a[:, 1].astype(np.int32),
+                ts=a[:, 2], te=a[:, 3], corr=a[:, 4], name=a[:, 5].astype(np.int32),
+                graph_node=a[:, 6].astype(np.int32))
+    params = empty_params(window_begin=w0, window_end=w0 + n_steps * period, gap_threshold=20 * US,
+                          n_procs=1, n_streams=n_streams, n_threads=1, n_names=2000, n_op_names=1 + eager,
+                          flags=1 | 32, n_graph_nodes=n_nodes)
+    return cols, params
+
+
 def config4_lengths(n_traces: int = 256) -> np.ndarray:
     return np.array([int(np.random.Generator(np.random.PCG64(4000 + t)).integers(200_000, 2_000_001))
                      for t in range(n_traces)], np.int64)

@@ -70,7 +70,9 @@ def analyze(cols: dict, p: dict):
                  corr=int(cols["corr"][i])) for i in range(n)]
     for i, r in enumerate(rows):
         fb = (int(cols["flops"][i]), int(cols["bytes"][i])) if p["flags"] & 8 else (0, 0)
-        if not _valid(r["kind"], r["pid"], r["lane"], r["name"], r["ts"], r["te"], r["corr"], p, *fb):
+        bad_node = bool(p["flags"] & 32) and r["kind"] == 2 and \
+            not -1 <= int(cols["graph_node"][i]) < int(p["n_graph_nodes"])
+        if bad_node or not _valid(r["kind"], r["pid"], r["lane"], r["name"], r["ts"], r["te"], r["corr"], p, *fb):
             return -2, dict(counters=dict(first_invalid=i))
     off = p.get("clock_offset")
     for r in rows:
@@ -378,10 +380,31 @@ def analyze(cols: dict, p: dict):
                 ev_ = tgt
         crit = dict(crit_time=ctime, crit_flags=cflag, crit_proc=cproc.reshape(-1))
 
+    graph = None
+    if p["flags"] & 32 and contain:
+        # graph replays: every launch's joined kernels, all pairs
+        NG = int(p["n_graph_nodes"])
+        lf, ll = {}, {}
+        for l in lau:
+            mine = [k for k in ker if link[k] == l]
+            lf[l] = min((rows[k]["t0"] for k in mine), default=I64_MAX)
+            ll[l] = max((rows[k]["t1"] for k in mine), default=I64_MIN)
+        gn = {k: [] for k in range(NG)}
+        for k in ker:
+            q = int(cols["graph_node"][k])
+            if q >= 0 and link[k] >= 0:
+                gn[q].append((rows[k]["t1"] - rows[k]["t0"], rows[k]["t0"] - lf[link[k]]))
+        graph = dict(launch_first=lf, launch_last=ll,
+                     gn_count=np.array([len(gn[q]) for q in range(NG)], np.int64),
+                     gn_sum=np.array([_wrap(sum(d for d, _ in gn[q])) for q in range(NG)], np.int64),
+                     gn_min=np.array([min((d for d, _ in gn[q]), default=I64_MAX) for q in range(NG)], np.int64),
+                     gn_max=np.array([max((d for d, _ in gn[q]), default=I64_MIN) for q in range(NG)], np.int64),
+                     gn_offset=np.array([_wrap(sum(o for _, o in gn[q])) for q in range(NG)], np.int64))
+
     out = dict(counters=cnt, link=np.array(link, np.int32), aux=np.array(aux, np.int32),
                busy=busy, idle=idle, gaps=gaps, lat_hist=np.array(hist, np.int64),
                name_count=np.array(ncount, np.int64), name_sum=np.array(nsum, np.int64),
                name_min=np.array(nmin, np.int64), name_max=np.array(nmax, np.int64),
-               op=op_arrays, overlap=ov, waits=waits, sol=sol, crit=crit, edge_wait=np.array(ew, np.int64),
+               op=op_arrays, overlap=ov, waits=waits, sol=sol, crit=crit, graph=graph, edge_wait=np.array(ew, np.int64),
                edge_status=np.array(es, np.int32))
     return 0, out

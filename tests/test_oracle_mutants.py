@@ -110,6 +110,14 @@ MUTANTS = [
      "if (par >= 0) y = par, ys = 0, rel = tE[par], cat = 4, who = par;"),
     ("api charged to the kernel", "y = l, ys = 0, rel = tS[l], cat = 2, who = l;", "y = l, ys = 0, rel = tS[l], cat = 2, who = x;"),
     ("op tail charged to the child", "y = lastc[x], ys = 1, cat = 4, who = x;", "y = lastc[x], ys = 1, cat = 4, who = lastc[x];"),
+    ("replay offset from the launch", "ts[i] - out->launch_first[out->link[i]]);",
+     "ts[i] - ts[out->link[i]]);"),
+    ("unmatched node kernels counted",
+     "if (!adm[i] || ev->kind[i] != K_KERNEL || out->link[i] < 0 || ev->graph_node[i] < 0) continue;",
+     "if (!adm[i] || ev->kind[i] != K_KERNEL || ev->graph_node[i] < 0) continue;"),
+    ("replay end from the start", "if (te[i] > out->launch_last[l]) out->launch_last[l] = te[i];",
+     "if (ts[i] > out->launch_last[l]) out->launch_last[l] = ts[i];"),
+    ("node minimum as maximum", "if (d < out->gn_min[q]) out->gn_min[q] = d;", "if (d > out->gn_min[q]) out->gn_min[q] = d;"),
     ("edge status bits swapped", "(found[0] ? 0 : 1) | (found[1] ? 0 : 2)", "(found[0] ? 0 : 2) | (found[1] ? 0 : 1)"),
 ]
 
@@ -142,6 +150,14 @@ def _battery(lib) -> None:
         assert o[k].tolist() == exp[k], k
     pins.check_pa_case(lib)
     pins.check_crit_golden(lib)
+    pins.check_graph_golden(lib)
+    for seed in range(0, 40, 3):
+        cols, p = pins.graph_case(seed)
+        code, o = oracle.analyze(cols, p, lib=lib)
+        bcode, b = bruteforce.analyze(cols, p)
+        assert code == bcode
+        if code == 0:
+            pins._bf_compare(cols, p, o, b, f"graph seed {seed}")
     for case in [c for c in pins.BF_CASES if c.get("flags", 3) & 16][::3]:
         tr = synth.random_small(**case)
         code, o = oracle.analyze(tr.columns(), tr.params, lib=lib)

@@ -106,6 +106,12 @@ def _bf_compare(cols, p, o, b, ctx):
                 assert int(o[k][r]) == v, f"{ctx}: {k} row {r}"
         for k in ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot"):
             assert o[k].tolist() == b["sol"][k].tolist(), f"{ctx}: {k}"
+    if p["flags"] & 32:
+        for k in ("launch_first", "launch_last"):
+            for r, v in b["graph"][k].items():
+                assert int(o[k][r]) == v, f"{ctx}: {k} row {r}"
+        for k in ("gn_count", "gn_sum", "gn_min", "gn_max", "gn_offset"):
+            assert o[k].tolist() == b["graph"][k].tolist(), f"{ctx}: {k}"
     if p["flags"] & 16:
         for r, v in b["crit"]["crit_time"].items():
             assert int(o["crit_time"][r]) == v, f"{ctx}: crit_time row {r}"
@@ -774,4 +780,83 @@ def test_crit_path_time_shift():
 def test_crit_path_needs_containment():
     name, cols, p, _ = crit_golden_cases()[0]
     assert oracle.analyze(cols, dict(p, flags=16))[0] == -1
+
+
+# --------------------------------------------------------------- graph replays
+
+def graph_golden():
+    g = load_golden_raw("graph_replay_case.json")
+    a = np.array(g["rows"], np.int64)
+    cols = dict(kind=a[:, 0].astype(np.uint8), pid=a[:, 1].astype(np.int32), lane=a[:, 2].astype(np.int32),
+                ts=a[:, 3], te=a[:, 4], corr=a[:, 5], name=a[:, 6].astype(np.int32),
+                graph_node=a[:, 7].astype(np.int32))
+    return cols, synth.empty_params(**g["params"]), g["expect"]
+
+
+def check_graph_golden(lib=None):
+    cols, p, exp = graph_golden()
+    code, o = oracle.analyze(cols, p, lib=lib)
+    assert code == 0
+    for k in ("launch_first", "launch_last"):
+        for r, v in exp[k].items():
+            assert int(o[k][int(r)]) == v, (k, r)
+    for k in ("gn_count", "gn_sum", "gn_min", "gn_max", "gn_offset"):
+        assert o[k].tolist() == exp[k], k
+
+
+def test_graph_replay_worked_case():
+    """Two replays of a three-node graph, an eager kernel and an unmatched
+    node kernel, worked by hand."""
+    check_graph_golden()
+
+
+def graph_case(seed):
+    """A tiny adversarial trace with graph nodes on its kernels (-1 for about
+    a quarter of them); launches owning several kernels come from repeated
+    correlation ids."""
+    tr = synth.random_small(seed=8000 + seed, n_rows=80, window=600, corr_range=6 + seed % 5,
+                            flags=33 if seed % 2 else 35)
+    rng = np.random.default_rng(seed)
+    cols = dict(tr.columns())
+    ng = 1 + seed % 7
+    cols["graph_node"] = np.where(rng.random(tr.n) < 0.25, -1, rng.integers(0, ng, tr.n)).astype(np.int32)
+    return cols, dict(tr.params, n_graph_nodes=ng)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_bruteforce_graph(seed):
+    cols, p = graph_case(seed)
+    code, o = oracle.analyze(cols, p)
+    bcode, b = bruteforce.analyze(cols, p)
+    assert code == bcode
+    if code == 0:
+        _bf_compare(cols, p, o, b, f"graph seed {seed}")
+
+
+def test_graph_replay_invariants():
+    cols, p = synth.graph_replay_trace(n_steps=30, n_nodes=200)
+    code, o = oracle.analyze(cols, p)
+    assert code == 0
+    k = (cols["kind"] == 2) & (o["link"] >= 0)
+    node = cols["graph_node"]
+    assert o["gn_count"].sum() == int((k & (node >= 0)).sum())
+    assert (o["gn_offset"] >= 0).all()
+    # every node of the graph is seen about once per replay inside the window
+    assert o["gn_count"].min() >= 25
+    # each joined kernel lies inside its launch's span
+    L = o["link"][k]
+    assert (o["launch_first"][L] <= cols["ts"][k]).all() and (o["launch_last"][L] >= cols["te"][k]).all()
+
+
+@pytest.mark.parametrize("change", ["no containment", "no nodes", "node out of range"])
+def test_graph_replay_errors(change):
+    cols, p, _ = graph_golden()
+    if change == "no containment":
+        assert oracle.analyze(cols, dict(p, flags=32))[0] == -1
+    elif change == "no nodes":
+        assert oracle.analyze(cols, dict(p, n_graph_nodes=0))[0] == -1
+    else:
+        cols["graph_node"][5] = 3
+        code, o = oracle.analyze(cols, p)
+        assert code == -2 and o["counters"]["first_invalid"] == 5
 
