@@ -71,6 +71,8 @@ enum {
                                      needs HERSCHEL_OUT_CONTAIN */
 #define HERSCHEL_OUT_CRIT 0x10u   /* critical path (Section 6.1, execution progress and state);
                                      needs HERSCHEL_OUT_CONTAIN */
+#define HERSCHEL_OUT_GRAPH 0x20u  /* graph replay separation (Section 6.1, operator execution);
+                                     needs HERSCHEL_OUT_CONTAIN */
 /* Not an output: repeated calls with equal arguments replay a captured HIP
  * graph of their launches (herschel_trace_analyze).  Off by default. */
 #define HERSCHEL_REPLAY 0x100u
@@ -87,11 +89,12 @@ enum {
                                               indexed with int32, radix look-back words hold 30-bit prefixes */
 
 /* Input records as a structure of arrays, n rows, in any order (delivery
- * order).  37 bytes per row (53 with HERSCHEL_OUT_SOL).  Row i is valid iff
+ * order).  37 bytes per row (+16 with HERSCHEL_OUT_SOL, +4 with HERSCHEL_OUT_GRAPH).  Row i is valid iff
  *   kind[i] in {CPU_OP, LAUNCH, KERNEL}, 0 <= pid[i] < n_procs,
  *   KERNEL: 0 <= lane < n_streams and 0 <= name < n_names,
  *   CPU_OP: 0 <= lane < n_threads and 0 <= name < n_op_names,
  *           and with HERSCHEL_OUT_SOL flops >= 0 and bytes >= 0,
+ *   KERNEL with HERSCHEL_OUT_GRAPH: -1 <= graph_node < n_graph_nodes,
  *   LAUNCH: 0 <= lane < n_threads and name >= 0 (an API id),
  *   -2^62 < ts <= te < 2^62.
  * corr may be any int64 (an opaque per-process id, Section 5.2). */
@@ -109,6 +112,12 @@ typedef struct {
    * "Python calls and object fields"); read at CPU_OP rows only. */
   const int64_t *flops;
   const int64_t *bytes;
+  /* HERSCHEL_OUT_GRAPH only (else may be NULL): per KERNEL row, the node
+   * of a captured graph that the kernel replays, as a dense id the caller
+   * gives to each node of each captured graph (graph identity and node, as
+   * activity records report them), or -1 for a kernel launched on its own;
+   * read at KERNEL rows only. */
+  const int32_t *graph_node;
 } herschel_events;
 
 /* A cross-process dependency edge (Figure "Key performance observations",
@@ -137,6 +146,7 @@ typedef struct {
    * NULL for no reference. */
   int64_t peak_flops, peak_bytes;
   const int64_t *ref_sol_ppm;   /* [n_op_names] or NULL */
+  int32_t n_graph_nodes;        /* HERSCHEL_OUT_GRAPH only: graph node ids, >= 1 */
 } herschel_params;
 
 typedef struct {
@@ -240,6 +250,18 @@ typedef struct {
                                         (launch end to kernel start), queue gap (previous kernel end to
                                         kernel start), host gap (sibling end to start); all zero for a
                                         process without admitted rows */
+  /* HERSCHEL_OUT_GRAPH (Section 6.1: graph replay hides operator calls;
+   * graph identities and launch correlations separate replays).  A replay
+   * is an admitted launch and the kernels joined to it; per graph node, over
+   * the admitted kernels of that node joined to a launch: count, sum,
+   * minimum and maximum of te' - ts', and the sum of the offsets
+   * ts' - launch_first of the kernel's launch (its place along the replayed
+   * layer sequence).  Empty nodes: 0, 0, INT64_MAX, INT64_MIN, 0. */
+  int64_t *launch_first, *launch_last; /* [n] at admitted launches: first start and last end of their
+                                          kernels (INT64_MAX, INT64_MIN with none) */
+  int64_t *gn_count, *gn_sum;        /* [n_graph_nodes] */
+  int64_t *gn_min, *gn_max;          /* [n_graph_nodes] */
+  int64_t *gn_offset;                /* [n_graph_nodes] */
 } herschel_outputs;
 
 /* Bytes of device workspace that herschel_trace_analyze needs for n rows
@@ -314,7 +336,8 @@ enum {
   HERSCHEL_STAGE_WAITS = 12,   /* device-lane and op-name unions, idle coincidence (OUT_WAITS) */
   HERSCHEL_STAGE_SOL = 13,     /* operator efficiency and per-name hotness (OUT_SOL), after OPAGG */
   HERSCHEL_STAGE_CRIT = 14,    /* critical path (OUT_CRIT), after SOL */
-  HERSCHEL_N_STAGES = 15
+  HERSCHEL_STAGE_GRAPH = 15,   /* graph replay separation (OUT_GRAPH), after CRIT */
+  HERSCHEL_N_STAGES = 16
 };
 
 /* Record start_event / stop_event (hipEvent_t, created by the caller) on

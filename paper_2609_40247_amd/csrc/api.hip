@@ -191,6 +191,10 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.op_first_ws = b.take<int64_t>(n);
     c.op_last_ws = b.take<int64_t>(n);
   }
+  if (c.graph) {
+    c.graph_blocks = graph_block_count(n, c.NG);
+    if (graph_uses_tables(c.NG)) c.graph_part = b.take<uint64_t>((int64_t)c.graph_blocks * c.NG * 5);
+  }
   if (c.crit) {
     c.crit_pred = b.take<int32_t>(2 * n);
     c.crit_code = b.take<uint8_t>(2 * n);
@@ -225,6 +229,8 @@ struct InitArgs {
   int64_t n_opn;      // P * n_op_names with the idle-coincidence outputs, else 0
   int64_t n_crit;     // P * 8 with the critical path, else 0
   int64_t* crit_proc;
+  int64_t n_gn;       // graph nodes with the graph replay outputs, else 0
+  int64_t* gn[5];     // count, sum, min, max, offset (each may be NULL)
   int64_t* op_span;
   int64_t* op_idle;
 };
@@ -263,6 +269,13 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
   // with many names, the kernels themselves) are combined into them with
   // atomics
   for (int64_t i = tid; i < a.n_crit; i += nth) a.crit_proc[i] = 0;  // accumulated with atomics
+  for (int64_t i = tid; i < a.n_gn; i += nth) {  // combined with atomics
+    if (a.gn[0]) a.gn[0][i] = 0;
+    if (a.gn[1]) a.gn[1][i] = 0;
+    if (a.gn[2]) a.gn[2][i] = I64MAX;
+    if (a.gn[3]) a.gn[3][i] = I64MIN;
+    if (a.gn[4]) a.gn[4][i] = 0;
+  }
   for (int64_t i = tid; i < a.n_opn; i += nth) {  // accumulated with atomics
     if (a.op_span) a.op_span[i] = 0;
     if (a.op_idle) a.op_idle[i] = 0;
@@ -301,9 +314,16 @@ void launch_init(Ctx& c) {
   a.n_opn = c.waits ? (int64_t)c.P * c.NOP : 0;
   a.n_crit = c.crit && c.o.crit_proc ? (int64_t)c.P * 8 : 0;
   a.crit_proc = c.o.crit_proc;
+  a.n_gn = c.graph ? c.NG : 0;
+  a.gn[0] = c.o.gn_count;
+  a.gn[1] = c.o.gn_sum;
+  a.gn[2] = c.o.gn_min;
+  a.gn[3] = c.o.gn_max;
+  a.gn[4] = c.o.gn_offset;
   a.op_span = c.o.op_span ? c.o.op_span : c.op_span_ws;
   a.op_idle = c.o.op_idle;
-  const int64_t work = std::max<int64_t>({a.zero_n, (int64_t)a.nps * (c.overlap ? c.S : 1), (int64_t)c.NN, a.n_opn, 1});
+  const int64_t work =
+      std::max<int64_t>({a.zero_n, (int64_t)a.nps * (c.overlap ? c.S : 1), (int64_t)c.NN, a.n_opn, a.n_gn, 1});
   const int grid = (int)std::min<int64_t>(cdiv(work, 256 * 4), 2048);
   hipLaunchKernelGGL(k_init, dim3(std::max(grid, 1)), dim3(256), 0, c.st, a);
 }
@@ -376,8 +396,14 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   if (p->n_op_names < 1) return HERSCHEL_EINVAL;
   if (p->n_edges < 0 || (p->n_edges > 0 && !p->edges)) return HERSCHEL_EINVAL;
   if (p->flags & ~(HERSCHEL_OUT_CONTAIN | HERSCHEL_OUT_OVERLAP | HERSCHEL_OUT_WAITS | HERSCHEL_OUT_SOL |
-                   HERSCHEL_OUT_CRIT | HERSCHEL_REPLAY))
+                   HERSCHEL_OUT_CRIT | HERSCHEL_OUT_GRAPH | HERSCHEL_REPLAY))
     return HERSCHEL_EINVAL;
+  // graph replay separation reads the join's per-launch spans (kept with
+  // containment), the kernels' nodes and their number
+  if (p->flags & HERSCHEL_OUT_GRAPH) {
+    if (!(p->flags & HERSCHEL_OUT_CONTAIN) || p->n_graph_nodes < 1) return HERSCHEL_EINVAL;
+    if (n > 0 && !ev->graph_node) return HERSCHEL_EINVAL;
+  }
   // the critical path walks the host nesting
   if ((p->flags & HERSCHEL_OUT_CRIT) && !(p->flags & HERSCHEL_OUT_CONTAIN)) return HERSCHEL_EINVAL;
   // operator efficiency reads the per-op aggregates of containment, the
@@ -413,6 +439,8 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
   c.sol = (p->flags & HERSCHEL_OUT_SOL) != 0;
   c.crit = (p->flags & HERSCHEL_OUT_CRIT) != 0;
+  c.graph = (p->flags & HERSCHEL_OUT_GRAPH) != 0;
+  c.NG = c.graph ? p->n_graph_nodes : 0;
   c.nob = bits_host((uint64_t)(c.NOP - 1));
   c.pb = bits_host((uint64_t)(c.P - 1));
   c.sb = bits_host((uint64_t)(c.S - 1));
@@ -593,6 +621,9 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_CRIT);
   if (c.crit) launch_crit(c);
   stage_end(c, HERSCHEL_STAGE_CRIT);
+  stage_begin(c, HERSCHEL_STAGE_GRAPH);
+  if (c.graph) launch_graph(c);
+  stage_end(c, HERSCHEL_STAGE_GRAPH);
   wait(c.st, 1);
   wait(c.st, 4);
   stage_begin(c, HERSCHEL_STAGE_FINAL);
@@ -832,6 +863,9 @@ int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) 
   c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
   c.sol = (p->flags & HERSCHEL_OUT_SOL) != 0;
   c.crit = (p->flags & HERSCHEL_OUT_CRIT) != 0;
+  c.graph = (p->flags & HERSCHEL_OUT_GRAPH) != 0;
+  if (c.graph && p->n_graph_nodes < 1) return HERSCHEL_EINVAL;
+  c.NG = c.graph ? p->n_graph_nodes : 0;
   c.NOP = p->n_op_names;
   c.nob = bits_host((uint64_t)(c.NOP > 0 ? c.NOP - 1 : 0));
   c.overlap = (p->flags & HERSCHEL_OUT_OVERLAP) != 0;
@@ -929,6 +963,7 @@ int herschel_trace_analyze_batch(const herschel_events* ev, const int64_t* trace
       e.kind += o;
       if (e.flops) e.flops += o;
       if (e.bytes) e.bytes += o;
+      if (e.graph_node) e.graph_node += o;
     }
     herschel_params pt = p[t];
     pt.hip_stream = p[0].hip_stream;

@@ -52,7 +52,8 @@ struct Ctx {
   herschel_outputs o{};
   int64_t W0 = 0, W1 = 0, W = 0, thr = 0;
   int P = 0, S = 0, T = 0, NN = 0, NOP = 0;
-  bool contain = false, overlap = false, waits = false, sol = false, crit = false;
+  bool contain = false, overlap = false, waits = false, sol = false, crit = false, graph = false;
+  int NG = 0;                          // graph nodes (graph replay separation)
   int nob = 0;                         // bits of an op name (idle coincidence)
   int pb = 0, sb = 0, tb = 0, wb = 0;  // key field widths: pid, stream, thread, ts'-W0
   int wb1 = 0;                         // bits of W (values 0..W)
@@ -134,6 +135,8 @@ struct Ctx {
   uint8_t* crit_hasnext = nullptr;   // [n] by containment position (zeroed)
   uint64_t* crit_zmax = nullptr;     // [P] (zeroed)
   uint32_t* crit_zrow1 = nullptr;    // [P] (zeroed)
+  uint64_t* graph_part = nullptr;    // [graph_blocks * NG * 5] per-block graph-node tables
+  int graph_blocks = 0;
   char* zero_begin = nullptr;        // region cleared at the start of a call
   size_t zero_bytes = 0;
 };
@@ -162,6 +165,9 @@ void launch_finalize(Ctx& c);
 void launch_sol(Ctx& c);
 void launch_crit_elist(Ctx& c);
 void launch_crit(Ctx& c);
+void launch_graph(Ctx& c);
+bool graph_uses_tables(int NG);
+int graph_block_count(int64_t n_max, int NG);
 int sol_block_count(int64_t n_max, int NOP);
 bool sol_uses_tables(int NOP);
 

@@ -32,6 +32,7 @@ struct PrepArgs {
   bool waits;     // the op-name list and device-lane keys (idle coincidence)
   int nob;        // bits of an op name
   bool sol;       // ops carry operation counts and bytes (operator efficiency), which must be >= 0
+  int NG;         // kernels carry a graph node in [-1, NG) (graph replay separation), 0: not read
   DevState* ds;
   herschel_counters* cnt;
   int32_t* link;
@@ -101,6 +102,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
     int kind_[PREP_BATCH];
     int32_t pid_[PREP_BATCH], lane_[PREP_BATCH], name_[PREP_BATCH];
     int64_t ts_[PREP_BATCH], te_[PREP_BATCH], corr_[PREP_BATCH], cost_[PREP_BATCH];
+    int32_t node_[PREP_BATCH];
 #pragma unroll
     for (int u = 0; u < PREP_BATCH; ++u) {
       const int64_t r = base + (int64_t)(j0 + u) * PREP_THREADS + tid;
@@ -114,6 +116,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
       corr_[u] = a.ev.corr[rc];
       // an op's counts: negative iff either is (loaded for every kind)
       cost_[u] = a.sol ? a.ev.flops[rc] | a.ev.bytes[rc] : 0;
+      node_[u] = a.NG ? a.ev.graph_node[rc] : -1;
     }
 #pragma unroll
     for (int u = 0; u < PREP_BATCH; ++u) {
@@ -130,7 +133,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(PrepArgs a) {
         constexpr int64_t LIM = HERSCHEL_MAX_ABS_TIME;
         bool ok = kind <= 2 && pid >= 0 && pid < a.P;
         if (kind == HERSCHEL_KERNEL)
-          ok = ok && ln >= 0 && ln < a.S && name >= 0 && name < a.NN;
+          ok = ok && ln >= 0 && ln < a.S && name >= 0 && name < a.NN && node_[u] >= -1 &&
+               (a.NG == 0 || node_[u] < a.NG);
         else
           ok = ok && ln >= 0 && ln < a.T && name >= 0 &&
                (kind != HERSCHEL_CPU_OP || (name < a.NOP && cost_[u] >= 0));
@@ -314,6 +318,7 @@ void launch_prep(Ctx& c) {
   a.waits = c.waits;
   a.nob = c.nob;
   a.sol = c.sol;
+  a.NG = c.NG;
   a.ds = c.ds;
   a.cnt = c.o.counters;
   a.link = c.o.link;

@@ -24,14 +24,15 @@ _LIBS = {"release": "libherschel.so", "checked": "libherschel_checked.so"}
 CPU_OP, LAUNCH, KERNEL = 0, 1, 2
 OK, EINVAL, EEVENT, ECAPACITY, EWORKSPACE, EDEVICE, ETOOBIG = 0, -1, -2, -3, -4, -5, -6
 STATIC_SCRATCH_BYTES = 64 << 20  # HERSCHEL_STATIC_SCRATCH_BYTES
-OUT_CONTAIN, OUT_OVERLAP, OUT_WAITS, OUT_SOL, OUT_CRIT = 0x1, 0x2, 0x4, 0x8, 0x10
+OUT_CONTAIN, OUT_OVERLAP, OUT_WAITS, OUT_SOL, OUT_CRIT, OUT_GRAPH = 0x1, 0x2, 0x4, 0x8, 0x10, 0x20
 REPLAY = 0x100  # not an output: repeated equal calls replay a captured HIP graph
 
 _P = ctypes.c_void_p
 
 
 class HerschelEvents(ctypes.Structure):
-    _fields_ = [(k, _P) for k in ("ts", "te", "corr", "pid", "lane", "name", "kind", "flops", "bytes")]
+    _fields_ = [(k, _P) for k in ("ts", "te", "corr", "pid", "lane", "name", "kind", "flops", "bytes",
+                                  "graph_node")]
 
 
 class HerschelParams(ctypes.Structure):
@@ -42,7 +43,8 @@ class HerschelParams(ctypes.Structure):
                 ("clock_offset", _P), ("stream_class", _P), ("edges", _P),
                 ("n_edges", ctypes.c_int64), ("flags", ctypes.c_uint32), ("hip_stream", _P),
                 ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
-                ("peak_flops", ctypes.c_int64), ("peak_bytes", ctypes.c_int64), ("ref_sol_ppm", _P)]
+                ("peak_flops", ctypes.c_int64), ("peak_bytes", ctypes.c_int64), ("ref_sol_ppm", _P),
+                ("n_graph_nodes", ctypes.c_int32)]
 
 
 COUNTERS = ("n_admitted_cpu", "n_admitted_launch", "n_admitted_kernel", "n_outside_window", "n_matched",
@@ -58,7 +60,10 @@ class HerschelOutputs(ctypes.Structure):
                                                                "gap_flags", "counters", "dev_idle", "op_span",
                                                                "op_idle", "op_mfu", "op_mbu", "op_sol",
                                                                "opn_flops", "opn_bytes", "opn_time", "opn_sol",
-                                                               "opn_hot", "crit_time", "crit_flags", "crit_proc")]
+                                                               "opn_hot", "crit_time", "crit_flags", "crit_proc",
+                                                               "launch_first", "launch_last", "gn_count", "gn_sum",
+                                                               "gn_min", "gn_max", "gn_offset")]
+GRAPH_NODE_OUTPUTS = ("gn_count", "gn_sum", "gn_min", "gn_max", "gn_offset")
 SOL_ROW_OUTPUTS = ("op_mfu", "op_mbu", "op_sol")
 SOL_NAME_OUTPUTS = ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot")
 
@@ -143,7 +148,7 @@ def herschel_trace_analyze_batch(events: HerschelEvents, offsets: np.ndarray, pa
 
 
 STAGES = ("init", "prep", "hist", "names", "sort", "timeline", "overlap", "contain", "join", "opagg", "edges",
-          "final", "waits", "sol", "crit")
+          "final", "waits", "sol", "crit", "graph")
 
 
 def herschel_time_stage(stage: int, start_event, stop_event, lib=None) -> int:
@@ -182,7 +187,7 @@ def device_columns(cols: dict, device="cuda") -> dict:
     """Host numpy columns -> contiguous device tensors of the ABI's types
     (flops and bytes only when the columns hold them)."""
     dt = dict(ts=np.int64, te=np.int64, corr=np.int64, pid=np.int32, lane=np.int32, name=np.int32, kind=np.uint8,
-              flops=np.int64, bytes=np.int64)
+              flops=np.int64, bytes=np.int64, graph_node=np.int32)
     return {k: torch.from_numpy(np.ascontiguousarray(cols[k], dtype=dt[k])).to(device)
             for k in dt if cols.get(k) is not None}
 
@@ -248,6 +253,8 @@ class Analyzer:
             **{k: z(n, torch.int64) for k in SOL_ROW_OUTPUTS},
             **{k: z(int(params["n_op_names"]), torch.int64) for k in SOL_NAME_OUTPUTS},
             crit_time=z(n, torch.int64), crit_flags=z(n, torch.uint8), crit_proc=z(P * 8, torch.int64),
+            launch_first=z(n, torch.int64), launch_last=z(n, torch.int64),
+            **{k: z(max(int(params.get("n_graph_nodes", 1)), 1), torch.int64) for k in GRAPH_NODE_OUTPUTS},
         )
         self.params = self._params_struct(self.ws.data_ptr(), self.ws_bytes)
         self.outs = HerschelOutputs(gap_capacity=self.gap_capacity,
@@ -263,12 +270,13 @@ class Analyzer:
             clock_offset=_ptr(self.d_off), stream_class=_ptr(self.d_cls), edges=_ptr(self.d_edges),
             n_edges=self.n_edges, flags=int(p.get("flags", 3)), hip_stream=st, workspace=ws,
             workspace_bytes=ws_bytes, peak_flops=int(p.get("peak_flops", 0)), peak_bytes=int(p.get("peak_bytes", 0)),
-            ref_sol_ppm=_ptr(self.d_ref))
+            ref_sol_ppm=_ptr(self.d_ref), n_graph_nodes=int(p.get("n_graph_nodes", 0)))
 
     def prefill(self) -> None:
         """Fill the op arrays with a marker so rows the library must not write
         can be checked."""
-        for k in ("op_nkern", "op_first", "op_last", "op_ksum", "crit_time") + SOL_ROW_OUTPUTS:
+        for k in ("op_nkern", "op_first", "op_last", "op_ksum", "crit_time", "launch_first",
+                  "launch_last") + SOL_ROW_OUTPUTS:
             self.o[k].fill_(self.op_fill)
         self.o["crit_flags"].fill_(0xFD)
 
@@ -282,10 +290,10 @@ class Analyzer:
         h = {k: v.cpu().numpy() for k, v in self.o.items()}
         c = dict(zip(COUNTERS, (int(x) for x in h.pop("counters"))))
         res = {k: h[k][:n] for k in ("link", "aux", "op_nkern", "op_first", "op_last", "op_ksum", "crit_time",
-                                     "crit_flags") + SOL_ROW_OUTPUTS}
+                                     "crit_flags", "launch_first", "launch_last") + SOL_ROW_OUTPUTS}
         for k in ("busy", "idle", "pair_overlap", "class_busy", "class_overlap", "any_busy", "name_count",
                   "name_sum", "name_min", "name_max", "lat_hist", "dev_idle", "op_span", "op_idle",
-                  "crit_proc") + SOL_NAME_OUTPUTS:
+                  "crit_proc") + SOL_NAME_OUTPUTS + GRAPH_NODE_OUTPUTS:
             res[k] = h[k]
         res["edge_wait"] = h["edge_wait"][:self.n_edges]
         res["edge_status"] = h["edge_status"][:self.n_edges]

@@ -46,5 +46,7 @@ def assert_same(got: tuple, want: tuple, params: dict, ctx: str = "") -> None:
         keys += ["op_mfu", "op_mbu", "op_sol", "opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot"]
     if params.get("flags", 3) & 16:
         keys += ["crit_time", "crit_flags", "crit_proc"]
+    if params.get("flags", 3) & 32:
+        keys += ["launch_first", "launch_last", "gn_count", "gn_sum", "gn_min", "gn_max", "gn_offset"]
     for k in keys:
         _eq(k, g[k], w[k], ctx)

@@ -918,3 +918,65 @@ def test_crit_null_outputs_and_errors(H):
             assert np.array_equal(res[k], o[k]), k
     code, _ = H.analyze(cols, dict(p, flags=16))
     assert code == -1
+
+
+# --------------------------------------------------------------- graph replays
+def test_graph_worked_case(H):
+    cols, p, exp = pins.graph_golden()
+    (code, g), _ = check(H, cols, p, "graph replays, worked case")
+    for k in ("gn_count", "gn_sum", "gn_min", "gn_max", "gn_offset"):
+        assert g[k].tolist() == exp[k], k
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_graph_random_small(H, seed):
+    cols, p = pins.graph_case(seed)
+    check(H, cols, p, f"graph seed {seed}")
+
+
+@pytest.mark.parametrize("shape", ["decode", "many nodes", "all outputs"])
+def test_graph_replay_workloads(H, shape):
+    """A graph-replayed decode trace at the decode-step trace's size (1000
+    replays of a 1000-node graph), nodes beyond the LDS tables (global
+    atomics), and every output together."""
+    if shape == "decode":
+        cols, p = synth.graph_replay_trace(n_steps=1000, n_nodes=1000)
+    elif shape == "many nodes":
+        cols, p = synth.graph_replay_trace(n_steps=40, n_nodes=3000, n_streams=3)
+    else:
+        cols, p = synth.graph_replay_trace(n_steps=100, n_nodes=500)
+        cols, p = synth.add_op_costs(cols, dict(p, flags=63), 4)
+    (code, g), _ = check(H, cols, p, f"graph replays, {shape}")
+    assert g["gn_count"].sum() > 0
+
+
+def test_graph_null_outputs_and_errors(H):
+    cols, p = synth.graph_replay_trace(n_steps=20, n_nodes=300)
+    n = len(cols["ts"])
+    cap = n + p["n_procs"] * p["n_streams"]
+    ocode, o = oracle.analyze(cols, p, gap_capacity=cap)
+    for keep in (("gn_min", "launch_last"), ("gn_count", "gn_offset", "busy"), ("launch_first",)):
+        an = H.Analyzer(p, n, gap_capacity=cap)
+        ptrs = {k: (v.data_ptr() if k in keep or k == "counters" else None) for k, v in an.o.items()}
+        outs = H.HerschelOutputs(gap_capacity=cap, **ptrs)
+        for k, v in an.o.items():
+            v.fill_(oracle.UNWRITTEN_U8 if k == "crit_flags" else 7 if v.dtype == torch.uint8 else oracle.UNWRITTEN_I64)
+        code = H.herschel_trace_analyze(H.events_struct(H.device_columns(cols)), n, an.params, outs)
+        torch.cuda.synchronize()
+        res = an.results(n)
+        assert code == ocode == 0
+        for k in keep:
+            assert np.array_equal(res[k], o[k]), k
+    assert H.analyze(cols, dict(p, flags=32))[0] == -1
+    with pytest.raises(ValueError):  # the workspace size already rejects it
+        H.analyze(cols, dict(p, n_graph_nodes=0))
+    an = H.Analyzer(p, n, gap_capacity=cap)
+    an.p = dict(p, n_graph_nodes=0)
+    params = an._params_struct(an.ws.data_ptr(), an.ws_bytes)
+    assert H.herschel_trace_analyze(H.events_struct(H.device_columns(cols)), n, params, an.outs) == -1
+    bad = dict(cols)
+    bad["graph_node"] = cols["graph_node"].copy()
+    k = int(np.flatnonzero(cols["kind"] == 2)[3])
+    bad["graph_node"][k] = 300
+    code, g = H.analyze(bad, p)
+    assert code == -2 and g["counters"]["first_invalid"] == oracle.analyze(bad, p)[1]["counters"]["first_invalid"]

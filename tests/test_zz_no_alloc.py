@@ -50,7 +50,8 @@ def _run_both(H, tr, label):
     flags = p.get("flags", 3)
     unwritten = (() if flags & 4 else ("dev_idle", "op_span", "op_idle")) + \
         (() if flags & 8 else H.SOL_ROW_OUTPUTS + H.SOL_NAME_OUTPUTS) + \
-        (() if flags & 16 else ("crit_time", "crit_flags", "crit_proc"))
+        (() if flags & 16 else ("crit_time", "crit_flags", "crit_proc")) + \
+        (() if flags & 32 else ("launch_first", "launch_last") + H.GRAPH_NODE_OUTPUTS)
     for k in r_ref:
         if k != "counters" and k not in unwritten:
             assert np.array_equal(r_st[k], r_ref[k]), (label, k)
