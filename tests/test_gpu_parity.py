@@ -980,3 +980,14 @@ def test_graph_null_outputs_and_errors(H):
     bad["graph_node"][k] = 300
     code, g = H.analyze(bad, p)
     assert code == -2 and g["counters"]["first_invalid"] == oracle.analyze(bad, p)[1]["counters"]["first_invalid"]
+
+
+# --------------------------------------------------------------- a real trace
+def test_real_trace_sample(H):
+    """The rocprofv3 sample through the adapter, every output but operator
+    efficiency (the sample carries no operation counts)."""
+    from paper_2609_40247_amd import ingest
+    import os
+    t = ingest.read_rocprofv3(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "rocprof_sample"))
+    p = dict(t.params, flags=t.params["flags"] | 2 | 4 | 16)
+    check(H, t.columns, p, "rocprofv3 sample")
