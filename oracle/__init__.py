@@ -87,7 +87,8 @@ class _Outputs(ctypes.Structure):
                 ("op_mfu", _P), ("op_mbu", _P), ("op_sol", _P), ("opn_flops", _P), ("opn_bytes", _P),
                 ("opn_time", _P), ("opn_sol", _P), ("opn_hot", _P), ("crit_time", _P), ("crit_flags", _P),
                 ("crit_proc", _P), ("launch_first", _P), ("launch_last", _P), ("gn_count", _P), ("gn_sum", _P),
-                ("gn_min", _P), ("gn_max", _P), ("gn_offset", _P)]
+                ("gn_min", _P), ("gn_max", _P), ("gn_offset", _P), ("opname_count", _P), ("opname_sum", _P),
+                ("opname_min", _P), ("opname_max", _P)]
 
 
 def _ptr(a):
@@ -148,6 +149,8 @@ def analyze(cols: dict, params: dict, gap_capacity: int | None = None, lib=None)
         launch_first=np.full(n, UNWRITTEN_I64, np.int64), launch_last=np.full(n, UNWRITTEN_I64, np.int64),
         **{k: np.zeros(max(int(params.get("n_graph_nodes", 1)), 1), np.int64)
            for k in ("gn_count", "gn_sum", "gn_min", "gn_max", "gn_offset")},
+        **{k: np.zeros(int(params["n_op_names"]), np.int64)
+           for k in ("opname_count", "opname_sum", "opname_min", "opname_max")},
     )
     counters = np.zeros(len(COUNTER_NAMES), np.int64)
     ev = _Events(**{k: _ptr(v) for k, v in c.items()})

@@ -477,6 +477,25 @@ int herschel_oracle_analyze(const hro_events *ev, int64_t n, const hro_params *p
     if (d > out->name_max[q]) out->name_max[q] = d;
   }
 
+  /* 13b. The same per op name over all admitted CPU ops (the per-op-name
+   *      variant): count, sum, min and max of te' - ts', unclipped.  Each
+   *      output may be NULL. */
+  for (int q = 0; q < p->n_op_names; ++q) {
+    if (out->opname_count) out->opname_count[q] = 0;
+    if (out->opname_sum) out->opname_sum[q] = 0;
+    if (out->opname_min) out->opname_min[q] = I64_MAX;
+    if (out->opname_max) out->opname_max[q] = I64_MIN;
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    if (!adm[i] || ev->kind[i] != K_CPU) continue;
+    int q = ev->name[i];
+    int64_t d = te[i] - ts[i];
+    if (out->opname_count) out->opname_count[q]++;
+    if (out->opname_sum) out->opname_sum[q] = wrap_add(out->opname_sum[q], d);
+    if (out->opname_min && d < out->opname_min[q]) out->opname_min[q] = d;
+    if (out->opname_max && d > out->opname_max[q]) out->opname_max[q] = d;
+  }
+
   /* 14. Overlap as interval coverage (panel "Overlap and exposed work"):
    *     per process, with U_s the covered set of stream s,
    *     pair_overlap[i][j] = |U_i and U_j|, class_busy[c] = |union over the

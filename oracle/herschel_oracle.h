@@ -74,6 +74,7 @@ typedef struct {
   int64_t *crit_proc;    /* [n_procs * 8] length, kernel, api, sync, op, launch gap, queue gap, host gap */
   int64_t *launch_first, *launch_last; /* [n] at admitted launches: span of their kernels (bit 5) */
   int64_t *gn_count, *gn_sum, *gn_min, *gn_max, *gn_offset; /* [n_graph_nodes] (bit 5) */
+  int64_t *opname_count, *opname_sum, *opname_min, *opname_max; /* [n_op_names], each may be NULL */
 } hro_outputs;
 
 /* Same return codes as the product: 0 ok, -1 bad parameter, -2 invalid row,

@@ -192,6 +192,14 @@ def analyze(cols: dict, p: dict):
         nsum[q] = _wrap(nsum[q] + d)
         nmin[q] = min(nmin[q], d)
         nmax[q] = max(nmax[q], d)
+    # the same over admitted ops, by op name, as lists of their durations
+    opd = {q: [] for q in range(p["n_op_names"])}
+    for i in ops:
+        opd[rows[i]["name"]].append(rows[i]["t1"] - rows[i]["t0"])
+    opname = dict(opname_count=np.array([len(v) for v in opd.values()], np.int64),
+                  opname_sum=np.array([_wrap(sum(v)) for v in opd.values()], np.int64),
+                  opname_min=np.array([min(v, default=I64_MAX) for v in opd.values()], np.int64),
+                  opname_max=np.array([max(v, default=I64_MIN) for v in opd.values()], np.int64))
 
     ov = None
     if overlap:
@@ -405,6 +413,7 @@ def analyze(cols: dict, p: dict):
                busy=busy, idle=idle, gaps=gaps, lat_hist=np.array(hist, np.int64),
                name_count=np.array(ncount, np.int64), name_sum=np.array(nsum, np.int64),
                name_min=np.array(nmin, np.int64), name_max=np.array(nmax, np.int64),
-               op=op_arrays, overlap=ov, waits=waits, sol=sol, crit=crit, graph=graph, edge_wait=np.array(ew, np.int64),
+               op=op_arrays, overlap=ov, waits=waits, sol=sol, crit=crit, graph=graph, opname=opname,
+               edge_wait=np.array(ew, np.int64),
                edge_status=np.array(es, np.int32))
     return 0, out

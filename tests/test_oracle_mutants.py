@@ -118,6 +118,10 @@ MUTANTS = [
     ("replay end from the start", "if (te[i] > out->launch_last[l]) out->launch_last[l] = te[i];",
      "if (ts[i] > out->launch_last[l]) out->launch_last[l] = ts[i];"),
     ("node minimum as maximum", "if (d < out->gn_min[q]) out->gn_min[q] = d;", "if (d > out->gn_min[q]) out->gn_min[q] = d;"),
+    ("op-name duration clipped", "    int64_t d = te[i] - ts[i];\n    if (out->opname_count)",
+     "    int64_t d = (te[i] < W1 ? te[i] : W1) - ts[i];\n    if (out->opname_count)"),
+    ("op-name maximum as minimum", "if (out->opname_max && d > out->opname_max[q]) out->opname_max[q] = d;",
+     "if (out->opname_max && d < out->opname_max[q]) out->opname_max[q] = d;"),
     ("edge status bits swapped", "(found[0] ? 0 : 1) | (found[1] ? 0 : 2)", "(found[0] ? 0 : 2) | (found[1] ? 0 : 1)"),
 ]
 

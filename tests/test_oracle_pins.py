@@ -90,6 +90,8 @@ def _bf_compare(cols, p, o, b, ctx):
     gaps = list(zip(o["gap_pid"].tolist(), o["gap_stream"].tolist(), o["gap_begin"].tolist(),
                     o["gap_end"].tolist(), o["gap_flags"].tolist()))
     assert gaps == [tuple(int(x) for x in g) for g in b["gaps"]], ctx
+    for k, v in b["opname"].items():
+        assert o[k].tolist() == v.tolist(), f"{ctx}: {k}"
     if p["flags"] & 1:
         for r, v in b["op"].items():
             assert (int(o["op_nkern"][r]), int(o["op_first"][r]), int(o["op_last"][r]), int(o["op_ksum"][r])) == v, \
@@ -860,3 +862,21 @@ def test_graph_replay_errors(change):
         code, o = oracle.analyze(cols, p)
         assert code == -2 and o["counters"]["first_invalid"] == 5
 
+
+
+def test_op_name_aggregates_worked():
+    """Per op name, over admitted ops, of the unclipped duration: the worked
+    critical-path cases hold one op of each name (prep 90 and use 80; step
+    600 and layer 290)."""
+    cases = crit_golden_cases()
+    for (name, cols, p, _), exp in zip(cases[:2], ([90, 80], [600, 290])):
+        code, o = oracle.analyze(cols, p)
+        assert code == 0
+        assert o["opname_count"].tolist() == [1, 1], name
+        for k in ("opname_sum", "opname_min", "opname_max"):
+            assert o[k].tolist() == exp, (name, k)
+    # an op crossing W1 keeps its whole duration; an op outside the window is not counted
+    cols, p, _ = pa_trace(10**9)
+    p = dict(p, window_end=500)
+    code, o = oracle.analyze(cols, p)
+    assert code == 0 and o["opname_sum"].tolist() == [10**9 + 2000]
