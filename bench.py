@@ -103,7 +103,7 @@ def algorithmic_bytes(n: int, counters: dict, params: dict, n_gaps: int) -> int:
     b = 37 * n + 8 * n
     if flags & 1:
         b += 28 * counters["n_admitted_cpu"]
-    b += 16 * P * S + 32 * NN + 64 * 8 + 25 * n_gaps + 8 * P + S + 112
+    b += 16 * P * S + 32 * NN + 32 * int(params["n_op_names"]) + 64 * 8 + 25 * n_gaps + 8 * P + S + 112
     if flags & 2:
         b += 8 * (P * S * S + 12 * P)
     b += 36 * E  # each edge read (24 B) and its wait and status written
@@ -155,7 +155,8 @@ def make_trace(workload: str):
             "config3": synth.config3}[workload]()
 
 
-BATCH_OUTPUTS = ("name_count", "name_sum", "name_min", "name_max", "busy", "idle", "gap_pid", "gap_stream",
+BATCH_OUTPUTS = ("name_count", "name_sum", "name_min", "name_max", "opname_count", "opname_sum", "opname_min",
+                 "opname_max", "busy", "idle", "gap_pid", "gap_stream",
                  "gap_begin", "gap_end", "gap_flags", "lat_hist", "counters")
 
 

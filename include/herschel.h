@@ -262,6 +262,11 @@ typedef struct {
   int64_t *gn_count, *gn_sum;        /* [n_graph_nodes] */
   int64_t *gn_min, *gn_max;          /* [n_graph_nodes] */
   int64_t *gn_offset;                /* [n_graph_nodes] */
+  /* The per-name aggregates of the kernels, for the admitted CPU ops by op
+   * name (no flag; each may be NULL): count, sum, min and max of the
+   * unclipped te' - ts'; empty names: 0, 0, INT64_MAX, INT64_MIN. */
+  int64_t *opname_count, *opname_sum;  /* [n_op_names] */
+  int64_t *opname_min, *opname_max;    /* [n_op_names] */
 } herschel_outputs;
 
 /* Bytes of device workspace that herschel_trace_analyze needs for n rows

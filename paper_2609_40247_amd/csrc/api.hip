@@ -182,6 +182,8 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.oev = b.take<uint64_t>(c.oev_cap);
     c.op_span_ws = b.take<int64_t>((int64_t)c.P * c.NOP);
   }
+  c.opn_blocks = opnames_block_count(n, c.NOP);
+  if (opnames_use_tables(c.NOP)) c.opn_part = b.take<uint64_t>((int64_t)c.opn_blocks * c.NOP * 4);
   c.name_blocks = names_block_count(n, c.NN);
   if (c.NN <= names_lds_limit()) c.name_part = b.take<uint64_t>((int64_t)c.name_blocks * c.NN * 4);
   if (c.sol) {
@@ -229,6 +231,8 @@ struct InitArgs {
   int64_t n_opn;      // P * n_op_names with the idle-coincidence outputs, else 0
   int64_t n_crit;     // P * 8 with the critical path, else 0
   int64_t* crit_proc;
+  int NOP;
+  int64_t* opn[4];    // per op name: count, sum, min, max (each may be NULL)
   int64_t n_gn;       // graph nodes with the graph replay outputs, else 0
   int64_t* gn[5];     // count, sum, min, max, offset (each may be NULL)
   int64_t* op_span;
@@ -269,6 +273,12 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
   // with many names, the kernels themselves) are combined into them with
   // atomics
   for (int64_t i = tid; i < a.n_crit; i += nth) a.crit_proc[i] = 0;  // accumulated with atomics
+  for (int64_t i = tid; i < a.NOP; i += nth) {  // combined with atomics
+    if (a.opn[0]) a.opn[0][i] = 0;
+    if (a.opn[1]) a.opn[1][i] = 0;
+    if (a.opn[2]) a.opn[2][i] = I64MAX;
+    if (a.opn[3]) a.opn[3][i] = I64MIN;
+  }
   for (int64_t i = tid; i < a.n_gn; i += nth) {  // combined with atomics
     if (a.gn[0]) a.gn[0][i] = 0;
     if (a.gn[1]) a.gn[1][i] = 0;
@@ -314,6 +324,11 @@ void launch_init(Ctx& c) {
   a.n_opn = c.waits ? (int64_t)c.P * c.NOP : 0;
   a.n_crit = c.crit && c.o.crit_proc ? (int64_t)c.P * 8 : 0;
   a.crit_proc = c.o.crit_proc;
+  a.NOP = c.NOP;
+  a.opn[0] = c.o.opname_count;
+  a.opn[1] = c.o.opname_sum;
+  a.opn[2] = c.o.opname_min;
+  a.opn[3] = c.o.opname_max;
   a.n_gn = c.graph ? c.NG : 0;
   a.gn[0] = c.o.gn_count;
   a.gn[1] = c.o.gn_sum;
@@ -323,7 +338,8 @@ void launch_init(Ctx& c) {
   a.op_span = c.o.op_span ? c.o.op_span : c.op_span_ws;
   a.op_idle = c.o.op_idle;
   const int64_t work =
-      std::max<int64_t>({a.zero_n, (int64_t)a.nps * (c.overlap ? c.S : 1), (int64_t)c.NN, a.n_opn, a.n_gn, 1});
+      std::max<int64_t>({a.zero_n, (int64_t)a.nps * (c.overlap ? c.S : 1), (int64_t)c.NN, a.n_opn, a.n_gn,
+                         (int64_t)c.NOP, 1});
   const int grid = (int)std::min<int64_t>(cdiv(work, 256 * 4), 2048);
   hipLaunchKernelGGL(k_init, dim3(std::max(grid, 1)), dim3(256), 0, c.st, a);
 }
@@ -589,6 +605,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_NAMES);
   launch_names(c);
   launch_names_reduce(c);
+  launch_opnames(c);
   stage_end(c, HERSCHEL_STAGE_NAMES);
   rec(4, c.st);
 

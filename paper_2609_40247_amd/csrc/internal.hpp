@@ -135,6 +135,8 @@ struct Ctx {
   uint8_t* crit_hasnext = nullptr;   // [n] by containment position (zeroed)
   uint64_t* crit_zmax = nullptr;     // [P] (zeroed)
   uint32_t* crit_zrow1 = nullptr;    // [P] (zeroed)
+  uint64_t* opn_part = nullptr;      // [opn_blocks * NOP * 4] per-block op-name tables
+  int opn_blocks = 0;
   uint64_t* graph_part = nullptr;    // [graph_blocks * NG * 5] per-block graph-node tables
   int graph_blocks = 0;
   char* zero_begin = nullptr;        // region cleared at the start of a call
@@ -159,6 +161,9 @@ void launch_contain(Ctx& c);
 void launch_depth(Ctx& c);
 void launch_opagg(Ctx& c);
 void launch_names_reduce(Ctx& c);
+void launch_opnames(Ctx& c);
+bool opnames_use_tables(int NOP);
+int opnames_block_count(int64_t n_max, int NOP);
 void launch_join_table(Ctx& c);
 void launch_edges(Ctx& c);
 void launch_finalize(Ctx& c);

@@ -201,6 +201,168 @@ void launch_names_reduce(Ctx& c) {
                      a);
 }
 
+// ---------------------------------------------------------------- op names
+// The same reductions per op name over the admitted CPU ops (the per-op-name
+// variant), from the containment list (prep's compacted ops and launches,
+// sorted with containment, in row order without it): a private LDS table per
+// workgroup, written out whole and folded by a second kernel; more op names
+// than the LDS budget go to the outputs by global atomics.
+constexpr int ON_THREADS = 512;
+constexpr int ON_LDS_NAMES = 2048;  // 64 KB of LDS, the default dynamic limit
+constexpr int ON_MAX_BLOCKS = 512;
+constexpr int ON_BATCH = 8;
+
+struct OpNamesArgs {
+  const uint64_t* keys[2];
+  const uint32_t* vals[2];
+  bool sorted;  // the containment list was sorted (its buffer is given by the parity)
+  DevState* ds;
+  const int32_t* name;
+  const int64_t* ts;
+  const int64_t* te;
+  int NOP;
+  bool lds;
+  uint64_t* part;  // [blocks][NOP][4]
+  int blocks;
+  int64_t* out[4];  // count, sum, min, max (each may be NULL)
+};
+
+__global__ __launch_bounds__(ON_THREADS) void k_opnames_partial(OpNamesArgs a) {
+  extern __shared__ unsigned long long otab[];  // [NOP][4]
+  const int tid = threadIdx.x;
+  if (a.lds) {
+    for (int q = tid; q < a.NOP; q += ON_THREADS) {
+      otab[q * 4 + 0] = 0;
+      otab[q * 4 + 1] = 0;
+      otab[q * 4 + 2] = (unsigned long long)I64MAX;
+      otab[q * 4 + 3] = (unsigned long long)I64MIN;
+    }
+    __syncthreads();
+  }
+  const int par = a.sorted ? (int)a.ds->sort_parity[SORT_C] : 0;
+  const uint64_t* keys = a.keys[par];
+  const uint32_t* vals = a.vals[par];
+  const int64_t n = a.ds->nCL;
+  // ON_BATCH entries per thread and round, each round of loads issued
+  // together (positions past the end take the last entry and are skipped)
+  const int64_t stride = (int64_t)gridDim.x * ON_THREADS;
+  for (int64_t i0 = (int64_t)blockIdx.x * ON_THREADS + tid; i0 < n; i0 += ON_BATCH * stride) {
+    uint32_t rr[ON_BATCH];
+    bool op[ON_BATCH];
+#pragma unroll
+    for (int u = 0; u < ON_BATCH; ++u) {
+      const int64_t i = i0 + u * stride;
+      const int64_t ic = i < n ? i : n - 1;
+      op[u] = i < n && (keys[ic] & 1) == 0;
+      rr[u] = vals[ic];
+    }
+    int qq[ON_BATCH];
+    int64_t dd[ON_BATCH];
+#pragma unroll
+    for (int u = 0; u < ON_BATCH; ++u) {
+      qq[u] = a.name[rr[u]];
+      dd[u] = a.te[rr[u]] - a.ts[rr[u]];
+    }
+#pragma unroll
+    for (int u = 0; u < ON_BATCH; ++u) {
+    if (!op[u]) continue;
+    const int q = qq[u];
+    const int64_t d = dd[u];
+    if (a.lds) {
+      atomicAdd(&otab[q * 4 + 0], 1ull);
+      atomicAdd(&otab[q * 4 + 1], (unsigned long long)d);
+      atomicMin((long long*)&otab[q * 4 + 2], (long long)d);
+      atomicMax((long long*)&otab[q * 4 + 3], (long long)d);
+    } else {
+      if (a.out[0]) atomicAdd((unsigned long long*)&a.out[0][q], 1ull);
+      if (a.out[1]) atomicAdd((unsigned long long*)&a.out[1][q], (unsigned long long)d);
+      if (a.out[2]) atomicMin((long long*)&a.out[2][q], (long long)d);
+      if (a.out[3]) atomicMax((long long*)&a.out[3][q], (long long)d);
+    }
+    }
+  }
+  if (!a.lds) return;
+  __syncthreads();
+  uint64_t* o = a.part + (int64_t)blockIdx.x * a.NOP * 4;
+  for (int i = tid; i < a.NOP * 4; i += ON_THREADS) o[i] = otab[i];
+}
+
+// One thread per (op name, statistic) and row of the grid; one atomic each
+// into the outputs, which start as the identities.
+__global__ __launch_bounds__(256) void k_opnames_fold(OpNamesArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t nv = (int64_t)a.NOP * 4;
+  if (t >= nv) return;
+  const int q = (int)(t >> 2), st = (int)(t & 3);
+  int64_t* const dst = a.out[st];
+  if (!dst) return;
+  uint64_t acc = st == 2 ? (uint64_t)I64MAX : st == 3 ? (uint64_t)I64MIN : 0;
+  for (int b0 = blockIdx.y; b0 < a.blocks; b0 += 16 * (int)gridDim.y) {
+    uint64_t v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int b = b0 + i * (int)gridDim.y;
+      v[i] = a.part[(int64_t)(b < a.blocks ? b : blockIdx.y) * nv + t];
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (b0 + i * (int)gridDim.y >= a.blocks) break;
+      if (st < 2)
+        acc += v[i];
+      else if (st == 2)
+        acc = (int64_t)v[i] < (int64_t)acc ? v[i] : acc;
+      else
+        acc = (int64_t)v[i] > (int64_t)acc ? v[i] : acc;
+    }
+  }
+  if (st < 2) {
+    if (acc) atomicAdd((unsigned long long*)&dst[q], (unsigned long long)acc);
+  } else if (st == 2) {
+    if ((int64_t)acc != I64MAX) atomicMin((long long*)&dst[q], (long long)acc);
+  } else if ((int64_t)acc != I64MIN) {
+    atomicMax((long long*)&dst[q], (long long)acc);
+  }
+}
+
+bool opnames_wanted(const Ctx& c) {
+  return c.o.opname_count || c.o.opname_sum || c.o.opname_min || c.o.opname_max;
+}
+bool opnames_use_tables(int NOP) { return NOP <= ON_LDS_NAMES; }
+// one workgroup per 4096 entries, capped at ON_MAX_BLOCKS and so that the
+// per-workgroup tables (NOP * 32 bytes each) stay within 4 MB
+int opnames_block_count(int64_t n_max, int NOP) {
+  const int64_t cap = std::max<int64_t>((int64_t)(4 << 20) / ((int64_t)std::max(NOP, 1) * 32), 1);
+  return (int)std::min<int64_t>({std::max<int64_t>(cdiv(n_max, 4096), 1), (int64_t)ON_MAX_BLOCKS, cap});
+}
+
+void launch_opnames(Ctx& c) {
+  if (!opnames_wanted(c)) return;
+  OpNamesArgs a;
+  for (int b = 0; b < 2; ++b) {
+    a.keys[b] = c.sC.k[b];
+    a.vals[b] = c.sC.v[b];
+  }
+  a.sorted = c.contain;
+  a.ds = c.ds;
+  a.name = c.ev.name;
+  a.ts = c.ev.ts;
+  a.te = c.ev.te;
+  a.NOP = c.NOP;
+  a.lds = opnames_use_tables(c.NOP);
+  a.part = c.opn_part;
+  a.blocks = c.opn_blocks;
+  a.out[0] = c.o.opname_count;
+  a.out[1] = c.o.opname_sum;
+  a.out[2] = c.o.opname_min;
+  a.out[3] = c.o.opname_max;
+  hipLaunchKernelGGL(k_opnames_partial, dim3((unsigned)c.opn_blocks), dim3(ON_THREADS),
+                     a.lds ? (size_t)c.NOP * 32 : 0, c.st, a);
+  if (a.lds) {
+    const unsigned gy = (unsigned)std::min(8, c.opn_blocks);
+    hipLaunchKernelGGL(k_opnames_fold, dim3((unsigned)cdiv((int64_t)c.NOP * 4, 256), gy), dim3(256), 0, c.st, a);
+  }
+}
+
 int names_lds_limit() { return NM_LDS_NAMES; }
 
 void names_set_lds_attr() {

@@ -62,7 +62,9 @@ class HerschelOutputs(ctypes.Structure):
                                                                "opn_flops", "opn_bytes", "opn_time", "opn_sol",
                                                                "opn_hot", "crit_time", "crit_flags", "crit_proc",
                                                                "launch_first", "launch_last", "gn_count", "gn_sum",
-                                                               "gn_min", "gn_max", "gn_offset")]
+                                                               "gn_min", "gn_max", "gn_offset", "opname_count",
+                                                               "opname_sum", "opname_min", "opname_max")]
+OPNAME_OUTPUTS = ("opname_count", "opname_sum", "opname_min", "opname_max")
 GRAPH_NODE_OUTPUTS = ("gn_count", "gn_sum", "gn_min", "gn_max", "gn_offset")
 SOL_ROW_OUTPUTS = ("op_mfu", "op_mbu", "op_sol")
 SOL_NAME_OUTPUTS = ("opn_flops", "opn_bytes", "opn_time", "opn_sol", "opn_hot")
@@ -255,6 +257,7 @@ class Analyzer:
             crit_time=z(n, torch.int64), crit_flags=z(n, torch.uint8), crit_proc=z(P * 8, torch.int64),
             launch_first=z(n, torch.int64), launch_last=z(n, torch.int64),
             **{k: z(max(int(params.get("n_graph_nodes", 1)), 1), torch.int64) for k in GRAPH_NODE_OUTPUTS},
+            **{k: z(int(params["n_op_names"]), torch.int64) for k in OPNAME_OUTPUTS},
         )
         self.params = self._params_struct(self.ws.data_ptr(), self.ws_bytes)
         self.outs = HerschelOutputs(gap_capacity=self.gap_capacity,
@@ -293,7 +296,7 @@ class Analyzer:
                                      "crit_flags", "launch_first", "launch_last") + SOL_ROW_OUTPUTS}
         for k in ("busy", "idle", "pair_overlap", "class_busy", "class_overlap", "any_busy", "name_count",
                   "name_sum", "name_min", "name_max", "lat_hist", "dev_idle", "op_span", "op_idle",
-                  "crit_proc") + SOL_NAME_OUTPUTS + GRAPH_NODE_OUTPUTS:
+                  "crit_proc") + SOL_NAME_OUTPUTS + GRAPH_NODE_OUTPUTS + OPNAME_OUTPUTS:
             res[k] = h[k]
         res["edge_wait"] = h["edge_wait"][:self.n_edges]
         res["edge_status"] = h["edge_status"][:self.n_edges]

@@ -35,6 +35,7 @@ def assert_same(got: tuple, want: tuple, params: dict, ctx: str = "") -> None:
         if g["counters"][k] != w["counters"][k]:
             raise AssertionError(f"{ctx}: counter {k}: {g['counters'][k]} != {w['counters'][k]}")
     keys = ["link", "aux", "busy", "idle", "lat_hist", "name_count", "name_sum", "name_min", "name_max",
+            "opname_count", "opname_sum", "opname_min", "opname_max",
             "gap_pid", "gap_stream", "gap_begin", "gap_end", "gap_flags", "edge_wait", "edge_status"]
     if params.get("flags", 3) & 1:
         keys += ["op_nkern", "op_first", "op_last", "op_ksum"]

@@ -613,7 +613,8 @@ def test_null_outputs(H, which, flags):
 
 
 # --------------------------------------------------------------- batch at full size
-BATCH_OUTPUTS = ("name_count", "name_sum", "name_min", "name_max", "busy", "idle", "gap_pid", "gap_stream",
+BATCH_OUTPUTS = ("name_count", "name_sum", "name_min", "name_max", "opname_count", "opname_sum", "opname_min",
+                 "opname_max", "busy", "idle", "gap_pid", "gap_stream",
                  "gap_begin", "gap_end", "gap_flags", "lat_hist")
 
 
