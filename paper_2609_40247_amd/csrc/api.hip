@@ -2,6 +2,7 @@
 // of the stages on the caller's stream, and the return code.
 #include <string.h>
 
+#include <chrono>
 #include <cstdio>
 #include <mutex>
 
@@ -357,12 +358,14 @@ __global__ __launch_bounds__(256) void k_nocontain(const uint64_t* keys, const u
 }
 
 __global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counters* cnt, int64_t* lat_hist,
-                                                  const int64_t* busy, int64_t* idle, int nps, int64_t W) {
+                                                  const int64_t* busy, int64_t* idle, int nps, int64_t W,
+                                                  Mailbox* mb, int64_t seq) {
   if (idle)
     for (int i = threadIdx.x; i < nps; i += 256) idle[i] = W - busy[i];
   // join counts and latency bins from their accumulator copies
   if (threadIdx.x < JC_N + 64) {
     unsigned long long v = 0;
+#pragma unroll
     for (int k = 0; k < JOIN_COPIES; ++k) v += ds->join_acc[k][threadIdx.x];
     if (threadIdx.x >= JC_N) {
       if (v && lat_hist) lat_hist[threadIdx.x - JC_N] += (int64_t)v;
@@ -387,11 +390,22 @@ __global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counter
     cnt->first_invalid = ds->first_invalid == I64MAX ? -1 : ds->first_invalid;
     cnt->device_status = ds->status;
   }
+  if (!mb) return;
+  // the counters to the calling thread's mailbox, then the sequence number
+  // with a release at system scope: the host that reads the number reads
+  // this call's counters
+  __syncthreads();
+  if (threadIdx.x < (int)(sizeof(herschel_counters) / 8)) {
+    const int64_t v = ((const int64_t*)cnt)[threadIdx.x];
+    __hip_atomic_store(&mb->c[threadIdx.x], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_store(&mb->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 void launch_finalize(Ctx& c) {
   hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, c.st, c.ds, c.o.counters, c.o.lat_hist,
-                     c.o.busy ? c.o.busy : c.busy_ws, c.o.idle, c.P * c.S, c.W);
+                     c.o.busy ? c.o.busy : c.busy_ws, c.o.idle, c.P * c.S, c.W, c.mailbox, c.mailbox_seq);
 }
 
 // ------------------------------------------------------------- the call
@@ -793,6 +807,57 @@ static void* static_scratch() {
   return g_scratch_ptr[dev];
 }
 
+// ------------------------------------------------------- completion
+// A call's end reaches the host through a mailbox in pinned host memory
+// (one per calling thread and device, allocated on the thread's first call
+// on the device and held until the process ends): the finalize kernel
+// copies the counters into it and then stores the call's sequence number.
+// The thread spins on that number, about 15 us sooner per call than a copy
+// of the counters back and a stream synchronisation.  It asks the stream
+// for errors every 100 us and blocks in hipStreamSynchronize after 2 ms (a
+// long call gains nothing from spinning).
+static thread_local Mailbox* tl_mailbox[64];
+static thread_local int64_t tl_mailbox_seq = 0;
+constexpr int MAILBOX_MISSED = -1000;  // the stream ended without the number: copy back instead
+
+static Mailbox* thread_mailbox() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  if (!tl_mailbox[dev]) {
+    void* m = nullptr;
+    if (hipHostMalloc(&m, sizeof(Mailbox), hipHostMallocCoherent) != hipSuccess || !m) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    memset(m, 0, sizeof(Mailbox));
+    tl_mailbox[dev] = (Mailbox*)m;
+  }
+  return tl_mailbox[dev];
+}
+
+static int wait_mailbox(hipStream_t st, Mailbox* mb, int64_t seq, herschel_counters* h) {
+  using clk = std::chrono::steady_clock;
+  const clk::time_point t0 = clk::now();
+  clk::time_point next_query = t0 + std::chrono::microseconds(100);
+  while (__atomic_load_n(&mb->seq, __ATOMIC_ACQUIRE) != seq) {
+    const clk::time_point t = clk::now();
+    if (t >= next_query) {
+      hipError_t e = hipStreamQuery(st);
+      if (e == hipErrorNotReady && t - t0 > std::chrono::milliseconds(2)) e = hipStreamSynchronize(st);
+      if (e == hipSuccess) {
+        if (__atomic_load_n(&mb->seq, __ATOMIC_ACQUIRE) == seq) break;
+        return MAILBOX_MISSED;
+      }
+      if (e != hipErrorNotReady) return HERSCHEL_EDEVICE;
+      next_query = t + std::chrono::microseconds(100);
+    }
+    __builtin_ia32_pause();
+  }
+  int64_t* dst = (int64_t*)h;
+  for (int i = 0; i < (int)(sizeof(herschel_counters) / 8); ++i) dst[i] = __atomic_load_n(&mb->c[i], __ATOMIC_RELAXED);
+  return HERSCHEL_OK;
+}
+
 static int code_from(const herschel_counters& h, int64_t gap_capacity) {
   if (h.device_status & DS_PARAM) return HERSCHEL_EINVAL;
   if (h.first_invalid >= 0) return HERSCHEL_EEVENT;
@@ -925,9 +990,21 @@ int herschel_trace_analyze(const herschel_events* ev, int64_t n, const herschel_
   Ctx c;
   int code = prepare(c, ev, n, p, out, p ? p->workspace : nullptr, p ? p->workspace_bytes : 0);
   if (code) return code;
+  // a call that launches its kernels directly reports its counters through
+  // the calling thread's mailbox (a replayed graph keeps the arguments it
+  // was captured with, so it copies them back)
+  if (!(c.p.flags & HERSCHEL_REPLAY)) {
+    c.mailbox = thread_mailbox();
+    c.mailbox_seq = c.mailbox ? ++tl_mailbox_seq : 0;
+  }
   code = enqueue_cached(c, ev, n, p, out);
   if (code) return code;
   herschel_counters h;
+  if (c.mailbox) {
+    code = wait_mailbox(c.st, c.mailbox, c.mailbox_seq, &h);
+    if (code == HERSCHEL_OK) return code_from(h, out->gap_capacity);
+    if (code != MAILBOX_MISSED) return code;
+  }
   if (hipMemcpyAsync(&h, out->counters, sizeof(h), hipMemcpyDeviceToHost, c.st) != hipSuccess) return HERSCHEL_EDEVICE;
   if (hipStreamSynchronize(c.st) != hipSuccess) return HERSCHEL_EDEVICE;
   return code_from(h, out->gap_capacity);

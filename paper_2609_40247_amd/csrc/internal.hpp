@@ -44,8 +44,17 @@ inline void sort_digits(int key_bits, bool refine, int* nd, int* first, int* sh1
   }
 }
 
+// Pinned host memory that the finalize kernel copies the counters into, with
+// a sequence number written last (one per calling thread and device).
+struct Mailbox {
+  int64_t c[sizeof(herschel_counters) / 8];
+  int64_t seq;
+};
+
 struct Ctx {
   hipStream_t st = nullptr;
+  Mailbox* mailbox = nullptr;  // NULL: the caller copies the counters back itself
+  int64_t mailbox_seq = 0;
   herschel_events ev{};
   int64_t n = 0;
   herschel_params p{};

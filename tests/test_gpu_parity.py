@@ -452,6 +452,52 @@ def test_batch_matches_single_calls(H):
         assert_same((0, a.results(t.n)), o, t.params, t.label)
 
 
+def test_calls_from_several_threads(H):
+    """Four host threads call at once, each on its own stream with its own
+    workspace and outputs, alternating a valid trace and the same trace with
+    an invalid row: every call returns its own status and first invalid row
+    (each thread's calls report through that thread's completion mailbox),
+    and every valid call matches the oracle."""
+    import threading
+    traces = [synth.config0(seed=s) for s in range(4)]
+    expect = [oracle.analyze(t.columns(), t.params) for t in traces]
+    bad_rows = [101 + 37 * i for i in range(4)]
+    errors = []
+
+    def work(i):
+        try:
+            t = traces[i]
+            st = torch.cuda.Stream()
+            with torch.cuda.stream(st):
+                an = H.Analyzer(t.params, t.n, gap_capacity=expect[i][1]["counters"]["n_gaps_total"] + 8, stream=st)
+                good = H.device_columns(t.columns())
+                bc = {k: v.copy() for k, v in t.columns().items()}
+                bc["kind"][bad_rows[i]] = 7
+                bad = H.device_columns(bc)
+                for rep in range(6):
+                    if rep % 2:
+                        code = an.run(H.events_struct(bad), t.n)
+                        st.synchronize()
+                        c = an.results(t.n)["counters"]
+                        assert code == -2 and c["first_invalid"] == bad_rows[i], (i, rep, code)
+                    else:
+                        an.prefill()
+                        code = an.run(H.events_struct(good), t.n)
+                        st.synchronize()
+                        o = oracle.analyze(t.columns(), t.params, gap_capacity=an.gap_capacity)
+                        assert_same((code, an.results(t.n)), o, t.params, f"thread {i} call {rep}")
+        except BaseException as e:  # reported by the main thread
+            errors.append((i, e))
+
+    ths = [threading.Thread(target=work, args=(i,)) for i in range(4)]
+    for th in ths:
+        th.start()
+    for th in ths:
+        th.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+
+
 # --------------------------------------------------------------- bounds-checked build
 @pytest.mark.parametrize("case", ["config0", "medium", "sparse", "config1_short"])
 def test_checked_library(H, case):
