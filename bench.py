@@ -407,6 +407,7 @@ def main() -> int:
             for _ in range(5):
                 H.herschel_time_stage(sid, e0, e1)
                 an.run(ev, n)
+                torch.cuda.synchronize()  # the call returns before HIP marks its events complete
                 tot += e0.elapsed_time(e1)
             H.herschel_time_stage(sid, None, None)
             print(f"stage {name:14s} {tot / 5 * 1e3:9.1f} us", file=sys.stderr)

@@ -277,7 +277,14 @@ int herschel_workspace_size(int64_t n, const herschel_params *p, size_t *bytes);
  * HERSCHEL_* code.  On EEVENT only counters->first_invalid is defined.
  * The work is ordered on p->hip_stream (it also runs on two library
  * streams that wait for, and are waited on by, that stream); the call
- * returns after synchronising with it.  With HERSCHEL_REPLAY in
+ * returns once the device has finished all of it.  A call that launches
+ * its kernels directly learns that from pinned host memory that its last
+ * kernel writes (one small block per calling thread and device, allocated
+ * on the thread's first call and held until the process ends), so HIP may
+ * report the stream's last commands, and events recorded among them, as
+ * pending for a few microseconds more: synchronise the stream before
+ * querying such events.  A replayed call synchronises with the stream.
+ * With HERSCHEL_REPLAY in
  * params->flags, a call whose event columns, n, parameters (all but
  * hip_stream) and output pointers equal those of one of the last four such
  * argument sets captured on the device replays that call's captured HIP

@@ -55,7 +55,7 @@ constexpr int PREP_LISTS = 4;  // timeline, containment, join, op names
 // Rows are loaded PREP_BATCH per thread at a time, every column of every row
 // of a batch in flight together: no load waits for another (the correlation
 // id is loaded for every kind, the clock offsets are read from LDS).
-constexpr int PREP_BATCH = 4;
+constexpr int PREP_BATCH = 2;
 constexpr int PREP_OFF_LDS = 512;  // processes whose clock offsets are staged in LDS
 // the four list flags of every item are packed into one 32-bit word
 static_assert(PREP_LISTS * PREP_ITEMS <= 32, "list flags of all items must fit the 32-bit flag word");
