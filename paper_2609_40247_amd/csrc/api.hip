@@ -3,6 +3,7 @@
 #include <string.h>
 
 #include <chrono>
+#include <cstddef>
 #include <cstdio>
 #include <mutex>
 
@@ -109,9 +110,6 @@ size_t layout_workspace(Ctx& c, char* base) {
     s->status0 = b.take<uint32_t>(s->tiles_max * RS_LB_WORDS);
     s->status1 = b.take<uint32_t>((int64_t)std::max(s->nd - 1, 1) * s->tiles_max * RS_LB_WORDS);
   }
-  // long runs of the refine pass (each has more than RF_SHORT keys)
-  c.rf_cap = cdiv(n, RF_SHORT + 1) + 1;
-  c.rf_list = b.take<int32_t>(N_SORTS * c.rf_cap);
   c.hist_part = b.take<uint32_t>((int64_t)N_SORTS * HIST_MAX_BLOCKS * 8 * 256);
   c.k_rows = b.take<uint32_t>(n);
   // the join: prep's list, the correlation table (two slots per row bound
@@ -240,14 +238,35 @@ struct InitArgs {
   int64_t* op_idle;
 };
 
+// The device state is cleared up to its digit offsets (the plan kernel
+// writes those whole, after this; the last 16-byte word may reach into
+// them), 16 bytes a thread over the grid; the word of the smallest invalid
+// row starts at INT64_MAX.  The status word lies in the first workgroup's
+// share, so its parameter check follows the clearing.
+constexpr int64_t DS_CLEAR = ((int64_t)offsetof(DevState, hist) + 15) / 16;
+constexpr int64_t DS_FI = (int64_t)offsetof(DevState, first_invalid);
+static_assert(DS_CLEAR * 16 <= (int64_t)sizeof(DevState) && DS_FI % 8 == 0, "16-byte clearing of the device state");
+static_assert(alignof(DevState) >= 8, "the device state starts the 256-byte aligned workspace");
+static_assert(offsetof(DevState, status) < 256 * 16, "the status word is cleared by the first workgroup");
+
 __global__ __launch_bounds__(256) void k_init(InitArgs a) {
   const int64_t tid = (int64_t)blockIdx.x * 256 + threadIdx.x, nth = (int64_t)gridDim.x * 256;
   for (int64_t i = tid; i < a.zero_n; i += nth) a.zero[i] = make_uint4(0, 0, 0, 0);
+  for (int64_t i = tid; i < DS_CLEAR; i += nth) {
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (i == DS_FI / 16) {
+      if (DS_FI % 16 == 0) {
+        v.x = 0xffffffffu;
+        v.y = 0x7fffffffu;
+      } else {
+        v.z = 0xffffffffu;
+        v.w = 0x7fffffffu;
+      }
+    }
+    reinterpret_cast<uint4*>(a.ds)[i] = v;
+  }
   if (blockIdx.x == 0) {
-    uint32_t* d = (uint32_t*)a.ds;
-    for (int i = threadIdx.x; i < (int)(sizeof(DevState) / 4); i += 256) d[i] = 0;
     __syncthreads();
-    if (threadIdx.x == 0) a.ds->first_invalid = I64MAX;
     int64_t* cz = (int64_t*)a.cnt;
     for (int i = threadIdx.x; i < (int)(sizeof(herschel_counters) / 8); i += 256) cz[i] = 0;
     if (a.lat_hist && threadIdx.x < 64) a.lat_hist[threadIdx.x] = 0;
@@ -340,8 +359,8 @@ void launch_init(Ctx& c) {
   a.op_idle = c.o.op_idle;
   const int64_t work =
       std::max<int64_t>({a.zero_n, (int64_t)a.nps * (c.overlap ? c.S : 1), (int64_t)c.NN, a.n_opn, a.n_gn,
-                         (int64_t)c.NOP, 1});
-  const int grid = (int)std::min<int64_t>(cdiv(work, 256 * 4), 2048);
+                         (int64_t)c.NOP, DS_CLEAR, 1});
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(work, 256 * 2), 8), 2048);
   hipLaunchKernelGGL(k_init, dim3(std::max(grid, 1)), dim3(256), 0, c.st, a);
 }
 

@@ -25,7 +25,6 @@ enum : uint32_t {
   DS_SPIN = 1u,      // a look-back wait exceeded its bound
   DS_OOB = 2u,       // checked build: an index left its buffer
   DS_PARAM = 4u,     // clock_offset or stream_class out of range
-  DS_TIES = 8u,      // more long runs of equal keys than the refine list holds
   DS_CAPACITY = 16u, // an internal list overflowed its bound
   DS_LOGIC = 32u     // an internal consistency check failed
 };
@@ -71,7 +70,6 @@ struct DevState {
   int32_t nCL;  // admitted ops + launches (containment list)
   int32_t nJ;   // admitted launches + kernels (join list)
   int32_t nEv;  // overlap events (2 per coverage run)
-  int32_t n_long[N_SORTS];  // long runs listed by the refine pass, per sort
   int32_t nO;          // admitted CPU ops (op-name list, idle coincidence)
   int32_t nOev;        // op-name run endpoints
   int64_t nDgap;       // device idle intervals

@@ -120,8 +120,6 @@ struct Ctx {
   int nlev = 0;
   uint64_t* pmt = nullptr;           // [vb_tiles] exclusive prefix max before each tile
   int32_t* par = nullptr;            // [n] answer position per sorted position
-  int32_t* rf_list = nullptr;        // [2][rf_cap] long runs found by the refine pass
-  int64_t rf_cap = 0;
   int64_t* lk_first = nullptr;       // [n] per launch row: first start of its kernels
   int64_t* lk_last = nullptr;        // [n] last end of its kernels
   int64_t* lk_sum = nullptr;         // [n] sum of its kernels' durations

@@ -704,8 +704,7 @@ void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
 // rule that nests an op that starts with its parent inside it).  The
 // containment list is refined even when every digit was sorted (runs of
 // equal keys, shift 0), for that tie rule.  Runs up to RF_SHORT are ordered
-// by one thread; longer runs are listed and each is sorted by one
-// workgroup.
+// by one thread; the workgroup that finds a longer run sorts it.
 struct RefineJob {
   uint64_t* k[2];
   uint32_t* v[2];
@@ -718,8 +717,6 @@ struct RefineJob {
 struct RefineJobs {
   RefineJob j[N_SORTS];
   const int64_t* te;
-  int32_t* list;  // [2][cap]
-  int64_t cap;
 };
 
 // a before b in the refined order (a and b from one run)
@@ -738,18 +735,77 @@ constexpr int RF_ITEMS = 4;
 constexpr int RF_TILE = RF_THREADS * RF_ITEMS;  // positions whose runs a workgroup orders
 constexpr int RF_SPAN = 1 + RF_TILE + RF_SHORT;  // the position before the tile, the tile, and its runs' reach
 
+// One long run (more than RF_SHORT keys, starting at position p), sorted by
+// the whole workgroup: the run is copied into the sort's other buffer (free
+// once the passes are done) at the same positions, sorted there by a
+// bitonic network that only compares pairs inside the run (the positions
+// past its end act as +infinity, and every comparator puts the smaller
+// element first), and copied back.  Only the high part of the run's keys
+// (above the shift) is read by other workgroups meanwhile, and it is the
+// same for every key of the run.
+__device__ void refine_long_run(const RefineJob& jb, const int64_t* te, uint64_t* keys, uint32_t* vals, uint64_t* sk,
+                                uint32_t* sv, int64_t p, int64_t n, int64_t* s_len) {
+  const uint64_t hi = keys[p] >> jb.shift;
+  if (threadIdx.x == 0) *s_len = n - p;
+  __syncthreads();
+  // the run's end: the first position past it, found RF_THREADS at a time
+  for (int64_t b = p; b < n; b += RF_THREADS) {
+    const int64_t i = b + threadIdx.x;
+    if (i < n && (keys[i] >> jb.shift) != hi) atomicMin((unsigned long long*)s_len, (unsigned long long)(i - p));
+    __syncthreads();
+    if (*s_len < n - p) break;
+    __syncthreads();
+  }
+  const int64_t len = *s_len;
+  for (int64_t i = threadIdx.x; i < len; i += RF_THREADS) {
+    sk[p + i] = keys[p + i];
+    sv[p + i] = vals[p + i];
+  }
+  __syncthreads();
+  int64_t m = 1;
+  while (m < len) m <<= 1;
+  for (int64_t size = 2; size <= m; size <<= 1) {
+    for (int64_t stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int64_t i = threadIdx.x; i < len; i += RF_THREADS) {
+        // first step of a merge: the mirror in the block; then halvings
+        const int64_t l = stride == (size >> 1) ? (i ^ (size - 1)) : (i ^ stride);
+        if (l > i && l < len) {
+          const uint64_t ki = sk[p + i], kl = sk[p + l];
+          const uint32_t ri = sv[p + i], rl = sv[p + l];
+          if (rf_before(jb, te, kl, rl, ki, ri)) {
+            sk[p + i] = kl;
+            sv[p + i] = rl;
+            sk[p + l] = ki;
+            sv[p + l] = ri;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int64_t i = threadIdx.x; i < len; i += RF_THREADS) {
+    keys[p + i] = sk[p + i];
+    vals[p + i] = sv[p + i];
+  }
+  __syncthreads();
+}
+
 // A workgroup stages its tile's keys and rows in LDS (coalesced), with the
 // position before the tile and the RF_SHORT after it, and finds the tile's
 // run starts there.  A thread per run orders it in LDS (insertion sort:
 // the runs are short, and many are in order already) and marks the
 // positions that moved; the workgroup then writes those back, coalesced.
-// A run longer than RF_SHORT is listed instead.
+// A run longer than RF_SHORT (rare) is noted, and the workgroup sorts it
+// afterwards in the sort's other buffer.
 __global__ __launch_bounds__(RF_THREADS) void k_refine(RefineJobs jobs, DevState* ds) {
   __shared__ uint64_t s_k[RF_SPAN];
   __shared__ uint32_t s_v[RF_SPAN];
   __shared__ uint8_t s_chg[RF_SPAN];       // 1: the position moved
   __shared__ int32_t s_run[RF_TILE / 2];  // span indices of the tile's run starts (a run has two keys or more)
   __shared__ int s_nrun;
+  __shared__ int64_t s_long[RF_TILE / (RF_SHORT + 1) + 1];  // positions of the tile's long runs
+  __shared__ int s_nlong;
+  __shared__ int64_t s_len;
   const RefineJob& jb = jobs.j[blockIdx.y];
   const int64_t n = *jb.count;
   const int64_t t0 = (int64_t)blockIdx.x * RF_TILE;
@@ -757,7 +813,10 @@ __global__ __launch_bounds__(RF_THREADS) void k_refine(RefineJobs jobs, DevState
   const int par = (int)ds->sort_parity[jb.id];
   uint64_t* keys = jb.k[par];
   uint32_t* vals = jb.v[par];
-  if (threadIdx.x == 0) s_nrun = 0;
+  if (threadIdx.x == 0) {
+    s_nrun = 0;
+    s_nlong = 0;
+  }
   // span index i holds position t0 - 1 + i (clamped to the list); the
   // loads are issued together (the span's last few are loaded twice)
   constexpr int RF_LD = (RF_SPAN + RF_THREADS - 1) / RF_THREADS;
@@ -804,9 +863,8 @@ __global__ __launch_bounds__(RF_THREADS) void k_refine(RefineJobs jobs, DevState
     int len = 2;
     while (i + len < RF_SPAN && p + len < n && (s_k[i + len] >> sh) == hk) ++len;
     if (len > RF_SHORT || (i + len == RF_SPAN && p + len < n)) {
-      const int at = atomicAdd(&ds->n_long[jb.slot], 1);
-      if (at < jobs.cap) jobs.list[(int64_t)jb.slot * jobs.cap + at] = (int32_t)p;
-      else set_status(ds, DS_TIES);
+      const int at = atomicAdd(&s_nlong, 1);
+      if (in_bounds(ds, at, RF_TILE / (RF_SHORT + 1) + 1)) s_long[at] = p;
       continue;
     }
     // insertion sort in LDS; `lo` is the first position that moved
@@ -837,70 +895,9 @@ __global__ __launch_bounds__(RF_THREADS) void k_refine(RefineJobs jobs, DevState
       vals[t0 - 1 + i] = s_v[i];
     }
   }
-}
-
-// One workgroup per long run: the run is copied into the sort's other
-// buffer (free once the passes are done) at the same positions, sorted there
-// by a bitonic network that only compares pairs inside the run (the
-// positions past its end act as +infinity, and every comparator puts the
-// smaller element first), and copied back.
-__global__ __launch_bounds__(256) void k_refine_long(RefineJobs jobs, DevState* ds) {
-  const RefineJob& jb = jobs.j[blockIdx.y];
-  const int64_t nl = min((int64_t)ds->n_long[jb.slot], jobs.cap);
-  if (nl == 0) return;
-  const int64_t n = *jb.count;
-  const int par = (int)ds->sort_parity[jb.id];
-  uint64_t* keys = jb.k[par];
-  uint32_t* vals = jb.v[par];
-  uint64_t* sk = jb.k[par ^ 1];
-  uint32_t* sv = jb.v[par ^ 1];
-  __shared__ int64_t s_len;
-  for (int64_t q = blockIdx.x; q < nl; q += gridDim.x) {
-    const int64_t p = jobs.list[(int64_t)jb.slot * jobs.cap + q];
-    const uint64_t hi = keys[p] >> jb.shift;
-    if (threadIdx.x == 0) s_len = n - p;
-    __syncthreads();
-    // the run's end: the first position past it, found 256 at a time
-    for (int64_t b = p; b < n; b += 256) {
-      const int64_t i = b + threadIdx.x;
-      if (i < n && (keys[i] >> jb.shift) != hi) atomicMin((unsigned long long*)&s_len, (unsigned long long)(i - p));
-      __syncthreads();
-      if (s_len < n - p) break;
-      __syncthreads();
-    }
-    const int64_t len = s_len;
-    for (int64_t i = threadIdx.x; i < len; i += 256) {
-      sk[p + i] = keys[p + i];
-      sv[p + i] = vals[p + i];
-    }
-    __syncthreads();
-    int64_t m = 1;
-    while (m < len) m <<= 1;
-    for (int64_t size = 2; size <= m; size <<= 1) {
-      for (int64_t stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int64_t i = threadIdx.x; i < len; i += 256) {
-          // first step of a merge: the mirror in the block; then halvings
-          const int64_t l = stride == (size >> 1) ? (i ^ (size - 1)) : (i ^ stride);
-          if (l > i && l < len) {
-            const uint64_t ki = sk[p + i], kl = sk[p + l];
-            const uint32_t ri = sv[p + i], rl = sv[p + l];
-            if (rf_before(jb, jobs.te, kl, rl, ki, ri)) {
-              sk[p + i] = kl;
-              sv[p + i] = rl;
-              sk[p + l] = ki;
-              sv[p + l] = ri;
-            }
-          }
-        }
-        __syncthreads();
-      }
-    }
-    for (int64_t i = threadIdx.x; i < len; i += 256) {
-      keys[p + i] = sk[p + i];
-      vals[p + i] = sv[p + i];
-    }
-    __syncthreads();
-  }
+  const int nlong = min(s_nlong, RF_TILE / (RF_SHORT + 1) + 1);
+  for (int q = 0; q < nlong; ++q)
+    refine_long_run(jb, jobs.te, keys, vals, jb.k[par ^ 1], jb.v[par ^ 1], s_long[q], n, &s_len);
 }
 
 void launch_refine(Ctx& c) {
@@ -924,11 +921,8 @@ void launch_refine(Ctx& c) {
   }
   if (m == 0) return;
   jobs.te = c.ev.te;
-  jobs.list = c.rf_list;
-  jobs.cap = c.rf_cap;
   const int64_t grid = cdiv(n_max, RF_TILE);
   hipLaunchKernelGGL(k_refine, dim3((unsigned)grid, (unsigned)m), dim3(RF_THREADS), 0, c.st, jobs, c.ds);
-  hipLaunchKernelGGL(k_refine_long, dim3(64, (unsigned)m), dim3(256), 0, c.st, jobs, c.ds);
 }
 
 }  // namespace hx
