@@ -116,7 +116,7 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
 // (consecutive threads read consecutive words), 16 in flight, and combines
 // its result into the output with one atomic (the outputs start as the
 // identities, set by the init kernel).
-constexpr int NR_GROUPS = 8;
+constexpr int NR_GROUPS = 16;
 
 __global__ __launch_bounds__(256) void k_names_reduce(NamesArgs a) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -358,7 +358,7 @@ void launch_opnames(Ctx& c) {
   hipLaunchKernelGGL(k_opnames_partial, dim3((unsigned)c.opn_blocks), dim3(ON_THREADS),
                      a.lds ? (size_t)c.NOP * 32 : 0, c.st, a);
   if (a.lds) {
-    const unsigned gy = (unsigned)std::min(8, c.opn_blocks);
+    const unsigned gy = (unsigned)std::min(32, c.opn_blocks);  // 16 tables or fewer per thread: one round of loads
     hipLaunchKernelGGL(k_opnames_fold, dim3((unsigned)cdiv((int64_t)c.NOP * 4, 256), gy), dim3(256), 0, c.st, a);
   }
 }
