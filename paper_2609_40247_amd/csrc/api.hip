@@ -632,13 +632,17 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   launch_edges(c);
   stage_end(c, HERSCHEL_STAGE_EDGES);
   rec(2, c.st);
-  // the name pass also gives each kernel its launch's op: after the join
-  // and after the launches' ops are known
-  if (c.contain) wait(c.st, 3);
+  // the per-name tables need neither the join nor containment; each kernel
+  // takes its launch's op once the containment query has given launches
+  // their ops
   stage_begin(c, HERSCHEL_STAGE_NAMES);
   launch_names(c);
   launch_names_reduce(c);
   launch_opnames(c);
+  if (c.contain) {
+    wait(c.st, 3);
+    launch_kernel_ops(c);
+  }
   stage_end(c, HERSCHEL_STAGE_NAMES);
   rec(4, c.st);
 

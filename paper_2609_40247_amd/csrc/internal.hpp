@@ -168,6 +168,7 @@ void launch_contain(Ctx& c);
 void launch_depth(Ctx& c);
 void launch_opagg(Ctx& c);
 void launch_names_reduce(Ctx& c);
+void launch_kernel_ops(Ctx& c);
 void launch_opnames(Ctx& c);
 bool opnames_use_tables(int NOP);
 int opnames_block_count(int64_t n_max, int NOP);

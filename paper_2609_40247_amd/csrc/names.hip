@@ -1,9 +1,10 @@
 // Per kernel-name aggregates: count, sum, min and max of the unclipped
 // kernel duration over all admitted kernels (Section 6.1 measures kernel
 // durations; grouping by kernel name is the per-name view of the same
-// records).  With containment the same pass over the kernels also gives each
-// matched kernel the op of its launch (kernel composition, Section 6.1) and
-// counts the matched kernels whose launch has no op.
+// records).  With containment a separate pass gives each matched kernel the
+// op of its launch (kernel composition, Section 6.1) and counts the matched
+// kernels whose launch has no op: it needs the launches' ops, the tables do
+// not, so the tables are built while the containment query still runs.
 //
 // Each workgroup keeps a private table of all names in LDS (32 bytes per
 // name) while it streams a slice of the admitted kernels, then writes the
@@ -32,9 +33,8 @@ struct NamesArgs {
   int64_t* sum;
   int64_t* mn;
   int64_t* mx;
-  // kernel -> op (with containment): the op of the kernel's launch
-  bool kernel_ops;
   bool tables;  // some name output is wanted
+  // kernel -> op (with containment): the op of the kernel's launch
   const int32_t* link;
   int32_t* aux;
 };
@@ -54,7 +54,6 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
   }
   const int64_t n = a.ds->nK;
   const uint32_t* rows = a.rows;
-  uint32_t unattr = 0;  // matched kernels whose launch has no op
   // NM_BATCH kernels per thread and round, each round of loads issued
   // together (positions past the end take the last kernel: clamped, not
   // branched on, and then skipped)
@@ -63,31 +62,18 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
     uint32_t r[NM_BATCH];
 #pragma unroll
     for (int u = 0; u < NM_BATCH; ++u) r[u] = rows[i0 + u * stride < n ? i0 + u * stride : n - 1];
-    int32_t q[NM_BATCH], l[NM_BATCH];
+    int32_t q[NM_BATCH];
     int64_t d[NM_BATCH];
 #pragma unroll
     for (int u = 0; u < NM_BATCH; ++u) {
       const int32_t nm = a.name[r[u]];
       const int64_t e = a.te[r[u]], s = a.ts[r[u]];
-      l[u] = a.kernel_ops ? a.link[r[u]] : -1;
       q[u] = i0 + u * stride < n ? nm : -1;
       d[u] = e - s;
     }
-    if (a.kernel_ops) {
-      // the op of each matched kernel's launch (one more round of gathers)
-      int32_t op[NM_BATCH];
-#pragma unroll
-      for (int u = 0; u < NM_BATCH; ++u) op[u] = a.link[l[u] >= 0 ? l[u] : 0];
-#pragma unroll
-      for (int u = 0; u < NM_BATCH; ++u) {
-        if (q[u] < 0 || l[u] < 0) continue;
-        a.aux[r[u]] = op[u];
-        if (op[u] < 0) ++unattr;
-      }
-    }
 #pragma unroll
     for (int u = 0; u < NM_BATCH; ++u) {
-      if (q[u] < 0 || !a.tables) continue;
+      if (q[u] < 0) continue;
       if (lds) {
         atomicAdd(&tab[q[u] * 4 + 0], 1ull);
         atomicAdd(&tab[q[u] * 4 + 1], (unsigned long long)d[u]);
@@ -101,14 +87,45 @@ __global__ __launch_bounds__(NM_THREADS) void k_names_partial(NamesArgs a) {
       }
     }
   }
-  if (a.kernel_ops) {
-    const uint64_t w = wave_sum_u64(unattr);
-    if (lane_id() == 0 && w) atomicAdd(&a.ds->join_acc[blockIdx.x % JOIN_COPIES][JC_UNATTR], (unsigned long long)w);
-  }
   if (!lds) return;
   __syncthreads();
   uint64_t* out = a.part + (int64_t)blockIdx.x * a.NN * 4;
   for (int i = tid; i < a.NN * 4; i += NM_THREADS) out[i] = tab[i];
+}
+
+// Kernel -> op: each matched kernel takes the op of its launch (the join
+// gave the kernel its launch, the containment query the launch its op;
+// unmatched kernels keep the join's -1).  KO_ITEMS kernels per thread, each
+// round of loads issued together.
+constexpr int KO_THREADS = 256;
+constexpr int KO_ITEMS = 8;
+
+__global__ __launch_bounds__(KO_THREADS) void k_kernel_ops(NamesArgs a) {
+  const int64_t n = a.ds->nK;
+  if (n == 0) return;
+  const int64_t p0 = (int64_t)blockIdx.x * KO_THREADS * KO_ITEMS + threadIdx.x;
+  if (p0 >= n) return;
+  uint32_t r[KO_ITEMS];
+#pragma unroll
+  for (int u = 0; u < KO_ITEMS; ++u) {
+    const int64_t p = p0 + u * KO_THREADS;
+    r[u] = a.rows[p < n ? p : n - 1];
+  }
+  int32_t l[KO_ITEMS];
+#pragma unroll
+  for (int u = 0; u < KO_ITEMS; ++u) l[u] = a.link[r[u]];
+  int32_t op[KO_ITEMS];
+#pragma unroll
+  for (int u = 0; u < KO_ITEMS; ++u) op[u] = a.link[l[u] >= 0 ? l[u] : 0];
+  uint32_t unattr = 0;  // matched kernels whose launch has no op
+#pragma unroll
+  for (int u = 0; u < KO_ITEMS; ++u) {
+    if (p0 + u * KO_THREADS >= n || l[u] < 0) continue;
+    a.aux[r[u]] = op[u];
+    if (op[u] < 0) ++unattr;
+  }
+  const uint64_t w = wave_sum_u64(unattr);
+  if (lane_id() == 0 && w) atomicAdd(&a.ds->join_acc[blockIdx.x % JOIN_COPIES][JC_UNATTR], (unsigned long long)w);
 }
 
 // One thread per (name, statistic) and group of tables: group g folds the
@@ -166,7 +183,6 @@ static NamesArgs names_args(Ctx& c) {
   a.sum = c.o.name_sum;
   a.mn = c.o.name_min;
   a.mx = c.o.name_max;
-  a.kernel_ops = c.contain;
   a.tables = c.o.name_count || c.o.name_sum || c.o.name_min || c.o.name_max;
   a.link = c.o.link;
   a.aux = c.o.aux;
@@ -178,19 +194,23 @@ int names_block_count(int64_t n_max, int NN) {
   return (int)std::min<int64_t>(std::max<int64_t>(cdiv(n_max, 8192), 1), 256);
 }
 
-// Names are wanted, or the pass gives kernels their ops (containment).
-static bool names_needed(const Ctx& c) {
-  return c.contain || c.o.name_count || c.o.name_sum || c.o.name_min || c.o.name_max;
-}
 static bool names_tables(const Ctx& c) {
   return c.o.name_count || c.o.name_sum || c.o.name_min || c.o.name_max;
 }
 
 void launch_names(Ctx& c) {
-  if (!names_needed(c)) return;
+  if (!names_tables(c)) return;
   NamesArgs a = names_args(c);
-  const size_t lds = a.tables && c.NN <= NM_LDS_NAMES ? (size_t)c.NN * 32 : 0;
+  const size_t lds = c.NN <= NM_LDS_NAMES ? (size_t)c.NN * 32 : 0;
   hipLaunchKernelGGL(k_names_partial, dim3(c.name_blocks), dim3(NM_THREADS), lds, c.st, a);
+}
+
+// after the join and the containment query
+void launch_kernel_ops(Ctx& c) {
+  if (!c.contain) return;
+  NamesArgs a = names_args(c);
+  const int64_t grid = std::max<int64_t>(cdiv(c.n, (int64_t)KO_THREADS * KO_ITEMS), 1);
+  hipLaunchKernelGGL(k_kernel_ops, dim3((unsigned)grid), dim3(KO_THREADS), 0, c.st, a);
 }
 
 void launch_names_reduce(Ctx& c) {
