@@ -201,6 +201,62 @@ __device__ __forceinline__ int64_t wave_max_i64(int64_t v) {
   }
   return shfl(v, 0);
 }
+// DPP (data-parallel primitives: a VALU move that reads another lane of the
+// same row) in its GFX9 forms.  A row is 16 lanes: row_shr:d moves lane
+// l - d of the row to lane l; row_bcast:15 carries lane 15 of each row to
+// the next row, row_bcast:31 lane 31 to rows 2 and 3; wave_shr:1 moves lane
+// l - 1 of the wave to lane l.  Lanes outside the row mask, and lanes whose
+// source lies outside the row (or the wave), keep `old`.  No LDS crossbar
+// and no LDS round trip, unlike the shuffles above.  Every lane of the wave
+// must be active.
+constexpr int DPP_ROW_SHR1 = 0x111;
+constexpr int DPP_ROW_SHR2 = 0x112;
+constexpr int DPP_ROW_SHR4 = 0x114;
+constexpr int DPP_ROW_SHR8 = 0x118;
+constexpr int DPP_WAVE_SHR1 = 0x138;
+constexpr int DPP_ROW_BCAST15 = 0x142;
+constexpr int DPP_ROW_BCAST31 = 0x143;
+
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ uint32_t dpp32(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWS, 0xf, false);
+}
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ uint64_t dpp64(uint64_t old, uint64_t v) {
+  return ((uint64_t)dpp32<CTRL, ROWS>((uint32_t)(old >> 32), (uint32_t)(v >> 32)) << 32) |
+         dpp32<CTRL, ROWS>((uint32_t)old, (uint32_t)v);
+}
+// Inclusive prefix maximum over the wave (unsigned, identity 0): doubling
+// shifts inside each row, then each row takes the maxima of the rows
+// before it by the two broadcasts.
+__device__ __forceinline__ uint64_t wave_prefix_max_u64(uint64_t v) {
+  uint64_t o;
+  o = dpp64<DPP_ROW_SHR1>(0ull, v);
+  v = o > v ? o : v;
+  o = dpp64<DPP_ROW_SHR2>(0ull, v);
+  v = o > v ? o : v;
+  o = dpp64<DPP_ROW_SHR4>(0ull, v);
+  v = o > v ? o : v;
+  o = dpp64<DPP_ROW_SHR8>(0ull, v);
+  v = o > v ? o : v;
+  o = dpp64<DPP_ROW_BCAST15, 0xa>(0ull, v);
+  v = o > v ? o : v;
+  o = dpp64<DPP_ROW_BCAST31, 0xc>(0ull, v);
+  v = o > v ? o : v;
+  return v;
+}
+// Lane l takes v of lane l - 1; lane 0 takes `fill`.
+__device__ __forceinline__ uint64_t wave_shift_up1_u64(uint64_t v, uint64_t fill) {
+  return dpp64<DPP_WAVE_SHR1>(fill, v);
+}
+// Maximum over the wave (unsigned), in every lane.
+__device__ __forceinline__ uint64_t wave_allmax_u64(uint64_t v) {
+  v = wave_prefix_max_u64(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, WAVE - 1);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), WAVE - 1);
+  return ((uint64_t)hi << 32) | lo;
+}
+
 // Inclusive prefix sum across the wave.
 __device__ __forceinline__ uint32_t wave_incl_sum_u32(uint32_t v) {
   int l = lane_id();

@@ -140,7 +140,7 @@ __global__ __launch_bounds__(VB_THREADS) void k_vbuild(ContainArgs a) {
       v = (key_seg(a, key[j]) << a.vb) | (uint64_t)(e + 1);
     }
     if (p < n) a.V[p] = v;
-    const uint64_t g = wave_max_u64(v);
+    const uint64_t g = wave_allmax_u64(v);
     if (lane == 0 && p - lane < n) a.M[1][(p - lane) >> 6] = g;
     wmax = g > wmax ? g : wmax;
   }
@@ -289,12 +289,7 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
       if (lane >= (1 << (k - 1))) w = o > w ? o : w;
       s_g[k][lane] = w;
     }
-    uint64_t inc = m1;
-    for (int d = 1; d < WAVE; d <<= 1) {
-      const uint64_t o = shfl_up(inc, d);
-      if (lane >= d) inc = o > inc ? o : inc;
-    }
-    const uint64_t ex = shfl_up(inc, 1);
+    const uint64_t ex = wave_shift_up1_u64(wave_prefix_max_u64(m1), 0ull);
     const uint64_t pt = a.pmt[tile];
     s_gpre[lane] = lane == 0 ? pt : (ex > pt ? ex : pt);
   }
@@ -314,13 +309,7 @@ __global__ __launch_bounds__(QY_THREADS) void k_query(ContainArgs a) {
       w[k] = (lane >= (1 << (k - 1)) && o > w[k - 1]) ? o : w[k - 1];
     }
     // exclusive prefix max inside the group, then the prefix before it
-    uint64_t inc = v;
-    for (int d = 1; d < WAVE; d <<= 1) {
-      const uint64_t o = shfl_up(inc, d);
-      if (lane >= d) inc = o > inc ? o : inc;
-    }
-    uint64_t pm = shfl_up(inc, 1);
-    if (lane == 0) pm = 0ull;
+    uint64_t pm = wave_shift_up1_u64(wave_prefix_max_u64(v), 0ull);
     const uint64_t gp = s_gpre[g];
     pm = pm > gp ? pm : gp;
     const bool want = live && pm > q;
