@@ -519,7 +519,7 @@ static inline void stage_end(Ctx& c, int s) {
 struct DeviceStreams {
   hipStream_t s[2] = {nullptr, nullptr};
   hipStream_t cap = nullptr;  // graphs are captured here (the caller's stream may be the null stream)
-  hipEvent_t e[5] = {};  // sorts, timeline chain, join, launches' ops, name tables
+  hipEvent_t e[6] = {};  // sorts, timeline chain, join, launches' ops, name tables, radix passes
   bool ok = false;
 };
 static std::mutex g_enqueue_mutex;
@@ -604,6 +604,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_SORT);
   launch_sort_multi(c, ss, cc, ks, 0, p_shared);
   stage_end(c, HERSCHEL_STAGE_SORT);
+  rec(5, s0);  // the join reads no sorted list: it starts beside the refine pass
   launch_refine(c);
   rec(0, s0);
 
@@ -624,7 +625,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
 
   // chain 2: the join by the correlation table, then the dependency waits
   c.st = lib1;
-  wait(c.st, 0);
+  wait(c.st, 5);
   stage_begin(c, HERSCHEL_STAGE_JOIN);
   launch_join_table(c);
   stage_end(c, HERSCHEL_STAGE_JOIN);
@@ -638,6 +639,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_NAMES);
   launch_names(c);
   launch_names_reduce(c);
+  wait(c.st, 0);  // the op-name tables read the refined containment list
   launch_opnames(c);
   if (c.contain) {
     wait(c.st, 3);
