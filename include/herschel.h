@@ -329,20 +329,21 @@ const char *herschel_strerror(int code);
 
 /* Diagnostics for benchmarks.  Stages of one analysis call.  INIT, PREP,
  * HIST and SORT (with the refine pass after it) run in this order on
- * params->hip_stream; after SORT the JOIN and EDGES stages run on a library
- * stream, the TIMELINE, OVERLAP and NAMES stages on another, while CONTAIN
- * and OPAGG follow on params->hip_stream; FINAL waits for all of them. */
+ * params->hip_stream; after SORT the JOIN, EDGES and NAMES stages run on a
+ * library stream (JOIN beside the refine pass), the TIMELINE, OVERLAP and
+ * WAITS stages on another after the refine pass, while CONTAIN, OPAGG, SOL,
+ * CRIT and GRAPH follow on params->hip_stream; FINAL waits for all of them. */
 enum {
   HERSCHEL_STAGE_INIT = 0,     /* clear the workspace state and accumulating outputs */
   HERSCHEL_STAGE_PREP = 1,     /* validate, correct, admit, compact (one kernel) */
   HERSCHEL_STAGE_HIST = 2,     /* digit histograms and pass plans of the timeline and containment sorts */
-  HERSCHEL_STAGE_NAMES = 3,    /* per-name partial tables */
+  HERSCHEL_STAGE_NAMES = 3,    /* per-name and per-op-name tables, then kernel -> op */
   HERSCHEL_STAGE_SORT = 4,     /* radix passes shared by the sorts (the timeline and containment digits) */
   HERSCHEL_STAGE_TIMELINE = 5, /* busy/idle, gaps, coverage runs (one kernel) */
   HERSCHEL_STAGE_OVERLAP = 6,  /* co-ranks of the coverage runs and the sweep */
   HERSCHEL_STAGE_CONTAIN = 7,  /* op nesting and launch -> op */
   HERSCHEL_STAGE_JOIN = 8,     /* launch <-> kernel join by correlation table, latency */
-  HERSCHEL_STAGE_OPAGG = 9,    /* kernel -> op, inclusive per-op aggregates */
+  HERSCHEL_STAGE_OPAGG = 9,    /* inclusive per-op aggregates */
   HERSCHEL_STAGE_EDGES = 10,   /* dependency waits */
   HERSCHEL_STAGE_FINAL = 11,   /* counters and histogram totals */
   HERSCHEL_STAGE_WAITS = 12,   /* device-lane and op-name unions, idle coincidence (OUT_WAITS) */
