@@ -376,6 +376,15 @@ __global__ __launch_bounds__(256) void k_nocontain(const uint64_t* keys, const u
   }
 }
 
+// Exits the critical path's walk follows per process before the doubling
+// pass takes over ($HERSCHEL_CRIT_WALK, for tests of that pass; 64 by default).
+static int crit_walk_max() {
+  const char* e = getenv("HERSCHEL_CRIT_WALK");
+  if (!e || !*e) return 64;
+  const long v = strtol(e, nullptr, 10);
+  return v < 0 ? 0 : v > (1L << 20) ? (1 << 20) : (int)v;
+}
+
 __global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counters* cnt, int64_t* lat_hist,
                                                   const int64_t* busy, int64_t* idle, int nps, int64_t W,
                                                   Mailbox* mb, int64_t seq) {
@@ -418,6 +427,8 @@ __global__ __launch_bounds__(256) void k_finalize(DevState* ds, herschel_counter
     const int64_t v = ((const int64_t*)cnt)[threadIdx.x];
     __hip_atomic_store(&mb->c[threadIdx.x], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&mb->crit_more, (int64_t)ds->crit_more, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __syncthreads();
   if (threadIdx.x == 0) __hip_atomic_store(&mb->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
@@ -488,6 +499,7 @@ static int check_and_plan(Ctx& c, const herschel_events* ev, int64_t n, const he
   c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
   c.sol = (p->flags & HERSCHEL_OUT_SOL) != 0;
   c.crit = (p->flags & HERSCHEL_OUT_CRIT) != 0;
+  c.crit_walk_max = crit_walk_max();
   c.graph = (p->flags & HERSCHEL_OUT_GRAPH) != 0;
   c.NG = c.graph ? p->n_graph_nodes : 0;
   c.nob = bits_host((uint64_t)(c.NOP - 1));
@@ -883,6 +895,15 @@ static int wait_mailbox(hipStream_t st, Mailbox* mb, int64_t seq, herschel_count
   return HERSCHEL_OK;
 }
 
+// The critical path's doubling pass when the call left it out and a walk
+// stopped short (DevState::crit_more), on the caller's stream, waited for.
+static int finish_crit(Ctx& c, uint32_t more) {
+  if (!c.crit_deferred || !more) return HERSCHEL_OK;
+  launch_crit_deferred(c);
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(c.st) != hipSuccess) return HERSCHEL_EDEVICE;
+  return HERSCHEL_OK;
+}
+
 static int code_from(const herschel_counters& h, int64_t gap_capacity) {
   if (h.device_status & DS_PARAM) return HERSCHEL_EINVAL;
   if (h.first_invalid >= 0) return HERSCHEL_EEVENT;
@@ -970,6 +991,7 @@ int herschel_workspace_size(int64_t n, const herschel_params* p, size_t* bytes) 
   c.waits = (p->flags & HERSCHEL_OUT_WAITS) != 0;
   c.sol = (p->flags & HERSCHEL_OUT_SOL) != 0;
   c.crit = (p->flags & HERSCHEL_OUT_CRIT) != 0;
+  c.crit_walk_max = crit_walk_max();
   c.graph = (p->flags & HERSCHEL_OUT_GRAPH) != 0;
   if (c.graph && p->n_graph_nodes < 1) return HERSCHEL_EINVAL;
   c.NG = c.graph ? p->n_graph_nodes : 0;
@@ -1022,17 +1044,33 @@ int herschel_trace_analyze(const herschel_events* ev, int64_t n, const herschel_
     c.mailbox = thread_mailbox();
     c.mailbox_seq = c.mailbox ? ++tl_mailbox_seq : 0;
   }
+  // the critical path's doubling pass is needed only when a walk stopped
+  // short: it is enqueued after the call if the call reports so (a replayed
+  // graph keeps it inline)
+  c.crit_deferred = c.crit && !(c.p.flags & HERSCHEL_REPLAY);
   code = enqueue_cached(c, ev, n, p, out);
   if (code) return code;
   herschel_counters h;
+  uint32_t more = 0;
+  bool have = false;
   if (c.mailbox) {
     code = wait_mailbox(c.st, c.mailbox, c.mailbox_seq, &h);
-    if (code == HERSCHEL_OK) return code_from(h, out->gap_capacity);
-    if (code != MAILBOX_MISSED) return code;
+    if (code == HERSCHEL_OK) {
+      have = true;
+      more = __atomic_load_n(&c.mailbox->crit_more, __ATOMIC_RELAXED) != 0;
+    } else if (code != MAILBOX_MISSED) {
+      return code;
+    }
   }
-  if (hipMemcpyAsync(&h, out->counters, sizeof(h), hipMemcpyDeviceToHost, c.st) != hipSuccess) return HERSCHEL_EDEVICE;
-  if (hipStreamSynchronize(c.st) != hipSuccess) return HERSCHEL_EDEVICE;
-  return code_from(h, out->gap_capacity);
+  if (!have) {
+    if (hipMemcpyAsync(&h, out->counters, sizeof(h), hipMemcpyDeviceToHost, c.st) != hipSuccess) return HERSCHEL_EDEVICE;
+    if (c.crit_deferred &&
+        hipMemcpyAsync(&more, &c.ds->crit_more, sizeof(more), hipMemcpyDeviceToHost, c.st) != hipSuccess)
+      return HERSCHEL_EDEVICE;
+    if (hipStreamSynchronize(c.st) != hipSuccess) return HERSCHEL_EDEVICE;
+  }
+  code = finish_crit(c, more);
+  return code ? code : code_from(h, out->gap_capacity);
 }
 
 int herschel_trace_analyze_static(const herschel_events* ev, int64_t n, const herschel_params* p,
@@ -1041,6 +1079,7 @@ int herschel_trace_analyze_static(const herschel_events* ev, int64_t n, const he
   int code = check_and_plan(c, ev, n, p, out);
   if (code) return code;
   if (layout_workspace(c, nullptr) > (size_t)HERSCHEL_STATIC_SCRATCH_BYTES) return HERSCHEL_ETOOBIG;
+  c.crit_deferred = c.crit;  // the critical path's doubling pass only if the call reports it needed
   {
     std::lock_guard<std::mutex> lock(g_enqueue_mutex);
     void* base = static_scratch();
@@ -1056,9 +1095,14 @@ int herschel_trace_analyze_static(const herschel_events* ev, int64_t n, const he
   }
   if (code) return code;
   herschel_counters h;
+  uint32_t more = 0;
   if (hipMemcpyAsync(&h, out->counters, sizeof(h), hipMemcpyDeviceToHost, c.st) != hipSuccess) return HERSCHEL_EDEVICE;
+  if (c.crit_deferred &&
+      hipMemcpyAsync(&more, &c.ds->crit_more, sizeof(more), hipMemcpyDeviceToHost, c.st) != hipSuccess)
+    return HERSCHEL_EDEVICE;
   if (hipStreamSynchronize(c.st) != hipSuccess) return HERSCHEL_EDEVICE;
-  return code_from(h, out->gap_capacity);
+  code = finish_crit(c, more);
+  return code ? code : code_from(h, out->gap_capacity);
 }
 
 int herschel_trace_analyze_batch(const herschel_events* ev, const int64_t* trace_offsets, int32_t n_traces,

@@ -81,6 +81,7 @@ struct DevState {
   int64_t n_gaps;
   uint32_t sort_trivial[N_SORTS];  // bit d: digit d moves no data (every key agrees on it, or it is
                                    // left to the refine pass: then bit 31 is set too)
+  uint32_t crit_more;              // critical path: a walk stopped short, the doubling must finish the path
   uint32_t join_direct;            // 1: dense correlation slots, 0: hashed slots
   uint32_t jt_nfix;                // entries of the join's fix-up list
   int64_t jt_slots;                // table slots in use (dense: the ids' ranges; hashed: the table)

@@ -24,10 +24,18 @@
 // Device form: one pass per list builds every event's release (the host
 // records from the containment order and its answers, the kernels from the
 // timeline order and the join, the synchronizing calls by a binary search
-// in the kernels sorted by (pid, end)); the path is marked by pointer
-// doubling from each process's last event (round r marks the events 2^r
-// steps behind the marked ones while the pointers double), which ends when
-// a round adds nothing; a last pass charges the marked steps.
+// in the kernels sorted by (pid, end)); then the path is marked in two
+// levels.  Event ids are cut into tiles of CP_TE consecutive ids (a tile
+// holds the rows of a few delivery blocks, so most releases stay inside
+// it): a workgroup per tile follows the releases inside its tile in LDS and
+// gives each event its exit, the first event of its release chain outside
+// the tile; one thread per process walks the exits from its last event and
+// marks each one (the entries of the path into tiles); a workgroup per tile
+// that holds a marked entry marks its chain inside the tile.  A path with
+// more than walk_max exits left after the walk is marked by pointer
+// doubling over the exits from the marked ones (round r marks the exits
+// 2^r steps behind while the pointers double, until a round adds nothing),
+// and the tiles are marked again.  A last pass charges the marked steps.
 #include "internal.hpp"
 
 namespace hx {
@@ -81,7 +89,17 @@ struct CritArgs {
   uint8_t* crit_flags;
   int64_t* crit_proc;
   int round;
+  int walk_max;  // exits a process's walk marks before the doubling takes over
+  bool final;    // the path is completely marked when the charging pass runs
 };
+
+// Tiles of event ids for the two-level marking: CP_TE ids per workgroup of
+// CP_LT threads, in LDS.
+constexpr int CP_TE = 8192;
+constexpr int CP_TE_LOG = 13;
+constexpr int CP_LT = 512;
+constexpr int CP_EPT = CP_TE / CP_LT;
+static_assert((1 << CP_TE_LOG) == CP_TE && CP_EPT * CP_LT == CP_TE, "tile of event ids");
 
 __device__ __forceinline__ int64_t cp_off(const CritArgs& a, int32_t p) { return a.off ? a.off[p] : 0; }
 __device__ __forceinline__ int64_t cp_start(const CritArgs& a, uint32_t r) { return a.ts[r] - cp_off(a, a.pid[r]); }
@@ -323,20 +341,131 @@ __global__ __launch_bounds__(256) void k_crit_rows(CritArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void k_crit_seed(CritArgs a) {
-  for (int p = blockIdx.x * 256 + threadIdx.x; p < a.P; p += gridDim.x * 256) {
-    const uint32_t z = a.zrow1[p];
-    if (z) a.mark[2 * (int64_t)(z - 1) + 1] = 1;
+// Each event's exit from its tile (into ptr1): the release of the last
+// event of its release chain inside the tile (-1 where the chain ends in the
+// tile).  In LDS every event points to its release inside the tile, or to
+// itself when the release lies outside it or there is none; pointer jumping
+// takes every event to the end of its chain inside the tile (at most CP_TE
+// events: CP_TE_LOG rounds, fewer when a round changes nothing).
+__global__ __launch_bounds__(CP_LT) void k_crit_local(CritArgs a) {
+  __shared__ int32_t s_j[CP_TE];
+  const int64_t ne = 2 * a.n;
+  const int64_t tb = (int64_t)blockIdx.x * CP_TE;
+  if (tb >= ne) return;
+  const int tn = (int)min((int64_t)CP_TE, ne - tb);
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int k = 0; k < CP_EPT; ++k) {
+    const int i = tid + k * CP_LT;
+    const int64_t y = i < tn ? (int64_t)a.pred[tb + i] : -1;
+    s_j[i] = (y >= tb && y < tb + tn) ? (int)(y - tb) : i;
+  }
+  __syncthreads();
+  for (int r = 0; r < CP_TE_LOG; ++r) {
+    int32_t v[CP_EPT];
+    bool ch = false;
+#pragma unroll
+    for (int k = 0; k < CP_EPT; ++k) {
+      const int t = s_j[tid + k * CP_LT];
+      v[k] = s_j[t];
+      ch |= v[k] != t;
+    }
+    if (!__syncthreads_or(ch)) break;  // (also orders the reads before the writes)
+#pragma unroll
+    for (int k = 0; k < CP_EPT; ++k) s_j[tid + k * CP_LT] = v[k];
+    __syncthreads();
+  }
+#pragma unroll
+  for (int k = 0; k < CP_EPT; ++k) {
+    const int i = tid + k * CP_LT;
+    if (i < tn) a.ptr1[tb + i] = a.pred[tb + s_j[i]];
   }
 }
 
-// One doubling round: every marked event marks the event its pointer names
-// (2^round releases back), and every pointer is replaced by its target's.
-// A round after one that marked nothing does nothing: the path is marked.
+// Each process's path from E of its last-ending record: the exits, walked
+// one after another and marked (they are the path's entries into tiles).
+// After walk_max exits the walk marks where it stands and leaves the rest to
+// the doubling.
+__global__ __launch_bounds__(256) void k_crit_walk(CritArgs a) {
+  const int p = blockIdx.x * 256 + threadIdx.x;
+  if (p >= a.P) return;
+  const uint32_t z = a.zrow1[p];
+  if (!z) return;
+  const int64_t ne = 2 * a.n;
+  int64_t e = 2 * (int64_t)(z - 1) + 1;
+  for (int s = 0; e >= 0 && in_range(a.ds, e, ne); ++s) {
+    a.mark[e] = 1;
+    if (s >= a.walk_max) {
+      atomicOr(&a.ds->crit_more, 1u);
+      break;
+    }
+    e = a.ptr1[e];
+  }
+}
+
+// The path inside each tile that holds a marked event: from every marked
+// event, its release chain inside the tile, by pointer doubling in LDS
+// (round r marks the events 2^r releases behind the marked ones).
+__global__ __launch_bounds__(CP_LT) void k_crit_mark_local(CritArgs a) {
+  __shared__ int32_t s_j[CP_TE];
+  __shared__ uint8_t s_m[CP_TE];
+  const int64_t ne = 2 * a.n;
+  const int64_t tb = (int64_t)blockIdx.x * CP_TE;
+  if (tb >= ne) return;
+  const int tn = (int)min((int64_t)CP_TE, ne - tb);
+  const int tid = threadIdx.x;
+  bool any = false;
+#pragma unroll
+  for (int k = 0; k < CP_EPT; ++k) {
+    const int i = tid + k * CP_LT;
+    const uint8_t m = i < tn ? a.mark[tb + i] : (uint8_t)0;
+    s_m[i] = m;
+    any |= m != 0;
+  }
+  if (!__syncthreads_or(any)) return;  // the path does not pass this tile
+#pragma unroll
+  for (int k = 0; k < CP_EPT; ++k) {
+    const int i = tid + k * CP_LT;
+    const int64_t y = i < tn ? (int64_t)a.pred[tb + i] : -1;
+    s_j[i] = (y >= tb && y < tb + tn) ? (int)(y - tb) : i;
+  }
+  __syncthreads();
+  for (int r = 0; r < CP_TE_LOG; ++r) {
+    int32_t t[CP_EPT], v[CP_EPT];
+    bool m[CP_EPT];
+    bool ch = false;
+#pragma unroll
+    for (int k = 0; k < CP_EPT; ++k) {
+      const int i = tid + k * CP_LT;
+      t[k] = s_j[i];
+      v[k] = s_j[t[k]];
+      m[k] = s_m[i] != 0;
+      ch |= v[k] != t[k] || (m[k] && !s_m[t[k]]);
+    }
+    if (!__syncthreads_or(ch)) break;
+#pragma unroll
+    for (int k = 0; k < CP_EPT; ++k) {
+      if (m[k]) s_m[t[k]] = 1;
+      s_j[tid + k * CP_LT] = v[k];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int k = 0; k < CP_EPT; ++k) {
+    const int i = tid + k * CP_LT;
+    if (i < tn && s_m[i]) a.mark[tb + i] = 1;
+  }
+}
+
+// One doubling round over the exits (only when a walk stopped short): every
+// marked event marks the event its pointer names (2^round exits back), and
+// every pointer is replaced by its target's.  A round after one that marked
+// nothing does nothing: the path's entries are marked.
 __global__ __launch_bounds__(256) void k_crit_round(CritArgs a) {
   const int rd = a.round;
+  if (!a.ds->crit_more) return;
   if (rd > 0 && a.ds->crit_new[rd - 1] == 0) return;
-  const int32_t* in = rd == 0 ? a.pred : (rd & 1) ? a.ptr0 : a.ptr1;
+  const int32_t* in = rd == 0 ? a.ptr1 : (rd & 1) ? a.ptr0 : a.ptr1;
   int32_t* out = (rd & 1) ? a.ptr1 : a.ptr0;
   const int64_t ne = 2 * a.n;
   for (int64_t i0 = (int64_t)blockIdx.x * 256; i0 < ne; i0 += (int64_t)gridDim.x * 256) {  // uniform per workgroup
@@ -364,6 +493,7 @@ __global__ __launch_bounds__(256) void k_crit_round(CritArgs a) {
 // Each of the three outputs may be NULL.
 __global__ __launch_bounds__(256) void k_crit_attr(CritArgs a) {
   __shared__ unsigned long long s_part[CP_LDS_PROCS * CP_PARTS];
+  if (!a.final && a.ds->crit_more) return;  // the doubling comes first
   int64_t* const proc = a.crit_proc;
   const bool lds = proc && a.P <= CP_LDS_PROCS;
   if (lds)
@@ -443,6 +573,8 @@ static CritArgs crit_args(Ctx& c) {
   a.crit_flags = c.o.crit_flags;
   a.crit_proc = c.o.crit_proc;
   a.round = 0;
+  a.walk_max = c.crit_walk_max;
+  a.final = !c.crit_deferred;
   return a;
 }
 
@@ -462,6 +594,22 @@ int crit_rounds(int64_t n) {
   return r;
 }
 
+// The doubling over the exits, the tiles marked again, the charges.
+static void launch_crit_rest(Ctx& c, CritArgs a) {
+  const int rounds = crit_rounds(c.n);
+  for (int rd = 0; rd < rounds; ++rd) {
+    a.round = rd;
+    hipLaunchKernelGGL(k_crit_round, dim3(crit_grid(2 * c.n)), dim3(256), 0, c.st, a);
+  }
+  const unsigned tiles = (unsigned)cdiv(2 * c.n, CP_TE);
+  hipLaunchKernelGGL(k_crit_mark_local, dim3(tiles), dim3(CP_LT), 0, c.st, a);
+  a.final = true;
+  hipLaunchKernelGGL(k_crit_attr, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
+}
+
+// With c.crit_deferred the doubling is left out: the charging pass then
+// does nothing if a walk stopped short (DevState::crit_more), and the caller
+// runs launch_crit_deferred once the call has ended.
 void launch_crit(Ctx& c) {
   if (c.n == 0) return;
   CritArgs a = crit_args(c);
@@ -469,13 +617,21 @@ void launch_crit(Ctx& c) {
   hipLaunchKernelGGL(k_crit_kernels, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
   hipLaunchKernelGGL(k_crit_ops, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
   hipLaunchKernelGGL(k_crit_rows, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_crit_seed, dim3((unsigned)cdiv(c.P, 256)), dim3(256), 0, c.st, a);
-  const int rounds = crit_rounds(c.n);
-  for (int rd = 0; rd < rounds; ++rd) {
-    a.round = rd;
-    hipLaunchKernelGGL(k_crit_round, dim3(crit_grid(2 * c.n)), dim3(256), 0, c.st, a);
+  const unsigned tiles = (unsigned)cdiv(2 * c.n, CP_TE);
+  hipLaunchKernelGGL(k_crit_local, dim3(tiles), dim3(CP_LT), 0, c.st, a);
+  hipLaunchKernelGGL(k_crit_walk, dim3((unsigned)cdiv(c.P, 256)), dim3(256), 0, c.st, a);
+  if (!c.crit_deferred) {
+    launch_crit_rest(c, a);
+    return;
   }
+  hipLaunchKernelGGL(k_crit_mark_local, dim3(tiles), dim3(CP_LT), 0, c.st, a);
   hipLaunchKernelGGL(k_crit_attr, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
+}
+
+void launch_crit_deferred(Ctx& c) {
+  if (c.n == 0) return;
+  CritArgs a = crit_args(c);
+  launch_crit_rest(c, a);
 }
 
 }  // namespace hx

@@ -48,6 +48,7 @@ inline void sort_digits(int key_bits, bool refine, int* nd, int* first, int* sh1
 // a sequence number written last (one per calling thread and device).
 struct Mailbox {
   int64_t c[sizeof(herschel_counters) / 8];
+  int64_t crit_more;  // the critical path needs its doubling pass (DevState::crit_more)
   int64_t seq;
 };
 
@@ -137,7 +138,9 @@ struct Ctx {
   int32_t* crit_pred = nullptr;      // [2n] critical path: each event's release
   uint8_t* crit_code = nullptr;      // [2n] its part and charged record
   uint8_t* crit_mark = nullptr;      // [2n] on the path (zeroed)
-  int32_t* crit_ptr[2] = {nullptr, nullptr};  // [2n] doubling pointers
+  int32_t* crit_ptr[2] = {nullptr, nullptr};  // [2n] exits, then doubling pointers
+  int crit_walk_max = 64;            // exits a process's walk follows before the doubling takes over
+  bool crit_deferred = false;        // the doubling pass, if needed, is enqueued after the call
   uint32_t* crit_lastc1 = nullptr;   // [n] by containment position (zeroed)
   uint8_t* crit_hasnext = nullptr;   // [n] by containment position (zeroed)
   uint64_t* crit_zmax = nullptr;     // [P] (zeroed)
@@ -169,6 +172,7 @@ void launch_depth(Ctx& c);
 void launch_opagg(Ctx& c);
 void launch_names_reduce(Ctx& c);
 void launch_kernel_ops(Ctx& c);
+void launch_crit_deferred(Ctx& c);
 void launch_opnames(Ctx& c);
 bool opnames_use_tables(int NOP);
 int opnames_block_count(int64_t n_max, int NOP);

@@ -944,6 +944,77 @@ def test_crit_workloads(H, which):
     assert (cp[:, 0] == cp[:, 1:].sum(axis=1)).all() and cp[:, 0].max() > 0
 
 
+def _queue_bound_trace(n_kernels: int, shuffle: bool, seed: int = 5):
+    """One process, one thread, one stream: a launch every microsecond and
+    kernels of 5 us, so the queue holds every kernel back to the end of the
+    one before it and the critical path runs through all of them (a path of
+    2 n_kernels events).  Rows by end time per kind, or shuffled."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    w0 = 1_000_000_000
+    l_ts = w0 + 1000 * np.arange(n_kernels, dtype=np.int64)
+    l_te = l_ts + 500
+    k_ts = np.empty(n_kernels, np.int64)
+    t = 0
+    for i in range(n_kernels):
+        t = max(int(l_te[i]) + 1000, t)
+        k_ts[i] = t
+        t += 5000
+    k_te = k_ts + 5000
+    n = 2 * n_kernels
+    kind = np.r_[np.full(n_kernels, synth.LAUNCH, np.uint8), np.full(n_kernels, synth.KERNEL, np.uint8)]
+    ts = np.r_[l_ts, k_ts]
+    te = np.r_[l_te, k_te]
+    corr = np.r_[np.arange(n_kernels), np.arange(n_kernels)].astype(np.int64)
+    order = rng.permutation(n) if shuffle else np.argsort(te, kind="stable")
+    cols = dict(ts=ts[order], te=te[order], corr=corr[order], pid=np.zeros(n, np.int32),
+                lane=np.zeros(n, np.int32), name=np.zeros(n, np.int32), kind=kind[order])
+    p = synth.empty_params(window_begin=w0, window_end=int(k_te.max()) + 1, gap_threshold=10, n_procs=1, n_streams=1,
+                           n_threads=1, n_names=1, n_op_names=1, flags=17)
+    return cols, p
+
+
+@pytest.mark.parametrize("shape", ["ordered", "shuffled"])
+def test_crit_long_path(H, shape):
+    """A critical path through every kernel of a queue-bound stream (200,000
+    events): in delivery order it crosses tiles of event ids now and then, shuffled at almost every step,
+    so the walk stops short and the doubling over the exits marks the rest."""
+    cols, p = _queue_bound_trace(100_000, shuffle=shape == "shuffled")
+    (code, g), _ = check(H, cols, p, f"long critical path, {shape}")
+    assert (g["crit_flags"] == 3).sum() >= 99_000
+
+
+@pytest.mark.parametrize("walk", ["0", "3"])
+@pytest.mark.parametrize("which", ["figure", "random", "config1", "config3", "static"])
+def test_crit_doubling_pass(H, monkeypatch, walk, which):
+    """The doubling pass over the exits forced on (each process's walk marks
+    at most `walk` exits): after a call of herschel_trace_analyze, and inside
+    herschel_trace_analyze_static."""
+    monkeypatch.setenv("HERSCHEL_CRIT_WALK", walk)
+    if which == "figure":
+        _, cols, p, _ = pins.crit_golden_cases()[0]
+    elif which == "random":
+        tr = synth.random_small(seed=7301, n_rows=400, window=2000, n_procs=100, n_streams=2, n_threads=2,
+                                corr_range=50, flags=17)
+        cols, p = tr.columns(), tr.params
+    elif which == "config1":
+        tr = synth.config1()
+        cols, p = tr.columns(), dict(tr.params, flags=17)
+    else:
+        tr = synth.config3(n_procs=8, n_steps=40, n_edges=2000) if which == "config3" else synth.config1(n_steps=40)
+        cols, p = tr.columns(), dict(tr.params, flags=17)
+    if which != "static":
+        check(H, cols, p, f"doubling pass, walk {walk}, {which}")
+        return
+    n = len(cols["ts"])
+    cap = n + p["n_procs"] * p["n_streams"]
+    st = H.Analyzer(p, n, gap_capacity=cap, workspace=False)
+    assert H.herschel_workspace_size(n, st.params) <= H.STATIC_SCRATCH_BYTES
+    st.prefill()
+    code = H.herschel_trace_analyze_static(H.events_struct(H.device_columns(cols)), n, st.params, st.outs)
+    torch.cuda.synchronize()
+    assert_same((code, st.results(n)), oracle.analyze(cols, p, gap_capacity=cap), p, f"static, walk {walk}")
+
+
 def test_crit_null_outputs_and_errors(H):
     """Any of the three outputs may be NULL; the path needs containment."""
     tr = synth.config3(n_procs=3, n_steps=10, n_edges=50)
