@@ -63,6 +63,7 @@ struct CritArgs {
   const int64_t* off;
   int64_t W0, W1;
   int wb, wb1;
+  int sb, tb;  // stream and thread bits of the timeline and containment keys
   DevState* ds;
   const uint64_t* kK[2];  // timeline order (pid, stream, ts')
   const uint32_t* vK[2];
@@ -100,11 +101,21 @@ constexpr int CP_TE_LOG = 13;
 constexpr int CP_LT = 512;
 constexpr int CP_EPT = CP_TE / CP_LT;
 static_assert((1 << CP_TE_LOG) == CP_TE && CP_EPT * CP_LT == CP_TE, "tile of event ids");
+// the marking pass works on the few tiles the path enters: more threads, fewer events each
+constexpr int CP_MLT = 1024;
+constexpr int CP_MEPT = CP_TE / CP_MLT;
+static_assert(CP_MEPT * CP_MLT == CP_TE, "marking tile");
 
 __device__ __forceinline__ int64_t cp_off(const CritArgs& a, int32_t p) { return a.off ? a.off[p] : 0; }
 __device__ __forceinline__ int64_t cp_start(const CritArgs& a, uint32_t r) { return a.ts[r] - cp_off(a, a.pid[r]); }
 __device__ __forceinline__ int64_t cp_end(const CritArgs& a, uint32_t r) {
   const int64_t e = a.te[r] - cp_off(a, a.pid[r]);
+  return e < a.W1 ? e : a.W1;
+}
+// The same for a record of process p whose clock offset o is known (records
+// of one process share it): one gather instead of three dependent ones.
+__device__ __forceinline__ int64_t cp_end_o(const CritArgs& a, uint32_t r, int64_t o) {
+  const int64_t e = a.te[r] - o;
   return e < a.W1 ? e : a.W1;
 }
 
@@ -191,9 +202,12 @@ __global__ __launch_bounds__(256) void k_crit_host(CritArgs a) {
         while (j >= 0 && in_range(a.ds, j, cnt) && j != pq && a.par[j] != pq) j = a.par[j];
         if (j >= 0 && j != pq) sibq = j;
       }
-      p = a.pid[r];
-      const int64_t ts_ = cp_start(a, r);
-      te_ = cp_end(a, r);
+      // the key holds the process and the corrected start; the parent and
+      // the sibling share the process, and so its clock offset
+      p = (int32_t)(key >> (a.tb + a.wb + 1));
+      const int64_t o = cp_off(a, p);
+      const int64_t ts_ = a.W0 + (int64_t)((key >> 1) & ((1ull << a.wb) - 1));
+      te_ = cp_end_o(a, r, o);
       int32_t y = -1;
       uint8_t cd = 0;
       int64_t rel = I64MIN;
@@ -201,12 +215,12 @@ __global__ __launch_bounds__(256) void k_crit_host(CritArgs a) {
         const uint32_t pr = vals[pq];
         y = (int32_t)(2 * pr);
         cd = CP_OP | CP_PRED;
-        rel = cp_start(a, pr);
+        rel = a.W0 + (int64_t)((keys[pq] >> 1) & ((1ull << a.wb) - 1));
       }
       if (sibq >= 0) {
         a.hasnext[sibq] = 1;  // not the last child of its parent
         const uint32_t sr = vals[sibq];
-        const int64_t es = cp_end(a, sr);
+        const int64_t es = cp_end_o(a, sr, o);
         if (es <= ts_ && es >= rel) {
           y = (int32_t)(2 * sr + 1);
           cd = CP_HOST_GAP;
@@ -269,14 +283,17 @@ __global__ __launch_bounds__(256) void k_crit_kernels(CritArgs a) {
       const uint32_t r = vals[i];
       const int64_t kr = i > 0 && (keys[i - 1] >> a.wb) == (keys[i] >> a.wb) ? (int64_t)vals[i - 1] : -1;
       const int32_t L = a.link[r];
-      const int64_t ts_ = cp_start(a, r);
-      te_ = cp_end(a, r);
-      p = a.pid[r];
+      // the key holds the process and the corrected start; the stream
+      // predecessor and the launch share the process, and so its offset
+      p = (int32_t)(keys[i] >> (a.sb + a.wb));
+      const int64_t o = cp_off(a, p);
+      const int64_t ts_ = a.W0 + (int64_t)(keys[i] & ((1ull << a.wb) - 1));
+      te_ = cp_end_o(a, r, o);
       int32_t y = -1;
       uint8_t cd = 0;
       int64_t rel = I64MIN;
       if (kr >= 0) {
-        const int64_t e = cp_end(a, (uint32_t)kr);
+        const int64_t e = cp_end_o(a, (uint32_t)kr, o);
         if (e <= ts_) {
           y = (int32_t)(2 * kr + 1);
           cd = CP_QUEUE_GAP;
@@ -284,7 +301,7 @@ __global__ __launch_bounds__(256) void k_crit_kernels(CritArgs a) {
         }
       }
       if (L >= 0) {
-        const int64_t eL = cp_end(a, (uint32_t)L), sL = cp_start(a, (uint32_t)L);
+        const int64_t eL = cp_end_o(a, (uint32_t)L, o), sL = a.ts[L] - o;
         if (eL <= ts_) {
           if (eL >= rel) {
             y = 2 * L + 1;
@@ -406,7 +423,7 @@ __global__ __launch_bounds__(256) void k_crit_walk(CritArgs a) {
 // The path inside each tile that holds a marked event: from every marked
 // event, its release chain inside the tile, by pointer doubling in LDS
 // (round r marks the events 2^r releases behind the marked ones).
-__global__ __launch_bounds__(CP_LT) void k_crit_mark_local(CritArgs a) {
+__global__ __launch_bounds__(CP_MLT) void k_crit_mark_local(CritArgs a) {
   __shared__ int32_t s_j[CP_TE];
   __shared__ uint8_t s_m[CP_TE];
   const int64_t ne = 2 * a.n;
@@ -416,27 +433,27 @@ __global__ __launch_bounds__(CP_LT) void k_crit_mark_local(CritArgs a) {
   const int tid = threadIdx.x;
   bool any = false;
 #pragma unroll
-  for (int k = 0; k < CP_EPT; ++k) {
-    const int i = tid + k * CP_LT;
+  for (int k = 0; k < CP_MEPT; ++k) {
+    const int i = tid + k * CP_MLT;
     const uint8_t m = i < tn ? a.mark[tb + i] : (uint8_t)0;
     s_m[i] = m;
     any |= m != 0;
   }
   if (!__syncthreads_or(any)) return;  // the path does not pass this tile
 #pragma unroll
-  for (int k = 0; k < CP_EPT; ++k) {
-    const int i = tid + k * CP_LT;
+  for (int k = 0; k < CP_MEPT; ++k) {
+    const int i = tid + k * CP_MLT;
     const int64_t y = i < tn ? (int64_t)a.pred[tb + i] : -1;
     s_j[i] = (y >= tb && y < tb + tn) ? (int)(y - tb) : i;
   }
   __syncthreads();
   for (int r = 0; r < CP_TE_LOG; ++r) {
-    int32_t t[CP_EPT], v[CP_EPT];
-    bool m[CP_EPT];
+    int32_t t[CP_MEPT], v[CP_MEPT];
+    bool m[CP_MEPT];
     bool ch = false;
 #pragma unroll
-    for (int k = 0; k < CP_EPT; ++k) {
-      const int i = tid + k * CP_LT;
+    for (int k = 0; k < CP_MEPT; ++k) {
+      const int i = tid + k * CP_MLT;
       t[k] = s_j[i];
       v[k] = s_j[t[k]];
       m[k] = s_m[i] != 0;
@@ -444,15 +461,15 @@ __global__ __launch_bounds__(CP_LT) void k_crit_mark_local(CritArgs a) {
     }
     if (!__syncthreads_or(ch)) break;
 #pragma unroll
-    for (int k = 0; k < CP_EPT; ++k) {
+    for (int k = 0; k < CP_MEPT; ++k) {
       if (m[k]) s_m[t[k]] = 1;
-      s_j[tid + k * CP_LT] = v[k];
+      s_j[tid + k * CP_MLT] = v[k];
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int k = 0; k < CP_EPT; ++k) {
-    const int i = tid + k * CP_LT;
+  for (int k = 0; k < CP_MEPT; ++k) {
+    const int i = tid + k * CP_MLT;
     if (i < tn && s_m[i]) a.mark[tb + i] = 1;
   }
 }
@@ -545,6 +562,8 @@ static CritArgs crit_args(Ctx& c) {
   a.W1 = c.W1;
   a.wb = c.wb;
   a.wb1 = c.wb1;
+  a.sb = c.sb;
+  a.tb = c.tb;
   a.ds = c.ds;
   for (int b = 0; b < 2; ++b) {
     a.kK[b] = c.sK.k[b];
@@ -602,7 +621,7 @@ static void launch_crit_rest(Ctx& c, CritArgs a) {
     hipLaunchKernelGGL(k_crit_round, dim3(crit_grid(2 * c.n)), dim3(256), 0, c.st, a);
   }
   const unsigned tiles = (unsigned)cdiv(2 * c.n, CP_TE);
-  hipLaunchKernelGGL(k_crit_mark_local, dim3(tiles), dim3(CP_LT), 0, c.st, a);
+  hipLaunchKernelGGL(k_crit_mark_local, dim3(tiles), dim3(CP_MLT), 0, c.st, a);
   a.final = true;
   hipLaunchKernelGGL(k_crit_attr, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
 }
@@ -624,7 +643,7 @@ void launch_crit(Ctx& c) {
     launch_crit_rest(c, a);
     return;
   }
-  hipLaunchKernelGGL(k_crit_mark_local, dim3(tiles), dim3(CP_LT), 0, c.st, a);
+  hipLaunchKernelGGL(k_crit_mark_local, dim3(tiles), dim3(CP_MLT), 0, c.st, a);
   hipLaunchKernelGGL(k_crit_attr, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
 }
 
