@@ -187,9 +187,12 @@ __global__ __launch_bounds__(256) void k_crit_host(CritArgs a) {
     const int64_t q = q0 + threadIdx.x;
     const bool valid = q < cnt;
     int32_t p = 0;
-    int64_t te_ = 0;
+    int64_t te_ = 0, ts_ = 0;
+    uint32_t r = 0;
+    bool launch = false, sync = false;  // a launch; one without a kernel of its own
+    uint64_t target = 0;
     if (valid) {
-      const uint32_t r = vals[q];
+      r = vals[q];
       const uint64_t key = keys[q];
       const bool isop = (key & 1) == 0;
       const uint64_t seg = key >> (a.wb + 1);
@@ -206,7 +209,7 @@ __global__ __launch_bounds__(256) void k_crit_host(CritArgs a) {
       // the sibling share the process, and so its clock offset
       p = (int32_t)(key >> (a.tb + a.wb + 1));
       const int64_t o = cp_off(a, p);
-      const int64_t ts_ = a.W0 + (int64_t)((key >> 1) & ((1ull << a.wb) - 1));
+      ts_ = a.W0 + (int64_t)((key >> 1) & ((1ull << a.wb) - 1));
       te_ = cp_end_o(a, r, o);
       int32_t y = -1;
       uint8_t cd = 0;
@@ -228,30 +231,51 @@ __global__ __launch_bounds__(256) void k_crit_host(CritArgs a) {
       }
       a.pred[2 * r] = y;
       a.code[2 * r] = cd;
-      if (!isop) {
-        int32_t g = -1;
-        if (a.aux[r] == 0) {  // no kernel of its own: a synchronizing call
-          const uint64_t target = ((uint64_t)p << a.wb1) | (uint64_t)(te_ - a.W0);
-          int64_t lo = 0, hi = ne;
-          while (lo < hi) {
-            const int64_t mid = lo + (hi - lo) / 2;
-            if (ekeys[mid] < target)
-              lo = mid + 1;
-            else
-              hi = mid;
-          }
-          if (lo > 0) {
-            const uint64_t k = ekeys[lo - 1];
-            if ((k >> a.wb1) == (uint64_t)p && (int64_t)(k & emask) > ts_ - a.W0) g = (int32_t)evals[lo - 1];
-          }
-        }
-        if (g >= 0) {
-          a.pred[2 * r + 1] = 2 * g + 1;
-          a.code[2 * r + 1] = CP_SYNC | CP_SELF;
-        } else {
-          a.pred[2 * r + 1] = (int32_t)(2 * r);
-          a.code[2 * r + 1] = CP_API | CP_SELF;
-        }
+      launch = !isop;
+      sync = launch && a.aux[r] == 0;  // no kernel of its own: a synchronizing call
+      target = ((uint64_t)p << a.wb1) | (uint64_t)(te_ - a.W0);
+    }
+    // A synchronizing call's end waits for the process's kernel ending last
+    // inside the call: the last kernel end below (process, the call's end)
+    // in the sorted kernel ends.  The whole wave searches for one call at a
+    // time, 64 ends per step (four dependent loads for a million kernels
+    // instead of twenty).
+    int64_t at = 0;  // first kernel end at or above the target
+    uint64_t todo = ne > 0 ? ballot(sync) : 0ull;
+    while (todo) {
+      const int src = __ffsll((unsigned long long)todo) - 1;
+      todo &= todo - 1;
+      const uint64_t tg = shfl(target, src);
+      int64_t lo = 0, hi = ne;  // every end below lo is below tg, every end from hi on is not
+      while (hi - lo > WAVE) {
+        const int64_t step = (hi - lo + WAVE - 1) / WAVE;
+        const int64_t pos = lo + (int64_t)lane_id() * step;
+        const bool in = pos < hi;
+        const uint64_t kv = ekeys[in ? pos : lo];
+        const int c = popc(ballot(in && kv < tg));
+        const int nin = popc(ballot(in));
+        const int64_t nlo = c > 0 ? lo + (int64_t)(c - 1) * step + 1 : lo;
+        hi = c < nin ? lo + (int64_t)c * step : hi;
+        lo = nlo;
+      }
+      const int64_t pos = lo + lane_id();
+      const bool in = pos < hi;
+      const uint64_t kv = ekeys[in ? pos : ne - 1];
+      const int64_t found = lo + popc(ballot(in && kv < tg));
+      if (lane_id() == src) at = found;
+    }
+    if (launch) {
+      int32_t g = -1;
+      if (sync && at > 0) {
+        const uint64_t k = ekeys[at - 1];
+        if ((k >> a.wb1) == (uint64_t)p && (int64_t)(k & emask) > ts_ - a.W0) g = (int32_t)evals[at - 1];
+      }
+      if (g >= 0) {
+        a.pred[2 * r + 1] = 2 * g + 1;
+        a.code[2 * r + 1] = CP_SYNC | CP_SELF;
+      } else {
+        a.pred[2 * r + 1] = (int32_t)(2 * r);
+        a.code[2 * r + 1] = CP_API | CP_SELF;
       }
     }
     z_add(a, s_z, valid, p, te_);
