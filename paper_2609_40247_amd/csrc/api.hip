@@ -177,6 +177,7 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.dg_begin = b.take<int64_t>(c.dg_cap);
     c.dg_end = b.take<int64_t>(c.dg_cap);
     c.dg_pre = b.take<int64_t>(c.dg_cap);
+    c.dg_key = b.take<uint64_t>(c.dg_cap);
     c.oev_cap = 2 * n;
     c.oev = b.take<uint64_t>(c.oev_cap);
     c.op_span_ws = b.take<int64_t>((int64_t)c.P * c.NOP);

@@ -82,6 +82,7 @@ struct Ctx {
   int64_t* dg_begin = nullptr;
   int64_t* dg_end = nullptr;
   int64_t* dg_pre = nullptr;         // [dg_cap] idle length before each interval (exclusive prefix)
+  uint64_t* dg_key = nullptr;        // [dg_cap] (pid, begin - W0) of each interval, one word
   int64_t dg_cap = 0;
   uint64_t* oev = nullptr;           // [oev_cap] op-name run endpoints
   int64_t oev_cap = 0;
