@@ -149,7 +149,6 @@ size_t layout_workspace(Ctx& c, char* base) {
     c.ev_cap = 2 * n;
     c.ev_keys = b.take<uint64_t>(c.ev_cap);
     c.seg_off = b.take<int32_t>((int64_t)c.P * c.S + 1);
-    if (c.S > 1 && c.S <= 8) c.corank = b.take<int32_t>(c.ev_cap * c.S);
   }
   if (c.contain) {
     c.V = b.take<uint64_t>(n);

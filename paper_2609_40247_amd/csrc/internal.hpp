@@ -115,7 +115,6 @@ struct Ctx {
   uint64_t* ev_keys = nullptr;       // [ev_cap] coverage run endpoints, grouped by (pid, stream)
   int64_t ev_cap = 0;
   int32_t* seg_off = nullptr;        // [P * S + 1] first endpoint of each (pid, stream)
-  int32_t* corank = nullptr;         // [ev_cap * S] endpoint co-ranks in sibling streams (S <= 8)
   uint64_t* V = nullptr;             // [n] containment encoding per sorted position
   uint64_t* M[6] = {};               // max pyramid, level l covers 64^l positions
   int64_t Mn[6] = {};

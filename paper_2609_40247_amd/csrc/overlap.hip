@@ -10,11 +10,12 @@
 // stream is active in it iff an odd number of its events precede it.  Both
 // follow from e's co-rank in each sibling group (how many of its events
 // order before e), so the events are never merged into one sorted list.
-// With up to 8 streams the co-ranks come from a merge path over every pair
-// of a process's groups (each thread takes a fixed number of merge steps,
-// whatever the two groups' densities); with more, from binary searches.
-// The interval's length is added to every active pair, to the classes
-// present and to "any".
+// With up to 8 streams (and up to 256 groups) every tile lies inside one
+// group; for each sibling it finds the stretch of that sibling's events its
+// own events fall among (two wave searches), stages it in LDS and takes each
+// co-rank by a binary search there.  More streams or groups: every event
+// searches its sibling groups in memory.  The interval's length is added to
+// every active pair, to the classes present and to "any".
 #include "internal.hpp"
 
 namespace hx {
@@ -22,14 +23,14 @@ namespace hx {
 constexpr int SW_THREADS = 512;
 constexpr int SW_ITEMS = 8;
 constexpr int SW_TILE = SW_THREADS * SW_ITEMS;
-constexpr int CR_STEPS = 8;  // merge-path steps per thread
-constexpr int CR_SMAX = 8;    // most streams handled with pairwise merges
+constexpr int SW_SMAX = 8;     // most streams summed per active-stream mask
+constexpr int SB_CAP = 8192;   // sibling events staged in LDS per tile (64 KB)
+constexpr int SW_GROUPS = 256; // most (pid, stream) groups for group-aligned tiles
+static_assert(SW_SMAX <= 8 && SW_ITEMS <= 8, "a thread's active-stream masks are packed 8 bits each into 64");
 
 struct SweepArgs {
   const uint64_t* ev;  // (pid << (wb1 + sb)) | (t << sb) | stream, grouped by (pid, stream)
   int32_t* seg_off;    // [P * S + 1] first event of each group
-  int32_t* corank;     // [S][ev_cap] co-rank of each event in each sibling group (S <= 8)
-  int64_t ev_cap;
   const uint8_t* cls;
   int P, S, sb, wb1;
   DevState* ds;
@@ -114,378 +115,324 @@ __global__ __launch_bounds__(256) void k_segoff(SweepArgs a) {
   }
 }
 
-// Co-ranks by merge path.  For process p the pairs (s, s2), s < s2, of its
-// groups are laid end to end; the merge of pair (s, s2) has n_s + n_s2
-// steps, so p owns (S - 1) * n_p steps and the steps of all processes form
-// one index space in process order.  A workgroup takes CR_TILE consecutive
-// steps.  Inside one pair (the common case) it finds the merge positions of
-// its two ends with 64-ary wave searches, stages the two key ranges in LDS,
-// gives each thread CR_STEPS steps located by a binary search in LDS, and
-// writes both co-rank ranges coalesced.  A workgroup whose steps straddle
-// pairs lets every thread find its own position in global memory instead.
-// Each merge step emits the co-rank of the smaller head in the other group
-// (keys of different streams never tie).
-constexpr int CR_THREADS = 512;
-constexpr int CR_TILE = CR_THREADS * CR_STEPS;
-
-struct PairPos {
-  int p, s, s2;
-  int32_t LA, nA, LB, nB;
-  int64_t dl;  // steps into the pair's merge
-};
-
-// Pair and offset of global step d (d < (S - 1) * n).
-__device__ PairPos locate_step(const SweepArgs& a, int64_t d) {
-  const int32_t* off = a.seg_off;
-  const int S = a.S;
-  int lo = 0, hi = a.P - 1;  // the last process whose steps start at or before d
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if ((int64_t)(S - 1) * off[mid * S] <= d)
-      lo = mid;
-    else
-      hi = mid - 1;
-  }
-  PairPos q;
-  q.p = lo;
-  q.s = 0;
-  q.s2 = 1;
-  q.dl = d - (int64_t)(S - 1) * off[lo * S];
-  const int32_t* o = off + (int64_t)lo * S;
-  q.LA = o[0];
-  q.nA = o[1] - q.LA;
-  q.LB = o[1];
-  q.nB = o[2] - q.LB;
-  while (q.dl >= (int64_t)q.nA + q.nB) {  // pairs wholly before d (all in process p)
-    q.dl -= (int64_t)q.nA + q.nB;
-    if (++q.s2 == S) {
-      ++q.s;
-      q.s2 = q.s + 1;
-    }
-    q.LA = o[q.s];
-    q.nA = o[q.s + 1] - q.LA;
-    q.LB = o[q.s2];
-    q.nB = o[q.s2 + 1] - q.LB;
-  }
-  return q;
-}
-
-// Number of A keys among the first d merged keys of A = ev[LA, LA + nA) and
-// B = ev[LB, LB + nB), by a 64-ary search of the diagonal: every lane probes
-// one point per round and a ballot keeps the stretch where the answer lies.
-// Called by a whole wave; every lane gets the answer.
-__device__ int32_t wave_diag_search(const uint64_t* __restrict__ ev, int32_t LA, int32_t nA, int32_t LB, int32_t nB,
-                                    int64_t d) {
+// First index in [lo, hi) whose key is not below `key` (hi if none), by a
+// 64-ary search: every lane probes one point per round and a ballot keeps
+// the stretch where the answer lies.  Called by a whole wave; every lane
+// gets the answer.
+__device__ int32_t wave_lower_bound(const uint64_t* __restrict__ ev, int32_t lo, int32_t hi, uint64_t key) {
   const int lane = lane_id();
-  int32_t lo = (int32_t)max<int64_t>(0, d - nB), hi = (int32_t)min<int64_t>(d, nA);
-  while (lo < hi) {  // answer in [lo, hi]; A[i] < B[d-1-i] holds exactly for i < answer
+  while (lo < hi) {  // answer in [lo, hi]
     const int32_t step = (hi - lo + WAVE - 1) / WAVE;
     const int32_t x = lo + lane * step;
-    const bool probe = x < hi;
-    const bool f = probe && ev[LA + x] < ev[LB + (int32_t)(d - 1 - x)];
-    const uint64_t bf = ballot(f);
-    const int k = popc(bf);  // lanes 0..k-1 probed true (monotone)
-    const int32_t nlo = k > 0 ? lo + (k - 1) * step + 1 : lo;
-    const int32_t xk = lo + k * step;
-    hi = xk < hi ? xk : hi;
+    const bool below = x < hi && ev[x] < key;
+    const int c = popc(ballot(below));  // lanes 0..c-1 probed below the key
+    const int32_t nlo = c > 0 ? lo + (c - 1) * step + 1 : lo;
+    const int32_t xc = lo + c * step;
+    hi = xc < hi ? xc : hi;
     lo = nlo;
   }
   return lo;
 }
 
-// Generic path: the thread locates its own first step and merges.
-__device__ void corank_steps(const SweepArgs& a, int64_t d0, int64_t steps) {
-  const int S = a.S;
-  const int32_t* off = a.seg_off;
-  PairPos q = locate_step(a, d0);
-  int p = q.p, s = q.s, s2 = q.s2;
-  int32_t LA = q.LA, nA = q.nA, LB = q.LB, nB = q.nB;
-  const int64_t dl = q.dl;
-  int32_t ilo = (int32_t)max<int64_t>(0, dl - nB), ihi = (int32_t)min<int64_t>(dl, nA);
-  while (ilo < ihi) {
-    const int32_t mid = (ilo + ihi) >> 1;
-    if (a.ev[LA + mid] < a.ev[LB + (int32_t)dl - mid - 1])
-      ilo = mid + 1;
-    else
-      ihi = mid;
-  }
-  int32_t i = ilo, j = (int32_t)dl - ilo;
-  uint64_t va = i < nA ? a.ev[LA + i] : ~0ull;
-  uint64_t vb = j < nB ? a.ev[LB + j] : ~0ull;
-  while (steps > 0) {
-    if (i == nA && j == nB) {  // next pair, or the first pair of the next process
-      if (++s2 == S) {
-        ++s;
-        s2 = s + 1;
-      }
-      if (s >= S - 1) {
-        ++p;
-        s = 0;
-        s2 = 1;
-      }
-      LA = off[p * S + s];
-      nA = off[p * S + s + 1] - LA;
-      LB = off[p * S + s2];
-      nB = off[p * S + s2 + 1] - LB;
-      i = j = 0;
-      va = nA > 0 ? a.ev[LA] : ~0ull;
-      vb = nB > 0 ? a.ev[LB] : ~0ull;
-      continue;
+// Copy cnt keys (cnt <= SB_CAP) into LDS, SW_STAGE loads in flight per
+// thread (indices clamped to the last key, so every load is in bounds).
+constexpr int SW_STAGE = 8;
+__device__ __forceinline__ void stage_keys(const uint64_t* __restrict__ src, int32_t cnt, uint64_t* dst) {
+  for (int32_t xb = 0; xb < cnt; xb += SW_STAGE * SW_THREADS) {
+    uint64_t v[SW_STAGE];
+#pragma unroll
+    for (int u = 0; u < SW_STAGE; ++u) {
+      const int32_t x = xb + u * SW_THREADS + (int32_t)threadIdx.x;
+      v[u] = src[x < cnt ? x : cnt - 1];
     }
-    if (va < vb) {
-      a.corank[(int64_t)s2 * a.ev_cap + LA + i] = j;
-      ++i;
-      va = i < nA ? a.ev[LA + i] : ~0ull;
-    } else {
-      a.corank[(int64_t)s * a.ev_cap + LB + j] = i;
-      ++j;
-      vb = j < nB ? a.ev[LB + j] : ~0ull;
+#pragma unroll
+    for (int u = 0; u < SW_STAGE; ++u) {
+      const int32_t x = xb + u * SW_THREADS + (int32_t)threadIdx.x;
+      if (x < cnt) dst[x] = v[u];
     }
-    --steps;
   }
 }
 
-__global__ __launch_bounds__(CR_THREADS) void k_corank(SweepArgs a) {
-  __shared__ uint64_t s_key[CR_TILE];  // A range, then B range
-  __shared__ int32_t s_out[CR_TILE];   // co-ranks in the same layout
-  __shared__ int32_t s_split[2];
-  const int tid = threadIdx.x, wv = tid / WAVE;
-  const int64_t n = a.ds->nEv;
+// Active-stream mask and next event time after event i (key `key`) from
+// binary searches of its process's sibling groups in memory; the own stream
+// is active after a start (even index in its group).
+__device__ __forceinline__ void item_global(const SweepArgs& a, int64_t i, uint64_t key, uint64_t tmask,
+                                            uint64_t smask, int pshift, uint64_t* m_out, uint64_t* tn_out) {
   const int S = a.S;
-  const int64_t total = (int64_t)(S - 1) * n;
-  const int64_t D0 = (int64_t)blockIdx.x * CR_TILE;
-  if (D0 >= total) return;
-  const int64_t cnt = min<int64_t>(CR_TILE, total - D0);
-  const PairPos q0 = locate_step(a, D0);
-  const bool one_pair = q0.dl + cnt <= (int64_t)q0.nA + q0.nB;
-  if (!one_pair) {
-    const int64_t d0 = D0 + (int64_t)tid * CR_STEPS;
-    if (d0 < total) corank_steps(a, d0, min<int64_t>(CR_STEPS, total - d0));
-    return;
-  }
-  // merge positions of the tile's two ends
-  if (wv < 2) {
-    const int64_t d = q0.dl + (wv == 0 ? 0 : cnt);
-    const int32_t i = wave_diag_search(a.ev, q0.LA, q0.nA, q0.LB, q0.nB, d);
-    if (lane_id() == 0) s_split[wv] = i;
-  }
-  __syncthreads();
-  const int32_t i0 = s_split[0], i1 = s_split[1];
-  const int32_t j0 = (int32_t)q0.dl - i0, j1 = (int32_t)(q0.dl + cnt) - i1;
-  const int32_t na = i1 - i0, nb = j1 - j0;  // na + nb == cnt
-  for (int x = tid; x < na; x += CR_THREADS) s_key[x] = a.ev[q0.LA + i0 + x];
-  for (int y = tid; y < nb; y += CR_THREADS) s_key[na + y] = a.ev[q0.LB + j0 + y];
-  __syncthreads();
-  const uint64_t* A = s_key;
-  const uint64_t* B = s_key + na;
-  const int32_t dd = tid * CR_STEPS;
-  if (dd < cnt) {
-    int32_t lo = max(0, dd - nb), hi = min(dd, na);
-    while (lo < hi) {
-      const int32_t mid = (lo + hi) >> 1;
-      if (A[mid] < B[dd - 1 - mid])
-        lo = mid + 1;
-      else
-        hi = mid;
-    }
-    int32_t i = lo, j = dd - lo;
-    const int32_t steps = min<int32_t>(CR_STEPS, (int32_t)cnt - dd);
-    for (int k = 0; k < steps; ++k) {
-      const bool takeA = j >= nb || (i < na && A[i] < B[j]);
-      if (takeA) {
-        s_out[i] = j0 + j;
-        ++i;
+  const int pid = (int)(key >> pshift);
+  const int st = (int)(key & smask);
+  const int32_t* off = a.seg_off + (int64_t)pid * S;
+  uint64_t m = 0, tn = ~0ull;
+#pragma unroll 1
+  for (int s = 0; s < S; ++s) {
+    if (s == st) continue;
+    const int32_t Lq = off[s], Rq = off[s + 1];
+    int32_t lo = Lq, len = Rq - Lq;
+    uint64_t nx = ~0ull;
+    while (len > 0) {
+      const int32_t half = len >> 1;
+      const uint64_t v = a.ev[lo + half];
+      if (v < key) {
+        lo += half + 1;
+        len -= half + 1;
       } else {
-        s_out[na + j] = i0 + i;
-        ++j;
+        nx = v;
+        len = half;
       }
     }
+    if ((lo - Lq) & 1) m |= 1ull << s;
+    if (lo < Rq) {
+      const uint64_t t2 = (nx >> a.sb) & tmask;
+      tn = t2 < tn ? t2 : tn;
+    }
   }
-  __syncthreads();
-  int32_t* outA = a.corank + (int64_t)q0.s2 * a.ev_cap + q0.LA + i0;
-  int32_t* outB = a.corank + (int64_t)q0.s * a.ev_cap + q0.LB + j0;
-  for (int x = tid; x < na; x += CR_THREADS) outA[x] = s_out[x];
-  for (int y = tid; y < nb; y += CR_THREADS) outB[y] = s_out[na + y];
+  const int32_t own_L = off[st], own_R = off[st + 1];
+  if (((i - own_L) & 1) == 0) m |= 1ull << st;
+  if (i + 1 < own_R) {
+    const uint64_t t2 = (a.ev[i + 1] >> a.sb) & tmask;
+    tn = t2 < tn ? t2 : tn;
+  }
+  *m_out = m;
+  *tn_out = tn;
 }
 
-// One event per thread and item (items striped over the workgroup).  With
-// at most 8 streams a workgroup sums interval lengths per active-stream mask
-// in LDS and expands the 2^S sums into pairs, classes and "any" at the end;
-// with more streams every interval is added to the pair matrix in LDS
-// directly.  Intervals of a process other than the workgroup's first go
-// straight to the outputs.
-template <int SMAX>
-__global__ __launch_bounds__(SW_THREADS) void k_sweep(SweepArgs a) {
-  constexpr bool SMALL = SMAX <= CR_SMAX;
-  __shared__ unsigned long long s_mlen[SMALL ? 256 : 1];
-  __shared__ unsigned long long s_pair[SMALL ? 1 : 64 * 64];
+// Per-mask interval sums of one process expanded into its pair matrix,
+// class coverage and "any" (one thread per output entry).
+__device__ __forceinline__ void flush_masks(const SweepArgs& a, int pid, const unsigned long long* s_mlen,
+                                            unsigned long long* s_cls, const uint64_t* cm) {
+  const int tid = threadIdx.x, S = a.S, nm = 1 << S;
+  if (tid < S * S) {
+    const int i = tid / S, jj = tid % S;
+    const uint64_t need = (1ull << i) | (1ull << jj);
+    unsigned long long v = 0;
+    for (int mk = 1; mk < nm; ++mk)
+      if (((uint64_t)mk & need) == need) v += s_mlen[mk];
+    if (v && a.pair) atomicAdd((unsigned long long*)&a.pair[((int64_t)pid * S + i) * S + jj], v);
+  } else if (tid >= 64 && tid < 64 + 13) {
+    const int e = tid - 64;  // 0..2 class busy, 3..11 class pairs, 12 any
+    unsigned long long v = 0;
+    for (int mk = 1; mk < nm; ++mk) {
+      const uint64_t mm = (uint64_t)mk;
+      bool hit;
+      if (e < 3)
+        hit = (mm & cm[e]) != 0;
+      else if (e < 12)
+        hit = (mm & cm[(e - 3) / 3]) != 0 && (mm & cm[(e - 3) % 3]) != 0;
+      else
+        hit = true;
+      if (hit) v += s_mlen[mk];
+    }
+    s_cls[e] = v;
+  }
+  __syncthreads();
+  if (a.class_busy && tid < 3 && s_cls[tid])
+    atomicAdd((unsigned long long*)&a.class_busy[pid * 3 + tid], s_cls[tid]);
+  if (a.class_overlap && tid >= 3 && tid < 12 && s_cls[tid])
+    atomicAdd((unsigned long long*)&a.class_overlap[pid * 9 + (tid - 3)], s_cls[tid]);
+  if (a.any_busy && tid == 12 && s_cls[12]) atomicAdd((unsigned long long*)&a.any_busy[pid], s_cls[12]);
+}
+
+__device__ __forceinline__ void class_masks(const SweepArgs& a, uint64_t* s_cmask) {
+  if (threadIdx.x < 3) {
+    uint64_t m = 0;
+    for (int s = 0; s < a.S; ++s)
+      if ((a.cls ? a.cls[s] : 0) == (int)threadIdx.x) m |= 1ull << s;
+    s_cmask[threadIdx.x] = m;
+  }
+}
+
+// Up to 8 streams and SW_GROUPS (pid, stream) groups: tiles of SW_TILE
+// events inside one group, numbered group after group (each workgroup
+// finds its group from the groups' tile counts), items striped over the
+// workgroup so that neighbouring lanes hold neighbouring events.  For each
+// sibling the tile's events fall among a stretch of the sibling's events
+// (its co-ranks of the tile's first and last events, by two wave searches),
+// which is staged in LDS in chunks of SB_CAP; every item takes its co-rank
+// by a binary search there (the reads of a step issued together), the
+// sibling is active in the item's interval iff the co-rank is odd, and the
+// event at the co-rank is the sibling's next event.  Interval lengths are
+// summed per active-stream mask in LDS and expanded at the end.
+__global__ __launch_bounds__(SW_THREADS) void k_sweep_groups(SweepArgs a) {
+  __shared__ uint64_t s_sib[SB_CAP];  // one chunk of a sibling's stretch
+  __shared__ unsigned long long s_mlen[256];
   __shared__ unsigned long long s_cls[13];  // class_busy[3], class_overlap[9], any
   __shared__ uint64_t s_cmask[3];
-  __shared__ int32_t s_off0[SMAX + 1];  // group starts of the workgroup's first process
+  __shared__ int32_t s_goff[SW_GROUPS + 1];  // first event of each group
+  __shared__ int32_t s_toff[SW_GROUPS + 1];  // first tile of each group
+  __shared__ int32_t s_rng[2 * SW_SMAX];     // per sibling: its co-ranks of the tile's first and last events
+  const int tid = threadIdx.x, wv = tid / WAVE, lane = lane_id();
+  const int S = a.S, G = a.P * S;
+  for (int g = tid; g <= G; g += SW_THREADS) s_goff[g] = a.seg_off[g];
+  for (int i = tid; i < 256; i += SW_THREADS) s_mlen[i] = 0;
+  if (tid < 13) s_cls[tid] = 0;
+  class_masks(a, s_cmask);
+  __syncthreads();
+  if (wv == 0) {  // tiles per group, exclusive prefix over the groups
+    int32_t run = 0;
+    for (int g0 = 0; g0 <= G; g0 += WAVE) {  // uniform over the wave
+      const int g = g0 + lane;
+      const int32_t c = g < G ? (int32_t)cdiv((int64_t)(s_goff[g + 1] - s_goff[g]), (int64_t)SW_TILE) : 0;
+      int32_t incl = c;
+      for (int d = 1; d < WAVE; d <<= 1) {
+        const int32_t o = shfl_up(incl, d);
+        if (lane >= d) incl += o;
+      }
+      if (g <= G) s_toff[g] = run + incl - c;
+      run += shfl(incl, WAVE - 1);
+    }
+  }
+  __syncthreads();
+  const int32_t b = (int32_t)blockIdx.x;
+  if (b >= s_toff[G]) return;  // past the last tile (uniform over the workgroup)
+  int glo = 0, ghi = G - 1;      // the last group whose tiles start at or before b
+  while (glo < ghi) {
+    const int mid = (glo + ghi + 1) >> 1;
+    if (s_toff[mid] <= b)
+      glo = mid;
+    else
+      ghi = mid - 1;
+  }
+  const int g = glo, pid = g / S, st = g - pid * S;
+  const int32_t own_L = s_goff[g], own_R = s_goff[g + 1];
+  const int64_t base = own_L + (int64_t)(b - s_toff[g]) * SW_TILE;
+  const int64_t end = min<int64_t>(base + SW_TILE, own_R);
+  const uint64_t tmask = (1ull << a.wb1) - 1;
+  const uint64_t cm[3] = {s_cmask[0], s_cmask[1], s_cmask[2]};
+
+  uint64_t key[SW_ITEMS], tn[SW_ITEMS];
+  uint64_t m8 = 0;    // item j's active-stream mask in bits [8 j, 8 j + 8)
+  uint32_t todo = 0;  // bit j: item j exists and its co-rank in the current sibling is not yet known
+#pragma unroll
+  for (int j = 0; j < SW_ITEMS; ++j) {
+    const int64_t i = base + (int64_t)j * SW_THREADS + tid;
+    const bool ok = i < end;
+    key[j] = ok ? a.ev[i] : ~0ull;
+    // the own stream: the next event, and active after a start (even index)
+    const uint64_t nk = ok && i + 1 < own_R ? a.ev[i + 1] : ~0ull;
+    tn[j] = nk != ~0ull ? (nk >> a.sb) & tmask : ~0ull;
+    m8 |= ok && ((i - own_L) & 1) == 0 ? (uint64_t)(1u << st) << (8 * j) : 0ull;
+    todo |= ok ? 1u << j : 0u;
+  }
+  const uint32_t valid = todo;
+  const uint64_t kf = a.ev[base], kl = a.ev[end - 1];
+  for (int q = wv; q < 2 * S; q += SW_THREADS / WAVE) {
+    const int s2 = q >> 1;
+    if (s2 == st) continue;
+    const int32_t c = wave_lower_bound(a.ev, s_goff[pid * S + s2], s_goff[pid * S + s2 + 1], (q & 1) ? kl : kf);
+    if (lane == 0) s_rng[q] = c;
+  }
+  __syncthreads();
+  for (int s2 = 0; s2 < S; ++s2) {  // uniform over the workgroup
+    if (s2 == st) continue;
+    // the tile's events fall among the sibling's events [c0, hi): up to the
+    // last one's co-rank, and the head after it
+    const int32_t L = s_goff[pid * S + s2], R = s_goff[pid * S + s2 + 1];
+    const int32_t c0 = s_rng[2 * s2];
+    const int32_t hi = min(s_rng[2 * s2 + 1] + 1, R);
+    todo = valid;
+    for (int32_t cb = c0;; cb += SB_CAP) {  // uniform over the workgroup
+      const int32_t cnt = min(SB_CAP, hi - cb);
+      const bool final = cb + SB_CAP >= hi;
+      stage_keys(a.ev + cb, cnt, s_sib);
+      __syncthreads();
+      if (todo) {
+        const int32_t cmax = cnt > 0 ? cnt - 1 : 0;
+        constexpr int HB = SW_ITEMS / 2;  // two halves, to bound the registers in flight
+#pragma unroll
+        for (int hb = 0; hb < SW_ITEMS; hb += HB) {
+          int32_t pos[HB];
+#pragma unroll
+          for (int u = 0; u < HB; ++u) pos[u] = 0;
+          int32_t len = cnt;
+          while (len > 1) {  // branchless lower bound, the same steps for every item
+            const int32_t half = len >> 1;
+            uint64_t v[HB];
+#pragma unroll
+            for (int u = 0; u < HB; ++u) v[u] = s_sib[pos[u] + half];
+#pragma unroll
+            for (int u = 0; u < HB; ++u) pos[u] = v[u] < key[hb + u] ? pos[u] + half : pos[u];
+            len -= half;
+          }
+          uint64_t v[HB];
+#pragma unroll
+          for (int u = 0; u < HB; ++u) v[u] = s_sib[pos[u]];
+#pragma unroll
+          for (int u = 0; u < HB; ++u) pos[u] += cnt > 0 && v[u] < key[hb + u];
+#pragma unroll
+          for (int u = 0; u < HB; ++u) v[u] = s_sib[min(pos[u], cmax)];  // the head
+#pragma unroll
+          for (int u = 0; u < HB; ++u) {
+            const int j = hb + u;
+            // resolved by this chunk if its lower bound lies inside (or it is the last)
+            const bool res = ((todo >> j) & 1) && (pos[u] < cnt || final);
+            // co-rank cb - L + pos: the sibling is active if it is odd
+            m8 |= res && ((cb - L + pos[u]) & 1) ? (uint64_t)(1u << s2) << (8 * j) : 0ull;
+            const uint64_t t2 = (v[u] >> a.sb) & tmask;
+            tn[j] = res && pos[u] < cnt && t2 < tn[j] ? t2 : tn[j];
+            todo &= res ? ~(1u << j) : ~0u;
+          }
+        }
+      }
+      __syncthreads();  // the next chunk or sibling overwrites this one
+      if (final) break;
+    }
+  }
+  // a thread's intervals with one mask are summed before the atomic
+  uint32_t cur_m = 0;
+  int64_t cur_len = 0;
+#pragma unroll
+  for (int j = 0; j < SW_ITEMS; ++j) {
+    const uint32_t mj = (uint32_t)(m8 >> (8 * j)) & 255;
+    if (!((valid >> j) & 1) || mj == 0 || tn[j] == ~0ull) continue;
+    const int64_t len = (int64_t)tn[j] - (int64_t)((key[j] >> a.sb) & tmask);
+    if (len <= 0) continue;
+    if (mj != cur_m) {
+      if (cur_len) atomicAdd(&s_mlen[cur_m], (unsigned long long)cur_len);
+      cur_m = mj;
+      cur_len = 0;
+    }
+    cur_len += len;
+  }
+  if (cur_len) atomicAdd(&s_mlen[cur_m], (unsigned long long)cur_len);
+  __syncthreads();
+  flush_masks(a, pid, s_mlen, s_cls, cm);
+}
+
+// Any number of streams and groups: tiles by position (several groups and
+// processes in one), every item searching its siblings in memory, intervals
+// added to the pair matrix of the workgroup's first process in LDS (others
+// straight to the outputs).
+__global__ __launch_bounds__(SW_THREADS) void k_sweep_global(SweepArgs a) {
+  __shared__ unsigned long long s_pair[64 * 64];
+  __shared__ unsigned long long s_cls[13];  // class_busy[3], class_overlap[9], any
+  __shared__ uint64_t s_cmask[3];
   const int tid = threadIdx.x;
   const int32_t n = a.ds->nEv;
   const int64_t base = (int64_t)blockIdx.x * SW_TILE;
   if (base >= n) return;
   const int S = a.S;
-  if (SMALL) {
-    for (int i = tid; i < 256; i += SW_THREADS) s_mlen[i] = 0;
-  } else {
-    for (int i = tid; i < 64 * 64; i += SW_THREADS) s_pair[i] = 0;
-  }
+  for (int i = tid; i < 64 * 64; i += SW_THREADS) s_pair[i] = 0;
   if (tid < 13) s_cls[tid] = 0;
-  if (tid < 3) {
-    uint64_t m = 0;
-    for (int s = 0; s < S; ++s)
-      if ((a.cls ? a.cls[s] : 0) == tid) m |= 1ull << s;
-    s_cmask[tid] = m;
-  }
+  class_masks(a, s_cmask);
   const uint64_t tmask = (1ull << a.wb1) - 1;
   const uint64_t smask = (1ull << a.sb) - 1;
   const int pshift = a.wb1 + a.sb;
   const int pid0 = (int)(a.ev[base] >> pshift);
-  if (SMALL && tid <= S) s_off0[tid] = a.seg_off[pid0 * S + tid];
   __syncthreads();
   const uint64_t cm[3] = {s_cmask[0], s_cmask[1], s_cmask[2]};
-
-  if constexpr (SMALL) {
-    // Items in batches whose loads are issued together: keys, own successors
-    // and co-ranks (addresses known up front), then the sibling heads.
-    constexpr int BT = 32 / SMAX;
-    for (int jb = 0; jb < SW_ITEMS; jb += BT) {
-      uint64_t key[BT], nk[BT];
-      int32_t cr[BT][SMAX];
-#pragma unroll
-      for (int b = 0; b < BT; ++b) {
-        const int64_t i = base + (int64_t)(jb + b) * SW_THREADS + tid;
-        key[b] = i < n ? a.ev[i] : ~0ull;
-        nk[b] = i + 1 < n ? a.ev[i + 1] : ~0ull;
-        // the co-rank buffer exists only with two or more streams; the entry
-        // of the event's own stream is loaded (it lies inside the buffer)
-        // before the stream is known, and never used
-#pragma unroll
-        for (int s = 0; s < SMAX; ++s)
-          cr[b][s] = S > 1 && i < n && s < S ? a.corank[(int64_t)s * a.ev_cap + i] : 0;
-      }
-#pragma unroll
-      for (int b = 0; b < BT; ++b) {
-        const int64_t i = base + (int64_t)(jb + b) * SW_THREADS + tid;
-        if (i >= n) continue;
-        const int pid = (int)(key[b] >> pshift);
-        const int st = (int)(key[b] & smask);
-        int32_t off[SMAX + 1];
-#pragma unroll
-        for (int s = 0; s <= SMAX; ++s)
-          off[s] = s <= S ? (pid == pid0 ? s_off0[s] : a.seg_off[pid * S + s]) : 0;
-        int32_t own_L = 0, own_R = 0;
-#pragma unroll
-        for (int s = 0; s < SMAX; ++s)
-          if (s == st) {
-            own_L = off[s];
-            own_R = off[s + 1];
-          }
-        // its own stream is active after a start (even index in its group);
-        // a sibling iff an odd number of its events precede this one
-        uint64_t m = ((i - own_L) & 1) == 0 ? 1ull << st : 0ull;
-        uint64_t tn = i + 1 < own_R ? (nk[b] >> a.sb) & tmask : ~0ull;
-        uint64_t hv[SMAX];
-#pragma unroll
-        for (int s = 0; s < SMAX; ++s) {
-          const bool sib = s < S && s != st;
-          hv[s] = sib && (uint32_t)cr[b][s] < (uint32_t)(off[s + 1] - off[s]) ? a.ev[off[s] + cr[b][s]] : ~0ull;
-        }
-#pragma unroll
-        for (int s = 0; s < SMAX; ++s) {
-          if (s >= S || s == st) continue;
-          if (cr[b][s] & 1) m |= 1ull << s;
-          if (hv[s] != ~0ull) {
-            const uint64_t t2 = (hv[s] >> a.sb) & tmask;
-            tn = t2 < tn ? t2 : tn;
-          }
-        }
-        if (m == 0 || tn == ~0ull) continue;
-        const int64_t len = (int64_t)tn - (int64_t)((key[b] >> a.sb) & tmask);
-        if (len <= 0) continue;
-        if (pid == pid0)
-          atomicAdd(&s_mlen[m], (unsigned long long)len);
-        else
-          add_interval(a, m, len, pid, pid0, cm, s_pair, s_cls);
-      }
-    }
-  } else {
-    for (int jt = 0; jt < SW_ITEMS; ++jt) {
-      const int64_t i = base + (int64_t)jt * SW_THREADS + tid;
-      if (i >= n) break;
-      const uint64_t key = a.ev[i];
-      const int pid = (int)(key >> pshift);
-      const int st = (int)(key & smask);
-      const int g = pid * S + st;
-      uint64_t m = 0, tn = ~0ull;
-      const int32_t own_L = a.seg_off[g], own_R = a.seg_off[g + 1];
-      // many streams: one plain binary search per sibling
-      for (int s = 0; s < S; ++s) {
-        if (s == st) continue;
-        const int32_t Lq = a.seg_off[pid * S + s], Rq = a.seg_off[pid * S + s + 1];
-        int32_t lo = Lq, len = Rq - Lq;
-        uint64_t nx = ~0ull;
-        while (len > 0) {
-          const int32_t half = len >> 1;
-          const uint64_t v = a.ev[lo + half];
-          if (v < key) {
-            lo += half + 1;
-            len -= half + 1;
-          } else {
-            nx = v;
-            len = half;
-          }
-        }
-        if ((lo - Lq) & 1) m |= 1ull << s;
-        if (lo < Rq) {
-          const uint64_t t2 = (nx >> a.sb) & tmask;
-          tn = t2 < tn ? t2 : tn;
-        }
-      }
-      // its own stream is active after a start (even index in its group)
-      if (((i - own_L) & 1) == 0) m |= 1ull << st;
-      if (i + 1 < own_R) {
-        const uint64_t t2 = (a.ev[i + 1] >> a.sb) & tmask;
-        tn = t2 < tn ? t2 : tn;
-      }
-      if (m == 0 || tn == ~0ull) continue;
-      const int64_t len = (int64_t)tn - (int64_t)((key >> a.sb) & tmask);
-      if (len <= 0) continue;
-      add_interval(a, m, len, pid, pid0, cm, s_pair, s_cls);
-    }
+  for (int jt = 0; jt < SW_ITEMS; ++jt) {
+    const int64_t i = base + (int64_t)jt * SW_THREADS + tid;
+    if (i >= n) break;
+    const uint64_t key = a.ev[i];
+    uint64_t m, tn;
+    item_global(a, i, key, tmask, smask, pshift, &m, &tn);
+    if (m == 0 || tn == ~0ull) continue;
+    const int64_t len = (int64_t)tn - (int64_t)((key >> a.sb) & tmask);
+    if (len <= 0) continue;
+    add_interval(a, m, len, (int)(key >> pshift), pid0, cm, s_pair, s_cls);
   }
   __syncthreads();
-  if (SMALL) {
-    // expand the per-mask sums: one thread per output entry
-    const int nm = 1 << S;
-    if (tid < S * S) {
-      const int i = tid / S, jj = tid % S;
-      const uint64_t need = (1ull << i) | (1ull << jj);
-      unsigned long long v = 0;
-      for (int mk = 1; mk < nm; ++mk)
-        if (((uint64_t)mk & need) == need) v += s_mlen[mk];
-      if (v && a.pair) atomicAdd((unsigned long long*)&a.pair[((int64_t)pid0 * S + i) * S + jj], v);
-    } else if (tid >= 64 && tid < 64 + 13) {
-      const int e = tid - 64;  // 0..2 class busy, 3..11 class pairs, 12 any
-      unsigned long long v = 0;
-      for (int mk = 1; mk < nm; ++mk) {
-        const uint64_t mm = (uint64_t)mk;
-        bool hit;
-        if (e < 3)
-          hit = (mm & cm[e]) != 0;
-        else if (e < 12)
-          hit = (mm & cm[(e - 3) / 3]) != 0 && (mm & cm[(e - 3) % 3]) != 0;
-        else
-          hit = true;
-        if (hit) v += s_mlen[mk];
-      }
-      s_cls[e] = v;
-    }
-    __syncthreads();
-  }
-  if (!SMALL && a.pair) {
+  if (a.pair) {
     for (int i = tid; i < S * S; i += SW_THREADS)
       if (s_pair[i]) atomicAdd((unsigned long long*)&a.pair[(int64_t)pid0 * S * S + i], s_pair[i]);
   }
@@ -510,22 +457,16 @@ void launch_overlap(Ctx& c) {
   a.class_busy = c.o.class_busy;
   a.class_overlap = c.o.class_overlap;
   a.any_busy = c.o.any_busy;
-  a.corank = c.corank;
-  a.ev_cap = c.ev_cap;
   const int64_t nseg = (int64_t)c.P * c.S + 1;
   hipLaunchKernelGGL(k_segoff, dim3((unsigned)std::min<int64_t>(cdiv(nseg, 256 / WAVE), 1024)), dim3(256), 0, c.st, a);
-  const dim3 grid((unsigned)std::max<int64_t>(cdiv(c.ev_cap, SW_TILE), 1));
-  if (c.S > 1 && c.S <= CR_SMAX) {
-    const int64_t steps = (int64_t)(c.S - 1) * c.ev_cap;
-    hipLaunchKernelGGL(k_corank, dim3((unsigned)std::max<int64_t>(cdiv(steps, CR_TILE), 1)), dim3(CR_THREADS), 0, c.st,
-                       a);
+  const int64_t G = (int64_t)c.P * c.S;
+  if (c.S <= SW_SMAX && G <= SW_GROUPS) {
+    // at most one partial tile per group beyond the full ones
+    hipLaunchKernelGGL(k_sweep_groups, dim3((unsigned)(cdiv(c.ev_cap, SW_TILE) + G)), dim3(SW_THREADS), 0, c.st, a);
+  } else {
+    hipLaunchKernelGGL(k_sweep_global, dim3((unsigned)std::max<int64_t>(cdiv(c.ev_cap, SW_TILE), 1)),
+                       dim3(SW_THREADS), 0, c.st, a);
   }
-  if (c.S <= 4)
-    hipLaunchKernelGGL(k_sweep<4>, grid, dim3(SW_THREADS), 0, c.st, a);
-  else if (c.S <= CR_SMAX)
-    hipLaunchKernelGGL(k_sweep<CR_SMAX>, grid, dim3(SW_THREADS), 0, c.st, a);
-  else
-    hipLaunchKernelGGL(k_sweep<64>, grid, dim3(SW_THREADS), 0, c.st, a);
 }
 
 }  // namespace hx

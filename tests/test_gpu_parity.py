@@ -242,6 +242,37 @@ def test_bursty_streams_overlap(H, seed):
     check(H, cols, p, f"bursty streams seed{seed}")
 
 
+@pytest.mark.parametrize("seed", range(2))
+def test_sparse_stream_beside_dense_streams(H, seed):
+    """Overlap where a tile of a sparse stream spans far more events of a
+    dense sibling than one LDS stretch holds (the sibling taken in several
+    chunks), tiles that cover several streams and processes, and a stream
+    whose events all come after a sibling's: per process, stream 0 holds
+    60,000 short kernels spread over the window, stream 1 holds 400 long
+    ones, stream 2 a few thousand in its second half, stream 3 none."""
+    rng = np.random.default_rng(910 + seed)
+    W = 40_000_000
+    rows = []
+    corr = 0
+
+    def kern(pid, s, t, d):
+        nonlocal corr
+        rows.append((2, pid, s, int(t), int(t + d), corr, corr % 4))
+        corr += 1
+
+    for pid in range(2):
+        for x in np.sort(rng.choice(W // 600, 60_000, replace=False)) * 600 + pid:   # dense, disjoint
+            kern(pid, 0, x, rng.integers(1, 500))
+        for x in np.sort(rng.integers(0, W - 200_000, 400)):                         # sparse, long
+            kern(pid, 1, x, rng.integers(10_000, 150_000))
+        for x in np.sort(rng.integers(W // 2, W - 1_000, 3_000)):                    # second half only
+            kern(pid, 2, x, rng.integers(1, 5_000))
+    perm = rng.permutation(len(rows))
+    rows = [rows[i] for i in perm]
+    cols, p = _rows(rows, P=2, S=4, W=W, thr=100, cls=np.array([0, 1, 2, 0], np.uint8))
+    check(H, cols, p, f"sparse beside dense seed{seed}")
+
+
 def test_64_streams_overlap(H):
     tr = synth.random_small(seed=77, n_rows=6000, window=20_000, n_procs=2, n_streams=64, n_threads=2,
                             corr_range=3000)
