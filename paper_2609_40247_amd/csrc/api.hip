@@ -658,7 +658,6 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     launch_kernel_ops(c);
   }
   stage_end(c, HERSCHEL_STAGE_NAMES);
-  rec(4, c.st);
 
   // chain 1: timeline and overlap
   c.st = lib0;
@@ -676,6 +675,11 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   }
   stage_end(c, HERSCHEL_STAGE_WAITS);
   rec(1, c.st);
+  // the join's stream takes the timeline's end too, so that the caller's
+  // stream waits on one event at the end (each wait is a barrier packet on
+  // its queue, handled after the kernel before it)
+  wait(lib1, 1);
+  rec(4, lib1);
 
   // back on the caller's stream: what needs both containment and the join
   c.st = s0;
@@ -692,8 +696,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_GRAPH);
   if (c.graph) launch_graph(c);
   stage_end(c, HERSCHEL_STAGE_GRAPH);
-  wait(c.st, 1);
-  wait(c.st, 4);
+  wait(c.st, 4);  // both other streams' work
   stage_begin(c, HERSCHEL_STAGE_FINAL);
   launch_finalize(c);
   stage_end(c, HERSCHEL_STAGE_FINAL);
