@@ -325,6 +325,34 @@ int herschel_trace_analyze_batch(const herschel_events *ev, const int64_t *trace
                                  int32_t n_traces, const herschel_params *p,
                                  herschel_outputs *out);
 
+/* The batch of herschel_trace_analyze_batch over traces that stay in host
+ * memory, streamed to the device in chunks of chunk_traces traces with
+ * double-buffered uploads: while chunk c is analysed on p[0].hip_stream, chunk
+ * c + 1 uploads on a copy stream of the library into the other staging set.
+ *   host           HOST struct of HOST column pointers, all traces back to
+ *                  back as in herschel_trace_analyze_batch; allocate them
+ *                  pinned (hipHostMalloc) for the uploads to overlap the
+ *                  analysis (pageable memory works, without overlap).  The
+ *                  optional columns (flops, bytes, graph_node) are uploaded
+ *                  when non-NULL.
+ *   trace_offsets  HOST array of n_traces + 1 row offsets into the host columns.
+ *   chunk_traces   traces per chunk (>= 1).
+ *   staging        HOST array of two herschel_events whose pointers are DEVICE
+ *                  buffers of staging_rows rows each (every column the host
+ *                  holds); owned by the caller, overwritten by the call.
+ *   p, out         as for herschel_trace_analyze_batch: n_traces entries;
+ *                  p[0]'s workspace and stream serve every trace.
+ * Returns HERSCHEL_EINVAL (nothing enqueued) for NULL pointers, offsets that
+ * fall, a chunk with more rows than staging_rows or a staging set without
+ * room for a column the host holds; otherwise the first non-OK code of a
+ * chunk in trace order, after which no further chunk is analysed.  Returns
+ * when every chunk analysed is done and no upload is in flight.  One call
+ * at a time per process (the copy stream is shared; calls are serialized). */
+int herschel_trace_analyze_chunked(const herschel_events *host, const int64_t *trace_offsets,
+                                   int32_t n_traces, int32_t chunk_traces,
+                                   const herschel_events *staging, int64_t staging_rows,
+                                   const herschel_params *p, herschel_outputs *out);
+
 const char *herschel_strerror(int code);
 
 /* Diagnostics for benchmarks.  Stages of one analysis call.  INIT, PREP,

@@ -6,6 +6,7 @@
 #include <cstddef>
 #include <cstdio>
 #include <mutex>
+#include <vector>
 
 #include <stdlib.h>
 
@@ -532,6 +533,8 @@ struct DeviceStreams {
   hipStream_t s[2] = {nullptr, nullptr};
   hipStream_t cap = nullptr;  // graphs are captured here (the caller's stream may be the null stream)
   hipEvent_t e[6] = {};  // sorts, timeline chain, join, launches' ops, name tables, radix passes
+  hipStream_t copy = nullptr;  // uploads of the chunked entry point
+  hipEvent_t up[2] = {};       // a staging set's upload done
   bool ok = false;
 };
 static std::mutex g_enqueue_mutex;
@@ -545,7 +548,10 @@ static DeviceStreams* device_streams() {
     for (auto& st : d.s)
       if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
     if (hipStreamCreateWithFlags(&d.cap, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipStreamCreateWithFlags(&d.copy, hipStreamNonBlocking) != hipSuccess) return nullptr;
     for (auto& ev : d.e)
+      if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return nullptr;
+    for (auto& ev : d.up)
       if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return nullptr;
     d.ok = true;
   }
@@ -1153,6 +1159,98 @@ int herschel_trace_analyze_batch(const herschel_events* ev, const int64_t* trace
     if (code != HERSCHEL_OK) return code;
   }
   return first_err;
+}
+
+// Chunks of chunk_traces traces: chunk c + 1 uploads into the other staging
+// set on the library's copy stream while chunk c is analysed by the batch
+// entry point on the caller's stream (which waits for the upload's event).
+// A batch call returns after its work is done, so the set that chunk c - 1
+// used is free when chunk c + 1's upload is enqueued.  One chunked call at a
+// time per process: the copy stream and its events are shared.
+static std::mutex g_chunk_mutex;
+
+int herschel_trace_analyze_chunked(const herschel_events* host, const int64_t* trace_offsets, int32_t n_traces,
+                                   int32_t chunk_traces, const herschel_events* staging, int64_t staging_rows,
+                                   const herschel_params* p, herschel_outputs* out) {
+  if (!host || !trace_offsets || !staging || !p || !out || n_traces < 0 || chunk_traces < 1 || staging_rows < 0)
+    return HERSCHEL_EINVAL;
+  if (n_traces == 0) return HERSCHEL_OK;
+  for (int32_t t = 0; t < n_traces; ++t)
+    if (trace_offsets[t + 1] < trace_offsets[t] || trace_offsets[t] < 0) return HERSCHEL_EINVAL;
+  const int32_t n_chunks = (int32_t)cdiv((int64_t)n_traces, (int64_t)chunk_traces);
+  for (int32_t ch = 0; ch < n_chunks; ++ch) {
+    const int32_t t0 = ch * chunk_traces, t1 = std::min(n_traces, t0 + chunk_traces);
+    if (trace_offsets[t1] - trace_offsets[t0] > staging_rows) return HERSCHEL_EINVAL;
+  }
+  // the columns every call reads, on both sides; an optional column the host
+  // holds must have room in both staging sets
+  if (!host->ts || !host->te || !host->corr || !host->pid || !host->lane || !host->name || !host->kind)
+    return HERSCHEL_EINVAL;
+  for (int b = 0; b < 2; ++b) {
+    const herschel_events& d = staging[b];
+    if (!d.ts || !d.te || !d.corr || !d.pid || !d.lane || !d.name || !d.kind) return HERSCHEL_EINVAL;
+    if ((host->flops && !d.flops) || (host->bytes && !d.bytes) || (host->graph_node && !d.graph_node))
+      return HERSCHEL_EINVAL;
+  }
+  std::lock_guard<std::mutex> chunk_lock(g_chunk_mutex);
+  DeviceStreams* dsx;
+  {
+    std::lock_guard<std::mutex> lock(g_enqueue_mutex);
+    dsx = enqueue_setup();
+  }
+  if (!dsx) return HERSCHEL_EDEVICE;
+  const hipStream_t cs = dsx->copy, st = (hipStream_t)p[0].hip_stream;
+  auto upload = [&](int32_t ch) -> bool {
+    const herschel_events& d = staging[ch & 1];
+    const int32_t t0 = ch * chunk_traces, t1 = std::min(n_traces, t0 + chunk_traces);
+    const int64_t r0 = trace_offsets[t0], rows = trace_offsets[t1] - r0;
+    bool ok = true;
+    auto put = [&](const void* dst, const void* src, size_t elem) {
+      if (ok && rows > 0 && src)
+        ok = hipMemcpyAsync(const_cast<void*>(dst), static_cast<const char*>(src) + r0 * elem, (size_t)rows * elem,
+                            hipMemcpyHostToDevice, cs) == hipSuccess;
+    };
+    put(d.ts, host->ts, 8);
+    put(d.te, host->te, 8);
+    put(d.corr, host->corr, 8);
+    put(d.pid, host->pid, 4);
+    put(d.lane, host->lane, 4);
+    put(d.name, host->name, 4);
+    put(d.kind, host->kind, 1);
+    put(d.flops, host->flops, 8);
+    put(d.bytes, host->bytes, 8);
+    put(d.graph_node, host->graph_node, 4);
+    return ok && hipEventRecord(dsx->up[ch & 1], cs) == hipSuccess;
+  };
+  int code = upload(0) ? HERSCHEL_OK : HERSCHEL_EDEVICE;
+  std::vector<int64_t> offs;
+  std::vector<herschel_params> pc;
+  for (int32_t ch = 0; ch < n_chunks && code == HERSCHEL_OK; ++ch) {
+    if (ch + 1 < n_chunks && !upload(ch + 1)) {
+      code = HERSCHEL_EDEVICE;
+      break;
+    }
+    if (hipStreamWaitEvent(st, dsx->up[ch & 1], 0) != hipSuccess) {
+      code = HERSCHEL_EDEVICE;
+      break;
+    }
+    const int32_t t0 = ch * chunk_traces, t1 = std::min(n_traces, t0 + chunk_traces);
+    offs.assign(trace_offsets + t0, trace_offsets + t1 + 1);
+    for (auto& o : offs) o -= trace_offsets[t0];
+    pc.assign(p + t0, p + t1);
+    pc[0].hip_stream = p[0].hip_stream;
+    pc[0].workspace = p[0].workspace;
+    pc[0].workspace_bytes = p[0].workspace_bytes;
+    // the staging set, without the optional columns the host does not hold
+    herschel_events e = staging[ch & 1];
+    if (!host->flops) e.flops = nullptr;
+    if (!host->bytes) e.bytes = nullptr;
+    if (!host->graph_node) e.graph_node = nullptr;
+    code = herschel_trace_analyze_batch(&e, offs.data(), t1 - t0, pc.data(), out + t0);
+  }
+  // no upload outlives the call
+  if (hipStreamSynchronize(cs) != hipSuccess && code == HERSCHEL_OK) code = HERSCHEL_EDEVICE;
+  return code;
 }
 
 }  // extern "C"

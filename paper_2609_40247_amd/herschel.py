@@ -2,7 +2,8 @@
 
 The names follow the C ABI in ``include/herschel.h``:
 ``herschel_workspace_size``, ``herschel_trace_analyze``,
-``herschel_trace_analyze_batch`` and ``herschel_strerror``.  Every step of the
+``herschel_trace_analyze_batch``, ``herschel_trace_analyze_chunked`` and
+``herschel_strerror``.  Every step of the
 analysis runs in the HIP library; PyTorch only provides device memory and the
 stream.  There is no CPU fallback: without the built library (or a GPU) the
 calls raise.
@@ -102,6 +103,12 @@ def load(variant: str | None = None) -> ctypes.CDLL:
         lib.herschel_trace_analyze_batch.argtypes = [ctypes.POINTER(HerschelEvents), ctypes.POINTER(ctypes.c_int64),
                                                      ctypes.c_int32, ctypes.POINTER(HerschelParams),
                                                      ctypes.POINTER(HerschelOutputs)]
+        lib.herschel_trace_analyze_chunked.restype = ctypes.c_int
+        lib.herschel_trace_analyze_chunked.argtypes = [ctypes.POINTER(HerschelEvents), ctypes.POINTER(ctypes.c_int64),
+                                                       ctypes.c_int32, ctypes.c_int32,
+                                                       ctypes.POINTER(HerschelEvents), ctypes.c_int64,
+                                                       ctypes.POINTER(HerschelParams),
+                                                       ctypes.POINTER(HerschelOutputs)]
         lib.herschel_strerror.restype = ctypes.c_char_p
         lib.herschel_strerror.argtypes = [ctypes.c_int]
         lib.herschel_time_stage.restype = ctypes.c_int
@@ -147,6 +154,21 @@ def herschel_trace_analyze_batch(events: HerschelEvents, offsets: np.ndarray, pa
     return int(lib.herschel_trace_analyze_batch(ctypes.byref(events),
                                                 offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
                                                 T, parr, oarr))
+
+
+def herschel_trace_analyze_chunked(host: HerschelEvents, offsets: np.ndarray, chunk_traces: int, staging: list,
+                                   staging_rows: int, params: list, outs: list, lib=None) -> int:
+    """The batch over host-resident traces, uploaded chunk by chunk into two
+    device staging sets (``staging``: two HerschelEvents of device pointers)."""
+    lib = lib or load()
+    T = len(params)
+    offs = np.ascontiguousarray(offsets, dtype=np.int64)
+    parr = (HerschelParams * T)(*params)
+    oarr = (HerschelOutputs * T)(*outs)
+    sarr = (HerschelEvents * 2)(*staging)
+    return int(lib.herschel_trace_analyze_chunked(ctypes.byref(host),
+                                                  offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                                  T, int(chunk_traces), sarr, int(staging_rows), parr, oarr))
 
 
 STAGES = ("init", "prep", "hist", "names", "sort", "timeline", "overlap", "contain", "join", "opagg", "edges",

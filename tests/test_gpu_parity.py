@@ -483,6 +483,74 @@ def test_batch_matches_single_calls(H):
         assert_same((0, a.results(t.n)), o, t.params, t.label)
 
 
+def _pinned(H, cols):
+    """Pinned host copies of the columns and a HerschelEvents of their pointers."""
+    dt = dict(ts=np.int64, te=np.int64, corr=np.int64, pid=np.int32, lane=np.int32, name=np.int32, kind=np.uint8,
+              flops=np.int64, bytes=np.int64, graph_node=np.int32)
+    h = {k: torch.from_numpy(np.ascontiguousarray(cols[k], dtype=dt[k])).pin_memory()
+         for k in dt if cols.get(k) is not None}
+    return h, H.HerschelEvents(**{k: v.data_ptr() for k, v in h.items()})
+
+
+def _chunk_setup(H, traces, chunk):
+    cols = {k: np.concatenate([t.columns()[k] for t in traces]) for k in traces[0].columns()}
+    offs = np.cumsum([0] + [t.n for t in traces]).astype(np.int64)
+    host, hev = _pinned(H, cols)
+    rows = max(int(offs[min(c + chunk, len(traces))] - offs[c]) for c in range(0, len(traces), chunk))
+    staging = [{k: torch.empty(rows, dtype=v.dtype, device="cuda") for k, v in host.items()} for _ in range(2)]
+    ans = [H.Analyzer(t.params, max(t.n for t in traces)) for t in traces]
+    for a in ans:
+        a.prefill()
+    big = max(ans, key=lambda a: a.ws_bytes)
+    plist = [ans[0]._params_struct(big.ws.data_ptr(), big.ws_bytes)] + [a.params for a in ans[1:]]
+    return host, hev, offs, staging, rows, ans, plist
+
+
+@pytest.mark.parametrize("chunk", [1, 2, 3, 5])
+def test_chunked_streaming_matches_oracle(H, chunk):
+    """Five traces of different shapes streamed from pinned host memory in
+    chunks of 1, 2, 3 and 5 traces (two staging sets alternate, each upload
+    on the library's copy stream beside the analysis of the chunk before):
+    every output of every trace equals the oracle's."""
+    traces = [synth.config4_trace(0, kernels=20_000), synth.config0(), synth.random_small(seed=3),
+              synth.config4_trace(1, kernels=7_000), synth.config1(n_steps=10)]
+    host, hev, offs, staging, rows, ans, plist = _chunk_setup(H, traces, chunk)
+    print(f"chunked: {len(traces)} traces, chunks of {chunk}, staging {rows} rows", flush=True)
+    code = H.herschel_trace_analyze_chunked(hev, offs, chunk, [H.events_struct(d) for d in staging], rows, plist,
+                                            [a.outs for a in ans])
+    torch.cuda.synchronize()
+    assert code == 0, H.herschel_strerror(code)
+    for t, a in zip(traces, ans):
+        o = oracle.analyze(t.columns(), t.params, gap_capacity=a.gap_capacity)
+        assert_same((0, a.results(t.n)), o, t.params, f"{t.label} (chunks of {chunk})")
+
+
+def test_chunked_streaming_errors(H):
+    """A chunk larger than the staging sets, falling offsets and a staging
+    set without a column are rejected before anything is enqueued; no
+    traces is a no-op; an invalid row in the second chunk returns its code
+    after the first chunk's results are written."""
+    traces = [synth.config0(), synth.random_small(seed=4), synth.random_small(seed=5)]
+    host, hev, offs, staging, rows, ans, plist = _chunk_setup(H, traces, 2)
+    sev = [H.events_struct(d) for d in staging]
+    outs = [a.outs for a in ans]
+    assert H.herschel_trace_analyze_chunked(hev, offs, 2, sev, rows - 1, plist, outs) == H.EINVAL
+    bad = offs.copy()
+    bad[1], bad[2] = bad[2], bad[1]
+    assert H.herschel_trace_analyze_chunked(hev, bad, 2, sev, rows, plist, outs) == H.EINVAL
+    no_kind = [H.events_struct({k: v for k, v in staging[0].items() if k != "kind"}), sev[1]]
+    assert H.herschel_trace_analyze_chunked(hev, offs, 2, no_kind, rows, plist, outs) == H.EINVAL
+    assert H.herschel_trace_analyze_chunked(hev, offs[:1], 2, sev, rows, [], []) == 0
+    # an invalid kind in trace 2 (the second chunk): the first chunk's traces are still analysed
+    host["kind"][int(offs[2]) + 3] = 7
+    code = H.herschel_trace_analyze_chunked(hev, offs, 2, sev, rows, plist, outs)
+    torch.cuda.synchronize()
+    assert code == H.EEVENT, H.herschel_strerror(code)
+    for t, a in zip(traces[:2], ans[:2]):
+        o = oracle.analyze(t.columns(), t.params, gap_capacity=a.gap_capacity)
+        assert_same((0, a.results(t.n)), o, t.params, t.label)
+
+
 def test_calls_from_several_threads(H):
     """Four host threads call at once, each on its own stream with its own
     workspace and outputs, alternating a valid trace and the same trace with
