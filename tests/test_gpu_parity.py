@@ -273,6 +273,38 @@ def test_sparse_stream_beside_dense_streams(H, seed):
     check(H, cols, p, f"sparse beside dense seed{seed}")
 
 
+@pytest.mark.parametrize("seed", range(2))
+def test_overlap_spans_beyond_32_bits(H, seed):
+    """Overlap over a 30 s window with spans beyond 32 bits of ns: stream 0
+    holds 6,000 short kernels in its first second and 3,000 in its 21st,
+    stream 1 ten long kernels spread over the window (its one tile spans
+    27 s), stream 2 two kernels at 12 s and 29 s (the next events that dense
+    tiles see lie more than 2^32 ns past their start), and stream 3 none."""
+    rng = np.random.default_rng(930 + seed)
+    W = 30_000_000_000
+    rows = []
+    corr = 0
+
+    def kern(pid, s, t, d):
+        nonlocal corr
+        rows.append((2, pid, s, int(t), int(t + d), corr, corr % 4))
+        corr += 1
+
+    for pid in range(2):
+        for x in np.sort(rng.choice(1_000_000, 6_000, replace=False)) * 1_000 + pid:
+            kern(pid, 0, x, rng.integers(1, 900))
+        for x in np.sort(rng.choice(1_000_000, 3_000, replace=False)) * 1_000 + 20_000_000_000:
+            kern(pid, 0, x, rng.integers(1, 900))
+        for k in range(10):
+            kern(pid, 1, k * 3_000_000_000 + rng.integers(0, 1_000_000), rng.integers(1, 2_000_000_000))
+        kern(pid, 2, 12_000_000_000 + pid, 5_000)
+        kern(pid, 2, 29_000_000_000, 700_000_000)
+    perm = rng.permutation(len(rows))
+    rows = [rows[i] for i in perm]
+    cols, p = _rows(rows, P=2, S=4, W=W, thr=10_000, cls=np.array([0, 1, 2, 0], np.uint8))
+    check(H, cols, p, f"spans beyond 32 bits seed{seed}")
+
+
 def test_64_streams_overlap(H):
     tr = synth.random_small(seed=77, n_rows=6000, window=20_000, n_procs=2, n_streams=64, n_threads=2,
                             corr_range=3000)
