@@ -532,7 +532,8 @@ static inline void stage_end(Ctx& c, int s) {
 struct DeviceStreams {
   hipStream_t s[2] = {nullptr, nullptr};
   hipStream_t cap = nullptr;  // graphs are captured here (the caller's stream may be the null stream)
-  hipEvent_t e[6] = {};  // sorts, timeline chain, join, launches' ops, name tables, radix passes
+  hipEvent_t e[8] = {};  // sorts, timeline chain, join, launches' ops, name tables, radix passes, depths,
+                         // kernels' critical-path releases
   hipStream_t copy = nullptr;  // uploads of the chunked entry point
   hipEvent_t up[2] = {};       // a staging set's upload done
   bool ok = false;
@@ -635,6 +636,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     launch_contain(c);
     rec(3, s0);  // each launch's op is known
     launch_depth(c);
+    if (c.crit) rec(6, s0);  // the per-op aggregates move beside the critical path
     stage_end(c, HERSCHEL_STAGE_CONTAIN);
   } else if (c.o.link || c.o.aux) {
     const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(c.n, 256 * 8), 1), 2048);
@@ -664,6 +666,10 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     launch_kernel_ops(c);
   }
   stage_end(c, HERSCHEL_STAGE_NAMES);
+  if (c.crit) {  // the kernels' releases (the join and the timeline order), beside the host records'
+    launch_crit_kernels(c);
+    rec(7, c.st);
+  }
 
   // chain 1: timeline and overlap
   c.st = lib0;
@@ -680,6 +686,19 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     launch_waits(c);
   }
   stage_end(c, HERSCHEL_STAGE_WAITS);
+  // with the critical path (which needs containment and the join, not the
+  // per-op aggregates) the aggregates and what reads them run here, beside it
+  const bool agg_side = c.crit && c.contain;
+  if (agg_side) {
+    wait(c.st, 6);
+    wait(c.st, 2);
+    stage_begin(c, HERSCHEL_STAGE_OPAGG);
+    launch_opagg(c);
+    stage_end(c, HERSCHEL_STAGE_OPAGG);
+    stage_begin(c, HERSCHEL_STAGE_SOL);
+    if (c.sol) launch_sol(c);
+    stage_end(c, HERSCHEL_STAGE_SOL);
+  }
   rec(1, c.st);
   // the join's stream takes the timeline's end too, so that the caller's
   // stream waits on one event at the end (each wait is a barrier packet on
@@ -690,14 +709,20 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   // back on the caller's stream: what needs both containment and the join
   c.st = s0;
   wait(c.st, 2);
-  stage_begin(c, HERSCHEL_STAGE_OPAGG);
-  if (c.contain) launch_opagg(c);
-  stage_end(c, HERSCHEL_STAGE_OPAGG);
-  stage_begin(c, HERSCHEL_STAGE_SOL);
-  if (c.sol) launch_sol(c);
-  stage_end(c, HERSCHEL_STAGE_SOL);
+  if (!agg_side) {
+    stage_begin(c, HERSCHEL_STAGE_OPAGG);
+    if (c.contain) launch_opagg(c);
+    stage_end(c, HERSCHEL_STAGE_OPAGG);
+    stage_begin(c, HERSCHEL_STAGE_SOL);
+    if (c.sol) launch_sol(c);
+    stage_end(c, HERSCHEL_STAGE_SOL);
+  }
   stage_begin(c, HERSCHEL_STAGE_CRIT);
-  if (c.crit) launch_crit(c);
+  if (c.crit) {
+    launch_crit_front(c);
+    wait(c.st, 7);
+    launch_crit(c);
+  }
   stage_end(c, HERSCHEL_STAGE_CRIT);
   stage_begin(c, HERSCHEL_STAGE_GRAPH);
   if (c.graph) launch_graph(c);

@@ -283,23 +283,17 @@ __global__ __launch_bounds__(256) void k_crit_host(CritArgs a) {
   z_flush(a, s_z);
 }
 
-// Kernels, one per timeline position; and each parent's last child (the
-// child that is no other child's previous sibling), one per containment
-// position.
+// Kernels, one per timeline position (the timeline order and the join: no
+// containment answer, so this pass runs beside the host records').
 __global__ __launch_bounds__(256) void k_crit_kernels(CritArgs a) {
   __shared__ unsigned long long s_z[CP_LDS_PROCS];
   z_init(s_z, a.P);
-  const int64_t cnt = a.ds->nK, ncl = a.ds->nCL;
-  const int64_t work = cnt > ncl ? cnt : ncl;
+  const int64_t cnt = a.ds->nK;
   const int pk = (int)a.ds->sort_parity[SORT_K];
   const uint64_t* keys = a.kK[pk];
   const uint32_t* vals = a.vK[pk];
-  for (int64_t i0 = (int64_t)blockIdx.x * 256; i0 < work; i0 += (int64_t)gridDim.x * 256) {  // uniform per workgroup
+  for (int64_t i0 = (int64_t)blockIdx.x * 256; i0 < cnt; i0 += (int64_t)gridDim.x * 256) {  // uniform per workgroup
     const int64_t i = i0 + threadIdx.x;
-    if (i < ncl && !a.hasnext[i]) {
-      const int32_t pq = a.par[i];
-      if (pq >= 0) a.lastc1[pq] = (uint32_t)(i + 1);
-    }
     const bool valid = i < cnt;
     int32_t p = 0;
     int64_t te_ = 0;
@@ -344,6 +338,17 @@ __global__ __launch_bounds__(256) void k_crit_kernels(CritArgs a) {
     z_add(a, s_z, valid, p, te_);
   }
   z_flush(a, s_z);
+}
+
+// Each parent's last child (the child that is no other child's previous
+// sibling, as the host pass has marked them), one per containment position.
+__global__ __launch_bounds__(256) void k_crit_last(CritArgs a) {
+  const int64_t ncl = a.ds->nCL;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < ncl; i += (int64_t)gridDim.x * 256)
+    if (!a.hasnext[i]) {
+      const int32_t pq = a.par[i];
+      if (pq >= 0) a.lastc1[pq] = (uint32_t)(i + 1);
+    }
 }
 
 // Ops' end events, once every last child is known.
@@ -653,12 +658,22 @@ static void launch_crit_rest(Ctx& c, CritArgs a) {
 // With c.crit_deferred the doubling is left out: the charging pass then
 // does nothing if a walk stopped short (DevState::crit_more), and the caller
 // runs launch_crit_deferred once the call has ended.
-void launch_crit(Ctx& c) {
+void launch_crit_kernels(Ctx& c) {
+  if (c.n == 0) return;
+  hipLaunchKernelGGL(k_crit_kernels, dim3(crit_grid(c.n)), dim3(256), 0, c.st, crit_args(c));
+}
+
+void launch_crit_front(Ctx& c) {
   if (c.n == 0) return;
   CritArgs a = crit_args(c);
   hipLaunchKernelGGL(k_crit_host, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
-  hipLaunchKernelGGL(k_crit_kernels, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
+  hipLaunchKernelGGL(k_crit_last, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
   hipLaunchKernelGGL(k_crit_ops, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
+}
+
+void launch_crit(Ctx& c) {
+  if (c.n == 0) return;
+  CritArgs a = crit_args(c);
   hipLaunchKernelGGL(k_crit_rows, dim3(crit_grid(c.n)), dim3(256), 0, c.st, a);
   const unsigned tiles = (unsigned)cdiv(2 * c.n, CP_TE);
   hipLaunchKernelGGL(k_crit_local, dim3(tiles), dim3(CP_LT), 0, c.st, a);

@@ -181,6 +181,12 @@ void launch_edges(Ctx& c);
 void launch_finalize(Ctx& c);
 void launch_sol(Ctx& c);
 void launch_crit_elist(Ctx& c);
+// the critical path: the kernels' releases (after the join and the
+// timeline sort; beside the host records'), the host records' releases, last
+// children and ops' ends (after containment and the join), then, once both
+// are done, the rows, the marking and the charges
+void launch_crit_kernels(Ctx& c);
+void launch_crit_front(Ctx& c);
 void launch_crit(Ctx& c);
 void launch_graph(Ctx& c);
 bool graph_uses_tables(int NG);
