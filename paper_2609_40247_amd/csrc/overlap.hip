@@ -134,16 +134,18 @@ __device__ int32_t wave_lower_bound(const uint64_t* __restrict__ ev, int32_t lo,
   return lo;
 }
 
-// Copy cnt keys (cnt <= SB_CAP) into LDS, SW_STAGE loads in flight per
-// thread (indices clamped to the last key, so every load is in bounds).
+// Copy the keys src[x * stride], x < cnt (cnt <= SB_CAP), into LDS, SW_STAGE
+// loads in flight per thread (indices clamped to the last one, so every load
+// is in bounds).
 constexpr int SW_STAGE = 8;
-__device__ __forceinline__ void stage_keys(const uint64_t* __restrict__ src, int32_t cnt, uint64_t* dst) {
+__device__ __forceinline__ void stage_keys(const uint64_t* __restrict__ src, int32_t cnt, uint64_t* dst,
+                                           int32_t stride = 1) {
   for (int32_t xb = 0; xb < cnt; xb += SW_STAGE * SW_THREADS) {
     uint64_t v[SW_STAGE];
 #pragma unroll
     for (int u = 0; u < SW_STAGE; ++u) {
       const int32_t x = xb + u * SW_THREADS + (int32_t)threadIdx.x;
-      v[u] = src[x < cnt ? x : cnt - 1];
+      v[u] = src[(int64_t)(x < cnt ? x : cnt - 1) * stride];
     }
 #pragma unroll
     for (int u = 0; u < SW_STAGE; ++u) {
@@ -196,31 +198,43 @@ __device__ __forceinline__ void item_global(const SweepArgs& a, int64_t i, uint6
   *tn_out = tn;
 }
 
-// Per-mask interval sums of one process expanded into its pair matrix,
-// class coverage and "any" (one thread per output entry).
-__device__ __forceinline__ void flush_masks(const SweepArgs& a, int pid, const unsigned long long* s_mlen,
-                                            unsigned long long* s_cls, const uint64_t* cm) {
-  const int tid = threadIdx.x, S = a.S, nm = 1 << S;
+// Per-mask interval sums T[m] of one process (s_mlen, 256 entries, zero
+// beyond 2^S) expanded into its pair matrix, class coverage and "any".  In
+// S steps of 256 threads, s_mlen becomes the superset sums F[m] (the time at
+// least the streams of m are active) and s_sub the subset sums G[m] (the
+// time only streams of m are): pair (i, j) is F[{i, j}]; with the total
+// T = G[all], a class's coverage is T - G[all but the class], and two
+// classes' overlap T - G[not c1] - G[not c2] + G[neither].
+__device__ __forceinline__ void flush_masks(const SweepArgs& a, int pid, unsigned long long* s_mlen,
+                                            unsigned long long* s_sub, unsigned long long* s_cls, const uint64_t* cm) {
+  const int tid = threadIdx.x, S = a.S;
+  static_assert(SW_THREADS >= 256, "one thread per mask");
+  if (tid < 256) s_sub[tid] = s_mlen[tid];
+  for (int bit = 0; bit < S; ++bit) {
+    __syncthreads();
+    if (tid < 256) {
+      const int m = 1 << bit;
+      if (!(tid & m)) s_mlen[tid] += s_mlen[tid | m];  // entries with the bit are not written this step
+      else s_sub[tid] += s_sub[tid ^ m];               // nor are those without it
+    }
+  }
+  __syncthreads();
+  const uint64_t all = (1ull << S) - 1;
   if (tid < S * S) {
     const int i = tid / S, jj = tid % S;
-    const uint64_t need = (1ull << i) | (1ull << jj);
-    unsigned long long v = 0;
-    for (int mk = 1; mk < nm; ++mk)
-      if (((uint64_t)mk & need) == need) v += s_mlen[mk];
+    const unsigned long long v = s_mlen[(1 << i) | (1 << jj)];
     if (v && a.pair) atomicAdd((unsigned long long*)&a.pair[((int64_t)pid * S + i) * S + jj], v);
   } else if (tid >= 64 && tid < 64 + 13) {
     const int e = tid - 64;  // 0..2 class busy, 3..11 class pairs, 12 any
-    unsigned long long v = 0;
-    for (int mk = 1; mk < nm; ++mk) {
-      const uint64_t mm = (uint64_t)mk;
-      bool hit;
-      if (e < 3)
-        hit = (mm & cm[e]) != 0;
-      else if (e < 12)
-        hit = (mm & cm[(e - 3) / 3]) != 0 && (mm & cm[(e - 3) % 3]) != 0;
-      else
-        hit = true;
-      if (hit) v += s_mlen[mk];
+    const unsigned long long T = s_sub[all];
+    unsigned long long v;
+    if (e < 3) {
+      v = T - s_sub[all & ~cm[e]];
+    } else if (e < 12) {
+      const uint64_t c1 = cm[(e - 3) / 3], c2 = cm[(e - 3) % 3];
+      v = T - s_sub[all & ~c1] - s_sub[all & ~c2] + s_sub[all & ~(c1 | c2)];
+    } else {
+      v = T;
     }
     s_cls[e] = v;
   }
@@ -241,13 +255,123 @@ __device__ __forceinline__ void class_masks(const SweepArgs& a, uint64_t* s_cmas
   }
 }
 
+// Every valid item's co-rank in sibling s2, whose stretch of events
+// cb .. cb + cnt - 1 (the item's lower bounds all lie in it or just past it)
+// is read from src (LDS, or memory when it is too long to stage): a
+// branchless binary search, the same steps for every item and the reads of
+// a step issued together.  The sibling is active in the item's interval iff
+// the co-rank (cb - L + position) is odd, and the event at the position is
+// the sibling's next event.
+__device__ __forceinline__ void sibling_search(const SweepArgs& a, const uint64_t* src, int32_t cnt, int32_t cb,
+                                               int32_t L, int s2, const uint64_t* key, uint32_t valid, uint64_t& m8,
+                                               uint64_t* tn) {
+  if (!valid) return;
+  const uint64_t tmask = (1ull << a.wb1) - 1;
+  const int32_t cmax = cnt > 0 ? cnt - 1 : 0;
+  constexpr int HB = SW_ITEMS / 2;  // two halves, to bound the registers in flight
+#pragma unroll
+  for (int hb = 0; hb < SW_ITEMS; hb += HB) {
+    int32_t pos[HB];
+#pragma unroll
+    for (int u = 0; u < HB; ++u) pos[u] = 0;
+    int32_t len = cnt;
+    while (len > 1) {
+      const int32_t half = len >> 1;
+      uint64_t v[HB];
+#pragma unroll
+      for (int u = 0; u < HB; ++u) v[u] = src[pos[u] + half];
+#pragma unroll
+      for (int u = 0; u < HB; ++u) pos[u] = v[u] < key[hb + u] ? pos[u] + half : pos[u];
+      len -= half;
+    }
+    uint64_t v[HB];
+#pragma unroll
+    for (int u = 0; u < HB; ++u) v[u] = src[pos[u]];
+#pragma unroll
+    for (int u = 0; u < HB; ++u) pos[u] += cnt > 0 && v[u] < key[hb + u];
+#pragma unroll
+    for (int u = 0; u < HB; ++u) v[u] = src[min(pos[u], cmax)];  // the head
+#pragma unroll
+    for (int u = 0; u < HB; ++u) {
+      const int j = hb + u;
+      const bool ok = (valid >> j) & 1;
+      m8 |= ok && ((cb - L + pos[u]) & 1) ? (uint64_t)(1u << s2) << (8 * j) : 0ull;
+      const uint64_t t2 = (v[u] >> a.sb) & tmask;
+      tn[j] = ok && pos[u] < cnt && t2 < tn[j] ? t2 : tn[j];
+    }
+  }
+}
+
+// sibling_search for a stretch too long to stage: samp[x] holds the key at
+// stretch position x * k (ns of them).  An item's first sample at or above
+// it (a branchless search in LDS) brackets its lower bound within k
+// positions, which a binary search in memory narrows.  Halves of the items
+// with none valid in the lane are skipped.
+__device__ __forceinline__ void sibling_search_sampled(const SweepArgs& a, const uint64_t* samp, int32_t ns, int32_t k,
+                                                       const uint64_t* src, int32_t cnt, int32_t cb, int32_t L, int s2,
+                                                       const uint64_t* key, uint32_t valid, uint64_t& m8,
+                                                       uint64_t* tn) {
+  const uint64_t tmask = (1ull << a.wb1) - 1;
+  constexpr int HB = SW_ITEMS / 2;
+#pragma unroll
+  for (int hb = 0; hb < SW_ITEMS; hb += HB) {
+    if (((valid >> hb) & ((1u << HB) - 1)) == 0) continue;
+    int32_t idx[HB];
+#pragma unroll
+    for (int u = 0; u < HB; ++u) idx[u] = 0;
+    int32_t len = ns;
+    while (len > 1) {  // last sample below the key (or 0)
+      const int32_t half = len >> 1;
+      uint64_t v[HB];
+#pragma unroll
+      for (int u = 0; u < HB; ++u) v[u] = samp[idx[u] + half];
+#pragma unroll
+      for (int u = 0; u < HB; ++u) idx[u] = v[u] < key[hb + u] ? idx[u] + half : idx[u];
+      len -= half;
+    }
+    // the lower bound lies in [lo, lo + w]: lo just past the last sample
+    // below the key, w up to k - 1 further
+    int32_t lo[HB], w[HB];
+#pragma unroll
+    for (int u = 0; u < HB; ++u) {
+      const bool below = samp[idx[u]] < key[hb + u];
+      lo[u] = below ? idx[u] * k + 1 : 0;
+      const int32_t top = below ? min((idx[u] + 1) * k, cnt) : 0;
+      w[u] = top - lo[u];
+    }
+    for (int32_t r = k; r > 0; r >>= 1) {  // at most log2(k) + 1 steps
+      uint64_t v[HB];
+#pragma unroll
+      for (int u = 0; u < HB; ++u) v[u] = src[min(lo[u] + (w[u] >> 1), cnt - 1)];
+#pragma unroll
+      for (int u = 0; u < HB; ++u) {
+        const int32_t h = w[u] >> 1;
+        const bool b = w[u] > 0 && v[u] < key[hb + u];
+        lo[u] = b ? lo[u] + h + 1 : lo[u];
+        w[u] = w[u] > 0 ? (b ? w[u] - h - 1 : h) : 0;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < HB; ++u) {
+      const int j = hb + u;
+      const bool ok = (valid >> j) & 1;
+      m8 |= ok && ((cb - L + lo[u]) & 1) ? (uint64_t)(1u << s2) << (8 * j) : 0ull;
+      if (ok && lo[u] < cnt) {
+        const uint64_t t2 = (src[lo[u]] >> a.sb) & tmask;
+        tn[j] = t2 < tn[j] ? t2 : tn[j];
+      }
+    }
+  }
+}
+
 // Up to 8 streams and SW_GROUPS (pid, stream) groups: tiles of SW_TILE
 // events inside one group, numbered group after group (each workgroup
 // finds its group from the groups' tile counts), items striped over the
 // workgroup so that neighbouring lanes hold neighbouring events.  For each
 // sibling the tile's events fall among a stretch of the sibling's events
 // (its co-ranks of the tile's first and last events, by two wave searches),
-// which is staged in LDS in chunks of SB_CAP; every item takes its co-rank
+// which is staged in LDS when it fits SB_CAP (else every k-th key of it is,
+// and a short search in memory follows); every item takes its co-rank
 // by a binary search there (the reads of a step issued together), the
 // sibling is active in the item's interval iff the co-rank is odd, and the
 // event at the co-rank is the sibling's next event.  Interval lengths are
@@ -255,6 +379,7 @@ __device__ __forceinline__ void class_masks(const SweepArgs& a, uint64_t* s_cmas
 __global__ __launch_bounds__(SW_THREADS) void k_sweep_groups(SweepArgs a) {
   __shared__ uint64_t s_sib[SB_CAP];  // one chunk of a sibling's stretch
   __shared__ unsigned long long s_mlen[256];
+  __shared__ unsigned long long s_sub[256];
   __shared__ unsigned long long s_cls[13];  // class_busy[3], class_overlap[9], any
   __shared__ uint64_t s_cmask[3];
   __shared__ int32_t s_goff[SW_GROUPS + 1];  // first event of each group
@@ -301,7 +426,7 @@ __global__ __launch_bounds__(SW_THREADS) void k_sweep_groups(SweepArgs a) {
 
   uint64_t key[SW_ITEMS], tn[SW_ITEMS];
   uint64_t m8 = 0;    // item j's active-stream mask in bits [8 j, 8 j + 8)
-  uint32_t todo = 0;  // bit j: item j exists and its co-rank in the current sibling is not yet known
+  uint32_t valid = 0;  // bit j: item j exists
 #pragma unroll
   for (int j = 0; j < SW_ITEMS; ++j) {
     const int64_t i = base + (int64_t)j * SW_THREADS + tid;
@@ -311,9 +436,8 @@ __global__ __launch_bounds__(SW_THREADS) void k_sweep_groups(SweepArgs a) {
     const uint64_t nk = ok && i + 1 < own_R ? a.ev[i + 1] : ~0ull;
     tn[j] = nk != ~0ull ? (nk >> a.sb) & tmask : ~0ull;
     m8 |= ok && ((i - own_L) & 1) == 0 ? (uint64_t)(1u << st) << (8 * j) : 0ull;
-    todo |= ok ? 1u << j : 0u;
+    valid |= ok ? 1u << j : 0u;
   }
-  const uint32_t valid = todo;
   const uint64_t kf = a.ev[base], kl = a.ev[end - 1];
   for (int q = wv; q < 2 * S; q += SW_THREADS / WAVE) {
     const int s2 = q >> 1;
@@ -329,52 +453,22 @@ __global__ __launch_bounds__(SW_THREADS) void k_sweep_groups(SweepArgs a) {
     const int32_t L = s_goff[pid * S + s2], R = s_goff[pid * S + s2 + 1];
     const int32_t c0 = s_rng[2 * s2];
     const int32_t hi = min(s_rng[2 * s2 + 1] + 1, R);
-    todo = valid;
-    for (int32_t cb = c0;; cb += SB_CAP) {  // uniform over the workgroup
-      const int32_t cnt = min(SB_CAP, hi - cb);
-      const bool final = cb + SB_CAP >= hi;
-      stage_keys(a.ev + cb, cnt, s_sib);
+    // a stretch that fits the LDS buffer is staged there; a longer one (a
+    // sparse stream's tile over a dense sibling) is searched in memory
+    const int32_t cnt = hi - c0;
+    if (cnt <= SB_CAP) {
+      stage_keys(a.ev + c0, cnt, s_sib);
       __syncthreads();
-      if (todo) {
-        const int32_t cmax = cnt > 0 ? cnt - 1 : 0;
-        constexpr int HB = SW_ITEMS / 2;  // two halves, to bound the registers in flight
-#pragma unroll
-        for (int hb = 0; hb < SW_ITEMS; hb += HB) {
-          int32_t pos[HB];
-#pragma unroll
-          for (int u = 0; u < HB; ++u) pos[u] = 0;
-          int32_t len = cnt;
-          while (len > 1) {  // branchless lower bound, the same steps for every item
-            const int32_t half = len >> 1;
-            uint64_t v[HB];
-#pragma unroll
-            for (int u = 0; u < HB; ++u) v[u] = s_sib[pos[u] + half];
-#pragma unroll
-            for (int u = 0; u < HB; ++u) pos[u] = v[u] < key[hb + u] ? pos[u] + half : pos[u];
-            len -= half;
-          }
-          uint64_t v[HB];
-#pragma unroll
-          for (int u = 0; u < HB; ++u) v[u] = s_sib[pos[u]];
-#pragma unroll
-          for (int u = 0; u < HB; ++u) pos[u] += cnt > 0 && v[u] < key[hb + u];
-#pragma unroll
-          for (int u = 0; u < HB; ++u) v[u] = s_sib[min(pos[u], cmax)];  // the head
-#pragma unroll
-          for (int u = 0; u < HB; ++u) {
-            const int j = hb + u;
-            // resolved by this chunk if its lower bound lies inside (or it is the last)
-            const bool res = ((todo >> j) & 1) && (pos[u] < cnt || final);
-            // co-rank cb - L + pos: the sibling is active if it is odd
-            m8 |= res && ((cb - L + pos[u]) & 1) ? (uint64_t)(1u << s2) << (8 * j) : 0ull;
-            const uint64_t t2 = (v[u] >> a.sb) & tmask;
-            tn[j] = res && pos[u] < cnt && t2 < tn[j] ? t2 : tn[j];
-            todo &= res ? ~(1u << j) : ~0u;
-          }
-        }
-      }
-      __syncthreads();  // the next chunk or sibling overwrites this one
-      if (final) break;
+      sibling_search(a, s_sib, cnt, c0, L, s2, key, valid, m8, tn);
+      __syncthreads();  // the next sibling's stretch overwrites this one
+    } else {
+      // every k-th key of the stretch in LDS: an item's lower bound lies
+      // within k keys after the first staged key at or above it
+      const int32_t k = (int32_t)cdiv((int64_t)cnt, (int64_t)SB_CAP), ns = (int32_t)cdiv((int64_t)cnt, (int64_t)k);
+      stage_keys(a.ev + c0, ns, s_sib, k);
+      __syncthreads();
+      sibling_search_sampled(a, s_sib, ns, k, a.ev + c0, cnt, c0, L, s2, key, valid, m8, tn);
+      __syncthreads();
     }
   }
   // a thread's intervals with one mask are summed before the atomic
@@ -395,7 +489,7 @@ __global__ __launch_bounds__(SW_THREADS) void k_sweep_groups(SweepArgs a) {
   }
   if (cur_len) atomicAdd(&s_mlen[cur_m], (unsigned long long)cur_len);
   __syncthreads();
-  flush_masks(a, pid, s_mlen, s_cls, cm);
+  flush_masks(a, pid, s_mlen, s_sub, s_cls, cm);
 }
 
 // Any number of streams and groups: tiles by position (several groups and
