@@ -532,8 +532,8 @@ static inline void stage_end(Ctx& c, int s) {
 struct DeviceStreams {
   hipStream_t s[2] = {nullptr, nullptr};
   hipStream_t cap = nullptr;  // graphs are captured here (the caller's stream may be the null stream)
-  hipEvent_t e[8] = {};  // sorts, timeline chain, join, launches' ops, name tables, radix passes, depths,
-                         // kernels' critical-path releases
+  hipEvent_t e[9] = {};  // sorts, timeline chain, join, launches' ops, name tables, radix passes, depths,
+                         // kernels' critical-path releases, op-name lanes' union
   hipStream_t copy = nullptr;  // uploads of the chunked entry point
   hipEvent_t up[2] = {};       // a staging set's upload done
   bool ok = false;
@@ -653,6 +653,11 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   launch_edges(c);
   stage_end(c, HERSCHEL_STAGE_EDGES);
   rec(2, c.st);
+  if (c.waits) {  // the op-name lanes' union, beside the timeline stream's device lane
+    wait(c.st, 0);
+    launch_union_opnames(c);
+    rec(8, c.st);
+  }
   // the per-name tables need neither the join nor containment; each kernel
   // takes its launch's op once the containment query has given launches
   // their ops
@@ -670,6 +675,7 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     launch_crit_kernels(c);
     rec(7, c.st);
   }
+  rec(4, c.st);
 
   // chain 1: timeline and overlap
   c.st = lib0;
@@ -682,7 +688,9 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_end(c, HERSCHEL_STAGE_OVERLAP);
   stage_begin(c, HERSCHEL_STAGE_WAITS);
   if (c.waits) {
-    launch_union_waits(c);
+    launch_union_device(c);
+    launch_dg_scan(c);
+    wait(c.st, 8);
     launch_waits(c);
   }
   stage_end(c, HERSCHEL_STAGE_WAITS);
@@ -700,11 +708,6 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
     stage_end(c, HERSCHEL_STAGE_SOL);
   }
   rec(1, c.st);
-  // the join's stream takes the timeline's end too, so that the caller's
-  // stream waits on one event at the end (each wait is a barrier packet on
-  // its queue, handled after the kernel before it)
-  wait(lib1, 1);
-  rec(4, lib1);
 
   // back on the caller's stream: what needs both containment and the join
   c.st = s0;
@@ -727,7 +730,8 @@ static int enqueue_locked(Ctx& c, DeviceStreams* dsx) {
   stage_begin(c, HERSCHEL_STAGE_GRAPH);
   if (c.graph) launch_graph(c);
   stage_end(c, HERSCHEL_STAGE_GRAPH);
-  wait(c.st, 4);  // both other streams' work
+  wait(c.st, 1);
+  wait(c.st, 4);
   stage_begin(c, HERSCHEL_STAGE_FINAL);
   launch_finalize(c);
   stage_end(c, HERSCHEL_STAGE_FINAL);

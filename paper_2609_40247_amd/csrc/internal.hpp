@@ -164,7 +164,12 @@ void launch_sort_multi(Ctx& c, SortBufs* const* s, const int32_t* const* count, 
 void launch_refine(Ctx& c);
 void launch_names(Ctx& c);
 void launch_timeline(Ctx& c);
-void launch_union_waits(Ctx& c);
+// idle coincidence: the device lane's union, the op-name lanes' union, the
+// prefix sums of the idle intervals (after the device lane's), the search
+// (after all three)
+void launch_union_device(Ctx& c);
+void launch_union_opnames(Ctx& c);
+void launch_dg_scan(Ctx& c);
 void launch_waits(Ctx& c);
 void launch_overlap(Ctx& c);
 void launch_contain(Ctx& c);

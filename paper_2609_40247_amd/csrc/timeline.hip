@@ -426,7 +426,7 @@ void launch_timeline(Ctx& c) {
 // its gaps above the threshold are the GPU's idle intervals, in (pid, begin)
 // order; and over the op-name lanes, whose busy time is each op name's span
 // and whose coverage-run endpoints bound its union.
-void launch_union_waits(Ctx& c) {
+void launch_union_device(Ctx& c) {
   UnionArgs d = union_args(c, c.sD, 1, 0);
   d.overlap = false;
   d.cnt = nullptr;
@@ -445,6 +445,9 @@ void launch_union_waits(Ctx& c) {
   d.gaps_out = &c.ds->nDgap;
   d.ev_out = &c.ds->nDev;
   hipLaunchKernelGGL(k_union, dim3((unsigned)c.union_tiles), dim3(UN_THREADS), 0, c.st, d);
+}
+
+void launch_union_opnames(Ctx& c) {
   UnionArgs o = union_args(c, c.sO, c.NOP, c.nob);
   o.overlap = true;
   o.want_gaps = false;

@@ -204,7 +204,7 @@ __global__ __launch_bounds__(WT_THREADS) void k_waits(WaitsArgs a) {
                       idle_before(a, s_key, ns, S, cnt, (int32_t)p, a.W0);
 }
 
-void launch_waits(Ctx& c) {
+static WaitsArgs waits_args(Ctx& c) {
   WaitsArgs a;
   a.ds = c.ds;
   a.dg_pid = c.dg_pid;
@@ -222,7 +222,16 @@ void launch_waits(Ctx& c) {
   a.W1 = c.W1;
   a.dev_idle = c.o.dev_idle;
   a.op_idle = c.o.op_idle;
+  return a;
+}
+
+void launch_dg_scan(Ctx& c) {
+  const WaitsArgs a = waits_args(c);
   hipLaunchKernelGGL(k_dg_scan, dim3((unsigned)c.dg_tiles), dim3(DG_THREADS), 0, c.st, a);
+}
+
+void launch_waits(Ctx& c) {
+  const WaitsArgs a = waits_args(c);
   // a grid of at most WT_BLOCKS workgroups: each stages the interval keys once
   const int64_t work = std::max<int64_t>(cdiv(c.oev_cap / 2, WT_THREADS), cdiv(c.P, WT_THREADS));
   hipLaunchKernelGGL(k_waits, dim3((unsigned)std::max<int64_t>(std::min<int64_t>(work, WT_BLOCKS), 1)),
