@@ -305,6 +305,45 @@ def test_overlap_spans_beyond_32_bits(H, seed):
     check(H, cols, p, f"spans beyond 32 bits seed{seed}")
 
 
+@pytest.mark.parametrize("n0", [4090, 4096, 4097, 4200, 9000])
+def test_overlap_stretch_at_lds_capacity(H, n0):
+    """A sparse stream's one tile against a dense sibling whose stretch holds
+    about 2 * n0 endpoints: below, at and just past the 8,192 a workgroup
+    stages in LDS (past it, every k-th key is staged, k = 2 and more, and the
+    search ends in memory); a third stream bursts in between."""
+    rng = np.random.default_rng(950 + n0)
+    W = 1_100_000_000
+    rows = []
+    corr = 0
+
+    def kern(s, t, d):
+        nonlocal corr
+        rows.append((2, 0, s, int(t), int(t + d), corr, corr % 4))
+        corr += 1
+
+    for x in np.sort(rng.choice(1_000_000, n0, replace=False)) * 1_000:     # disjoint, 2 n0 endpoints
+        kern(0, x + 5, rng.integers(1, 995))
+    for x in np.sort(rng.integers(0, 1_000_000_000, 50)):
+        kern(1, x, rng.integers(1, 40_000_000))
+    for x in 500_000_000 + np.sort(rng.integers(0, 2_000_000, 300)):
+        kern(2, x, rng.integers(1, 3_000))
+    perm = rng.permutation(len(rows))
+    rows = [rows[i] for i in perm]
+    cols, p = _rows(rows, P=1, S=3, W=W, thr=1_000, cls=np.array([0, 1, 2], np.uint8))
+    check(H, cols, p, f"stretch of about {2 * n0} endpoints")
+
+
+@pytest.mark.parametrize("P", [32, 33])
+def test_overlap_group_count_limit(H, P):
+    """8 streams in 32 processes (256 groups: tiles inside one group) and in
+    33 (264 groups: tiles over several groups, every event searching its
+    siblings in memory)."""
+    tr = synth.random_small(seed=61 + P, n_rows=40_000, window=2_000_000, n_procs=P, n_streams=8, n_threads=2,
+                            corr_range=20_000)
+    p = dict(tr.params, stream_class=(np.arange(8) % 3).astype(np.uint8))
+    check(H, tr.columns(), p, f"{P} processes x 8 streams")
+
+
 def test_64_streams_overlap(H):
     tr = synth.random_small(seed=77, n_rows=6000, window=20_000, n_procs=2, n_streams=64, n_threads=2,
                             corr_range=3000)
