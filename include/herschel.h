@@ -358,9 +358,12 @@ const char *herschel_strerror(int code);
 /* Diagnostics for benchmarks.  Stages of one analysis call.  INIT, PREP,
  * HIST and SORT (with the refine pass after it) run in this order on
  * params->hip_stream; after SORT the JOIN, EDGES and NAMES stages run on a
- * library stream (JOIN beside the refine pass), the TIMELINE, OVERLAP and
- * WAITS stages on another after the refine pass, while CONTAIN, OPAGG, SOL,
- * CRIT and GRAPH follow on params->hip_stream; FINAL waits for all of them. */
+ * library stream (JOIN beside the refine pass; with OUT_WAITS the op-name
+ * lanes' union after EDGES; with OUT_CRIT the kernels' critical-path
+ * releases after NAMES), the TIMELINE, OVERLAP and WAITS stages on another
+ * after the refine pass, while CONTAIN, OPAGG, SOL, CRIT and GRAPH follow on
+ * params->hip_stream (with OUT_CRIT, OPAGG and SOL move to the end of the
+ * TIMELINE stream, beside CRIT); FINAL waits for all of them. */
 enum {
   HERSCHEL_STAGE_INIT = 0,     /* clear the workspace state and accumulating outputs */
   HERSCHEL_STAGE_PREP = 1,     /* validate, correct, admit, compact (one kernel) */
@@ -368,7 +371,7 @@ enum {
   HERSCHEL_STAGE_NAMES = 3,    /* per-name and per-op-name tables, then kernel -> op */
   HERSCHEL_STAGE_SORT = 4,     /* radix passes shared by the sorts (the timeline and containment digits) */
   HERSCHEL_STAGE_TIMELINE = 5, /* busy/idle, gaps, coverage runs (one kernel) */
-  HERSCHEL_STAGE_OVERLAP = 6,  /* co-ranks of the coverage runs and the sweep */
+  HERSCHEL_STAGE_OVERLAP = 6,  /* group starts of the coverage-run endpoints and the sweep */
   HERSCHEL_STAGE_CONTAIN = 7,  /* op nesting and launch -> op */
   HERSCHEL_STAGE_JOIN = 8,     /* launch <-> kernel join by correlation table, latency */
   HERSCHEL_STAGE_OPAGG = 9,    /* inclusive per-op aggregates */
@@ -376,7 +379,7 @@ enum {
   HERSCHEL_STAGE_FINAL = 11,   /* counters and histogram totals */
   HERSCHEL_STAGE_WAITS = 12,   /* device-lane and op-name unions, idle coincidence (OUT_WAITS) */
   HERSCHEL_STAGE_SOL = 13,     /* operator efficiency and per-name hotness (OUT_SOL), after OPAGG */
-  HERSCHEL_STAGE_CRIT = 14,    /* critical path (OUT_CRIT), after SOL */
+  HERSCHEL_STAGE_CRIT = 14,    /* critical path (OUT_CRIT), after CONTAIN and the join */
   HERSCHEL_STAGE_GRAPH = 15,   /* graph replay separation (OUT_GRAPH), after CRIT */
   HERSCHEL_N_STAGES = 16
 };
