@@ -15,8 +15,8 @@
 
 namespace hx {
 
-constexpr int UN_THREADS = 512;
-constexpr int UN_ITEMS = 8;
+constexpr int UN_THREADS = 1024;
+constexpr int UN_ITEMS = 4;
 constexpr int UN_TILE = UN_THREADS * UN_ITEMS;
 static_assert(UN_ITEMS % 4 == 0, "a thread's keys and rows are loaded 16 bytes at a time");
 
