@@ -133,7 +133,7 @@ __device__ __forceinline__ int lat_bin(int64_t x) { return x <= 0 ? 0 : bits_of(
 // issue each round of their loads together: a pass is a short chain of
 // dependent loads, and batching entries per thread keeps the number of waves
 // the chip must cycle through low.
-constexpr int JT_IT_STORE = 4, JT_IT_RESOLVE = 8;
+constexpr int JT_IT_STORE = 4, JT_IT_RESOLVE = 6;
 
 // Pass 1: every launch writes its row to its slot's launch word, every kernel
 // to the kernel word (plain stores; one writer of each wins).
