@@ -170,7 +170,10 @@ def run_config4(args) -> int:
     from paper_2609_40247_amd import synth
     first = 32 * args.chunk
     ids = list(range(first, first + 32))
-    gen = synth.config4_chunk(ids)  # spawned workers, before the GPU is touched
+    def progress(done, total):
+        print(f"generated {done}/{total} traces", file=sys.stderr, flush=True)
+
+    gen = synth.config4_chunk(ids, progress=progress)  # spawned workers, before the GPU is touched
     cols_l = [c for c, _ in gen]
     params_l = [p for _, p in gen]
     ns = [len(c["ts"]) for c in cols_l]

@@ -481,17 +481,26 @@ def _config4_columns(t: int):
     return tr.columns(), tr.params
 
 
-def config4_chunk(ids, workers: int = 16):
+def config4_chunk(ids, workers: int = 16, progress=None):
     """Columns and params of the batch traces `ids`, generated by a pool of
     fresh worker processes (spawned, so that a parent that already uses the
-    GPU forks nothing)."""
+    GPU forks nothing); `progress(done, total)` is called as traces finish."""
     import multiprocessing as mp
     ids = [int(t) for t in ids]
     workers = max(1, min(workers, len(ids), os.cpu_count() or 1))
+    out = []
     if workers == 1:
-        return [_config4_columns(t) for t in ids]
+        for t in ids:
+            out.append(_config4_columns(t))
+            if progress:
+                progress(len(out), len(ids))
+        return out
     with mp.get_context("spawn").Pool(workers) as pool:
-        return pool.map(_config4_columns, ids)
+        for r in pool.imap(_config4_columns, ids):
+            out.append(r)
+            if progress:
+                progress(len(out), len(ids))
+    return out
 
 
 def add_op_costs(cols: dict, params: dict, seed: int, ref: bool = True, flops_median: float = 2e9,
