@@ -1071,6 +1071,40 @@ def test_sol_batch(H):
 
 
 
+@pytest.mark.parametrize("which", ["sol", "graph"])
+def test_chunked_streaming_optional_columns(H, which):
+    """The chunked entry point uploads the optional columns the host holds:
+    op counts (operator efficiency) or graph nodes (replay separation),
+    three traces in chunks of two, every output equal to the oracle's."""
+    if which == "sol":
+        traces = [synth.config4_trace(t, kernels=k) for t, k in enumerate((20_000, 7_000))]
+        traces.insert(1, synth.config1(n_steps=15))
+        sets = [synth.add_op_costs(t.columns(), t.params, 40 + i) for i, t in enumerate(traces)]
+    else:
+        sets = []
+        for i, (st, nn) in enumerate(((30, 200), (12, 60), (25, 150))):
+            c, q = synth.graph_replay_trace(seed=50 + i, n_steps=st, n_nodes=nn)
+            sets.append((c, dict(q, flags=q["flags"] | 32)))
+    ns = [len(c["ts"]) for c, _ in sets]
+    cols = {k: np.concatenate([c[k] for c, _ in sets]) for k in sets[0][0]}
+    offs = np.cumsum([0] + ns).astype(np.int64)
+    host, hev = _pinned(H, cols)
+    rows = max(int(offs[min(c + 2, 3)] - offs[c]) for c in range(0, 3, 2))
+    staging = [{k: torch.empty(rows, dtype=v.dtype, device="cuda") for k, v in host.items()} for _ in range(2)]
+    ans = [H.Analyzer(q, max(ns)) for _, q in sets]
+    for a in ans:
+        a.prefill()
+    big = max(ans, key=lambda a: a.ws_bytes)
+    plist = [ans[0]._params_struct(big.ws.data_ptr(), big.ws_bytes)] + [a.params for a in ans[1:]]
+    code = H.herschel_trace_analyze_chunked(hev, offs, 2, [H.events_struct(d) for d in staging], rows, plist,
+                                            [a.outs for a in ans])
+    torch.cuda.synchronize()
+    assert code == 0, H.herschel_strerror(code)
+    for (c, q), a, n in zip(sets, ans, ns):
+        o = oracle.analyze(c, q, gap_capacity=a.gap_capacity)
+        assert_same((0, a.results(n)), o, q, f"{which} chunked")
+
+
 # --------------------------------------------------------------- critical path
 @pytest.mark.parametrize("case", [0, 1, 2], ids=["figure", "nested", "ties"])
 def test_crit_worked_cases(H, case):
